@@ -1,0 +1,210 @@
+"""CPU oracle for NetKV decode-instance selection -- TEST INFRASTRUCTURE.
+
+Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its binding) never imports, links or calls it, and this package never imports
+the product.  The arithmetic lives in ``netkv_oracle.c`` (plain C, fp64);
+this module only builds it with gcc and marshals numpy arrays through ctypes.
+
+Sources of every computed quantity are cited in ``netkv_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "netkv_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle_netkv.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no intrinsics)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+                               "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Snap(C.Structure):
+    _fields_ = [
+        ("n_prefill", C.c_uint32), ("n_decode", C.c_uint32),
+        ("tier_map", C.c_void_p), ("util", C.c_void_p), ("n_inflight", C.c_void_p),
+        ("tier_bw", C.c_double * 4), ("tier_lat", C.c_double * 4),
+        ("free_mem", C.c_void_p), ("queue_depth", C.c_void_p), ("batch_size", C.c_void_p),
+        ("t_iter_a", C.c_double), ("t_iter_b", C.c_double), ("beta_max", C.c_uint32),
+        ("alpha", C.c_double), ("m_min", C.c_uint64), ("kv_bytes_per_token", C.c_uint64),
+        ("block_tokens", C.c_uint32),
+    ]
+
+
+class _Req(C.Structure):
+    _fields_ = [("n_req", C.c_uint32), ("prefill", C.c_void_p), ("len_tokens", C.c_void_p),
+                ("hash_off", C.c_void_p), ("hashes", C.c_void_p)]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        lib = C.CDLL(_LIB)
+        lib.orc_cache_build.restype = C.c_void_p
+        lib.orc_cache_build.argtypes = [C.c_uint32, C.c_void_p, C.c_void_p]
+        lib.orc_cache_free.argtypes = [C.c_void_p]
+        lib.orc_select.restype = C.c_uint64
+        lib.orc_select.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32,
+                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                   C.c_void_p, C.c_int]
+        lib.orc_rank_sweep.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32,
+                                       C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p,
+                                       C.c_void_p, C.c_int]
+        lib.orc_commit.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                   C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p,
+                                   C.c_void_p, C.c_void_p]
+        lib.orc_prefix_len.restype = C.c_uint32
+        lib.orc_prefix_len.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint32]
+        lib.orc_max_threads.restype = C.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def _arr(a, dt):
+    return np.ascontiguousarray(np.asarray(a, dtype=dt))
+
+
+class Snapshot:
+    """Keeps the numpy arrays alive behind the C struct."""
+
+    def __init__(self, snap: Dict[str, object]):
+        self.keep = dict(
+            tier_map=_arr(snap["tier_map"], np.uint8), util=_arr(snap["util"], np.float32),
+            n_inflight=_arr(snap["n_inflight"], np.uint16),
+            free_mem=_arr(snap["free_mem"], np.uint64),
+            queue_depth=_arr(snap["queue_depth"], np.uint32),
+            batch_size=_arr(snap["batch_size"], np.uint32))
+        s = _Snap()
+        s.n_prefill = int(snap["n_prefill"])
+        s.n_decode = int(snap["n_decode"])
+        for f in ("tier_map", "util", "n_inflight", "free_mem", "queue_depth", "batch_size"):
+            setattr(s, f, self.keep[f].ctypes.data)
+        for i in range(4):
+            s.tier_bw[i] = float(snap["tier_bw"][i])
+            s.tier_lat[i] = float(snap["tier_lat"][i])
+        s.t_iter_a = float(snap["t_iter_a"])
+        s.t_iter_b = float(snap["t_iter_b"])
+        s.beta_max = int(snap["beta_max"])
+        s.alpha = float(snap["alpha"])
+        s.m_min = int(snap["m_min"])
+        s.kv_bytes_per_token = int(snap["kv_bytes_per_token"])
+        s.block_tokens = int(snap["block_tokens"])
+        self.s = s
+        self.n_prefill, self.n_decode = s.n_prefill, s.n_decode
+
+
+class Requests:
+    def __init__(self, req: Dict[str, np.ndarray]):
+        self.keep = dict(prefill=_arr(req["prefill"], np.uint32),
+                         len_tokens=_arr(req["len_tokens"], np.uint32),
+                         hash_off=_arr(req["hash_off"], np.uint64),
+                         hashes=_arr(req["hashes"], np.uint64))
+        r = _Req()
+        r.n_req = len(self.keep["prefill"])
+        for f in ("prefill", "len_tokens", "hash_off", "hashes"):
+            setattr(r, f, self.keep[f].ctypes.data)
+        self.r = r
+        self.n_req = r.n_req
+
+
+class Cache:
+    """Sorted copies of every decode's resident hash list."""
+
+    def __init__(self, cache: Dict[str, np.ndarray]):
+        lib = _load()
+        off = _arr(cache["hash_off"], np.uint64)
+        h = _arr(cache["hashes"], np.uint64)
+        self.n_decode = len(off) - 1
+        self.h = lib.orc_cache_build(self.n_decode, off.ctypes.data, h.ctypes.data)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.orc_cache_free(self.h)
+            self.h = None
+
+    def prefix_len(self, d: int, hashes: np.ndarray) -> int:
+        hashes = _arr(hashes, np.uint64)
+        return int(_load().orc_prefix_len(self.h, d, hashes.ctypes.data, len(hashes)))
+
+
+def max_threads() -> int:
+    return int(_load().orc_max_threads())
+
+
+def select(snap, cache, req, k: int = 1, pairs: bool = False, n_threads: int = 1):
+    """Top-k selection for every request.
+
+    Returns dict(idx [R,k] int32, score [R,k] float64, tests (sum of
+    membership tests), and if ``pairs``: j [R,D] uint16, feasible [R,D]
+    uint8, cost [R,D] float64)."""
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    c = cache if isinstance(cache, Cache) else Cache(cache)
+    q = req if isinstance(req, Requests) else Requests(req)
+    R, D = q.n_req, s.n_decode
+    idx = np.empty((R, k), dtype=np.int32)
+    score = np.empty((R, k), dtype=np.float64)
+    out = dict(idx=idx, score=score)
+    pj = pf = pc = None
+    if pairs:
+        pj = np.empty((R, D), dtype=np.uint16)
+        pf = np.empty((R, D), dtype=np.uint8)
+        pc = np.empty((R, D), dtype=np.float64)
+        out.update(j=pj, feasible=pf, cost=pc)
+    out["tests"] = int(lib.orc_select(C.byref(s.s), c.h, C.byref(q.r), k, idx.ctypes.data,
+                                      score.ctypes.data, _ptr(pj), _ptr(pf), _ptr(pc),
+                                      int(n_threads)))
+    return out
+
+
+def rank_sweep(snap, cache, req, util_scen: np.ndarray, k: int = 3, n_threads: int = 1):
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    c = cache if isinstance(cache, Cache) else Cache(cache)
+    q = req if isinstance(req, Requests) else Requests(req)
+    u = _arr(util_scen, np.float32)
+    S = u.shape[0]
+    R = q.n_req
+    idx = np.empty((S, R, k), dtype=np.int32)
+    score = np.empty((S, R, k), dtype=np.float64)
+    flips = np.empty((S, 2), dtype=np.uint64)
+    lib.orc_rank_sweep(C.byref(s.s), c.h, C.byref(q.r), S, u.ctypes.data, k, idx.ctypes.data,
+                       score.ctypes.data, flips.ctypes.data, int(n_threads))
+    return dict(idx=idx, score=score, flips=flips)
+
+
+def commit(snap, cache, req, sel: np.ndarray, cap: int, mu: int, state: Dict[str, np.ndarray]):
+    """Between-batch state update (in place on copies); returns the new state
+    dict with n_inflight, queue_depth, free_mem, admitted_prev."""
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    c = cache if isinstance(cache, Cache) else Cache(cache)
+    q = req if isinstance(req, Requests) else Requests(req)
+    st = dict(n_inflight=_arr(state["n_inflight"], np.uint16).copy(),
+              queue_depth=_arr(state["queue_depth"], np.uint32).copy(),
+              free_mem=_arr(state["free_mem"], np.uint64).copy(),
+              admitted_prev=_arr(state["admitted_prev"], np.uint64).copy())
+    sel = _arr(sel, np.int32)
+    lib.orc_commit(C.byref(s.s), c.h, C.byref(q.r), sel.ctypes.data, int(cap), int(mu),
+                   st["n_inflight"].ctypes.data, st["queue_depth"].ctypes.data,
+                   st["free_mem"].ctypes.data, st["admitted_prev"].ctypes.data)
+    return st

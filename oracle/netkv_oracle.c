@@ -1,0 +1,364 @@
+/*
+ * Plain CPU oracle for NetKV decode-instance selection.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or
+ * load this file; only the tests, the smoke check and the benchmark's CPU
+ * baseline use it.  It shares no source, header, table or helper with the
+ * HIP library: it has its own structures, its own resident-set structure
+ * (a sorted copy of each decode's hash list, searched by bisection -- the
+ * GPU path uses open-addressed tables instead) and computes in fp64.
+ *
+ * What it computes (paper: "NetKV: Network-Aware Decode Instance Selection
+ * for Disaggregated LLM Inference"):
+ *   - Sec. III-B: n_r = floor(l_r / B_tok) hashed blocks; the cache hit is
+ *     B_tok times the number of leading blocks of h_r resident on d (the
+ *     block-level longest common prefix, scanned up to the first miss).
+ *   - Eq. (2): non-cached bytes s_eff = s_r (1 - lambda / l_r), evaluated in
+ *     the algebraically identical integer form bpt * (l_r - lambda), with
+ *     bpt the per-GPU-pair KV bytes per token of Eq. (1).
+ *   - Eq. (4): B_eff = B_tau (1 - c) / (1 + n_inflight[tau][p]).
+ *   - Eq. (3): T_transfer = s_eff / B_eff + L_tau.
+ *   - Sec. IV-B, Eqs. (6)-(7): T_queue = max(0, q_d - (beta_max - beta_d)) t_iter(beta_d),
+ *     T_decode = t_iter(beta_d + 1), t_iter(beta) = a + b beta (Sec. III-C).
+ *   - Eq. (5) / Algorithm 1: feasible set m_d >= s_eff + m_min; cost
+ *     C = T_transfer + alpha (T_queue + T_decode) (alpha = 1 is Eq. (5));
+ *     select the minimum-cost feasible d, ties to the lowest index; reject
+ *     (index -1, cost +inf) when no d is feasible.
+ *   Every request is scored against the same snapshot (the in-flight counter
+ *   update of Algorithm 1 happens between batches, see orc_commit).
+ *
+ * Readings where the paper is silent are listed in the design notes of the
+ * repository: congestion is given per (p, d) pair; the block size is a
+ * parameter; all decodes are matched before the feasibility filter.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+typedef struct {
+    uint32_t n_prefill, n_decode;
+    const uint8_t *tier_map;      /* [n_prefill * n_decode] */
+    const float *util;            /* [n_prefill * n_decode] congestion c(p,d) */
+    const uint16_t *n_inflight;   /* [4 * n_prefill], tier-major */
+    double tier_bw[4];            /* bytes/s */
+    double tier_lat[4];           /* s */
+    const uint64_t *free_mem;     /* [n_decode] m_d, bytes */
+    const uint32_t *queue_depth;  /* [n_decode] q_d */
+    const uint32_t *batch_size;   /* [n_decode] beta_d */
+    double t_iter_a, t_iter_b;
+    uint32_t beta_max;
+    double alpha;
+    uint64_t m_min;
+    uint64_t kv_bytes_per_token;
+    uint32_t block_tokens;
+} orc_snapshot;
+
+typedef struct {
+    uint32_t n_req;
+    const uint32_t *prefill;
+    const uint32_t *len_tokens;
+    const uint64_t *hash_off;     /* [n_req + 1] */
+    const uint64_t *hashes;
+} orc_requests;
+
+/* ---------------------------------------------------------------- cache */
+
+typedef struct {
+    uint32_t n_decode;
+    uint64_t *off;      /* [n_decode + 1] */
+    uint64_t *keys;     /* each decode's hashes, sorted ascending */
+} orc_cache;
+
+static int cmp_u64(const void *a, const void *b) {
+    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
+    return (x > y) - (x < y);
+}
+
+orc_cache *orc_cache_build(uint32_t n_decode, const uint64_t *off, const uint64_t *hashes) {
+    orc_cache *c = (orc_cache *)calloc(1, sizeof(orc_cache));
+    uint64_t total = off[n_decode];
+    c->n_decode = n_decode;
+    c->off = (uint64_t *)malloc(sizeof(uint64_t) * (n_decode + 1));
+    c->keys = (uint64_t *)malloc(sizeof(uint64_t) * (total ? total : 1));
+    memcpy(c->off, off, sizeof(uint64_t) * (n_decode + 1));
+    memcpy(c->keys, hashes, sizeof(uint64_t) * total);
+    for (uint32_t d = 0; d < n_decode; ++d)
+        qsort(c->keys + off[d], (size_t)(off[d + 1] - off[d]), sizeof(uint64_t), cmp_u64);
+    return c;
+}
+
+void orc_cache_free(orc_cache *c) {
+    if (!c) return;
+    free(c->off);
+    free(c->keys);
+    free(c);
+}
+
+/* Is block hash h in K_d?  (bisection over the sorted copy) */
+static int resident(const orc_cache *c, uint32_t d, uint64_t h) {
+    const uint64_t *k = c->keys + c->off[d];
+    uint64_t lo = 0, hi = c->off[d + 1] - c->off[d];
+    while (lo < hi) {
+        uint64_t mid = lo + (hi - lo) / 2;
+        if (k[mid] < h) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo < c->off[d + 1] - c->off[d] && k[lo] == h;
+}
+
+/* |LCP_block(h_r, K_d)|: leading blocks resident on d, up to the first miss
+ * (Sec. III-B).  *tests receives the number of membership tests made. */
+static uint32_t prefix_blocks(const orc_cache *c, uint32_t d, const uint64_t *h, uint32_t n,
+                              uint32_t *tests) {
+    uint32_t j = 0;
+    while (j < n && resident(c, d, h[j])) ++j;
+    *tests = (j < n) ? j + 1 : n;
+    return j;
+}
+
+/* ---------------------------------------------------------------- costs */
+
+static double t_iter(const orc_snapshot *s, double beta) { return s->t_iter_a + s->t_iter_b * beta; }
+
+/* T_queue(d) + T_decode(d), Sec. IV-B */
+static double load_time(const orc_snapshot *s, uint32_t d) {
+    int64_t q = s->queue_depth[d], beta = s->batch_size[d];
+    int64_t blocked = q - ((int64_t)s->beta_max - beta);
+    if (blocked < 0) blocked = 0;
+    double tq = (double)blocked * t_iter(s, (double)beta);
+    double tdec = t_iter(s, (double)(beta + 1));
+    return tq + tdec;
+}
+
+/* Eq. (4) */
+static double eff_bandwidth(const orc_snapshot *s, uint32_t p, uint32_t d) {
+    uint64_t pd = (uint64_t)p * s->n_decode + d;
+    int tau = s->tier_map[pd];
+    double c = (double)s->util[pd];
+    double n = (double)s->n_inflight[(uint64_t)tau * s->n_prefill + p];
+    return s->tier_bw[tau] * (1.0 - c) / (1.0 + n);
+}
+
+typedef struct {
+    double cost;
+    int32_t d;
+} cand;
+
+static int cmp_cand(const void *a, const void *b) {
+    const cand *x = (const cand *)a, *y = (const cand *)b;
+    if (x->cost < y->cost) return -1;
+    if (x->cost > y->cost) return 1;
+    return (x->d > y->d) - (x->d < y->d);
+}
+
+/* Score request r against every decode with the congestion matrix `util`
+ * (the snapshot's own, or a scenario's).  j_row, if given, supplies the
+ * prefix lengths instead of matching again. */
+static void score_request(const orc_snapshot *s, const float *util, const orc_cache *c,
+                          const orc_requests *q, uint32_t r, const uint16_t *j_row, cand *buf,
+                          uint32_t k, int32_t *out_idx, double *out_score, uint16_t *pj,
+                          uint8_t *pf, double *pc, uint64_t *tests_sum) {
+    orc_snapshot sv = *s;
+    sv.util = util;
+    uint32_t p = q->prefill[r];
+    uint64_t len = q->len_tokens[r];
+    uint64_t a = q->hash_off[r], b = q->hash_off[r + 1];
+    uint32_t n = (uint32_t)(b - a);
+    uint32_t nfeas = 0;
+    uint64_t tests_r = 0;
+    for (uint32_t d = 0; d < s->n_decode; ++d) {
+        uint32_t j, t = 0;
+        if (j_row) {
+            j = j_row[d];
+        } else {
+            j = prefix_blocks(c, d, q->hashes + a, n, &t);
+            tests_r += t;
+        }
+        uint64_t lambda = (uint64_t)s->block_tokens * j;               /* tokens */
+        uint64_t s_eff = s->kv_bytes_per_token * (len - lambda);       /* Eq. (2) */
+        uint64_t m = s->free_mem[d];
+        int feas = (m >= s->m_min) && (m - s->m_min >= s_eff);         /* m >= s_eff + m_min */
+        int tau = s->tier_map[(uint64_t)p * s->n_decode + d];
+        double t_x = (double)s_eff / eff_bandwidth(&sv, p, d) + s->tier_lat[tau];   /* Eq. (3) */
+        double cost = t_x + s->alpha * load_time(s, d);
+        if (pj) pj[d] = (uint16_t)j;
+        if (pf) pf[d] = (uint8_t)feas;
+        if (pc) pc[d] = cost;
+        if (feas) {
+            buf[nfeas].cost = cost;
+            buf[nfeas].d = (int32_t)d;
+            ++nfeas;
+        }
+    }
+    qsort(buf, nfeas, sizeof(cand), cmp_cand);
+    for (uint32_t i = 0; i < k; ++i) {
+        out_idx[i] = i < nfeas ? buf[i].d : -1;
+        out_score[i] = i < nfeas ? buf[i].cost : INFINITY;
+    }
+    *tests_sum += tests_r;
+}
+
+/* Select top-k decodes for every request.  Per-pair outputs (row-major
+ * [n_req][n_decode]) may be NULL.  Returns the number of block membership
+ * tests made by the first-miss scans (sum over pairs of min(j + 1, n_r)). */
+uint64_t orc_select(const orc_snapshot *s, const orc_cache *c, const orc_requests *q, uint32_t k,
+                    int32_t *out_idx, double *out_score, uint16_t *pair_j, uint8_t *pair_feas,
+                    double *pair_cost, int n_threads) {
+    uint64_t tests = 0;
+    const uint32_t D = s->n_decode;
+#ifdef _OPENMP
+    if (n_threads < 1) n_threads = 1;
+#pragma omp parallel num_threads(n_threads) reduction(+ : tests)
+#endif
+    {
+        cand *buf = (cand *)malloc(sizeof(cand) * (D ? D : 1));
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 8)
+#endif
+        for (int64_t r = 0; r < (int64_t)q->n_req; ++r) {
+            uint64_t row = (uint64_t)r * D;
+            score_request(s, s->util, c, q, (uint32_t)r, NULL, buf, k, out_idx + (uint64_t)r * k,
+                          out_score + (uint64_t)r * k, pair_j ? pair_j + row : NULL,
+                          pair_feas ? pair_feas + row : NULL, pair_cost ? pair_cost + row : NULL,
+                          &tests);
+        }
+        free(buf);
+    }
+    return tests;
+}
+
+/* Ranking sweep over telemetry scenarios.  The prefix lengths do not depend
+ * on telemetry, so they are matched once and reused for every scenario.
+ * For each scenario the top-k is written to out_idx/out_score
+ * ([n_scen][n_req][k]); out_flips[2*s] counts requests whose selected
+ * decode's tier differs from the tier selected under the snapshot's own
+ * congestion, out_flips[2*s+1] those whose selected decode differs
+ * (a rejection counts as its own tier and index). */
+void orc_rank_sweep(const orc_snapshot *s, const orc_cache *c, const orc_requests *q,
+                    uint32_t n_scen, const float *util_scen, uint32_t k, int32_t *out_idx,
+                    double *out_score, uint64_t *out_flips, int n_threads) {
+    const uint32_t D = s->n_decode, R = q->n_req;
+    uint16_t *jm = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)R * (D ? D : 1));
+    int32_t *base = (int32_t *)malloc(sizeof(int32_t) * (R ? R : 1));
+#ifdef _OPENMP
+    if (n_threads < 1) n_threads = 1;
+#pragma omp parallel num_threads(n_threads)
+#endif
+    {
+        cand *buf = (cand *)malloc(sizeof(cand) * (D ? D : 1));
+        int32_t *idx = (int32_t *)malloc(sizeof(int32_t) * (k ? k : 1));
+        double *sc = (double *)malloc(sizeof(double) * (k ? k : 1));
+        uint64_t dummy = 0;
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 8)
+#endif
+        for (int64_t r = 0; r < (int64_t)R; ++r) {
+            score_request(s, s->util, c, q, (uint32_t)r, NULL, buf, 1, idx, sc,
+                          jm + (uint64_t)r * D, NULL, NULL, &dummy);
+            base[r] = idx[0];
+        }
+        free(buf);
+        free(idx);
+        free(sc);
+    }
+    for (uint32_t sn = 0; sn < n_scen; ++sn) {
+        const float *u = util_scen + (uint64_t)sn * s->n_prefill * D;
+        uint64_t tier_flips = 0, idx_flips = 0;
+#ifdef _OPENMP
+#pragma omp parallel num_threads(n_threads) reduction(+ : tier_flips, idx_flips)
+#endif
+        {
+            cand *buf = (cand *)malloc(sizeof(cand) * (D ? D : 1));
+            uint64_t dummy = 0;
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 8)
+#endif
+            for (int64_t r = 0; r < (int64_t)R; ++r) {
+                uint64_t o = ((uint64_t)sn * R + (uint64_t)r) * k;
+                score_request(s, u, c, q, (uint32_t)r, jm + (uint64_t)r * D, buf, k, out_idx + o,
+                              out_score + o, NULL, NULL, NULL, &dummy);
+                int32_t a = base[r], b = out_idx[o];
+                uint32_t p = q->prefill[r];
+                int ta = a < 0 ? -1 : s->tier_map[(uint64_t)p * D + (uint32_t)a];
+                int tb = b < 0 ? -1 : s->tier_map[(uint64_t)p * D + (uint32_t)b];
+                tier_flips += (ta != tb);
+                idx_flips += (a != b);
+            }
+            free(buf);
+        }
+        if (out_flips) {
+            out_flips[2 * sn] = tier_flips;
+            out_flips[2 * sn + 1] = idx_flips;
+        }
+    }
+    free(jm);
+    free(base);
+}
+
+/* State carried from one batch to the next (streaming workload).
+ * Algorithm 1 increments n_inflight[tau(p, d*)][p] after each selection and
+ * the paper caps the counter (default 16); the transfer-complete callback
+ * decrements it.  Reading used here, with one batch as the unit of time:
+ * transfers of earlier batches have completed, so after a batch
+ *   n_inflight[tau][p] = min(cap, #selections of the batch from p on tau);
+ * each decode serves up to `mu` queued requests per batch interval,
+ *   q_d = max(0, q_d + admitted_d - mu);
+ * the KV bytes admitted in this batch occupy decode memory until the next
+ * batch completes them,
+ *   m_d = max(0, m_d - A_d) + A_prev_d,   A_prev_d <- A_d,
+ * with A_d the sum of s_eff over the requests admitted to d.
+ * All of it is integer arithmetic. */
+void orc_commit(const orc_snapshot *s, const orc_cache *c, const orc_requests *q,
+                const int32_t *sel, uint32_t cap, uint32_t mu, uint16_t *n_inflight,
+                uint32_t *queue_depth, uint64_t *free_mem, uint64_t *admitted_prev) {
+    const uint32_t P = s->n_prefill, D = s->n_decode;
+    uint64_t *cnt = (uint64_t *)calloc((size_t)4 * P, sizeof(uint64_t));
+    uint64_t *adm = (uint64_t *)calloc(D ? D : 1, sizeof(uint64_t));
+    uint64_t *bytes = (uint64_t *)calloc(D ? D : 1, sizeof(uint64_t));
+    for (uint32_t r = 0; r < q->n_req; ++r) {
+        int32_t d = sel[r];
+        if (d < 0) continue;
+        uint32_t p = q->prefill[r];
+        int tau = s->tier_map[(uint64_t)p * D + (uint32_t)d];
+        uint32_t t;
+        uint64_t a = q->hash_off[r];
+        uint32_t n = (uint32_t)(q->hash_off[r + 1] - a);
+        uint32_t j = prefix_blocks(c, (uint32_t)d, q->hashes + a, n, &t);
+        uint64_t s_eff = s->kv_bytes_per_token * ((uint64_t)q->len_tokens[r] - (uint64_t)s->block_tokens * j);
+        cnt[(uint64_t)tau * P + p] += 1;
+        adm[d] += 1;
+        bytes[d] += s_eff;
+    }
+    for (uint64_t i = 0; i < (uint64_t)4 * P; ++i) n_inflight[i] = (uint16_t)(cnt[i] < cap ? cnt[i] : cap);
+    for (uint32_t d = 0; d < D; ++d) {
+        int64_t nq = (int64_t)queue_depth[d] + (int64_t)adm[d] - (int64_t)mu;
+        queue_depth[d] = (uint32_t)(nq < 0 ? 0 : nq);
+        uint64_t m = free_mem[d];
+        m = (m > bytes[d]) ? m - bytes[d] : 0;
+        free_mem[d] = m + admitted_prev[d];
+        admitted_prev[d] = bytes[d];
+    }
+    free(cnt);
+    free(adm);
+    free(bytes);
+}
+
+/* The first-miss prefix length of one hash run against one decode's set
+ * (exposed for tests). */
+uint32_t orc_prefix_len(const orc_cache *c, uint32_t d, const uint64_t *h, uint32_t n) {
+    uint32_t t;
+    return prefix_blocks(c, d, h, n, &t);
+}
+
+int orc_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

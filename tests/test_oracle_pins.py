@@ -1,0 +1,527 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle (``oracle/``) against something other than
+itself: values the paper prints (``tests/golden/``), the two propositions,
+closed forms of the component equations computed by hand, exact rational
+brute force and set-membership brute force on tiny inputs, and invariants.
+The choice is such that a dropped term, a wrong sign, a wrong index or a
+transposed operand in the oracle fails at least one of them.
+"""
+import itertools
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------- helpers
+
+def tiny_snapshot(P, D, tier_map, util, *, bw=(900e9, 50e9, 25e9, 12.5e9),
+                  lat=(0.0, 0.0, 0.0, 0.0), n_inflight=None, free_mem=None, queue=None,
+                  batch=None, a=0.05, b=0.0, beta_max=64, alpha=1.0, m_min=0, bpt=1,
+                  block_tokens=1):
+    return dict(
+        n_prefill=P, n_decode=D,
+        tier_map=np.asarray(tier_map, dtype=np.uint8).reshape(-1),
+        util=np.asarray(util, dtype=np.float32).reshape(-1),
+        n_inflight=(np.zeros(4 * P, np.uint16) if n_inflight is None
+                    else np.asarray(n_inflight, np.uint16).reshape(-1)),
+        tier_bw=np.asarray(bw, dtype=np.float64), tier_lat=np.asarray(lat, dtype=np.float64),
+        free_mem=(np.full(D, 1 << 62, np.uint64) if free_mem is None
+                  else np.asarray(free_mem, np.uint64)),
+        queue_depth=np.zeros(D, np.uint32) if queue is None else np.asarray(queue, np.uint32),
+        batch_size=(np.full(D, beta_max, np.uint32) if batch is None
+                    else np.asarray(batch, np.uint32)),
+        t_iter_a=a, t_iter_b=b, beta_max=beta_max, alpha=alpha, m_min=m_min,
+        kv_bytes_per_token=bpt, block_tokens=block_tokens)
+
+
+def requests(rows):
+    """rows: list of (prefill, len_tokens, [hashes])"""
+    off = np.zeros(len(rows) + 1, np.uint64)
+    off[1:] = np.cumsum([len(h) for _, _, h in rows])
+    hs = np.array([x for _, _, h in rows for x in h], dtype=np.uint64)
+    return dict(prefill=np.array([p for p, _, _ in rows], np.uint32),
+                len_tokens=np.array([l for _, l, _ in rows], np.uint32),
+                hash_off=off, hashes=hs)
+
+
+def caches(sets):
+    off = np.zeros(len(sets) + 1, np.uint64)
+    off[1:] = np.cumsum([len(s) for s in sets])
+    hs = np.array([x for s in sets for x in s], dtype=np.uint64)
+    return dict(hash_off=off, hashes=hs)
+
+
+# ---------------------------------------------------------------- paper values
+
+def _worked_example(c3):
+    g = _gold("worked_example.json")
+    bw = (1e12, 1e12, g["tier_bw_bytes_per_s"]["2"], g["tier_bw_bytes_per_s"]["3"])
+    n_inf = np.zeros(4, np.uint16)
+    n_inf[2] = g["n_inflight"]["2"]
+    n_inf[3] = g["n_inflight"]["3"]
+    # bpt = 1e9 bytes/token with 1-token blocks: a 10-token request is 10 GB;
+    # d1 holds the first 5 blocks (50 % hit), d2 the first 9 (90 % hit).
+    h = list(range(101, 111))
+    snap = tiny_snapshot(1, 2, [2, 3], [g["congestion"]["2"], c3], bw=bw, n_inflight=n_inf,
+                         alpha=0.0, bpt=10 ** 9)
+    out = oracle.select(snap, caches([h[:5], h[:9]]), requests([(0, 10, h)]), k=2, pairs=True)
+    return g, snap, out
+
+
+def test_worked_example_transfer_times():
+    g, _, out = _worked_example(0.2)
+    e = g["expected"]
+    assert out["j"][0].tolist() == [5, 9]
+    s_eff = np.array([10 - 5, 10 - 9]) * 1e9
+    assert s_eff.tolist() == [g["s_eff_bytes"]["d1"], g["s_eff_bytes"]["d2"]]
+    np.testing.assert_allclose(out["cost"][0], [e["t_transfer_d1"], e["t_transfer_d2"]], rtol=1e-7)
+    np.testing.assert_allclose(s_eff / out["cost"][0], [e["b_eff_d1"], e["b_eff_d2"]], rtol=1e-7)
+    assert out["idx"][0, 0] == 1  # d2 wins
+    assert out["cost"][0, 0] / out["cost"][0, 1] == pytest.approx(e["ratio"], rel=1e-7)
+
+
+def test_worked_example_perturbed_congestion():
+    g, _, out = _worked_example(g_c3 := _gold("worked_example.json")["perturbed"]["congestion_tier3"])
+    pert = g["perturbed"]
+    b_eff_d2 = 1e9 / out["cost"][0, 1]
+    assert round(b_eff_d2 / 1e9, pert["b_eff_d2_printed_decimals"]) == pert["b_eff_d2_printed"]
+    assert out["cost"][0, 1] == pytest.approx(pert["t_transfer_d2"], rel=1e-7)
+    ratio = out["cost"][0, 0] / out["cost"][0, 1]
+    assert round(ratio) == pert["ratio_printed"]
+    assert out["idx"][0, 0] == 1
+    assert g_c3 == 0.5
+
+
+def test_worked_example_with_latencies():
+    g = _gold("worked_example.json")
+    lat = g["latencies_s_for_full_formula"]
+    h = list(range(101, 111))
+    snap = tiny_snapshot(1, 2, [2, 3], [0.2, 0.2],
+                         bw=(1e12, 1e12, 6.25e9, 3.125e9), lat=(0, 0, lat["2"], lat["3"]),
+                         n_inflight=[0, 0, 1, 0], alpha=0.0, bpt=10 ** 9)
+    out = oracle.select(snap, caches([h[:5], h[:9]]), requests([(0, 10, h)]), k=2, pairs=True)
+    np.testing.assert_allclose(out["cost"][0], [2.0 + lat["2"], 0.4 + lat["3"]], rtol=1e-7)
+
+
+def test_intro_transfer_time():
+    g = _gold("paper_constants.json")["intro_transfer"]
+    snap = tiny_snapshot(1, 1, [3], [0.0], bw=(1, 1, 1, g["link_gbps"] * 1e9 / 8), alpha=0.0,
+                         bpt=10 ** 9)
+    out = oracle.select(snap, caches([[7]]), requests([(0, 10, [1] * 0 + list(range(11, 21)))]),
+                        k=1, pairs=True)
+    assert out["cost"][0, 0] == pytest.approx(g["seconds"], rel=1e-12)
+
+
+def test_kv_bytes_per_token_eq1():
+    from paper_2606_03910_amd import workload as W
+    g = _gold("paper_constants.json")["kv_bytes"]
+    assert W.KV_LLAMA3_70B == g["aggregate_kib_per_token"] * 1024
+    assert W.CONFIGS["c1"].kv_bytes_per_token == g["tp4_shard_kib_per_token"] * 1024
+
+
+# ---------------------------------------------------------------- Proposition 1
+
+def _two_candidate(rho1, rho2, c1, c3, k, q1=0, q2=0, n_blocks=20, a=0.05, bpt=1000, scale=1):
+    """d0 same-rack (tier 1), d1 cross-pod (tier 3); B1 = k B3."""
+    B3 = 1e6
+    h = list(range(1, n_blocks + 1))
+    j1, j2 = int(round(rho1 * n_blocks)), int(round(rho2 * n_blocks))
+    snap = tiny_snapshot(1, 2, [1, 3], [c1, c3], bw=(1e12, k * B3, 1e12, B3),
+                         queue=[64 + q1, 64 + q2], batch=[64, 64], a=a, b=0.0,
+                         bpt=bpt * scale)
+    out = oracle.select(snap, caches([h[:j1], h[:j2]]), requests([(0, n_blocks, h)]), k=2,
+                        pairs=True)
+    return snap, out
+
+
+def test_prop1_numerical_example():
+    g = _gold("paper_constants.json")["prop1_example"]
+    snap, out = _two_candidate(g["rho1"], g["rho2"], 0.3, 0.3, g["k"], a=0.0)
+    t1, t2 = out["cost"][0]
+    # the cache-only choice (larger hit) is d1 = cross-pod; the oracle picks d0
+    assert out["j"][0, 1] > out["j"][0, 0]
+    assert out["idx"][0, 0] == 0
+    assert t2 / t1 == pytest.approx(g["transfer_time_ratio"], rel=1e-6)
+    lhs = 1 - g["rho1"]
+    rhs = g["k"] * (1 - g["rho2"])
+    assert (lhs, rhs) == (g["lhs"], g["rhs"])
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_prop1_inequality_decides_the_oracle(seed):
+    """Proposition 1: d_same-rack beats d_cross-pod iff
+    (1-rho1) < k (1-c1)/(1-c3) (1-rho2) + B1 (1-c1)/s (Tq2 - Tq1)."""
+    rng = np.random.default_rng(seed)
+    n = 40
+    checked = 0
+    for _ in range(200):
+        j1, j2 = sorted(rng.integers(0, n + 1, 2))
+        rho1, rho2 = j1 / n, j2 / n
+        c1, c3 = np.float32(rng.uniform(0, 0.9)), np.float32(rng.uniform(0, 0.9))
+        k = float(rng.choice([1, 2, 4, 8]))
+        q1, q2 = (int(x) for x in rng.integers(0, 6, 2))
+        a = 0.01
+        snap, out = _two_candidate(rho1, rho2, c1, c3, k, q1=q1, q2=q2, n_blocks=n, a=a)
+        B1 = k * 1e6
+        s = snap["kv_bytes_per_token"] * n
+        lhs = 1 - rho1
+        rhs = k * (1 - float(c1)) / (1 - float(c3)) * (1 - rho2) + B1 * (1 - float(c1)) / s * (
+            q2 * a - q1 * a)
+        if abs(lhs - rhs) < 1e-9:
+            continue
+        assert (out["idx"][0, 0] == 0) == (lhs < rhs)
+        checked += 1
+    assert checked > 150
+
+
+def test_prop1_regret_grows_linearly_with_context():
+    """Cache-only choice regret is affine and increasing in the context length."""
+    reg = []
+    for scale in (1, 2, 4, 8):
+        _, out = _two_candidate(0.0, 0.5, 0.2, 0.2, 4.0, n_blocks=16, scale=scale)
+        c = out["cost"][0]
+        reg.append(c[1] - c[0])
+    reg = np.array(reg)
+    assert np.all(np.diff(reg) > 0)
+    np.testing.assert_allclose(reg / reg[0], [1, 2, 4, 8], rtol=1e-9)
+
+
+# ---------------------------------------------------------------- Proposition 2
+
+def test_prop2_numerical_bound():
+    g = _gold("paper_constants.json")["prop2_example"]
+    Bf, Bs = float(g["bw_ratio"]), 1.0
+    eps = (Bf * (1 - g["c_fast"]) - Bs * (1 - g["c_slow"])) / (Bf + Bs)
+    assert eps == pytest.approx(g["epsilon_bound"], abs=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_prop2_no_inversion_below_bound(seed):
+    """Equal non-cached bytes, no in-flight transfers, no load term: the
+    oracle's choice between a faster and a slower tier is unchanged by any
+    congestion error below the bound, and the worst-case error just above it
+    inverts the choice."""
+    rng = np.random.default_rng(100 + seed)
+    h = [5, 6, 7, 8]
+    inverted = 0
+    for _ in range(100):
+        Bf, Bs = 1e9 * rng.uniform(1, 8), 1e9
+        cf, cs = rng.uniform(0, 0.9, 2)
+        if Bf * (1 - cf) <= Bs * (1 - cs):
+            continue
+        bound = (Bf * (1 - cf) - Bs * (1 - cs)) / (Bf + Bs)
+        mk = lambda uf, us: tiny_snapshot(1, 2, [1, 3], [uf, us], bw=(1, Bf, 1, Bs),
+                                          alpha=0.0, bpt=10 ** 6)
+        cs_, rq = caches([[], []]), requests([(0, 4, h)])
+        truth = oracle.select(mk(cf, cs), cs_, rq)["idx"][0, 0]
+        assert truth == 0
+        for _ in range(10):
+            e = rng.uniform(0, 0.98) * bound
+            uf = np.clip(cf + rng.uniform(-e, e), 0, 0.99)
+            us = np.clip(cs + rng.uniform(-e, e), 0, 0.99)
+            assert oracle.select(mk(uf, us), cs_, rq)["idx"][0, 0] == truth
+        e = bound * 1.05
+        if cf + e < 0.99 and cs - e > 0:
+            inverted += oracle.select(mk(cf + e, cs - e), cs_, rq)["idx"][0, 0] == 1
+    assert inverted > 10
+
+
+# ---------------------------------------------------------------- tiers
+
+def test_tier_ordering_at_equal_load():
+    """Same hit, congestion, in-flight count and load: cost strictly grows
+    with the tier (same node < same leaf < same pod < cross pod), whatever
+    position each tier's decode has in the pool."""
+    from paper_2606_03910_amd import workload as W
+    cfg = W.CONFIGS["c0"]
+    h = list(range(1, 9))
+    for perm in itertools.permutations(range(4)):
+        snap = tiny_snapshot(1, 4, list(perm), [0.3] * 4, bw=cfg.tier_bw, lat=cfg.tier_lat,
+                             bpt=cfg.kv_bytes_per_token, block_tokens=512)
+        out = oracle.select(snap, caches([h[:3]] * 4), requests([(0, 8 * 512 + 17, h)]), k=4,
+                            pairs=True)
+        cost_by_tier = [out["cost"][0, perm.index(t)] for t in range(4)]
+        assert all(x < y for x, y in zip(cost_by_tier, cost_by_tier[1:]))
+        assert out["idx"][0].tolist() == [perm.index(t) for t in range(4)]
+
+
+def test_inflight_counter_is_tier_major_per_prefill():
+    """n_inflight is indexed [tier][prefill]: only (p=1, tier 2) is derated."""
+    P, D = 2, 4
+    tmap = np.array([[0, 1, 2, 3], [0, 1, 2, 3]], np.uint8)
+    n = np.zeros((4, P), np.uint16)
+    n[2, 1] = 3
+    bw = (8e9, 4e9, 2e9, 1e9)
+    snap = tiny_snapshot(P, D, tmap, np.full(P * D, 0.5), bw=bw, n_inflight=n, alpha=0.0,
+                         bpt=10 ** 6)
+    rq = requests([(0, 4, [1, 2, 3, 4]), (1, 4, [1, 2, 3, 4])])
+    out = oracle.select(snap, caches([[]] * 4), rq, k=1, pairs=True)
+    s = 4e6
+    want0 = [s / (b * 0.5) for b in bw]
+    want1 = list(want0)
+    want1[2] = s / (bw[2] * 0.5 / 4)
+    np.testing.assert_allclose(out["cost"][0], want0, rtol=1e-12)
+    np.testing.assert_allclose(out["cost"][1], want1, rtol=1e-12)
+
+
+# ---------------------------------------------------------------- load terms
+
+def test_queue_and_decode_terms_closed_form():
+    """t_iter(beta) = a + b beta with a = 0.03, b = 0.001, beta_max = 64:
+    q = 10, beta = 60 -> 6 blocked, T_queue = 6 * 0.09 = 0.54,
+    T_decode = t_iter(61) = 0.091; q = 3, beta = 60 -> nothing blocked."""
+    h = [1, 2]
+    snap = tiny_snapshot(1, 3, [0, 0, 0], [0, 0, 0], queue=[10, 3, 0], batch=[60, 60, 64],
+                         a=0.03, b=0.001, beta_max=64, bpt=1)
+    rq = requests([(0, 2, h)])  # fully cached below: no transfer bytes
+    out = oracle.select(snap, caches([h, h, h]), rq, k=3, pairs=True)
+    np.testing.assert_allclose(out["cost"][0], [0.631, 0.091, 0.095], rtol=1e-12, atol=1e-15)
+    snap["alpha"] = 2.0
+    out = oracle.select(snap, caches([h, h, h]), rq, k=3, pairs=True)
+    np.testing.assert_allclose(out["cost"][0], [1.262, 0.182, 0.19], rtol=1e-12)
+
+
+def test_alpha_zero_is_pure_network_cost():
+    h = list(range(1, 11))
+    snap = tiny_snapshot(1, 2, [2, 2], [0.1, 0.1], queue=[1000, 0], alpha=0.0, bpt=10 ** 6)
+    out = oracle.select(snap, caches([h[:8], h[:2]]), requests([(0, 10, h)]), k=1, pairs=True)
+    assert out["idx"][0, 0] == 0
+    snap["alpha"] = 1.0
+    out = oracle.select(snap, caches([h[:8], h[:2]]), requests([(0, 10, h)]), k=1)
+    assert out["idx"][0, 0] == 1
+
+
+def test_equal_tiers_rank_by_cache_then_load():
+    """Equal bandwidth and latency on every tier and no congestion: the
+    network term only sees the non-cached bytes, so the largest hit wins and
+    equal hits fall back to the load term (the cache+load ordering)."""
+    h = list(range(1, 11))
+    snap = tiny_snapshot(1, 4, [0, 1, 2, 3], [0, 0, 0, 0], bw=(1e9,) * 4, lat=(1e-6,) * 4,
+                         queue=[66, 65, 66, 64], batch=[64] * 4, bpt=10 ** 9)
+    sets = [h[:3], h[:7], h[:7], h[:1]]
+    out = oracle.select(snap, caches(sets), requests([(0, 10, h)]), k=4, pairs=True)
+    assert out["idx"][0].tolist() == [1, 2, 0, 3]
+
+
+# ---------------------------------------------------------------- feasibility
+
+def test_feasibility_boundary_and_rejection():
+    """m_d >= s_eff + m_min, exactly at the boundary; no feasible -> -1, +inf."""
+    h = [1, 2, 3, 4]
+    bpt, m_min = 1000, 500
+    s_eff = bpt * (4 - 1)  # one cached block
+    snap = tiny_snapshot(1, 3, [0, 0, 0], [0, 0, 0],
+                         free_mem=[s_eff + m_min, s_eff + m_min - 1, 2 ** 64 - 1],
+                         m_min=m_min, bpt=bpt)
+    out = oracle.select(snap, caches([h[:1]] * 3), requests([(0, 4, h)]), k=3, pairs=True)
+    assert out["feasible"][0].tolist() == [1, 0, 1]
+    assert out["idx"][0].tolist() == [0, 2, -1]
+    assert np.isinf(out["score"][0, 2])
+    snap["m_min"] = 2 ** 63
+    out = oracle.select(snap, caches([h[:1]] * 3), requests([(0, 4, h)]), k=2, pairs=True)
+    assert out["feasible"][0].tolist() == [0, 0, 1]
+    snap["free_mem"] = np.array([5, 6, 7], np.uint64)
+    out = oracle.select(snap, caches([h[:1]] * 3), requests([(0, 4, h)]), k=2, pairs=True)
+    assert out["idx"][0].tolist() == [-1, -1] and np.all(np.isinf(out["score"][0]))
+
+
+def test_full_hit_has_no_transfer_bytes_but_a_partial_block_does():
+    """n_r = floor(l_r / B_tok): the trailing partial block is never cached."""
+    h = [9, 8]
+    snap = tiny_snapshot(1, 1, [0], [0], bw=(1e3,) * 4, alpha=0.0, bpt=1, block_tokens=16)
+    out = oracle.select(snap, caches([h]), requests([(0, 32, h), (0, 40, h)]), k=1, pairs=True)
+    assert out["j"][:, 0].tolist() == [2, 2]
+    np.testing.assert_allclose(out["cost"][:, 0], [0.0, 8 / 1e3])
+
+
+# ---------------------------------------------------------------- prefix match
+
+def _brute_lcp(hs, kset):
+    j = 0
+    while j < len(hs) and hs[j] in kset:
+        j += 1
+    return j
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_prefix_match_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    universe = rng.integers(1, 2 ** 63, 60).astype(np.uint64)
+    D = 7
+    sets = []
+    for d in range(D):
+        if d % 2 == 0:   # prefix-closed sets: leading segment of the run
+            sets.append(list(universe[: rng.integers(0, 30)]))
+        else:            # arbitrary subsets: holes stop the scan
+            sets.append(list(universe[rng.random(60) < 0.7]))
+    rows = []
+    for _ in range(25):
+        n = int(rng.integers(0, 20))
+        start = 0 if rng.random() < 0.7 else int(rng.integers(0, 5))
+        hs = list(universe[start:start + n])
+        rows.append((0, n * 3 + int(rng.integers(0, 3)), hs))
+    snap = tiny_snapshot(1, D, [0] * D, [0] * D, block_tokens=3)
+    out = oracle.select(snap, caches(sets), requests(rows), k=1, pairs=True)
+    tests = 0
+    for r, (_, _, hs) in enumerate(rows):
+        for d in range(D):
+            j = _brute_lcp(hs, set(sets[d]))
+            assert out["j"][r, d] == j
+            if d % 2 == 0 and hs and hs[0] == universe[0]:
+                # a prefix-closed set covering the run's start: j = overlap depth
+                assert j == min(len(hs), len(sets[d]))
+            tests += min(j + 1, len(hs))
+    assert out["tests"] == tests
+
+
+def test_prefix_match_first_miss_not_longest_run():
+    h = [11, 12, 13, 14, 15]
+    c = oracle.Cache(caches([[12, 13, 14, 15], [11, 13, 14, 15], [11, 12, 13, 14, 15]]))
+    assert [c.prefix_len(d, h) for d in range(3)] == [0, 1, 5]
+
+
+def test_prefix_match_monotone_in_resident_set():
+    rng = np.random.default_rng(7)
+    h = list(range(1, 30))
+    base = set(rng.choice(h, 15, replace=False).tolist())
+    grown = base | set(rng.choice(h, 10, replace=False).tolist())
+    c = oracle.Cache(caches([sorted(base), sorted(grown)]))
+    for start in range(10):
+        run = h[start:]
+        assert c.prefix_len(0, run) <= c.prefix_len(1, run)
+
+
+# ---------------------------------------------------------------- exact brute force
+
+def _exact_costs(snap, sets, rows):
+    """Eq. (5) over every decode in exact rational arithmetic."""
+    D, P = snap["n_decode"], snap["n_prefill"]
+    res = []
+    for p, l, hs in rows:
+        costs = []
+        for d in range(D):
+            j = _brute_lcp(hs, set(sets[d]))
+            s_eff = snap["kv_bytes_per_token"] * (l - snap["block_tokens"] * j)
+            feas = int(snap["free_mem"][d]) >= s_eff + snap["m_min"]
+            tau = int(snap["tier_map"][p * D + d])
+            c = Fraction(float(snap["util"][p * D + d]))
+            n = int(snap["n_inflight"][tau * P + p])
+            beff = Fraction(float(snap["tier_bw"][tau])) * (1 - c) / (1 + n)
+            tx = s_eff / beff + Fraction(float(snap["tier_lat"][tau]))
+            q, beta = int(snap["queue_depth"][d]), int(snap["batch_size"][d])
+            A, B = Fraction(snap["t_iter_a"]), Fraction(snap["t_iter_b"])
+            tq = max(0, q - (snap["beta_max"] - beta)) * (A + B * beta)
+            td = A + B * (beta + 1)
+            costs.append((tx + Fraction(snap["alpha"]) * (tq + td), feas))
+        res.append(costs)
+    return res
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_exact_rational_brute_force_small_cluster(seed):
+    """16-GPU two-pod cluster with four prefill and twelve decode instances."""
+    from paper_2606_03910_amd import workload as W
+    cl = W.Cluster(4, 2, 1, 2, prefill_every=4)
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=cl, n_requests=30, cache_per_decode=64,
+                   n_prefixes=12, len_median=3000.0)
+    snap = W.make_snapshot(cfg, seed, inflight="random")
+    snap["t_iter_b"] = 0.0007
+    ch = W.prefix_chains(cfg, seed)
+    req = W.make_requests(cfg, seed, chains=ch)
+    cache = W.make_caches(cfg, seed, chains=ch)
+    D = cfg.n_decode
+    assert (cfg.n_prefill, D) == (4, 12)
+    sets = [cache["hashes"][cache["hash_off"][d]:cache["hash_off"][d + 1]].tolist()
+            for d in range(D)]
+    rows = [(int(req["prefill"][r]), int(req["len_tokens"][r]),
+             req["hashes"][req["hash_off"][r]:req["hash_off"][r + 1]].tolist())
+            for r in range(cfg.n_requests)]
+    out = oracle.select(snap, cache, req, k=3, pairs=True)
+    exact = _exact_costs(snap, sets, rows)
+    for r in range(cfg.n_requests):
+        feas = [d for d in range(D) if exact[r][d][1]]
+        assert out["feasible"][r].tolist() == [int(exact[r][d][1]) for d in range(D)]
+        for d in range(D):
+            assert float(exact[r][d][0]) == pytest.approx(out["cost"][r, d], rel=1e-13)
+        order = sorted(feas, key=lambda d: (exact[r][d][0], d))[:3]
+        order += [-1] * (3 - len(order))
+        assert out["idx"][r].tolist() == order
+
+
+# ---------------------------------------------------------------- ranking sweep
+
+def test_rank_sweep_noise_free_scenario_has_no_flips():
+    from paper_2606_03910_amd import workload as W
+    cfg = W.scaled(W.CONFIGS["c3"], n_requests=200, n_scenarios=4)
+    snap = W.make_snapshot(cfg, 1)
+    ch = W.prefix_chains(cfg, 1)
+    req = W.make_requests(cfg, 1, chains=ch)
+    cache = W.make_caches(cfg, 1, chains=ch)
+    util = np.stack([snap["util"]] * 2)
+    sw = oracle.rank_sweep(snap, cache, req, util, k=3)
+    base = oracle.select(snap, cache, req, k=3)
+    assert sw["flips"].tolist() == [[0, 0], [0, 0]]
+    for s in range(2):
+        assert (sw["idx"][s] == base["idx"]).all()
+        np.testing.assert_array_equal(sw["score"][s], base["score"])
+
+
+def test_rank_sweep_congested_fast_tiers_flip_to_slow_ones():
+    """Saturating every tier below cross-pod moves selections across tiers."""
+    from paper_2606_03910_amd import workload as W
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=W.Cluster(8, 2, 1, 2), n_requests=300)
+    snap = W.make_snapshot(cfg, 2)
+    ch = W.prefix_chains(cfg, 2)
+    req = W.make_requests(cfg, 2, chains=ch)
+    cache = W.make_caches(cfg, 2, chains=ch)
+    u = snap["util"].copy()
+    tm = snap["tier_map"]
+    u2 = np.where(tm < 3, 0.99, 0.0).astype(np.float32)
+    sw = oracle.rank_sweep(snap, cache, req, np.stack([u, u2]), k=1)
+    base = oracle.select(snap, cache, req, k=1)
+    assert sw["flips"][0].tolist() == [0, 0]
+    sel_tiers = tm.reshape(cfg.n_prefill, -1)[req["prefill"], sw["idx"][1, :, 0]]
+    base_tiers = tm.reshape(cfg.n_prefill, -1)[req["prefill"], base["idx"][:, 0]]
+    assert int(sw["flips"][1, 0]) == int((sel_tiers != base_tiers).sum()) > 0
+    assert int(sw["flips"][1, 1]) == int((sw["idx"][1, :, 0] != base["idx"][:, 0]).sum())
+
+
+# ---------------------------------------------------------------- between-batch update
+
+def test_commit_closed_form():
+    """Hand-worked between-batch update (counter cap 16, service mu = 2)."""
+    cap = _gold("paper_constants.json")["counter_cap"]["value"]
+    P, D = 2, 3
+    tmap = np.array([[0, 1, 3], [2, 0, 1]], np.uint8)
+    snap = tiny_snapshot(P, D, tmap, np.zeros(6), bpt=100, block_tokens=1)
+    h = [1, 2, 3]
+    cache = caches([[1], [1, 2, 3], []])
+    rows = [(0, 3, h)] * 18 + [(1, 3, h), (1, 5, h), (0, 3, h)]
+    sel = [2] * 18 + [0, 0, -1]
+    state = dict(n_inflight=np.full(4 * P, 7, np.uint16), queue_depth=np.array([1, 5, 0], np.uint32),
+                 free_mem=np.array([10 ** 6, 10 ** 6, 1000], np.uint64),
+                 admitted_prev=np.array([0, 7, 11], np.uint64))
+    st = oracle.commit(snap, cache, requests(rows), np.array(sel, np.int32), cap, 2, state)
+    # p=0 -> d2 is tier 3 (18 selections, capped); p=1 -> d0 is tier 2 (2)
+    want_n = np.zeros((4, P), np.uint16)
+    want_n[3, 0] = cap
+    want_n[2, 1] = 2
+    assert st["n_inflight"].tolist() == want_n.reshape(-1).tolist()
+    assert st["queue_depth"].tolist() == [1 + 2 - 2, max(0, 5 - 2), 18 - 2]
+    # d0: two requests with j = 1: s_eff = 100*(3-1) + 100*(5-1) = 600
+    # d2: 18 requests with j = 0: 18 * 300 = 5400 > 1000 -> clamps to 0
+    assert st["free_mem"].tolist() == [10 ** 6 - 600 + 0, 10 ** 6 + 7, 0 + 11]
+    assert st["admitted_prev"].tolist() == [600, 0, 5400]
