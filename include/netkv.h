@@ -1,0 +1,201 @@
+/*
+ * netkv.h -- C ABI of libnetkv, NetKV decode-instance selection on MI355X.
+ *
+ * Method: "NetKV: Network-Aware Decode Instance Selection for Disaggregated
+ * LLM Inference".  For a request that finished prefill on instance p, every
+ * decode instance d is scored with Eq. (5):
+ *     C(d) = s_eff(d) / B_eff(p,d) + L_tau          (Eqs. (3), (4))
+ *          + alpha * (T_queue(d) + T_decode(d))      (Sec. IV-B, Eqs. (6)-(7))
+ * with s_eff(d) = bpt * (l_r - B_tok * j) (Eq. (2), j = leading blocks of the
+ * request's hash run resident on d, Sec. III-B) under the memory feasibility
+ * mask m_d >= s_eff(d) + m_min (Eq. (5) feasible set), and the minimum-cost
+ * feasible d is selected, ties to the lowest index (Algorithm 1).  A batch of
+ * requests is scored against one telemetry snapshot; the in-flight counter
+ * update of Algorithm 1 is applied between batches (netkv_commit_batch).
+ *
+ * Conventions for every call:
+ *   - Returns NETKV_OK (0) or a negative status; netkv_last_error(h) gives
+ *     the message of the last failing call on h.
+ *   - Every argument is validated before anything is launched, so a call
+ *     that returns an error has written no output.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *   - Units: bytes, seconds, bytes per second.
+ *   - A handle is used by one host thread at a time; handles are independent.
+ *   - Output bytes are identical from run to run (no floating-point atomics;
+ *     reductions are minima over packed (score, index) keys).
+ */
+#ifndef NETKV_H
+#define NETKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct netkv_ctx *netkv_handle;
+typedef int32_t netkv_status;
+
+enum {
+    NETKV_OK = 0,
+    NETKV_EINVAL = -1,     /* bad argument or bad input values */
+    NETKV_ENOTREADY = -2,  /* select/sweep/commit before both loads */
+    NETKV_ENOMEM = -3,     /* device allocation failed */
+    NETKV_EDEVICE = -4,    /* a HIP runtime error */
+    NETKV_ECAPACITY = -5   /* a resident-set table cannot be built */
+};
+
+/* Create a handle bound to HIP device `device`.  *out receives the handle. */
+netkv_status netkv_create(netkv_handle *out, int device);
+
+/* Release the handle and every device buffer it owns (waits for its work). */
+void netkv_destroy(netkv_handle h);
+
+/* Message of the last failing call on h (empty string if none; never NULL).
+ * The string stays valid until the next call on h. */
+const char *netkv_last_error(netkv_handle h);
+
+/*
+ * One telemetry snapshot: the network cost oracle's maps (Sec. III-E:
+ * tier map, tier bandwidth, tier latency, congestion) plus the scheduler's
+ * view of decode state (Sec. III-C) and the cost-model parameters.
+ * Array pointers may be host or device memory; they are copied.
+ */
+typedef struct {
+    uint32_t n_prefill, n_decode;   /* P >= 1, D >= 1 */
+    const uint8_t *tier_map;        /* [P*D], row-major by prefill: tau(p,d) in 0..3 */
+    const float *util;              /* [P*D] congestion c(p,d) in [0,1) for the pair's tier
+                                       (per-pair form of the per-tier c_tau) */
+    double tier_bw[4];              /* B_k > 0, bytes/s (the oracle's Gbps / 8 * 1e9) */
+    double tier_lat[4];             /* L_k >= 0, seconds (the oracle's microseconds * 1e-6) */
+    const uint16_t *n_inflight;     /* [4*P], tier-major: n_inflight[tau*P + p] (Eq. (4)) */
+    const uint64_t *free_mem;       /* [D] m_d, bytes */
+    const uint32_t *queue_depth;    /* [D] q_d */
+    const uint32_t *batch_size;     /* [D] beta_d <= beta_max */
+    double t_iter_a, t_iter_b;      /* t_iter(beta) = a + b*beta, seconds (Sec. III-C), >= 0 */
+    uint32_t beta_max;              /* maximum batch size (Sec. IV-B) */
+    double alpha;                   /* weight of T_queue + T_decode; 1 is Eq. (5) exactly, >= 0 */
+    uint64_t m_min;                 /* per-instance memory reserve, bytes (Eq. (5)) */
+    uint64_t kv_bytes_per_token;    /* per prefill/decode GPU pair (Eq. (1) / TP), < 2^32 */
+    uint32_t block_tokens;          /* B_tok >= 1, tokens per hashed block (Sec. III-B) */
+} netkv_oracle_t;
+
+/* Load a snapshot (synchronous: returns after the copy and validation are
+ * complete on `stream`, so the caller may free its arrays on return).
+ * Also resets the between-batch state (n_inflight, queue_depth, free_mem
+ * from the snapshot; admitted bytes of the previous batch to 0).
+ * EINVAL: NULL pointer, P or D zero, tier > 3, util outside [0,1) or NaN,
+ * beta_d > beta_max, non-positive or non-finite bandwidth, negative or
+ * non-finite latency/a/b/alpha, block_tokens 0, kv_bytes_per_token >= 2^32,
+ * or D different from a loaded cache. */
+netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *stream);
+
+/* Replace only the congestion matrix util [P*D] of the loaded snapshot
+ * (a refreshed or stale congestion map; Sec. V-D).  Synchronous; host or
+ * device pointer.  EINVAL for values outside [0,1) or NaN; ENOTREADY with
+ * no snapshot loaded. */
+netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stream);
+
+/* Load the resident block-hash sets K_d (Sec. III-B, III-C) of n_decode
+ * decode instances as CSR: the hashes of decode d are
+ * hashes[hash_off[d] .. hash_off[d+1]), n_hashes = hash_off[n_decode].
+ * Host or device pointers.  Value 0 is reserved (EINVAL); repeated hashes
+ * of one decode are allowed and count once.  Builds one open-addressed
+ * table per decode with at most `max_load_factor` (0 < lf < 1) occupancy.
+ * Synchronous.  EINVAL: bad CSR, hash 0, lf out of range, D different
+ * from a loaded snapshot; ECAPACITY: a table would need more than 2^31
+ * slots; ENOMEM: out of device memory. */
+netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t *hash_off,
+                              const uint64_t *hashes, uint64_t n_hashes, float max_load_factor,
+                              void *stream);
+
+/* A batch of requests (DEVICE pointers), Sec. III-B: request r finished
+ * prefill on instance prefill[r] < P, has l_r = len_tokens[r] >= 1 input
+ * tokens and the block-hash run hashes[hash_off[r] .. hash_off[r+1]) of
+ * length n_r = floor(l_r / B_tok), block 0 first; n_hashes bounds the
+ * hashes array.  A request violating this is answered with index -1 and
+ * score NaN and is reported by netkv_sync_errors. */
+typedef struct {
+    uint32_t n_req;
+    const uint32_t *prefill;        /* [n_req] */
+    const uint32_t *len_tokens;     /* [n_req] */
+    const uint64_t *hash_off;       /* [n_req + 1] */
+    const uint64_t *hashes;         /* [n_hashes], nonzero */
+    uint64_t n_hashes;
+} netkv_requests_t;
+
+/* Optional per-pair outputs, row-major [n_req][n_decode] DEVICE arrays;
+ * any member may be NULL. */
+typedef struct {
+    uint16_t *prefix_blocks;        /* j: leading resident blocks (lambda = B_tok * j) */
+    uint8_t *feasible;              /* 1 iff m_d >= s_eff + m_min */
+    float *score;                   /* C(r,d), also for infeasible pairs */
+} netkv_pairs_t;
+
+/* Score every (request, decode) pair and select, per request, the k
+ * (1 <= k <= 8) feasible decodes of lowest cost in ascending (score, index)
+ * order (Algorithm 1 line 13 generalised to top-k); fewer than k feasible
+ * decodes are padded with index -1 and score +inf (Algorithm 1 line 2:
+ * reject).  out_idx, out_score: [n_req * k] DEVICE arrays.  `pairs` may be
+ * NULL.  Asynchronous on `stream`: inputs must stay valid and outputs are
+ * defined once the stream completes.  Allocates nothing.
+ * EINVAL: NULL pointers, k out of range; ENOTREADY: snapshot or cache
+ * missing; n_req = 0 is a no-op. */
+netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uint32_t k,
+                                int32_t *out_idx, float *out_score, netkv_pairs_t *pairs,
+                                void *stream);
+
+/* Stale-telemetry ranking sweep (Sec. V-D, Proposition 2): re-rank the
+ * batch under n_scen congestion scenarios util_scen [n_scen][P*D] (DEVICE,
+ * each value in [0,1)).  Prefix matches do not depend on telemetry and are
+ * computed once.  Writes the top-k (1 <= k <= 8) of every scenario to
+ * out_idx / out_score [n_scen][n_req][k] and, if out_flips is not NULL,
+ * out_flips[2*s] = number of requests whose selected decode lies on a
+ * different tier than the one selected under the loaded snapshot's own
+ * congestion, out_flips[2*s+1] = number whose selected decode differs (a
+ * rejection counts as its own tier and index).  Asynchronous; grows an
+ * internal work buffer (n_req * n_decode * 2 bytes) on first use.
+ * Scenario values are not validated (values >= 1 give non-positive
+ * bandwidth and meaningless costs). */
+netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen,
+                              const float *util_scen, uint32_t k, int32_t *out_idx,
+                              float *out_score, uint64_t *out_flips, void *stream);
+
+/* Between-batch update after the selections sel[n_req] (DEVICE; -1 =
+ * rejected) of a batch (Algorithm 1 line 14 and the counter cap of
+ * Sec. V-C, with one batch as the unit of time):
+ *   n_inflight[tau][p] = min(cap, selections of the batch from p on tau);
+ *   q_d = max(0, q_d + admitted_d - mu);
+ *   m_d = max(0, m_d - A_d) + A_prev_d;  A_prev_d = A_d,
+ * A_d = sum of s_eff over the requests admitted to d.  Integer arithmetic;
+ * asynchronous.  EINVAL: NULL pointers or an index >= D in sel is reported
+ * by netkv_sync_errors; ENOTREADY as for select. */
+netkv_status netkv_commit_batch(netkv_handle h, const netkv_requests_t *req, const int32_t *sel,
+                                uint32_t cap, uint32_t mu, void *stream);
+
+/* Copy the between-batch state into caller arrays (host or device; any may
+ * be NULL): n_inflight [4*P], queue_depth [D], free_mem [D],
+ * admitted_prev [D].  Synchronous. */
+netkv_status netkv_state_get(netkv_handle h, uint16_t *n_inflight, uint32_t *queue_depth,
+                             uint64_t *free_mem, uint64_t *admitted_prev, void *stream);
+
+/* Wait for `stream`, then report (and clear) input errors the kernels found
+ * in requests or selections since the last check: EINVAL with a message
+ * naming the first kind of error, or NETKV_OK. */
+netkv_status netkv_sync_errors(netkv_handle h, void *stream);
+
+/* Kernel timing: when enabled, the library records HIP events on `stream`
+ * around the scoring kernel of each netkv_select_batch / sweep kernel of
+ * netkv_rank_sweep, and netkv_kernel_ms returns (after synchronising) the
+ * milliseconds of the last such kernel. */
+netkv_status netkv_set_timing(netkv_handle h, int enable);
+netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
+
+/* Table geometry of the loaded cache: slots per decode (a power of two)
+ * and the device bytes of all tables. */
+netkv_status netkv_cache_info(netkv_handle h, uint64_t *slots_per_decode, uint64_t *table_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NETKV_H */

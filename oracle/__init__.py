@@ -56,7 +56,7 @@ def _load():
         build(force=False)
         lib = C.CDLL(_LIB)
         lib.orc_cache_build.restype = C.c_void_p
-        lib.orc_cache_build.argtypes = [C.c_uint32, C.c_void_p, C.c_void_p]
+        lib.orc_cache_build.argtypes = [C.c_uint32, C.c_void_p, C.c_void_p, C.c_int]
         lib.orc_cache_free.argtypes = [C.c_void_p]
         lib.orc_select.restype = C.c_uint64
         lib.orc_select.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32,
@@ -129,12 +129,12 @@ class Requests:
 class Cache:
     """Sorted copies of every decode's resident hash list."""
 
-    def __init__(self, cache: Dict[str, np.ndarray]):
+    def __init__(self, cache: Dict[str, np.ndarray], n_threads: int = 1):
         lib = _load()
         off = _arr(cache["hash_off"], np.uint64)
         h = _arr(cache["hashes"], np.uint64)
         self.n_decode = len(off) - 1
-        self.h = lib.orc_cache_build(self.n_decode, off.ctypes.data, h.ctypes.data)
+        self.h = lib.orc_cache_build(self.n_decode, off.ctypes.data, h.ctypes.data, int(n_threads))
 
     def __del__(self):
         if getattr(self, "h", None) and _lib is not None:

@@ -79,7 +79,8 @@ static int cmp_u64(const void *a, const void *b) {
     return (x > y) - (x < y);
 }
 
-orc_cache *orc_cache_build(uint32_t n_decode, const uint64_t *off, const uint64_t *hashes) {
+orc_cache *orc_cache_build(uint32_t n_decode, const uint64_t *off, const uint64_t *hashes,
+                           int n_threads) {
     orc_cache *c = (orc_cache *)calloc(1, sizeof(orc_cache));
     uint64_t total = off[n_decode];
     c->n_decode = n_decode;
@@ -87,8 +88,13 @@ orc_cache *orc_cache_build(uint32_t n_decode, const uint64_t *off, const uint64_
     c->keys = (uint64_t *)malloc(sizeof(uint64_t) * (total ? total : 1));
     memcpy(c->off, off, sizeof(uint64_t) * (n_decode + 1));
     memcpy(c->keys, hashes, sizeof(uint64_t) * total);
-    for (uint32_t d = 0; d < n_decode; ++d)
+#ifdef _OPENMP
+    if (n_threads < 1) n_threads = 1;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads)
+#endif
+    for (int64_t d = 0; d < (int64_t)n_decode; ++d)
         qsort(c->keys + off[d], (size_t)(off[d + 1] - off[d]), sizeof(uint64_t), cmp_u64);
+    (void)n_threads;
     return c;
 }
 

@@ -21,12 +21,15 @@ here; the workload recipes below (lognormal lengths, Zipf-shared prefixes,
 Poisson queues, uniform link utilisation) are synthetic stand-ins whose shapes
 follow the configurations listed in ``CONFIGS``.
 
-Hashes are produced by the splitmix64 output finaliser (Steele, Lea, Flood,
-"Fast splittable pseudorandom number generators", OOPSLA 2014), which is a
-bijection on 64-bit words.  Every hash is the finaliser applied to a distinct
-structured counter (domain, owner, block index) xor-ed with a per-seed key, so
-distinct blocks never share a hash.  Hash value 0 is reserved as the empty
-slot marker of the device tables and is never produced (it is remapped to 1).
+Block hashes of the shared prefix chains are the splitmix64 output finaliser
+(Steele, Lea, Flood, "Fast splittable pseudorandom number generators",
+OOPSLA 2014) -- a bijection on 64-bit words -- applied to a distinct
+structured counter (domain, prefix id, block index) xor-ed with a per-seed
+key, so the same block of the same prefix has the same hash in every request
+and every cache, and distinct chain blocks never collide.  Request-private
+blocks and decode-private resident blocks are independent uniform 64-bit
+draws.  Hash value 0 is reserved as the empty-slot marker of the device
+tables and is never produced.
 """
 from __future__ import annotations
 
@@ -43,8 +46,6 @@ _M64 = np.uint64(0xFFFFFFFFFFFFFFFF)
 # hash domains (top byte of the counter fed to the finaliser)
 _DOM_CHAIN = 1      # shared prefix chain k, block i
 _DOM_SYSTEM = 2     # long system prefix k, block i (long-context workload)
-_DOM_UNIQUE = 3     # request-private block (global request id, block i)
-_DOM_FILLER = 4     # decode-private resident block (decode d, index i)
 
 
 def mix64(x: np.ndarray) -> np.ndarray:
@@ -357,14 +358,14 @@ def make_requests(cfg: Config, seed: int = 0, n_req: Optional[int] = None,
     shared = np.minimum(nblk, chains["blocks"][k])
     if cfg.system_prefixes:
         shared = np.where(rng.random(n_req) < cfg.system_share, shared, 0)
-    rows, pos = _ragged_index(nblk)
-    gid = np.uint64(batch) * np.uint64(1 << 24) + rows.astype(np.uint64)
-    is_shared = pos < shared[rows]
-    hashes = np.where(is_shared,
-                      block_hash(seed, int(chains["domain"]), k[rows], pos),
-                      block_hash(seed, _DOM_UNIQUE, gid, pos))
     off = np.zeros(n_req + 1, dtype=np.uint64)
     off[1:] = np.cumsum(nblk)
+    # request-private blocks: independent uniform nonzero 64-bit values
+    hashes = _rng(seed, 32, batch).integers(1, (1 << 64) - 1, int(off[-1]), dtype=np.uint64,
+                                            endpoint=True)
+    # shared blocks: leading blocks of the request's prefix chain
+    sr, sp = _ragged_index(shared)
+    hashes[off[:-1][sr].astype(np.int64) + sp] = block_hash(seed, int(chains["domain"]), k[sr], sp)
     return dict(n_req=n_req, prefill=prefill, len_tokens=length,
                 hash_off=off, hashes=hashes.astype(np.uint64), prefix_id=k,
                 shared_blocks=shared)
@@ -403,6 +404,7 @@ def make_caches(cfg: Config, seed: int = 0, chains: Optional[Dict[str, np.ndarra
     off = np.arange(D + 1, dtype=np.uint64) * np.uint64(cap)
     out = np.empty(D * cap, dtype=np.uint64)
     n_chain = np.zeros(D, dtype=np.int64)
+    rng_fill = _rng(seed, 42)
     step = max(1, (1 << 24) // max(cap, 1))
     for d0 in range(0, D, step):
         d1 = min(D, d0 + step)
@@ -423,14 +425,10 @@ def make_caches(cfg: Config, seed: int = 0, chains: Optional[Dict[str, np.ndarra
         seg_start = np.cumsum(cnt) - cnt
         dec_start = np.cumsum(nch) - nch
         local = seg_start[rows] - dec_start[dd[rows]] + pos
-        block = np.empty((nd, cap), dtype=np.uint64)
+        # decode-private filler: independent uniform nonzero 64-bit values
+        block = out[d0 * cap:d1 * cap].reshape(nd, cap)
+        block[:] = rng_fill.integers(1, (1 << 64) - 1, (nd, cap), dtype=np.uint64, endpoint=True)
         block[dd[rows], local] = ch
-        fpos = np.arange(cap, dtype=np.int64)[None, :]
-        fill = fpos >= nch[:, None]
-        fr, fc = np.nonzero(fill)
-        block[fr, fc] = block_hash(seed, _DOM_FILLER, (d0 + fr).astype(np.uint64),
-                                   (fc - nch[fr]).astype(np.uint64))
-        out[d0 * cap:d1 * cap] = block.reshape(-1)
     return dict(n_decode=D, hash_off=off, hashes=out, n_chain=n_chain)
 
 

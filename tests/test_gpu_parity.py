@@ -1,0 +1,286 @@
+"""HIP path against the CPU oracle on the same seeded inputs (64-GPU sizes,
+edge cases, the C-ABI contract).  Needs an MI355X and the built library."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_03910_amd import workload as W
+from tests.parity import check_pairs, check_topk, subset_requests
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print("[gpu-case]", *a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def nk():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_03910_amd import netkv
+    netkv.load_library()
+    return netkv
+
+
+def _inputs(cfg, seed, inflight="zero", **snap_over):
+    snap = W.make_snapshot(cfg, seed, inflight=inflight)
+    snap.update(snap_over)
+    ch = W.prefix_chains(cfg, seed)
+    req = W.make_requests(cfg, seed, chains=ch)
+    cache = W.make_caches(cfg, seed, chains=ch)
+    return snap, req, cache
+
+
+def _gpu(nk, snap, cache, lf=0.5):
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, lf)
+    return sel
+
+
+def _run(nk, sel, req, k, pairs=True):
+    rd = nk.requests_to_device(req, sel.device)
+    out = sel.select(rd, k=k, pairs=pairs)
+    sel.sync_errors()
+    res = dict(idx=nk.to_numpy(out["idx"]).reshape(-1, k), score=nk.to_numpy(out["score"]).reshape(-1, k))
+    if pairs:
+        p = out["pairs"]
+        res.update(j=nk.to_numpy(p["prefix_blocks"]), feas=nk.to_numpy(p["feasible"]),
+                   cost=nk.to_numpy(p["score"]))
+    return res
+
+
+@pytest.mark.parametrize("inflight", ["zero", "random"])
+@pytest.mark.parametrize("k", [1, 3, 8])
+def test_c0_full_parity(nk, inflight, k):
+    _say("c0 full", inflight, "k", k)
+    cfg = W.CONFIGS["c0"]
+    snap, req, cache = _inputs(cfg, 0, inflight)
+    sel = _gpu(nk, snap, cache)
+    g = _run(nk, sel, req, k)
+    o = oracle.select(snap, cache, req, k=k, pairs=True, n_threads=8)
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    n, near = check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    assert n > 0.99 * cfg.n_requests * k
+    sel.close()
+
+
+def test_c0_load_terms_and_memory_pressure(nk):
+    """Non-zero slope of t_iter, alpha != 1, wide batch sizes and a reserve
+    that makes a third of the pairs infeasible."""
+    _say("c0 variant load terms")
+    cfg = W.scaled(W.CONFIGS["c0"], beta_range=(0, 64), t_iter_a=0.02, t_iter_b=0.0006,
+                   alpha=0.5, queue_mean=30.0)
+    snap, req, cache = _inputs(cfg, 3, "random")
+    snap["m_min"] = 60 * 10 ** 9
+    sel = _gpu(nk, snap, cache)
+    g = _run(nk, sel, req, 4)
+    o = oracle.select(snap, cache, req, k=4, pairs=True, n_threads=8)
+    assert 0.05 < 1 - o["feasible"].mean() < 0.9
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    sel.close()
+
+
+def test_ragged_decodes_long_runs_and_empty_runs(nk):
+    """90 decodes (a full and a partial wavefront of decodes), 16-token
+    blocks so runs exceed the LDS staging length, and requests shorter than
+    one block (empty runs)."""
+    _say("ragged decodes / long runs")
+    cl = W.Cluster(8, 5, 1, 3)
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=cl, block_tokens=16, n_requests=700,
+                   cache_per_decode=6000, len_median=3000.0)
+    snap, req, cache = _inputs(cfg, 5, "random")
+    assert cfg.n_decode == 90
+    # a few requests with fewer tokens than one block
+    req["len_tokens"][:5] = np.array([1, 5, 15, 3, 9], np.uint32)
+    n = (req["len_tokens"] // 16).astype(np.int64)
+    old = req["hash_off"].astype(np.int64)
+    keep = np.concatenate([np.arange(old[r], old[r] + n[r]) for r in range(len(n))])
+    req["hashes"] = req["hashes"][keep]
+    req["hash_off"] = np.concatenate([[0], np.cumsum(n)]).astype(np.uint64)
+    assert n.max() > 256
+    sel = _gpu(nk, snap, cache)
+    g = _run(nk, sel, req, 3)
+    o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    assert o["j"].max() > 256
+    sel.close()
+
+
+@pytest.mark.parametrize("lf", [0.9, 0.99])
+def test_dense_tables_long_probe_chains(nk, lf):
+    """Nearly full tables: long linear-probe chains that wrap the table end."""
+    _say("dense tables lf", lf)
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=1500, cache_per_decode=3000)
+    snap, req, cache = _inputs(cfg, 7)
+    sel = _gpu(nk, snap, cache, lf=lf)
+    slots, _ = nk.netkv_cache_info(sel.h)
+    assert slots == 4096
+    g = _run(nk, sel, req, 2)
+    o = oracle.select(snap, cache, req, k=2, pairs=True, n_threads=8)
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    sel.close()
+
+
+def test_all_infeasible_and_full_hits(nk):
+    _say("all infeasible / full hits")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=300)
+    snap, req, cache = _inputs(cfg, 9)
+    # every decode caches the whole run of request 0..9: full hits, s_eff = bpt * (l mod B_tok)
+    off = req["hash_off"].astype(np.int64)
+    extra = np.concatenate([req["hashes"][off[r]:off[r + 1]] for r in range(10)])
+    extra = np.unique(extra)
+    per = []
+    coff = cache["hash_off"].astype(np.int64)
+    for d in range(cfg.n_decode):
+        h = cache["hashes"][coff[d]:coff[d + 1]]
+        per.append(np.union1d(h, extra))
+    cache2 = dict(hash_off=np.concatenate([[0], np.cumsum([len(x) for x in per])]).astype(np.uint64),
+                  hashes=np.concatenate(per).astype(np.uint64))
+    sel = _gpu(nk, snap, cache2)
+    g = _run(nk, sel, req, 2)
+    o = oracle.select(snap, cache2, req, k=2, pairs=True, n_threads=8)
+    n10 = (np.diff(off)[:10])
+    assert (o["j"][:10] == n10[:, None]).all()
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    # a reserve larger than any free memory rejects every request
+    snap2 = dict(snap)
+    snap2["m_min"] = 2 ** 63
+    sel.load_snapshot(snap2)
+    g2 = _run(nk, sel, req, 3, pairs=False)
+    assert (g2["idx"] == -1).all() and np.isinf(g2["score"]).all()
+    sel.close()
+
+
+def test_determinism_and_insertion_order(nk):
+    _say("determinism / insertion order")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=2000)
+    snap, req, cache = _inputs(cfg, 11)
+    sel = _gpu(nk, snap, cache)
+    a = _run(nk, sel, req, 3)
+    b = _run(nk, sel, req, 3)
+    for key in a:
+        np.testing.assert_array_equal(a[key], b[key])
+    # permute each decode's hash list: slots move, membership does not
+    rng = np.random.default_rng(0)
+    off = cache["hash_off"].astype(np.int64)
+    perm = np.concatenate([off[d] + rng.permutation(off[d + 1] - off[d]) for d in range(cfg.n_decode)])
+    cache_p = dict(hash_off=cache["hash_off"], hashes=cache["hashes"][perm])
+    sel.load_cache(cache_p, 0.5)
+    c = _run(nk, sel, req, 3)
+    for key in a:
+        np.testing.assert_array_equal(a[key], c[key])
+    sel.close()
+
+
+def test_subset_batches_match_full_batch(nk):
+    """Scoring is per request: any subset, in any order, gives the same rows."""
+    _say("subset batches")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=3000)
+    snap, req, cache = _inputs(cfg, 13)
+    sel = _gpu(nk, snap, cache)
+    full = _run(nk, sel, req, 2, pairs=False)
+    rows = np.random.default_rng(1).permutation(3000)[:777]
+    sub = _run(nk, sel, subset_requests(req, rows), 2, pairs=False)
+    np.testing.assert_array_equal(sub["idx"], full["idx"][rows])
+    np.testing.assert_array_equal(sub["score"], full["score"][rows])
+    sel.close()
+
+
+def test_invalid_requests_are_flagged(nk):
+    _say("invalid requests")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=64)
+    snap, req, cache = _inputs(cfg, 15)
+    sel = _gpu(nk, snap, cache)
+    bad = {k: v.copy() for k, v in req.items() if k in ("prefill", "len_tokens", "hash_off", "hashes")}
+    bad["prefill"][3] = 999            # no such prefill instance
+    bad["len_tokens"][7] += 512 * 3    # run length inconsistent with l_r
+    i = int(bad["hash_off"][10])
+    if int(bad["hash_off"][11]) > i:
+        bad["hashes"][i] = 0           # reserved hash value
+    rd = nk.requests_to_device(bad, sel.device)
+    out = sel.select(rd, k=2)
+    with pytest.raises(nk.NetKVError) as e:
+        sel.sync_errors()
+    assert e.value.status == -1
+    idx = nk.to_numpy(out["idx"]).reshape(-1, 2)
+    sc = nk.to_numpy(out["score"]).reshape(-1, 2)
+    for r in (3, 7):
+        assert (idx[r] == -1).all() and np.isnan(sc[r]).all()
+    good = [r for r in range(64) if r not in (3, 7, 10)]
+    o = oracle.select(snap, cache, subset_requests(req, good), k=2, pairs=True)
+    check_topk(idx[good], sc[good], o["idx"], o["cost"], o["feasible"])
+    sel.sync_errors()  # cleared
+    sel.close()
+
+
+def test_contract_errors_write_nothing(nk):
+    _say("contract errors")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=32)
+    snap, req, cache = _inputs(cfg, 17)
+    sel = nk.Selector(0)
+    rd = nk.requests_to_device(req, sel.device)
+    idx = torch.full((32 * 9,), 7, dtype=torch.int32, device=sel.device)
+    sc = torch.full((32 * 9,), 7.0, dtype=torch.float32, device=sel.device)
+    with pytest.raises(nk.NetKVError) as e:
+        nk.netkv_select_batch(sel.h, rd, 2, idx, sc, None, sel.device)
+    assert e.value.status == -2  # ENOTREADY
+    sel.load_snapshot(snap)
+    with pytest.raises(nk.NetKVError) as e:
+        nk.netkv_select_batch(sel.h, rd, 2, idx, sc, None, sel.device)
+    assert e.value.status == -2
+    sel.load_cache(cache)
+    for kk in (0, 9):
+        with pytest.raises(nk.NetKVError) as e:
+            nk.netkv_select_batch(sel.h, rd, kk, idx, sc, None, sel.device)
+        assert e.value.status == -1
+    torch.cuda.synchronize()
+    assert (idx == 7).all() and (sc == 7.0).all()
+    # invalid snapshot values are rejected and the old snapshot is kept
+    s2 = dict(snap)
+    s2["util"] = snap["util"].copy()
+    s2["util"][5] = 1.0
+    with pytest.raises(nk.NetKVError) as e:
+        sel.load_snapshot(s2)
+    assert e.value.status == -1
+    s3 = dict(snap)
+    s3["tier_map"] = snap["tier_map"].copy()
+    s3["tier_map"][0] = 4
+    with pytest.raises(nk.NetKVError):
+        sel.load_snapshot(s3)
+    s4 = dict(snap)
+    s4["batch_size"] = snap["batch_size"].copy()
+    s4["batch_size"][0] = 65
+    with pytest.raises(nk.NetKVError):
+        sel.load_snapshot(s4)
+    s5 = dict(snap)
+    s5["tier_bw"] = np.array([1.0, 0.0, 1.0, 1.0])
+    with pytest.raises(nk.NetKVError):
+        sel.load_snapshot(s5)
+    # a cache with the reserved value or a mismatched decode count
+    c2 = dict(hash_off=cache["hash_off"], hashes=cache["hashes"].copy())
+    c2["hashes"][17] = 0
+    with pytest.raises(nk.NetKVError) as e:
+        sel.load_cache(c2)
+    assert e.value.status == -1
+    c3 = dict(hash_off=cache["hash_off"][:-1], hashes=cache["hashes"])
+    with pytest.raises(nk.NetKVError):
+        sel.load_cache(c3)
+    with pytest.raises(nk.NetKVError):
+        sel.load_cache(cache, 1.0)
+    # the previously loaded state still answers like the oracle
+    g = _run(nk, sel, req, 2)
+    o = oracle.select(snap, cache, req, k=2, pairs=True)
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    # empty batch is a no-op
+    empty = dict(prefill=np.zeros(0, np.uint32), len_tokens=np.zeros(0, np.uint32),
+                 hash_off=np.zeros(1, np.uint64), hashes=np.zeros(1, np.uint64))
+    sel.select(nk.requests_to_device(empty, sel.device), k=1)
+    sel.sync_errors()
+    sel.close()
