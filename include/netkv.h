@@ -134,11 +134,13 @@ typedef struct {
 
 /* Score every (request, decode) pair and select, per request, the k
  * (1 <= k <= 8) feasible decodes of lowest cost in ascending (score, index)
- * order (Algorithm 1 line 13 generalised to top-k); fewer than k feasible
- * decodes are padded with index -1 and score +inf (Algorithm 1 line 2:
- * reject).  out_idx, out_score: [n_req * k] DEVICE arrays.  `pairs` may be
+ * order (the argmin of Algorithm 1 generalised to top-k); fewer than k
+ * feasible decodes are padded with index -1 and score +inf (Algorithm 1
+ * rejects a request with no feasible decode).  out_idx, out_score: [n_req * k] DEVICE arrays.  `pairs` may be
  * NULL.  Asynchronous on `stream`: inputs must stay valid and outputs are
- * defined once the stream completes.  Allocates nothing.
+ * defined once the stream completes.  Allocates only when a batch is
+ * larger than every earlier one on the handle (its ordering and per-chunk
+ * work buffers grow; about 21 + 8*k*ceil(D/64) bytes per request).
  * EINVAL: NULL pointers, k out of range; ENOTREADY: snapshot or cache
  * missing; n_req = 0 is a no-op. */
 netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uint32_t k,
@@ -162,7 +164,7 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
                               float *out_score, uint64_t *out_flips, void *stream);
 
 /* Between-batch update after the selections sel[n_req] (DEVICE; -1 =
- * rejected) of a batch (Algorithm 1 line 14 and the counter cap of
+ * rejected) of a batch (the in-flight increment of Algorithm 1 and the counter cap of
  * Sec. V-C, with one batch as the unit of time):
  *   n_inflight[tau][p] = min(cap, selections of the batch from p on tau);
  *   q_d = max(0, q_d + admitted_d - mu);
@@ -185,11 +187,22 @@ netkv_status netkv_state_get(netkv_handle h, uint16_t *n_inflight, uint32_t *que
 netkv_status netkv_sync_errors(netkv_handle h, void *stream);
 
 /* Kernel timing: when enabled, the library records HIP events on `stream`
- * around the scoring kernel of each netkv_select_batch / sweep kernel of
- * netkv_rank_sweep, and netkv_kernel_ms returns (after synchronising) the
- * milliseconds of the last such kernel. */
+ * around the scoring kernels (scan and merge) of each netkv_select_batch,
+ * and around the sweep kernel of netkv_rank_sweep; netkv_kernel_ms returns
+ * (after synchronising on the end event) the milliseconds of the last one. */
 netkv_status netkv_set_timing(netkv_handle h, int enable);
 netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
+
+/* Tuning options (results never depend on them):
+ *   NETKV_OPT_RUN_LEN -- requests per wavefront run in the batch order
+ *                        (0 = automatic, else 1..2^20);
+ *   NETKV_OPT_REUSE   -- 1 (default): a request's first-miss index on a
+ *                        decode is taken from the preceding request of the
+ *                        batch order when it lies inside their common
+ *                        leading blocks (an exact identity, no probe);
+ *                        0: every pair is scanned from block 0. */
+enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2 };
+netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 
 /* Table geometry of the loaded cache: slots per decode (a power of two)
  * and the device bytes of all tables. */

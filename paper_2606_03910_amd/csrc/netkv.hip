@@ -18,14 +18,20 @@
 //     batch u32[D], plus the admitted bytes of the previous batch u64[D].
 //
 // Kernels:
-//   select_kernel  -- prefix match (Sec. III-B) + Eqs. (2)-(7) + feasibility
-//                     + per-request top-k, fused; one wavefront per request,
-//                     lanes over decodes; optional per-pair outputs.
+//   prep / sort / lcp -- validate requests, order the batch so requests with
+//                     equal leading blocks are neighbours (rocPRIM radix
+//                     sort), and measure each one's common leading run with
+//                     its predecessor.
+//   scan_kernel    -- prefix match (Sec. III-B) + Eqs. (2)-(7) + feasibility
+//                     + per-chunk top-k, fused; one wavefront per (run of
+//                     sorted requests, 64 decodes); optional per-pair outputs.
+//   reduce_kernel  -- merges the per-chunk keys into each request's top-k.
 //   sweep_kernel   -- re-scoring under congestion scenarios with the prefix
 //                     lengths reused; lanes over requests.
 //   insert_kernel  -- builds the tables with 64-bit compare-and-swap.
 //   commit kernels -- between-batch counter / queue / memory update.
 #include <hip/hip_runtime.h>
+#include <rocprim/device/device_radix_sort.hpp>
 
 #include <algorithm>
 #include <cmath>
@@ -43,7 +49,6 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
-constexpr int kStage = 256;           // hashes of one request staged in LDS
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kEmptyKey = ~0ull; // empty top-k entry (sorts last)
 
@@ -118,14 +123,13 @@ struct PairCost {
     bool feas;
 };
 
-__device__ inline PairCost pair_cost(const Snap &s, uint32_t p, uint32_t d, uint32_t len, uint32_t j,
-                                     float util, float load) {
-    uint64_t s_eff = (uint64_t)s.bpt * (uint64_t)(len - s.block_tokens * j);
-    uint64_t m = s.free_mem[d];
-    bool feas = (m >= s.m_min) && (m - s.m_min >= s_eff);
-    uint32_t tau = s.tier_map[(uint64_t)p * s.D + d] & 3u;
-    float n = (float)s.n_inflight[tau * s.P + p];
-    float t_x = ((float)s_eff * (1.0f + n)) / (s.bw[tau] * (1.0f - util)) + s.lat[tau];
+__device__ inline PairCost pair_cost(const Snap &s, uint32_t p, uint64_t m, uint32_t len, uint32_t j,
+                                     uint32_t tau_raw, float util, float load) {
+    const uint64_t s_eff = (uint64_t)s.bpt * (uint64_t)(len - s.block_tokens * j);
+    const bool feas = (m >= s.m_min) && (m - s.m_min >= s_eff);
+    const uint32_t tau = tau_raw & 3u;
+    const float n = (float)s.n_inflight[tau * s.P + p];
+    const float t_x = ((float)s_eff * (1.0f + n)) / (s.bw[tau] * (1.0f - util)) + s.lat[tau];
     PairCost pc;
     pc.cost = t_x + load;
     pc.feas = feas;
@@ -146,41 +150,29 @@ __device__ inline void topk_insert(uint64_t (&lst)[K], uint64_t x) {
     }
 }
 
-__device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
-    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-    lo = __shfl_xor(lo, m, kWave);
-    hi = __shfl_xor(hi, m, kWave);
-    return ((uint64_t)hi << 32) | lo;
-}
-
-__device__ inline uint64_t wave_min_u64(uint64_t v) {
-#pragma unroll
-    for (int m = 1; m < kWave; m <<= 1) {
-        uint64_t o = shfl_xor_u64(v, m);
-        v = o < v ? o : v;
-    }
-    return v;
-}
-
 __device__ inline uint32_t wave_sum_u32(uint32_t v) {
 #pragma unroll
     for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
     return v;
 }
 
-__device__ inline uint64_t uniform_u64(uint64_t v) {
-    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-    return ((uint64_t)hi << 32) | lo;
+// Index of the calling wavefront in its workgroup, as a wave-uniform value
+// (so everything derived from it stays in scalar registers).
+__device__ inline uint32_t wave_index() {
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
 }
 
-// Blocks are handed to the 8 XCDs round-robin; give each XCD a contiguous
-// range of logical blocks so neighbouring requests share an L2.
-__device__ inline uint32_t xcd_block(uint32_t b, uint32_t g) {
-    const uint32_t nx = 8;
-    uint32_t q = g / nx, rem = g % nx;
-    uint32_t x = b % nx, i = b / nx;
-    return x < rem ? x * (q + 1) + i : rem * (q + 1) + (x - rem) * q + i;
+// Minimum of a 32-bit value over the 64 lanes with DPP row operations
+// (quad permutes, row rotates, then the row broadcasts of wave64); every lane
+// must be active.  The result is read from lane 63.
+__device__ inline uint32_t wave_min_u32_dpp(uint32_t v) {
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x124, 0xF, 0xF, false));  // row_ror 4
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x128, 0xF, 0xF, false));  // row_ror 8
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x142, 0xA, 0xF, false));  // row_bcast 15
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x143, 0xC, 0xF, false));  // row_bcast 31
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
 // Validate request r's header; returns false (and flags) if inconsistent.
@@ -196,24 +188,155 @@ __device__ inline bool request_ok(const Reqs &rq, const Snap &s, uint32_t r, uin
     return true;
 }
 
-// First-miss prefix match of one request against 64 decodes (lanes), with
-// W home-slot loads issued together per step.  `col` points at this lane's
-// column of the slot-major table; the hash run is wave-uniform.
+// ---------------------------------------------------------------- batch order
+//
+// Requests are scored in an order that groups equal leading blocks: the sort
+// key is 19 bits of the first block hash above 12 bits of the run length, so
+// requests that start with the same prefix become neighbours in ascending
+// length.  For neighbours r' -> r with a common leading run of L blocks, the
+// first-miss index of r on decode d follows from that of r' without any
+// probe whenever it lies inside the common run (j' < L gives j = j'), and
+// otherwise scanning resumes at block L (j' >= L implies blocks 0..L-1 are
+// resident).  The order changes which probes are made, never a result.
+
+constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
+constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
+
+// One sorted request, everything the scan needs without indirection.
+struct alignas(32) Rec {
+    uint32_t r;      // request index in the caller's batch
+    uint32_t p;      // prefill instance
+    uint32_t len;    // input tokens
+    uint32_t n;      // hashed blocks
+    uint32_t lcp;    // leading blocks in common with the previous sorted request
+    uint32_t pad;
+    uint64_t a;      // offset of the hash run
+};
+
+struct Order {
+    const uint32_t *perm;     // sorted position -> request
+    const Rec *rec;           // [n_valid] sorted request records
+    const uint32_t *n_valid;  // valid requests (they sort first)
+};
+
+// Validate each request and build its sort key.  One wavefront handles 16
+// requests in turn; lanes scan the hash run for the reserved value 0.
+__global__ __launch_bounds__(kBlock) void prep_kernel(Snap s, Reqs rq, uint32_t *__restrict__ keys,
+                                                      uint32_t *__restrict__ vals, uint32_t *__restrict__ err) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t w = blockIdx.x * kWavesPerBlock + wave_index();
+    uint32_t flags = 0;
+    for (uint32_t q = 0; q < 16; ++q) {
+        const uint32_t r = w * 16 + q;
+        if (r >= rq.n_req) break;
+        uint32_t p, len, n;
+        uint64_t a;
+        bool ok = request_ok(rq, s, r, p, len, a, n);
+        bool zero = false;
+        if (ok)
+            for (uint32_t i = lane; i < n; i += kWave) zero |= rq.hashes[a + i] == 0;
+        const bool bad_hash = __any(zero);
+        const bool good = ok && !bad_hash;
+        if (!ok) flags |= kErrRequest;
+        else if (bad_hash) flags |= kErrZeroHash;
+        if (lane == 0) {
+            uint32_t key = kKeyInvalid;
+            if (good) {
+                if (n == 0) {
+                    key = kKeyEmptyRun;
+                } else {
+                    uint64_t h0 = rq.hashes[a];
+                    uint32_t top = (uint32_t)((h0 * kGolden) >> 32);
+                    key = ((top >> 13) << 12) | (n < 4095u ? n : 4095u);
+                }
+            }
+            keys[r] = key;
+            vals[r] = r;
+        }
+    }
+    if (flags && lane == 0) atomicOr(err, flags);
+}
+
+// Number of valid requests = position of the first invalid key in sorted order.
+__global__ void count_valid_kernel(const uint32_t *__restrict__ sorted_keys, uint32_t n, uint32_t *__restrict__ out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    uint32_t lo = 0, hi = n;
+    while (lo < hi) {
+        uint32_t mid = lo + (hi - lo) / 2;
+        if (sorted_keys[mid] < kKeyInvalid) lo = mid + 1;
+        else hi = mid;
+    }
+    *out = lo;
+}
+
+// Record of each sorted request, with its common leading blocks with the
+// previous sorted request.
+__global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
+                                                  const uint32_t *__restrict__ n_valid, Rec *__restrict__ rec) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= *n_valid) return;
+    const uint32_t r = perm[i];
+    const uint64_t a = rq.off[r];
+    const uint64_t nr = rq.off[r + 1] - a;
+    uint32_t l = 0;
+    if (i > 0) {
+        const uint32_t q = perm[i - 1];
+        const uint64_t b = rq.off[q];
+        const uint64_t nq = rq.off[q + 1] - b;
+        const uint64_t m = nr < nq ? nr : nq;
+        while (l < m && rq.hashes[a + l] == rq.hashes[b + l]) ++l;
+    }
+    Rec x;
+    x.r = r;
+    x.p = rq.prefill[r];
+    x.len = rq.len[r];
+    x.n = (uint32_t)nr;
+    x.lcp = l;
+    x.pad = 0;
+    x.a = a;
+    rec[i] = x;
+}
+
+// Read-only data that is uniform across a wavefront (request records, hash
+// runs) is read through the constant address space, which the compiler
+// serves with scalar loads into SGPRs.
+template <typename T>
+using cptr = const __attribute__((address_space(4))) T *;
+
+template <typename T>
+__device__ inline cptr<T> as_const(const T *p) {
+    return (cptr<T>)(const __attribute__((address_space(4))) void *)(uintptr_t)p;
+}
+
+__device__ inline Rec load_rec(const Rec *base, uint32_t i) {
+    const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
+    Rec x;
+    x.r = w[0];
+    x.p = w[1];
+    x.len = w[2];
+    x.n = w[3];
+    x.lcp = w[4];
+    x.pad = 0;
+    x.a = ((uint64_t)w[7] << 32) | (uint64_t)w[6];
+    return x;
+}
+
+// First-miss scan of one request's run on the 64 decodes of a wavefront,
+// for the lanes in `need`, starting at block `start` (uniform).  W home-slot
+// loads are issued together per step; colliding slots are followed by
+// linear probing.  Lanes not in `need` return j_in.
 template <int W>
-__device__ inline uint32_t prefix_match(const uint64_t *__restrict__ col, const Table &t,
-                                        const uint64_t *lds_run, const uint64_t *__restrict__ g_run,
-                                        uint32_t n, bool active) {
-    uint32_t j = 0;
-    bool alive = active;
-    for (uint32_t i0 = 0; i0 < n; i0 += W) {
+__device__ inline uint32_t probe_from(const uint64_t *__restrict__ col, const Table &t, cptr<uint64_t> run,
+                                      uint32_t n, uint32_t start, bool need, uint32_t j_in) {
+    uint32_t j = start;
+    bool alive = need;
+    for (uint32_t i0 = start; i0 < n; i0 += W) {
         if (!__any(alive)) break;
         uint64_t h[W], sl[W], key[W];
 #pragma unroll
         for (int w = 0; w < W; ++w) {
-            uint32_t i = i0 + w;
-            uint64_t v = 0;
-            if (i < n) v = i < (uint32_t)kStage ? lds_run[i] : g_run[i];
-            h[w] = uniform_u64(v);
+            const uint32_t i = i0 + w;
+            h[w] = i < n ? run[i] : 0;
             sl[w] = home_slot(h[w], t.shift);
             key[w] = 0;
             if (alive && i < n) key[w] = col[sl[w] * t.pitch];
@@ -227,7 +350,7 @@ __device__ inline uint32_t prefix_match(const uint64_t *__restrict__ col, const 
             while (__any(pend)) {
                 s2 = (s2 + 1) & t.mask;
                 if (pend) {
-                    uint64_t k2 = col[s2 * t.pitch];
+                    const uint64_t k2 = col[s2 * t.pitch];
                     if (k2 == h[w]) {
                         hit = true;
                         pend = false;
@@ -240,81 +363,118 @@ __device__ inline uint32_t prefix_match(const uint64_t *__restrict__ col, const 
             j += alive ? 1u : 0u;
         }
     }
-    return j;
+    return need ? j : j_in;
 }
 
-// One wavefront per request; lanes are decodes c*64 + lane, c = 0..ceil(D/64)-1.
+// One wavefront per (run of sorted requests, chunk of 64 decodes).  For each
+// request of the run: first-miss prefix length per decode (carried from the
+// previous request where the common leading run decides it), non-cached
+// bytes, feasibility and cost (Eqs. (2)-(7)), then the chunk's K best
+// feasible (score, index) keys into partial[chunk][sorted position][0..K).
+// Request records are fetched two requests ahead and the congestion row one
+// request ahead, so the per-request chain of dependent loads is short.
 template <int K, int W, bool PAIRS>
-__global__ __launch_bounds__(kBlock) void select_kernel(Snap s, Table t, Reqs rq, uint32_t k,
-                                                        int32_t *__restrict__ out_idx,
-                                                        float *__restrict__ out_score, PairOut po,
-                                                        uint32_t *__restrict__ err) {
-    __shared__ uint64_t run[kWavesPerBlock][kStage];
-    const uint32_t wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
-    const uint32_t r = blk * kWavesPerBlock + wave;
-    if (r >= rq.n_req) return;
-
-    uint32_t p, len, n;
-    uint64_t a;
-    bool ok = request_ok(rq, s, r, p, len, a, n);
-    bool zero = false;
-    if (ok) {
-        const uint64_t *g = rq.hashes + a;
-        for (uint32_t i = lane; i < n; i += kWave) {
-            uint64_t v = g[i];
-            if (i < (uint32_t)kStage) run[wave][i] = v;
-            zero |= (v == 0);
+__global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec *__restrict__ rec,
+                                                      const uint64_t *__restrict__ hashes,
+                                                      const uint32_t *__restrict__ n_valid, uint32_t n_req,
+                                                      uint32_t run_len, uint32_t n_runs, uint32_t nchunk,
+                                                      uint32_t reuse, uint64_t *__restrict__ partial, PairOut po) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t gw = blockIdx.x * kWavesPerBlock + wave_index();
+    const uint32_t run = gw / nchunk, chunk = gw % nchunk;
+    if (run >= n_runs) return;
+    const uint32_t nv = *n_valid;
+    const uint32_t i0 = run * run_len;
+    if (i0 >= nv) return;
+    const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
+    const uint32_t d = chunk * kWave + lane;
+    const bool act = d < s.D;
+    const uint32_t dd = act ? d : 0;
+    const uint64_t *col = t.keys + dd;
+    const float load = act ? load_term(s, d) : 0.0f;
+    const uint64_t mem = act ? s.free_mem[d] : 0;
+    const cptr<uint64_t> chash = as_const(hashes);
+    Rec c0 = load_rec(rec, i0);
+    Rec c1 = load_rec(rec, i0 + 1 < i1 ? i0 + 1 : i0);
+    uint8_t tau0 = s.tier_map[(uint64_t)c0.p * s.D + dd];
+    float u0 = s.util[(uint64_t)c0.p * s.D + dd];
+    uint32_t j_prev = 0;
+    for (uint32_t i = i0; i < i1; ++i) {
+        const Rec c2 = load_rec(rec, i + 2 < i1 ? i + 2 : i1 - 1);
+        const uint8_t tau1 = s.tier_map[(uint64_t)c1.p * s.D + dd];
+        const float u1 = s.util[(uint64_t)c1.p * s.D + dd];
+        const uint32_t L = (reuse && i != i0) ? c0.lcp : 0u;
+        const bool carry = j_prev < L;
+        uint32_t j = carry ? j_prev : L;
+        if (L < c0.n) j = probe_from<W>(col, t, chash + c0.a, c0.n, L, act && !carry, j);
+        j_prev = j;
+        const PairCost pc = pair_cost(s, c0.p, mem, c0.len, j, tau0, u0, load);
+        const bool feas = act && pc.feas;
+        const float cost = pc.cost;
+        if (PAIRS && act) {
+            const uint64_t o = (uint64_t)c0.r * s.D + d;
+            if (po.j) po.j[o] = (uint16_t)j;
+            if (po.feas) po.feas[o] = feas ? 1 : 0;
+            if (po.score) po.score[o] = cost;
+            if (po.jT) po.jT[(uint64_t)d * n_req + c0.r] = (uint16_t)j;
         }
+        // the chunk's K best feasible decodes: minimum cost bits over lanes,
+        // ties to the lowest lane (= lowest decode index)
+        uint32_t cb = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
+        uint64_t mine = kEmptyKey;
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            const uint32_t mn = wave_min_u32_dpp(cb);
+            const uint64_t tie = __ballot(cb == mn && mn != 0xFFFFFFFFu);
+            const uint32_t wl = tie ? (uint32_t)__builtin_ctzll(tie) : 64u;
+            if (lane == wl) cb = 0xFFFFFFFFu;
+            if (lane == (uint32_t)q)
+                mine = tie ? (((uint64_t)mn << 32) | (uint64_t)(chunk * kWave + wl)) : kEmptyKey;
+        }
+        if (lane < (uint32_t)K) partial[((uint64_t)chunk * n_req + i) * K + lane] = mine;
+        c0 = c1;
+        c1 = c2;
+        tau0 = tau1;
+        u0 = u1;
     }
-    const bool any_zero = __any(zero);
-    if (!ok || any_zero) {
-        if (lane < k) {
-            out_idx[(uint64_t)r * k + lane] = -1;
-            out_score[(uint64_t)r * k + lane] = __builtin_nanf("");
+}
+
+// Merge the per-chunk keys of every sorted request into its top-k
+// (ascending (score, index)) and write it at the request's own position;
+// invalid requests (sorted last) get index -1 and score NaN.
+template <int K>
+__global__ __launch_bounds__(256) void reduce_kernel(uint32_t n_req, uint32_t nchunk, uint32_t k,
+                                                     const uint64_t *__restrict__ partial,
+                                                     const uint32_t *__restrict__ perm,
+                                                     const uint32_t *__restrict__ n_valid,
+                                                     int32_t *__restrict__ out_idx, float *__restrict__ out_score) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_req) return;
+    const uint64_t o = (uint64_t)perm[i] * k;
+    if (i >= *n_valid) {
+        for (uint32_t q = 0; q < k; ++q) {
+            out_idx[o + q] = -1;
+            out_score[o + q] = __builtin_nanf("");
         }
-        if (lane == 0) atomicOr(err, ok ? kErrZeroHash : kErrRequest);
         return;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
     uint64_t best[K];
 #pragma unroll
-    for (int i = 0; i < K; ++i) best[i] = kEmptyKey;
-
-    const uint64_t *g_run = rq.hashes + a;
-    const uint32_t nchunk = (s.D + kWave - 1) / kWave;
+    for (int q = 0; q < K; ++q) best[q] = kEmptyKey;
     for (uint32_t c = 0; c < nchunk; ++c) {
-        const uint32_t d = c * kWave + lane;
-        const bool act = d < s.D;
-        const uint32_t dd = act ? d : 0;
-        uint32_t j = prefix_match<W>(t.keys + dd, t, run[wave], g_run, n, act);
-        if (act) {
-            float util = s.util[(uint64_t)p * s.D + d];
-            PairCost pc = pair_cost(s, p, d, len, j, util, load_term(s, d));
-            if (PAIRS) {
-                uint64_t o = (uint64_t)r * s.D + d;
-                if (po.j) po.j[o] = (uint16_t)j;
-                if (po.feas) po.feas[o] = pc.feas ? 1 : 0;
-                if (po.score) po.score[o] = pc.cost;
-                if (po.jT) po.jT[(uint64_t)d * rq.n_req + r] = (uint16_t)j;
-            }
-            if (pc.feas) topk_insert<K>(best, pack_key(pc.cost, d));
+        const uint64_t *src = partial + ((uint64_t)c * n_req + i) * K;
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            const uint64_t x = src[q];
+            if (x < best[K - 1]) topk_insert<K>(best, x);
         }
     }
-    for (uint32_t i = 0; i < k; ++i) {
-        uint64_t m = wave_min_u64(best[0]);
-        if (best[0] == m && m != kEmptyKey) {
 #pragma unroll
-            for (int q = 0; q + 1 < K; ++q) best[q] = best[q + 1];
-            best[K - 1] = kEmptyKey;
-        }
-        if (lane == 0) {
-            out_idx[(uint64_t)r * k + i] = m == kEmptyKey ? -1 : (int32_t)(uint32_t)m;
-            out_score[(uint64_t)r * k + i] = m == kEmptyKey ? __builtin_inff()
-                                                            : __uint_as_float((uint32_t)(m >> 32));
+    for (int q = 0; q < K; ++q) {
+        if ((uint32_t)q < k) {
+            const uint64_t m = best[q];
+            out_idx[o + q] = m == kEmptyKey ? -1 : (int32_t)(uint32_t)m;
+            out_score[o + q] = m == kEmptyKey ? __builtin_inff() : __uint_as_float((uint32_t)(m >> 32));
         }
     }
 }
@@ -347,7 +507,8 @@ __global__ __launch_bounds__(256) void sweep_kernel(Snap s, Reqs rq, const float
             for (int i = 0; i < K; ++i) best[i] = kEmptyKey;
             for (uint32_t d = 0; d < s.D; ++d) {
                 uint32_t j = jT[(uint64_t)d * rq.n_req + r];
-                PairCost pc = pair_cost(s, p, d, len, j, u[d], load_term(s, d));
+                PairCost pc = pair_cost(s, p, s.free_mem[d], len, j, s.tier_map[(uint64_t)p * s.D + d], u[d],
+                                        load_term(s, d));
                 if (pc.feas) topk_insert<K>(best, pack_key(pc.cost, d));
             }
             for (uint32_t i = 0; i < k; ++i) {
@@ -543,6 +704,18 @@ struct netkv_ctx {
     uint32_t *cnt = nullptr, *adm = nullptr;
     unsigned long long *bytes = nullptr;
     uint32_t commit_P = 0, commit_D = 0;
+    // batch-order scratch (grows to the largest batch seen)
+    uint64_t order_cap = 0;
+    uint32_t *keys_in = nullptr, *keys_out = nullptr, *vals_in = nullptr, *perm = nullptr;
+    Rec *rec = nullptr;
+    uint32_t *n_valid = nullptr;
+    void *sort_tmp = nullptr;
+    size_t sort_tmp_bytes = 0;
+    uint64_t *partial = nullptr;
+    uint64_t partial_cap = 0;
+    // options
+    uint32_t run_len_opt = 0;   // 0 = automatic
+    uint32_t reuse_opt = 1;     // carry first-miss indices along sorted runs
     // timing
     bool timing = false;
     bool timed = false;
@@ -664,26 +837,109 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-template <int K, int W>
-void launch_select_k(const Snap &s, const Table &t, const Reqs &rq, uint32_t k, int32_t *idx,
-                     float *score, const PairOut &po, bool pairs, uint32_t *err, hipStream_t st) {
-    uint32_t grid = (rq.n_req + kWavesPerBlock - 1) / kWavesPerBlock;
-    if (pairs)
-        hipLaunchKernelGGL((select_kernel<K, W, true>), dim3(grid), dim3(kBlock), 0, st, s, t, rq, k, idx,
-                           score, po, err);
-    else
-        hipLaunchKernelGGL((select_kernel<K, W, false>), dim3(grid), dim3(kBlock), 0, st, s, t, rq, k, idx,
-                           score, po, err);
-}
-
 constexpr int kSpec = 4;   // home-slot loads issued together per probe step
 
-void launch_select(const Snap &s, const Table &t, const Reqs &rq, uint32_t k, int32_t *idx, float *score,
-                   const PairOut &po, bool pairs, uint32_t *err, hipStream_t st) {
-    if (k <= 1) launch_select_k<1, kSpec>(s, t, rq, k, idx, score, po, pairs, err, st);
-    else if (k <= 2) launch_select_k<2, kSpec>(s, t, rq, k, idx, score, po, pairs, err, st);
-    else if (k <= 4) launch_select_k<4, kSpec>(s, t, rq, k, idx, score, po, pairs, err, st);
-    else launch_select_k<8, kSpec>(s, t, rq, k, idx, score, po, pairs, err, st);
+netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, hipStream_t st) {
+    if (R > h->order_cap) {
+        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->rec);
+        dfree(h->sort_tmp);
+        h->order_cap = 0;
+        h->sort_tmp_bytes = 0;
+        if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
+            dalloc(h->vals_in, R) != hipSuccess || dalloc(h->perm, R) != hipSuccess ||
+            dalloc(h->rec, R) != hipSuccess)
+            return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
+        size_t bytes = 0;
+        if (rocprim::radix_sort_pairs(nullptr, bytes, h->keys_in, h->keys_out, h->vals_in, h->perm, (uint32_t)R, 0,
+                                      32, st) != hipSuccess)
+            return fail(h, NETKV_EDEVICE, "sort size query failed");
+        uint8_t *tmp = nullptr;
+        if (dalloc(tmp, std::max<size_t>(bytes, 16)) != hipSuccess)
+            return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
+        h->sort_tmp = tmp;
+        h->sort_tmp_bytes = std::max<size_t>(bytes, 16);
+        h->order_cap = R;
+    }
+    if (!h->n_valid && dalloc(h->n_valid, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    if (partial_elems > h->partial_cap) {
+        dfree(h->partial);
+        h->partial_cap = 0;
+        if (dalloc(h->partial, partial_elems) != hipSuccess)
+            return fail(h, NETKV_ENOMEM, "partial top-k scratch allocation failed");
+        h->partial_cap = partial_elems;
+    }
+    return NETKV_OK;
+}
+
+uint32_t auto_run_len(uint64_t R, uint32_t nchunk) {
+    // about 64K wavefronts in flight; runs of 8..1024 sorted requests
+    uint64_t rl = (R * nchunk) / 65536;
+    if (rl < 8) rl = 8;
+    if (rl > 1024) rl = 1024;
+    return (uint32_t)rl;
+}
+
+template <int K>
+void launch_scan_reduce(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
+                        uint32_t n_runs, uint32_t nchunk, uint32_t reuse, uint64_t *partial, const PairOut &po,
+                        bool pairs, uint32_t k, int32_t *idx, float *score, hipStream_t st) {
+    const uint64_t waves = (uint64_t)n_runs * nchunk;
+    const uint32_t grid = (uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    if (pairs)
+        hipLaunchKernelGGL((scan_kernel<K, kSpec, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
+                           ord.n_valid, rq.n_req, run_len, n_runs, nchunk, reuse, partial, po);
+    else
+        hipLaunchKernelGGL((scan_kernel<K, kSpec, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
+                           ord.n_valid, rq.n_req, run_len, n_runs, nchunk, reuse, partial, po);
+    hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, nchunk, k,
+                       (const uint64_t *)partial, ord.perm, ord.n_valid, idx, score);
+}
+
+// The whole selection of one batch on `st`: validate + order, sort, common
+// prefixes, scan, merge.
+netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
+                        const PairOut &po, bool pairs, hipStream_t st) {
+    const uint64_t R = req->n_req;
+    const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
+    const uint32_t nchunk = (h->D + kWave - 1) / kWave;
+    netkv_status e = ensure_order_scratch(h, R, R * nchunk * K, st);
+    if (e) return e;
+    const Snap sn = make_snap(h);
+    const Table t = make_table(h);
+    const Reqs rq = make_reqs(req);
+    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 16 * kWavesPerBlock - 1) / (16 * kWavesPerBlock))),
+                       dim3(kBlock), 0, st, sn, rq, h->keys_in, h->vals_in, h->errword);
+    HIPCHK(h, hipGetLastError());
+    size_t tb = h->sort_tmp_bytes;
+    HIPCHK(h, rocprim::radix_sort_pairs(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm, (uint32_t)R, 0,
+                                        32, st));
+    hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(64), 0, st, (const uint32_t *)h->keys_out, (uint32_t)R,
+                       h->n_valid);
+    hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
+                       (const uint32_t *)h->n_valid, h->rec);
+    HIPCHK(h, hipGetLastError());
+    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, nchunk);
+    const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
+    Order ord{h->perm, h->rec, h->n_valid};
+    if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, st));
+    if (K == 1)
+        launch_scan_reduce<1>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
+                              idx, score, st);
+    else if (K == 2)
+        launch_scan_reduce<2>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
+                              idx, score, st);
+    else if (K == 4)
+        launch_scan_reduce<4>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
+                              idx, score, st);
+    else
+        launch_scan_reduce<8>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
+                              idx, score, st);
+    HIPCHK(h, hipGetLastError());
+    if (h->timing) {
+        HIPCHK(h, hipEventRecord(h->ev1, st));
+        h->timed = true;
+    }
+    return NETKV_OK;
 }
 
 bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
@@ -733,6 +989,8 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->cnt);
         dfree(h->adm);
         dfree(h->bytes);
+        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->rec);
+        dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial);
         if (h->ev0) (void)hipEventDestroy(h->ev0);
         if (h->ev1) (void)hipEventDestroy(h->ev1);
     }
@@ -982,14 +1240,7 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
         po.score = pairs->score;
         want_pairs = po.j || po.feas || po.score;
     }
-    if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, s));
-    launch_select(make_snap(h), make_table(h), make_reqs(req), k, out_idx, out_score, po, want_pairs, h->errword, s);
-    HIPCHK(h, hipGetLastError());
-    if (h->timing) {
-        HIPCHK(h, hipEventRecord(h->ev1, s));
-        h->timed = true;
-    }
-    return NETKV_OK;
+    return run_select(h, req, k, out_idx, out_score, po, want_pairs, s);
 }
 
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen, const float *util_scen,
@@ -1025,8 +1276,7 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
     Reqs rq = make_reqs(req);
     // prefix lengths (transposed) and the selection under the loaded congestion
     PairOut po{nullptr, nullptr, nullptr, h->jT};
-    launch_select(sn, make_table(h), rq, 1, h->base_idx, h->base_score, po, true, h->errword, s);
-    HIPCHK(h, hipGetLastError());
+    if ((st = run_select(h, req, 1, h->base_idx, h->base_score, po, true, s))) return st;
     if (out_flips) {
         hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(2ull * n_scen, 256)), dim3(256), 0, s, out_flips,
                            2ull * n_scen, 0ull);
@@ -1141,6 +1391,22 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms) {
     HIPCHK(h, hipEventSynchronize(h->ev1));
     HIPCHK(h, hipEventElapsedTime(ms, h->ev0, h->ev1));
     return NETKV_OK;
+}
+
+netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    switch (option) {
+    case NETKV_OPT_RUN_LEN:
+        if (value > (1u << 20)) return fail(h, NETKV_EINVAL, "run length must be <= 2^20");
+        h->run_len_opt = value;
+        return NETKV_OK;
+    case NETKV_OPT_REUSE:
+        h->reuse_opt = value ? 1u : 0u;
+        return NETKV_OK;
+    default:
+        return fail(h, NETKV_EINVAL, "unknown option %d", option);
+    }
 }
 
 netkv_status netkv_cache_info(netkv_handle h, uint64_t *slots_per_decode, uint64_t *table_bytes) {

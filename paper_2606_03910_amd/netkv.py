@@ -77,7 +77,11 @@ _SIGS = {
     "netkv_set_timing": (C.c_int32, [C.c_void_p, C.c_int]),
     "netkv_kernel_ms": (C.c_int32, [C.c_void_p, C.POINTER(C.c_float)]),
     "netkv_cache_info": (C.c_int32, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]),
+    "netkv_set_option": (C.c_int32, [C.c_void_p, C.c_int, C.c_uint32]),
 }
+
+NETKV_OPT_RUN_LEN = 1
+NETKV_OPT_REUSE = 2
 
 
 def load_library(path: str = LIB_PATH):
@@ -258,6 +262,10 @@ def netkv_kernel_ms(h: int) -> float:
     ms = C.c_float()
     _check(h, load_library().netkv_kernel_ms(h, C.byref(ms)))
     return float(ms.value)
+
+
+def netkv_set_option(h: int, option: int, value: int) -> None:
+    _check(h, load_library().netkv_set_option(h, int(option), int(value)))
 
 
 def netkv_cache_info(h: int):
