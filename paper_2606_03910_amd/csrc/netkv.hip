@@ -50,6 +50,7 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
+constexpr uint32_t kFib32 = 0x9E3779B1u;
 constexpr uint64_t kEmptyKey = ~0ull; // empty top-k entry (sorts last)
 
 enum : uint32_t {
@@ -81,7 +82,7 @@ struct Snap {
 struct Table {
     const uint64_t *keys;
     uint64_t mask;
-    uint32_t shift;   // 64 - log2(capacity)
+    uint32_t shift;   // 32 - log2(capacity)
     uint32_t pitch;
 };
 
@@ -101,8 +102,11 @@ struct PairOut {
     uint16_t *jT;       // [D][R] (internal, for the sweep)
 };
 
+// Home slot of hash h in a table of 2^b slots (shift = 32 - b): the hash is
+// folded to 32 bits and spread by Fibonacci (multiplicative) hashing.
 __host__ __device__ inline uint64_t home_slot(uint64_t h, uint32_t shift) {
-    return (h * kGolden) >> shift;
+    const uint32_t fold = (uint32_t)h ^ (uint32_t)(h >> 32);
+    return (uint64_t)((fold * kFib32) >> shift);
 }
 
 // T_queue + T_decode of decode d, scaled by alpha (Sec. IV-B, Eqs. (6)-(7)).
@@ -321,121 +325,216 @@ __device__ inline Rec load_rec(const Rec *base, uint32_t i) {
     return x;
 }
 
-// First-miss scan of one request's run on the 64 decodes of a wavefront,
-// for the lanes in `need`, starting at block `start` (uniform).  W home-slot
-// loads are issued together per step; colliding slots are followed by
-// linear probing.  Lanes not in `need` return j_in.
-template <int W>
-__device__ inline uint32_t probe_from(const uint64_t *__restrict__ col, const Table &t, cptr<uint64_t> run,
-                                      uint32_t n, uint32_t start, bool need, uint32_t j_in) {
-    uint32_t j = start;
-    bool alive = need;
-    for (uint32_t i0 = start; i0 < n; i0 += W) {
-        if (!__any(alive)) break;
-        uint64_t h[W], sl[W], key[W];
+// Resolve one membership test on the C columns of a lane: key[q] is column
+// q's value at the home slot of h; colliding slots are followed by linear
+// probing (the slot sequence is the same for every lane and column, so
+// continuation rows stay coalesced).  Columns not alive stay dead.
+template <int C>
+__device__ inline void member(const uint64_t *const (&col)[C], const Table &t, uint64_t h, uint64_t home,
+                              const uint64_t (&key)[C], bool (&alive)[C]) {
+    bool pend[C];
+    bool any = false;
+#pragma unroll
+    for (int q = 0; q < C; ++q) {
+        pend[q] = alive[q] && key[q] != h && key[q] != 0;
+        alive[q] = alive[q] && key[q] == h;
+        any = any || pend[q];
+    }
+    if (!__any(any)) return;
+#pragma unroll
+    for (int q = 0; q < C; ++q) {
+        uint64_t s2 = home;
+        while (__any(pend[q])) {
+            s2 = (s2 + 1) & t.mask;
+            if (pend[q]) {
+                const uint64_t k2 = col[q][s2 * t.pitch];
+                if (k2 == h) {
+                    alive[q] = true;
+                    pend[q] = false;
+                } else if (k2 == 0) {
+                    pend[q] = false;
+                }
+            }
+        }
+    }
+}
+
+// First-miss scan of one request's run on the C columns of every lane of a
+// wavefront, for the columns in need[], starting at block `start` (uniform,
+// < n) whose hash h0 and home-slot values key0[] were loaded beforehand.
+// Past the first block, W home-slot loads per column are issued together per
+// step.  j[] holds, for the columns in need, `start` on entry and the
+// first-miss index on return; other columns are left alone.
+template <int W, int C>
+__device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &t, cptr<uint64_t> run, uint32_t n,
+                                  uint32_t start, const bool (&need)[C], uint32_t (&j)[C], uint64_t h0,
+                                  const uint64_t (&key0)[C]) {
+    bool alive[C];
+#pragma unroll
+    for (int q = 0; q < C; ++q) alive[q] = need[q];
+    member<C>(col, t, h0, home_slot(h0, t.shift), key0, alive);
+#pragma unroll
+    for (int q = 0; q < C; ++q) j[q] += alive[q] ? 1u : 0u;
+    for (uint32_t i0 = start + 1; i0 < n; i0 += W) {
+        bool any = false;
+#pragma unroll
+        for (int q = 0; q < C; ++q) any = any || alive[q];
+        if (!__any(any)) break;
+        uint64_t h[W], sl[W];
+        uint64_t key[W][C];
+        if (i0 + W <= n) {
+#pragma unroll
+            for (int w = 0; w < W; ++w) h[w] = run[i0 + w];
+        } else {
+#pragma unroll
+            for (int w = 0; w < W; ++w) h[w] = i0 + w < n ? run[i0 + w] : 0;
+        }
 #pragma unroll
         for (int w = 0; w < W; ++w) {
-            const uint32_t i = i0 + w;
-            h[w] = i < n ? run[i] : 0;
             sl[w] = home_slot(h[w], t.shift);
-            key[w] = 0;
-            if (alive && i < n) key[w] = col[sl[w] * t.pitch];
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                key[w][q] = 0;
+                if (alive[q] && i0 + w < n) key[w][q] = col[q][sl[w] * t.pitch];
+            }
         }
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             if (i0 + w >= n) break;
-            bool hit = alive && key[w] == h[w];
-            bool pend = alive && key[w] != h[w] && key[w] != 0;
-            uint64_t s2 = sl[w];
-            while (__any(pend)) {
-                s2 = (s2 + 1) & t.mask;
-                if (pend) {
-                    const uint64_t k2 = col[s2 * t.pitch];
-                    if (k2 == h[w]) {
-                        hit = true;
-                        pend = false;
-                    } else if (k2 == 0) {
-                        pend = false;
-                    }
-                }
-            }
-            alive = hit;
-            j += alive ? 1u : 0u;
+            member<C>(col, t, h[w], sl[w], key[w], alive);
+#pragma unroll
+            for (int q = 0; q < C; ++q) j[q] += alive[q] ? 1u : 0u;
         }
     }
-    return need ? j : j_in;
 }
 
-// One wavefront per (run of sorted requests, chunk of 64 decodes).  For each
-// request of the run: first-miss prefix length per decode (carried from the
-// previous request where the common leading run decides it), non-cached
-// bytes, feasibility and cost (Eqs. (2)-(7)), then the chunk's K best
-// feasible (score, index) keys into partial[chunk][sorted position][0..K).
-// Request records are fetched two requests ahead and the congestion row one
-// request ahead, so the per-request chain of dependent loads is short.
-template <int K, int W, bool PAIRS>
+// One wavefront per (run of sorted requests, group of 64*C decodes); lane l
+// holds decodes g*64*C + q*64 + l, q < C.  For each request of the run:
+// first-miss prefix length per decode (carried from the previous request
+// where the common leading run decides it), non-cached bytes, feasibility
+// and cost (Eqs. (2)-(7)), then the group's K best feasible (score, index)
+// keys into partial[group][sorted position][0..K).  Request records are
+// fetched two requests ahead, and the congestion row and the first probe
+// row one request ahead.
+template <int K, int W, int C, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec *__restrict__ rec,
                                                       const uint64_t *__restrict__ hashes,
                                                       const uint32_t *__restrict__ n_valid, uint32_t n_req,
-                                                      uint32_t run_len, uint32_t n_runs, uint32_t nchunk,
+                                                      uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
                                                       uint32_t reuse, uint64_t *__restrict__ partial, PairOut po) {
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t gw = blockIdx.x * kWavesPerBlock + wave_index();
-    const uint32_t run = gw / nchunk, chunk = gw % nchunk;
+    const uint32_t run = gw / ngroup, grp = gw % ngroup;
     if (run >= n_runs) return;
     const uint32_t nv = *n_valid;
     const uint32_t i0 = run * run_len;
     if (i0 >= nv) return;
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
-    const uint32_t d = chunk * kWave + lane;
-    const bool act = d < s.D;
-    const uint32_t dd = act ? d : 0;
-    const uint64_t *col = t.keys + dd;
-    const float load = act ? load_term(s, d) : 0.0f;
-    const uint64_t mem = act ? s.free_mem[d] : 0;
+    const uint32_t base = grp * (kWave * C);
+    uint32_t d[C];
+    bool act[C];
+    const uint64_t *col[C];
+    float load[C];
+    uint64_t mem[C];
+#pragma unroll
+    for (int q = 0; q < C; ++q) {
+        d[q] = base + q * kWave + lane;
+        act[q] = d[q] < s.D;
+        col[q] = t.keys + (act[q] ? d[q] : 0);
+        load[q] = act[q] ? load_term(s, d[q]) : 0.0f;
+        mem[q] = act[q] ? s.free_mem[d[q]] : 0;
+    }
     const cptr<uint64_t> chash = as_const(hashes);
     Rec c0 = load_rec(rec, i0);
     Rec c1 = load_rec(rec, i0 + 1 < i1 ? i0 + 1 : i0);
-    uint8_t tau0 = s.tier_map[(uint64_t)c0.p * s.D + dd];
-    float u0 = s.util[(uint64_t)c0.p * s.D + dd];
-    uint32_t j_prev = 0;
+    uint8_t tau0[C];
+    float u0[C];
+#pragma unroll
+    for (int q = 0; q < C; ++q) {
+        const uint64_t o = (uint64_t)c0.p * s.D + (act[q] ? d[q] : 0);
+        tau0[q] = s.tier_map[o];
+        u0[q] = s.util[o];
+    }
+    // first membership test of the current request (block L0), loaded ahead
+    uint32_t L0 = 0;
+    uint64_t h0 = c0.n ? chash[c0.a] : 0;
+    uint64_t k0[C];
+#pragma unroll
+    for (int q = 0; q < C; ++q) k0[q] = (act[q] && c0.n) ? col[q][home_slot(h0, t.shift) * t.pitch] : 0;
+    uint32_t j_prev[C];
+#pragma unroll
+    for (int q = 0; q < C; ++q) j_prev[q] = 0;
     for (uint32_t i = i0; i < i1; ++i) {
         const Rec c2 = load_rec(rec, i + 2 < i1 ? i + 2 : i1 - 1);
-        const uint8_t tau1 = s.tier_map[(uint64_t)c1.p * s.D + dd];
-        const float u1 = s.util[(uint64_t)c1.p * s.D + dd];
-        const uint32_t L = (reuse && i != i0) ? c0.lcp : 0u;
-        const bool carry = j_prev < L;
-        uint32_t j = carry ? j_prev : L;
-        if (L < c0.n) j = probe_from<W>(col, t, chash + c0.a, c0.n, L, act && !carry, j);
-        j_prev = j;
-        const PairCost pc = pair_cost(s, c0.p, mem, c0.len, j, tau0, u0, load);
-        const bool feas = act && pc.feas;
-        const float cost = pc.cost;
-        if (PAIRS && act) {
-            const uint64_t o = (uint64_t)c0.r * s.D + d;
-            if (po.j) po.j[o] = (uint16_t)j;
-            if (po.feas) po.feas[o] = feas ? 1 : 0;
-            if (po.score) po.score[o] = cost;
-            if (po.jT) po.jT[(uint64_t)d * n_req + c0.r] = (uint16_t)j;
+        uint8_t tau1[C];
+        float u1[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            const uint64_t o = (uint64_t)c1.p * s.D + (act[q] ? d[q] : 0);
+            tau1[q] = s.tier_map[o];
+            u1[q] = s.util[o];
         }
-        // the chunk's K best feasible decodes: minimum cost bits over lanes,
-        // ties to the lowest lane (= lowest decode index)
-        uint32_t cb = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
+        const uint32_t L1 = reuse ? c1.lcp : 0u;
+        const bool more = i + 1 < i1 && L1 < c1.n;
+        const uint64_t h1 = more ? chash[c1.a + L1] : 0;
+        uint64_t k1[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) k1[q] = (act[q] && more) ? col[q][home_slot(h1, t.shift) * t.pitch] : 0;
+        // prefix lengths: carried where the common leading run decides them
+        uint32_t j[C];
+        bool need[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            const bool carry = j_prev[q] < L0;
+            j[q] = carry ? j_prev[q] : L0;
+            need[q] = act[q] && !carry;
+        }
+        if (L0 < c0.n) probe_from<W, C>(col, t, chash + c0.a, c0.n, L0, need, j, h0, k0);
+        // Eq. (2) in integer form, feasibility and the cost of Eqs. (3)-(7)
+        uint32_t cb[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            j_prev[q] = j[q];
+            const PairCost pc = pair_cost(s, c0.p, mem[q], c0.len, j[q], tau0[q], u0[q], load[q]);
+            if (PAIRS && act[q]) {
+                const uint64_t o = (uint64_t)c0.r * s.D + d[q];
+                if (po.j) po.j[o] = (uint16_t)j[q];
+                if (po.feas) po.feas[o] = pc.feas ? 1 : 0;
+                if (po.score) po.score[o] = pc.cost;
+                if (po.jT) po.jT[(uint64_t)d[q] * n_req + c0.r] = (uint16_t)j[q];
+            }
+            cb[q] = (act[q] && pc.feas) ? __float_as_uint(pc.cost) : 0xFFFFFFFFu;
+        }
+        // the group's K best: least cost bits, then least decode index
         uint64_t mine = kEmptyKey;
 #pragma unroll
-        for (int q = 0; q < K; ++q) {
-            const uint32_t mn = wave_min_u32_dpp(cb);
-            const uint64_t tie = __ballot(cb == mn && mn != 0xFFFFFFFFu);
-            const uint32_t wl = tie ? (uint32_t)__builtin_ctzll(tie) : 64u;
-            if (lane == wl) cb = 0xFFFFFFFFu;
-            if (lane == (uint32_t)q)
-                mine = tie ? (((uint64_t)mn << 32) | (uint64_t)(chunk * kWave + wl)) : kEmptyKey;
+        for (int r = 0; r < K; ++r) {
+            uint32_t lm = cb[0], lq = 0;
+#pragma unroll
+            for (int q = 1; q < C; ++q)
+                if (cb[q] < lm) {
+                    lm = cb[q];
+                    lq = q;
+                }
+            const uint32_t mn = wave_min_u32_dpp(lm);
+            const uint32_t dm = wave_min_u32_dpp((lm == mn && mn != 0xFFFFFFFFu) ? base + lq * kWave + lane
+                                                                                    : 0xFFFFFFFFu);
+#pragma unroll
+            for (int q = 0; q < C; ++q)
+                if (mn != 0xFFFFFFFFu && d[q] == dm) cb[q] = 0xFFFFFFFFu;
+            if (lane == (uint32_t)r) mine = mn != 0xFFFFFFFFu ? (((uint64_t)mn << 32) | (uint64_t)dm) : kEmptyKey;
         }
-        if (lane < (uint32_t)K) partial[((uint64_t)chunk * n_req + i) * K + lane] = mine;
+        if (lane < (uint32_t)K) partial[((uint64_t)grp * n_req + i) * K + lane] = mine;
         c0 = c1;
         c1 = c2;
-        tau0 = tau1;
-        u0 = u1;
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            tau0[q] = tau1[q];
+            u0[q] = u1[q];
+            k0[q] = k1[q];
+        }
+        L0 = L1;
+        h0 = h1;
     }
 }
 
@@ -804,7 +903,7 @@ Table make_table(netkv_handle h) {
     Table t;
     t.keys = h->table;
     t.mask = h->cap - 1;
-    t.shift = 64 - h->log2cap;
+    t.shift = 32 - h->log2cap;
     t.pitch = h->pitch;
     return t;
 }
@@ -871,27 +970,41 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
     return NETKV_OK;
 }
 
-uint32_t auto_run_len(uint64_t R, uint32_t nchunk) {
+uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
     // about 64K wavefronts in flight; runs of 8..1024 sorted requests
-    uint64_t rl = (R * nchunk) / 65536;
+    uint64_t rl = (R * ngroup) / 65536;
     if (rl < 8) rl = 8;
     if (rl > 1024) rl = 1024;
     return (uint32_t)rl;
 }
 
-template <int K>
-void launch_scan_reduce(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
-                        uint32_t n_runs, uint32_t nchunk, uint32_t reuse, uint64_t *partial, const PairOut &po,
-                        bool pairs, uint32_t k, int32_t *idx, float *score, hipStream_t st) {
-    const uint64_t waves = (uint64_t)n_runs * nchunk;
+// decodes per lane: 4 when there are many decodes, else 1
+inline uint32_t cols_per_lane(uint32_t D) { return D >= 8u * kWave ? 4u : 1u; }
+
+template <int K, int C>
+void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
+                 uint32_t n_runs, uint32_t ngroup, uint32_t reuse, uint64_t *partial, const PairOut &po, bool pairs,
+                 hipStream_t st) {
+    constexpr int W = C >= 4 ? 2 : kSpec;
+    const uint64_t waves = (uint64_t)n_runs * ngroup;
     const uint32_t grid = (uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (pairs)
-        hipLaunchKernelGGL((scan_kernel<K, kSpec, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
-                           ord.n_valid, rq.n_req, run_len, n_runs, nchunk, reuse, partial, po);
+        hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
+                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, reuse, partial, po);
     else
-        hipLaunchKernelGGL((scan_kernel<K, kSpec, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
-                           ord.n_valid, rq.n_req, run_len, n_runs, nchunk, reuse, partial, po);
-    hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, nchunk, k,
+        hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
+                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, reuse, partial, po);
+}
+
+template <int K>
+void launch_scan_reduce(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
+                        uint32_t n_runs, uint32_t ngroup, uint32_t C, uint32_t reuse, uint64_t *partial,
+                        const PairOut &po, bool pairs, uint32_t k, int32_t *idx, float *score, hipStream_t st) {
+    if (C == 4)
+        launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+    else
+        launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+    hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
                        (const uint64_t *)partial, ord.perm, ord.n_valid, idx, score);
 }
 
@@ -901,8 +1014,9 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
                         const PairOut &po, bool pairs, hipStream_t st) {
     const uint64_t R = req->n_req;
     const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
-    const uint32_t nchunk = (h->D + kWave - 1) / kWave;
-    netkv_status e = ensure_order_scratch(h, R, R * nchunk * K, st);
+    const uint32_t C = cols_per_lane(h->D);
+    const uint32_t ngroup = (h->D + kWave * C - 1) / (kWave * C);
+    netkv_status e = ensure_order_scratch(h, R, R * ngroup * K, st);
     if (e) return e;
     const Snap sn = make_snap(h);
     const Table t = make_table(h);
@@ -918,22 +1032,22 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
                        (const uint32_t *)h->n_valid, h->rec);
     HIPCHK(h, hipGetLastError());
-    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, nchunk);
+    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{h->perm, h->rec, h->n_valid};
     if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, st));
     if (K == 1)
-        launch_scan_reduce<1>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
-                              idx, score, st);
+        launch_scan_reduce<1>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
+                              k, idx, score, st);
     else if (K == 2)
-        launch_scan_reduce<2>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
-                              idx, score, st);
+        launch_scan_reduce<2>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
+                              k, idx, score, st);
     else if (K == 4)
-        launch_scan_reduce<4>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
-                              idx, score, st);
+        launch_scan_reduce<4>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
+                              k, idx, score, st);
     else
-        launch_scan_reduce<8>(sn, t, rq, ord, run_len, n_runs, nchunk, h->reuse_opt, h->partial, po, pairs, k,
-                              idx, score, st);
+        launch_scan_reduce<8>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
+                              k, idx, score, st);
     HIPCHK(h, hipGetLastError());
     if (h->timing) {
         HIPCHK(h, hipEventRecord(h->ev1, st));
@@ -1197,7 +1311,7 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     e = hipMemsetAsync(tab, 0, tbytes, st);
     if (e == hipSuccess && !tdec.empty()) {
         hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, cap - 1,
-                           64u - log2cap, pitch, (const uint64_t *)dh, (const uint32_t *)ddec,
+                           32u - log2cap, pitch, (const uint64_t *)dh, (const uint32_t *)ddec,
                            (const uint64_t *)dbeg, (const uint64_t *)dend, h->loadword);
         e = hipGetLastError();
     }
