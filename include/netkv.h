@@ -187,7 +187,8 @@ netkv_status netkv_state_get(netkv_handle h, uint16_t *n_inflight, uint32_t *que
 netkv_status netkv_sync_errors(netkv_handle h, void *stream);
 
 /* Kernel timing: when enabled, the library records HIP events on `stream`
- * around the scoring kernels (scan and merge) of each netkv_select_batch,
+ * around the scoring kernel (the fused match / score / per-group top-k scan,
+ * not the ordering or merge kernels) of each netkv_select_batch,
  * and around the sweep kernel of netkv_rank_sweep; netkv_kernel_ms returns
  * (after synchronising on the end event) the milliseconds of the last one. */
 netkv_status netkv_set_timing(netkv_handle h, int enable);

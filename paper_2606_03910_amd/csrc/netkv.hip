@@ -996,16 +996,26 @@ void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &or
                            ord.n_valid, rq.n_req, run_len, n_runs, ngroup, reuse, partial, po);
 }
 
+// Scan, bracketed by the handle's timing events when enabled, then merge.
 template <int K>
-void launch_scan_reduce(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
-                        uint32_t n_runs, uint32_t ngroup, uint32_t C, uint32_t reuse, uint64_t *partial,
-                        const PairOut &po, bool pairs, uint32_t k, int32_t *idx, float *score, hipStream_t st) {
+hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
+                              uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C, uint32_t reuse,
+                              uint64_t *partial, const PairOut &po, bool pairs, uint32_t k, int32_t *idx,
+                              float *score, hipStream_t st) {
+    hipError_t e = hipSuccess;
+    if (h->timing && (e = hipEventRecord(h->ev0, st)) != hipSuccess) return e;
     if (C == 4)
         launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
     else
         launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (h->timing) {
+        if ((e = hipEventRecord(h->ev1, st)) != hipSuccess) return e;
+        h->timed = true;
+    }
     hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
                        (const uint64_t *)partial, ord.perm, ord.n_valid, idx, score);
+    return hipGetLastError();
 }
 
 // The whole selection of one batch on `st`: validate + order, sort, common
@@ -1035,24 +1045,18 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{h->perm, h->rec, h->n_valid};
-    if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, st));
     if (K == 1)
-        launch_scan_reduce<1>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
-                              k, idx, score, st);
+        HIPCHK(h, launch_scan_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+                                        pairs, k, idx, score, st));
     else if (K == 2)
-        launch_scan_reduce<2>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
-                              k, idx, score, st);
+        HIPCHK(h, launch_scan_reduce<2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+                                        pairs, k, idx, score, st));
     else if (K == 4)
-        launch_scan_reduce<4>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
-                              k, idx, score, st);
+        HIPCHK(h, launch_scan_reduce<4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+                                        pairs, k, idx, score, st));
     else
-        launch_scan_reduce<8>(sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po, pairs,
-                              k, idx, score, st);
-    HIPCHK(h, hipGetLastError());
-    if (h->timing) {
-        HIPCHK(h, hipEventRecord(h->ev1, st));
-        h->timed = true;
-    }
+        HIPCHK(h, launch_scan_reduce<8>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+                                        pairs, k, idx, score, st));
     return NETKV_OK;
 }
 
