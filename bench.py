@@ -58,13 +58,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="c2", choices=["c0", "c1", "c2", "c4"])
+    ap.add_argument("--workload", default="c2", choices=["c0", "c1", "c2", "c3", "c4"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-reuse", action="store_true",
                     help="scan every pair from block 0 (no first-miss carry along the batch order)")
     ap.add_argument("--run-len", type=int, default=0, help="requests per wavefront run (0 = auto)")
+    ap.add_argument("--cols", type=int, default=0, help="decodes per lane (0 = auto, 1, 2, 4)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (K launches) and exit: the "
                          "reference kernel for scaling HBM byte counters")
@@ -93,6 +94,10 @@ def main():
 
     cfg = W.CONFIGS[args.workload]
     dev = torch.device("cuda", 0)
+    if args.workload == "c3":
+        return bench_sweep(args, cfg, dev)
+    if args.workload == "c1":
+        return bench_stream(args, cfg, dev)
     t0 = time.time()
     snap = W.make_snapshot(cfg, args.seed)
     ch = W.prefix_chains(cfg, args.seed)
@@ -104,6 +109,7 @@ def main():
     sel = netkv.Selector(0)
     netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_REUSE, 0 if args.no_reuse else 1)
     netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_RUN_LEN, args.run_len)
+    netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_COLS, args.cols)
     t0 = time.time()
     sel.load_snapshot(snap)
     sel.load_cache(cache, 0.5)
@@ -248,7 +254,7 @@ def main():
             "algorithmic_bytes_per_launch": b_alg,
             "membership_tests_per_launch": tests,
             "mean_tests_per_pair": tests / pairs,
-            "kernel": "scan_kernel (k=1; %d decodes per lane)" % (4 if D >= 512 else 1),
+            "kernel": "scan_kernel (k=1; %d decodes per lane)" % (args.cols or (4 if D >= 512 else 1)),
             "kernel_source_sha256_16": digest,
             "note": ("achieved counts 8 B per first-miss membership test of every pair, as if each "
                      "were read from HBM; the kernel takes most tests from its predecessor in the "
@@ -256,6 +262,149 @@ def main():
                      "traffic is the counter-measured HBM traffic of the same kernel."),
         },
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    sel.close()
+
+
+FP32_PEAK_TFLOPS = 157.3   # MI355X published fp32 vector peak (counts packed fp32)
+SWEEP_FLOPS_PER_PAIR = 7    # (1 - c), B (1 - c), s_eff (1 + n), the division, + L, + load, (1 + n)
+
+
+def bench_sweep(args, cfg, dev):
+    """Ranking sweep: one step = netkv_rank_sweep over all scenarios."""
+    import torch
+
+    from paper_2606_03910_amd import netkv
+    from paper_2606_03910_amd import workload as W
+    snap = W.make_snapshot(cfg, args.seed)
+    ch = W.prefix_chains(cfg, args.seed)
+    req = W.make_requests(cfg, args.seed, chains=ch)
+    cache = W.make_caches(cfg, args.seed, chains=ch)
+    util_s, _ = W.scenario_utils(cfg, args.seed, snap["links"])
+    S, R, D, P, k = cfg.n_scenarios, cfg.n_requests, cfg.n_decode, cfg.n_prefill, 3
+    sel = netkv.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = netkv.requests_to_device(req, dev)
+    us = netkv.to_device(util_s.reshape(-1), dev)
+    out = dict(idx=torch.empty(S * R * k, dtype=torch.int32, device=dev),
+               score=torch.empty(S * R * k, dtype=torch.float32, device=dev),
+               flips=torch.empty(2 * S, dtype=torch.uint64, device=dev))
+
+    def step():
+        netkv.netkv_rank_sweep(sel.h, rd, S, us, k, out["idx"], out["score"], out["flips"], dev, P * D)
+
+    for _ in range(args.warmup):
+        step()
+    sel.sync_errors()
+    stream = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    netkv.netkv_set_timing(sel.h, True)
+    kms = []
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+        kms.append(netkv.netkv_kernel_ms(sel.h))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    sel.sync_errors()
+    step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    kern_ms = float(np.mean(kms))
+    log(f"sweep: step {step_ms:.3f} ms, sweep kernel {kern_ms:.3f} ms")
+    pairs = S * R * D
+    flops = SWEEP_FLOPS_PER_PAIR * pairs
+    achieved = flops / (kern_ms * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = oracle.max_threads()
+        ns = 8
+        t0 = time.perf_counter()
+        o = oracle.rank_sweep(snap, cache, req, util_s[:ns], k=k, n_threads=threads)
+        dt = time.perf_counter() - t0
+        cpu = dict(value=ns * R * D / dt, unit="pairs/s", cores=threads, kind="oracle",
+                   sample=f"{ns} scenarios x {R} requests x {D} decodes (prefix match once, "
+                          f"then rescoring), {dt:.1f} s")
+    rec = {
+        "metric": "scored (request,decode) pairs/sec + selections/sec; achieved HBM GB/s vs peak",
+        "value": pairs / (step_ms * 1e-3), "unit": "pairs/s",
+        "selections_per_s": S * R / (step_ms * 1e-3),
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps, "step_ms_events": step_ms, "kernel_ms": kern_ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded; lognormal link-noise scenarios)",
+        "config": {"workload": cfg.name, "requests": R, "decodes": D, "prefills": P,
+                   "scenarios": S, "sigmas": list(cfg.noise_sigmas), "k": k,
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": FP32_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / FP32_PEAK_TFLOPS, "traffic": None,
+                     "algorithmic_flops_per_launch": flops,
+                     "kernel": "sweep_kernel<4> (k=3)",
+                     "note": "7 fp32 operations per scenario-pair of Eqs. (3)-(5); the peak counts "
+                             "packed fp32, which this build does not emit"},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    sel.close()
+
+
+def bench_stream(args, cfg, dev):
+    """Streaming batches: one step = all batches, each a congestion refresh,
+    a selection and the between-batch update."""
+    import torch
+
+    from paper_2606_03910_amd import netkv
+    from paper_2606_03910_amd import workload as W
+    snap = W.make_snapshot(cfg, args.seed)
+    ch = W.prefix_chains(cfg, args.seed)
+    cache = W.make_caches(cfg, args.seed, chains=ch)
+    links = W.ar1_links(cfg, args.seed, snap["links"], cfg.n_batches)
+    utils = [netkv.to_device(W.pair_util(cfg.cluster, links[t]).reshape(-1), dev)
+             for t in range(cfg.n_batches)]
+    reqs = [netkv.requests_to_device(W.make_requests(cfg, args.seed, batch=t, chains=ch), dev)
+            for t in range(cfg.n_batches)]
+    R, D, B = cfg.n_requests, cfg.n_decode, cfg.n_batches
+    mu = -(-R // D)
+    sel = netkv.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    idx = torch.empty(R, dtype=torch.int32, device=dev)
+    sc = torch.empty(R, dtype=torch.float32, device=dev)
+
+    def step():
+        sel.load_snapshot(snap)
+        for t in range(B):
+            netkv.netkv_oracle_set_util(sel.h, utils[max(0, t - 1)], dev)
+            netkv.netkv_select_batch(sel.h, reqs[t], 1, idx, sc, None, dev)
+            netkv.netkv_commit_batch(sel.h, reqs[t], idx, 16, mu, dev)
+
+    for _ in range(args.warmup):
+        step()
+    sel.sync_errors()
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    sel.sync_errors()
+    ms = wall * 1e3 / args.steps
+    rec = {
+        "metric": "scored (request,decode) pairs/sec + selections/sec; achieved HBM GB/s vs peak",
+        "value": B * R * D / (ms * 1e-3), "unit": "pairs/s", "selections_per_s": B * R / (ms * 1e-3),
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32+u64",
+        "data": "synthetic (seeded; AR(1) congestion, staleness 1 batch)",
+        "config": {"workload": cfg.name, "requests_per_batch": R, "batches": B, "decodes": D,
+                   "prefills": cfg.n_prefill, "staleness": 1, "parallelism": "single-gpu"},
+        "roofline": None, "cpu_baseline": None,
+        "note": "wall time of the whole stream (snapshot load, per-batch congestion refresh, "
+                "selection and update); small batches are launch- and latency-bound",
     }
     print(json.dumps(rec), flush=True)
     sel.close()

@@ -201,8 +201,10 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
  *                        decode is taken from the preceding request of the
  *                        batch order when it lies inside their common
  *                        leading blocks (an exact identity, no probe);
- *                        0: every pair is scanned from block 0. */
-enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2 };
+ *                        0: every pair is scanned from block 0;
+ *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
+ *                        automatic (4 on pools of 512+ decodes, else 1), 1, 2, 4. */
+enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3 };
 netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 
 /* Table geometry of the loaded cache: slots per decode (a power of two)

@@ -6,13 +6,14 @@
 // of requests against one telemetry snapshot.
 //
 // Data layout in device memory (all owned by the handle):
-//   * resident-set tables: one open-addressed table per decode, all with the
-//     same power-of-two capacity and the same slot function, stored
-//     slot-major: table[slot * pitch + d] (pitch = D rounded up to 16).
-//     A wavefront scoring one request against 64 consecutive decodes probes
-//     the same slot index in all 64 tables, so each probe step is one
-//     contiguous 512-byte row segment: fully coalesced, whatever the hash.
-//     Empty slots hold 0 (hash value 0 is reserved).  Linear probing.
+//   * resident-set tables: one bucketized cuckoo table per decode (two
+//     candidate buckets per hash, two 8-byte slots per bucket), all with the
+//     same power-of-two bucket count and the same bucket functions, stored
+//     bucket-major: table[(bucket * pitch + d) * 2 + slot] (pitch = D rounded
+//     up to 16).  A membership test is exactly two independent 16-byte loads
+//     (no data-dependent continuation), and a wavefront testing one hash on
+//     64 consecutive decodes reads two contiguous 1 KiB row segments.
+//     Empty slots hold 0 (hash value 0 is reserved).
 //   * snapshot: tier_map u8[P*D], util f32[P*D] (row-major by prefill),
 //     n_inflight u16[4*P] (tier-major), free_mem u64[D], queue u32[D],
 //     batch u32[D], plus the admitted bytes of the previous batch u64[D].
@@ -28,7 +29,8 @@
 //   reduce_kernel  -- merges the per-chunk keys into each request's top-k.
 //   sweep_kernel   -- re-scoring under congestion scenarios with the prefix
 //                     lengths reused; lanes over requests.
-//   insert_kernel  -- builds the tables with 64-bit compare-and-swap.
+//   insert_kernel  -- builds the tables (cuckoo insertion with 64-bit CAS and
+//                     atomic exchange).
 //   commit kernels -- between-batch counter / queue / memory update.
 #include <hip/hip_runtime.h>
 #include <rocprim/device/device_radix_sort.hpp>
@@ -51,6 +53,7 @@ constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint32_t kFib32 = 0x9E3779B1u;
+constexpr uint32_t kMix32 = 0x85EBCA77u;
 constexpr uint64_t kEmptyKey = ~0ull; // empty top-k entry (sorts last)
 
 enum : uint32_t {
@@ -77,12 +80,15 @@ struct Snap {
     uint32_t bpt;
     uint32_t block_tokens;
     uint32_t P, D;
+    // derived once per call by derive_kernel (Eqs. (3)-(7) factored by (p, d) and d)
+    const float2 *pcon;      // [P*D] {seconds per non-cached token, tier latency}
+    const float *dbase;      // [D] alpha (T_queue + T_decode)
+    const uint64_t *dxlim;   // [D] x = l - lambda is feasible iff x < dxlim
 };
 
 struct Table {
-    const uint64_t *keys;
-    uint64_t mask;
-    uint32_t shift;   // 32 - log2(capacity)
+    const uint64_t *keys;   // [buckets][pitch][2]
+    uint32_t shift;         // 32 - log2(buckets)
     uint32_t pitch;
 };
 
@@ -102,11 +108,20 @@ struct PairOut {
     uint16_t *jT;       // [D][R] (internal, for the sweep)
 };
 
-// Home slot of hash h in a table of 2^b slots (shift = 32 - b): the hash is
-// folded to 32 bits and spread by Fibonacci (multiplicative) hashing.
-__host__ __device__ inline uint64_t home_slot(uint64_t h, uint32_t shift) {
+// The two candidate buckets of hash h in a table of 2^b buckets (shift =
+// 32 - b): the hash is folded to 32 bits and spread by two multiplicative
+// (Fibonacci-style) hashes; the second bucket is the first xor a nonzero
+// value below 2^b, so the two always differ.
+__host__ __device__ inline void buckets_of(uint64_t h, uint32_t shift, uint32_t &b1, uint32_t &b2) {
     const uint32_t fold = (uint32_t)h ^ (uint32_t)(h >> 32);
-    return (uint64_t)((fold * kFib32) >> shift);
+    b1 = (fold * kFib32) >> shift;
+    b2 = b1 ^ (((fold * kMix32) >> shift) | 1u);
+}
+
+// Is h in bucket b of the table column `col` (this decode's column)?
+__device__ inline bool bucket_has(const uint64_t *__restrict__ col, const Table &t, uint32_t b, uint64_t h) {
+    const ulonglong2 v = *(const ulonglong2 *)(col + (uint64_t)b * t.pitch * 2);
+    return v.x == h || v.y == h;
 }
 
 // T_queue + T_decode of decode d, scaled by alpha (Sec. IV-B, Eqs. (6)-(7)).
@@ -120,24 +135,25 @@ __device__ inline float load_term(const Snap &s, uint32_t d) {
     return s.alpha * ((float)blocked * t_cur + t_next);
 }
 
-// Eq. (2) in integer form, the feasibility mask and the cost C of Eq. (5)
-// with Eqs. (3)-(4), for prefix length j on decode d.
-struct PairCost {
-    float cost;
-    bool feas;
-};
-
-__device__ inline PairCost pair_cost(const Snap &s, uint32_t p, uint64_t m, uint32_t len, uint32_t j,
-                                     uint32_t tau_raw, float util, float load) {
-    const uint64_t s_eff = (uint64_t)s.bpt * (uint64_t)(len - s.block_tokens * j);
-    const bool feas = (m >= s.m_min) && (m - s.m_min >= s_eff);
-    const uint32_t tau = tau_raw & 3u;
+// The cost of Eq. (5) factored by what each factor depends on.  With
+// x = l_r - lambda non-cached tokens (Eq. (2) divided by the bytes per token):
+//   s_eff / B_eff(p,d) = x * bpt (1 + n_inflight[tau][p]) / (B_tau (1 - c(p,d)))
+// (Eqs. (3)-(4)), so the pair contributes x * spt(p,d) + L_tau, and the decode
+// alpha (T_queue + T_decode); feasibility m_d >= bpt x + m_min holds iff
+// x < xlim_d = floor((m_d - m_min) / bpt) + 1 (integer, exact).
+__device__ inline float sec_per_token(const Snap &s, uint32_t tau, uint32_t p, float c) {
     const float n = (float)s.n_inflight[tau * s.P + p];
-    const float t_x = ((float)s_eff * (1.0f + n)) / (s.bw[tau] * (1.0f - util)) + s.lat[tau];
-    PairCost pc;
-    pc.cost = t_x + load;
-    pc.feas = feas;
-    return pc;
+    return ((float)s.bpt * (1.0f + n)) / (s.bw[tau] * (1.0f - c));
+}
+
+__device__ inline uint64_t feasible_limit(const Snap &s, uint64_t m) {
+    if (m < s.m_min) return 0;
+    if (s.bpt == 0) return ~0ull;
+    return (m - s.m_min) / s.bpt + 1;
+}
+
+__device__ inline float pair_score(uint32_t x, float spt, float lat, float base) {
+    return fmaf((float)x, spt, lat + base);
 }
 
 __device__ inline uint64_t pack_key(float cost, uint32_t d) {
@@ -192,6 +208,24 @@ __device__ inline bool request_ok(const Reqs &rq, const Snap &s, uint32_t r, uin
     return true;
 }
 
+// Per-call factors of the cost: spt and tier latency for every (p, d), the
+// load term and feasibility limit for every d.  Reads the current snapshot
+// (congestion, in-flight counters, queue, batch, free memory).
+__global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict__ pcon, float *__restrict__ dbase,
+                                                     uint64_t *__restrict__ dxlim) {
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t npd = (uint64_t)s.P * s.D;
+    if (i < npd) {
+        const uint32_t p = (uint32_t)(i / s.D);
+        const uint32_t tau = s.tier_map[i] & 3u;
+        pcon[i] = make_float2(sec_per_token(s, tau, p, s.util[i]), s.lat[tau]);
+    }
+    if (i < s.D) {
+        dbase[i] = load_term(s, (uint32_t)i);
+        dxlim[i] = feasible_limit(s, s.free_mem[i]);
+    }
+}
+
 // ---------------------------------------------------------------- batch order
 //
 // Requests are scored in an order that groups equal leading blocks: the sort
@@ -207,14 +241,17 @@ constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
 
 // One sorted request, everything the scan needs without indirection.
-struct alignas(32) Rec {
+struct alignas(16) Rec {
     uint32_t r;      // request index in the caller's batch
     uint32_t p;      // prefill instance
     uint32_t len;    // input tokens
     uint32_t n;      // hashed blocks
     uint32_t lcp;    // leading blocks in common with the previous sorted request
-    uint32_t pad;
+    uint32_t b1;     // first candidate bucket of hf
     uint64_t a;      // offset of the hash run
+    uint64_t hf;     // hash of block lcp (the first one a carried scan tests), 0 if lcp == n
+    uint32_t b2;     // second candidate bucket of hf
+    uint32_t pad;
 };
 
 struct Order {
@@ -276,7 +313,8 @@ __global__ void count_valid_kernel(const uint32_t *__restrict__ sorted_keys, uin
 // Record of each sorted request, with its common leading blocks with the
 // previous sorted request.
 __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
-                                                  const uint32_t *__restrict__ n_valid, Rec *__restrict__ rec) {
+                                                  const uint32_t *__restrict__ n_valid, uint32_t shift,
+                                                  Rec *__restrict__ rec) {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= *n_valid) return;
     const uint32_t r = perm[i];
@@ -296,8 +334,10 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__res
     x.len = rq.len[r];
     x.n = (uint32_t)nr;
     x.lcp = l;
-    x.pad = 0;
     x.a = a;
+    x.hf = l < nr ? rq.hashes[a + l] : 0;
+    buckets_of(x.hf, shift, x.b1, x.b2);
+    x.pad = 0;
     rec[i] = x;
 }
 
@@ -320,59 +360,51 @@ __device__ inline Rec load_rec(const Rec *base, uint32_t i) {
     x.len = w[2];
     x.n = w[3];
     x.lcp = w[4];
-    x.pad = 0;
+    x.b1 = w[5];
     x.a = ((uint64_t)w[7] << 32) | (uint64_t)w[6];
+    x.hf = ((uint64_t)w[9] << 32) | (uint64_t)w[8];
+    x.b2 = w[10];
+    x.pad = 0;
     return x;
 }
 
-// Resolve one membership test on the C columns of a lane: key[q] is column
-// q's value at the home slot of h; colliding slots are followed by linear
-// probing (the slot sequence is the same for every lane and column, so
-// continuation rows stay coalesced).  Columns not alive stay dead.
+// A membership test of one hash on the C columns of a lane, from the two
+// candidate buckets loaded beforehand (v1, v2).
 template <int C>
-__device__ inline void member(const uint64_t *const (&col)[C], const Table &t, uint64_t h, uint64_t home,
-                              const uint64_t (&key)[C], bool (&alive)[C]) {
-    bool pend[C];
-    bool any = false;
+__device__ inline void member(uint64_t h, const ulonglong2 (&v1)[C], const ulonglong2 (&v2)[C], bool (&alive)[C]) {
+#pragma unroll
+    for (int q = 0; q < C; ++q)
+        alive[q] = alive[q] && (v1[q].x == h || v1[q].y == h || v2[q].x == h || v2[q].y == h);
+}
+
+template <int C>
+__device__ inline void load_buckets(const uint64_t *const (&col)[C], const Table &t, uint32_t b1, uint32_t b2,
+                                    bool go, ulonglong2 (&v1)[C], ulonglong2 (&v2)[C]) {
 #pragma unroll
     for (int q = 0; q < C; ++q) {
-        pend[q] = alive[q] && key[q] != h && key[q] != 0;
-        alive[q] = alive[q] && key[q] == h;
-        any = any || pend[q];
-    }
-    if (!__any(any)) return;
-#pragma unroll
-    for (int q = 0; q < C; ++q) {
-        uint64_t s2 = home;
-        while (__any(pend[q])) {
-            s2 = (s2 + 1) & t.mask;
-            if (pend[q]) {
-                const uint64_t k2 = col[q][s2 * t.pitch];
-                if (k2 == h) {
-                    alive[q] = true;
-                    pend[q] = false;
-                } else if (k2 == 0) {
-                    pend[q] = false;
-                }
-            }
+        v1[q] = make_ulonglong2(0, 0);
+        v2[q] = make_ulonglong2(0, 0);
+        if (go) {
+            v1[q] = *(const ulonglong2 *)(col[q] + (uint64_t)b1 * t.pitch * 2);
+            v2[q] = *(const ulonglong2 *)(col[q] + (uint64_t)b2 * t.pitch * 2);
         }
     }
 }
 
 // First-miss scan of one request's run on the C columns of every lane of a
 // wavefront, for the columns in need[], starting at block `start` (uniform,
-// < n) whose hash h0 and home-slot values key0[] were loaded beforehand.
-// Past the first block, W home-slot loads per column are issued together per
-// step.  j[] holds, for the columns in need, `start` on entry and the
-// first-miss index on return; other columns are left alone.
+// < n) whose hash h0 and candidate buckets (v1_0, v2_0) were loaded
+// beforehand.  Past the first block, W blocks are tested per step with all
+// their bucket loads issued together.  j[] holds, for the columns in need,
+// `start` on entry and the first-miss index on return.
 template <int W, int C>
 __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &t, cptr<uint64_t> run, uint32_t n,
                                   uint32_t start, const bool (&need)[C], uint32_t (&j)[C], uint64_t h0,
-                                  const uint64_t (&key0)[C]) {
+                                  const ulonglong2 (&v1_0)[C], const ulonglong2 (&v2_0)[C]) {
     bool alive[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) alive[q] = need[q];
-    member<C>(col, t, h0, home_slot(h0, t.shift), key0, alive);
+    member<C>(h0, v1_0, v2_0, alive);
 #pragma unroll
     for (int q = 0; q < C; ++q) j[q] += alive[q] ? 1u : 0u;
     for (uint32_t i0 = start + 1; i0 < n; i0 += W) {
@@ -380,8 +412,7 @@ __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &
 #pragma unroll
         for (int q = 0; q < C; ++q) any = any || alive[q];
         if (!__any(any)) break;
-        uint64_t h[W], sl[W];
-        uint64_t key[W][C];
+        uint64_t h[W];
         if (i0 + W <= n) {
 #pragma unroll
             for (int w = 0; w < W; ++w) h[w] = run[i0 + w];
@@ -389,19 +420,25 @@ __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &
 #pragma unroll
             for (int w = 0; w < W; ++w) h[w] = i0 + w < n ? run[i0 + w] : 0;
         }
+        ulonglong2 v1[W][C], v2[W][C];
 #pragma unroll
         for (int w = 0; w < W; ++w) {
-            sl[w] = home_slot(h[w], t.shift);
+            uint32_t b1, b2;
+            buckets_of(h[w], t.shift, b1, b2);
 #pragma unroll
             for (int q = 0; q < C; ++q) {
-                key[w][q] = 0;
-                if (alive[q] && i0 + w < n) key[w][q] = col[q][sl[w] * t.pitch];
+                v1[w][q] = make_ulonglong2(0, 0);
+                v2[w][q] = make_ulonglong2(0, 0);
+                if (alive[q] && i0 + w < n) {
+                    v1[w][q] = *(const ulonglong2 *)(col[q] + (uint64_t)b1 * t.pitch * 2);
+                    v2[w][q] = *(const ulonglong2 *)(col[q] + (uint64_t)b2 * t.pitch * 2);
+                }
             }
         }
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             if (i0 + w >= n) break;
-            member<C>(col, t, h[w], sl[w], key[w], alive);
+            member<C>(h[w], v1[w], v2[w], alive);
 #pragma unroll
             for (int q = 0; q < C; ++q) j[q] += alive[q] ? 1u : 0u;
         }
@@ -434,52 +471,46 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
     uint32_t d[C];
     bool act[C];
     const uint64_t *col[C];
-    float load[C];
-    uint64_t mem[C];
+    float dload[C];
+    uint64_t xlim[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
         act[q] = d[q] < s.D;
-        col[q] = t.keys + (act[q] ? d[q] : 0);
-        load[q] = act[q] ? load_term(s, d[q]) : 0.0f;
-        mem[q] = act[q] ? s.free_mem[d[q]] : 0;
+        col[q] = t.keys + 2 * (uint64_t)(act[q] ? d[q] : 0);
+        dload[q] = act[q] ? s.dbase[d[q]] : 0.0f;
+        xlim[q] = act[q] ? s.dxlim[d[q]] : 0;
     }
     const cptr<uint64_t> chash = as_const(hashes);
     Rec c0 = load_rec(rec, i0);
     Rec c1 = load_rec(rec, i0 + 1 < i1 ? i0 + 1 : i0);
-    uint8_t tau0[C];
-    float u0[C];
+    float2 pc0[C];
 #pragma unroll
-    for (int q = 0; q < C; ++q) {
-        const uint64_t o = (uint64_t)c0.p * s.D + (act[q] ? d[q] : 0);
-        tau0[q] = s.tier_map[o];
-        u0[q] = s.util[o];
-    }
+    for (int q = 0; q < C; ++q) pc0[q] = s.pcon[(uint64_t)c0.p * s.D + (act[q] ? d[q] : 0)];
     // first membership test of the current request (block L0), loaded ahead
     uint32_t L0 = 0;
     uint64_t h0 = c0.n ? chash[c0.a] : 0;
-    uint64_t k0[C];
-#pragma unroll
-    for (int q = 0; q < C; ++q) k0[q] = (act[q] && c0.n) ? col[q][home_slot(h0, t.shift) * t.pitch] : 0;
+    ulonglong2 v10[C], v20[C];
+    {
+        uint32_t b1, b2;
+        buckets_of(h0, t.shift, b1, b2);
+        load_buckets<C>(col, t, b1, b2, c0.n != 0, v10, v20);
+    }
     uint32_t j_prev[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) j_prev[q] = 0;
     for (uint32_t i = i0; i < i1; ++i) {
         const Rec c2 = load_rec(rec, i + 2 < i1 ? i + 2 : i1 - 1);
-        uint8_t tau1[C];
-        float u1[C];
+        float2 pc1[C];
 #pragma unroll
-        for (int q = 0; q < C; ++q) {
-            const uint64_t o = (uint64_t)c1.p * s.D + (act[q] ? d[q] : 0);
-            tau1[q] = s.tier_map[o];
-            u1[q] = s.util[o];
-        }
+        for (int q = 0; q < C; ++q) pc1[q] = s.pcon[(uint64_t)c1.p * s.D + (act[q] ? d[q] : 0)];
         const uint32_t L1 = reuse ? c1.lcp : 0u;
         const bool more = i + 1 < i1 && L1 < c1.n;
-        const uint64_t h1 = more ? chash[c1.a + L1] : 0;
-        uint64_t k1[C];
-#pragma unroll
-        for (int q = 0; q < C; ++q) k1[q] = (act[q] && more) ? col[q][home_slot(h1, t.shift) * t.pitch] : 0;
+        const uint64_t h1 = !more ? 0 : reuse ? c1.hf : chash[c1.a];
+        uint32_t b11 = c1.b1, b21 = c1.b2;
+        if (!reuse) buckets_of(h1, t.shift, b11, b21);
+        ulonglong2 v11[C], v21[C];
+        load_buckets<C>(col, t, b11, b21, more, v11, v21);
         // prefix lengths: carried where the common leading run decides them
         uint32_t j[C];
         bool need[C];
@@ -489,21 +520,23 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             j[q] = carry ? j_prev[q] : L0;
             need[q] = act[q] && !carry;
         }
-        if (L0 < c0.n) probe_from<W, C>(col, t, chash + c0.a, c0.n, L0, need, j, h0, k0);
-        // Eq. (2) in integer form, feasibility and the cost of Eqs. (3)-(7)
+        if (L0 < c0.n) probe_from<W, C>(col, t, chash + c0.a, c0.n, L0, need, j, h0, v10, v20);
+        // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t cb[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) {
             j_prev[q] = j[q];
-            const PairCost pc = pair_cost(s, c0.p, mem[q], c0.len, j[q], tau0[q], u0[q], load[q]);
+            const uint32_t x = c0.len - s.block_tokens * j[q];
+            const bool feas = (uint64_t)x < xlim[q];
+            const float cost = pair_score(x, pc0[q].x, pc0[q].y, dload[q]);
             if (PAIRS && act[q]) {
                 const uint64_t o = (uint64_t)c0.r * s.D + d[q];
                 if (po.j) po.j[o] = (uint16_t)j[q];
-                if (po.feas) po.feas[o] = pc.feas ? 1 : 0;
-                if (po.score) po.score[o] = pc.cost;
+                if (po.feas) po.feas[o] = feas ? 1 : 0;
+                if (po.score) po.score[o] = cost;
                 if (po.jT) po.jT[(uint64_t)d[q] * n_req + c0.r] = (uint16_t)j[q];
             }
-            cb[q] = (act[q] && pc.feas) ? __float_as_uint(pc.cost) : 0xFFFFFFFFu;
+            cb[q] = (act[q] && feas) ? __float_as_uint(cost) : 0xFFFFFFFFu;
         }
         // the group's K best: least cost bits, then least decode index
         uint64_t mine = kEmptyKey;
@@ -529,9 +562,9 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         c1 = c2;
 #pragma unroll
         for (int q = 0; q < C; ++q) {
-            tau0[q] = tau1[q];
-            u0[q] = u1[q];
-            k0[q] = k1[q];
+            pc0[q] = pc1[q];
+            v10[q] = v11[q];
+            v20[q] = v21[q];
         }
         L0 = L1;
         h0 = h1;
@@ -606,9 +639,12 @@ __global__ __launch_bounds__(256) void sweep_kernel(Snap s, Reqs rq, const float
             for (int i = 0; i < K; ++i) best[i] = kEmptyKey;
             for (uint32_t d = 0; d < s.D; ++d) {
                 uint32_t j = jT[(uint64_t)d * rq.n_req + r];
-                PairCost pc = pair_cost(s, p, s.free_mem[d], len, j, s.tier_map[(uint64_t)p * s.D + d], u[d],
-                                        load_term(s, d));
-                if (pc.feas) topk_insert<K>(best, pack_key(pc.cost, d));
+                const uint32_t tau = s.tier_map[(uint64_t)p * s.D + d] & 3u;
+                const uint32_t x = len - s.block_tokens * j;
+                if ((uint64_t)x < s.dxlim[d]) {
+                    const float cost = pair_score(x, sec_per_token(s, tau, p, u[d]), s.lat[tau], s.dbase[d]);
+                    topk_insert<K>(best, pack_key(cost, d));
+                }
             }
             for (uint32_t i = 0; i < k; ++i) {
                 uint64_t m = i < (uint32_t)K ? best[i] : kEmptyKey;
@@ -642,27 +678,54 @@ __global__ void count_zero_kernel(const uint64_t *__restrict__ h, uint64_t n, ui
     if (__any(z) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrZeroHash);
 }
 
-// Tiles of one decode's hash list: tile_dec[b], tile_beg[b], tile_end[b].
-__global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys, uint64_t mask, uint32_t shift,
-                                                     uint32_t pitch, const uint64_t *__restrict__ h,
+// Cuckoo insertion of one decode's hashes (tiles: tile_dec[b], tile_beg[b],
+// tile_end[b]).  A key goes to an empty slot of either candidate bucket
+// (compare-and-swap 0 -> key); when all four slots are taken it displaces a
+// slot's key by atomic exchange and carries the displaced key on, to its
+// other bucket.  A key is always either in the table or carried by exactly
+// one thread, so none is lost.  A repeated hash (already in a slot) stops.
+constexpr uint32_t kMaxKicks = 512;
+
+__device__ inline bool try_place(unsigned long long *bk, uint64_t key) {
+    for (int slot = 0; slot < 2; ++slot) {
+        const unsigned long long prev = atomicCAS(bk + slot, 0ull, (unsigned long long)key);
+        if (prev == 0ull || prev == key) return true;
+    }
+    return false;
+}
+
+__global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys, uint32_t shift, uint32_t pitch,
+                                                     const uint64_t *__restrict__ h,
                                                      const uint32_t *__restrict__ tile_dec,
                                                      const uint64_t *__restrict__ tile_beg,
                                                      const uint64_t *__restrict__ tile_end,
                                                      uint32_t *__restrict__ err) {
     const uint32_t d = tile_dec[blockIdx.x];
     const uint64_t beg = tile_beg[blockIdx.x], end = tile_end[blockIdx.x];
+    unsigned long long *col = (unsigned long long *)keys + 2 * (uint64_t)d;
     for (uint64_t i = beg + threadIdx.x; i < end; i += blockDim.x) {
         uint64_t key = h[i];
-        uint64_t sl = home_slot(key, shift);
+        uint32_t from = 0xFFFFFFFFu;   // bucket the carried key was displaced from
         bool done = false;
-        for (uint64_t step = 0; step <= mask; ++step) {
-            unsigned long long prev =
-                atomicCAS((unsigned long long *)(keys + sl * pitch + d), 0ull, (unsigned long long)key);
-            if (prev == 0ull || prev == key) {
+        for (uint32_t kick = 0; kick < kMaxKicks && !done; ++kick) {
+            uint32_t b1, b2;
+            buckets_of(key, shift, b1, b2);
+            unsigned long long *k1 = col + (uint64_t)b1 * pitch * 2;
+            unsigned long long *k2 = col + (uint64_t)b2 * pitch * 2;
+            if (try_place(k1, key) || try_place(k2, key)) {
                 done = true;
                 break;
             }
-            sl = (sl + 1) & mask;
+            // displace from the bucket the key did not just leave
+            const uint32_t b = (b1 == from) ? b2 : (b2 == from) ? b1 : ((kick & 1) ? b2 : b1);
+            unsigned long long *bk = col + (uint64_t)b * pitch * 2;
+            const unsigned long long old = atomicExch(bk + ((kick >> 1) & 1), (unsigned long long)key);
+            if (old == 0ull || old == key) {
+                done = true;
+                break;
+            }
+            key = old;
+            from = b;
         }
         if (!done) atomicOr(err, kErrTableFull);
     }
@@ -701,24 +764,16 @@ __global__ void check_snapshot_kernel(const uint8_t *__restrict__ tier, const fl
 
 // ------------------------------------------------------------------ between-batch update
 
-// Probe one (hash run, decode) pair by itself (one thread).
+// First-miss scan of one (hash run, decode) pair by one thread.
 __device__ inline uint32_t prefix_match_one(const Table &t, uint32_t d, const uint64_t *__restrict__ run,
                                             uint32_t n) {
+    const uint64_t *col = t.keys + 2 * (uint64_t)d;
     uint32_t j = 0;
     for (; j < n; ++j) {
-        uint64_t h = run[j];
-        uint64_t sl = home_slot(h, t.shift);
-        bool hit = false;
-        for (uint64_t step = 0; step <= t.mask; ++step) {
-            uint64_t key = t.keys[sl * t.pitch + d];
-            if (key == h) {
-                hit = true;
-                break;
-            }
-            if (key == 0) break;
-            sl = (sl + 1) & t.mask;
-        }
-        if (!hit || h == 0) break;
+        const uint64_t h = run[j];
+        uint32_t b1, b2;
+        buckets_of(h, t.shift, b1, b2);
+        if (h == 0 || !(bucket_has(col, t, b1, h) || bucket_has(col, t, b2, h))) break;
     }
     return j;
 }
@@ -782,6 +837,9 @@ struct netkv_ctx {
     uint32_t *queue = nullptr;
     uint32_t *batch = nullptr;
     uint64_t *adm_prev = nullptr;
+    float2 *pcon = nullptr;      // derived per call: [P*D]
+    float *dbase = nullptr;      // [D]
+    uint64_t *dxlim = nullptr;   // [D]
     float bw[4] = {0, 0, 0, 0}, lat[4] = {0, 0, 0, 0};
     float t_a = 0, t_b = 0, alpha = 0;
     uint32_t beta_max = 0, bpt = 0, block_tokens = 1;
@@ -790,8 +848,8 @@ struct netkv_ctx {
     bool have_cache = false;
     uint32_t cache_D = 0;
     uint64_t *table = nullptr;
-    uint64_t table_bytes = 0, cap = 0;
-    uint32_t log2cap = 0, pitch = 0;
+    uint64_t table_bytes = 0, buckets = 0;
+    uint32_t log2b = 0, pitch = 0;
     // scratch
     uint32_t *errword = nullptr;          // request / selection errors (sticky)
     uint32_t *loadword = nullptr;         // validation flags of the load calls
@@ -815,6 +873,7 @@ struct netkv_ctx {
     // options
     uint32_t run_len_opt = 0;   // 0 = automatic
     uint32_t reuse_opt = 1;     // carry first-miss indices along sorted runs
+    uint32_t cols_opt = 0;      // decodes per lane (0 = automatic)
     // timing
     bool timing = false;
     bool timed = false;
@@ -896,14 +955,16 @@ Snap make_snap(netkv_handle h) {
     s.block_tokens = h->block_tokens;
     s.P = h->P;
     s.D = h->D;
+    s.pcon = h->pcon;
+    s.dbase = h->dbase;
+    s.dxlim = h->dxlim;
     return s;
 }
 
 Table make_table(netkv_handle h) {
     Table t;
     t.keys = h->table;
-    t.mask = h->cap - 1;
-    t.shift = 32 - h->log2cap;
+    t.shift = 32 - h->log2b;
     t.pitch = h->pitch;
     return t;
 }
@@ -978,14 +1039,17 @@ uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
     return (uint32_t)rl;
 }
 
-// decodes per lane: 4 when there are many decodes, else 1
-inline uint32_t cols_per_lane(uint32_t D) { return D >= 8u * kWave ? 4u : 1u; }
+// decodes per lane: 4 when there are many decodes, else 1 (or the option)
+inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
+    if (opt == 1 || opt == 2 || opt == 4) return opt;
+    return D >= 8u * kWave ? 4u : 1u;
+}
 
 template <int K, int C>
 void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
                  uint32_t n_runs, uint32_t ngroup, uint32_t reuse, uint64_t *partial, const PairOut &po, bool pairs,
                  hipStream_t st) {
-    constexpr int W = C >= 4 ? 2 : kSpec;
+    constexpr int W = C >= 4 ? 2 : C == 2 ? 2 : kSpec;
     const uint64_t waves = (uint64_t)n_runs * ngroup;
     const uint32_t grid = (uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (pairs)
@@ -1006,6 +1070,8 @@ hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, co
     if (h->timing && (e = hipEventRecord(h->ev0, st)) != hipSuccess) return e;
     if (C == 4)
         launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+    else if (C == 2)
+        launch_scan<K, 2>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
     else
         launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1024,13 +1090,16 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
                         const PairOut &po, bool pairs, hipStream_t st) {
     const uint64_t R = req->n_req;
     const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
-    const uint32_t C = cols_per_lane(h->D);
+    const uint32_t C = cols_per_lane(h->D, h->cols_opt);
     const uint32_t ngroup = (h->D + kWave * C - 1) / (kWave * C);
     netkv_status e = ensure_order_scratch(h, R, R * ngroup * K, st);
     if (e) return e;
     const Snap sn = make_snap(h);
     const Table t = make_table(h);
     const Reqs rq = make_reqs(req);
+    const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
+    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->pcon, h->dbase,
+                       h->dxlim);
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 16 * kWavesPerBlock - 1) / (16 * kWavesPerBlock))),
                        dim3(kBlock), 0, st, sn, rq, h->keys_in, h->vals_in, h->errword);
     HIPCHK(h, hipGetLastError());
@@ -1040,7 +1109,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(64), 0, st, (const uint32_t *)h->keys_out, (uint32_t)R,
                        h->n_valid);
     hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->n_valid, h->rec);
+                       (const uint32_t *)h->n_valid, t.shift, h->rec);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
@@ -1098,6 +1167,9 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->queue);
         dfree(h->batch);
         dfree(h->adm_prev);
+        dfree(h->pcon);
+        dfree(h->dbase);
+        dfree(h->dxlim);
         dfree(h->table);
         dfree(h->errword);
         dfree(h->loadword);
@@ -1181,6 +1253,15 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
         return fail(h, NETKV_EINVAL, "invalid snapshot:%s%s%s", (bad & 1) ? " tier_map value > 3" : "",
                     (bad & 2) ? " util outside [0,1) or NaN" : "", (bad & 4) ? " batch_size > beta_max" : "");
     }
+    if (!h->have_snap || h->P != P || h->D != D) {
+        dfree(h->pcon); dfree(h->dbase); dfree(h->dxlim);
+        h->have_snap = false;
+        if (dalloc(h->pcon, npd) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
+            dalloc(h->dxlim, D) != hipSuccess) {
+            cleanup();
+            return fail(h, NETKV_ENOMEM, "snapshot allocation failed");
+        }
+    }
     dfree(h->tier_map); dfree(h->util); dfree(h->n_inflight); dfree(h->free_mem);
     dfree(h->adm_prev); dfree(h->queue); dfree(h->batch);
     h->tier_map = tm; h->util = ut; h->n_inflight = ni; h->free_mem = fm;
@@ -1253,13 +1334,17 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
         maxn = std::max(maxn, off[d + 1] - off[d]);
     }
     if (off[n_decode] > n_hashes) return fail(h, NETKV_EINVAL, "hash_off[n_decode] exceeds n_hashes");
-    uint64_t need = (uint64_t)std::ceil((double)maxn / (double)max_load_factor);
-    uint32_t log2cap = 4;
-    while ((1ull << log2cap) < need || (1ull << log2cap) <= maxn) {
-        ++log2cap;
-        if (log2cap > 31) return fail(h, NETKV_ECAPACITY, "a table would need more than 2^31 slots");
+    // two slots per bucket; cuckoo tables with two 2-slot buckets per key stay
+    // buildable well above load factor 0.5, and are capped at 0.85
+    const double lf = std::min(0.85, (double)max_load_factor);
+    const uint64_t need = (uint64_t)std::ceil((double)maxn / (2.0 * lf));
+    uint32_t log2b = 3;
+    while ((1ull << log2b) < need) {
+        ++log2b;
+        if (log2b > 30) return fail(h, NETKV_ECAPACITY, "a table would need more than 2^31 slots");
     }
-    const uint64_t cap = 1ull << log2cap;
+    const uint64_t nbk = 1ull << log2b;
+    const uint64_t cap = 2 * nbk;
     const uint32_t pitch = (n_decode + 15u) & ~15u;
     const uint64_t tbytes = cap * pitch * 8ull;
     // tiles of at most 4096 hashes, each within one decode
@@ -1314,8 +1399,8 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     }
     e = hipMemsetAsync(tab, 0, tbytes, st);
     if (e == hipSuccess && !tdec.empty()) {
-        hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, cap - 1,
-                           32u - log2cap, pitch, (const uint64_t *)dh, (const uint32_t *)ddec,
+        hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, 32u - log2b, pitch,
+                           (const uint64_t *)dh, (const uint32_t *)ddec,
                            (const uint64_t *)dbeg, (const uint64_t *)dend, h->loadword);
         e = hipGetLastError();
     }
@@ -1325,11 +1410,11 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     if (e != hipSuccess || bad) {
         dfree(tab);
         return e != hipSuccess ? fail(h, NETKV_EDEVICE, "table build failed: %s", hipGetErrorString(e))
-                               : fail(h, NETKV_ECAPACITY, "table build ran out of slots");
+                               : fail(h, NETKV_ECAPACITY, "table build could not place every hash");
     }
     h->table = tab;
-    h->cap = cap;
-    h->log2cap = log2cap;
+    h->buckets = nbk;
+    h->log2b = log2b;
     h->pitch = pitch;
     h->table_bytes = tbytes;
     h->cache_D = n_decode;
@@ -1522,6 +1607,11 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
     case NETKV_OPT_REUSE:
         h->reuse_opt = value ? 1u : 0u;
         return NETKV_OK;
+    case NETKV_OPT_COLS:
+        if (value != 0 && value != 1 && value != 2 && value != 4)
+            return fail(h, NETKV_EINVAL, "decodes per lane must be 0 (automatic), 1, 2 or 4");
+        h->cols_opt = value;
+        return NETKV_OK;
     default:
         return fail(h, NETKV_EINVAL, "unknown option %d", option);
     }
@@ -1530,7 +1620,7 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
 netkv_status netkv_cache_info(netkv_handle h, uint64_t *slots_per_decode, uint64_t *table_bytes) {
     if (!h) return NETKV_EINVAL;
     if (!h->have_cache) return fail(h, NETKV_ENOTREADY, "no cache loaded");
-    if (slots_per_decode) *slots_per_decode = h->cap;
+    if (slots_per_decode) *slots_per_decode = 2 * h->buckets;
     if (table_bytes) *table_bytes = h->table_bytes;
     return NETKV_OK;
 }

@@ -82,6 +82,7 @@ _SIGS = {
 
 NETKV_OPT_RUN_LEN = 1
 NETKV_OPT_REUSE = 2
+NETKV_OPT_COLS = 3
 
 
 def load_library(path: str = LIB_PATH):

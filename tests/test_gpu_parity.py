@@ -112,8 +112,9 @@ def test_ragged_decodes_long_runs_and_empty_runs(nk):
 
 
 @pytest.mark.parametrize("lf", [0.9, 0.99])
-def test_dense_tables_long_probe_chains(nk, lf):
-    """Nearly full tables: long linear-probe chains that wrap the table end."""
+def test_dense_tables(nk, lf):
+    """Dense tables (load factor capped at 0.85, rounded to a power of two):
+    many displacements while building; membership must be unaffected."""
     _say("dense tables lf", lf)
     cfg = W.scaled(W.CONFIGS["c0"], n_requests=1500, cache_per_decode=3000)
     snap, req, cache = _inputs(cfg, 7)
