@@ -1032,10 +1032,12 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
 }
 
 uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
-    // about 64K wavefronts in flight; runs of 8..1024 sorted requests
-    uint64_t rl = (R * ngroup) / 65536;
+    // about 32K wavefronts; runs of 8..512 sorted requests (measured on MI355X:
+    // longer runs carry more first-miss indices, shorter ones keep more
+    // wavefronts in flight)
+    uint64_t rl = (R * ngroup) / 32768;
     if (rl < 8) rl = 8;
-    if (rl > 1024) rl = 1024;
+    if (rl > 512) rl = 512;
     return (uint32_t)rl;
 }
 
