@@ -175,6 +175,27 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
 netkv_status netkv_commit_batch(netkv_handle h, const netkv_requests_t *req, const int32_t *sel,
                                 uint32_t cap, uint32_t mu, void *stream);
 
+/* Selections per tier (Sec. VII, the tier-shift statistic): counts[t] for
+ * t = 0..3 = requests whose selected decode sel[r] (DEVICE, -1 = rejected)
+ * lies on tier t from the request's prefill instance, counts[4] = rejected
+ * requests.  counts: DEVICE u64[5], overwritten.  Asynchronous.  An index
+ * >= D is not counted and is reported by netkv_sync_errors. */
+netkv_status netkv_tier_counts(netkv_handle h, const netkv_requests_t *req, const int32_t *sel,
+                               uint64_t *counts, void *stream);
+
+/* Algorithm 1 applied request after request in batch order (Sec. V-A,
+ * V-C): each request is scored with the in-flight counters as left by the
+ * earlier requests of the batch from the same prefill instance, and its
+ * selection increments n_inflight[tau(p, d*)][p] unless the counter has
+ * reached `cap` (Sec. V-C default 16).  Requests of different prefill
+ * instances do not interact.  Writes the argmin (index, score) per request
+ * to out_idx / out_score ([n_req] DEVICE); invalid requests get -1 / NaN.
+ * The handle's between-batch state is not changed (netkv_commit_batch
+ * applies the batch).  Asynchronous; grows an internal buffer of
+ * n_req * n_decode * 2 bytes (per-pair prefix lengths) on first use. */
+netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req, uint32_t cap,
+                                     int32_t *out_idx, float *out_score, void *stream);
+
 /* Copy the between-batch state into caller arrays (host or device; any may
  * be NULL): n_inflight [4*P], queue_depth [D], free_mem [D],
  * admitted_prev [D].  Synchronous. */
@@ -203,8 +224,14 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
  *                        leading blocks (an exact identity, no probe);
  *                        0: every pair is scanned from block 0;
  *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
- *                        automatic (4 on pools of 512+ decodes, else 1), 1, 2, 4. */
-enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3 };
+ *                        automatic (4 on pools of 512+ decodes, else 1), 1, 2, 4.
+ * and one option that does change results, selecting the rung of the
+ * method's ablation (Sec. VI, Experiment 6) the costs use:
+ *   NETKV_OPT_POLICY  -- 0 (default): the full cost; 1: static tier map and
+ *                        self-contention counter, live congestion taken as 0;
+ *                        2: static tier map only (congestion and in-flight
+ *                        counters taken as 0). */
+enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3, NETKV_OPT_POLICY = 4 };
 netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 
 /* Table geometry of the loaded cache: slots per decode (a power of two)

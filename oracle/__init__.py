@@ -68,6 +68,9 @@ def _load():
         lib.orc_commit.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p,
                                    C.c_void_p, C.c_void_p]
+        lib.orc_select_sequential.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32,
+                                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        lib.orc_tier_counts.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         lib.orc_prefix_len.restype = C.c_uint32
         lib.orc_prefix_len.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint32]
         lib.orc_max_threads.restype = C.c_int
@@ -208,3 +211,37 @@ def commit(snap, cache, req, sel: np.ndarray, cap: int, mu: int, state: Dict[str
                    st["n_inflight"].ctypes.data, st["queue_depth"].ctypes.data,
                    st["free_mem"].ctypes.data, st["admitted_prev"].ctypes.data)
     return st
+
+
+def select_sequential(snap, cache, req, cap: int = 16, follow: Optional[np.ndarray] = None):
+    """Algorithm 1 request by request in batch order (in-flight counters
+    incremented after each selection).  Returns dict(idx [R], score [R],
+    and with `follow`: follow_cost [R])."""
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    c = cache if isinstance(cache, Cache) else Cache(cache)
+    q = req if isinstance(req, Requests) else Requests(req)
+    R = q.n_req
+    idx = np.empty(R, dtype=np.int32)
+    score = np.empty(R, dtype=np.float64)
+    fc = None
+    f = None
+    if follow is not None:
+        f = _arr(follow, np.int32)
+        fc = np.empty(R, dtype=np.float64)
+    lib.orc_select_sequential(C.byref(s.s), c.h, C.byref(q.r), int(cap), _ptr(f), idx.ctypes.data,
+                              score.ctypes.data, _ptr(fc))
+    out = dict(idx=idx, score=score)
+    if fc is not None:
+        out["follow_cost"] = fc
+    return out
+
+
+def tier_counts(snap, req, sel: np.ndarray) -> np.ndarray:
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    q = req if isinstance(req, Requests) else Requests(req)
+    sel = _arr(sel, np.int32)
+    out = np.empty(5, dtype=np.uint64)
+    lib.orc_tier_counts(C.byref(s.s), C.byref(q.r), sel.ctypes.data, out.ctypes.data)
+    return out

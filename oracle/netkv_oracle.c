@@ -354,6 +354,56 @@ void orc_commit(const orc_snapshot *s, const orc_cache *c, const orc_requests *q
     free(bytes);
 }
 
+/* Algorithm 1 request by request, in batch order: each request is scored
+ * with the in-flight counters left by the earlier requests (Algorithm 1
+ * increments n_inflight[tau(p, d*)][p] after every selection; Sec. V-C caps
+ * the counter, read here as a saturating increment: n < cap ? n + 1 : n).
+ * out_idx/out_score receive each request's argmin.  If `follow` is not NULL
+ * the counters advance with follow[r] instead of the oracle's own choice
+ * (so a comparison can continue from another implementation's choices), and
+ * follow_cost[r] receives the cost of follow[r] under the same counters
+ * (+inf for -1, NaN when follow[r] is not a feasible decode). */
+void orc_select_sequential(const orc_snapshot *s, const orc_cache *c, const orc_requests *q, uint32_t cap,
+                           const int32_t *follow, int32_t *out_idx, double *out_score, double *follow_cost) {
+    const uint32_t P = s->n_prefill, D = s->n_decode;
+    uint16_t *n = (uint16_t *)malloc(sizeof(uint16_t) * 4 * (size_t)P);
+    memcpy(n, s->n_inflight, sizeof(uint16_t) * 4 * (size_t)P);
+    cand *buf = (cand *)malloc(sizeof(cand) * (D ? D : 1));
+    uint8_t *feas = (uint8_t *)malloc(D ? D : 1);
+    double *cost = (double *)malloc(sizeof(double) * (D ? D : 1));
+    orc_snapshot sv = *s;
+    sv.n_inflight = n;
+    for (uint32_t r = 0; r < q->n_req; ++r) {
+        uint64_t tests = 0;
+        score_request(&sv, s->util, c, q, r, NULL, buf, 1, out_idx + r, out_score + r, NULL, feas, cost, &tests);
+        int32_t take = follow ? follow[r] : out_idx[r];
+        if (follow_cost) {
+            if (take < 0) follow_cost[r] = INFINITY;
+            else if ((uint32_t)take < D && feas[take]) follow_cost[r] = cost[take];
+            else follow_cost[r] = NAN;
+        }
+        if (take >= 0 && (uint32_t)take < D) {
+            uint32_t p = q->prefill[r];
+            int tau = s->tier_map[(uint64_t)p * D + (uint32_t)take];
+            uint16_t *cnt = &n[(uint64_t)tau * P + p];
+            if (*cnt < cap) *cnt += 1;
+        }
+    }
+    free(n);
+    free(buf);
+    free(feas);
+    free(cost);
+}
+
+/* Requests per tier of the selected decode; counts[4] = rejected. */
+void orc_tier_counts(const orc_snapshot *s, const orc_requests *q, const int32_t *sel, uint64_t *counts) {
+    for (int t = 0; t < 5; ++t) counts[t] = 0;
+    for (uint32_t r = 0; r < q->n_req; ++r) {
+        if (sel[r] < 0) counts[4] += 1;
+        else counts[s->tier_map[(uint64_t)q->prefill[r] * s->n_decode + (uint32_t)sel[r]]] += 1;
+    }
+}
+
 /* The first-miss prefix length of one hash run against one decode's set
  * (exposed for tests). */
 uint32_t orc_prefix_len(const orc_cache *c, uint32_t d, const uint64_t *h, uint32_t n) {

@@ -80,6 +80,7 @@ struct Snap {
     uint32_t bpt;
     uint32_t block_tokens;
     uint32_t P, D;
+    uint32_t policy;         // 0: full NetKV, 1: no live congestion, 2: neither congestion nor in-flight
     // derived once per call by derive_kernel (Eqs. (3)-(7) factored by (p, d) and d)
     const float2 *pcon;      // [P*D] {seconds per non-cached token, tier latency}
     const float *dbase;      // [D] alpha (T_queue + T_decode)
@@ -141,9 +142,17 @@ __device__ inline float load_term(const Snap &s, uint32_t d) {
 // (Eqs. (3)-(4)), so the pair contributes x * spt(p,d) + L_tau, and the decode
 // alpha (T_queue + T_decode); feasibility m_d >= bpt x + m_min holds iff
 // x < xlim_d = floor((m_d - m_min) / bpt) + 1 (integer, exact).
+// Seconds per non-cached token with an explicit in-flight count n.  The
+// ablation rungs of the method drop the live congestion (policy 1) or both
+// the congestion and the in-flight term (policy 2).
+__device__ inline float sec_per_token_n(const Snap &s, uint32_t tau, float n, float c) {
+    const float ce = s.policy >= 1 ? 0.0f : c;
+    const float ne = s.policy >= 2 ? 0.0f : n;
+    return ((float)s.bpt * (1.0f + ne)) / (s.bw[tau] * (1.0f - ce));
+}
+
 __device__ inline float sec_per_token(const Snap &s, uint32_t tau, uint32_t p, float c) {
-    const float n = (float)s.n_inflight[tau * s.P + p];
-    return ((float)s.bpt * (1.0f + n)) / (s.bw[tau] * (1.0f - c));
+    return sec_per_token_n(s, tau, (float)s.n_inflight[tau * s.P + p], c);
 }
 
 __device__ inline uint64_t feasible_limit(const Snap &s, uint64_t m) {
@@ -820,6 +829,125 @@ __global__ void commit_apply_kernel(uint32_t P, uint32_t D, uint32_t cap, uint32
     }
 }
 
+// ---------------------------------------------------------------- tier counts
+
+// Requests per tier of the selected decode (index 4: rejected), the tier
+// shift statistic.  Invalid selections are flagged and not counted.
+__global__ __launch_bounds__(256) void tier_count_kernel(Snap s, Reqs rq, const int32_t *__restrict__ sel,
+                                                         unsigned long long *__restrict__ counts,
+                                                         uint32_t *__restrict__ err) {
+    __shared__ uint32_t local[5];
+    if (threadIdx.x < 5) local[threadIdx.x] = 0;
+    __syncthreads();
+    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < rq.n_req) {
+        const int32_t d = sel[r];
+        const uint32_t p = rq.prefill[r];
+        if (d < 0) {
+            atomicAdd(&local[4], 1u);
+        } else if ((uint32_t)d < s.D && p < s.P) {
+            atomicAdd(&local[s.tier_map[(uint64_t)p * s.D + (uint32_t)d] & 3u], 1u);
+        } else {
+            atomicOr(err, kErrSelection);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < 5 && local[threadIdx.x]) atomicAdd(counts + threadIdx.x, (unsigned long long)local[threadIdx.x]);
+}
+
+// ---------------------------------------------------------------- sequential selection
+//
+// Algorithm 1 applied request after request in batch order: the in-flight
+// counter of the chosen tier grows by one (up to the cap) before the next
+// request from the same prefill instance is scored.  Requests of different
+// prefill instances do not interact, so each prefill instance's requests are
+// a sequential chain run by one workgroup, over prefix lengths computed
+// beforehand by the batch scan.
+
+// start/end of each prefill instance's run in the order sorted by prefill
+__global__ void segment_kernel(const uint32_t *__restrict__ keys, uint32_t n, uint32_t P, uint32_t *__restrict__ start,
+                               uint32_t *__restrict__ end) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint32_t k = keys[i];
+    if (k >= P) return;
+    if (i == 0 || keys[i - 1] != k) start[k] = i;
+    if (i + 1 == n || keys[i + 1] != k) end[k] = i + 1;
+}
+
+__global__ void prefill_key_kernel(Reqs rq, uint32_t P, const uint32_t *__restrict__ order_keys,
+                                   uint32_t *__restrict__ keys, uint32_t *__restrict__ vals) {
+    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rq.n_req) return;
+    keys[r] = order_keys[r] == kKeyInvalid ? P : rq.prefill[r];
+    vals[r] = r;
+}
+
+constexpr int kSeqThreads = 256;
+
+__global__ __launch_bounds__(kSeqThreads) void sequential_kernel(Snap s, uint32_t n_req, uint32_t cap,
+                                                                 const uint16_t *__restrict__ jm,
+                                                                 const uint32_t *__restrict__ len,
+                                                                 const uint32_t *__restrict__ order,
+                                                                 const uint32_t *__restrict__ start,
+                                                                 const uint32_t *__restrict__ end,
+                                                                 int32_t *__restrict__ out_idx,
+                                                                 float *__restrict__ out_score) {
+    __shared__ float n_tier[4];
+    __shared__ uint32_t best_cost[kSeqThreads / kWave];
+    __shared__ uint32_t best_d[kSeqThreads / kWave];
+    const uint32_t p = blockIdx.x;
+    const uint32_t i0 = start[p], i1 = end[p];
+    if (i0 >= i1) return;
+    const uint32_t lane = threadIdx.x % kWave, wave = wave_index();
+    if (threadIdx.x < 4) n_tier[threadIdx.x] = (float)s.n_inflight[threadIdx.x * s.P + p];
+    __syncthreads();
+    for (uint32_t i = i0; i < i1; ++i) {
+        const uint32_t r = order[i];
+        const uint32_t l = len[r];
+        uint32_t lb = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
+        for (uint32_t d = threadIdx.x; d < s.D; d += kSeqThreads) {
+            const uint32_t x = l - s.block_tokens * jm[(uint64_t)r * s.D + d];
+            if ((uint64_t)x < s.dxlim[d]) {
+                const uint64_t o = (uint64_t)p * s.D + d;
+                const uint32_t tau = s.tier_map[o] & 3u;
+                const float cost = pair_score(x, sec_per_token_n(s, tau, n_tier[tau], s.util[o]), s.lat[tau],
+                                              s.dbase[d]);
+                const uint32_t cbits = __float_as_uint(cost);
+                if (cbits < lb) {   // d grows within a thread: first strict minimum wins ties
+                    lb = cbits;
+                    ld = d;
+                }
+            }
+        }
+        const uint32_t mn = wave_min_u32_dpp(lb);
+        const uint32_t dm = wave_min_u32_dpp(lb == mn ? ld : 0xFFFFFFFFu);
+        if (lane == 0) {
+            best_cost[wave] = mn;
+            best_d[wave] = dm;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t bc = best_cost[0], bd = best_d[0];
+            for (int w = 1; w < kSeqThreads / kWave; ++w)
+                if (best_cost[w] < bc || (best_cost[w] == bc && best_d[w] < bd)) {
+                    bc = best_cost[w];
+                    bd = best_d[w];
+                }
+            if (bc == 0xFFFFFFFFu) {
+                out_idx[r] = -1;
+                out_score[r] = __builtin_inff();
+            } else {
+                out_idx[r] = (int32_t)bd;
+                out_score[r] = __uint_as_float(bc);
+                const uint32_t tau = s.tier_map[(uint64_t)p * s.D + bd] & 3u;
+                if (n_tier[tau] < (float)cap) n_tier[tau] += 1.0f;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 // ====================================================================== host side
@@ -874,6 +1002,14 @@ struct netkv_ctx {
     uint32_t run_len_opt = 0;   // 0 = automatic
     uint32_t reuse_opt = 1;     // carry first-miss indices along sorted runs
     uint32_t cols_opt = 0;      // decodes per lane (0 = automatic)
+    uint32_t policy_opt = 0;    // 0 full, 1 without live congestion, 2 topology only
+    // sequential-selection scratch
+    uint16_t *seq_j = nullptr;
+    uint64_t seq_j_cap = 0;
+    uint32_t *seq_keys = nullptr, *seq_vals = nullptr, *seq_keys_out = nullptr, *seq_perm = nullptr;
+    uint32_t *seq_start = nullptr, *seq_end = nullptr;
+    uint64_t seq_cap = 0;
+    uint32_t seq_P = 0;
     // timing
     bool timing = false;
     bool timed = false;
@@ -958,6 +1094,7 @@ Snap make_snap(netkv_handle h) {
     s.pcon = h->pcon;
     s.dbase = h->dbase;
     s.dxlim = h->dxlim;
+    s.policy = h->policy_opt;
     return s;
 }
 
@@ -1183,6 +1320,8 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->bytes);
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->rec);
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial);
+        dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
+        dfree(h->seq_start); dfree(h->seq_end);
         if (h->ev0) (void)hipEventDestroy(h->ev0);
         if (h->ev1) (void)hipEventDestroy(h->ev1);
     }
@@ -1598,6 +1737,86 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms) {
     return NETKV_OK;
 }
 
+netkv_status netkv_tier_counts(netkv_handle h, const netkv_requests_t *req, const int32_t *sel, uint64_t *counts,
+                               void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    netkv_status st = check_requests(h, req);
+    if (st) return st;
+    if (!counts || (req->n_req && !sel)) return fail(h, NETKV_EINVAL, "sel and counts must not be NULL");
+    if (!h->have_snap) return fail(h, NETKV_ENOTREADY, "no snapshot loaded");
+    DeviceGuard g(h->device);
+    hipStream_t s = (hipStream_t)stream;
+    hipLaunchKernelGGL(fill_u64_kernel, dim3(1), dim3(64), 0, s, counts, (uint64_t)5, 0ull);
+    if (req->n_req)
+        hipLaunchKernelGGL(tier_count_kernel, dim3((req->n_req + 255) / 256), dim3(256), 0, s, make_snap(h),
+                           make_reqs(req), sel, (unsigned long long *)counts, h->errword);
+    HIPCHK(h, hipGetLastError());
+    return NETKV_OK;
+}
+
+netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req, uint32_t cap, int32_t *out_idx,
+                                     float *out_score, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    netkv_status st = check_requests(h, req);
+    if (st) return st;
+    if (req->n_req && (!out_idx || !out_score)) return fail(h, NETKV_EINVAL, "out_idx and out_score must not be NULL");
+    if (cap > 65535) return fail(h, NETKV_EINVAL, "cap must be <= 65535");
+    if ((st = ready(h))) return st;
+    if (req->n_req == 0) return NETKV_OK;
+    DeviceGuard g(h->device);
+    hipStream_t s = (hipStream_t)stream;
+    const uint64_t R = req->n_req, D = h->D, P = h->P;
+    if (h->seq_j_cap < R * D) {
+        dfree(h->seq_j);
+        h->seq_j_cap = 0;
+        HIPCHK(h, dalloc(h->seq_j, R * D));
+        h->seq_j_cap = R * D;
+    }
+    if (h->seq_cap < R) {
+        dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
+        h->seq_cap = 0;
+        HIPCHK(h, dalloc(h->seq_keys, R));
+        HIPCHK(h, dalloc(h->seq_vals, R));
+        HIPCHK(h, dalloc(h->seq_keys_out, R));
+        HIPCHK(h, dalloc(h->seq_perm, R));
+        h->seq_cap = R;
+    }
+    if (h->seq_P != P) {
+        dfree(h->seq_start); dfree(h->seq_end);
+        h->seq_P = 0;
+        HIPCHK(h, dalloc(h->seq_start, P));
+        HIPCHK(h, dalloc(h->seq_end, P));
+        h->seq_P = (uint32_t)P;
+    }
+    // prefix lengths of every pair (and validation) by the batch scan
+    PairOut po{h->seq_j, nullptr, nullptr, nullptr};
+    if ((st = run_select(h, req, 1, out_idx, out_score, po, true, s))) return st;
+    // requests grouped by prefill instance, batch order kept inside a group
+    const Reqs rq = make_reqs(req);
+    hipLaunchKernelGGL(prefill_key_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s, rq, (uint32_t)P,
+                       (const uint32_t *)h->keys_in, h->seq_keys, h->seq_vals);
+    size_t tb = h->sort_tmp_bytes;
+    HIPCHK(h, rocprim::radix_sort_pairs(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals, h->seq_perm,
+                                        (uint32_t)R, 0, 32, s));
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_start, P, 0u);
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_end, P, 0u);
+    hipLaunchKernelGGL(segment_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s,
+                       (const uint32_t *)h->seq_keys_out, (uint32_t)R, (uint32_t)P, h->seq_start, h->seq_end);
+    HIPCHK(h, hipGetLastError());
+    if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, s));
+    hipLaunchKernelGGL(sequential_kernel, dim3((uint32_t)P), dim3(kSeqThreads), 0, s, make_snap(h), (uint32_t)R, cap,
+                       (const uint16_t *)h->seq_j, req->len_tokens, (const uint32_t *)h->seq_perm,
+                       (const uint32_t *)h->seq_start, (const uint32_t *)h->seq_end, out_idx, out_score);
+    HIPCHK(h, hipGetLastError());
+    if (h->timing) {
+        HIPCHK(h, hipEventRecord(h->ev1, s));
+        h->timed = true;
+    }
+    return NETKV_OK;
+}
+
 netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
     if (!h) return NETKV_EINVAL;
     h->err.clear();
@@ -1608,6 +1827,10 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
         return NETKV_OK;
     case NETKV_OPT_REUSE:
         h->reuse_opt = value ? 1u : 0u;
+        return NETKV_OK;
+    case NETKV_OPT_POLICY:
+        if (value > 2) return fail(h, NETKV_EINVAL, "policy must be 0 (full), 1 (no congestion) or 2 (topology only)");
+        h->policy_opt = value;
         return NETKV_OK;
     case NETKV_OPT_COLS:
         if (value != 0 && value != 1 && value != 2 && value != 4)

@@ -78,11 +78,16 @@ _SIGS = {
     "netkv_kernel_ms": (C.c_int32, [C.c_void_p, C.POINTER(C.c_float)]),
     "netkv_cache_info": (C.c_int32, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]),
     "netkv_set_option": (C.c_int32, [C.c_void_p, C.c_int, C.c_uint32]),
+    "netkv_tier_counts": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_void_p, C.c_void_p,
+                                      C.c_void_p]),
+    "netkv_select_sequential": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
+                                            C.c_void_p, C.c_void_p, C.c_void_p]),
 }
 
 NETKV_OPT_RUN_LEN = 1
 NETKV_OPT_REUSE = 2
 NETKV_OPT_COLS = 3
+NETKV_OPT_POLICY = 4
 
 
 def load_library(path: str = LIB_PATH):
@@ -265,6 +270,21 @@ def netkv_kernel_ms(h: int) -> float:
     return float(ms.value)
 
 
+def netkv_tier_counts(h: int, req: Dict[str, torch.Tensor], sel: torch.Tensor, counts: torch.Tensor,
+                      device) -> None:
+    r = _requests(req)
+    _check(h, load_library().netkv_tier_counts(h, C.byref(r), _dptr(sel, torch.int32, r.n_req, "sel"),
+                                               _dptr(counts, torch.uint64, 5, "counts"), _stream(device)))
+
+
+def netkv_select_sequential(h: int, req: Dict[str, torch.Tensor], cap: int, out_idx: torch.Tensor,
+                            out_score: torch.Tensor, device) -> None:
+    r = _requests(req)
+    _check(h, load_library().netkv_select_sequential(
+        h, C.byref(r), int(cap), _dptr(out_idx, torch.int32, r.n_req, "out_idx"),
+        _dptr(out_score, torch.float32, r.n_req, "out_score"), _stream(device)))
+
+
 def netkv_set_option(h: int, option: int, value: int) -> None:
     _check(h, load_library().netkv_set_option(h, int(option), int(value)))
 
@@ -381,6 +401,21 @@ class Selector:
 
     def commit(self, req_dev, sel: torch.Tensor, cap: int, mu: int) -> None:
         netkv_commit_batch(self.h, req_dev, sel, cap, mu, self.device)
+
+    def select_sequential(self, req_dev, cap: int = 16):
+        n = int(req_dev["prefill"].numel())
+        out = dict(idx=torch.empty(n, dtype=torch.int32, device=self.device),
+                   score=torch.empty(n, dtype=torch.float32, device=self.device))
+        netkv_select_sequential(self.h, req_dev, cap, out["idx"], out["score"], self.device)
+        return out
+
+    def tier_counts(self, req_dev, sel: torch.Tensor) -> np.ndarray:
+        c = torch.empty(5, dtype=torch.uint64, device=self.device)
+        netkv_tier_counts(self.h, req_dev, sel, c, self.device)
+        return to_numpy(c)
+
+    def set_policy(self, policy: int) -> None:
+        netkv_set_option(self.h, NETKV_OPT_POLICY, policy)
 
     def state(self) -> Dict[str, np.ndarray]:
         return netkv_state_get(self.h, self.P, self.D, self.device)

@@ -1,0 +1,166 @@
+"""Ablation rungs of the cost, per-tier selection counts and the sequential
+(request-by-request) form of Algorithm 1 on the GPU, against the CPU
+oracle.  Needs an MI355X and the built library."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_03910_amd import workload as W
+from tests.parity import NEAR_TIE, SCORE_RTOL, check_pairs, check_topk, subset_requests
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print("[gpu-case]", *a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def nk():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_03910_amd import netkv
+    netkv.load_library()
+    return netkv
+
+
+def _inputs(cfg, seed, inflight="random"):
+    snap = W.make_snapshot(cfg, seed, inflight=inflight)
+    ch = W.prefix_chains(cfg, seed)
+    req = W.make_requests(cfg, seed, chains=ch)
+    cache = W.make_caches(cfg, seed, chains=ch)
+    return snap, req, cache
+
+
+@pytest.mark.parametrize("policy", [1, 2])
+def test_policy_rungs_match_zeroed_snapshots(nk, policy):
+    """Rung 1 (static tier map + self-contention) is the full cost with zero
+    congestion; rung 2 (static tier map only) also zeroes the in-flight
+    counters (Sec. VI, Experiment 6)."""
+    _say("policy", policy)
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=W.Cluster(8, 2, 2, 2), n_requests=2000)
+    snap, req, cache = _inputs(cfg, 41)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    sel.set_policy(policy)
+    out = sel.select(nk.requests_to_device(req, sel.device), k=3, pairs=True)
+    sel.sync_errors()
+    osnap = dict(snap)
+    osnap["util"] = np.zeros_like(snap["util"])
+    if policy == 2:
+        osnap["n_inflight"] = np.zeros_like(snap["n_inflight"])
+    o = oracle.select(osnap, cache, req, k=3, pairs=True, n_threads=8)
+    p = out["pairs"]
+    check_pairs(nk.to_numpy(p["prefix_blocks"]), nk.to_numpy(p["feasible"]), nk.to_numpy(p["score"]), o)
+    check_topk(nk.to_numpy(out["idx"]).reshape(-1, 3), nk.to_numpy(out["score"]).reshape(-1, 3),
+               o["idx"], o["cost"], o["feasible"])
+    sel.close()
+
+
+def test_tier_counts(nk):
+    _say("tier counts")
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=W.Cluster(8, 2, 2, 2), n_requests=3000)
+    snap, req, cache = _inputs(cfg, 43)
+    # a reserve only the three freest decodes can meet (by 5 GB): requests
+    # with more non-cached bytes than that are rejected
+    snap["m_min"] = int(np.sort(snap["free_mem"])[-3]) - 5 * 10 ** 9
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = nk.requests_to_device(req, sel.device)
+    out = sel.select(rd, k=1)
+    g_idx = nk.to_numpy(out["idx"])
+    counts = sel.tier_counts(rd, out["idx"])
+    sel.sync_errors()
+    want = oracle.tier_counts(snap, req, g_idx)
+    np.testing.assert_array_equal(counts, want)
+    assert counts.sum() == cfg.n_requests and 0 < counts[4] < cfg.n_requests
+    assert (counts[:4] > 0).sum() >= 2
+    o = oracle.select(snap, cache, req, k=1, n_threads=8)
+    ocounts = oracle.tier_counts(snap, req, o["idx"][:, 0])
+    assert np.abs(counts.astype(np.int64) - ocounts.astype(np.int64)).sum() <= 2 * int(
+        (g_idx != o["idx"][:, 0]).sum())
+    sel.close()
+
+
+def _check_sequential(g_idx, g_score, ref):
+    """GPU choices against the oracle run in follow mode (counters advanced
+    with the GPU's own choices): each choice must be the oracle's argmin or
+    a near-tie of it, with its score within the fp32 tolerance."""
+    o_idx, o_sc, f_cost = ref["idx"], ref["score"], ref["follow_cost"]
+    rej = o_idx < 0
+    assert (g_idx[rej] == -1).all()
+    ok = ~rej
+    assert (g_idx[ok] >= 0).all()
+    assert np.isfinite(f_cost[ok]).all(), "GPU picked an infeasible decode"
+    diff = ok & (g_idx != o_idx)
+    assert (np.abs(f_cost[diff] - o_sc[diff]) <= NEAR_TIE * o_sc[diff]).all()
+    rel = np.abs(g_score[ok].astype(np.float64) - f_cost[ok]) / f_cost[ok]
+    assert rel.max() <= SCORE_RTOL
+    return int(diff.sum())
+
+
+@pytest.mark.parametrize("cap", [16, 2])
+def test_sequential_stream_batch(nk, cap):
+    """A 65,536-request batch at TP=4 sizing on the 64-GPU cluster, with
+    in-flight counters starting from random values."""
+    _say("sequential c1 batch cap", cap)
+    cfg = W.CONFIGS["c1"]
+    snap, req, cache = _inputs(cfg, 45)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = nk.requests_to_device(req, sel.device)
+    out = sel.select_sequential(rd, cap=cap)
+    sel.sync_errors()
+    g_idx, g_sc = nk.to_numpy(out["idx"]), nk.to_numpy(out["score"])
+    ref = oracle.select_sequential(snap, oracle.Cache(cache, n_threads=8), req, cap=cap, follow=g_idx)
+    near = _check_sequential(g_idx, g_sc, ref)
+    assert near < 0.001 * cfg.n_requests
+    # the sequential counters change selections relative to the snapshot semantics
+    snap_sel = nk.to_numpy(sel.select(rd, k=1)["idx"])
+    assert (snap_sel != g_idx).sum() > 0
+    sel.close()
+
+
+def test_sequential_cap_zero_is_snapshot_selection(nk):
+    _say("sequential cap 0")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=3000)
+    snap, req, cache = _inputs(cfg, 47)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = nk.requests_to_device(req, sel.device)
+    a = sel.select_sequential(rd, cap=0)
+    b = sel.select(rd, k=1)
+    sel.sync_errors()
+    np.testing.assert_array_equal(nk.to_numpy(a["idx"]), nk.to_numpy(b["idx"]))
+    np.testing.assert_array_equal(nk.to_numpy(a["score"]), nk.to_numpy(b["score"]))
+    sel.close()
+
+
+@pytest.mark.timeout(900)
+def test_sequential_full_size_two_prefill_instances(nk):
+    """The full 4,096-GPU batch, sequential; every request of two prefill
+    instances (in batch order, which is all that couples them) is checked
+    against the oracle."""
+    _say("sequential c2 full")
+    cfg = W.CONFIGS["c2"]
+    snap, req, cache = _inputs(cfg, 49)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = nk.requests_to_device(req, sel.device)
+    out = sel.select_sequential(rd, cap=16)
+    sel.sync_errors()
+    g_idx, g_sc = nk.to_numpy(out["idx"]), nk.to_numpy(out["score"])
+    ocache = oracle.Cache(cache, n_threads=16)
+    del cache
+    for p in (5, 777):
+        rows = np.flatnonzero(req["prefill"] == p)
+        _say("oracle prefill", p, len(rows), "requests")
+        ref = oracle.select_sequential(snap, ocache, subset_requests(req, rows), cap=16, follow=g_idx[rows])
+        _check_sequential(g_idx[rows], g_sc[rows], ref)
+    sel.close()

@@ -525,3 +525,86 @@ def test_commit_closed_form():
     # d2: 18 requests with j = 0: 18 * 300 = 5400 > 1000 -> clamps to 0
     assert st["free_mem"].tolist() == [10 ** 6 - 600 + 0, 10 ** 6 + 7, 0 + 11]
     assert st["admitted_prev"].tolist() == [600, 0, 5400]
+
+
+# ---------------------------------------------------------------- sequential Algorithm 1
+
+def test_sequential_increment_moves_the_second_request():
+    """Two identical requests from one prefill instance: the first takes the
+    faster same-leaf decode; its in-flight increment halves that tier's
+    effective bandwidth (Eq. (4): 1 + n), so the second takes the same-pod
+    decode.  Numbers: s = 1e9 B, B1 = 4e9, B2 = 3e9 B/s, no congestion:
+    first 0.25 s vs 0.333 s; then 0.5 s vs 0.333 s."""
+    h = [1, 2]
+    snap = tiny_snapshot(1, 2, [1, 2], [0, 0], bw=(1, 4e9, 3e9, 1), alpha=0.0, bpt=5 * 10 ** 8)
+    rq = requests([(0, 2, h), (0, 2, h)])
+    seq = oracle.select_sequential(snap, caches([[], []]), rq, cap=16)
+    assert seq["idx"].tolist() == [0, 1]
+    np.testing.assert_allclose(seq["score"], [0.25, 1e9 / 3e9], rtol=1e-12)
+    snapshot_sel = oracle.select(snap, caches([[], []]), rq, k=1)["idx"][:, 0]
+    assert snapshot_sel.tolist() == [0, 0]
+    # a cap of 0 freezes the counters: the batch reduces to snapshot semantics
+    seq0 = oracle.select_sequential(snap, caches([[], []]), rq, cap=0)
+    assert seq0["idx"].tolist() == [0, 0]
+
+
+def test_sequential_counter_saturates_at_cap():
+    """Five requests, one decode per tier 1 and 2 with B1 = 10 B2: tier 1
+    stays best while 1 + n <= 10; with cap 3 the counter stops at 3, so
+    every request keeps tier 1."""
+    h = [1]
+    snap = tiny_snapshot(1, 2, [1, 2], [0, 0], bw=(1, 10e9, 1e9, 1), alpha=0.0, bpt=10 ** 9)
+    rq = requests([(0, 1, h)] * 5)
+    assert oracle.select_sequential(snap, caches([[], []]), rq, cap=3)["idx"].tolist() == [0] * 5
+    # without a binding cap: costs 0.1 n' for tier 1 (n' = 1 + n) vs 1.0 for tier 2
+    out = oracle.select_sequential(snap, caches([[], []]), rq, cap=100)
+    np.testing.assert_allclose(out["score"], [0.1, 0.2, 0.3, 0.4, 0.5], rtol=1e-12)
+
+
+def test_sequential_prefill_instances_do_not_interact():
+    """Interleaving the requests of two prefill instances does not change any
+    selection (counters are per prefill instance)."""
+    from paper_2606_03910_amd import workload as W
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=400)
+    snap = W.make_snapshot(cfg, 4)
+    ch = W.prefix_chains(cfg, 4)
+    req = W.make_requests(cfg, 4, chains=ch)
+    cache = W.make_caches(cfg, 4, chains=ch)
+    from tests.parity import subset_requests
+    base = oracle.select_sequential(snap, cache, req, cap=16)
+    rng = np.random.default_rng(0)
+    # a random interleaving that keeps each prefill instance's order
+    groups = {}
+    for r in range(cfg.n_requests):
+        groups.setdefault(int(req["prefill"][r]), []).append(r)
+    keys = list(groups)
+    perm = []
+    ptr = {k: 0 for k in keys}
+    while len(perm) < cfg.n_requests:
+        k = keys[rng.integers(len(keys))]
+        if ptr[k] < len(groups[k]):
+            perm.append(groups[k][ptr[k]])
+            ptr[k] += 1
+    perm = np.array(perm)
+    inter = oracle.select_sequential(snap, cache, subset_requests(req, perm), cap=16)
+    np.testing.assert_array_equal(inter["idx"], base["idx"][perm])
+    np.testing.assert_array_equal(inter["score"], base["score"][perm])
+
+
+def test_sequential_follow_mode_reports_costs_of_given_choices():
+    h = [1, 2]
+    snap = tiny_snapshot(1, 2, [1, 2], [0, 0], bw=(1, 4e9, 3e9, 1), alpha=0.0, bpt=5 * 10 ** 8)
+    rq = requests([(0, 2, h), (0, 2, h)])
+    # follow the other choice first: then decode 0 keeps its bandwidth
+    out = oracle.select_sequential(snap, caches([[], []]), rq, cap=16, follow=np.array([1, 0], np.int32))
+    np.testing.assert_allclose(out["follow_cost"], [1e9 / 3e9, 0.25], rtol=1e-12)
+    assert out["idx"].tolist() == [0, 0]
+
+
+def test_tier_counts_closed_form():
+    tmap = np.array([[0, 1, 2, 3], [3, 2, 1, 0]], np.uint8)
+    snap = tiny_snapshot(2, 4, tmap, np.zeros(8))
+    rq = requests([(0, 1, [5]), (1, 1, [5]), (1, 1, [5]), (0, 1, [5]), (1, 1, [5])])
+    cnt = oracle.tier_counts(snap, rq, np.array([2, 2, 3, -1, 0], np.int32))
+    # p0->d2 tier 2, p1->d2 tier 1, p1->d3 tier 0, rejected, p1->d0 tier 3
+    assert cnt.tolist() == [1, 1, 1, 1, 1]
