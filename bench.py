@@ -66,6 +66,10 @@ def main():
                     help="scan every pair from block 0 (no first-miss carry along the batch order)")
     ap.add_argument("--run-len", type=int, default=0, help="requests per wavefront run (0 = auto)")
     ap.add_argument("--cols", type=int, default=0, help="decodes per lane (0 = auto, 1, 2, 4)")
+    ap.add_argument("--policy", type=int, default=0,
+                    help="cost rung: 0 full, 1 without live congestion, 2 topology only")
+    ap.add_argument("--sequential", action="store_true",
+                    help="time the request-by-request form (in-batch in-flight increments, cap 16)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (K launches) and exit: the "
                          "reference kernel for scaling HBM byte counters")
@@ -110,6 +114,7 @@ def main():
     netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_REUSE, 0 if args.no_reuse else 1)
     netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_RUN_LEN, args.run_len)
     netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_COLS, args.cols)
+    netkv.netkv_set_option(sel.h, netkv.NETKV_OPT_POLICY, args.policy)
     t0 = time.time()
     sel.load_snapshot(snap)
     sel.load_cache(cache, 0.5)
@@ -124,7 +129,10 @@ def main():
                score=torch.empty(R * k, dtype=torch.float32, device=dev))
 
     def step():
-        netkv.netkv_select_batch(sel.h, rd, k, out["idx"], out["score"], None, dev)
+        if args.sequential:
+            netkv.netkv_select_sequential(sel.h, rd, 16, out["idx"], out["score"], dev)
+        else:
+            netkv.netkv_select_batch(sel.h, rd, k, out["idx"], out["score"], None, dev)
 
     for _ in range(args.warmup):
         step()
@@ -244,7 +252,8 @@ def main():
             "resident_hashes_per_decode": cfg.cache_per_decode, "slots_per_decode": slots,
             "block_tokens": cfg.block_tokens, "mean_blocks_per_request": float(nblk.mean()),
             "k": k, "parallelism": "single-gpu", "first_miss_carry": not args.no_reuse,
-            "run_len": args.run_len or "auto",
+            "run_len": args.run_len or "auto", "policy": args.policy,
+            "selection": "sequential (in-batch in-flight increments)" if args.sequential else "snapshot",
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
