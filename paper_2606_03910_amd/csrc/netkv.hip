@@ -388,12 +388,12 @@ __device__ inline void member(uint64_t h, const ulonglong2 (&v1)[C], const ulong
 
 template <int C>
 __device__ inline void load_buckets(const uint64_t *const (&col)[C], const Table &t, uint32_t b1, uint32_t b2,
-                                    bool go, ulonglong2 (&v1)[C], ulonglong2 (&v2)[C]) {
+                                    const bool (&go)[C], ulonglong2 (&v1)[C], ulonglong2 (&v2)[C]) {
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         v1[q] = make_ulonglong2(0, 0);
         v2[q] = make_ulonglong2(0, 0);
-        if (go) {
+        if (go[q]) {
             v1[q] = *(const ulonglong2 *)(col[q] + (uint64_t)b1 * t.pitch * 2);
             v2[q] = *(const ulonglong2 *)(col[q] + (uint64_t)b2 * t.pitch * 2);
         }
@@ -503,7 +503,10 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
     {
         uint32_t b1, b2;
         buckets_of(h0, t.shift, b1, b2);
-        load_buckets<C>(col, t, b1, b2, c0.n != 0, v10, v20);
+        bool go[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) go[q] = act[q] && c0.n != 0;
+        load_buckets<C>(col, t, b1, b2, go, v10, v20);
     }
     uint32_t j_prev[C];
 #pragma unroll
@@ -518,8 +521,14 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         const uint64_t h1 = !more ? 0 : reuse ? c1.hf : chash[c1.a];
         uint32_t b11 = c1.b1, b21 = c1.b2;
         if (!reuse) buckets_of(h1, t.shift, b11, b21);
+        // the next request's first test is needed on a column iff its
+        // first-miss index after this request is >= L1; a column that carries
+        // this request (j_prev < L0) keeps j_prev, so it is known now
+        bool go1[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) go1[q] = act[q] && more && (j_prev[q] >= L0 || j_prev[q] >= L1);
         ulonglong2 v11[C], v21[C];
-        load_buckets<C>(col, t, b11, b21, more, v11, v21);
+        load_buckets<C>(col, t, b11, b21, go1, v11, v21);
         // prefix lengths: carried where the common leading run decides them
         uint32_t j[C];
         bool need[C];
