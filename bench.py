@@ -263,7 +263,7 @@ def main():
             "algorithmic_bytes_per_launch": b_alg,
             "membership_tests_per_launch": tests,
             "mean_tests_per_pair": tests / pairs,
-            "kernel": "scan_kernel (k=1; %d decodes per lane)" % (args.cols or (4 if D >= 512 else 1)),
+            "kernel": "scan_kernel (k=1; %d decodes per lane)" % (args.cols or (2 if D >= 256 else 1)),
             "kernel_source_sha256_16": digest,
             "note": ("achieved counts 8 B per first-miss membership test of every pair, as if each "
                      "were read from HBM; the kernel takes most tests from its predecessor in the "

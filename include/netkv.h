@@ -224,7 +224,7 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
  *                        leading blocks (an exact identity, no probe);
  *                        0: every pair is scanned from block 0;
  *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
- *                        automatic (4 on pools of 512+ decodes, else 1), 1, 2, 4.
+ *                        automatic (2 on pools of 256+ decodes, else 1), 1, 2, 4.
  * and one option that does change results, selecting the rung of the
  * method's ablation (Sec. VI, Experiment 6) the costs use:
  *   NETKV_OPT_POLICY  -- 0 (default): the full cost; 1: static tier map and

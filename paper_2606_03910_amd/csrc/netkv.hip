@@ -1177,20 +1177,23 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
     return NETKV_OK;
 }
 
-uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
-    // about 32K wavefronts; runs of 8..512 sorted requests (measured on MI355X:
-    // longer runs carry more first-miss indices, shorter ones keep more
-    // wavefronts in flight)
-    uint64_t rl = (R * ngroup) / 32768;
+uint32_t auto_run_len(uint64_t R, uint32_t ngroup, uint32_t C) {
+    // runs of 384 sorted requests (256 at 4 decodes per lane), shortened
+    // while that leaves fewer than 16K wavefronts (measured on MI355X: longer
+    // runs carry more first-miss indices, shorter ones keep more wavefronts
+    // in flight)
+    const uint64_t base = C >= 4 ? 256 : 384;
+    uint64_t rl = base;
+    if (R * ngroup < base * 16384) rl = (R * ngroup) / 16384;
     if (rl < 8) rl = 8;
-    if (rl > 512) rl = 512;
     return (uint32_t)rl;
 }
 
-// decodes per lane: 4 when there are many decodes, else 1 (or the option)
+// decodes per lane: 2 when there are at least 256 decodes, else 1 (or the
+// option: 1, 2 or 4)
 inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
     if (opt == 1 || opt == 2 || opt == 4) return opt;
-    return D >= 8u * kWave ? 4u : 1u;
+    return D >= 4u * kWave ? 2u : 1u;
 }
 
 template <int K, int C>
@@ -1259,7 +1262,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
                        (const uint32_t *)h->n_valid, t.shift, h->rec);
     HIPCHK(h, hipGetLastError());
-    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
+    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup, C);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{h->perm, h->rec, h->n_valid};
     if (K == 1)

@@ -111,6 +111,39 @@ def test_ragged_decodes_long_runs_and_empty_runs(nk):
     sel.close()
 
 
+def test_tuning_options_leave_results_unchanged(nk):
+    """Decodes per lane (1, 2, 4), run lengths (1, 7, automatic, longer
+    than the batch) and first-miss reuse on/off are layout choices only:
+    every pair and every top-k entry is bit-identical across them, and the
+    first matches the oracle.  270 decodes leave a partial last group of
+    decodes at every width."""
+    _say("tuning options")
+    cl = W.Cluster(8, 5, 3, 3)
+    cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=3000, cache_per_decode=4096)
+    assert cfg.n_decode == 270
+    snap, req, cache = _inputs(cfg, 8, "random")
+    sel = _gpu(nk, snap, cache)
+    base = None
+    for cols in (1, 2, 4):
+        for rl in (1, 7, 0, 5000):
+            for reuse in (1, 0):
+                if reuse == 0 and rl not in (0, 7):
+                    continue
+                nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, cols)
+                nk.netkv_set_option(sel.h, nk.NETKV_OPT_RUN_LEN, rl)
+                nk.netkv_set_option(sel.h, nk.NETKV_OPT_REUSE, reuse)
+                g = _run(nk, sel, req, 3)
+                if base is None:
+                    base = g
+                    o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
+                    check_pairs(g["j"], g["feas"], g["cost"], o)
+                    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+                    continue
+                for key in base:
+                    assert np.array_equal(g[key], base[key]), (cols, rl, reuse, key)
+    sel.close()
+
+
 @pytest.mark.parametrize("lf", [0.9, 0.99])
 def test_dense_tables(nk, lf):
     """Dense tables (load factor capped at 0.85, rounded to a power of two):
