@@ -101,7 +101,10 @@ netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stre
  * hashes[hash_off[d] .. hash_off[d+1]), n_hashes = hash_off[n_decode].
  * Host or device pointers.  Value 0 is reserved (EINVAL); repeated hashes
  * of one decode are allowed and count once.  Builds one open-addressed
- * table per decode with at most `max_load_factor` (0 < lf < 1) occupancy.
+ * table per decode with at most `max_load_factor` (0 < lf < 1) occupancy
+ * (capped at 0.85), and one filter over the union of all sets (8 bits per
+ * resident hash) that proves a hash absent from every decode, so a scan
+ * can skip that hash's per-decode tests without changing any result.
  * Synchronous.  EINVAL: bad CSR, hash 0, lf out of range, D different
  * from a loaded snapshot; ECAPACITY: a table would need more than 2^31
  * slots; ENOMEM: out of device memory. */
@@ -235,7 +238,7 @@ enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3, NETKV_OPT
 netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 
 /* Table geometry of the loaded cache: slots per decode (a power of two)
- * and the device bytes of all tables. */
+ * and the device bytes of all tables and the filter. */
 netkv_status netkv_cache_info(netkv_handle h, uint64_t *slots_per_decode, uint64_t *table_bytes);
 
 #ifdef __cplusplus

@@ -91,6 +91,8 @@ struct Table {
     const uint64_t *keys;   // [buckets][pitch][2]
     uint32_t shift;         // 32 - log2(buckets)
     uint32_t pitch;
+    const uint64_t *any;    // [2^(64 - any_shift)] resident-anywhere filter words
+    uint32_t any_shift;
 };
 
 struct Reqs {
@@ -117,6 +119,28 @@ __host__ __device__ inline void buckets_of(uint64_t h, uint32_t shift, uint32_t 
     const uint32_t fold = (uint32_t)h ^ (uint32_t)(h >> 32);
     b1 = (fold * kFib32) >> shift;
     b2 = b1 ^ (((fold * kMix32) >> shift) | 1u);
+}
+
+// The resident-anywhere filter: a blocked Bloom filter over the union of all
+// decodes' resident hashes, one 64-bit word per key with four bits set in
+// it.  A clear bit proves that no decode holds the key; a full match only
+// says it may be held somewhere, so a scan that skips a test on a clear bit
+// stays exact.  Word from the top bits of one multiplicative hash, bit
+// positions from the top 24 bits of another.
+constexpr uint64_t kAnyWordMul = 0xD1B54A32D192ED03ull;
+constexpr uint64_t kAnyBitsMul = 0xAEF17502108EF2D9ull;
+
+__host__ __device__ inline void any_of(uint64_t h, uint32_t any_shift, uint64_t &word, uint64_t &mask) {
+    word = (h * kAnyWordMul) >> any_shift;
+    const uint32_t y = (uint32_t)((h * kAnyBitsMul) >> 40);
+    mask = (1ull << (y & 63u)) | (1ull << ((y >> 6) & 63u)) | (1ull << ((y >> 12) & 63u)) |
+           (1ull << ((y >> 18) & 63u));
+}
+
+__device__ inline bool maybe_anywhere(const uint64_t *__restrict__ any, uint32_t any_shift, uint64_t h) {
+    uint64_t w, m;
+    any_of(h, any_shift, w, m);
+    return (any[w] & m) == m;
 }
 
 // Is h in bucket b of the table column `col` (this decode's column)?
@@ -260,7 +284,7 @@ struct alignas(16) Rec {
     uint64_t a;      // offset of the hash run
     uint64_t hf;     // hash of block lcp (the first one a carried scan tests), 0 if lcp == n
     uint32_t b2;     // second candidate bucket of hf
-    uint32_t pad;
+    uint32_t gp;     // 0 when the filter proves that no decode holds hf
 };
 
 struct Order {
@@ -322,7 +346,7 @@ __global__ void count_valid_kernel(const uint32_t *__restrict__ sorted_keys, uin
 // Record of each sorted request, with its common leading blocks with the
 // previous sorted request.
 __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
-                                                  const uint32_t *__restrict__ n_valid, uint32_t shift,
+                                                  const uint32_t *__restrict__ n_valid, Table t,
                                                   Rec *__restrict__ rec) {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= *n_valid) return;
@@ -345,8 +369,8 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__res
     x.lcp = l;
     x.a = a;
     x.hf = l < nr ? rq.hashes[a + l] : 0;
-    buckets_of(x.hf, shift, x.b1, x.b2);
-    x.pad = 0;
+    buckets_of(x.hf, t.shift, x.b1, x.b2);
+    x.gp = l < nr && maybe_anywhere(t.any, t.any_shift, x.hf) ? 1u : 0u;
     rec[i] = x;
 }
 
@@ -373,7 +397,7 @@ __device__ inline Rec load_rec(const Rec *base, uint32_t i) {
     x.a = ((uint64_t)w[7] << 32) | (uint64_t)w[6];
     x.hf = ((uint64_t)w[9] << 32) | (uint64_t)w[8];
     x.b2 = w[10];
-    x.pad = 0;
+    x.gp = w[11];
     return x;
 }
 
@@ -496,8 +520,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
     float2 pc0[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) pc0[q] = s.pcon[(uint64_t)c0.p * s.D + (act[q] ? d[q] : 0)];
-    // first membership test of the current request (block L0), loaded ahead
+    // first membership test of the current request (block L0), loaded ahead;
+    // t0: whether it is needed at all (not when the filter rules block L0 out
+    // on every decode)
     uint32_t L0 = 0;
+    bool t0 = c0.n != 0;
     uint64_t h0 = c0.n ? chash[c0.a] : 0;
     ulonglong2 v10[C], v20[C];
     {
@@ -517,7 +544,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
 #pragma unroll
         for (int q = 0; q < C; ++q) pc1[q] = s.pcon[(uint64_t)c1.p * s.D + (act[q] ? d[q] : 0)];
         const uint32_t L1 = reuse ? c1.lcp : 0u;
-        const bool more = i + 1 < i1 && L1 < c1.n;
+        const bool more = i + 1 < i1 && L1 < c1.n && (!reuse || c1.gp);
         const uint64_t h1 = !more ? 0 : reuse ? c1.hf : chash[c1.a];
         uint32_t b11 = c1.b1, b21 = c1.b2;
         if (!reuse) buckets_of(h1, t.shift, b11, b21);
@@ -538,7 +565,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             j[q] = carry ? j_prev[q] : L0;
             need[q] = act[q] && !carry;
         }
-        if (L0 < c0.n) probe_from<W, C>(col, t, chash + c0.a, c0.n, L0, need, j, h0, v10, v20);
+        if (t0) probe_from<W, C>(col, t, chash + c0.a, c0.n, L0, need, j, h0, v10, v20);
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t cb[C];
 #pragma unroll
@@ -586,6 +613,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         }
         L0 = L1;
         h0 = h1;
+        t0 = more;
     }
 }
 
@@ -710,6 +738,19 @@ __device__ inline bool try_place(unsigned long long *bk, uint64_t key) {
         if (prev == 0ull || prev == key) return true;
     }
     return false;
+}
+
+// Resident-anywhere filter: set each key's four bits (grid-stride).
+__global__ __launch_bounds__(256) void any_build_kernel(const uint64_t *__restrict__ h, uint64_t n,
+                                                        uint64_t *__restrict__ any, uint32_t any_shift) {
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride) {
+        uint64_t w, m;
+        any_of(h[i], any_shift, w, m);
+        // bits are only ever set, so a word that already holds them needs no atomic
+        if ((any[w] & m) != m) atomicOr((unsigned long long *)(any + w), (unsigned long long)m);
+    }
 }
 
 __global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys, uint32_t shift, uint32_t pitch,
@@ -987,6 +1028,9 @@ struct netkv_ctx {
     uint64_t *table = nullptr;
     uint64_t table_bytes = 0, buckets = 0;
     uint32_t log2b = 0, pitch = 0;
+    uint64_t *any = nullptr;     // resident-anywhere filter words
+    uint64_t any_words = 0;
+    uint32_t any_shift = 0;
     // scratch
     uint32_t *errword = nullptr;          // request / selection errors (sticky)
     uint32_t *loadword = nullptr;         // validation flags of the load calls
@@ -1112,6 +1156,8 @@ Table make_table(netkv_handle h) {
     t.keys = h->table;
     t.shift = 32 - h->log2b;
     t.pitch = h->pitch;
+    t.any = h->any;
+    t.any_shift = h->any_shift;
     return t;
 }
 
@@ -1260,7 +1306,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(64), 0, st, (const uint32_t *)h->keys_out, (uint32_t)R,
                        h->n_valid);
     hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->n_valid, t.shift, h->rec);
+                       (const uint32_t *)h->n_valid, t, h->rec);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup, C);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
@@ -1322,6 +1368,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->dbase);
         dfree(h->dxlim);
         dfree(h->table);
+        dfree(h->any);
         dfree(h->errword);
         dfree(h->loadword);
         dfree(h->jT);
@@ -1542,15 +1589,34 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
         cleanup();
         return fail(h, NETKV_EINVAL, "cache contains the reserved hash value 0");
     }
-    // release the old table first: the new one may be large
+    // release the old table and filter first: the new ones may be large
     dfree(h->table);
+    dfree(h->any);
+    h->table = nullptr;
+    h->any = nullptr;
     h->have_cache = false;
+    // filter: a power-of-two number of 64-bit words, 8 bits per resident hash
+    uint32_t log2w = 6;
+    while ((1ull << log2w) * 8ull < total && log2w < 40) ++log2w;
+    const uint64_t any_words = 1ull << log2w;
+    uint64_t *anyw = nullptr;
+    if (dalloc(anyw, any_words) != hipSuccess) {
+        cleanup();
+        return fail(h, NETKV_ENOMEM, "filter allocation of %llu bytes failed", (unsigned long long)(8 * any_words));
+    }
     e = dalloc(tab, cap * pitch);
     if (e != hipSuccess) {
         cleanup();
+        dfree(anyw);
         return fail(h, NETKV_ENOMEM, "table allocation of %llu bytes failed", (unsigned long long)tbytes);
     }
     e = hipMemsetAsync(tab, 0, tbytes, st);
+    if (e == hipSuccess) e = hipMemsetAsync(anyw, 0, 8 * any_words, st);
+    if (e == hipSuccess && total) {
+        hipLaunchKernelGGL(any_build_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st,
+                           (const uint64_t *)(dh + first), total, anyw, 64u - log2w);
+        e = hipGetLastError();
+    }
     if (e == hipSuccess && !tdec.empty()) {
         hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, 32u - log2b, pitch,
                            (const uint64_t *)dh, (const uint32_t *)ddec,
@@ -1562,6 +1628,7 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     dfree(dh); dfree(dbeg); dfree(dend); dfree(ddec);
     if (e != hipSuccess || bad) {
         dfree(tab);
+        dfree(anyw);
         return e != hipSuccess ? fail(h, NETKV_EDEVICE, "table build failed: %s", hipGetErrorString(e))
                                : fail(h, NETKV_ECAPACITY, "table build could not place every hash");
     }
@@ -1569,7 +1636,10 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     h->buckets = nbk;
     h->log2b = log2b;
     h->pitch = pitch;
-    h->table_bytes = tbytes;
+    h->table_bytes = tbytes + 8 * any_words;
+    h->any = anyw;
+    h->any_words = any_words;
+    h->any_shift = 64u - log2w;
     h->cache_D = n_decode;
     h->have_cache = true;
     return NETKV_OK;
