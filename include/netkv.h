@@ -225,7 +225,9 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
  *                        decode is taken from the preceding request of the
  *                        batch order when it lies inside their common
  *                        leading blocks (an exact identity, no probe);
- *                        0: every pair is scanned from block 0;
+ *                        0: nothing is carried, every pair is scanned
+ *                        from block 0 (a block that the cache filter
+ *                        proves absent from every decode is not probed);
  *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
  *                        automatic (2 on pools of 256+ decodes, else 1), 1, 2, 4.
  * and one option that does change results, selecting the rung of the

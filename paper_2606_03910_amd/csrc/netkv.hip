@@ -346,7 +346,7 @@ __global__ void count_valid_kernel(const uint32_t *__restrict__ sorted_keys, uin
 // Record of each sorted request, with its common leading blocks with the
 // previous sorted request.
 __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
-                                                  const uint32_t *__restrict__ n_valid, Table t,
+                                                  const uint32_t *__restrict__ n_valid, Table t, uint32_t reuse,
                                                   Rec *__restrict__ rec) {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= *n_valid) return;
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__res
     const uint64_t a = rq.off[r];
     const uint64_t nr = rq.off[r + 1] - a;
     uint32_t l = 0;
-    if (i > 0) {
+    if (i > 0 && reuse) {
         const uint32_t q = perm[i - 1];
         const uint64_t b = rq.off[q];
         const uint64_t nq = rq.off[q + 1] - b;
@@ -405,9 +405,10 @@ __device__ inline Rec load_rec(const Rec *base, uint32_t i) {
 // candidate buckets loaded beforehand (v1, v2).
 template <int C>
 __device__ inline void member(uint64_t h, const ulonglong2 (&v1)[C], const ulonglong2 (&v2)[C], bool (&alive)[C]) {
+    // bitwise, not short-circuit: the four compares become lane masks
 #pragma unroll
     for (int q = 0; q < C; ++q)
-        alive[q] = alive[q] && (v1[q].x == h || v1[q].y == h || v2[q].x == h || v2[q].y == h);
+        alive[q] = alive[q] & ((v1[q].x == h) | (v1[q].y == h) | (v2[q].x == h) | (v2[q].y == h));
 }
 
 template <int C>
@@ -491,7 +492,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
                                                       const uint64_t *__restrict__ hashes,
                                                       const uint32_t *__restrict__ n_valid, uint32_t n_req,
                                                       uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
-                                                      uint32_t reuse, uint64_t *__restrict__ partial, PairOut po) {
+                                                      uint64_t *__restrict__ partial, PairOut po) {
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t gw = blockIdx.x * kWavesPerBlock + wave_index();
     const uint32_t run = gw / ngroup, grp = gw % ngroup;
@@ -543,11 +544,10 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         float2 pc1[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) pc1[q] = s.pcon[(uint64_t)c1.p * s.D + (act[q] ? d[q] : 0)];
-        const uint32_t L1 = reuse ? c1.lcp : 0u;
-        const bool more = i + 1 < i1 && L1 < c1.n && (!reuse || c1.gp);
-        const uint64_t h1 = !more ? 0 : reuse ? c1.hf : chash[c1.a];
-        uint32_t b11 = c1.b1, b21 = c1.b2;
-        if (!reuse) buckets_of(h1, t.shift, b11, b21);
+        const uint32_t L1 = c1.lcp;
+        const bool more = i + 1 < i1 && L1 < c1.n && c1.gp;
+        const uint64_t h1 = more ? c1.hf : 0;
+        const uint32_t b11 = c1.b1, b21 = c1.b2;
         // the next request's first test is needed on a column iff its
         // first-miss index after this request is >= L1; a column that carries
         // this request (j_prev < L0) keeps j_prev, so it is known now
@@ -583,24 +583,28 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             }
             cb[q] = (act[q] && feas) ? __float_as_uint(cost) : 0xFFFFFFFFu;
         }
-        // the group's K best: least cost bits, then least decode index
+        // the group's K best: least cost bits, then least decode index, i.e.
+        // the lowest lane holding the minimum in the first column that holds it
         uint64_t mine = kEmptyKey;
 #pragma unroll
         for (int r = 0; r < K; ++r) {
-            uint32_t lm = cb[0], lq = 0;
+            uint32_t lm = cb[0];
 #pragma unroll
-            for (int q = 1; q < C; ++q)
-                if (cb[q] < lm) {
-                    lm = cb[q];
-                    lq = q;
-                }
+            for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
             const uint32_t mn = wave_min_u32_dpp(lm);
-            const uint32_t dm = wave_min_u32_dpp((lm == mn && mn != 0xFFFFFFFFu) ? base + lq * kWave + lane
-                                                                                    : 0xFFFFFFFFu);
+            if (mn == 0xFFFFFFFFu) break;  // no feasible candidate left (uniform)
+            uint32_t dm = 0;
 #pragma unroll
-            for (int q = 0; q < C; ++q)
-                if (mn != 0xFFFFFFFFu && d[q] == dm) cb[q] = 0xFFFFFFFFu;
-            if (lane == (uint32_t)r) mine = mn != 0xFFFFFFFFu ? (((uint64_t)mn << 32) | (uint64_t)dm) : kEmptyKey;
+            for (int q = 0; q < C; ++q) {
+                const uint64_t m = __ballot(cb[q] == mn);
+                if (m) {
+                    const uint32_t l = (uint32_t)__builtin_ctzll(m);
+                    dm = base + q * kWave + l;
+                    if (lane == l) cb[q] = 0xFFFFFFFFu;
+                    break;
+                }
+            }
+            if (lane == (uint32_t)r) mine = ((uint64_t)mn << 32) | (uint64_t)dm;
         }
         if (lane < (uint32_t)K) partial[((uint64_t)grp * n_req + i) * K + lane] = mine;
         c0 = c1;
@@ -1244,33 +1248,33 @@ inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
 
 template <int K, int C>
 void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
-                 uint32_t n_runs, uint32_t ngroup, uint32_t reuse, uint64_t *partial, const PairOut &po, bool pairs,
+                 uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po, bool pairs,
                  hipStream_t st) {
-    constexpr int W = C >= 4 ? 2 : C == 2 ? 2 : kSpec;
+    constexpr int W = C >= 4 ? 1 : C == 2 ? 2 : kSpec;
     const uint64_t waves = (uint64_t)n_runs * ngroup;
     const uint32_t grid = (uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
     if (pairs)
         hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
-                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, reuse, partial, po);
+                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
     else
         hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
-                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, reuse, partial, po);
+                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
 }
 
 // Scan, bracketed by the handle's timing events when enabled, then merge.
 template <int K>
 hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
-                              uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C, uint32_t reuse,
+                              uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C,
                               uint64_t *partial, const PairOut &po, bool pairs, uint32_t k, int32_t *idx,
                               float *score, hipStream_t st) {
     hipError_t e = hipSuccess;
     if (h->timing && (e = hipEventRecord(h->ev0, st)) != hipSuccess) return e;
     if (C == 4)
-        launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+        launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 2)
-        launch_scan<K, 2>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+        launch_scan<K, 2>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else
-        launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, reuse, partial, po, pairs, st);
+        launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (h->timing) {
         if ((e = hipEventRecord(h->ev1, st)) != hipSuccess) return e;
@@ -1306,22 +1310,22 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(64), 0, st, (const uint32_t *)h->keys_out, (uint32_t)R,
                        h->n_valid);
     hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->n_valid, t, h->rec);
+                       (const uint32_t *)h->n_valid, t, h->reuse_opt, h->rec);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup, C);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{h->perm, h->rec, h->n_valid};
     if (K == 1)
-        HIPCHK(h, launch_scan_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+        HIPCHK(h, launch_scan_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
                                         pairs, k, idx, score, st));
     else if (K == 2)
-        HIPCHK(h, launch_scan_reduce<2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+        HIPCHK(h, launch_scan_reduce<2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
                                         pairs, k, idx, score, st));
     else if (K == 4)
-        HIPCHK(h, launch_scan_reduce<4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+        HIPCHK(h, launch_scan_reduce<4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
                                         pairs, k, idx, score, st));
     else
-        HIPCHK(h, launch_scan_reduce<8>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->reuse_opt, h->partial, po,
+        HIPCHK(h, launch_scan_reduce<8>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
                                         pairs, k, idx, score, st));
     return NETKV_OK;
 }
