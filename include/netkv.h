@@ -211,10 +211,14 @@ netkv_status netkv_state_get(netkv_handle h, uint16_t *n_inflight, uint32_t *que
 netkv_status netkv_sync_errors(netkv_handle h, void *stream);
 
 /* Kernel timing: when enabled, the library records HIP events on `stream`
- * around the scoring kernel (the fused match / score / per-group top-k scan,
- * not the ordering or merge kernels) of each netkv_select_batch,
- * and around the sweep kernel of netkv_rank_sweep; netkv_kernel_ms returns
- * (after synchronising on the end event) the milliseconds of the last one. */
+ * around the one scoring kernel of each call -- the fused match / score /
+ * per-group top-k scan of netkv_select_batch (not the ordering or merge
+ * kernels), the sweep kernel of netkv_rank_sweep, the per-prefill kernel of
+ * netkv_select_sequential -- without synchronising.  netkv_kernel_ms waits
+ * for the last of them and returns the mean milliseconds over the launches
+ * timed since timing was last enabled (the latest 256 when there were more);
+ * ENOTREADY when there were none.  Enabling creates the events (EDEVICE if
+ * that fails) and restarts the count. */
 netkv_status netkv_set_timing(netkv_handle h, int enable);
 netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
 

@@ -1006,6 +1006,8 @@ __global__ __launch_bounds__(kSeqThreads) void sequential_kernel(Snap s, uint32_
 
 // ====================================================================== host side
 
+constexpr uint32_t kTimeSlots = 256;   // timed launches kept for netkv_kernel_ms
+
 struct netkv_ctx {
     int device = 0;
     std::string err;
@@ -1069,8 +1071,9 @@ struct netkv_ctx {
     uint32_t seq_P = 0;
     // timing
     bool timing = false;
-    bool timed = false;
-    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    // kernel timing: begin/end event pairs in a ring, created on first enable
+    std::vector<hipEvent_t> tev;
+    uint32_t tcount = 0;    // launches timed since timing was enabled
 };
 
 namespace {
@@ -1085,6 +1088,27 @@ struct DeviceGuard {
         int cur = -1;
         if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
     }
+};
+
+// Events around the one timed kernel of an API call (when timing is on).
+hipError_t time_begin(netkv_handle h, hipStream_t st) {
+    if (!h->timing) return hipSuccess;
+    return hipEventRecord(h->tev[2 * (h->tcount % kTimeSlots)], st);
+}
+
+hipError_t time_end(netkv_handle h, hipStream_t st) {
+    if (!h->timing) return hipSuccess;
+    const hipError_t e = hipEventRecord(h->tev[2 * (h->tcount % kTimeSlots) + 1], st);
+    if (e == hipSuccess) ++h->tcount;
+    return e;
+}
+
+// Timing suspended for a scope (inner steps of a call that times another kernel).
+struct TimingOff {
+    netkv_handle h;
+    bool was;
+    explicit TimingOff(netkv_handle hh) : h(hh), was(hh->timing) { h->timing = false; }
+    ~TimingOff() { h->timing = was; }
 };
 
 netkv_status fail(netkv_handle h, netkv_status st, const char *fmt, ...) {
@@ -1268,7 +1292,7 @@ hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, co
                               uint64_t *partial, const PairOut &po, bool pairs, uint32_t k, int32_t *idx,
                               float *score, hipStream_t st) {
     hipError_t e = hipSuccess;
-    if (h->timing && (e = hipEventRecord(h->ev0, st)) != hipSuccess) return e;
+    if ((e = time_begin(h, st)) != hipSuccess) return e;
     if (C == 4)
         launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 2)
@@ -1276,10 +1300,7 @@ hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, co
     else
         launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (h->timing) {
-        if ((e = hipEventRecord(h->ev1, st)) != hipSuccess) return e;
-        h->timed = true;
-    }
+    if ((e = time_end(h, st)) != hipSuccess) return e;
     hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
                        (const uint64_t *)partial, ord.perm, ord.n_valid, idx, score);
     return hipGetLastError();
@@ -1347,8 +1368,7 @@ netkv_status netkv_create(netkv_handle *out, int device) {
     h->device = device;
     DeviceGuard g(device);
     if (dalloc(h->errword, 1) != hipSuccess || dalloc(h->loadword, 1) != hipSuccess ||
-        hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess ||
-        hipEventCreate(&h->ev0) != hipSuccess || hipEventCreate(&h->ev1) != hipSuccess) {
+        hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess) {
         netkv_destroy(h);
         return NETKV_EDEVICE;
     }
@@ -1385,8 +1405,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
-        if (h->ev0) (void)hipEventDestroy(h->ev0);
-        if (h->ev1) (void)hipEventDestroy(h->ev1);
+        for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
     }
     delete h;
 }
@@ -1706,13 +1725,16 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
     Reqs rq = make_reqs(req);
     // prefix lengths (transposed) and the selection under the loaded congestion
     PairOut po{nullptr, nullptr, nullptr, h->jT};
-    if ((st = run_select(h, req, 1, h->base_idx, h->base_score, po, true, s))) return st;
+    {
+        TimingOff off(h);  // only the sweep kernel is timed
+        if ((st = run_select(h, req, 1, h->base_idx, h->base_score, po, true, s))) return st;
+    }
     if (out_flips) {
         hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(2ull * n_scen, 256)), dim3(256), 0, s, out_flips,
                            2ull * n_scen, 0ull);
         HIPCHK(h, hipGetLastError());
     }
-    if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, s));
+    HIPCHK(h, time_begin(h, s));
     dim3 grid((uint32_t)((R + 255) / 256), n_scen);
     unsigned long long *fl = (unsigned long long *)out_flips;
     if (k <= 1)
@@ -1728,10 +1750,7 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
         hipLaunchKernelGGL(sweep_kernel<8>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, k, out_idx,
                            out_score, fl);
     HIPCHK(h, hipGetLastError());
-    if (h->timing) {
-        HIPCHK(h, hipEventRecord(h->ev1, s));
-        h->timed = true;
-    }
+    HIPCHK(h, time_end(h, s));
     return NETKV_OK;
 }
 
@@ -1808,18 +1827,33 @@ netkv_status netkv_sync_errors(netkv_handle h, void *stream) {
 
 netkv_status netkv_set_timing(netkv_handle h, int enable) {
     if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    if (enable && h->tev.empty()) {
+        DeviceGuard g(h->device);
+        h->tev.assign(2 * kTimeSlots, nullptr);
+        for (hipEvent_t &ev : h->tev) HIPCHK(h, hipEventCreate(&ev));
+    }
     h->timing = enable != 0;
-    h->timed = false;
+    h->tcount = 0;
     return NETKV_OK;
 }
 
 netkv_status netkv_kernel_ms(netkv_handle h, float *ms) {
     if (!h || !ms) return NETKV_EINVAL;
     h->err.clear();
-    if (!h->timed) return fail(h, NETKV_ENOTREADY, "no timed kernel yet");
+    if (h->tcount == 0) return fail(h, NETKV_ENOTREADY, "no timed kernel yet");
     DeviceGuard g(h->device);
-    HIPCHK(h, hipEventSynchronize(h->ev1));
-    HIPCHK(h, hipEventElapsedTime(ms, h->ev0, h->ev1));
+    const uint32_t n = std::min(h->tcount, kTimeSlots);
+    const uint32_t last = (h->tcount - 1) % kTimeSlots;
+    HIPCHK(h, hipEventSynchronize(h->tev[2 * last + 1]));
+    double sum = 0.0;
+    for (uint32_t i = 0; i < n; ++i) {
+        const uint32_t slot = (h->tcount - 1 - i) % kTimeSlots;
+        float one = 0.0f;
+        HIPCHK(h, hipEventElapsedTime(&one, h->tev[2 * slot], h->tev[2 * slot + 1]));
+        sum += one;
+    }
+    *ms = (float)(sum / n);
     return NETKV_OK;
 }
 
@@ -1878,7 +1912,10 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     }
     // prefix lengths of every pair (and validation) by the batch scan
     PairOut po{h->seq_j, nullptr, nullptr, nullptr};
-    if ((st = run_select(h, req, 1, out_idx, out_score, po, true, s))) return st;
+    {
+        TimingOff off(h);  // only the sequential kernel is timed
+        if ((st = run_select(h, req, 1, out_idx, out_score, po, true, s))) return st;
+    }
     // requests grouped by prefill instance, batch order kept inside a group
     const Reqs rq = make_reqs(req);
     hipLaunchKernelGGL(prefill_key_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s, rq, (uint32_t)P,
@@ -1891,15 +1928,12 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     hipLaunchKernelGGL(segment_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s,
                        (const uint32_t *)h->seq_keys_out, (uint32_t)R, (uint32_t)P, h->seq_start, h->seq_end);
     HIPCHK(h, hipGetLastError());
-    if (h->timing) HIPCHK(h, hipEventRecord(h->ev0, s));
+    HIPCHK(h, time_begin(h, s));
     hipLaunchKernelGGL(sequential_kernel, dim3((uint32_t)P), dim3(kSeqThreads), 0, s, make_snap(h), (uint32_t)R, cap,
                        (const uint16_t *)h->seq_j, req->len_tokens, (const uint32_t *)h->seq_perm,
                        (const uint32_t *)h->seq_start, (const uint32_t *)h->seq_end, out_idx, out_score);
     HIPCHK(h, hipGetLastError());
-    if (h->timing) {
-        HIPCHK(h, hipEventRecord(h->ev1, s));
-        h->timed = true;
-    }
+    HIPCHK(h, time_end(h, s));
     return NETKV_OK;
 }
 

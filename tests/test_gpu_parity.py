@@ -318,3 +318,31 @@ def test_contract_errors_write_nothing(nk):
     sel.select(nk.requests_to_device(empty, sel.device), k=1)
     sel.sync_errors()
     sel.close()
+
+
+def test_kernel_timing_mean_over_launches(nk):
+    """Timing records one scan per select without synchronising; the mean
+    covers the launches since timing was enabled, and enabling restarts it."""
+    _say("kernel timing")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=512)
+    snap, req, cache = _inputs(cfg, 21)
+    sel = _gpu(nk, snap, cache)
+    rd = nk.requests_to_device(req, sel.device)
+    idx = torch.empty(512, dtype=torch.int32, device=sel.device)
+    sc = torch.empty(512, dtype=torch.float32, device=sel.device)
+    nk.netkv_set_timing(sel.h, True)
+    with pytest.raises(nk.NetKVError) as e:
+        nk.netkv_kernel_ms(sel.h)
+    assert e.value.status == -2
+    for _ in range(300):          # more than the ring holds
+        nk.netkv_select_batch(sel.h, rd, 1, idx, sc, None, sel.device)
+    ms = nk.netkv_kernel_ms(sel.h)
+    assert 0.0 < ms < 100.0
+    nk.netkv_set_timing(sel.h, True)
+    with pytest.raises(nk.NetKVError):
+        nk.netkv_kernel_ms(sel.h)
+    nk.netkv_set_timing(sel.h, False)
+    nk.netkv_select_batch(sel.h, rd, 1, idx, sc, None, sel.device)
+    with pytest.raises(nk.NetKVError):
+        nk.netkv_kernel_ms(sel.h)
+    sel.close()
