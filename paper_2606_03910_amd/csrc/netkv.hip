@@ -50,6 +50,7 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
+constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint32_t kFib32 = 0x9E3779B1u;
@@ -82,7 +83,8 @@ struct Snap {
     uint32_t P, D;
     uint32_t policy;         // 0: full NetKV, 1: no live congestion, 2: neither congestion nor in-flight
     // derived once per call by derive_kernel (Eqs. (3)-(7) factored by (p, d) and d)
-    const float2 *pcon;      // [P*D] {seconds per non-cached token, tier latency}
+    const float *spt;        // [P*D] seconds per non-cached token (the tier latency
+                             // comes from tier_map and lat[])
     const float *dbase;      // [D] alpha (T_queue + T_decode)
     const uint64_t *dxlim;   // [D] x = l - lambda is feasible iff x < dxlim
 };
@@ -244,14 +246,14 @@ __device__ inline bool request_ok(const Reqs &rq, const Snap &s, uint32_t r, uin
 // Per-call factors of the cost: spt and tier latency for every (p, d), the
 // load term and feasibility limit for every d.  Reads the current snapshot
 // (congestion, in-flight counters, queue, batch, free memory).
-__global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict__ pcon, float *__restrict__ dbase,
+__global__ __launch_bounds__(256) void derive_kernel(Snap s, float *__restrict__ spt, float *__restrict__ dbase,
                                                      uint64_t *__restrict__ dxlim) {
     const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint64_t npd = (uint64_t)s.P * s.D;
     if (i < npd) {
         const uint32_t p = (uint32_t)(i / s.D);
         const uint32_t tau = s.tier_map[i] & 3u;
-        pcon[i] = make_float2(sec_per_token(s, tau, p, s.util[i]), s.lat[tau]);
+        spt[i] = sec_per_token(s, tau, p, s.util[i]);
     }
     if (i < s.D) {
         dbase[i] = load_term(s, (uint32_t)i);
@@ -401,51 +403,65 @@ __device__ inline Rec load_rec(const Rec *base, uint32_t i) {
     return x;
 }
 
-// A membership test of one hash on the C columns of a lane, from the two
-// candidate buckets loaded beforehand (v1, v2).
-template <int C>
-__device__ inline void member(uint64_t h, const ulonglong2 (&v1)[C], const ulonglong2 (&v2)[C], bool (&alive)[C]) {
-    // bitwise, not short-circuit: the four compares become lane masks
-#pragma unroll
-    for (int q = 0; q < C; ++q)
-        alive[q] = alive[q] & ((v1[q].x == h) | (v1[q].y == h) | (v2[q].x == h) | (v2[q].y == h));
-}
+// Lane masks of a wavefront: ballot turns a per-lane predicate into a
+// uniform 64-bit mask (held in scalar registers), in_mask reads a lane's
+// bit back as a predicate.  Per-column "alive" and "need" sets are kept as
+// masks so that their tests and combinations are scalar operations.
+using lmask = uint64_t;
 
+__device__ inline lmask ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+__device__ inline bool in_mask(lmask m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
+
+// The two candidate buckets of one hash on the C columns of a lane.
 template <int C>
-__device__ inline void load_buckets(const uint64_t *const (&col)[C], const Table &t, uint32_t b1, uint32_t b2,
-                                    const bool (&go)[C], ulonglong2 (&v1)[C], ulonglong2 (&v2)[C]) {
+struct Buckets {
+    ulonglong2 v1[C], v2[C];
+};
+
+// Load the buckets at element offsets row1 / row2 of each column, on the
+// lanes in go[q] only (zero elsewhere: no key is 0).
+template <int C>
+__device__ inline void load_buckets(const uint64_t *const (&col)[C], uint64_t row1, uint64_t row2,
+                                    const lmask (&go)[C], Buckets<C> &b) {
 #pragma unroll
     for (int q = 0; q < C; ++q) {
-        v1[q] = make_ulonglong2(0, 0);
-        v2[q] = make_ulonglong2(0, 0);
-        if (go[q]) {
-            v1[q] = *(const ulonglong2 *)(col[q] + (uint64_t)b1 * t.pitch * 2);
-            v2[q] = *(const ulonglong2 *)(col[q] + (uint64_t)b2 * t.pitch * 2);
+        b.v1[q] = make_ulonglong2(0, 0);
+        b.v2[q] = make_ulonglong2(0, 0);
+        if (in_mask(go[q])) {
+            b.v1[q] = *(const ulonglong2 *)(col[q] + row1);
+            b.v2[q] = *(const ulonglong2 *)(col[q] + row2);
         }
     }
 }
 
-// First-miss scan of one request's run on the C columns of every lane of a
-// wavefront, for the columns in need[], starting at block `start` (uniform,
-// < n) whose hash h0 and candidate buckets (v1_0, v2_0) were loaded
-// beforehand.  Past the first block, W blocks are tested per step with all
-// their bucket loads issued together.  j[] holds, for the columns in need,
-// `start` on entry and the first-miss index on return.
+// A membership test of h (nonzero) on the C columns: alive[q] keeps the
+// lanes whose column holds h in one of its two buckets.
+template <int C>
+__device__ inline void member(uint64_t h, const Buckets<C> &b, lmask (&alive)[C]) {
+#pragma unroll
+    for (int q = 0; q < C; ++q)
+        alive[q] &= ballot(b.v1[q].x == h) | ballot(b.v1[q].y == h) | ballot(b.v2[q].x == h) |
+                    ballot(b.v2[q].y == h);
+}
+
+// First-miss scan of one request's run on the columns in alive[] (the
+// columns that need it), starting at block `start` (uniform, < n) whose hash
+// h0 and buckets b0 were loaded beforehand.  Past the first block, W blocks
+// are tested per step with all their bucket loads issued together.  j[]
+// holds `start` on entry for those columns and the first-miss index on
+// return.
 template <int W, int C>
-__device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &t, cptr<uint64_t> run, uint32_t n,
-                                  uint32_t start, const bool (&need)[C], uint32_t (&j)[C], uint64_t h0,
-                                  const ulonglong2 (&v1_0)[C], const ulonglong2 (&v2_0)[C]) {
-    bool alive[C];
+__device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &t, uint64_t rs, cptr<uint64_t> run,
+                                  uint32_t n, uint32_t start, lmask (&alive)[C], uint32_t (&j)[C], uint64_t h0,
+                                  const Buckets<C> &b0) {
+    member<C>(h0, b0, alive);
 #pragma unroll
-    for (int q = 0; q < C; ++q) alive[q] = need[q];
-    member<C>(h0, v1_0, v2_0, alive);
-#pragma unroll
-    for (int q = 0; q < C; ++q) j[q] += alive[q] ? 1u : 0u;
+    for (int q = 0; q < C; ++q) j[q] += in_mask(alive[q]) ? 1u : 0u;
     for (uint32_t i0 = start + 1; i0 < n; i0 += W) {
-        bool any = false;
+        lmask any = 0;
 #pragma unroll
-        for (int q = 0; q < C; ++q) any = any || alive[q];
-        if (!__any(any)) break;
+        for (int q = 0; q < C; ++q) any |= alive[q];
+        if (!any) break;
         uint64_t h[W];
         if (i0 + W <= n) {
 #pragma unroll
@@ -454,29 +470,40 @@ __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &
 #pragma unroll
             for (int w = 0; w < W; ++w) h[w] = i0 + w < n ? run[i0 + w] : 0;
         }
-        ulonglong2 v1[W][C], v2[W][C];
+        Buckets<C> bw[W];
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             uint32_t b1, b2;
             buckets_of(h[w], t.shift, b1, b2);
+            lmask go[C];
 #pragma unroll
-            for (int q = 0; q < C; ++q) {
-                v1[w][q] = make_ulonglong2(0, 0);
-                v2[w][q] = make_ulonglong2(0, 0);
-                if (alive[q] && i0 + w < n) {
-                    v1[w][q] = *(const ulonglong2 *)(col[q] + (uint64_t)b1 * t.pitch * 2);
-                    v2[w][q] = *(const ulonglong2 *)(col[q] + (uint64_t)b2 * t.pitch * 2);
-                }
-            }
+            for (int q = 0; q < C; ++q) go[q] = i0 + w < n ? alive[q] : 0;
+            load_buckets<C>(col, (uint64_t)b1 * rs, (uint64_t)b2 * rs, go, bw[w]);
         }
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             if (i0 + w >= n) break;
-            member<C>(h[w], v1[w], v2[w], alive);
+            member<C>(h[w], bw[w], alive);
 #pragma unroll
-            for (int q = 0; q < C; ++q) j[q] += alive[q] ? 1u : 0u;
+            for (int q = 0; q < C; ++q) j[q] += in_mask(alive[q]) ? 1u : 0u;
         }
     }
+}
+
+// What one scan step fetches for the next request: its congestion row
+// (seconds per token and tier per column) and the buckets of its first test.
+template <int C>
+struct Ahead {
+    float spt[C];
+    uint32_t tau[C];
+    Buckets<C> bk;
+};
+
+// Tier latency by a per-lane tier index, without indexing an array.
+__device__ inline float tier_latency(const Snap &s, uint32_t tau) {
+    const float lo = (tau & 1u) ? s.lat[1] : s.lat[0];
+    const float hi = (tau & 1u) ? s.lat[3] : s.lat[2];
+    return (tau & 2u) ? hi : lo;
 }
 
 // One wavefront per (run of sorted requests, group of 64*C decodes); lane l
@@ -485,8 +512,9 @@ __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &
 // where the common leading run decides it), non-cached bytes, feasibility
 // and cost (Eqs. (2)-(7)), then the group's K best feasible (score, index)
 // keys into partial[group][sorted position][0..K).  Request records are
-// fetched two requests ahead, and the congestion row and the first probe
-// row one request ahead.
+// fetched two requests ahead, and the congestion row and the first test's
+// buckets one request ahead into the other of two buffers (the loop is
+// unrolled by two so that neither buffer is copied).
 template <int K, int W, int C, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec *__restrict__ rec,
                                                       const uint64_t *__restrict__ hashes,
@@ -494,16 +522,29 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
                                                       uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
                                                       uint64_t *__restrict__ partial, PairOut po) {
     const uint32_t lane = threadIdx.x % kWave;
-    const uint32_t gw = blockIdx.x * kWavesPerBlock + wave_index();
-    const uint32_t run = gw / ngroup, grp = gw % ngroup;
+    uint32_t run, grp;
+    if (ngroup % kXcds == 0) {
+        // workgroups go to the XCDs in turn: XCD x takes groups
+        // [x*gx, (x+1)*gx), so its decodes' congestion columns stay in its
+        // own L2; the waves of a workgroup take consecutive runs of one group
+        const uint32_t gx = ngroup / kXcds, x = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
+        grp = x * gx + k % gx;
+        run = (k / gx) * kWavesPerBlock + wave_index();
+    } else {
+        const uint32_t gw = blockIdx.x * kWavesPerBlock + wave_index();
+        run = gw / ngroup;
+        grp = gw % ngroup;
+    }
     if (run >= n_runs) return;
     const uint32_t nv = *n_valid;
     const uint32_t i0 = run * run_len;
     if (i0 >= nv) return;
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
     const uint32_t base = grp * (kWave * C);
-    uint32_t d[C];
+    const uint64_t rs = 2ull * t.pitch;   // elements per bucket row
+    uint32_t d[C], pcol[C];
     bool act[C];
+    lmask actm[C];
     const uint64_t *col[C];
     float dload[C];
     uint64_t xlim[C];
@@ -511,61 +552,70 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
         act[q] = d[q] < s.D;
-        col[q] = t.keys + 2 * (uint64_t)(act[q] ? d[q] : 0);
+        actm[q] = ballot(act[q]);
+        pcol[q] = act[q] ? d[q] : 0;
+        col[q] = t.keys + 2 * (uint64_t)pcol[q];
         dload[q] = act[q] ? s.dbase[d[q]] : 0.0f;
         xlim[q] = act[q] ? s.dxlim[d[q]] : 0;
     }
     const cptr<uint64_t> chash = as_const(hashes);
     Rec c0 = load_rec(rec, i0);
     Rec c1 = load_rec(rec, i0 + 1 < i1 ? i0 + 1 : i0);
-    float2 pc0[C];
+    Ahead<C> A, B;
 #pragma unroll
-    for (int q = 0; q < C; ++q) pc0[q] = s.pcon[(uint64_t)c0.p * s.D + (act[q] ? d[q] : 0)];
-    // first membership test of the current request (block L0), loaded ahead;
-    // t0: whether it is needed at all (not when the filter rules block L0 out
-    // on every decode)
+    for (int q = 0; q < C; ++q) {
+        A.spt[q] = s.spt[(uint64_t)c0.p * s.D + pcol[q]];
+        A.tau[q] = s.tier_map[(uint64_t)c0.p * s.D + pcol[q]];
+    }
+    // first test of the current request: block L0 (0 for the run's first);
+    // t0 says whether it is needed at all (not when the cache filter rules
+    // the block out on every decode)
     uint32_t L0 = 0;
     bool t0 = c0.n != 0;
-    uint64_t h0 = c0.n ? chash[c0.a] : 0;
-    ulonglong2 v10[C], v20[C];
+    uint64_t h0 = t0 ? chash[c0.a] : 0;
     {
         uint32_t b1, b2;
         buckets_of(h0, t.shift, b1, b2);
-        bool go[C];
+        lmask go[C];
 #pragma unroll
-        for (int q = 0; q < C; ++q) go[q] = act[q] && c0.n != 0;
-        load_buckets<C>(col, t, b1, b2, go, v10, v20);
+        for (int q = 0; q < C; ++q) go[q] = t0 ? actm[q] : 0;
+        load_buckets<C>(col, (uint64_t)b1 * rs, (uint64_t)b2 * rs, go, A.bk);
     }
     uint32_t j_prev[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) j_prev[q] = 0;
-    for (uint32_t i = i0; i < i1; ++i) {
+
+    auto step = [&](uint32_t i, const Ahead<C> &cur, Ahead<C> &nxt) {
         const Rec c2 = load_rec(rec, i + 2 < i1 ? i + 2 : i1 - 1);
-        float2 pc1[C];
 #pragma unroll
-        for (int q = 0; q < C; ++q) pc1[q] = s.pcon[(uint64_t)c1.p * s.D + (act[q] ? d[q] : 0)];
+        for (int q = 0; q < C; ++q) {
+            nxt.spt[q] = s.spt[(uint64_t)c1.p * s.D + pcol[q]];
+            nxt.tau[q] = s.tier_map[(uint64_t)c1.p * s.D + pcol[q]];
+        }
         const uint32_t L1 = c1.lcp;
         const bool more = i + 1 < i1 && L1 < c1.n && c1.gp;
         const uint64_t h1 = more ? c1.hf : 0;
-        const uint32_t b11 = c1.b1, b21 = c1.b2;
-        // the next request's first test is needed on a column iff its
-        // first-miss index after this request is >= L1; a column that carries
-        // this request (j_prev < L0) keeps j_prev, so it is known now
-        bool go1[C];
+        {
+            // the next request's first test is needed on a column iff its
+            // first-miss index after this request is >= L1; a column that
+            // carries this request (j_prev < L0) keeps j_prev, so
+            // j_prev >= min(L0, L1) covers every column that can need it
+            const uint32_t lo = L0 < L1 ? L0 : L1;
+            lmask go[C];
 #pragma unroll
-        for (int q = 0; q < C; ++q) go1[q] = act[q] && more && (j_prev[q] >= L0 || j_prev[q] >= L1);
-        ulonglong2 v11[C], v21[C];
-        load_buckets<C>(col, t, b11, b21, go1, v11, v21);
+            for (int q = 0; q < C; ++q) go[q] = more ? ballot(j_prev[q] >= lo) & actm[q] : 0;
+            load_buckets<C>(col, (uint64_t)c1.b1 * rs, (uint64_t)c1.b2 * rs, go, nxt.bk);
+        }
         // prefix lengths: carried where the common leading run decides them
         uint32_t j[C];
-        bool need[C];
+        lmask need[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) {
             const bool carry = j_prev[q] < L0;
             j[q] = carry ? j_prev[q] : L0;
-            need[q] = act[q] && !carry;
+            need[q] = ballot(!carry) & actm[q];
         }
-        if (t0) probe_from<W, C>(col, t, chash + c0.a, c0.n, L0, need, j, h0, v10, v20);
+        if (t0) probe_from<W, C>(col, t, rs, chash + c0.a, c0.n, L0, need, j, h0, cur.bk);
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t cb[C];
 #pragma unroll
@@ -573,7 +623,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             j_prev[q] = j[q];
             const uint32_t x = c0.len - s.block_tokens * j[q];
             const bool feas = (uint64_t)x < xlim[q];
-            const float cost = pair_score(x, pc0[q].x, pc0[q].y, dload[q]);
+            const float cost = pair_score(x, cur.spt[q], tier_latency(s, cur.tau[q] & 3u), dload[q]);
             if (PAIRS && act[q]) {
                 const uint64_t o = (uint64_t)c0.r * s.D + d[q];
                 if (po.j) po.j[o] = (uint16_t)j[q];
@@ -596,7 +646,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             uint32_t dm = 0;
 #pragma unroll
             for (int q = 0; q < C; ++q) {
-                const uint64_t m = __ballot(cb[q] == mn);
+                const lmask m = ballot(cb[q] == mn);
                 if (m) {
                     const uint32_t l = (uint32_t)__builtin_ctzll(m);
                     dm = base + q * kWave + l;
@@ -609,15 +659,14 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         if (lane < (uint32_t)K) partial[((uint64_t)grp * n_req + i) * K + lane] = mine;
         c0 = c1;
         c1 = c2;
-#pragma unroll
-        for (int q = 0; q < C; ++q) {
-            pc0[q] = pc1[q];
-            v10[q] = v11[q];
-            v20[q] = v21[q];
-        }
         L0 = L1;
         h0 = h1;
         t0 = more;
+    };
+    for (uint32_t i = i0; i < i1; i += 2) {
+        step(i, A, B);
+        if (i + 1 >= i1) break;
+        step(i + 1, B, A);
     }
 }
 
@@ -1021,7 +1070,7 @@ struct netkv_ctx {
     uint32_t *queue = nullptr;
     uint32_t *batch = nullptr;
     uint64_t *adm_prev = nullptr;
-    float2 *pcon = nullptr;      // derived per call: [P*D]
+    float *spt = nullptr;        // derived per call: [P*D]
     float *dbase = nullptr;      // [D]
     uint64_t *dxlim = nullptr;   // [D]
     float bw[4] = {0, 0, 0, 0}, lat[4] = {0, 0, 0, 0};
@@ -1172,7 +1221,7 @@ Snap make_snap(netkv_handle h) {
     s.block_tokens = h->block_tokens;
     s.P = h->P;
     s.D = h->D;
-    s.pcon = h->pcon;
+    s.spt = h->spt;
     s.dbase = h->dbase;
     s.dxlim = h->dxlim;
     s.policy = h->policy_opt;
@@ -1251,14 +1300,14 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
     return NETKV_OK;
 }
 
-uint32_t auto_run_len(uint64_t R, uint32_t ngroup, uint32_t C) {
-    // runs of 384 sorted requests (256 at 4 decodes per lane), shortened
-    // while that leaves fewer than 16K wavefronts (measured on MI355X: longer
-    // runs carry more first-miss indices, shorter ones keep more wavefronts
-    // in flight)
-    const uint64_t base = C >= 4 ? 256 : 384;
-    uint64_t rl = base;
-    if (R * ngroup < base * 16384) rl = (R * ngroup) / 16384;
+uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
+    // runs of 256 sorted requests on large batches (R * groups >= 2^24), else
+    // 512, shortened while that leaves fewer than 8K wavefronts (measured on
+    // MI355X: longer runs carry more first-miss indices, shorter ones keep
+    // more wavefronts in flight)
+    const uint64_t work = R * ngroup;
+    uint64_t rl = work >= (1ull << 24) ? 256 : 512;
+    if (rl > work / 8192) rl = work / 8192;
     if (rl < 8) rl = 8;
     return (uint32_t)rl;
 }
@@ -1275,8 +1324,12 @@ void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &or
                  uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po, bool pairs,
                  hipStream_t st) {
     constexpr int W = C >= 4 ? 1 : C == 2 ? 2 : kSpec;
-    const uint64_t waves = (uint64_t)n_runs * ngroup;
-    const uint32_t grid = (uint32_t)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    // one workgroup per (kWavesPerBlock runs, group) when the groups split
+    // evenly over the XCDs (see scan_kernel), else per kWavesPerBlock waves
+    const uint64_t grid64 = ngroup % kXcds == 0
+                                ? (uint64_t)((n_runs + kWavesPerBlock - 1) / kWavesPerBlock) * ngroup
+                                : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
+    const uint32_t grid = (uint32_t)grid64;
     if (pairs)
         hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
                            ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
@@ -1320,7 +1373,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     const Table t = make_table(h);
     const Reqs rq = make_reqs(req);
     const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
-    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->pcon, h->dbase,
+    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->spt, h->dbase,
                        h->dxlim);
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 16 * kWavesPerBlock - 1) / (16 * kWavesPerBlock))),
                        dim3(kBlock), 0, st, sn, rq, h->keys_in, h->vals_in, h->errword);
@@ -1333,7 +1386,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
                        (const uint32_t *)h->n_valid, t, h->reuse_opt, h->rec);
     HIPCHK(h, hipGetLastError());
-    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup, C);
+    const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{h->perm, h->rec, h->n_valid};
     if (K == 1)
@@ -1388,7 +1441,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->queue);
         dfree(h->batch);
         dfree(h->adm_prev);
-        dfree(h->pcon);
+        dfree(h->spt);
         dfree(h->dbase);
         dfree(h->dxlim);
         dfree(h->table);
@@ -1477,9 +1530,9 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
                     (bad & 2) ? " util outside [0,1) or NaN" : "", (bad & 4) ? " batch_size > beta_max" : "");
     }
     if (!h->have_snap || h->P != P || h->D != D) {
-        dfree(h->pcon); dfree(h->dbase); dfree(h->dxlim);
+        dfree(h->spt); dfree(h->dbase); dfree(h->dxlim);
         h->have_snap = false;
-        if (dalloc(h->pcon, npd) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
+        if (dalloc(h->spt, npd) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
             dalloc(h->dxlim, D) != hipSuccess) {
             cleanup();
             return fail(h, NETKV_ENOMEM, "snapshot allocation failed");
