@@ -295,85 +295,118 @@ struct Order {
     const uint32_t *n_valid;  // valid requests (they sort first)
 };
 
-// Validate each request and build its sort key.  One wavefront handles 16
-// requests in turn; lanes scan the hash run for the reserved value 0.
-__global__ __launch_bounds__(kBlock) void prep_kernel(Snap s, Reqs rq, uint32_t *__restrict__ keys,
-                                                      uint32_t *__restrict__ vals, uint32_t *__restrict__ err) {
-    const uint32_t lane = threadIdx.x % kWave;
-    const uint32_t w = blockIdx.x * kWavesPerBlock + wave_index();
-    uint32_t flags = 0;
-    for (uint32_t q = 0; q < 16; ++q) {
-        const uint32_t r = w * 16 + q;
-        if (r >= rq.n_req) break;
+// Validate each request and build its sort key, one thread per request.
+// The reserved hash value 0 is looked for separately: a flat scan of the
+// batch's hash array (count_zero_kernel) raises `zflag`, and only then does
+// zero_fix_kernel check each request's run and invalidate those holding it.
+// Thread 0 clears zflag for that scan.
+__global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t *__restrict__ keys,
+                                                   uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
+                                                   uint32_t *__restrict__ zflag) {
+    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r == 0) *zflag = 0;
+    bool bad = false;
+    if (r < rq.n_req) {
         uint32_t p, len, n;
         uint64_t a;
-        bool ok = request_ok(rq, s, r, p, len, a, n);
-        bool zero = false;
-        if (ok)
-            for (uint32_t i = lane; i < n; i += kWave) zero |= rq.hashes[a + i] == 0;
-        const bool bad_hash = __any(zero);
-        const bool good = ok && !bad_hash;
-        if (!ok) flags |= kErrRequest;
-        else if (bad_hash) flags |= kErrZeroHash;
-        if (lane == 0) {
-            uint32_t key = kKeyInvalid;
-            if (good) {
-                if (n == 0) {
-                    key = kKeyEmptyRun;
-                } else {
-                    uint64_t h0 = rq.hashes[a];
-                    uint32_t top = (uint32_t)((h0 * kGolden) >> 32);
-                    key = ((top >> 13) << 12) | (n < 4095u ? n : 4095u);
-                }
+        const bool ok = request_ok(rq, s, r, p, len, a, n);
+        uint32_t key = kKeyInvalid;
+        if (ok) {
+            if (n == 0) {
+                key = kKeyEmptyRun;
+            } else {
+                const uint32_t top = (uint32_t)((rq.hashes[a] * kGolden) >> 32);
+                key = ((top >> 13) << 12) | (n < 4095u ? n : 4095u);
             }
-            keys[r] = key;
-            vals[r] = r;
         }
+        keys[r] = key;
+        vals[r] = r;
+        bad = !ok;
     }
-    if (flags && lane == 0) atomicOr(err, flags);
+    if (__ballot(bad) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrRequest);
 }
 
-// Number of valid requests = position of the first invalid key in sorted order.
-__global__ void count_valid_kernel(const uint32_t *__restrict__ sorted_keys, uint32_t n, uint32_t *__restrict__ out) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    uint32_t lo = 0, hi = n;
-    while (lo < hi) {
-        uint32_t mid = lo + (hi - lo) / 2;
-        if (sorted_keys[mid] < kKeyInvalid) lo = mid + 1;
-        else hi = mid;
+// Requests whose run holds the value 0 become invalid (only when the flat
+// scan found a 0 somewhere; otherwise every wavefront returns at once).
+// Wavefronts take 16 requests at a time, lanes stride over each run.
+__global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint32_t *__restrict__ keys,
+                                                          const uint32_t *__restrict__ zflag,
+                                                          uint32_t *__restrict__ err) {
+    if (*zflag == 0) return;
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t nw = gridDim.x * kWavesPerBlock;
+    bool found = false;
+    for (uint32_t w = blockIdx.x * kWavesPerBlock + wave_index(); w * 16 < rq.n_req; w += nw) {
+        for (uint32_t q = 0; q < 16; ++q) {
+            const uint32_t r = w * 16 + q;
+            if (r >= rq.n_req) break;
+            uint32_t p, len, n;
+            uint64_t a;
+            if (!request_ok(rq, s, r, p, len, a, n)) continue;
+            bool zero = false;
+            for (uint32_t i = lane; i < n; i += kWave) zero |= rq.hashes[a + i] == 0;
+            if (__any(zero)) {
+                if (lane == 0) keys[r] = kKeyInvalid;
+                found = true;
+            }
+        }
     }
-    *out = lo;
+    if (found && lane == 0) atomicOr(err, kErrZeroHash);
 }
 
 // Record of each sorted request, with its common leading blocks with the
-// previous sorted request.
+// previous sorted request: G lanes per sorted position (G divides 64)
+// compare G blocks per step, their loads issued together.  Also stores the
+// number of valid requests (valid keys sort first): the last valid position
+// writes it, or position 0 writes 0.
+template <uint32_t G>
 __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
-                                                  const uint32_t *__restrict__ n_valid, Table t, uint32_t reuse,
-                                                  Rec *__restrict__ rec) {
-    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= *n_valid) return;
+                                                  const uint32_t *__restrict__ sorted_keys, Table t, uint32_t reuse,
+                                                  Rec *__restrict__ rec, uint32_t *__restrict__ n_valid) {
+    const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t sub = threadIdx.x % G;
+    const uint32_t seg = (threadIdx.x % kWave) - sub;   // first lane of this position's lanes
+    const uint64_t i = tid / G;
+    if (i >= rq.n_req) return;
+    const bool valid = sorted_keys[i] < kKeyInvalid;
+    if (sub == 0) {
+        if (valid && (i + 1 == rq.n_req || sorted_keys[i + 1] >= kKeyInvalid)) *n_valid = (uint32_t)(i + 1);
+        if (i == 0 && !valid) *n_valid = 0;
+    }
+    if (!valid) return;
     const uint32_t r = perm[i];
     const uint64_t a = rq.off[r];
     const uint64_t nr = rq.off[r + 1] - a;
-    uint32_t l = 0;
+    uint64_t l = 0;
     if (i > 0 && reuse) {
         const uint32_t q = perm[i - 1];
         const uint64_t b = rq.off[q];
         const uint64_t nq = rq.off[q + 1] - b;
         const uint64_t m = nr < nq ? nr : nq;
-        while (l < m && rq.hashes[a + l] == rq.hashes[b + l]) ++l;
+        l = m;
+        for (uint64_t base = 0; base < m; base += G) {
+            const uint64_t x = base + sub;
+            const bool stop = x >= m || rq.hashes[a + x] != rq.hashes[b + x];
+            const uint32_t bits = (uint32_t)(__ballot(stop) >> seg) & (uint32_t)((1ull << G) - 1);
+            if (bits) {
+                const uint64_t first = base + (uint64_t)__builtin_ctz(bits);
+                l = first < m ? first : m;
+                break;
+            }
+        }
     }
-    Rec x;
-    x.r = r;
-    x.p = rq.prefill[r];
-    x.len = rq.len[r];
-    x.n = (uint32_t)nr;
-    x.lcp = l;
-    x.a = a;
-    x.hf = l < nr ? rq.hashes[a + l] : 0;
-    buckets_of(x.hf, t.shift, x.b1, x.b2);
-    x.gp = l < nr && maybe_anywhere(t.any, t.any_shift, x.hf) ? 1u : 0u;
-    rec[i] = x;
+    if (sub != 0) return;
+    Rec o;
+    o.r = r;
+    o.p = rq.prefill[r];
+    o.len = rq.len[r];
+    o.n = (uint32_t)nr;
+    o.lcp = (uint32_t)l;
+    o.a = a;
+    o.hf = l < nr ? rq.hashes[a + l] : 0;
+    buckets_of(o.hf, t.shift, o.b1, o.b2);
+    o.gp = l < nr && maybe_anywhere(t.any, t.any_shift, o.hf) ? 1u : 0u;
+    rec[i] = o;
 }
 
 // Read-only data that is uniform across a wavefront (request records, hash
@@ -1089,6 +1122,7 @@ struct netkv_ctx {
     // scratch
     uint32_t *errword = nullptr;          // request / selection errors (sticky)
     uint32_t *loadword = nullptr;         // validation flags of the load calls
+    uint32_t *zflag = nullptr;            // a batch hash array holds the value 0
     uint16_t *jT = nullptr;
     uint64_t jT_bytes = 0;
     int32_t *base_idx = nullptr;
@@ -1266,7 +1300,12 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-constexpr int kSpec = 4;   // home-slot loads issued together per probe step
+constexpr int kSpec = 4;            // blocks tested together per extension step at one decode per lane
+constexpr uint32_t kLcpLanes = 8;   // lanes per sorted position in lcp_kernel
+
+// Radix sort configuration of the batch-order keys (rocPRIM's own choice of
+// algorithm by size).
+using SortConfig = rocprim::default_config;
 
 netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, hipStream_t st) {
     if (R > h->order_cap) {
@@ -1279,8 +1318,8 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
             dalloc(h->rec, R) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
         size_t bytes = 0;
-        if (rocprim::radix_sort_pairs(nullptr, bytes, h->keys_in, h->keys_out, h->vals_in, h->perm, (uint32_t)R, 0,
-                                      32, st) != hipSuccess)
+        if (rocprim::radix_sort_pairs<SortConfig>(nullptr, bytes, h->keys_in, h->keys_out, h->vals_in, h->perm,
+                                                  (uint32_t)R, 0, 32, st) != hipSuccess)
             return fail(h, NETKV_EDEVICE, "sort size query failed");
         uint8_t *tmp = nullptr;
         if (dalloc(tmp, std::max<size_t>(bytes, 16)) != hipSuccess)
@@ -1375,16 +1414,20 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
     hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->spt, h->dbase,
                        h->dxlim);
-    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 16 * kWavesPerBlock - 1) / (16 * kWavesPerBlock))),
-                       dim3(kBlock), 0, st, sn, rq, h->keys_in, h->vals_in, h->errword);
+    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, h->keys_in,
+                       h->vals_in, h->errword, h->zflag);
+    if (rq.n_hashes)
+        hipLaunchKernelGGL(count_zero_kernel, dim3(grid_for(rq.n_hashes, 256, 8192)), dim3(256), 0, st, rq.hashes,
+                           rq.n_hashes, h->zflag);
+    hipLaunchKernelGGL(zero_fix_kernel, dim3(grid_for((R + 15) / 16, kWavesPerBlock, 2048)), dim3(kBlock), 0, st,
+                       sn, rq, h->keys_in, (const uint32_t *)h->zflag, h->errword);
     HIPCHK(h, hipGetLastError());
     size_t tb = h->sort_tmp_bytes;
-    HIPCHK(h, rocprim::radix_sort_pairs(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm, (uint32_t)R, 0,
-                                        32, st));
-    hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(64), 0, st, (const uint32_t *)h->keys_out, (uint32_t)R,
+    HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
+                                                    (uint32_t)R, 0, 32, st));
+    hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
+                       (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->rec,
                        h->n_valid);
-    hipLaunchKernelGGL(lcp_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, rq, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->n_valid, t, h->reuse_opt, h->rec);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
@@ -1421,6 +1464,7 @@ netkv_status netkv_create(netkv_handle *out, int device) {
     h->device = device;
     DeviceGuard g(device);
     if (dalloc(h->errword, 1) != hipSuccess || dalloc(h->loadword, 1) != hipSuccess ||
+        dalloc(h->zflag, 1) != hipSuccess ||
         hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess) {
         netkv_destroy(h);
         return NETKV_EDEVICE;
@@ -1448,6 +1492,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->any);
         dfree(h->errword);
         dfree(h->loadword);
+        dfree(h->zflag);
         dfree(h->jT);
         dfree(h->base_idx);
         dfree(h->base_score);
@@ -1974,8 +2019,8 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     hipLaunchKernelGGL(prefill_key_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s, rq, (uint32_t)P,
                        (const uint32_t *)h->keys_in, h->seq_keys, h->seq_vals);
     size_t tb = h->sort_tmp_bytes;
-    HIPCHK(h, rocprim::radix_sort_pairs(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals, h->seq_perm,
-                                        (uint32_t)R, 0, 32, s));
+    HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals,
+                                                    h->seq_perm, (uint32_t)R, 0, 32, s));
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_start, P, 0u);
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_end, P, 0u);
     hipLaunchKernelGGL(segment_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s,
