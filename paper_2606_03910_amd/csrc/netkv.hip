@@ -1084,6 +1084,132 @@ __global__ __launch_bounds__(kSeqThreads) void sequential_kernel(Snap s, uint32_
     }
 }
 
+// One of four uniform values by a per-lane index, without indexing an array.
+__device__ inline float pick4(const float (&v)[4], uint32_t t) {
+    const float lo = (t & 1u) ? v[1] : v[0];
+    const float hi = (t & 1u) ? v[3] : v[2];
+    return (t & 2u) ? hi : lo;
+}
+
+// The same chain with each thread's decodes (d = thread + T*k, k < MAXC)
+// held in registers: tier (2 bits each in one word), seconds per token,
+// tier latency plus load term, and the feasibility limit (32 bits, with a
+// bit for limits of 2^32 and more, which every x meets).  Between requests
+// only the factors of the tier whose counter grew change, and they are
+// recomputed with the same expression.  The next request's prefix lengths
+// are loaded a request ahead into the other of two buffers; the waves'
+// minima go to alternating LDS slots and every thread picks the winner, so
+// one barrier per request suffices (a wave can write a slot again only after
+// the barrier that follows every wave's reading of it).
+template <int T, int MAXC>
+__global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, uint32_t cap, const uint16_t *__restrict__ jm,
+                                                              const uint32_t *__restrict__ len,
+                                                              const uint32_t *__restrict__ order,
+                                                              const uint32_t *__restrict__ start,
+                                                              const uint32_t *__restrict__ end,
+                                                              int32_t *__restrict__ out_idx,
+                                                              float *__restrict__ out_score) {
+    static_assert(MAXC <= 16, "two tier bits per decode in one word");
+    constexpr int NW = T / kWave;
+    __shared__ uint32_t slot_c[2][NW], slot_d[2][NW];
+    const uint32_t p = blockIdx.x;
+    const uint32_t i0 = start[p], i1 = end[p];
+    if (i0 >= i1) return;
+    const uint32_t lane = threadIdx.x % kWave, wave = wave_index();
+    const uint64_t row = (uint64_t)p * s.D;
+    float n_tier[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) n_tier[t] = (float)s.n_inflight[t * s.P + p];
+    uint32_t tmask = 0, big = 0;
+    float sk[MAXC], lk[MAXC];
+    uint32_t xk[MAXC];
+#pragma unroll
+    for (int k = 0; k < MAXC; ++k) {
+        const uint32_t d = threadIdx.x + T * k;
+        const bool ok = d < s.D;
+        const uint32_t dd = ok ? d : 0;
+        const uint32_t t = s.tier_map[row + dd] & 3u;
+        tmask |= t << (2 * k);
+        sk[k] = sec_per_token_n(s, t, pick4(n_tier, t), s.util[row + dd]);
+        lk[k] = tier_latency(s, t) + s.dbase[dd];
+        const uint64_t xl = ok ? s.dxlim[dd] : 0;   // 0: never feasible, so never chosen
+        xk[k] = xl > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)xl;
+        big |= (xl > 0xFFFFFFFFull ? 1u : 0u) << k;
+    }
+    auto load_j = [&](uint32_t r, uint16_t (&jj)[MAXC]) {
+#pragma unroll
+        for (int k = 0; k < MAXC; ++k) {
+            const uint32_t d = threadIdx.x + T * k;
+            jj[k] = d < s.D ? jm[(uint64_t)r * s.D + d] : 0;
+        }
+    };
+    // score request r (prefix lengths jc), choose, count the choice
+    auto step = [&](uint32_t i, uint32_t r, const uint16_t (&jc)[MAXC]) {
+        const uint32_t l = len[r];
+        uint32_t lb = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
+#pragma unroll
+        for (int k = 0; k < MAXC; ++k) {
+            const uint32_t x = l - s.block_tokens * jc[k];
+            if (x < xk[k] || ((big >> k) & 1u)) {
+                const uint32_t cbits = __float_as_uint(fmaf((float)x, sk[k], lk[k]));
+                if (cbits < lb) {   // d grows with k: the first strict minimum wins ties
+                    lb = cbits;
+                    ld = threadIdx.x + T * k;
+                }
+            }
+        }
+        const uint32_t mn = wave_min_u32_dpp(lb);
+        const uint32_t dm = wave_min_u32_dpp(lb == mn ? ld : 0xFFFFFFFFu);
+        const uint32_t b = i & 1u;
+        if (lane == 0) {
+            slot_c[b][wave] = mn;
+            slot_d[b][wave] = dm;
+        }
+        __syncthreads();
+        uint32_t bc = slot_c[b][0], bd = slot_d[b][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            const uint32_t c = slot_c[b][w], dw = slot_d[b][w];
+            if (c < bc || (c == bc && dw < bd)) {
+                bc = c;
+                bd = dw;
+            }
+        }
+        if (threadIdx.x == 0) {
+            out_idx[r] = bc == 0xFFFFFFFFu ? -1 : (int32_t)bd;
+            out_score[r] = bc == 0xFFFFFFFFu ? __builtin_inff() : __uint_as_float(bc);
+        }
+        if (bc != 0xFFFFFFFFu) {
+            const uint32_t tw = s.tier_map[row + bd] & 3u;
+            const float nw = pick4(n_tier, tw);
+            if (nw < (float)cap) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if ((uint32_t)t == tw) n_tier[t] = nw + 1.0f;
+#pragma unroll
+                for (int k = 0; k < MAXC; ++k) {
+                    const uint32_t d = threadIdx.x + T * k;
+                    if (((tmask >> (2 * k)) & 3u) == tw && d < s.D)
+                        sk[k] = sec_per_token_n(s, tw, nw + 1.0f, s.util[row + d]);
+                }
+            }
+        }
+    };
+    uint16_t ja[MAXC], jb[MAXC];
+    uint32_t r = order[i0];
+    load_j(r, ja);
+    for (uint32_t i = i0; i < i1; i += 2) {
+        const uint32_t r1 = i + 1 < i1 ? order[i + 1] : r;
+        if (i + 1 < i1) load_j(r1, jb);
+        step(i, r, ja);
+        if (i + 1 >= i1) break;
+        const uint32_t r2 = i + 2 < i1 ? order[i + 2] : r1;
+        if (i + 2 < i1) load_j(r2, ja);
+        step(i + 1, r1, jb);
+        r = r2;
+    }
+}
+
 }  // namespace
 
 // ====================================================================== host side
@@ -2027,9 +2153,21 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
                        (const uint32_t *)h->seq_keys_out, (uint32_t)R, (uint32_t)P, h->seq_start, h->seq_end);
     HIPCHK(h, hipGetLastError());
     HIPCHK(h, time_begin(h, s));
-    hipLaunchKernelGGL(sequential_kernel, dim3((uint32_t)P), dim3(kSeqThreads), 0, s, make_snap(h), (uint32_t)R, cap,
-                       (const uint16_t *)h->seq_j, req->len_tokens, (const uint32_t *)h->seq_perm,
-                       (const uint32_t *)h->seq_start, (const uint32_t *)h->seq_end, out_idx, out_score);
+    const Snap sn = make_snap(h);
+    const uint16_t *jm = h->seq_j;
+    const uint32_t *ord = h->seq_perm, *b0 = h->seq_start, *b1 = h->seq_end;
+    if (h->D <= 512u * 4)
+        hipLaunchKernelGGL((sequential_cached_kernel<512, 4>), dim3((uint32_t)P), dim3(512), 0, s, sn, cap, jm,
+                           req->len_tokens, ord, b0, b1, out_idx, out_score);
+    else if (h->D <= 512u * 6)
+        hipLaunchKernelGGL((sequential_cached_kernel<512, 6>), dim3((uint32_t)P), dim3(512), 0, s, sn, cap, jm,
+                           req->len_tokens, ord, b0, b1, out_idx, out_score);
+    else if (h->D <= 512u * 8)
+        hipLaunchKernelGGL((sequential_cached_kernel<512, 8>), dim3((uint32_t)P), dim3(512), 0, s, sn, cap, jm,
+                           req->len_tokens, ord, b0, b1, out_idx, out_score);
+    else
+        hipLaunchKernelGGL(sequential_kernel, dim3((uint32_t)P), dim3(kSeqThreads), 0, s, sn, (uint32_t)R, cap, jm,
+                           req->len_tokens, ord, b0, b1, out_idx, out_score);
     HIPCHK(h, hipGetLastError());
     HIPCHK(h, time_end(h, s));
     return NETKV_OK;

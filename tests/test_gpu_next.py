@@ -164,3 +164,27 @@ def test_sequential_full_size_two_prefill_instances(nk):
         ref = oracle.select_sequential(snap, ocache, subset_requests(req, rows), cap=16, follow=g_idx[rows])
         _check_sequential(g_idx[rows], g_sc[rows], ref)
     sel.close()
+
+
+@pytest.mark.parametrize("shape", [(8, 8, 8, 4), (8, 8, 8, 6), (8, 8, 10, 8), (8, 8, 12, 8)])
+def test_sequential_pool_sizes(nk, shape):
+    """Pools of 1,536 / 2,304 / 3,840 / 4,608 decodes (each register layout
+    of the sequential kernel and the general form beyond them), with 6,000
+    requests from three prefill instances so that the counters of every
+    tier grow and saturate within the batch."""
+    cl = W.Cluster(*shape)
+    cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=6000, cache_per_decode=512)
+    _say("sequential pool", cfg.n_decode)
+    snap, req, cache = _inputs(cfg, 51)
+    req["prefill"] = (np.arange(cfg.n_requests) % 3 * 7).astype(np.uint32)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = nk.requests_to_device(req, sel.device)
+    out = sel.select_sequential(rd, cap=16)
+    sel.sync_errors()
+    g_idx, g_sc = nk.to_numpy(out["idx"]), nk.to_numpy(out["score"])
+    ref = oracle.select_sequential(snap, oracle.Cache(cache, n_threads=8), req, cap=16, follow=g_idx)
+    near = _check_sequential(g_idx, g_sc, ref)
+    assert near < 0.01 * cfg.n_requests
+    sel.close()
