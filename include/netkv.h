@@ -102,12 +102,14 @@ netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stre
  * Host or device pointers.  Value 0 is reserved (EINVAL); repeated hashes
  * of one decode are allowed and count once.  Builds one open-addressed
  * table per decode with at most `max_load_factor` (0 < lf < 1) occupancy
- * (capped at 0.85), and one filter over the union of all sets (8 bits per
+ * (capped at 0.85; a build that cannot place every hash is retried with
+ * twice the buckets, twice), and one filter over the union of all sets (8 bits per
  * resident hash) that proves a hash absent from every decode, so a scan
  * can skip that hash's per-decode tests without changing any result.
  * Synchronous.  EINVAL: bad CSR, hash 0, lf out of range, D different
  * from a loaded snapshot; ECAPACITY: a table would need more than 2^31
- * slots; ENOMEM: out of device memory. */
+ * slots, or could not be built even at four times the planned buckets;
+ * ENOMEM: out of device memory. */
 netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t *hash_off,
                               const uint64_t *hashes, uint64_t n_hashes, float max_load_factor,
                               void *stream);

@@ -812,11 +812,12 @@ __global__ void count_zero_kernel(const uint64_t *__restrict__ h, uint64_t n, ui
 
 // Cuckoo insertion of one decode's hashes (tiles: tile_dec[b], tile_beg[b],
 // tile_end[b]).  A key goes to an empty slot of either candidate bucket
-// (compare-and-swap 0 -> key); when all four slots are taken it displaces a
-// slot's key by atomic exchange and carries the displaced key on, to its
-// other bucket.  A key is always either in the table or carried by exactly
-// one thread, so none is lost.  A repeated hash (already in a slot) stops.
-constexpr uint32_t kMaxKicks = 512;
+// (compare-and-swap 0 -> key); when all four slots are taken it displaces the
+// key of a random slot by atomic exchange (a random walk: a fresh key picks
+// either bucket, a displaced key its other bucket) and carries the displaced
+// key on.  A key is always either in the table or carried by exactly one
+// thread, so none is lost.  A repeated hash (already in a slot) stops.
+constexpr uint32_t kMaxKicks = 2048;
 
 __device__ inline bool try_place(unsigned long long *bk, uint64_t key) {
     for (int slot = 0; slot < 2; ++slot) {
@@ -851,6 +852,7 @@ __global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys
     for (uint64_t i = beg + threadIdx.x; i < end; i += blockDim.x) {
         uint64_t key = h[i];
         uint32_t from = 0xFFFFFFFFu;   // bucket the carried key was displaced from
+        uint32_t rnd = (uint32_t)(key ^ (key >> 32)) ^ (uint32_t)i;   // walk state (a 32-bit LCG)
         bool done = false;
         for (uint32_t kick = 0; kick < kMaxKicks && !done; ++kick) {
             uint32_t b1, b2;
@@ -862,9 +864,10 @@ __global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys
                 break;
             }
             // displace from the bucket the key did not just leave
-            const uint32_t b = (b1 == from) ? b2 : (b2 == from) ? b1 : ((kick & 1) ? b2 : b1);
+            rnd = rnd * 1664525u + 1013904223u;
+            const uint32_t b = (b1 == from) ? b2 : (b2 == from) ? b1 : ((rnd >> 31) ? b2 : b1);
             unsigned long long *bk = col + (uint64_t)b * pitch * 2;
-            const unsigned long long old = atomicExch(bk + ((kick >> 1) & 1), (unsigned long long)key);
+            const unsigned long long old = atomicExch(bk + ((rnd >> 30) & 1u), (unsigned long long)key);
             if (old == 0ull || old == key) {
                 done = true;
                 break;
@@ -1790,10 +1793,10 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
         ++log2b;
         if (log2b > 30) return fail(h, NETKV_ECAPACITY, "a table would need more than 2^31 slots");
     }
-    const uint64_t nbk = 1ull << log2b;
-    const uint64_t cap = 2 * nbk;
+    uint64_t nbk = 1ull << log2b;
+    uint64_t cap = 2 * nbk;
     const uint32_t pitch = (n_decode + 15u) & ~15u;
-    const uint64_t tbytes = cap * pitch * 8ull;
+    uint64_t tbytes = cap * pitch * 8ull;
     // tiles of at most 4096 hashes, each within one decode
     const uint64_t kTile = 4096;
     std::vector<uint32_t> tdec;
@@ -1851,27 +1854,38 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
         cleanup();
         return fail(h, NETKV_ENOMEM, "filter allocation of %llu bytes failed", (unsigned long long)(8 * any_words));
     }
-    e = dalloc(tab, cap * pitch);
-    if (e != hipSuccess) {
-        cleanup();
-        dfree(anyw);
-        return fail(h, NETKV_ENOMEM, "table allocation of %llu bytes failed", (unsigned long long)tbytes);
-    }
-    e = hipMemsetAsync(tab, 0, tbytes, st);
-    if (e == hipSuccess) e = hipMemsetAsync(anyw, 0, 8 * any_words, st);
+    e = hipMemsetAsync(anyw, 0, 8 * any_words, st);
     if (e == hipSuccess && total) {
         hipLaunchKernelGGL(any_build_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st,
                            (const uint64_t *)(dh + first), total, anyw, 64u - log2w);
         e = hipGetLastError();
     }
-    if (e == hipSuccess && !tdec.empty()) {
-        hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, 32u - log2b, pitch,
-                           (const uint64_t *)dh, (const uint32_t *)ddec,
-                           (const uint64_t *)dbeg, (const uint64_t *)dend, h->loadword);
-        e = hipGetLastError();
+    // build at the planned size; should a build fail to place every key (a
+    // random walk that did not end), rebuild with twice the buckets, twice
+    for (int attempt = 0;; ++attempt) {
+        nbk = 1ull << log2b;
+        cap = 2 * nbk;
+        tbytes = cap * pitch * 8ull;
+        if (e == hipSuccess && dalloc(tab, cap * pitch) != hipSuccess) {
+            cleanup();
+            dfree(anyw);
+            return fail(h, NETKV_ENOMEM, "table allocation of %llu bytes failed", (unsigned long long)tbytes);
+        }
+        if (e == hipSuccess) e = hipMemsetAsync(tab, 0, tbytes, st);
+        if (e == hipSuccess) e = hipMemsetAsync(h->loadword, 0, 4, st);
+        if (e == hipSuccess && !tdec.empty()) {
+            hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, 32u - log2b,
+                               pitch, (const uint64_t *)dh, (const uint32_t *)ddec, (const uint64_t *)dbeg,
+                               (const uint64_t *)dend, h->loadword);
+            e = hipGetLastError();
+        }
+        bad = 0;
+        if (e == hipSuccess) e = hipMemcpyAsync(&bad, h->loadword, 4, hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess || !bad || attempt == 2 || log2b >= 30) break;
+        dfree(tab);
+        ++log2b;
     }
-    if (e == hipSuccess) e = hipMemcpyAsync(&bad, h->loadword, 4, hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipStreamSynchronize(st);
     dfree(dh); dfree(dbeg); dfree(dend); dfree(ddec);
     if (e != hipSuccess || bad) {
         dfree(tab);
