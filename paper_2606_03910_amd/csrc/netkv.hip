@@ -524,12 +524,11 @@ __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &
 }
 
 // What one scan step fetches for the next request: its congestion row
-// (seconds per token and tier per column) and the buckets of its first test.
+// (seconds per token and tier per column).
 template <int C>
 struct Ahead {
     float spt[C];
     uint32_t tau[C];
-    Buckets<C> bk;
 };
 
 // Tier latency by a per-lane tier index, without indexing an array.
@@ -545,9 +544,9 @@ __device__ inline float tier_latency(const Snap &s, uint32_t tau) {
 // where the common leading run decides it), non-cached bytes, feasibility
 // and cost (Eqs. (2)-(7)), then the group's K best feasible (score, index)
 // keys into partial[group][sorted position][0..K).  Request records are
-// fetched two requests ahead, and the congestion row and the first test's
-// buckets one request ahead into the other of two buffers (the loop is
-// unrolled by two so that neither buffer is copied).
+// fetched two requests ahead, and the congestion row one request ahead into
+// the other of two buffers (the loop is unrolled by two so that neither
+// buffer is copied).
 template <int K, int W, int C, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec *__restrict__ rec,
                                                       const uint64_t *__restrict__ hashes,
@@ -606,14 +605,8 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
     uint32_t L0 = 0;
     bool t0 = c0.n != 0;
     uint64_t h0 = t0 ? chash[c0.a] : 0;
-    {
-        uint32_t b1, b2;
-        buckets_of(h0, t.shift, b1, b2);
-        lmask go[C];
-#pragma unroll
-        for (int q = 0; q < C; ++q) go[q] = t0 ? actm[q] : 0;
-        load_buckets<C>(col, (uint64_t)b1 * rs, (uint64_t)b2 * rs, go, A.bk);
-    }
+    uint32_t hb1, hb2;   // candidate buckets of h0
+    buckets_of(h0, t.shift, hb1, hb2);
     uint32_t j_prev[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) j_prev[q] = 0;
@@ -628,17 +621,6 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         const uint32_t L1 = c1.lcp;
         const bool more = i + 1 < i1 && L1 < c1.n && c1.gp;
         const uint64_t h1 = more ? c1.hf : 0;
-        {
-            // the next request's first test is needed on a column iff its
-            // first-miss index after this request is >= L1; a column that
-            // carries this request (j_prev < L0) keeps j_prev, so
-            // j_prev >= min(L0, L1) covers every column that can need it
-            const uint32_t lo = L0 < L1 ? L0 : L1;
-            lmask go[C];
-#pragma unroll
-            for (int q = 0; q < C; ++q) go[q] = more ? ballot(j_prev[q] >= lo) & actm[q] : 0;
-            load_buckets<C>(col, (uint64_t)c1.b1 * rs, (uint64_t)c1.b2 * rs, go, nxt.bk);
-        }
         // prefix lengths: carried where the common leading run decides them
         uint32_t j[C];
         lmask need[C];
@@ -648,7 +630,14 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             j[q] = carry ? j_prev[q] : L0;
             need[q] = ballot(!carry) & actm[q];
         }
-        if (t0) probe_from<W, C>(col, t, rs, chash + c0.a, c0.n, L0, need, j, h0, cur.bk);
+        if (t0) {
+            // the first test's buckets, on the columns that need it (after the
+            // filter only a small share of requests needs any test: loading
+            // them here rather than a request ahead keeps no buffer live)
+            Buckets<C> b0;
+            load_buckets<C>(col, (uint64_t)hb1 * rs, (uint64_t)hb2 * rs, need, b0);
+            probe_from<W, C>(col, t, rs, chash + c0.a, c0.n, L0, need, j, h0, b0);
+        }
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t cb[C];
 #pragma unroll
@@ -695,6 +684,8 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         L0 = L1;
         h0 = h1;
         t0 = more;
+        hb1 = c0.b1;   // c0 is now the next request's record
+        hb2 = c0.b2;
     };
     for (uint32_t i = i0; i < i1; i += 2) {
         step(i, A, B);
