@@ -276,22 +276,28 @@ constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
 
 // One sorted request, everything the scan needs without indirection.
-struct alignas(16) Rec {
-    uint32_t r;      // request index in the caller's batch
+// The part every scan step reads (one 16-byte scalar load) ...
+struct alignas(16) Hot {
     uint32_t p;      // prefill instance
     uint32_t len;    // input tokens
-    uint32_t n;      // hashed blocks
     uint32_t lcp;    // leading blocks in common with the previous sorted request
-    uint32_t b1;     // first candidate bucket of hf
+    uint32_t tf;     // 1 if block lcp exists and the filter admits its hash: a carried scan tests it
+};
+
+// ... and the part read only by requests that probe (and for per-pair output).
+struct alignas(16) Cold {
     uint64_t a;      // offset of the hash run
-    uint64_t hf;     // hash of block lcp (the first one a carried scan tests), 0 if lcp == n
-    uint32_t b2;     // second candidate bucket of hf
-    uint32_t gp;     // 0 when the filter proves that no decode holds hf
+    uint64_t hf;     // hash of block lcp, 0 if lcp == n
+    uint32_t r;      // request index in the caller's batch
+    uint32_t n;      // hashed blocks
+    uint32_t b1;     // candidate buckets of hf
+    uint32_t b2;
 };
 
 struct Order {
     const uint32_t *perm;     // sorted position -> request
-    const Rec *rec;           // [n_valid] sorted request records
+    const Hot *hot;           // [n_valid] sorted request records
+    const Cold *cold;
     const uint32_t *n_valid;  // valid requests (they sort first)
 };
 
@@ -362,7 +368,8 @@ __global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint3
 template <uint32_t G>
 __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
                                                   const uint32_t *__restrict__ sorted_keys, Table t, uint32_t reuse,
-                                                  Rec *__restrict__ rec, uint32_t *__restrict__ n_valid) {
+                                                  Hot *__restrict__ hot, Cold *__restrict__ cold,
+                                                  uint32_t *__restrict__ n_valid) {
     const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t sub = threadIdx.x % G;
     const uint32_t seg = (threadIdx.x % kWave) - sub;   // first lane of this position's lanes
@@ -396,17 +403,19 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__res
         }
     }
     if (sub != 0) return;
-    Rec o;
-    o.r = r;
+    Cold c;
+    c.a = a;
+    c.hf = l < nr ? rq.hashes[a + l] : 0;
+    c.r = r;
+    c.n = (uint32_t)nr;
+    buckets_of(c.hf, t.shift, c.b1, c.b2);
+    Hot o;
     o.p = rq.prefill[r];
     o.len = rq.len[r];
-    o.n = (uint32_t)nr;
     o.lcp = (uint32_t)l;
-    o.a = a;
-    o.hf = l < nr ? rq.hashes[a + l] : 0;
-    buckets_of(o.hf, t.shift, o.b1, o.b2);
-    o.gp = l < nr && maybe_anywhere(t.any, t.any_shift, o.hf) ? 1u : 0u;
-    rec[i] = o;
+    o.tf = l < nr && maybe_anywhere(t.any, t.any_shift, c.hf) ? 1u : 0u;
+    hot[i] = o;
+    cold[i] = c;
 }
 
 // Read-only data that is uniform across a wavefront (request records, hash
@@ -420,19 +429,25 @@ __device__ inline cptr<T> as_const(const T *p) {
     return (cptr<T>)(const __attribute__((address_space(4))) void *)(uintptr_t)p;
 }
 
-__device__ inline Rec load_rec(const Rec *base, uint32_t i) {
+__device__ inline Hot load_hot(const Hot *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
-    Rec x;
-    x.r = w[0];
-    x.p = w[1];
-    x.len = w[2];
-    x.n = w[3];
-    x.lcp = w[4];
-    x.b1 = w[5];
-    x.a = ((uint64_t)w[7] << 32) | (uint64_t)w[6];
-    x.hf = ((uint64_t)w[9] << 32) | (uint64_t)w[8];
-    x.b2 = w[10];
-    x.gp = w[11];
+    Hot x;
+    x.p = w[0];
+    x.len = w[1];
+    x.lcp = w[2];
+    x.tf = w[3];
+    return x;
+}
+
+__device__ inline Cold load_cold(const Cold *base, uint32_t i) {
+    const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
+    Cold x;
+    x.a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
+    x.hf = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
+    x.r = w[4];
+    x.n = w[5];
+    x.b1 = w[6];
+    x.b2 = w[7];
     return x;
 }
 
@@ -543,12 +558,15 @@ __device__ inline float tier_latency(const Snap &s, uint32_t tau) {
 // first-miss prefix length per decode (carried from the previous request
 // where the common leading run decides it), non-cached bytes, feasibility
 // and cost (Eqs. (2)-(7)), then the group's K best feasible (score, index)
-// keys into partial[group][sorted position][0..K).  Request records are
-// fetched two requests ahead, and the congestion row one request ahead into
-// the other of two buffers (the loop is unrolled by two so that neither
-// buffer is copied).
+// keys into partial[group][sorted position][0..K).  Hot request records
+// are fetched two requests ahead and the congestion row one request ahead
+// into the other of two buffers (the loop is unrolled by two so that neither
+// buffer is copied); a request's cold record and first-test buckets only
+// when it probes.  The keys of 64/K consecutive requests are gathered in
+// lanes and stored together.
 template <int K, int W, int C, bool PAIRS>
-__global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec *__restrict__ rec,
+__global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot *__restrict__ hot,
+                                                      const Cold *__restrict__ cold,
                                                       const uint64_t *__restrict__ hashes,
                                                       const uint32_t *__restrict__ n_valid, uint32_t n_req,
                                                       uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
@@ -591,36 +609,38 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
         xlim[q] = act[q] ? s.dxlim[d[q]] : 0;
     }
     const cptr<uint64_t> chash = as_const(hashes);
-    Rec c0 = load_rec(rec, i0);
-    Rec c1 = load_rec(rec, i0 + 1 < i1 ? i0 + 1 : i0);
+    Hot c0 = load_hot(hot, i0);
+    Hot c1 = load_hot(hot, i0 + 1 < i1 ? i0 + 1 : i0);
     Ahead<C> A, B;
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         A.spt[q] = s.spt[(uint64_t)c0.p * s.D + pcol[q]];
         A.tau[q] = s.tier_map[(uint64_t)c0.p * s.D + pcol[q]];
     }
-    // first test of the current request: block L0 (0 for the run's first);
-    // t0 says whether it is needed at all (not when the cache filter rules
-    // the block out on every decode)
+    // the run's first request is scanned from block 0
+    const Cold k0 = load_cold(cold, i0);
+    const uint64_t h00 = k0.n ? chash[k0.a] : 0;
+    uint32_t b00, b01;
+    buckets_of(h00, t.shift, b00, b01);
+    // first test of the current request: block L0; t0 says whether it is
+    // needed at all (not when the cache filter rules the block out on every
+    // decode)
     uint32_t L0 = 0;
-    bool t0 = c0.n != 0;
-    uint64_t h0 = t0 ? chash[c0.a] : 0;
-    uint32_t hb1, hb2;   // candidate buckets of h0
-    buckets_of(h0, t.shift, hb1, hb2);
+    bool t0 = k0.n != 0;
     uint32_t j_prev[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) j_prev[q] = 0;
+    constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
+    uint64_t pend = kEmptyKey;
 
     auto step = [&](uint32_t i, const Ahead<C> &cur, Ahead<C> &nxt) {
-        const Rec c2 = load_rec(rec, i + 2 < i1 ? i + 2 : i1 - 1);
+        const Hot c2 = load_hot(hot, i + 2 < i1 ? i + 2 : i1 - 1);
 #pragma unroll
         for (int q = 0; q < C; ++q) {
             nxt.spt[q] = s.spt[(uint64_t)c1.p * s.D + pcol[q]];
             nxt.tau[q] = s.tier_map[(uint64_t)c1.p * s.D + pcol[q]];
         }
-        const uint32_t L1 = c1.lcp;
-        const bool more = i + 1 < i1 && L1 < c1.n && c1.gp;
-        const uint64_t h1 = more ? c1.hf : 0;
+        const bool more = i + 1 < i1 && c1.tf;
         // prefix lengths: carried where the common leading run decides them
         uint32_t j[C];
         lmask need[C];
@@ -631,14 +651,32 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             need[q] = ballot(!carry) & actm[q];
         }
         if (t0) {
-            // the first test's buckets, on the columns that need it (after the
-            // filter only a small share of requests needs any test: loading
-            // them here rather than a request ahead keeps no buffer live)
+            // the cold record and the first test's buckets, on the columns
+            // that need it (after the filter only a small share of requests
+            // probes at all, so nothing is fetched ahead for this)
+            uint64_t a, h0;
+            uint32_t n, hb1, hb2;
+            if (i == i0) {
+                a = k0.a;
+                n = k0.n;
+                h0 = h00;
+                hb1 = b00;
+                hb2 = b01;
+            } else {
+                const Cold k = load_cold(cold, i);
+                a = k.a;
+                n = k.n;
+                h0 = k.hf;
+                hb1 = k.b1;
+                hb2 = k.b2;
+            }
             Buckets<C> b0;
             load_buckets<C>(col, (uint64_t)hb1 * rs, (uint64_t)hb2 * rs, need, b0);
-            probe_from<W, C>(col, t, rs, chash + c0.a, c0.n, L0, need, j, h0, b0);
+            probe_from<W, C>(col, t, rs, chash + a, n, L0, need, j, h0, b0);
         }
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
+        uint32_t r_out = 0;
+        if (PAIRS) r_out = load_cold(cold, i).r;
         uint32_t cb[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) {
@@ -647,17 +685,17 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
             const bool feas = (uint64_t)x < xlim[q];
             const float cost = pair_score(x, cur.spt[q], tier_latency(s, cur.tau[q] & 3u), dload[q]);
             if (PAIRS && act[q]) {
-                const uint64_t o = (uint64_t)c0.r * s.D + d[q];
+                const uint64_t o = (uint64_t)r_out * s.D + d[q];
                 if (po.j) po.j[o] = (uint16_t)j[q];
                 if (po.feas) po.feas[o] = feas ? 1 : 0;
                 if (po.score) po.score[o] = cost;
-                if (po.jT) po.jT[(uint64_t)d[q] * n_req + c0.r] = (uint16_t)j[q];
+                if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)j[q];
             }
             cb[q] = (act[q] && feas) ? __float_as_uint(cost) : 0xFFFFFFFFu;
         }
         // the group's K best: least cost bits, then least decode index, i.e.
         // the lowest lane holding the minimum in the first column that holds it
-        uint64_t mine = kEmptyKey;
+        const uint32_t slot = (i - i0) % kPer;
 #pragma unroll
         for (int r = 0; r < K; ++r) {
             uint32_t lm = cb[0];
@@ -676,16 +714,17 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Rec
                     break;
                 }
             }
-            if (lane == (uint32_t)r) mine = ((uint64_t)mn << 32) | (uint64_t)dm;
+            if (lane == slot * K + (uint32_t)r) pend = ((uint64_t)mn << 32) | (uint64_t)dm;
         }
-        if (lane < (uint32_t)K) partial[((uint64_t)grp * n_req + i) * K + lane] = mine;
+        if (slot == kPer - 1 || i + 1 == i1) {
+            const uint32_t first = i - slot;
+            if (lane < (slot + 1) * K) partial[((uint64_t)grp * n_req + first) * K + lane] = pend;
+            pend = kEmptyKey;
+        }
+        L0 = c1.lcp;
         c0 = c1;
         c1 = c2;
-        L0 = L1;
-        h0 = h1;
         t0 = more;
-        hb1 = c0.b1;   // c0 is now the next request's record
-        hb2 = c0.b2;
     };
     for (uint32_t i = i0; i < i1; i += 2) {
         step(i, A, B);
@@ -1254,7 +1293,8 @@ struct netkv_ctx {
     // batch-order scratch (grows to the largest batch seen)
     uint64_t order_cap = 0;
     uint32_t *keys_in = nullptr, *keys_out = nullptr, *vals_in = nullptr, *perm = nullptr;
-    Rec *rec = nullptr;
+    Hot *hot = nullptr;   // sorted request records, the part every scan step reads
+    Cold *cold = nullptr; // and the part read by probing requests
     uint32_t *n_valid = nullptr;
     void *sort_tmp = nullptr;
     size_t sort_tmp_bytes = 0;
@@ -1429,13 +1469,13 @@ using SortConfig = rocprim::default_config;
 
 netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, hipStream_t st) {
     if (R > h->order_cap) {
-        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->rec);
+        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->sort_tmp);
         h->order_cap = 0;
         h->sort_tmp_bytes = 0;
         if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
             dalloc(h->vals_in, R) != hipSuccess || dalloc(h->perm, R) != hipSuccess ||
-            dalloc(h->rec, R) != hipSuccess)
+            dalloc(h->hot, R) != hipSuccess || dalloc(h->cold, R) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
         size_t bytes = 0;
         if (rocprim::radix_sort_pairs<SortConfig>(nullptr, bytes, h->keys_in, h->keys_out, h->vals_in, h->perm,
@@ -1490,11 +1530,11 @@ void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &or
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
     const uint32_t grid = (uint32_t)grid64;
     if (pairs)
-        hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
-                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
+        hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
+                           rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
     else
-        hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.rec, rq.hashes,
-                           ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
+        hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
+                           rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
 }
 
 // Scan, bracketed by the handle's timing events when enabled, then merge.
@@ -1546,12 +1586,12 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                     (uint32_t)R, 0, 32, st));
     hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
-                       (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->rec,
+                       (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->hot, h->cold,
                        h->n_valid);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
-    Order ord{h->perm, h->rec, h->n_valid};
+    Order ord{h->perm, h->hot, h->cold, h->n_valid};
     if (K == 1)
         HIPCHK(h, launch_scan_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
                                         pairs, k, idx, score, st));
@@ -1619,7 +1659,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->cnt);
         dfree(h->adm);
         dfree(h->bytes);
-        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->rec);
+        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
@@ -1810,9 +1850,12 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     }
     hipError_t e = hipSuccess;
     if (total) e = hipMemcpyAsync(dh + first, hashes + first, 8ull * total, hipMemcpyDefault, st);
-    if (e == hipSuccess && !tdec.empty()) e = hipMemcpyAsync(ddec, tdec.data(), 4ull * tdec.size(), hipMemcpyHostToDevice, st);
-    if (e == hipSuccess && !tbeg.empty()) e = hipMemcpyAsync(dbeg, tbeg.data(), 8ull * tbeg.size(), hipMemcpyHostToDevice, st);
-    if (e == hipSuccess && !tend.empty()) e = hipMemcpyAsync(dend, tend.data(), 8ull * tend.size(), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess && !tdec.empty())
+        e = hipMemcpyAsync(ddec, tdec.data(), 4ull * tdec.size(), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess && !tbeg.empty())
+        e = hipMemcpyAsync(dbeg, tbeg.data(), 8ull * tbeg.size(), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess && !tend.empty())
+        e = hipMemcpyAsync(dend, tend.data(), 8ull * tend.size(), hipMemcpyHostToDevice, st);
     if (e == hipSuccess) e = hipMemsetAsync(h->loadword, 0, 4, st);
     uint32_t bad = 0;
     if (e == hipSuccess && total) {
