@@ -84,7 +84,7 @@ typedef struct {
  * complete on `stream`, so the caller may free its arrays on return).
  * Also resets the between-batch state (n_inflight, queue_depth, free_mem
  * from the snapshot; admitted bytes of the previous batch to 0).
- * EINVAL: NULL pointer, P or D zero, tier > 3, util outside [0,1) or NaN,
+ * EINVAL: NULL pointer, P or D zero, P * (D + 32) >= 2^29, tier > 3, util outside [0,1) or NaN,
  * beta_d > beta_max, non-positive or non-finite bandwidth, negative or
  * non-finite latency/a/b/alpha, block_tokens 0, kv_bytes_per_token >= 2^32,
  * or D different from a loaded cache. */
@@ -132,7 +132,8 @@ typedef struct {
 /* Optional per-pair outputs, row-major [n_req][n_decode] DEVICE arrays;
  * any member may be NULL. */
 typedef struct {
-    uint16_t *prefix_blocks;        /* j: leading resident blocks (lambda = B_tok * j) */
+    uint16_t *prefix_blocks;        /* j: leading resident blocks (lambda = B_tok * j),
+                                       written as min(j, 65535) */
     uint8_t *feasible;              /* 1 iff m_d >= s_eff + m_min */
     float *score;                   /* C(r,d), also for infeasible pairs */
 } netkv_pairs_t;
@@ -161,7 +162,9 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
  * different tier than the one selected under the loaded snapshot's own
  * congestion, out_flips[2*s+1] = number whose selected decode differs (a
  * rejection counts as its own tier and index).  Asynchronous; grows an
- * internal work buffer (n_req * n_decode * 2 bytes) on first use.
+ * internal work buffer (n_req * n_decode * 2 bytes) on first use.  Prefix
+ * lengths are kept in 16 bits: a request of more than 65535 blocks is
+ * invalid here (index -1, score NaN, reported by netkv_sync_errors).
  * Scenario values are not validated (values >= 1 give non-positive
  * bandwidth and meaningless costs). */
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen,
@@ -197,7 +200,9 @@ netkv_status netkv_tier_counts(netkv_handle h, const netkv_requests_t *req, cons
  * to out_idx / out_score ([n_req] DEVICE); invalid requests get -1 / NaN.
  * The handle's between-batch state is not changed (netkv_commit_batch
  * applies the batch).  Asynchronous; grows an internal buffer of
- * n_req * n_decode * 2 bytes (per-pair prefix lengths) on first use. */
+ * n_req * n_decode * 2 bytes (per-pair prefix lengths) on first use; a
+ * request of more than 65535 blocks is invalid here, as for
+ * netkv_rank_sweep. */
 netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req, uint32_t cap,
                                      int32_t *out_idx, float *out_score, void *stream);
 

@@ -157,7 +157,7 @@ def select(snap, cache, req, k: int = 1, pairs: bool = False, n_threads: int = 1
     """Top-k selection for every request.
 
     Returns dict(idx [R,k] int32, score [R,k] float64, tests (sum of
-    membership tests), and if ``pairs``: j [R,D] uint16, feasible [R,D]
+    membership tests), and if ``pairs``: j [R,D] uint32, feasible [R,D]
     uint8, cost [R,D] float64)."""
     lib = _load()
     s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
@@ -169,7 +169,7 @@ def select(snap, cache, req, k: int = 1, pairs: bool = False, n_threads: int = 1
     out = dict(idx=idx, score=score)
     pj = pf = pc = None
     if pairs:
-        pj = np.empty((R, D), dtype=np.uint16)
+        pj = np.empty((R, D), dtype=np.uint32)
         pf = np.empty((R, D), dtype=np.uint8)
         pc = np.empty((R, D), dtype=np.float64)
         out.update(j=pj, feasible=pf, cost=pc)

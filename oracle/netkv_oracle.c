@@ -166,8 +166,8 @@ static int cmp_cand(const void *a, const void *b) {
  * (the snapshot's own, or a scenario's).  j_row, if given, supplies the
  * prefix lengths instead of matching again. */
 static void score_request(const orc_snapshot *s, const float *util, const orc_cache *c,
-                          const orc_requests *q, uint32_t r, const uint16_t *j_row, cand *buf,
-                          uint32_t k, int32_t *out_idx, double *out_score, uint16_t *pj,
+                          const orc_requests *q, uint32_t r, const uint32_t *j_row, cand *buf,
+                          uint32_t k, int32_t *out_idx, double *out_score, uint32_t *pj,
                           uint8_t *pf, double *pc, uint64_t *tests_sum) {
     orc_snapshot sv = *s;
     sv.util = util;
@@ -192,7 +192,7 @@ static void score_request(const orc_snapshot *s, const float *util, const orc_ca
         int tau = s->tier_map[(uint64_t)p * s->n_decode + d];
         double t_x = (double)s_eff / eff_bandwidth(&sv, p, d) + s->tier_lat[tau];   /* Eq. (3) */
         double cost = t_x + s->alpha * load_time(s, d);
-        if (pj) pj[d] = (uint16_t)j;
+        if (pj) pj[d] = j;
         if (pf) pf[d] = (uint8_t)feas;
         if (pc) pc[d] = cost;
         if (feas) {
@@ -213,7 +213,7 @@ static void score_request(const orc_snapshot *s, const float *util, const orc_ca
  * [n_req][n_decode]) may be NULL.  Returns the number of block membership
  * tests made by the first-miss scans (sum over pairs of min(j + 1, n_r)). */
 uint64_t orc_select(const orc_snapshot *s, const orc_cache *c, const orc_requests *q, uint32_t k,
-                    int32_t *out_idx, double *out_score, uint16_t *pair_j, uint8_t *pair_feas,
+                    int32_t *out_idx, double *out_score, uint32_t *pair_j, uint8_t *pair_feas,
                     double *pair_cost, int n_threads) {
     uint64_t tests = 0;
     const uint32_t D = s->n_decode;
@@ -249,7 +249,7 @@ void orc_rank_sweep(const orc_snapshot *s, const orc_cache *c, const orc_request
                     uint32_t n_scen, const float *util_scen, uint32_t k, int32_t *out_idx,
                     double *out_score, uint64_t *out_flips, int n_threads) {
     const uint32_t D = s->n_decode, R = q->n_req;
-    uint16_t *jm = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)R * (D ? D : 1));
+    uint32_t *jm = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)R * (D ? D : 1));
     int32_t *base = (int32_t *)malloc(sizeof(int32_t) * (R ? R : 1));
 #ifdef _OPENMP
     if (n_threads < 1) n_threads = 1;

@@ -83,8 +83,9 @@ struct Snap {
     uint32_t P, D;
     uint32_t policy;         // 0: full NetKV, 1: no live congestion, 2: neither congestion nor in-flight
     // derived once per call by derive_kernel (Eqs. (3)-(7) factored by (p, d) and d)
-    const float *spt;        // [P*D] seconds per non-cached token (the tier latency
-                             // comes from tier_map and lat[])
+    const float2 *sl;        // [P][slp] per (p, d): seconds per non-cached token, and the
+                             // constant part L_tau + alpha (T_queue + T_decode)
+    uint32_t slp;            // row pitch of sl in elements (an odd number of 128-byte lines)
     const float *dbase;      // [D] alpha (T_queue + T_decode)
     const uint64_t *dxlim;   // [D] x = l - lambda is feasible iff x < dxlim
 };
@@ -121,6 +122,15 @@ __host__ __device__ inline void buckets_of(uint64_t h, uint32_t shift, uint32_t 
     const uint32_t fold = (uint32_t)h ^ (uint32_t)(h >> 32);
     b1 = (fold * kFib32) >> shift;
     b2 = b1 ^ (((fold * kMix32) >> shift) | 1u);
+}
+
+// Row pitch (elements) of the per-(p, d) float2 rows: D rounded up to whole
+// 128-byte lines, then to an odd number of lines, so that rows spread over
+// all L2 sets instead of aliasing on the sets of a power-of-two stride.
+__host__ __device__ inline uint32_t sl_pitch(uint32_t D) {
+    uint32_t lines = (D + 15u) / 16u;
+    if ((lines & 1u) == 0) ++lines;
+    return lines * 16u;
 }
 
 // The resident-anywhere filter: a blocked Bloom filter over the union of all
@@ -179,6 +189,13 @@ __device__ inline float sec_per_token_n(const Snap &s, uint32_t tau, float n, fl
 
 __device__ inline float sec_per_token(const Snap &s, uint32_t tau, uint32_t p, float c) {
     return sec_per_token_n(s, tau, (float)s.n_inflight[tau * s.P + p], c);
+}
+
+// Tier latency by a per-lane tier index, without indexing an array.
+__device__ inline float tier_latency(const Snap &s, uint32_t tau) {
+    const float lo = (tau & 1u) ? s.lat[1] : s.lat[0];
+    const float hi = (tau & 1u) ? s.lat[3] : s.lat[2];
+    return (tau & 2u) ? hi : lo;
 }
 
 __device__ inline uint64_t feasible_limit(const Snap &s, uint64_t m) {
@@ -243,17 +260,22 @@ __device__ inline bool request_ok(const Reqs &rq, const Snap &s, uint32_t r, uin
     return true;
 }
 
-// Per-call factors of the cost: spt and tier latency for every (p, d), the
-// load term and feasibility limit for every d.  Reads the current snapshot
+// Per-call factors of the cost: seconds per token and the constant part
+// (tier latency plus load term) for every (p, d), the load term and the
+// feasibility limit for every d.  Reads the current snapshot
 // (congestion, in-flight counters, queue, batch, free memory).
-__global__ __launch_bounds__(256) void derive_kernel(Snap s, float *__restrict__ spt, float *__restrict__ dbase,
+__global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict__ sl, float *__restrict__ dbase,
                                                      uint64_t *__restrict__ dxlim) {
     const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint64_t npd = (uint64_t)s.P * s.D;
     if (i < npd) {
         const uint32_t p = (uint32_t)(i / s.D);
+        const uint32_t d = (uint32_t)(i - (uint64_t)p * s.D);
         const uint32_t tau = s.tier_map[i] & 3u;
-        spt[i] = sec_per_token(s, tau, p, s.util[i]);
+        // the constant part is rounded exactly as latency + load term would
+        // be when added after loading both (no contraction into an FMA)
+        sl[(uint64_t)p * s.slp + d] =
+            make_float2(sec_per_token(s, tau, p, s.util[i]), __fadd_rn(tier_latency(s, tau), load_term(s, d)));
     }
     if (i < s.D) {
         dbase[i] = load_term(s, (uint32_t)i);
@@ -264,13 +286,16 @@ __global__ __launch_bounds__(256) void derive_kernel(Snap s, float *__restrict__
 // ---------------------------------------------------------------- batch order
 //
 // Requests are scored in an order that groups equal leading blocks: the sort
-// key is 19 bits of the first block hash above 12 bits of the run length, so
-// requests that start with the same prefix become neighbours in ascending
-// length.  For neighbours r' -> r with a common leading run of L blocks, the
-// first-miss index of r on decode d follows from that of r' without any
-// probe whenever it lies inside the common run (j' < L gives j = j'), and
-// otherwise scanning resumes at block L (j' >= L implies blocks 0..L-1 are
-// resident).  The order changes which probes are made, never a result.
+// key is 19 bits of the first block hash above 12 bits of the complemented
+// run length, so requests that start with the same prefix become neighbours
+// in descending length.  For neighbours r' -> r with a common leading run of
+// L blocks, the first-miss index of r on decode d follows from that of r'
+// without any probe whenever it lies inside the common run (j' < L gives
+// j = j'), and otherwise scanning resumes at block L (j' >= L implies blocks
+// 0..L-1 are resident).  Longest first, a request that is a prefix of its
+// predecessor has L = n_r and never probes; one that leaves the shared chain
+// first resumes at a block of its own, which the cache filter mostly rules
+// out.  The order changes which probes are made, never a result.
 
 constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
@@ -278,11 +303,14 @@ constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
 // One sorted request, everything the scan needs without indirection.
 // The part every scan step reads (one 16-byte scalar load) ...
 struct alignas(16) Hot {
-    uint32_t p;      // prefill instance
+    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * D * 8
+    uint32_t test;   // lcp + 1 if block lcp exists and the filter admits its hash (a carried
+                     // scan tests it), else 0
     uint32_t len;    // input tokens
-    uint32_t lcp;    // leading blocks in common with the previous sorted request
-    uint32_t tf;     // 1 if block lcp exists and the filter admits its hash: a carried scan tests it
+    uint32_t lam;    // B_tok * lcp: tokens of the leading blocks in common with the
+                     // previous sorted request
 };
+constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead by the scan
 
 // ... and the part read only by requests that probe (and for per-pair output).
 struct alignas(16) Cold {
@@ -302,11 +330,13 @@ struct Order {
 };
 
 // Validate each request and build its sort key, one thread per request.
+// A request of more than max_blocks blocks is invalid (calls that keep
+// per-pair prefix lengths in 16 bits pass 65535).
 // The reserved hash value 0 is looked for separately: a flat scan of the
 // batch's hash array (count_zero_kernel) raises `zflag`, and only then does
 // zero_fix_kernel check each request's run and invalidate those holding it.
 // Thread 0 clears zflag for that scan.
-__global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t *__restrict__ keys,
+__global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max_blocks, uint32_t *__restrict__ keys,
                                                    uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
                                                    uint32_t *__restrict__ zflag) {
     const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
@@ -315,14 +345,14 @@ __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t *__
     if (r < rq.n_req) {
         uint32_t p, len, n;
         uint64_t a;
-        const bool ok = request_ok(rq, s, r, p, len, a, n);
+        const bool ok = request_ok(rq, s, r, p, len, a, n) && n <= max_blocks;
         uint32_t key = kKeyInvalid;
         if (ok) {
             if (n == 0) {
                 key = kKeyEmptyRun;
             } else {
                 const uint32_t top = (uint32_t)((rq.hashes[a] * kGolden) >> 32);
-                key = ((top >> 13) << 12) | (n < 4095u ? n : 4095u);
+                key = ((top >> 13) << 12) | (4095u - (n < 4095u ? n : 4095u));
             }
         }
         keys[r] = key;
@@ -364,9 +394,11 @@ __global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint3
 // previous sorted request: G lanes per sorted position (G divides 64)
 // compare G blocks per step, their loads issued together.  Also stores the
 // number of valid requests (valid keys sort first): the last valid position
-// writes it, or position 0 writes 0.
+// writes it, or position 0 writes 0.  Positions of invalid requests and the
+// kHotPad positions past the batch get a record that the scan may read ahead
+// but never scores (row 0, no blocks, no test).
 template <uint32_t G>
-__global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__restrict__ perm,
+__global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_t bt, const uint32_t *__restrict__ perm,
                                                   const uint32_t *__restrict__ sorted_keys, Table t, uint32_t reuse,
                                                   Hot *__restrict__ hot, Cold *__restrict__ cold,
                                                   uint32_t *__restrict__ n_valid) {
@@ -374,13 +406,16 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__res
     const uint32_t sub = threadIdx.x % G;
     const uint32_t seg = (threadIdx.x % kWave) - sub;   // first lane of this position's lanes
     const uint64_t i = tid / G;
-    if (i >= rq.n_req) return;
-    const bool valid = sorted_keys[i] < kKeyInvalid;
+    if (i >= (uint64_t)rq.n_req + kHotPad) return;
+    const bool valid = i < rq.n_req && sorted_keys[i] < kKeyInvalid;
     if (sub == 0) {
         if (valid && (i + 1 == rq.n_req || sorted_keys[i + 1] >= kKeyInvalid)) *n_valid = (uint32_t)(i + 1);
         if (i == 0 && !valid) *n_valid = 0;
     }
-    if (!valid) return;
+    if (!valid) {
+        if (sub == 0) hot[i] = Hot{0, 0, 0, 0};
+        return;
+    }
     const uint32_t r = perm[i];
     const uint64_t a = rq.off[r];
     const uint64_t nr = rq.off[r + 1] - a;
@@ -410,10 +445,10 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, const uint32_t *__res
     c.n = (uint32_t)nr;
     buckets_of(c.hf, t.shift, c.b1, c.b2);
     Hot o;
-    o.p = rq.prefill[r];
+    o.row = rq.prefill[r] * slp * (uint32_t)sizeof(float2);   // < 2^32 (checked at load)
+    o.test = l < nr && maybe_anywhere(t.any, t.any_shift, c.hf) ? (uint32_t)l + 1 : 0;
     o.len = rq.len[r];
-    o.lcp = (uint32_t)l;
-    o.tf = l < nr && maybe_anywhere(t.any, t.any_shift, c.hf) ? 1u : 0u;
+    o.lam = bt * (uint32_t)l;   // <= len
     hot[i] = o;
     cold[i] = c;
 }
@@ -432,10 +467,10 @@ __device__ inline cptr<T> as_const(const T *p) {
 __device__ inline Hot load_hot(const Hot *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
     Hot x;
-    x.p = w[0];
-    x.len = w[1];
-    x.lcp = w[2];
-    x.tf = w[3];
+    x.row = w[0];
+    x.test = w[1];
+    x.len = w[2];
+    x.lam = w[3];
     return x;
 }
 
@@ -495,16 +530,16 @@ __device__ inline void member(uint64_t h, const Buckets<C> &b, lmask (&alive)[C]
 // First-miss scan of one request's run on the columns in alive[] (the
 // columns that need it), starting at block `start` (uniform, < n) whose hash
 // h0 and buckets b0 were loaded beforehand.  Past the first block, W blocks
-// are tested per step with all their bucket loads issued together.  j[]
-// holds `start` on entry for those columns and the first-miss index on
-// return.
+// are tested per step with all their bucket loads issued together.  lam[]
+// holds bt * start on entry for those columns and bt * (first-miss index)
+// on return (bt = tokens per block).
 template <int W, int C>
 __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &t, uint64_t rs, cptr<uint64_t> run,
-                                  uint32_t n, uint32_t start, lmask (&alive)[C], uint32_t (&j)[C], uint64_t h0,
-                                  const Buckets<C> &b0) {
+                                  uint32_t n, uint32_t start, lmask (&alive)[C], uint32_t (&lam)[C], uint32_t bt,
+                                  uint64_t h0, const Buckets<C> &b0) {
     member<C>(h0, b0, alive);
 #pragma unroll
-    for (int q = 0; q < C; ++q) j[q] += in_mask(alive[q]) ? 1u : 0u;
+    for (int q = 0; q < C; ++q) lam[q] += in_mask(alive[q]) ? bt : 0u;
     for (uint32_t i0 = start + 1; i0 < n; i0 += W) {
         lmask any = 0;
 #pragma unroll
@@ -533,37 +568,40 @@ __device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &
             if (i0 + w >= n) break;
             member<C>(h[w], bw[w], alive);
 #pragma unroll
-            for (int q = 0; q < C; ++q) j[q] += in_mask(alive[q]) ? 1u : 0u;
+            for (int q = 0; q < C; ++q) lam[q] += in_mask(alive[q]) ? bt : 0u;
         }
     }
 }
 
-// What one scan step fetches for the next request: its congestion row
-// (seconds per token and tier per column).
+// What one scan step fetches for the next request: its row of (seconds per
+// token, constant part) on each column.
 template <int C>
 struct Ahead {
-    float spt[C];
-    uint32_t tau[C];
+    float2 v[C];
 };
 
-// Tier latency by a per-lane tier index, without indexing an array.
-__device__ inline float tier_latency(const Snap &s, uint32_t tau) {
-    const float lo = (tau & 1u) ? s.lat[1] : s.lat[0];
-    const float hi = (tau & 1u) ? s.lat[3] : s.lat[2];
-    return (tau & 2u) ? hi : lo;
+// Buffer-resource word 3 for raw (untyped, unswizzled) buffer access on gfx9-class targets.
+constexpr int kBufferFlags = 0x00020000;
+
+__device__ inline float2 load_row(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t row_off) {
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)lane_off, (int)row_off, 0));
 }
 
 // One wavefront per (run of sorted requests, group of 64*C decodes); lane l
 // holds decodes g*64*C + q*64 + l, q < C.  For each request of the run:
 // first-miss prefix length per decode (carried from the previous request
-// where the common leading run decides it), non-cached bytes, feasibility
+// where the common leading run decides it), non-cached tokens, feasibility
 // and cost (Eqs. (2)-(7)), then the group's K best feasible (score, index)
-// keys into partial[group][sorted position][0..K).  Hot request records
-// are fetched two requests ahead and the congestion row one request ahead
-// into the other of two buffers (the loop is unrolled by two so that neither
-// buffer is copied); a request's cold record and first-test buckets only
-// when it probes.  The keys of 64/K consecutive requests are gathered in
-// lanes and stored together.
+// keys into partial[group][sorted position][0..K).
+//
+// The prefix length is kept as lambda = B_tok * j (tokens), so the
+// non-cached tokens are one subtraction.  Request records are read two
+// requests ahead (the record array is padded so that this never needs a
+// bound), the request's row of (seconds per token, constant part) one
+// request ahead into the other of two buffers (the loop is unrolled by two
+// so neither buffer is copied); a request's cold record and first-test
+// buckets only when it probes.  Requests are taken in chunks of 64/K whose
+// keys are gathered one per lane and stored together.
 template <int K, int W, int C, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot *__restrict__ hot,
                                                       const Cold *__restrict__ cold,
@@ -575,7 +613,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     uint32_t run, grp;
     if (ngroup % kXcds == 0) {
         // workgroups go to the XCDs in turn: XCD x takes groups
-        // [x*gx, (x+1)*gx), so its decodes' congestion columns stay in its
+        // [x*gx, (x+1)*gx), so its decodes' snapshot columns stay in its
         // own L2; the waves of a workgroup take consecutive runs of one group
         const uint32_t gx = ngroup / kXcds, x = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
         grp = x * gx + k % gx;
@@ -592,63 +630,64 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
     const uint32_t base = grp * (kWave * C);
     const uint64_t rs = 2ull * t.pitch;   // elements per bucket row
-    uint32_t d[C], pcol[C];
+    const uint32_t bt = s.block_tokens;
+    uint32_t d[C], voff[C], xm[C];
     bool act[C];
-    lmask actm[C];
+    lmask actm[C], okm[C];
     const uint64_t *col[C];
-    float dload[C];
-    uint64_t xlim[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
         act[q] = d[q] < s.D;
         actm[q] = ballot(act[q]);
-        pcol[q] = act[q] ? d[q] : 0;
-        col[q] = t.keys + 2 * (uint64_t)pcol[q];
-        dload[q] = act[q] ? s.dbase[d[q]] : 0.0f;
-        xlim[q] = act[q] ? s.dxlim[d[q]] : 0;
+        const uint32_t pc = act[q] ? d[q] : 0;
+        voff[q] = pc * (uint32_t)sizeof(float2);
+        col[q] = t.keys + 2 * (uint64_t)pc;
+        // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
+        // xlim >= 1 (capped to 32 bits, as x is); xlim = 0 never is
+        const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
+        okm[q] = ballot(xlim != 0);
+        xm[q] = xlim == 0 ? 0u : xlim - 1 > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)(xlim - 1);
     }
     const cptr<uint64_t> chash = as_const(hashes);
+    // rows of (seconds per token, constant part) through a buffer resource:
+    // a row's byte offset is the scalar offset, the column's the lane offset
+    const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);   // < 2^32 (checked at load)
+    const __amdgpu_buffer_rsrc_t slr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)s.sl, (short)0, (int)(uint32_t)(sl_bytes < 0xFFFFFFFFull ? sl_bytes : 0xFFFFFFFFull), kBufferFlags);
     Hot c0 = load_hot(hot, i0);
-    Hot c1 = load_hot(hot, i0 + 1 < i1 ? i0 + 1 : i0);
+    Hot c1 = load_hot(hot, i0 + 1);
     Ahead<C> A, B;
 #pragma unroll
-    for (int q = 0; q < C; ++q) {
-        A.spt[q] = s.spt[(uint64_t)c0.p * s.D + pcol[q]];
-        A.tau[q] = s.tier_map[(uint64_t)c0.p * s.D + pcol[q]];
-    }
+    for (int q = 0; q < C; ++q) A.v[q] = load_row(slr, voff[q], c0.row);
     // the run's first request is scanned from block 0
     const Cold k0 = load_cold(cold, i0);
     const uint64_t h00 = k0.n ? chash[k0.a] : 0;
     uint32_t b00, b01;
     buckets_of(h00, t.shift, b00, b01);
-    // first test of the current request: block L0; t0 says whether it is
-    // needed at all (not when the cache filter rules the block out on every
-    // decode)
-    uint32_t L0 = 0;
-    bool t0 = k0.n != 0;
-    uint32_t j_prev[C];
+    // the current request's carried tokens lamL = B_tok * L0 and its first
+    // test, of block L0 when t0 = L0 + 1 (0: no test, when block L0 does not
+    // exist or the cache filter rules it out on every decode)
+    uint32_t lamL = 0;
+    uint32_t t0 = k0.n != 0 ? 1u : 0u;
+    uint32_t lam_prev[C];
 #pragma unroll
-    for (int q = 0; q < C; ++q) j_prev[q] = 0;
+    for (int q = 0; q < C; ++q) lam_prev[q] = 0;
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
-    uint64_t pend = kEmptyKey;
+    static_assert(kPer % 2 == 0, "chunks pair up with the two row buffers");
+    uint32_t pc_bits = 0xFFFFFFFFu, pc_idx = 0xFFFFFFFFu;   // gathered keys (empty = ~0)
 
-    auto step = [&](uint32_t i, const Ahead<C> &cur, Ahead<C> &nxt) {
-        const Hot c2 = load_hot(hot, i + 2 < i1 ? i + 2 : i1 - 1);
+    auto step = [&](uint32_t i, uint32_t slot, const Ahead<C> &cur, Ahead<C> &nxt) {
+        const Hot c2 = load_hot(hot, i + 2);
 #pragma unroll
-        for (int q = 0; q < C; ++q) {
-            nxt.spt[q] = s.spt[(uint64_t)c1.p * s.D + pcol[q]];
-            nxt.tau[q] = s.tier_map[(uint64_t)c1.p * s.D + pcol[q]];
-        }
-        const bool more = i + 1 < i1 && c1.tf;
+        for (int q = 0; q < C; ++q) nxt.v[q] = load_row(slr, voff[q], c1.row);
         // prefix lengths: carried where the common leading run decides them
-        uint32_t j[C];
+        uint32_t lam[C];
         lmask need[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) {
-            const bool carry = j_prev[q] < L0;
-            j[q] = carry ? j_prev[q] : L0;
-            need[q] = ballot(!carry) & actm[q];
+            lam[q] = min(lam_prev[q], lamL);
+            need[q] = ballot(lam_prev[q] >= lamL) & actm[q];
         }
         if (t0) {
             // the cold record and the first test's buckets, on the columns
@@ -672,7 +711,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
             }
             Buckets<C> b0;
             load_buckets<C>(col, (uint64_t)hb1 * rs, (uint64_t)hb2 * rs, need, b0);
-            probe_from<W, C>(col, t, rs, chash + a, n, L0, need, j, h0, b0);
+            probe_from<W, C>(col, t, rs, chash + a, n, t0 - 1, need, lam, bt, h0, b0);
         }
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t r_out = 0;
@@ -680,22 +719,22 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         uint32_t cb[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) {
-            j_prev[q] = j[q];
-            const uint32_t x = c0.len - s.block_tokens * j[q];
-            const bool feas = (uint64_t)x < xlim[q];
-            const float cost = pair_score(x, cur.spt[q], tier_latency(s, cur.tau[q] & 3u), dload[q]);
+            lam_prev[q] = lam[q];
+            const uint32_t x = c0.len - lam[q];
+            const bool feas = in_mask(okm[q]) && x <= xm[q];
+            const float cost = fmaf((float)x, cur.v[q].x, cur.v[q].y);
             if (PAIRS && act[q]) {
                 const uint64_t o = (uint64_t)r_out * s.D + d[q];
-                if (po.j) po.j[o] = (uint16_t)j[q];
+                const uint32_t jq = lam[q] / bt;
+                if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                 if (po.feas) po.feas[o] = feas ? 1 : 0;
                 if (po.score) po.score[o] = cost;
-                if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)j[q];
+                if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
             }
-            cb[q] = (act[q] && feas) ? __float_as_uint(cost) : 0xFFFFFFFFu;
+            cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
         }
         // the group's K best: least cost bits, then least decode index, i.e.
         // the lowest lane holding the minimum in the first column that holds it
-        const uint32_t slot = (i - i0) % kPer;
 #pragma unroll
         for (int r = 0; r < K; ++r) {
             uint32_t lm = cb[0];
@@ -710,26 +749,31 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
                 if (m) {
                     const uint32_t l = (uint32_t)__builtin_ctzll(m);
                     dm = base + q * kWave + l;
-                    if (lane == l) cb[q] = 0xFFFFFFFFu;
+                    if (r + 1 < K && lane == l) cb[q] = 0xFFFFFFFFu;
                     break;
                 }
             }
-            if (lane == slot * K + (uint32_t)r) pend = ((uint64_t)mn << 32) | (uint64_t)dm;
+            if (lane == slot * K + (uint32_t)r) {
+                pc_bits = mn;
+                pc_idx = dm;
+            }
         }
-        if (slot == kPer - 1 || i + 1 == i1) {
-            const uint32_t first = i - slot;
-            if (lane < (slot + 1) * K) partial[((uint64_t)grp * n_req + first) * K + lane] = pend;
-            pend = kEmptyKey;
-        }
-        L0 = c1.lcp;
+        lamL = c1.lam;
+        t0 = c1.test;
         c0 = c1;
         c1 = c2;
-        t0 = more;
     };
-    for (uint32_t i = i0; i < i1; i += 2) {
-        step(i, A, B);
-        if (i + 1 >= i1) break;
-        step(i + 1, B, A);
+    for (uint32_t g0 = i0; g0 < i1; g0 += kPer) {
+        const uint32_t g1 = (g0 + kPer < i1) ? g0 + kPer : i1;
+        for (uint32_t i = g0; i < g1; i += 2) {
+            step(i, i - g0, A, B);
+            if (i + 1 >= g1) break;   // an odd count: only the run's last chunk (kPer is even)
+            step(i + 1, i + 1 - g0, B, A);
+        }
+        if (lane < (g1 - g0) * K)
+            partial[((uint64_t)grp * n_req + g0) * K + lane] = ((uint64_t)pc_bits << 32) | (uint64_t)pc_idx;
+        pc_bits = 0xFFFFFFFFu;
+        pc_idx = 0xFFFFFFFFu;
     }
 }
 
@@ -777,7 +821,8 @@ __global__ __launch_bounds__(256) void reduce_kernel(uint32_t n_req, uint32_t nc
 template <int K>
 __global__ __launch_bounds__(256) void sweep_kernel(Snap s, Reqs rq, const float *__restrict__ util_scen,
                                                     const uint16_t *__restrict__ jT,
-                                                    const int32_t *__restrict__ base_idx, uint32_t k,
+                                                    const int32_t *__restrict__ base_idx,
+                                                    const float *__restrict__ base_score, uint32_t k,
                                                     int32_t *__restrict__ out_idx,
                                                     float *__restrict__ out_score,
                                                     unsigned long long *__restrict__ flips) {
@@ -789,7 +834,10 @@ __global__ __launch_bounds__(256) void sweep_kernel(Snap s, Reqs rq, const float
         uint32_t p, len, n;
         uint64_t a;
         uint64_t o = ((uint64_t)sc * rq.n_req + r) * k;
-        if (!request_ok(rq, s, r, p, len, a, n)) {
+        // invalid requests (also those the batch selection found invalid:
+        // a zero hash, a run too long for 16-bit prefix lengths) have a NaN
+        // selection score
+        if (!request_ok(rq, s, r, p, len, a, n) || __builtin_isnan(base_score[r])) {
             for (uint32_t i = 0; i < k; ++i) {
                 out_idx[o + i] = -1;
                 out_score[o + i] = __builtin_nanf("");
@@ -1262,7 +1310,7 @@ struct netkv_ctx {
     uint32_t *queue = nullptr;
     uint32_t *batch = nullptr;
     uint64_t *adm_prev = nullptr;
-    float *spt = nullptr;        // derived per call: [P*D]
+    float2 *sl = nullptr;        // derived per call: [P*D]
     float *dbase = nullptr;      // [D]
     uint64_t *dxlim = nullptr;   // [D]
     float bw[4] = {0, 0, 0, 0}, lat[4] = {0, 0, 0, 0};
@@ -1415,7 +1463,8 @@ Snap make_snap(netkv_handle h) {
     s.block_tokens = h->block_tokens;
     s.P = h->P;
     s.D = h->D;
-    s.spt = h->spt;
+    s.sl = h->sl;
+    s.slp = sl_pitch(h->D);
     s.dbase = h->dbase;
     s.dxlim = h->dxlim;
     s.policy = h->policy_opt;
@@ -1462,6 +1511,7 @@ netkv_status ready(netkv_handle h) {
 
 constexpr int kSpec = 4;            // blocks tested together per extension step at one decode per lane
 constexpr uint32_t kLcpLanes = 8;   // lanes per sorted position in lcp_kernel
+constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
 // Radix sort configuration of the batch-order keys (rocPRIM's own choice of
 // algorithm by size).
@@ -1475,7 +1525,7 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         h->sort_tmp_bytes = 0;
         if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
             dalloc(h->vals_in, R) != hipSuccess || dalloc(h->perm, R) != hipSuccess ||
-            dalloc(h->hot, R) != hipSuccess || dalloc(h->cold, R) != hipSuccess)
+            dalloc(h->hot, R + kHotPad) != hipSuccess || dalloc(h->cold, R) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
         size_t bytes = 0;
         if (rocprim::radix_sort_pairs<SortConfig>(nullptr, bytes, h->keys_in, h->keys_out, h->vals_in, h->perm,
@@ -1561,7 +1611,7 @@ hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, co
 // The whole selection of one batch on `st`: validate + order, sort, common
 // prefixes, scan, merge.
 netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
-                        const PairOut &po, bool pairs, hipStream_t st) {
+                        const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st) {
     const uint64_t R = req->n_req;
     const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
     const uint32_t C = cols_per_lane(h->D, h->cols_opt);
@@ -1572,9 +1622,9 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     const Table t = make_table(h);
     const Reqs rq = make_reqs(req);
     const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
-    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->spt, h->dbase,
+    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
                        h->dxlim);
-    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, h->keys_in,
+    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
                        h->vals_in, h->errword, h->zflag);
     if (rq.n_hashes)
         hipLaunchKernelGGL(count_zero_kernel, dim3(grid_for(rq.n_hashes, 256, 8192)), dim3(256), 0, st, rq.hashes,
@@ -1585,8 +1635,8 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     size_t tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                     (uint32_t)R, 0, 32, st));
-    hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
-                       (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->hot, h->cold,
+    hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)(((R + kHotPad) * kLcpLanes + 255) / 256)), dim3(256), 0,
+                       st, rq, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->hot, h->cold,
                        h->n_valid);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
@@ -1645,7 +1695,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->queue);
         dfree(h->batch);
         dfree(h->adm_prev);
-        dfree(h->spt);
+        dfree(h->sl);
         dfree(h->dbase);
         dfree(h->dxlim);
         dfree(h->table);
@@ -1676,7 +1726,8 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
     if (!o) return fail(h, NETKV_EINVAL, "oracle is NULL");
     const uint32_t P = o->n_prefill, D = o->n_decode;
     if (P == 0 || D == 0) return fail(h, NETKV_EINVAL, "n_prefill and n_decode must be >= 1");
-    if ((uint64_t)P * D > (1ull << 34)) return fail(h, NETKV_EINVAL, "P*D too large");
+    if (D >= (1u << 28) || (uint64_t)P * sl_pitch(D) * 8 >= (1ull << 32))
+        return fail(h, NETKV_EINVAL, "n_prefill * (n_decode + 32) must be < 2^29");
     if (!o->tier_map || !o->util || !o->n_inflight || !o->free_mem || !o->queue_depth || !o->batch_size)
         return fail(h, NETKV_EINVAL, "oracle arrays must not be NULL");
     for (int i = 0; i < 4; ++i) {
@@ -1735,9 +1786,9 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
                     (bad & 2) ? " util outside [0,1) or NaN" : "", (bad & 4) ? " batch_size > beta_max" : "");
     }
     if (!h->have_snap || h->P != P || h->D != D) {
-        dfree(h->spt); dfree(h->dbase); dfree(h->dxlim);
+        dfree(h->sl); dfree(h->dbase); dfree(h->dxlim);
         h->have_snap = false;
-        if (dalloc(h->spt, npd) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
+        if (dalloc(h->sl, (uint64_t)P * sl_pitch(D)) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
             dalloc(h->dxlim, D) != hipSuccess) {
             cleanup();
             return fail(h, NETKV_ENOMEM, "snapshot allocation failed");
@@ -1961,7 +2012,7 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
         po.score = pairs->score;
         want_pairs = po.j || po.feas || po.score;
     }
-    return run_select(h, req, k, out_idx, out_score, po, want_pairs, s);
+    return run_select(h, req, k, out_idx, out_score, po, want_pairs, 0xFFFFFFFFu, s);
 }
 
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen, const float *util_scen,
@@ -1999,7 +2050,7 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
     PairOut po{nullptr, nullptr, nullptr, h->jT};
     {
         TimingOff off(h);  // only the sweep kernel is timed
-        if ((st = run_select(h, req, 1, h->base_idx, h->base_score, po, true, s))) return st;
+        if ((st = run_select(h, req, 1, h->base_idx, h->base_score, po, true, kMaxBlocks16, s))) return st;
     }
     if (out_flips) {
         hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(2ull * n_scen, 256)), dim3(256), 0, s, out_flips,
@@ -2010,16 +2061,16 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
     dim3 grid((uint32_t)((R + 255) / 256), n_scen);
     unsigned long long *fl = (unsigned long long *)out_flips;
     if (k <= 1)
-        hipLaunchKernelGGL(sweep_kernel<1>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, k, out_idx,
+        hipLaunchKernelGGL(sweep_kernel<1>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
                            out_score, fl);
     else if (k <= 2)
-        hipLaunchKernelGGL(sweep_kernel<2>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, k, out_idx,
+        hipLaunchKernelGGL(sweep_kernel<2>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
                            out_score, fl);
     else if (k <= 4)
-        hipLaunchKernelGGL(sweep_kernel<4>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, k, out_idx,
+        hipLaunchKernelGGL(sweep_kernel<4>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
                            out_score, fl);
     else
-        hipLaunchKernelGGL(sweep_kernel<8>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, k, out_idx,
+        hipLaunchKernelGGL(sweep_kernel<8>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
                            out_score, fl);
     HIPCHK(h, hipGetLastError());
     HIPCHK(h, time_end(h, s));
@@ -2186,7 +2237,7 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     PairOut po{h->seq_j, nullptr, nullptr, nullptr};
     {
         TimingOff off(h);  // only the sequential kernel is timed
-        if ((st = run_select(h, req, 1, out_idx, out_score, po, true, s))) return st;
+        if ((st = run_select(h, req, 1, out_idx, out_score, po, true, kMaxBlocks16, s))) return st;
     }
     // requests grouped by prefill instance, batch order kept inside a group
     const Reqs rq = make_reqs(req);

@@ -346,3 +346,61 @@ def test_kernel_timing_mean_over_launches(nk):
     with pytest.raises(nk.NetKVError):
         nk.netkv_kernel_ms(sel.h)
     sel.close()
+
+
+def test_long_runs_and_invalid_requests_in_every_mode(nk):
+    """Runs longer than 65535 blocks (B_tok = 1): the batch selection scores
+    them exactly and writes prefix lengths saturated at 65535; the ranking
+    sweep and the sequential form, which keep prefix lengths in 16 bits,
+    answer them (and a request holding the reserved hash 0) with -1 / NaN
+    and report them."""
+    _say("long runs, B_tok 1")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=6, block_tokens=1)
+    snap = W.make_snapshot(cfg, 21)
+    D = cfg.n_decode
+    rng = np.random.default_rng(21)
+    chain = np.arange(1, 70001, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15) | np.uint64(1)
+    # decode 0 holds the whole chain, decode 1 its first 100 blocks, the rest random filler
+    sets = [chain, chain[:100]] + [rng.integers(1, 2**63, 500, dtype=np.uint64) for _ in range(D - 2)]
+    cache = dict(n_decode=D, hash_off=np.concatenate([[0], np.cumsum([len(x) for x in sets])]).astype(np.uint64),
+                 hashes=np.concatenate(sets).astype(np.uint64))
+    lens = np.array([70000, 70500, 1000, 900, 40, 66000], dtype=np.uint32)
+    runs = [chain, np.concatenate([chain, rng.integers(1, 2**63, 500, dtype=np.uint64)]),
+            chain[:1000], rng.integers(1, 2**63, 900, dtype=np.uint64), chain[:40],
+            np.concatenate([chain[:50], rng.integers(1, 2**63, 65950, dtype=np.uint64)])]
+    runs[3][17] = 0   # reserved value: request 3 is invalid everywhere
+    req = dict(n_req=6, prefill=rng.integers(0, cfg.n_prefill, 6).astype(np.uint32), len_tokens=lens,
+               hash_off=np.concatenate([[0], np.cumsum([len(x) for x in runs])]).astype(np.uint64),
+               hashes=np.concatenate(runs).astype(np.uint64))
+    sel = _gpu(nk, snap, cache)
+    rd = nk.requests_to_device(req, sel.device)
+    out = sel.select(rd, k=2, pairs=True)
+    with pytest.raises(nk.NetKVError):
+        sel.sync_errors()
+    idx = nk.to_numpy(out["idx"]).reshape(-1, 2)
+    sc = nk.to_numpy(out["score"]).reshape(-1, 2)
+    good = [0, 1, 2, 4, 5]
+    o = oracle.select(snap, cache, subset_requests(req, good), k=2, pairs=True)
+    assert int(o["j"][0, 0]) == 70000 and int(o["j"][1, 0]) == 70000
+    check_topk(idx[good], sc[good], o["idx"], o["cost"], o["feasible"])
+    j = nk.to_numpy(out["pairs"]["prefix_blocks"]).reshape(6, D)[good].astype(np.int64)
+    assert np.array_equal(j, np.minimum(o["j"], 65535))
+    assert (idx[3] == -1).all() and np.isnan(sc[3]).all()
+    # ranking sweep under the snapshot's own congestion, and the sequential form
+    us = nk.to_device(np.asarray(snap["util"], np.float32).reshape(-1), sel.device)
+    sw = sel.rank_sweep(rd, us, k=2)
+    with pytest.raises(nk.NetKVError):
+        sel.sync_errors()
+    sq = sel.select_sequential(rd, cap=0)
+    with pytest.raises(nk.NetKVError):
+        sel.sync_errors()
+    si = nk.to_numpy(sw["idx"]).reshape(-1, 2)
+    ss = nk.to_numpy(sw["score"]).reshape(-1, 2)
+    qi, qs = nk.to_numpy(sq["idx"]), nk.to_numpy(sq["score"])
+    for r in (0, 1, 3, 5):   # more than 65535 blocks, or a zero hash
+        assert (si[r] == -1).all() and np.isnan(ss[r]).all()
+        assert qi[r] == -1 and np.isnan(qs[r])
+    for r in (2, 4):
+        assert np.array_equal(si[r], idx[r]) and np.array_equal(ss[r], sc[r])
+        assert qi[r] == idx[r, 0] and qs[r] == sc[r, 0]
+    sel.close()

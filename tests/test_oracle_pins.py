@@ -347,6 +347,23 @@ def test_full_hit_has_no_transfer_bytes_but_a_partial_block_does():
     np.testing.assert_allclose(out["cost"][:, 0], [0.0, 8 / 1e3])
 
 
+def test_runs_longer_than_16_bits():
+    """Sec. III-B bounds no run: with one-token blocks a 70,000-block request
+    fully resident on decode 0 has j = 70,000 and no transfer bytes there,
+    and 70,000 - 100 non-cached tokens on decode 1, which holds its first 100
+    blocks; the sweep, which reuses j, agrees with the selection."""
+    h = list(range(1, 70001))
+    snap = tiny_snapshot(1, 2, [0, 0], [0, 0], bw=(1e3,) * 4, alpha=0.0, bpt=1, block_tokens=1)
+    cache = caches([h, h[:100]])
+    out = oracle.select(snap, cache, requests([(0, 70000, h)]), k=2, pairs=True)
+    assert out["j"][0].tolist() == [70000, 100]
+    np.testing.assert_allclose(out["cost"][0], [0.0, 69900 / 1e3])
+    assert out["idx"][0].tolist() == [0, 1]
+    sw = oracle.rank_sweep(snap, cache, requests([(0, 70000, h)]), np.zeros((1, 2), np.float32), k=2)
+    assert sw["idx"][0, 0].tolist() == [0, 1]
+    np.testing.assert_allclose(sw["score"][0, 0], [0.0, 69900 / 1e3])
+
+
 # ---------------------------------------------------------------- prefix match
 
 def _brute_lcp(hs, kset):
