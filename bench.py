@@ -121,9 +121,10 @@ def main():
     sel.load_snapshot(snap)
     sel.load_cache(cache, 0.5)
     torch.cuda.synchronize()
-    slots, tbytes = netkv.netkv_cache_info(sel.h)
-    log(f"snapshot + tables loaded in {time.time() - t0:.1f}s: {slots} slots/decode, "
-        f"{tbytes / 2**30:.2f} GiB")
+    ci = netkv.netkv_cache_info(sel.h)
+    log(f"snapshot + holder index loaded in {time.time() - t0:.1f}s: {ci['distinct_hashes']} distinct "
+        f"hashes ({ci['shared_hashes']} on several decodes), {ci['index_slots']} slots, "
+        f"{ci['index_bytes'] / 2**30:.2f} GiB")
     rd = netkv.requests_to_device(req, dev)
     R, D, P = cfg.n_requests, cfg.n_decode, cfg.n_prefill
     k = 1
@@ -262,7 +263,7 @@ def main():
         "config": {
             "workload": cfg.name,
             "requests": R, "decodes": D, "prefills": P, "gpus_modelled": cfg.cluster.n_gpus,
-            "resident_hashes_per_decode": cfg.cache_per_decode, "slots_per_decode": slots,
+            "resident_hashes_per_decode": cfg.cache_per_decode, "index": ci,
             "block_tokens": cfg.block_tokens, "mean_blocks_per_request": float(nblk.mean()),
             "k": k, "parallelism": "single-gpu", "first_miss_carry": not args.no_reuse,
             "run_len": args.run_len or "auto", "policy": args.policy,

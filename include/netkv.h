@@ -100,16 +100,18 @@ netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stre
  * decode instances as CSR: the hashes of decode d are
  * hashes[hash_off[d] .. hash_off[d+1]), n_hashes = hash_off[n_decode].
  * Host or device pointers.  Value 0 is reserved (EINVAL); repeated hashes
- * of one decode are allowed and count once.  Builds one open-addressed
- * table per decode with at most `max_load_factor` (0 < lf < 1) occupancy
- * (capped at 0.85; a build that cannot place every hash is retried with
- * twice the buckets, twice), and one filter over the union of all sets (8 bits per
- * resident hash) that proves a hash absent from every decode, so a scan
- * can skip that hash's per-decode tests without changing any result.
- * Synchronous.  EINVAL: bad CSR, hash 0, lf out of range, D different
- * from a loaded snapshot; ECAPACITY: a table would need more than 2^31
- * slots, or could not be built even at four times the planned buckets;
- * ENOMEM: out of device memory. */
+ * of one decode are allowed and count once.  Builds the holder index: one
+ * open-addressed set of every distinct resident hash, with at most
+ * `max_load_factor` (0 < lf < 1) occupancy (capped at 0.85; a build that
+ * cannot place every hash is retried with twice the buckets, twice), and
+ * for each hash its holders -- one decode, or a bitmap over the decodes
+ * (ceil(n_decode / 256) * 32 bytes per hash held by two or more) -- so
+ * that one lookup answers a membership test on every decode at once.
+ * Synchronous; needs about 28 bytes of temporary device memory per
+ * resident hash while building.  EINVAL: bad CSR, hash 0, lf out of range,
+ * D different from a loaded snapshot; ECAPACITY: 2^31 or more resident
+ * hashes, a set of more than 2^31 slots, or one that could not be built
+ * even at four times the planned buckets; ENOMEM: out of device memory. */
 netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t *hash_off,
                               const uint64_t *hashes, uint64_t n_hashes, float max_load_factor,
                               void *stream);
@@ -237,8 +239,7 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
  *                        batch order when it lies inside their common
  *                        leading blocks (an exact identity, no probe);
  *                        0: nothing is carried, every pair is scanned
- *                        from block 0 (a block that the cache filter
- *                        proves absent from every decode is not probed);
+ *                        from block 0;
  *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
  *                        automatic (2 on pools of 256+ decodes, else 1), 1, 2, 4.
  * and one option that does change results, selecting the rung of the
@@ -250,9 +251,13 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
 enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3, NETKV_OPT_POLICY = 4 };
 netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 
-/* Table geometry of the loaded cache: slots per decode (a power of two)
- * and the device bytes of all tables and the filter. */
-netkv_status netkv_cache_info(netkv_handle h, uint64_t *slots_per_decode, uint64_t *table_bytes);
+/* Geometry of the loaded cache's holder index (any pointer may be NULL):
+ * slots of the hash set (two per bucket, a power of two of buckets),
+ * distinct resident hashes, hashes resident on two or more decodes (one
+ * bitmap row each), and device bytes of the set and the bitmaps.
+ * ENOTREADY with no cache loaded. */
+netkv_status netkv_cache_info(netkv_handle h, uint64_t *index_slots, uint64_t *distinct_hashes,
+                              uint64_t *shared_hashes, uint64_t *index_bytes);
 
 #ifdef __cplusplus
 }

@@ -53,8 +53,7 @@ constexpr int kWavesPerBlock = 4;
 constexpr uint32_t kXcds = 8;   // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
-constexpr uint32_t kFib32 = 0x9E3779B1u;
-constexpr uint32_t kMix32 = 0x85EBCA77u;
+constexpr uint64_t kMix64 = 0xBF58476D1CE4E5B9ull;
 constexpr uint64_t kEmptyKey = ~0ull; // empty top-k entry (sorts last)
 
 enum : uint32_t {
@@ -90,12 +89,24 @@ struct Snap {
     const uint64_t *dxlim;   // [D] x = l - lambda is feasible iff x < dxlim
 };
 
+// The holder index of the resident block hashes K_d of all decodes: every
+// distinct resident hash once, in a bucketized two-choice cuckoo set (two
+// candidate buckets of two 8-byte slots; 0 = empty), and in a parallel array
+// the 32-bit holder value of the key in the same slot:
+//   kHeldOne | d -- the hash is resident on decode d alone;
+//   row          -- it is resident on two or more decodes, the set bits of
+//                   row `row` of the bitmap pool (bit d % 64 of word d / 64).
+// A hash that is not in the set is resident nowhere (kNoHolder).  One lookup
+// answers a membership test for every decode at once.
+constexpr uint32_t kHeldOne = 0x80000000u;
+constexpr uint32_t kNoHolder = 0xFFFFFFFFu;
+
 struct Table {
-    const uint64_t *keys;   // [buckets][pitch][2]
-    uint32_t shift;         // 32 - log2(buckets)
-    uint32_t pitch;
-    const uint64_t *any;    // [2^(64 - any_shift)] resident-anywhere filter words
-    uint32_t any_shift;
+    const uint64_t *keys;   // [buckets][2] distinct resident hashes
+    const uint32_t *vals;   // [buckets][2] holder values
+    const uint64_t *bits;   // [rows][bpitch] holder bitmaps (at least one row, row 0 of zeros if unused)
+    uint32_t shift;         // 64 - log2(buckets)
+    uint32_t bpitch;        // 64-bit words per bitmap row, a multiple of 4
 };
 
 struct Reqs {
@@ -114,14 +125,15 @@ struct PairOut {
     uint16_t *jT;       // [D][R] (internal, for the sweep)
 };
 
-// The two candidate buckets of hash h in a table of 2^b buckets (shift =
-// 32 - b): the hash is folded to 32 bits and spread by two multiplicative
-// (Fibonacci-style) hashes; the second bucket is the first xor a nonzero
-// value below 2^b, so the two always differ.
+// The two candidate buckets of hash h in a set of 2^b buckets (shift =
+// 64 - b): the top b bits of two 64-bit multiplicative hashes of the whole
+// key (Fibonacci hashing, and the multiplier of splitmix64 after an
+// xor-shift), the second xored onto the first with its low bit set, so the
+// two buckets always differ.  Both use all 64 bits, so keys that agree in
+// part of their bits still get independent bucket pairs.
 __host__ __device__ inline void buckets_of(uint64_t h, uint32_t shift, uint32_t &b1, uint32_t &b2) {
-    const uint32_t fold = (uint32_t)h ^ (uint32_t)(h >> 32);
-    b1 = (fold * kFib32) >> shift;
-    b2 = b1 ^ (((fold * kMix32) >> shift) | 1u);
+    b1 = (uint32_t)((h * kGolden) >> shift);
+    b2 = b1 ^ ((uint32_t)(((h ^ (h >> 31)) * kMix64) >> shift) | 1u);
 }
 
 // Row pitch (elements) of the per-(p, d) float2 rows: D rounded up to whole
@@ -133,32 +145,24 @@ __host__ __device__ inline uint32_t sl_pitch(uint32_t D) {
     return lines * 16u;
 }
 
-// The resident-anywhere filter: a blocked Bloom filter over the union of all
-// decodes' resident hashes, one 64-bit word per key with four bits set in
-// it.  A clear bit proves that no decode holds the key; a full match only
-// says it may be held somewhere, so a scan that skips a test on a clear bit
-// stays exact.  Word from the top bits of one multiplicative hash, bit
-// positions from the top 24 bits of another.
-constexpr uint64_t kAnyWordMul = 0xD1B54A32D192ED03ull;
-constexpr uint64_t kAnyBitsMul = 0xAEF17502108EF2D9ull;
-
-__host__ __device__ inline void any_of(uint64_t h, uint32_t any_shift, uint64_t &word, uint64_t &mask) {
-    word = (h * kAnyWordMul) >> any_shift;
-    const uint32_t y = (uint32_t)((h * kAnyBitsMul) >> 40);
-    mask = (1ull << (y & 63u)) | (1ull << ((y >> 6) & 63u)) | (1ull << ((y >> 12) & 63u)) |
-           (1ull << ((y >> 18) & 63u));
+// Holder value of h, by one thread (vector loads of both candidate buckets).
+__device__ inline uint32_t holder_lane(const Table &t, uint64_t h) {
+    if (h == 0) return kNoHolder;
+    uint32_t b1, b2;
+    buckets_of(h, t.shift, b1, b2);
+    const ulonglong2 k1 = *(const ulonglong2 *)(t.keys + 2 * (uint64_t)b1);
+    const ulonglong2 k2 = *(const ulonglong2 *)(t.keys + 2 * (uint64_t)b2);
+    const uint2 v1 = *(const uint2 *)(t.vals + 2 * (uint64_t)b1);
+    const uint2 v2 = *(const uint2 *)(t.vals + 2 * (uint64_t)b2);
+    return k1.x == h ? v1.x : k1.y == h ? v1.y : k2.x == h ? v2.x : k2.y == h ? v2.y : kNoHolder;
 }
 
-__device__ inline bool maybe_anywhere(const uint64_t *__restrict__ any, uint32_t any_shift, uint64_t h) {
-    uint64_t w, m;
-    any_of(h, any_shift, w, m);
-    return (any[w] & m) == m;
-}
-
-// Is h in bucket b of the table column `col` (this decode's column)?
-__device__ inline bool bucket_has(const uint64_t *__restrict__ col, const Table &t, uint32_t b, uint64_t h) {
-    const ulonglong2 v = *(const ulonglong2 *)(col + (uint64_t)b * t.pitch * 2);
-    return v.x == h || v.y == h;
+// Is h resident on decode d?
+__device__ inline bool holds(const Table &t, uint64_t h, uint32_t d) {
+    const uint32_t v = holder_lane(t, h);
+    if (v == kNoHolder) return false;
+    if (v & kHeldOne) return (v & ~kHeldOne) == d;
+    return (t.bits[(uint64_t)v * t.bpitch + d / 64u] >> (d % 64u)) & 1ull;
 }
 
 // T_queue + T_decode of decode d, scaled by alpha (Sec. IV-B, Eqs. (6)-(7)).
@@ -294,8 +298,9 @@ __global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict_
 // j = j'), and otherwise scanning resumes at block L (j' >= L implies blocks
 // 0..L-1 are resident).  Longest first, a request that is a prefix of its
 // predecessor has L = n_r and never probes; one that leaves the shared chain
-// first resumes at a block of its own, which the cache filter mostly rules
-// out.  The order changes which probes are made, never a result.
+// first resumes at a block of its own, which usually no decode holds (known
+// from the holder index before the scan, so no probe).  The order changes
+// which probes are made, never a result.
 
 constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
@@ -303,9 +308,9 @@ constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
 // One sorted request, everything the scan needs without indirection.
 // The part every scan step reads (one 16-byte scalar load) ...
 struct alignas(16) Hot {
-    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * D * 8
-    uint32_t test;   // lcp + 1 if block lcp exists and the filter admits its hash (a carried
-                     // scan tests it), else 0
+    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * slp * 8
+    uint32_t test;   // lcp + 1 if block lcp exists and some decode holds it (a carried scan
+                     // tests it), else 0
     uint32_t len;    // input tokens
     uint32_t lam;    // B_tok * lcp: tokens of the leading blocks in common with the
                      // previous sorted request
@@ -315,11 +320,10 @@ constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead 
 // ... and the part read only by requests that probe (and for per-pair output).
 struct alignas(16) Cold {
     uint64_t a;      // offset of the hash run
-    uint64_t hf;     // hash of block lcp, 0 if lcp == n
     uint32_t r;      // request index in the caller's batch
     uint32_t n;      // hashed blocks
-    uint32_t b1;     // candidate buckets of hf
-    uint32_t b2;
+    uint32_t v;      // holder value of block lcp (kNoHolder if there is no such block)
+    uint32_t pad[3];
 };
 
 struct Order {
@@ -440,13 +444,13 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_
     if (sub != 0) return;
     Cold c;
     c.a = a;
-    c.hf = l < nr ? rq.hashes[a + l] : 0;
     c.r = r;
     c.n = (uint32_t)nr;
-    buckets_of(c.hf, t.shift, c.b1, c.b2);
+    c.v = l < nr ? holder_lane(t, rq.hashes[a + l]) : kNoHolder;
+    c.pad[0] = c.pad[1] = c.pad[2] = 0;
     Hot o;
     o.row = rq.prefill[r] * slp * (uint32_t)sizeof(float2);   // < 2^32 (checked at load)
-    o.test = l < nr && maybe_anywhere(t.any, t.any_shift, c.hf) ? (uint32_t)l + 1 : 0;
+    o.test = c.v != kNoHolder ? (uint32_t)l + 1 : 0;
     o.len = rq.len[r];
     o.lam = bt * (uint32_t)l;   // <= len
     hot[i] = o;
@@ -478,11 +482,9 @@ __device__ inline Cold load_cold(const Cold *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
     Cold x;
     x.a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
-    x.hf = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
-    x.r = w[4];
-    x.n = w[5];
-    x.b1 = w[6];
-    x.b2 = w[7];
+    x.r = w[2];
+    x.n = w[3];
+    x.v = w[4];
     return x;
 }
 
@@ -495,80 +497,72 @@ using lmask = uint64_t;
 __device__ inline lmask ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 __device__ inline bool in_mask(lmask m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
 
-// The two candidate buckets of one hash on the C columns of a lane.
-template <int C>
-struct Buckets {
-    ulonglong2 v1[C], v2[C];
-};
+// Holder value of a hash that is the same on every lane (scalar loads of
+// both candidate buckets' keys and values).
+__device__ inline uint32_t holder_uniform(const Table &t, uint64_t h) {
+    uint32_t b1, b2;
+    buckets_of(h, t.shift, b1, b2);
+    const cptr<uint64_t> k = as_const(t.keys);
+    const cptr<uint32_t> v = as_const(t.vals);
+    const uint64_t k10 = k[2 * (uint64_t)b1], k11 = k[2 * (uint64_t)b1 + 1];
+    const uint64_t k20 = k[2 * (uint64_t)b2], k21 = k[2 * (uint64_t)b2 + 1];
+    const uint32_t v10 = v[2 * (uint64_t)b1], v11 = v[2 * (uint64_t)b1 + 1];
+    const uint32_t v20 = v[2 * (uint64_t)b2], v21 = v[2 * (uint64_t)b2 + 1];
+    if (h == 0) return kNoHolder;
+    return k10 == h ? v10 : k11 == h ? v11 : k20 == h ? v20 : k21 == h ? v21 : kNoHolder;
+}
 
-// Load the buckets at element offsets row1 / row2 of each column, on the
-// lanes in go[q] only (zero elsewhere: no key is 0).
+// Lane masks of the holders of a (uniform) holder value on the C columns of
+// the wavefront whose first decode is `base` (a multiple of 64 * C): the
+// wavefront's words of the bitmap row (always loaded, from row 0 when the
+// value is not a row, so that the load does not wait on a branch), or the
+// one lane of a single holder, or none.
 template <int C>
-__device__ inline void load_buckets(const uint64_t *const (&col)[C], uint64_t row1, uint64_t row2,
-                                    const lmask (&go)[C], Buckets<C> &b) {
+__device__ inline void holder_masks(const Table &t, uint32_t v, uint32_t base, lmask (&m)[C]) {
+    const bool row = v < kHeldOne;
+    const cptr<uint64_t> w = as_const(t.bits + (uint64_t)(row ? v : 0u) * t.bpitch + base / kWave);
+    const uint32_t d = v & ~kHeldOne;
 #pragma unroll
     for (int q = 0; q < C; ++q) {
-        b.v1[q] = make_ulonglong2(0, 0);
-        b.v2[q] = make_ulonglong2(0, 0);
-        if (in_mask(go[q])) {
-            b.v1[q] = *(const ulonglong2 *)(col[q] + row1);
-            b.v2[q] = *(const ulonglong2 *)(col[q] + row2);
-        }
+        const uint32_t o = d - (base + (uint32_t)q * kWave);
+        const lmask one = (v != kNoHolder && o < (uint32_t)kWave) ? (1ull << o) : 0ull;
+        m[q] = row ? w[q] : one;
     }
 }
 
-// A membership test of h (nonzero) on the C columns: alive[q] keeps the
-// lanes whose column holds h in one of its two buckets.
-template <int C>
-__device__ inline void member(uint64_t h, const Buckets<C> &b, lmask (&alive)[C]) {
-#pragma unroll
-    for (int q = 0; q < C; ++q)
-        alive[q] &= ballot(b.v1[q].x == h) | ballot(b.v1[q].y == h) | ballot(b.v2[q].x == h) |
-                    ballot(b.v2[q].y == h);
-}
-
 // First-miss scan of one request's run on the columns in alive[] (the
-// columns that need it), starting at block `start` (uniform, < n) whose hash
-// h0 and buckets b0 were loaded beforehand.  Past the first block, W blocks
-// are tested per step with all their bucket loads issued together.  lam[]
+// columns that need it), starting at block `start` (uniform, < n) whose
+// holder value v0 was looked up beforehand.  Past the first block, W blocks
+// are looked up per step, their holder lookups issued together.  lam[]
 // holds bt * start on entry for those columns and bt * (first-miss index)
 // on return (bt = tokens per block).
 template <int W, int C>
-__device__ inline void probe_from(const uint64_t *const (&col)[C], const Table &t, uint64_t rs, cptr<uint64_t> run,
-                                  uint32_t n, uint32_t start, lmask (&alive)[C], uint32_t (&lam)[C], uint32_t bt,
-                                  uint64_t h0, const Buckets<C> &b0) {
-    member<C>(h0, b0, alive);
+__device__ inline void probe_from(const Table &t, uint32_t base, cptr<uint64_t> run, uint32_t n, uint32_t start,
+                                  lmask (&alive)[C], uint32_t (&lam)[C], uint32_t bt, uint32_t v0) {
+    lmask m[C];
+    holder_masks<C>(t, v0, base, m);
 #pragma unroll
-    for (int q = 0; q < C; ++q) lam[q] += in_mask(alive[q]) ? bt : 0u;
+    for (int q = 0; q < C; ++q) {
+        alive[q] &= m[q];
+        lam[q] += in_mask(alive[q]) ? bt : 0u;
+    }
     for (uint32_t i0 = start + 1; i0 < n; i0 += W) {
         lmask any = 0;
 #pragma unroll
         for (int q = 0; q < C; ++q) any |= alive[q];
         if (!any) break;
-        uint64_t h[W];
-        if (i0 + W <= n) {
+        uint32_t v[W];
 #pragma unroll
-            for (int w = 0; w < W; ++w) h[w] = run[i0 + w];
-        } else {
-#pragma unroll
-            for (int w = 0; w < W; ++w) h[w] = i0 + w < n ? run[i0 + w] : 0;
-        }
-        Buckets<C> bw[W];
-#pragma unroll
-        for (int w = 0; w < W; ++w) {
-            uint32_t b1, b2;
-            buckets_of(h[w], t.shift, b1, b2);
-            lmask go[C];
-#pragma unroll
-            for (int q = 0; q < C; ++q) go[q] = i0 + w < n ? alive[q] : 0;
-            load_buckets<C>(col, (uint64_t)b1 * rs, (uint64_t)b2 * rs, go, bw[w]);
-        }
+        for (int w = 0; w < W; ++w) v[w] = i0 + w < n ? holder_uniform(t, run[i0 + w]) : kNoHolder;
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             if (i0 + w >= n) break;
-            member<C>(h[w], bw[w], alive);
+            holder_masks<C>(t, v[w], base, m);
 #pragma unroll
-            for (int q = 0; q < C; ++q) lam[q] += in_mask(alive[q]) ? bt : 0u;
+            for (int q = 0; q < C; ++q) {
+                alive[q] &= m[q];
+                lam[q] += in_mask(alive[q]) ? bt : 0u;
+            }
         }
     }
 }
@@ -629,12 +623,10 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     if (i0 >= nv) return;
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
     const uint32_t base = grp * (kWave * C);
-    const uint64_t rs = 2ull * t.pitch;   // elements per bucket row
     const uint32_t bt = s.block_tokens;
     uint32_t d[C], voff[C], xm[C];
     bool act[C];
     lmask actm[C], okm[C];
-    const uint64_t *col[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
@@ -642,7 +634,6 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         actm[q] = ballot(act[q]);
         const uint32_t pc = act[q] ? d[q] : 0;
         voff[q] = pc * (uint32_t)sizeof(float2);
-        col[q] = t.keys + 2 * (uint64_t)pc;
         // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
         // xlim >= 1 (capped to 32 bits, as x is); xlim = 0 never is
         const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
@@ -662,14 +653,12 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     for (int q = 0; q < C; ++q) A.v[q] = load_row(slr, voff[q], c0.row);
     // the run's first request is scanned from block 0
     const Cold k0 = load_cold(cold, i0);
-    const uint64_t h00 = k0.n ? chash[k0.a] : 0;
-    uint32_t b00, b01;
-    buckets_of(h00, t.shift, b00, b01);
+    const uint32_t v00 = k0.n ? holder_uniform(t, chash[k0.a]) : kNoHolder;
     // the current request's carried tokens lamL = B_tok * L0 and its first
     // test, of block L0 when t0 = L0 + 1 (0: no test, when block L0 does not
-    // exist or the cache filter rules it out on every decode)
+    // exist or no decode holds it)
     uint32_t lamL = 0;
-    uint32_t t0 = k0.n != 0 ? 1u : 0u;
+    uint32_t t0 = v00 != kNoHolder ? 1u : 0u;
     uint32_t lam_prev[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) lam_prev[q] = 0;
@@ -690,28 +679,22 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
             need[q] = ballot(lam_prev[q] >= lamL) & actm[q];
         }
         if (t0) {
-            // the cold record and the first test's buckets, on the columns
-            // that need it (after the filter only a small share of requests
-            // probes at all, so nothing is fetched ahead for this)
-            uint64_t a, h0;
-            uint32_t n, hb1, hb2;
+            // the cold record (holder of the first tested block) and the
+            // first-miss scan on the columns that need it (only a small
+            // share of requests probes at all, so nothing is fetched ahead)
+            uint64_t a;
+            uint32_t n, v0;
             if (i == i0) {
                 a = k0.a;
                 n = k0.n;
-                h0 = h00;
-                hb1 = b00;
-                hb2 = b01;
+                v0 = v00;
             } else {
                 const Cold k = load_cold(cold, i);
                 a = k.a;
                 n = k.n;
-                h0 = k.hf;
-                hb1 = k.b1;
-                hb2 = k.b2;
+                v0 = k.v;
             }
-            Buckets<C> b0;
-            load_buckets<C>(col, (uint64_t)hb1 * rs, (uint64_t)hb2 * rs, need, b0);
-            probe_from<W, C>(col, t, rs, chash + a, n, t0 - 1, need, lam, bt, h0, b0);
+            probe_from<W, C>(t, base, chash + a, n, t0 - 1, need, lam, bt, v0);
         }
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t r_out = 0;
@@ -888,13 +871,78 @@ __global__ void count_zero_kernel(const uint64_t *__restrict__ h, uint64_t n, ui
     if (__any(z) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrZeroHash);
 }
 
-// Cuckoo insertion of one decode's hashes (tiles: tile_dec[b], tile_beg[b],
-// tile_end[b]).  A key goes to an empty slot of either candidate bucket
-// (compare-and-swap 0 -> key); when all four slots are taken it displaces the
-// key of a random slot by atomic exchange (a random walk: a fresh key picks
-// either bucket, a displaced key its other bucket) and carries the displaced
-// key on.  A key is always either in the table or carried by exactly one
-// thread, so none is lost.  A repeated hash (already in a slot) stops.
+// ---- holder index build (once per cache load)
+//
+// The (hash, decode) pairs of all resident sets are sorted by hash (rocPRIM
+// radix sort), so the holders of one hash form a run.  The first element of
+// each run ("head") stands for the run: classify_kernel counts distinct
+// hashes and those with two or more holders, index_insert_kernel puts every
+// distinct hash into the cuckoo set, and index_value_kernel finds each one's
+// slot and writes its holder value (for several holders, a fresh bitmap row
+// with their bits set).
+
+// Decode of every resident hash of the CSR (binary search of the offsets).
+__global__ void owner_kernel(const uint64_t *__restrict__ off, uint32_t D, uint64_t first, uint64_t n,
+                             uint32_t *__restrict__ owner) {
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride) {
+        const uint64_t x = first + i;
+        uint32_t lo = 0, hi = D;   // largest d with off[d] <= x
+        while (hi - lo > 1) {
+            const uint32_t mid = lo + (hi - lo) / 2;
+            if (off[mid] <= x) lo = mid;
+            else hi = mid;
+        }
+        owner[i] = lo;
+    }
+}
+
+__device__ inline bool run_head(const uint64_t *__restrict__ key, uint64_t i) {
+    return i == 0 || key[i] != key[i - 1];
+}
+
+// Smallest and largest holder of the run starting at head i; returns the
+// run's end.
+__device__ inline uint64_t run_span(const uint64_t *__restrict__ key, const uint32_t *__restrict__ dec, uint64_t n,
+                                    uint64_t i, uint32_t &dmin, uint32_t &dmax) {
+    dmin = dmax = dec[i];
+    uint64_t e = i + 1;
+    for (; e < n && key[e] == key[i]; ++e) {
+        dmin = min(dmin, dec[e]);
+        dmax = max(dmax, dec[e]);
+    }
+    return e;
+}
+
+// cnt[0] += distinct hashes, cnt[1] += hashes with two or more holders.
+__global__ __launch_bounds__(256) void classify_kernel(const uint64_t *__restrict__ key,
+                                                       const uint32_t *__restrict__ dec, uint64_t n,
+                                                       unsigned long long *__restrict__ cnt) {
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    uint32_t heads = 0, multi = 0;
+    for (; i < n; i += stride) {
+        if (!run_head(key, i)) continue;
+        uint32_t dmin, dmax;
+        run_span(key, dec, n, i, dmin, dmax);
+        ++heads;
+        multi += dmin != dmax ? 1u : 0u;
+    }
+    heads = wave_sum_u32(heads);
+    multi = wave_sum_u32(multi);
+    if ((threadIdx.x % kWave) == 0) {
+        if (heads) atomicAdd(cnt, (unsigned long long)heads);
+        if (multi) atomicAdd(cnt + 1, (unsigned long long)multi);
+    }
+}
+
+// Cuckoo insertion of the distinct hashes.  A key goes to an empty slot of
+// either candidate bucket (compare-and-swap 0 -> key); when all four slots
+// are taken it displaces the key of a random slot by atomic exchange (a
+// random walk: a fresh key picks either bucket, a displaced key its other
+// bucket) and carries the displaced key on.  A key is always either in the
+// set or carried by exactly one thread, so none is lost.
 constexpr uint32_t kMaxKicks = 2048;
 
 __device__ inline bool try_place(unsigned long long *bk, uint64_t key) {
@@ -905,47 +953,30 @@ __device__ inline bool try_place(unsigned long long *bk, uint64_t key) {
     return false;
 }
 
-// Resident-anywhere filter: set each key's four bits (grid-stride).
-__global__ __launch_bounds__(256) void any_build_kernel(const uint64_t *__restrict__ h, uint64_t n,
-                                                        uint64_t *__restrict__ any, uint32_t any_shift) {
+__global__ __launch_bounds__(256) void index_insert_kernel(uint64_t *__restrict__ keys, uint32_t shift,
+                                                           const uint64_t *__restrict__ skey, uint64_t n,
+                                                           uint32_t *__restrict__ err) {
     uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    unsigned long long *tab = (unsigned long long *)keys;
     for (; i < n; i += stride) {
-        uint64_t w, m;
-        any_of(h[i], any_shift, w, m);
-        // bits are only ever set, so a word that already holds them needs no atomic
-        if ((any[w] & m) != m) atomicOr((unsigned long long *)(any + w), (unsigned long long)m);
-    }
-}
-
-__global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys, uint32_t shift, uint32_t pitch,
-                                                     const uint64_t *__restrict__ h,
-                                                     const uint32_t *__restrict__ tile_dec,
-                                                     const uint64_t *__restrict__ tile_beg,
-                                                     const uint64_t *__restrict__ tile_end,
-                                                     uint32_t *__restrict__ err) {
-    const uint32_t d = tile_dec[blockIdx.x];
-    const uint64_t beg = tile_beg[blockIdx.x], end = tile_end[blockIdx.x];
-    unsigned long long *col = (unsigned long long *)keys + 2 * (uint64_t)d;
-    for (uint64_t i = beg + threadIdx.x; i < end; i += blockDim.x) {
-        uint64_t key = h[i];
+        if (!run_head(skey, i)) continue;
+        uint64_t key = skey[i];
         uint32_t from = 0xFFFFFFFFu;   // bucket the carried key was displaced from
         uint32_t rnd = (uint32_t)(key ^ (key >> 32)) ^ (uint32_t)i;   // walk state (a 32-bit LCG)
         bool done = false;
         for (uint32_t kick = 0; kick < kMaxKicks && !done; ++kick) {
             uint32_t b1, b2;
             buckets_of(key, shift, b1, b2);
-            unsigned long long *k1 = col + (uint64_t)b1 * pitch * 2;
-            unsigned long long *k2 = col + (uint64_t)b2 * pitch * 2;
-            if (try_place(k1, key) || try_place(k2, key)) {
+            if (try_place(tab + 2 * (uint64_t)b1, key) || try_place(tab + 2 * (uint64_t)b2, key)) {
                 done = true;
                 break;
             }
             // displace from the bucket the key did not just leave
             rnd = rnd * 1664525u + 1013904223u;
             const uint32_t b = (b1 == from) ? b2 : (b2 == from) ? b1 : ((rnd >> 31) ? b2 : b1);
-            unsigned long long *bk = col + (uint64_t)b * pitch * 2;
-            const unsigned long long old = atomicExch(bk + ((rnd >> 30) & 1u), (unsigned long long)key);
+            const unsigned long long old = atomicExch(tab + 2 * (uint64_t)b + ((rnd >> 30) & 1u),
+                                                      (unsigned long long)key);
             if (old == 0ull || old == key) {
                 done = true;
                 break;
@@ -954,6 +985,42 @@ __global__ __launch_bounds__(256) void insert_kernel(uint64_t *__restrict__ keys
             from = b;
         }
         if (!done) atomicOr(err, kErrTableFull);
+    }
+}
+
+// Holder values, once every key has its final slot.  Bitmap rows are
+// handed out by rows_used (row 0 stays zero: the scan reads it when a value
+// is not a row); each row is written by the one thread of its run.
+__global__ __launch_bounds__(256) void index_value_kernel(const uint64_t *__restrict__ keys, uint32_t *__restrict__ vals,
+                                                          uint32_t shift, uint64_t *__restrict__ bits,
+                                                          uint32_t bpitch, const uint64_t *__restrict__ skey,
+                                                          const uint32_t *__restrict__ dec, uint64_t n,
+                                                          uint32_t *__restrict__ rows_used,
+                                                          uint32_t *__restrict__ err) {
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride) {
+        if (!run_head(skey, i)) continue;
+        const uint64_t key = skey[i];
+        uint32_t dmin, dmax;
+        const uint64_t e = run_span(skey, dec, n, i, dmin, dmax);
+        uint32_t v;
+        if (dmin == dmax) {
+            v = kHeldOne | dmin;
+        } else {
+            v = atomicAdd(rows_used, 1u);
+            uint64_t *row = bits + (uint64_t)v * bpitch;
+            for (uint64_t x = i; x < e; ++x) row[dec[x] / 64u] |= 1ull << (dec[x] % 64u);
+        }
+        uint32_t b1, b2;
+        buckets_of(key, shift, b1, b2);
+        uint64_t slot = ~0ull;
+        if (keys[2 * (uint64_t)b1] == key) slot = 2 * (uint64_t)b1;
+        else if (keys[2 * (uint64_t)b1 + 1] == key) slot = 2 * (uint64_t)b1 + 1;
+        else if (keys[2 * (uint64_t)b2] == key) slot = 2 * (uint64_t)b2;
+        else if (keys[2 * (uint64_t)b2 + 1] == key) slot = 2 * (uint64_t)b2 + 1;
+        if (slot == ~0ull) atomicOr(err, kErrTableFull);
+        else vals[slot] = v;
     }
 }
 
@@ -993,14 +1060,8 @@ __global__ void check_snapshot_kernel(const uint8_t *__restrict__ tier, const fl
 // First-miss scan of one (hash run, decode) pair by one thread.
 __device__ inline uint32_t prefix_match_one(const Table &t, uint32_t d, const uint64_t *__restrict__ run,
                                             uint32_t n) {
-    const uint64_t *col = t.keys + 2 * (uint64_t)d;
     uint32_t j = 0;
-    for (; j < n; ++j) {
-        const uint64_t h = run[j];
-        uint32_t b1, b2;
-        buckets_of(h, t.shift, b1, b2);
-        if (h == 0 || !(bucket_has(col, t, b1, h) || bucket_has(col, t, b2, h))) break;
-    }
+    while (j < n && holds(t, run[j], d)) ++j;
     return j;
 }
 
@@ -1320,12 +1381,12 @@ struct netkv_ctx {
     // cache
     bool have_cache = false;
     uint32_t cache_D = 0;
-    uint64_t *table = nullptr;
-    uint64_t table_bytes = 0, buckets = 0;
-    uint32_t log2b = 0, pitch = 0;
-    uint64_t *any = nullptr;     // resident-anywhere filter words
-    uint64_t any_words = 0;
-    uint32_t any_shift = 0;
+    // holder index of the resident sets
+    uint64_t *table = nullptr;   // [buckets][2] distinct resident hashes
+    uint32_t *tvals = nullptr;   // [buckets][2] holder values
+    uint64_t *bits = nullptr;    // [rows][bpitch] holder bitmaps
+    uint64_t table_bytes = 0, buckets = 0, rows = 0, distinct = 0;
+    uint32_t log2b = 0, bpitch = 0;
     // scratch
     uint32_t *errword = nullptr;          // request / selection errors (sticky)
     uint32_t *loadword = nullptr;         // validation flags of the load calls
@@ -1474,10 +1535,10 @@ Snap make_snap(netkv_handle h) {
 Table make_table(netkv_handle h) {
     Table t;
     t.keys = h->table;
-    t.shift = 32 - h->log2b;
-    t.pitch = h->pitch;
-    t.any = h->any;
-    t.any_shift = h->any_shift;
+    t.vals = h->tvals;
+    t.bits = h->bits;
+    t.shift = 64 - h->log2b;
+    t.bpitch = h->bpitch;
     return t;
 }
 
@@ -1509,7 +1570,7 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-constexpr int kSpec = 4;            // blocks tested together per extension step at one decode per lane
+constexpr int kSpec = 2;            // blocks looked up together per extension step
 constexpr uint32_t kLcpLanes = 8;   // lanes per sorted position in lcp_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
@@ -1572,7 +1633,7 @@ template <int K, int C>
 void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
                  uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po, bool pairs,
                  hipStream_t st) {
-    constexpr int W = C >= 4 ? 1 : C == 2 ? 2 : kSpec;
+    constexpr int W = kSpec;
     // one workgroup per (kWavesPerBlock runs, group) when the groups split
     // evenly over the XCDs (see scan_kernel), else per kWavesPerBlock waves
     const uint64_t grid64 = ngroup % kXcds == 0
@@ -1699,7 +1760,8 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->dbase);
         dfree(h->dxlim);
         dfree(h->table);
-        dfree(h->any);
+        dfree(h->tvals);
+        dfree(h->bits);
         dfree(h->errword);
         dfree(h->loadword);
         dfree(h->zflag);
@@ -1860,53 +1922,29 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     std::vector<uint64_t> off(n_decode + 1);
     HIPCHK(h, hipMemcpyAsync(off.data(), hash_off, 8ull * (n_decode + 1), hipMemcpyDefault, st));
     HIPCHK(h, hipStreamSynchronize(st));
-    uint64_t maxn = 0;
-    for (uint32_t d = 0; d < n_decode; ++d) {
-        if (off[d + 1] < off[d]) return fail(h, NETKV_EINVAL, "hash_off decreases at decode %u", d);
-        maxn = std::max(maxn, off[d + 1] - off[d]);
-    }
-    if (off[n_decode] > n_hashes) return fail(h, NETKV_EINVAL, "hash_off[n_decode] exceeds n_hashes");
-    // two slots per bucket; cuckoo tables with two 2-slot buckets per key stay
-    // buildable well above load factor 0.5, and are capped at 0.85
-    const double lf = std::min(0.85, (double)max_load_factor);
-    const uint64_t need = (uint64_t)std::ceil((double)maxn / (2.0 * lf));
-    uint32_t log2b = 3;
-    while ((1ull << log2b) < need) {
-        ++log2b;
-        if (log2b > 30) return fail(h, NETKV_ECAPACITY, "a table would need more than 2^31 slots");
-    }
-    uint64_t nbk = 1ull << log2b;
-    uint64_t cap = 2 * nbk;
-    const uint32_t pitch = (n_decode + 15u) & ~15u;
-    uint64_t tbytes = cap * pitch * 8ull;
-    // tiles of at most 4096 hashes, each within one decode
-    const uint64_t kTile = 4096;
-    std::vector<uint32_t> tdec;
-    std::vector<uint64_t> tbeg, tend;
     for (uint32_t d = 0; d < n_decode; ++d)
-        for (uint64_t b = off[d]; b < off[d + 1]; b += kTile) {
-            tdec.push_back(d);
-            tbeg.push_back(b);
-            tend.push_back(std::min(off[d + 1], b + kTile));
-        }
+        if (off[d + 1] < off[d]) return fail(h, NETKV_EINVAL, "hash_off decreases at decode %u", d);
+    if (off[n_decode] > n_hashes) return fail(h, NETKV_EINVAL, "hash_off[n_decode] exceeds n_hashes");
     const uint64_t first = off[0], total = off[n_decode] - off[0];
-    uint64_t *dh = nullptr, *dbeg = nullptr, *dend = nullptr, *tab = nullptr;
-    uint32_t *ddec = nullptr;
-    auto cleanup = [&]() { dfree(dh); dfree(dbeg); dfree(dend); dfree(ddec); dfree(tab); };
+    if (total >= (1ull << 31)) return fail(h, NETKV_ECAPACITY, "more than 2^31 - 1 resident hashes");
+    // words per holder bitmap row: whole 64-decode words, a multiple of 4
+    // (32-byte rows, so a wavefront's words are one aligned scalar load)
+    const uint32_t bpitch = (uint32_t)((((uint64_t)n_decode + 63) / 64 + 3) & ~3ull);
+    uint64_t *dh = nullptr, *dkey = nullptr, *doff = nullptr;
+    uint32_t *dec_in = nullptr, *dec = nullptr;
+    unsigned long long *cnt = nullptr;
+    uint8_t *stmp = nullptr;
+    auto cleanup = [&]() { dfree(dh); dfree(dkey); dfree(doff); dfree(dec_in); dfree(dec); dfree(cnt); dfree(stmp); };
     // the device copy keeps the caller's absolute offsets valid: copy from `first`
-    if (dalloc(dh, off[n_decode]) != hipSuccess || dalloc(dbeg, tbeg.size()) != hipSuccess ||
-        dalloc(dend, tend.size()) != hipSuccess || dalloc(ddec, tdec.size()) != hipSuccess) {
+    if (dalloc(dh, off[n_decode]) != hipSuccess || dalloc(doff, (uint64_t)n_decode + 1) != hipSuccess ||
+        dalloc(dkey, total) != hipSuccess || dalloc(dec_in, total) != hipSuccess ||
+        dalloc(dec, total) != hipSuccess || dalloc(cnt, 2) != hipSuccess) {
         cleanup();
         return fail(h, NETKV_ENOMEM, "staging allocation failed");
     }
     hipError_t e = hipSuccess;
     if (total) e = hipMemcpyAsync(dh + first, hashes + first, 8ull * total, hipMemcpyDefault, st);
-    if (e == hipSuccess && !tdec.empty())
-        e = hipMemcpyAsync(ddec, tdec.data(), 4ull * tdec.size(), hipMemcpyHostToDevice, st);
-    if (e == hipSuccess && !tbeg.empty())
-        e = hipMemcpyAsync(dbeg, tbeg.data(), 8ull * tbeg.size(), hipMemcpyHostToDevice, st);
-    if (e == hipSuccess && !tend.empty())
-        e = hipMemcpyAsync(dend, tend.data(), 8ull * tend.size(), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(doff, off.data(), 8ull * (n_decode + 1), hipMemcpyHostToDevice, st);
     if (e == hipSuccess) e = hipMemsetAsync(h->loadword, 0, 4, st);
     uint32_t bad = 0;
     if (e == hipSuccess && total) {
@@ -1924,44 +1962,85 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
         cleanup();
         return fail(h, NETKV_EINVAL, "cache contains the reserved hash value 0");
     }
-    // release the old table and filter first: the new ones may be large
-    dfree(h->table);
-    dfree(h->any);
-    h->table = nullptr;
-    h->any = nullptr;
-    h->have_cache = false;
-    // filter: a power-of-two number of 64-bit words, 8 bits per resident hash
-    uint32_t log2w = 6;
-    while ((1ull << log2w) * 8ull < total && log2w < 40) ++log2w;
-    const uint64_t any_words = 1ull << log2w;
-    uint64_t *anyw = nullptr;
-    if (dalloc(anyw, any_words) != hipSuccess) {
-        cleanup();
-        return fail(h, NETKV_ENOMEM, "filter allocation of %llu bytes failed", (unsigned long long)(8 * any_words));
-    }
-    e = hipMemsetAsync(anyw, 0, 8 * any_words, st);
-    if (e == hipSuccess && total) {
-        hipLaunchKernelGGL(any_build_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st,
-                           (const uint64_t *)(dh + first), total, anyw, 64u - log2w);
+    // (hash, decode) pairs sorted by hash; per distinct hash: one holder or several
+    unsigned long long counts[2] = {0, 0};
+    if (total) {
+        hipLaunchKernelGGL(owner_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st, (const uint64_t *)doff,
+                           n_decode, first, total, dec_in);
         e = hipGetLastError();
+        size_t tb = 0;
+        if (e == hipSuccess)
+            e = rocprim::radix_sort_pairs(nullptr, tb, (const uint64_t *)(dh + first), dkey, (const uint32_t *)dec_in,
+                                          dec, (uint32_t)total, 0, 64, st);
+        if (e == hipSuccess && dalloc(stmp, std::max<size_t>(tb, 16)) != hipSuccess) {
+            cleanup();
+            return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
+        }
+        if (e == hipSuccess)
+            e = rocprim::radix_sort_pairs(stmp, tb, (const uint64_t *)(dh + first), dkey, (const uint32_t *)dec_in,
+                                          dec, (uint32_t)total, 0, 64, st);
+        if (e == hipSuccess) e = hipMemsetAsync(cnt, 0, 16, st);
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL(classify_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st,
+                               (const uint64_t *)dkey, (const uint32_t *)dec, total, cnt);
+            e = hipGetLastError();
+        }
+        if (e == hipSuccess) e = hipMemcpyAsync(counts, cnt, 16, hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
     }
+    dfree(dh);
+    dfree(doff);
+    dfree(dec_in);
+    dfree(stmp);
+    if (e != hipSuccess) {
+        cleanup();
+        return fail(h, NETKV_EDEVICE, "holder sort failed: %s", hipGetErrorString(e));
+    }
+    const uint64_t distinct = counts[0], rows = counts[1] + 1;   // row 0: all zero
+    if (rows >= (uint64_t)kHeldOne) {
+        cleanup();
+        return fail(h, NETKV_ECAPACITY, "more than 2^31 - 2 hashes held by several decodes");
+    }
+    // release the old index first: the new one may be large
+    dfree(h->table);
+    dfree(h->tvals);
+    dfree(h->bits);
+    h->have_cache = false;
+    // two slots per bucket; two-choice cuckoo sets of 2-slot buckets stay
+    // buildable well above load factor 0.5, and are capped at 0.85
+    const double lf = std::min(0.85, (double)max_load_factor);
+    const uint64_t need = (uint64_t)std::ceil((double)distinct / (2.0 * lf));
+    uint32_t log2b = 3;
+    while ((1ull << log2b) < need) {
+        ++log2b;
+        if (log2b > 30) {
+            cleanup();
+            return fail(h, NETKV_ECAPACITY, "the index would need more than 2^31 slots");
+        }
+    }
+    uint64_t *tab = nullptr, *bm = nullptr;
+    uint32_t *tv = nullptr;
+    if (dalloc(bm, rows * bpitch) != hipSuccess) {
+        cleanup();
+        return fail(h, NETKV_ENOMEM, "holder bitmap allocation of %llu bytes failed",
+                    (unsigned long long)(8 * rows * bpitch));
+    }
+    e = hipMemsetAsync(bm, 0, 8 * rows * bpitch, st);
     // build at the planned size; should a build fail to place every key (a
     // random walk that did not end), rebuild with twice the buckets, twice
+    uint64_t nbk = 0;
     for (int attempt = 0;; ++attempt) {
         nbk = 1ull << log2b;
-        cap = 2 * nbk;
-        tbytes = cap * pitch * 8ull;
-        if (e == hipSuccess && dalloc(tab, cap * pitch) != hipSuccess) {
+        if (e == hipSuccess && (dalloc(tab, 2 * nbk) != hipSuccess || dalloc(tv, 2 * nbk) != hipSuccess)) {
             cleanup();
-            dfree(anyw);
-            return fail(h, NETKV_ENOMEM, "table allocation of %llu bytes failed", (unsigned long long)tbytes);
+            dfree(tab); dfree(tv); dfree(bm);
+            return fail(h, NETKV_ENOMEM, "index allocation of %llu bytes failed", (unsigned long long)(24 * nbk));
         }
-        if (e == hipSuccess) e = hipMemsetAsync(tab, 0, tbytes, st);
+        if (e == hipSuccess) e = hipMemsetAsync(tab, 0, 16 * nbk, st);
         if (e == hipSuccess) e = hipMemsetAsync(h->loadword, 0, 4, st);
-        if (e == hipSuccess && !tdec.empty()) {
-            hipLaunchKernelGGL(insert_kernel, dim3((uint32_t)tdec.size()), dim3(256), 0, st, tab, 32u - log2b,
-                               pitch, (const uint64_t *)dh, (const uint32_t *)ddec, (const uint64_t *)dbeg,
-                               (const uint64_t *)dend, h->loadword);
+        if (e == hipSuccess && total) {
+            hipLaunchKernelGGL(index_insert_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st, tab,
+                               64u - log2b, (const uint64_t *)dkey, total, h->loadword);
             e = hipGetLastError();
         }
         bad = 0;
@@ -1969,23 +2048,39 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
         if (e == hipSuccess) e = hipStreamSynchronize(st);
         if (e != hipSuccess || !bad || attempt == 2 || log2b >= 30) break;
         dfree(tab);
+        dfree(tv);
         ++log2b;
     }
-    dfree(dh); dfree(dbeg); dfree(dend); dfree(ddec);
+    if (e == hipSuccess && !bad && total) {
+        // rows are handed out from 1 (cnt[0] doubles as the counter)
+        const uint32_t one = 1;
+        e = hipMemcpyAsync(cnt, &one, 4, hipMemcpyHostToDevice, st);
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL(index_value_kernel, dim3(grid_for(total, 256, 16384)), dim3(256), 0, st,
+                               (const uint64_t *)tab, tv, 64u - log2b, bm, bpitch, (const uint64_t *)dkey,
+                               (const uint32_t *)dec, total, (uint32_t *)cnt, h->loadword);
+            e = hipGetLastError();
+        }
+        if (e == hipSuccess) e = hipMemcpyAsync(&bad, h->loadword, 4, hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+    }
+    cleanup();
     if (e != hipSuccess || bad) {
         dfree(tab);
-        dfree(anyw);
-        return e != hipSuccess ? fail(h, NETKV_EDEVICE, "table build failed: %s", hipGetErrorString(e))
-                               : fail(h, NETKV_ECAPACITY, "table build could not place every hash");
+        dfree(tv);
+        dfree(bm);
+        return e != hipSuccess ? fail(h, NETKV_EDEVICE, "index build failed: %s", hipGetErrorString(e))
+                               : fail(h, NETKV_ECAPACITY, "index build could not place every hash");
     }
     h->table = tab;
+    h->tvals = tv;
+    h->bits = bm;
     h->buckets = nbk;
     h->log2b = log2b;
-    h->pitch = pitch;
-    h->table_bytes = tbytes + 8 * any_words;
-    h->any = anyw;
-    h->any_words = any_words;
-    h->any_shift = 64u - log2w;
+    h->bpitch = bpitch;
+    h->rows = rows;
+    h->distinct = distinct;
+    h->table_bytes = 24 * nbk + 8 * rows * bpitch;
     h->cache_D = n_decode;
     h->have_cache = true;
     return NETKV_OK;
@@ -2297,11 +2392,15 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
     }
 }
 
-netkv_status netkv_cache_info(netkv_handle h, uint64_t *slots_per_decode, uint64_t *table_bytes) {
+netkv_status netkv_cache_info(netkv_handle h, uint64_t *index_slots, uint64_t *distinct_hashes,
+                              uint64_t *shared_hashes, uint64_t *index_bytes) {
     if (!h) return NETKV_EINVAL;
-    if (!h->have_cache) return fail(h, NETKV_ENOTREADY, "no cache loaded");
-    if (slots_per_decode) *slots_per_decode = 2 * h->buckets;
-    if (table_bytes) *table_bytes = h->table_bytes;
+    h->err.clear();
+    if (!h->have_cache) return fail(h, NETKV_ENOTREADY, "no cache loaded (netkv_cache_load)");
+    if (index_slots) *index_slots = 2 * h->buckets;
+    if (distinct_hashes) *distinct_hashes = h->distinct;
+    if (shared_hashes) *shared_hashes = h->rows - 1;
+    if (index_bytes) *index_bytes = h->table_bytes;
     return NETKV_OK;
 }
 

@@ -76,7 +76,8 @@ _SIGS = {
     "netkv_sync_errors": (C.c_int32, [C.c_void_p, C.c_void_p]),
     "netkv_set_timing": (C.c_int32, [C.c_void_p, C.c_int]),
     "netkv_kernel_ms": (C.c_int32, [C.c_void_p, C.POINTER(C.c_float)]),
-    "netkv_cache_info": (C.c_int32, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]),
+    "netkv_cache_info": (C.c_int32, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                                     C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]),
     "netkv_set_option": (C.c_int32, [C.c_void_p, C.c_int, C.c_uint32]),
     "netkv_tier_counts": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_void_p, C.c_void_p,
                                       C.c_void_p]),
@@ -289,10 +290,11 @@ def netkv_set_option(h: int, option: int, value: int) -> None:
     _check(h, load_library().netkv_set_option(h, int(option), int(value)))
 
 
-def netkv_cache_info(h: int):
-    slots, nbytes = C.c_uint64(), C.c_uint64()
-    _check(h, load_library().netkv_cache_info(h, C.byref(slots), C.byref(nbytes)))
-    return int(slots.value), int(nbytes.value)
+def netkv_cache_info(h: int) -> Dict[str, int]:
+    v = [C.c_uint64() for _ in range(4)]
+    _check(h, load_library().netkv_cache_info(h, *[C.byref(x) for x in v]))
+    return dict(index_slots=int(v[0].value), distinct_hashes=int(v[1].value),
+                shared_hashes=int(v[2].value), index_bytes=int(v[3].value))
 
 
 # ---------------------------------------------------------------- convenience

@@ -146,14 +146,25 @@ def test_tuning_options_leave_results_unchanged(nk):
 
 @pytest.mark.parametrize("lf", [0.9, 0.99])
 def test_dense_tables(nk, lf):
-    """Dense tables (load factor capped at 0.85, rounded to a power of two):
-    many displacements while building; membership must be unaffected."""
+    """A dense holder index (load factor capped at 0.85, buckets rounded to a
+    power of two): many displacements while building; membership must be
+    unaffected.  The index holds exactly the distinct resident hashes, and
+    a bitmap row for exactly those resident on two or more decodes."""
     _say("dense tables lf", lf)
     cfg = W.scaled(W.CONFIGS["c0"], n_requests=1500, cache_per_decode=3000)
     snap, req, cache = _inputs(cfg, 7)
     sel = _gpu(nk, snap, cache, lf=lf)
-    slots, _ = nk.netkv_cache_info(sel.h)
-    assert slots == 4096
+    ci = nk.netkv_cache_info(sel.h)
+    off = cache["hash_off"].astype(np.int64)
+    owner = np.repeat(np.arange(cfg.n_decode), np.diff(off))
+    pairs = np.unique(np.stack([cache["hashes"].astype(np.uint64), owner.astype(np.uint64)]), axis=1)
+    hs, holders = np.unique(pairs[0], return_counts=True)
+    assert ci["distinct_hashes"] == hs.size
+    assert ci["shared_hashes"] == int((holders >= 2).sum()) > 0
+    buckets = 8
+    while 2 * buckets * min(lf, 0.85) < hs.size:
+        buckets *= 2
+    assert ci["index_slots"] in (2 * buckets, 4 * buckets, 8 * buckets)
     g = _run(nk, sel, req, 2)
     o = oracle.select(snap, cache, req, k=2, pairs=True, n_threads=8)
     check_pairs(g["j"], g["feas"], g["cost"], o)

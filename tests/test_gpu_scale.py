@@ -42,9 +42,12 @@ def test_full_size_sampled(nk, name, n_sample):
     sel = nk.Selector(0)
     sel.load_snapshot(snap)
     sel.load_cache(cache, 0.5)
-    slots, tbytes = nk.netkv_cache_info(sel.h)
-    assert slots == 2 * cfg.cache_per_decode
-    _say(name, "tables built: %d slots/decode, %.2f GiB" % (slots, tbytes / 2 ** 30))
+    ci = nk.netkv_cache_info(sel.h)
+    n_res = int(cache["hashes"].size)
+    assert 0 < ci["shared_hashes"] < ci["distinct_hashes"] <= n_res
+    assert ci["distinct_hashes"] <= 0.85 * ci["index_slots"]
+    _say(name, "holder index built: %d distinct hashes, %d shared, %d slots, %.2f GiB"
+         % (ci["distinct_hashes"], ci["shared_hashes"], ci["index_slots"], ci["index_bytes"] / 2 ** 30))
     rd = nk.requests_to_device(req, sel.device)
     out = sel.select(rd, k=1)
     sel.sync_errors()
