@@ -36,6 +36,15 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def cols_per_lane(D: int) -> int:
+    """The library's automatic decodes per lane (see NETKV_OPT_COLS)."""
+    for c in (6, 3, 2):
+        g = -(-D // (64 * c))
+        if g >= 8 and g % 8 == 0:
+            return c
+    return 2 if D >= 256 else 1
+
+
 def kernel_source_digest() -> str:
     with open(os.path.join(ROOT, "paper_2606_03910_amd", "csrc", "netkv.hip"), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -277,7 +286,7 @@ def main():
             "algorithmic_bytes_per_launch": b_alg,
             "membership_tests_per_launch": tests,
             "mean_tests_per_pair": tests / pairs,
-            "kernel": "scan_kernel (k=1; %d decodes per lane)" % (args.cols or (2 if D >= 256 else 1)),
+            "kernel": "scan_kernel (k=1; %d decodes per lane)" % (args.cols or cols_per_lane(D)),
             "kernel_source_sha256_16": digest,
             "issue": issue,
             "note": ("achieved counts 8 B per first-miss membership test of every pair, as if each "

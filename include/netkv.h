@@ -105,7 +105,7 @@ netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stre
  * `max_load_factor` (0 < lf < 1) occupancy (capped at 0.85; a build that
  * cannot place every hash is retried with twice the buckets, twice), and
  * for each hash its holders -- one decode, or a bitmap over the decodes
- * (ceil(n_decode / 256) * 32 bytes per hash held by two or more) -- so
+ * (8 * ceil(ceil(n_decode / 64) / 12) * 12 bytes per hash held by two or more) -- so
  * that one lookup answers a membership test on every decode at once.
  * Synchronous; needs about 28 bytes of temporary device memory per
  * resident hash while building.  EINVAL: bad CSR, hash 0, lf out of range,
@@ -241,7 +241,10 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
  *                        0: nothing is carried, every pair is scanned
  *                        from block 0;
  *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
- *                        automatic (2 on pools of 256+ decodes, else 1), 1, 2, 4.
+ *                        automatic (the widest of 6, 3, 2 whose groups of
+ *                        64 per lane-column split evenly over the 8 XCDs,
+ *                        else 2 on pools of 256+ decodes, else 1), 1, 2,
+ *                        3, 4, 6.
  * and one option that does change results, selecting the rung of the
  * method's ablation (Sec. VI, Experiment 6) the costs use:
  *   NETKV_OPT_POLICY  -- 0 (default): the full cost; 1: static tier map and

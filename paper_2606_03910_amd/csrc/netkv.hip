@@ -106,7 +106,7 @@ struct Table {
     const uint32_t *vals;   // [buckets][2] holder values
     const uint64_t *bits;   // [rows][bpitch] holder bitmaps (at least one row, row 0 of zeros if unused)
     uint32_t shift;         // 64 - log2(buckets)
-    uint32_t bpitch;        // 64-bit words per bitmap row, a multiple of 4
+    uint32_t bpitch;        // 64-bit words per bitmap row, a multiple of 12
 };
 
 struct Reqs {
@@ -320,16 +320,20 @@ constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead 
 // ... and the part read only by requests that probe (and for per-pair output).
 struct alignas(16) Cold {
     uint64_t a;      // offset of the hash run
+    uint64_t hoff;   // offset of the holder values of the blocks from the first tested one
     uint32_t r;      // request index in the caller's batch
     uint32_t n;      // hashed blocks
-    uint32_t v;      // holder value of block lcp (kNoHolder if there is no such block)
-    uint32_t pad[3];
+    uint32_t v;      // holder value of the first tested block (kNoHolder: no test)
+    uint32_t m;      // holder values stored at hoff (the block after them, if any, is held by
+                     // no decode); kNoPre if none could be stored
 };
+constexpr uint32_t kNoPre = 0xFFFFFFFFu;
 
 struct Order {
     const uint32_t *perm;     // sorted position -> request
     const Hot *hot;           // [n_valid] sorted request records
     const Cold *cold;
+    const uint32_t *hv;       // holder values of the blocks probing positions test
     const uint32_t *n_valid;  // valid requests (they sort first)
 };
 
@@ -339,12 +343,17 @@ struct Order {
 // The reserved hash value 0 is looked for separately: a flat scan of the
 // batch's hash array (count_zero_kernel) raises `zflag`, and only then does
 // zero_fix_kernel check each request's run and invalidate those holding it.
-// Thread 0 clears zflag for that scan.
+// Thread 0 clears zflag for that scan, and the holder-value counter of the
+// order kernel.
 __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max_blocks, uint32_t *__restrict__ keys,
                                                    uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
-                                                   uint32_t *__restrict__ zflag) {
+                                                   uint32_t *__restrict__ zflag,
+                                                   unsigned long long *__restrict__ hv_used) {
     const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r == 0) *zflag = 0;
+    if (r == 0) {
+        *zflag = 0;
+        *hv_used = 0;
+    }
     bool bad = false;
     if (r < rq.n_req) {
         uint32_t p, len, n;
@@ -401,10 +410,18 @@ __global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint3
 // writes it, or position 0 writes 0.  Positions of invalid requests and the
 // kHotPad positions past the batch get a record that the scan may read ahead
 // but never scores (row 0, no blocks, no test).
+//
+// The first block a scan tests for a position is block 0 at the start of a
+// run (nothing is carried across runs) and else the end of the common run.
+// If some decode holds it, the position's lanes look up the holders of the
+// following blocks too, up to the first one no decode holds, into hv (from a
+// shared counter), so that the scan waits on bitmap words only.
 template <uint32_t G>
 __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_t bt, const uint32_t *__restrict__ perm,
                                                   const uint32_t *__restrict__ sorted_keys, Table t, uint32_t reuse,
-                                                  Hot *__restrict__ hot, Cold *__restrict__ cold,
+                                                  uint32_t run_len, Hot *__restrict__ hot, Cold *__restrict__ cold,
+                                                  uint32_t *__restrict__ hv, uint64_t hv_cap,
+                                                  unsigned long long *__restrict__ hv_used,
                                                   uint32_t *__restrict__ n_valid) {
     const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t sub = threadIdx.x % G;
@@ -441,16 +458,47 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_
             }
         }
     }
+    const uint64_t st = (i % run_len == 0) ? 0 : l;   // first tested block
+    uint32_t v = kNoHolder;
+    if (sub == 0 && st < nr) v = holder_lane(t, rq.hashes[a + st]);
+    v = __shfl(v, (int)seg, kWave);
+    uint64_t hoff = 0;
+    uint32_t m = kNoPre;
+    if (v != kNoHolder) {
+        // room for every block from st on; the holders end at the first block
+        // no decode holds
+        unsigned long long o = 0;
+        if (sub == 0) o = atomicAdd(hv_used, (unsigned long long)(nr - st));
+        hoff = __shfl(o, (int)seg, kWave);
+        if (hoff + (nr - st) <= hv_cap) {
+            m = (uint32_t)(nr - st);
+            for (uint64_t k0 = 0; k0 < nr - st; k0 += G) {
+                const uint64_t k = k0 + sub;
+                uint32_t hk = kNoHolder;
+                if (k < nr - st) {
+                    hk = k == 0 ? v : holder_lane(t, rq.hashes[a + st + k]);
+                    hv[hoff + k] = hk;
+                }
+                const uint32_t none = (uint32_t)(__ballot(k < nr - st && hk == kNoHolder) >> seg) &
+                                      (uint32_t)((1ull << G) - 1);
+                if (none) {
+                    m = (uint32_t)(k0 + (uint64_t)__builtin_ctz(none));
+                    break;
+                }
+            }
+        }
+    }
     if (sub != 0) return;
     Cold c;
     c.a = a;
+    c.hoff = hoff;
     c.r = r;
     c.n = (uint32_t)nr;
-    c.v = l < nr ? holder_lane(t, rq.hashes[a + l]) : kNoHolder;
-    c.pad[0] = c.pad[1] = c.pad[2] = 0;
+    c.v = v;
+    c.m = m;
     Hot o;
     o.row = rq.prefill[r] * slp * (uint32_t)sizeof(float2);   // < 2^32 (checked at load)
-    o.test = c.v != kNoHolder ? (uint32_t)l + 1 : 0;
+    o.test = v != kNoHolder ? (uint32_t)st + 1 : 0;
     o.len = rq.len[r];
     o.lam = bt * (uint32_t)l;   // <= len
     hot[i] = o;
@@ -482,9 +530,11 @@ __device__ inline Cold load_cold(const Cold *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
     Cold x;
     x.a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
-    x.r = w[2];
-    x.n = w[3];
-    x.v = w[4];
+    x.hoff = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
+    x.r = w[4];
+    x.n = w[5];
+    x.v = w[6];
+    x.m = w[7];
     return x;
 }
 
@@ -567,6 +617,35 @@ __device__ inline void probe_from(const Table &t, uint32_t base, cptr<uint64_t> 
     }
 }
 
+// The same scan over holder values looked up beforehand: hv[0..m) are the
+// holders of consecutive blocks from the first tested one, and the block
+// after them (if any) is held by no decode, so every lane still alive there
+// stops.  W values are read per step, then their bitmap words.
+template <int W, int C>
+__device__ inline void probe_pre(const Table &t, uint32_t base, cptr<uint32_t> hv, uint32_t m, lmask (&alive)[C],
+                                 uint32_t (&lam)[C], uint32_t bt) {
+    lmask mk[C];
+    for (uint32_t k0 = 0; k0 < m; k0 += W) {
+        lmask any = 0;
+#pragma unroll
+        for (int q = 0; q < C; ++q) any |= alive[q];
+        if (!any) break;
+        uint32_t v[W];
+#pragma unroll
+        for (int w = 0; w < W; ++w) v[w] = k0 + w < m ? hv[k0 + w] : kNoHolder;
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            if (k0 + w >= m) break;
+            holder_masks<C>(t, v[w], base, mk);
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                alive[q] &= mk[q];
+                lam[q] += in_mask(alive[q]) ? bt : 0u;
+            }
+        }
+    }
+}
+
 // What one scan step fetches for the next request: its row of (seconds per
 // token, constant part) on each column.
 template <int C>
@@ -599,6 +678,7 @@ __device__ inline float2 load_row(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, u
 template <int K, int W, int C, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot *__restrict__ hot,
                                                       const Cold *__restrict__ cold,
+                                                      const uint32_t *__restrict__ hvals,
                                                       const uint64_t *__restrict__ hashes,
                                                       const uint32_t *__restrict__ n_valid, uint32_t n_req,
                                                       uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
@@ -626,12 +706,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     const uint32_t bt = s.block_tokens;
     uint32_t d[C], voff[C], xm[C];
     bool act[C];
-    lmask actm[C], okm[C];
+    lmask okm[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
         act[q] = d[q] < s.D;
-        actm[q] = ballot(act[q]);
         const uint32_t pc = act[q] ? d[q] : 0;
         voff[q] = pc * (uint32_t)sizeof(float2);
         // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
@@ -641,6 +720,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         xm[q] = xlim == 0 ? 0u : xlim - 1 > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)(xlim - 1);
     }
     const cptr<uint64_t> chash = as_const(hashes);
+    const cptr<uint32_t> chv = as_const(hvals);
     // rows of (seconds per token, constant part) through a buffer resource:
     // a row's byte offset is the scalar offset, the column's the lane offset
     const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);   // < 2^32 (checked at load)
@@ -651,17 +731,16 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     Ahead<C> A, B;
 #pragma unroll
     for (int q = 0; q < C; ++q) A.v[q] = load_row(slr, voff[q], c0.row);
-    // the run's first request is scanned from block 0
+    // the run's first request is scanned from block 0 (its records say so)
     const Cold k0 = load_cold(cold, i0);
-    const uint32_t v00 = k0.n ? holder_uniform(t, chash[k0.a]) : kNoHolder;
     // the current request's carried tokens lamL = B_tok * L0 and its first
-    // test, of block L0 when t0 = L0 + 1 (0: no test, when block L0 does not
+    // test, of block T when t0 = T + 1 (0: no test, when the block does not
     // exist or no decode holds it)
     uint32_t lamL = 0;
-    uint32_t t0 = v00 != kNoHolder ? 1u : 0u;
-    uint32_t lam_prev[C];
+    uint32_t t0 = c0.test;
+    uint32_t lam[C];   // B_tok * (prefix length) of the current request, carried over
 #pragma unroll
-    for (int q = 0; q < C; ++q) lam_prev[q] = 0;
+    for (int q = 0; q < C; ++q) lam[q] = 0;
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
     static_assert(kPer % 2 == 0, "chunks pair up with the two row buffers");
     uint32_t pc_bits = 0xFFFFFFFFu, pc_idx = 0xFFFFFFFFu;   // gathered keys (empty = ~0)
@@ -670,31 +749,26 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         const Hot c2 = load_hot(hot, i + 2);
 #pragma unroll
         for (int q = 0; q < C; ++q) nxt.v[q] = load_row(slr, voff[q], c1.row);
-        // prefix lengths: carried where the common leading run decides them
-        uint32_t lam[C];
+        // prefix lengths: carried where the common leading run decides them;
+        // the columns whose previous length reaches the common run need a
+        // test (lanes past the last decode hold no bitmap bits and stop at
+        // their first test)
         lmask need[C];
-#pragma unroll
-        for (int q = 0; q < C; ++q) {
-            lam[q] = min(lam_prev[q], lamL);
-            need[q] = ballot(lam_prev[q] >= lamL) & actm[q];
-        }
         if (t0) {
-            // the cold record (holder of the first tested block) and the
+#pragma unroll
+            for (int q = 0; q < C; ++q) need[q] = ballot(lam[q] >= lamL);
+        }
+#pragma unroll
+        for (int q = 0; q < C; ++q) lam[q] = min(lam[q], lamL);
+        if (t0) {
+            // the cold record (holders of the blocks to test) and the
             // first-miss scan on the columns that need it (only a small
             // share of requests probes at all, so nothing is fetched ahead)
-            uint64_t a;
-            uint32_t n, v0;
-            if (i == i0) {
-                a = k0.a;
-                n = k0.n;
-                v0 = v00;
-            } else {
-                const Cold k = load_cold(cold, i);
-                a = k.a;
-                n = k.n;
-                v0 = k.v;
-            }
-            probe_from<W, C>(t, base, chash + a, n, t0 - 1, need, lam, bt, v0);
+            const Cold k = i == i0 ? k0 : load_cold(cold, i);
+            if (k.m != kNoPre)
+                probe_pre<W, C>(t, base, chv + k.hoff, k.m, need, lam, bt);
+            else
+                probe_from<W, C>(t, base, chash + k.a, k.n, t0 - 1, need, lam, bt, k.v);
         }
         // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
         uint32_t r_out = 0;
@@ -702,7 +776,6 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         uint32_t cb[C];
 #pragma unroll
         for (int q = 0; q < C; ++q) {
-            lam_prev[q] = lam[q];
             const uint32_t x = c0.len - lam[q];
             const bool feas = in_mask(okm[q]) && x <= xm[q];
             const float cost = fmaf((float)x, cur.v[q].x, cur.v[q].y);
@@ -1405,6 +1478,9 @@ struct netkv_ctx {
     Hot *hot = nullptr;   // sorted request records, the part every scan step reads
     Cold *cold = nullptr; // and the part read by probing requests
     uint32_t *n_valid = nullptr;
+    uint32_t *hv = nullptr;                  // holder values of the blocks probing positions test
+    uint64_t hv_cap = 0;
+    unsigned long long *hv_used = nullptr;
     void *sort_tmp = nullptr;
     size_t sort_tmp_bytes = 0;
     uint64_t *partial = nullptr;
@@ -1570,7 +1646,7 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-constexpr int kSpec = 2;            // blocks looked up together per extension step
+constexpr int kSpec = 4;            // blocks looked up together per extension step
 constexpr uint32_t kLcpLanes = 8;   // lanes per sorted position in lcp_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
@@ -1578,7 +1654,8 @@ constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths
 // algorithm by size).
 using SortConfig = rocprim::default_config;
 
-netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, hipStream_t st) {
+netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, uint64_t n_hashes,
+                                  hipStream_t st) {
     if (R > h->order_cap) {
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->sort_tmp);
@@ -1600,6 +1677,17 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         h->order_cap = R;
     }
     if (!h->n_valid && dalloc(h->n_valid, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    if (!h->hv_used && dalloc(h->hv_used, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    // holder values of probing positions: at most one per block of the batch
+    // (fewer if runs overlap in the hash array; positions that do not fit
+    // look their blocks up during the scan)
+    if (n_hashes > h->hv_cap || !h->hv) {
+        dfree(h->hv);
+        h->hv_cap = 0;
+        if (dalloc(h->hv, std::max<uint64_t>(n_hashes, 1)) != hipSuccess)
+            return fail(h, NETKV_ENOMEM, "holder value scratch allocation failed");
+        h->hv_cap = std::max<uint64_t>(n_hashes, 1);
+    }
     if (partial_elems > h->partial_cap) {
         dfree(h->partial);
         h->partial_cap = 0;
@@ -1611,21 +1699,27 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
 }
 
 uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
-    // runs of 256 sorted requests on large batches (R * groups >= 2^24), else
-    // 512, shortened while that leaves fewer than 8K wavefronts (measured on
-    // MI355X: longer runs carry more first-miss indices, shorter ones keep
-    // more wavefronts in flight)
+    // runs of 128 sorted requests, shortened (to 8 at least) while that
+    // leaves fewer than 8K wavefronts (measured on MI355X: on the
+    // 4,096-GPU workloads 128 beats both 64, which starts more runs with a
+    // full scan, and 256, which keeps fewer wavefronts in flight)
     const uint64_t work = R * ngroup;
-    uint64_t rl = work >= (1ull << 24) ? 256 : 512;
-    if (rl > work / 8192) rl = work / 8192;
-    if (rl < 8) rl = 8;
+    uint64_t rl = 128;
+    while (rl > 8 && work / rl < 8192) rl /= 2;
     return (uint32_t)rl;
 }
 
-// decodes per lane: 2 when there are at least 256 decodes, else 1 (or the
-// option: 1, 2 or 4)
+// decodes per lane (or the option: 1, 2, 3, 4 or 6): the widest of 6, 3
+// and 2 whose groups of 64 * C decodes split evenly over the XCDs (at least
+// one each), so that every XCD's L2 keeps its own slice of the snapshot
+// rows; else 2 on pools of 256+ decodes, else 1 (measured on MI355X: wider
+// groups share each request's scalar work over more decodes)
 inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
-    if (opt == 1 || opt == 2 || opt == 4) return opt;
+    if (opt == 1 || opt == 2 || opt == 3 || opt == 4 || opt == 6) return opt;
+    for (uint32_t c : {6u, 3u, 2u}) {
+        const uint32_t g = (D + kWave * c - 1) / (kWave * c);
+        if (g >= kXcds && g % kXcds == 0) return c;
+    }
     return D >= 4u * kWave ? 2u : 1u;
 }
 
@@ -1641,10 +1735,10 @@ void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &or
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
     const uint32_t grid = (uint32_t)grid64;
     if (pairs)
-        hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
+        hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, ord.hv,
                            rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
     else
-        hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
+        hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, ord.hv,
                            rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
 }
 
@@ -1656,8 +1750,12 @@ hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, co
                               float *score, hipStream_t st) {
     hipError_t e = hipSuccess;
     if ((e = time_begin(h, st)) != hipSuccess) return e;
-    if (C == 4)
+    if (C == 6)
+        launch_scan<K, 6>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+    else if (C == 4)
         launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+    else if (C == 3)
+        launch_scan<K, 3>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 2)
         launch_scan<K, 2>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else
@@ -1677,7 +1775,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
     const uint32_t C = cols_per_lane(h->D, h->cols_opt);
     const uint32_t ngroup = (h->D + kWave * C - 1) / (kWave * C);
-    netkv_status e = ensure_order_scratch(h, R, R * ngroup * K, st);
+    netkv_status e = ensure_order_scratch(h, R, R * ngroup * K, req->n_hashes, st);
     if (e) return e;
     const Snap sn = make_snap(h);
     const Table t = make_table(h);
@@ -1686,7 +1784,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
                        h->dxlim);
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
-                       h->vals_in, h->errword, h->zflag);
+                       h->vals_in, h->errword, h->zflag, h->hv_used);
     if (rq.n_hashes)
         hipLaunchKernelGGL(count_zero_kernel, dim3(grid_for(rq.n_hashes, 256, 8192)), dim3(256), 0, st, rq.hashes,
                            rq.n_hashes, h->zflag);
@@ -1696,13 +1794,14 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     size_t tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                     (uint32_t)R, 0, 32, st));
-    hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)(((R + kHotPad) * kLcpLanes + 255) / 256)), dim3(256), 0,
-                       st, rq, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->hot, h->cold,
-                       h->n_valid);
-    HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
-    Order ord{h->perm, h->hot, h->cold, h->n_valid};
+    hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)(((R + kHotPad) * kLcpLanes + 255) / 256)), dim3(256), 0,
+                       st, rq, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
+                       (const uint32_t *)h->keys_out, t, h->reuse_opt, run_len, h->hot, h->cold, h->hv, h->hv_cap,
+                       h->hv_used, h->n_valid);
+    HIPCHK(h, hipGetLastError());
+    Order ord{h->perm, h->hot, h->cold, h->hv, h->n_valid};
     if (K == 1)
         HIPCHK(h, launch_scan_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
                                         pairs, k, idx, score, st));
@@ -1772,7 +1871,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->adm);
         dfree(h->bytes);
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
-        dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial);
+        dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial); dfree(h->hv); dfree(h->hv_used);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
         for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
@@ -1927,9 +2026,11 @@ netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t 
     if (off[n_decode] > n_hashes) return fail(h, NETKV_EINVAL, "hash_off[n_decode] exceeds n_hashes");
     const uint64_t first = off[0], total = off[n_decode] - off[0];
     if (total >= (1ull << 31)) return fail(h, NETKV_ECAPACITY, "more than 2^31 - 1 resident hashes");
-    // words per holder bitmap row: whole 64-decode words, a multiple of 4
-    // (32-byte rows, so a wavefront's words are one aligned scalar load)
-    const uint32_t bpitch = (uint32_t)((((uint64_t)n_decode + 63) / 64 + 3) & ~3ull);
+    // words per holder bitmap row: whole 64-decode words, rounded up to a
+    // multiple of 12 so that every decodes-per-lane choice C (1, 2, 3, 4, 6)
+    // reads its groups' C words inside the row, at 8 * C-byte alignment
+    const uint64_t bwords = ((uint64_t)n_decode + 63) / 64;
+    const uint32_t bpitch = (uint32_t)((bwords + 11) / 12 * 12);
     uint64_t *dh = nullptr, *dkey = nullptr, *doff = nullptr;
     uint32_t *dec_in = nullptr, *dec = nullptr;
     unsigned long long *cnt = nullptr;
@@ -2383,8 +2484,8 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
         h->policy_opt = value;
         return NETKV_OK;
     case NETKV_OPT_COLS:
-        if (value != 0 && value != 1 && value != 2 && value != 4)
-            return fail(h, NETKV_EINVAL, "decodes per lane must be 0 (automatic), 1, 2 or 4");
+        if (value != 0 && value != 1 && value != 2 && value != 3 && value != 4 && value != 6)
+            return fail(h, NETKV_EINVAL, "decodes per lane must be 0 (automatic), 1, 2, 3, 4 or 6");
         h->cols_opt = value;
         return NETKV_OK;
     default:

@@ -112,7 +112,7 @@ def test_ragged_decodes_long_runs_and_empty_runs(nk):
 
 
 def test_tuning_options_leave_results_unchanged(nk):
-    """Decodes per lane (1, 2, 4), run lengths (1, 7, automatic, longer
+    """Decodes per lane (1, 2, 3, 4, 6), run lengths (1, 7, automatic, longer
     than the batch) and first-miss reuse on/off are layout choices only:
     every pair and every top-k entry is bit-identical across them, and the
     first matches the oracle.  270 decodes leave a partial last group of
@@ -124,7 +124,7 @@ def test_tuning_options_leave_results_unchanged(nk):
     snap, req, cache = _inputs(cfg, 8, "random")
     sel = _gpu(nk, snap, cache)
     base = None
-    for cols in (1, 2, 4):
+    for cols in (1, 2, 3, 4, 6):
         for rl in (1, 7, 0, 5000):
             for reuse in (1, 0):
                 if reuse == 0 and rl not in (0, 7):
