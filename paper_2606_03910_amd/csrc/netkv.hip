@@ -34,6 +34,7 @@
 //   commit kernels -- between-batch counter / queue / memory update.
 #include <hip/hip_runtime.h>
 #include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/device/device_scan.hpp>
 
 #include <algorithm>
 #include <cmath>
@@ -145,16 +146,18 @@ __host__ __device__ inline uint32_t sl_pitch(uint32_t D) {
     return lines * 16u;
 }
 
-// Holder value of h, by one thread (vector loads of both candidate buckets).
+// Holder value of h, by one thread: both candidate buckets' keys, then the
+// value of the slot that holds h (most looked-up hashes are held by no
+// decode and need no value).
 __device__ inline uint32_t holder_lane(const Table &t, uint64_t h) {
     if (h == 0) return kNoHolder;
     uint32_t b1, b2;
     buckets_of(h, t.shift, b1, b2);
     const ulonglong2 k1 = *(const ulonglong2 *)(t.keys + 2 * (uint64_t)b1);
     const ulonglong2 k2 = *(const ulonglong2 *)(t.keys + 2 * (uint64_t)b2);
-    const uint2 v1 = *(const uint2 *)(t.vals + 2 * (uint64_t)b1);
-    const uint2 v2 = *(const uint2 *)(t.vals + 2 * (uint64_t)b2);
-    return k1.x == h ? v1.x : k1.y == h ? v1.y : k2.x == h ? v2.x : k2.y == h ? v2.y : kNoHolder;
+    const uint64_t slot = k1.x == h ? 2 * (uint64_t)b1 : k1.y == h ? 2 * (uint64_t)b1 + 1
+                        : k2.x == h ? 2 * (uint64_t)b2 : k2.y == h ? 2 * (uint64_t)b2 + 1 : ~0ull;
+    return slot == ~0ull ? kNoHolder : t.vals[slot];
 }
 
 // Is h resident on decode d?
@@ -289,51 +292,84 @@ __global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict_
 
 // ---------------------------------------------------------------- batch order
 //
-// Requests are scored in an order that groups equal leading blocks: the sort
-// key is 19 bits of the first block hash above 12 bits of the complemented
-// run length, so requests that start with the same prefix become neighbours
-// in descending length.  For neighbours r' -> r with a common leading run of
-// L blocks, the first-miss index of r on decode d follows from that of r'
-// without any probe whenever it lies inside the common run (j' < L gives
-// j = j'), and otherwise scanning resumes at block L (j' >= L implies blocks
-// 0..L-1 are resident).  Longest first, a request that is a prefix of its
-// predecessor has L = n_r and never probes; one that leaves the shared chain
-// first resumes at a block of its own, which usually no decode holds (known
-// from the holder index before the scan, so no probe).  The order changes
-// which probes are made, never a result.
+// Prefix lengths follow from a batch order that groups equal leading blocks.
+// The sort key is 19 bits of the first block hash above 12 bits of the
+// complemented run length, so requests that start with the same prefix are
+// neighbours in descending length ("hash order").  For neighbours r' -> r
+// with a common leading run of L blocks, the first-miss index of r on any
+// decode d is j(r', d) whenever that lies inside the common run (blocks
+// 0..j(r',d) of r are those of r'), and otherwise it is at least L.  So if
+// block L of r is held by no decode (or r has no block L), j(r, d) =
+// min(j(r', d), L) exactly, on every decode.
+//
+// A position whose block L some decode holds is a "leader": its prefix
+// lengths are computed from block 0 on every decode (leader kernel).  Every
+// other position m then has j(m, d) = min(j(ell, d), L*) with ell the last
+// leader before it in hash order and L* the least common run L over the
+// positions after ell up to m; with no leader before it, j = 0.  A
+// segmented scan over the hash order gives each position its (ell, L*).
+// Longest first, a request that is a prefix of its predecessor has L = n_r
+// and one that leaves the shared chain first resumes at a block of its own,
+// which usually no decode holds, so leaders are about one per shared chain.
+//
+// Scoring then runs in prefill order (the hash order kept within each
+// prefill, a stable radix sort): consecutive requests share their row of
+// the snapshot and often their leader, so both are re-read from L1.
 
 constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
+constexpr uint32_t kNoLead = 0xFFFFFFFFu;        // no leader before the position
+constexpr uint32_t kLeadOver = 0xFFFFFFFEu;      // a leader beyond the leader table's capacity
+constexpr uint32_t kNoCap = 0xFFFFFFFFu;         // L* of a leader itself (no cap)
 
-// One sorted request, everything the scan needs without indirection.
-// The part every scan step reads (one 16-byte scalar load) ...
-struct alignas(16) Hot {
-    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * slp * 8
-    uint32_t test;   // lcp + 1 if block lcp exists and some decode holds it (a carried scan
-                     // tests it), else 0
-    uint32_t len;    // input tokens
-    uint32_t lam;    // B_tok * lcp: tokens of the leading blocks in common with the
-                     // previous sorted request
+// Segmented-scan element of a hash-order position: leader slot (or kNoLead
+// for a non-leader) in the high word, common run L (kNoCap for a leader) in
+// the low word.  Combining keeps the later leader, else the earlier leader
+// with the smaller L; the combination is associative.
+__host__ __device__ inline uint64_t seg_elem(uint32_t slot, uint32_t l) { return ((uint64_t)slot << 32) | l; }
+struct SegOp {
+    __host__ __device__ uint64_t operator()(uint64_t a, uint64_t b) const {
+        if ((uint32_t)(b >> 32) != kNoLead) return b;
+        const uint32_t la = (uint32_t)a, lb = (uint32_t)b;
+        return (a & 0xFFFFFFFF00000000ull) | (la < lb ? la : lb);
+    }
 };
-constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead by the scan
 
-// ... and the part read only by requests that probe (and for per-pair output).
-struct alignas(16) Cold {
+// A leader: where its blocks' holder values start in hv (from block 0, up
+// to the first block no decode holds; m = kNoPre if they did not fit), and
+// its hash run for lookups otherwise.
+struct alignas(16) Lead {
     uint64_t a;      // offset of the hash run
-    uint64_t hoff;   // offset of the holder values of the blocks from the first tested one
-    uint32_t r;      // request index in the caller's batch
+    uint64_t hoff;   // offset of the holder values
     uint32_t n;      // hashed blocks
-    uint32_t v;      // holder value of the first tested block (kNoHolder: no test)
-    uint32_t m;      // holder values stored at hoff (the block after them, if any, is held by
-                     // no decode); kNoPre if none could be stored
+    uint32_t m;      // stored holder values, or kNoPre
+    uint32_t pad[2];
 };
 constexpr uint32_t kNoPre = 0xFFFFFFFFu;
 
+// One request in scoring order: the part every scoring step reads (one
+// 16-byte scalar load) ...
+struct alignas(16) Hot {
+    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * slp * 8
+    uint32_t slot;   // leader slot, kNoLead (prefix length 0 everywhere) or kLeadOver
+    uint32_t len;    // input tokens
+    uint32_t lams;   // B_tok * L* (kNoCap for a leader)
+};
+constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead by the scan
+
+// ... and the rest (output index; hash run, read only when a request has
+// to be matched on its own).
+struct alignas(16) Cold {
+    uint64_t a;      // offset of the hash run
+    uint32_t r;      // request index in the caller's batch
+    uint32_t n;      // hashed blocks
+};
+
 struct Order {
-    const uint32_t *perm;     // sorted position -> request
-    const Hot *hot;           // [n_valid] sorted request records
-    const Cold *cold;
-    const uint32_t *hv;       // holder values of the blocks probing positions test
+    const Hot *hot;           // [n_valid + kHotPad] scoring-order request records
+    const Cold *cold;         // [n_req]
+    const uint32_t *lam;      // [leaders][D] B_tok * prefix length of each leader on each decode
+    const uint32_t *hv;       // holder values of the leaders' blocks
     const uint32_t *n_valid;  // valid requests (they sort first)
 };
 
@@ -343,16 +379,18 @@ struct Order {
 // The reserved hash value 0 is looked for separately: a flat scan of the
 // batch's hash array (count_zero_kernel) raises `zflag`, and only then does
 // zero_fix_kernel check each request's run and invalidate those holding it.
-// Thread 0 clears zflag for that scan, and the holder-value counter of the
-// order kernel.
+// Thread 0 clears zflag for that scan, and the holder-value and leader
+// counters of the order kernel.
 __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max_blocks, uint32_t *__restrict__ keys,
                                                    uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
                                                    uint32_t *__restrict__ zflag,
-                                                   unsigned long long *__restrict__ hv_used) {
+                                                   unsigned long long *__restrict__ hv_used,
+                                                   unsigned int *__restrict__ n_lead) {
     const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
     if (r == 0) {
         *zflag = 0;
         *hv_used = 0;
+        *n_lead = 0;
     }
     bool bad = false;
     if (r < rq.n_req) {
@@ -403,38 +441,40 @@ __global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint3
     if (found && lane == 0) atomicOr(err, kErrZeroHash);
 }
 
-// Record of each sorted request, with its common leading blocks with the
-// previous sorted request: G lanes per sorted position (G divides 64)
-// compare G blocks per step, their loads issued together.  Also stores the
+// Per hash-order position i (G lanes, G divides 64): the common leading run
+// L with the previous position (G blocks compared per step, their loads
+// issued together), whether the position is a leader (some decode holds its
+// block L), and for a leader a slot of the leader table and the holder
+// values of its blocks from block 0 (into hv, from a shared counter).
+// Writes the segmented-scan element and the prefill sort key of i, and the
 // number of valid requests (valid keys sort first): the last valid position
-// writes it, or position 0 writes 0.  Positions of invalid requests and the
-// kHotPad positions past the batch get a record that the scan may read ahead
-// but never scores (row 0, no blocks, no test).
-//
-// The first block a scan tests for a position is block 0 at the start of a
-// run (nothing is carried across runs) and else the end of the common run.
-// If some decode holds it, the position's lanes look up the holders of the
-// following blocks too, up to the first one no decode holds, into hv (from a
-// shared counter), so that the scan waits on bitmap words only.
+// writes it, or position 0 writes 0.  Invalid positions sort after every
+// prefill (key P).
 template <uint32_t G>
-__global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_t bt, const uint32_t *__restrict__ perm,
-                                                  const uint32_t *__restrict__ sorted_keys, Table t, uint32_t reuse,
-                                                  uint32_t run_len, Hot *__restrict__ hot, Cold *__restrict__ cold,
-                                                  uint32_t *__restrict__ hv, uint64_t hv_cap,
-                                                  unsigned long long *__restrict__ hv_used,
-                                                  uint32_t *__restrict__ n_valid) {
+__global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, const uint32_t *__restrict__ perm,
+                                                    const uint32_t *__restrict__ sorted_keys, Table t,
+                                                    uint32_t reuse, uint64_t *__restrict__ seg,
+                                                    uint32_t *__restrict__ pkey, uint32_t *__restrict__ pval,
+                                                    Lead *__restrict__ lead, uint32_t lead_cap,
+                                                    unsigned int *__restrict__ n_lead, uint32_t *__restrict__ hv,
+                                                    uint64_t hv_cap, unsigned long long *__restrict__ hv_used,
+                                                    uint32_t *__restrict__ n_valid) {
     const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t sub = threadIdx.x % G;
-    const uint32_t seg = (threadIdx.x % kWave) - sub;   // first lane of this position's lanes
+    const uint32_t seg0 = (threadIdx.x % kWave) - sub;   // first lane of this position's lanes
     const uint64_t i = tid / G;
-    if (i >= (uint64_t)rq.n_req + kHotPad) return;
-    const bool valid = i < rq.n_req && sorted_keys[i] < kKeyInvalid;
+    if (i >= (uint64_t)rq.n_req) return;
+    const bool valid = sorted_keys[i] < kKeyInvalid;
     if (sub == 0) {
         if (valid && (i + 1 == rq.n_req || sorted_keys[i + 1] >= kKeyInvalid)) *n_valid = (uint32_t)(i + 1);
         if (i == 0 && !valid) *n_valid = 0;
+        pval[i] = (uint32_t)i;
     }
     if (!valid) {
-        if (sub == 0) hot[i] = Hot{0, 0, 0, 0};
+        if (sub == 0) {
+            seg[i] = seg_elem(kNoLead, 0);
+            pkey[i] = P;
+        }
         return;
     }
     const uint32_t r = perm[i];
@@ -450,7 +490,7 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_
         for (uint64_t base = 0; base < m; base += G) {
             const uint64_t x = base + sub;
             const bool stop = x >= m || rq.hashes[a + x] != rq.hashes[b + x];
-            const uint32_t bits = (uint32_t)(__ballot(stop) >> seg) & (uint32_t)((1ull << G) - 1);
+            const uint32_t bits = (uint32_t)(__ballot(stop) >> seg0) & (uint32_t)((1ull << G) - 1);
             if (bits) {
                 const uint64_t first = base + (uint64_t)__builtin_ctz(bits);
                 l = first < m ? first : m;
@@ -458,51 +498,96 @@ __global__ __launch_bounds__(256) void lcp_kernel(Reqs rq, uint32_t slp, uint32_
             }
         }
     }
-    const uint64_t st = (i % run_len == 0) ? 0 : l;   // first tested block
-    uint32_t v = kNoHolder;
-    if (sub == 0 && st < nr) v = holder_lane(t, rq.hashes[a + st]);
-    v = __shfl(v, (int)seg, kWave);
-    uint64_t hoff = 0;
-    uint32_t m = kNoPre;
-    if (v != kNoHolder) {
-        // room for every block from st on; the holders end at the first block
-        // no decode holds
-        unsigned long long o = 0;
-        if (sub == 0) o = atomicAdd(hv_used, (unsigned long long)(nr - st));
-        hoff = __shfl(o, (int)seg, kWave);
-        if (hoff + (nr - st) <= hv_cap) {
-            m = (uint32_t)(nr - st);
-            for (uint64_t k0 = 0; k0 < nr - st; k0 += G) {
-                const uint64_t k = k0 + sub;
-                uint32_t hk = kNoHolder;
-                if (k < nr - st) {
-                    hk = k == 0 ? v : holder_lane(t, rq.hashes[a + st + k]);
-                    hv[hoff + k] = hk;
+    // a leader if some decode holds block L
+    uint32_t vl = kNoHolder;
+    if (sub == 0 && l < nr) vl = holder_lane(t, rq.hashes[a + l]);
+    vl = __shfl(vl, (int)seg0, kWave);
+    uint64_t e = seg_elem(kNoLead, (uint32_t)l);
+    if (vl != kNoHolder) {
+        unsigned int slot = 0;
+        if (sub == 0) slot = atomicAdd(n_lead, 1u);
+        slot = __shfl(slot, (int)seg0, kWave);
+        if (slot >= lead_cap) {
+            e = seg_elem(kLeadOver, kNoCap);
+        } else {
+            e = seg_elem(slot, kNoCap);
+            // holder values of blocks 0, 1, ... up to the first block no decode holds
+            unsigned long long o = 0;
+            if (sub == 0) o = atomicAdd(hv_used, (unsigned long long)nr);
+            const uint64_t hoff = __shfl(o, (int)seg0, kWave);
+            uint32_t m = kNoPre;
+            if (hoff + nr <= hv_cap) {
+                m = (uint32_t)nr;
+                for (uint64_t k0 = 0; k0 < nr; k0 += G) {
+                    const uint64_t k = k0 + sub;
+                    uint32_t hk = kNoHolder;
+                    if (k < nr) {
+                        hk = k == l ? vl : holder_lane(t, rq.hashes[a + k]);
+                        hv[hoff + k] = hk;
+                    }
+                    const uint32_t none = (uint32_t)(__ballot(k < nr && hk == kNoHolder) >> seg0) &
+                                          (uint32_t)((1ull << G) - 1);
+                    if (none) {
+                        m = (uint32_t)(k0 + (uint64_t)__builtin_ctz(none));
+                        break;
+                    }
                 }
-                const uint32_t none = (uint32_t)(__ballot(k < nr - st && hk == kNoHolder) >> seg) &
-                                      (uint32_t)((1ull << G) - 1);
-                if (none) {
-                    m = (uint32_t)(k0 + (uint64_t)__builtin_ctz(none));
-                    break;
-                }
+            }
+            if (sub == 0) {
+                Lead ld;
+                ld.a = a;
+                ld.hoff = hoff;
+                ld.n = (uint32_t)nr;
+                ld.m = m;
+                ld.pad[0] = ld.pad[1] = 0;
+                lead[slot] = ld;
             }
         }
     }
-    if (sub != 0) return;
+    if (sub == 0) {
+        seg[i] = e;
+        pkey[i] = rq.prefill[r];
+    }
+}
+
+// Scoring-order records: position k of the prefill order holds hash-order
+// position pord[k]; its leader slot and L* come from the scan.  Positions
+// past the batch (kHotPad of them) get a record that the scan may read
+// ahead but never scores (row 0, no leader).
+__global__ __launch_bounds__(256) void assemble_kernel(Reqs rq, uint32_t slp, uint32_t bt,
+                                                       const uint32_t *__restrict__ perm,
+                                                       const uint32_t *__restrict__ pord,
+                                                       const uint64_t *__restrict__ scanned,
+                                                       const uint32_t *__restrict__ n_valid,
+                                                       Hot *__restrict__ hot, Cold *__restrict__ cold) {
+    const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= (uint64_t)rq.n_req + kHotPad) return;
+    if (k >= rq.n_req) {
+        hot[k] = Hot{0, kNoLead, 0, 0};
+        return;
+    }
+    const uint32_t i = pord[k];
+    const uint32_t r = perm[i];
     Cold c;
-    c.a = a;
-    c.hoff = hoff;
     c.r = r;
-    c.n = (uint32_t)nr;
-    c.v = v;
-    c.m = m;
+    c.a = 0;
+    c.n = 0;
+    if (k >= *n_valid) {
+        hot[k] = Hot{0, kNoLead, 0, 0};
+        cold[k] = c;
+        return;
+    }
+    const uint64_t e = scanned[i];
+    const uint32_t slot = (uint32_t)(e >> 32), ls = (uint32_t)e;
+    c.a = rq.off[r];
+    c.n = (uint32_t)(rq.off[r + 1] - c.a);
     Hot o;
     o.row = rq.prefill[r] * slp * (uint32_t)sizeof(float2);   // < 2^32 (checked at load)
-    o.test = v != kNoHolder ? (uint32_t)st + 1 : 0;
+    o.slot = slot;
     o.len = rq.len[r];
-    o.lam = bt * (uint32_t)l;   // <= len
-    hot[i] = o;
-    cold[i] = c;
+    o.lams = ls == kNoCap ? kNoCap : bt * ls;   // ls <= n_r, so bt * ls <= len
+    hot[k] = o;
+    cold[k] = c;
 }
 
 // Read-only data that is uniform across a wavefront (request records, hash
@@ -520,9 +605,9 @@ __device__ inline Hot load_hot(const Hot *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
     Hot x;
     x.row = w[0];
-    x.test = w[1];
+    x.slot = w[1];
     x.len = w[2];
-    x.lam = w[3];
+    x.lams = w[3];
     return x;
 }
 
@@ -530,11 +615,8 @@ __device__ inline Cold load_cold(const Cold *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
     Cold x;
     x.a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
-    x.hoff = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
-    x.r = w[4];
-    x.n = w[5];
-    x.v = w[6];
-    x.m = w[7];
+    x.r = w[2];
+    x.n = w[3];
     return x;
 }
 
@@ -646,12 +728,51 @@ __device__ inline void probe_pre(const Table &t, uint32_t base, cptr<uint32_t> h
     }
 }
 
-// What one scan step fetches for the next request: its row of (seconds per
-// token, constant part) on each column.
-template <int C>
-struct Ahead {
-    float2 v[C];
-};
+// Prefix lengths of every leader on every decode: one wavefront per
+// (leader, group of 64*C decodes) runs the first-miss scan from block 0 over
+// the holder values the order kernel looked up (or over the hash run when
+// they did not fit) and writes B_tok * j for its decodes.  The wavefronts
+// loop over the (leader, group) tasks; the leader count is read from device
+// memory, so every wavefront ends after at most ceil(tasks / wavefronts)
+// tasks.
+template <int W, int C>
+__global__ __launch_bounds__(kBlock) void lead_kernel(Table t, uint32_t D, uint32_t bt, const Lead *__restrict__ lead,
+                                                      const unsigned int *__restrict__ n_lead, uint32_t lead_cap,
+                                                      const uint32_t *__restrict__ hv,
+                                                      const uint64_t *__restrict__ hashes, uint32_t ngroup,
+                                                      uint32_t *__restrict__ lam_out) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t nl_all = *n_lead;
+    const uint32_t nl = nl_all < lead_cap ? nl_all : lead_cap;
+    const uint64_t tasks = (uint64_t)nl * ngroup;
+    const uint64_t nw = (uint64_t)gridDim.x * kWavesPerBlock;
+    const cptr<uint64_t> chash = as_const(hashes);
+    const cptr<uint32_t> chv = as_const(hv);
+    for (uint64_t task = (uint64_t)blockIdx.x * kWavesPerBlock + wave_index(); task < tasks; task += nw) {
+        const uint32_t slot = (uint32_t)(task / ngroup), g = (uint32_t)(task % ngroup);
+        const uint32_t base = g * (kWave * C);
+        const cptr<uint32_t> w = as_const((const uint32_t *)(lead + slot));
+        const uint64_t a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
+        const uint64_t hoff = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
+        const uint32_t n = w[4], m = w[5];
+        uint32_t lam[C];
+        lmask alive[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            lam[q] = 0;
+            alive[q] = ~0ull;
+        }
+        if (m != kNoPre)
+            probe_pre<W, C>(t, base, chv + hoff, m, alive, lam, bt);
+        else if (n)
+            probe_from<W, C>(t, base, chash + a, n, 0, alive, lam, bt, holder_uniform(t, chash[a]));
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            const uint32_t d = base + q * kWave + lane;
+            if (d < D) lam_out[(uint64_t)slot * D + d] = lam[q];
+        }
+    }
+}
 
 // Buffer-resource word 3 for raw (untyped, unswizzled) buffer access on gfx9-class targets.
 constexpr int kBufferFlags = 0x00020000;
@@ -660,29 +781,29 @@ __device__ inline float2 load_row(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, u
     return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)lane_off, (int)row_off, 0));
 }
 
-// One wavefront per (run of sorted requests, group of 64*C decodes); lane l
-// holds decodes g*64*C + q*64 + l, q < C.  For each request of the run:
-// first-miss prefix length per decode (carried from the previous request
-// where the common leading run decides it), non-cached tokens, feasibility
-// and cost (Eqs. (2)-(7)), then the group's K best feasible (score, index)
-// keys into partial[group][sorted position][0..K).
-//
-// The prefix length is kept as lambda = B_tok * j (tokens), so the
-// non-cached tokens are one subtraction.  Request records are read two
-// requests ahead (the record array is padded so that this never needs a
-// bound), the request's row of (seconds per token, constant part) one
-// request ahead into the other of two buffers (the loop is unrolled by two
-// so neither buffer is copied); a request's cold record and first-test
-// buckets only when it probes.  Requests are taken in chunks of 64/K whose
-// keys are gathered one per lane and stored together.
+__device__ inline uint32_t load_lam(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t row_off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)lane_off, (int)row_off, 0);
+}
+
+// One wavefront per (run of scoring-order requests, group of 64*C decodes);
+// lane l holds decodes g*64*C + q*64 + l, q < C.  For each request of the
+// run: prefix lengths min(leader's, L*) (matched on its own when its leader
+// did not fit the leader table), non-cached tokens, feasibility and cost
+// (Eqs. (2)-(7)), then the group's K best feasible (score, index) keys into
+// partial[group][position][0..K).  Requests of one prefill are consecutive,
+// so the snapshot row stays in registers and is reloaded only when the
+// prefill changes; the leader's prefix lengths are kept too, and the next
+// request's are fetched during the current step only when its leader
+// differs.  Records are read two requests ahead.  Requests are taken in
+// chunks of 64/K whose keys are gathered one per lane and stored together.
 template <int K, int W, int C, bool PAIRS>
-__global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot *__restrict__ hot,
-                                                      const Cold *__restrict__ cold,
-                                                      const uint32_t *__restrict__ hvals,
-                                                      const uint64_t *__restrict__ hashes,
-                                                      const uint32_t *__restrict__ n_valid, uint32_t n_req,
-                                                      uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
-                                                      uint64_t *__restrict__ partial, PairOut po) {
+__global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Hot *__restrict__ hot,
+                                                       const Cold *__restrict__ cold,
+                                                       const uint32_t *__restrict__ lead_lam, uint32_t lead_cap,
+                                                       const uint64_t *__restrict__ hashes,
+                                                       const uint32_t *__restrict__ n_valid, uint32_t n_req,
+                                                       uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
+                                                       uint64_t *__restrict__ partial, PairOut po) {
     const uint32_t lane = threadIdx.x % kWave;
     uint32_t run, grp;
     if (ngroup % kXcds == 0) {
@@ -704,7 +825,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
     const uint32_t base = grp * (kWave * C);
     const uint32_t bt = s.block_tokens;
-    uint32_t d[C], voff[C], xm[C];
+    uint32_t d[C], voff[C], loff[C], xm[C];
     bool act[C];
     lmask okm[C];
 #pragma unroll
@@ -713,6 +834,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         act[q] = d[q] < s.D;
         const uint32_t pc = act[q] ? d[q] : 0;
         voff[q] = pc * (uint32_t)sizeof(float2);
+        loff[q] = pc * (uint32_t)sizeof(uint32_t);
         // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
         // xlim >= 1 (capped to 32 bits, as x is); xlim = 0 never is
         const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
@@ -720,111 +842,115 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
         xm[q] = xlim == 0 ? 0u : xlim - 1 > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)(xlim - 1);
     }
     const cptr<uint64_t> chash = as_const(hashes);
-    const cptr<uint32_t> chv = as_const(hvals);
-    // rows of (seconds per token, constant part) through a buffer resource:
-    // a row's byte offset is the scalar offset, the column's the lane offset
-    const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);   // < 2^32 (checked at load)
+    // rows of (seconds per token, constant part) and the leaders' prefix
+    // lengths through buffer resources: a row's byte offset is the scalar
+    // offset, the column's the lane offset
+    const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);        // < 2^32 (checked at load)
+    const uint64_t ll_bytes = (uint64_t)lead_cap * s.D * sizeof(uint32_t);   // < 2^32 (capacity is capped)
     const __amdgpu_buffer_rsrc_t slr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)s.sl, (short)0, (int)(uint32_t)(sl_bytes < 0xFFFFFFFFull ? sl_bytes : 0xFFFFFFFFull), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t llr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)lead_lam, (short)0, (int)(uint32_t)(ll_bytes < 0xFFFFFFFFull ? ll_bytes : 0xFFFFFFFFull),
+        kBufferFlags);
+    const uint32_t lstride = s.D * (uint32_t)sizeof(uint32_t);
     Hot c0 = load_hot(hot, i0);
     Hot c1 = load_hot(hot, i0 + 1);
-    Ahead<C> A, B;
+    float2 rowv[C];           // the current prefill's row
+    uint32_t rowcur = c0.row;
+    uint32_t laml[C], stg[C]; // the current leader's B_tok * j, and the next one's while it loads
 #pragma unroll
-    for (int q = 0; q < C; ++q) A.v[q] = load_row(slr, voff[q], c0.row);
-    // the run's first request is scanned from block 0 (its records say so)
-    const Cold k0 = load_cold(cold, i0);
-    // the current request's carried tokens lamL = B_tok * L0 and its first
-    // test, of block T when t0 = T + 1 (0: no test, when the block does not
-    // exist or no decode holds it)
-    uint32_t lamL = 0;
-    uint32_t t0 = c0.test;
-    uint32_t lam[C];   // B_tok * (prefix length) of the current request, carried over
-#pragma unroll
-    for (int q = 0; q < C; ++q) lam[q] = 0;
+    for (int q = 0; q < C; ++q) {
+        rowv[q] = load_row(slr, voff[q], c0.row);
+        laml[q] = c0.slot < kLeadOver ? load_lam(llr, loff[q], c0.slot * lstride) : 0u;
+        stg[q] = 0;
+    }
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
-    static_assert(kPer % 2 == 0, "chunks pair up with the two row buffers");
     uint32_t pc_bits = 0xFFFFFFFFu, pc_idx = 0xFFFFFFFFu;   // gathered keys (empty = ~0)
 
-    auto step = [&](uint32_t i, uint32_t slot, const Ahead<C> &cur, Ahead<C> &nxt) {
-        const Hot c2 = load_hot(hot, i + 2);
-#pragma unroll
-        for (int q = 0; q < C; ++q) nxt.v[q] = load_row(slr, voff[q], c1.row);
-        // prefix lengths: carried where the common leading run decides them;
-        // the columns whose previous length reaches the common run need a
-        // test (lanes past the last decode hold no bitmap bits and stop at
-        // their first test)
-        lmask need[C];
-        if (t0) {
-#pragma unroll
-            for (int q = 0; q < C; ++q) need[q] = ballot(lam[q] >= lamL);
-        }
-#pragma unroll
-        for (int q = 0; q < C; ++q) lam[q] = min(lam[q], lamL);
-        if (t0) {
-            // the cold record (holders of the blocks to test) and the
-            // first-miss scan on the columns that need it (only a small
-            // share of requests probes at all, so nothing is fetched ahead)
-            const Cold k = i == i0 ? k0 : load_cold(cold, i);
-            if (k.m != kNoPre)
-                probe_pre<W, C>(t, base, chv + k.hoff, k.m, need, lam, bt);
-            else
-                probe_from<W, C>(t, base, chash + k.a, k.n, t0 - 1, need, lam, bt, k.v);
-        }
-        // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
-        uint32_t r_out = 0;
-        if (PAIRS) r_out = load_cold(cold, i).r;
-        uint32_t cb[C];
-#pragma unroll
-        for (int q = 0; q < C; ++q) {
-            const uint32_t x = c0.len - lam[q];
-            const bool feas = in_mask(okm[q]) && x <= xm[q];
-            const float cost = fmaf((float)x, cur.v[q].x, cur.v[q].y);
-            if (PAIRS && act[q]) {
-                const uint64_t o = (uint64_t)r_out * s.D + d[q];
-                const uint32_t jq = lam[q] / bt;
-                if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
-                if (po.feas) po.feas[o] = feas ? 1 : 0;
-                if (po.score) po.score[o] = cost;
-                if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
-            }
-            cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
-        }
-        // the group's K best: least cost bits, then least decode index, i.e.
-        // the lowest lane holding the minimum in the first column that holds it
-#pragma unroll
-        for (int r = 0; r < K; ++r) {
-            uint32_t lm = cb[0];
-#pragma unroll
-            for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
-            const uint32_t mn = wave_min_u32_dpp(lm);
-            if (mn == 0xFFFFFFFFu) break;  // no feasible candidate left (uniform)
-            uint32_t dm = 0;
-#pragma unroll
-            for (int q = 0; q < C; ++q) {
-                const lmask m = ballot(cb[q] == mn);
-                if (m) {
-                    const uint32_t l = (uint32_t)__builtin_ctzll(m);
-                    dm = base + q * kWave + l;
-                    if (r + 1 < K && lane == l) cb[q] = 0xFFFFFFFFu;
-                    break;
-                }
-            }
-            if (lane == slot * K + (uint32_t)r) {
-                pc_bits = mn;
-                pc_idx = dm;
-            }
-        }
-        lamL = c1.lam;
-        t0 = c1.test;
-        c0 = c1;
-        c1 = c2;
-    };
     for (uint32_t g0 = i0; g0 < i1; g0 += kPer) {
         const uint32_t g1 = (g0 + kPer < i1) ? g0 + kPer : i1;
-        for (uint32_t i = g0; i < g1; i += 2) {
-            step(i, i - g0, A, B);
-            if (i + 1 >= g1) break;   // an odd count: only the run's last chunk (kPer is even)
-            step(i + 1, i + 1 - g0, B, A);
+        for (uint32_t i = g0; i < g1; ++i) {
+            const Hot c2 = load_hot(hot, i + 2);
+            // the next request's leader values, if they differ
+            const bool nl = c1.slot != c0.slot;
+            if (nl && c1.slot < kLeadOver) {
+#pragma unroll
+                for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, loff[q], c1.slot * lstride);
+            }
+            if (c0.row != rowcur) {
+#pragma unroll
+                for (int q = 0; q < C; ++q) rowv[q] = load_row(slr, voff[q], c0.row);
+                rowcur = c0.row;
+            }
+            // prefix lengths (as B_tok * j): the leader's, capped by L*
+            uint32_t lam[C];
+#pragma unroll
+            for (int q = 0; q < C; ++q) lam[q] = min(laml[q], c0.lams);
+            if (c0.slot == kLeadOver) {
+                // the leader did not fit the leader table: match this request
+                // on its own from block 0 (exact)
+                const Cold k = load_cold(cold, i);
+                lmask alive[C];
+#pragma unroll
+                for (int q = 0; q < C; ++q) {
+                    lam[q] = 0;
+                    alive[q] = ~0ull;
+                }
+                if (k.n)
+                    probe_from<W, C>(t, base, chash + k.a, k.n, 0, alive, lam, bt, holder_uniform(t, chash[k.a]));
+            }
+            // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
+            uint32_t r_out = 0;
+            if (PAIRS) r_out = load_cold(cold, i).r;
+            uint32_t cb[C];
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                const uint32_t x = c0.len - lam[q];
+                const bool feas = in_mask(okm[q]) && x <= xm[q];
+                const float cost = fmaf((float)x, rowv[q].x, rowv[q].y);
+                if (PAIRS && act[q]) {
+                    const uint64_t o = (uint64_t)r_out * s.D + d[q];
+                    const uint32_t jq = lam[q] / bt;
+                    if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                    if (po.feas) po.feas[o] = feas ? 1 : 0;
+                    if (po.score) po.score[o] = cost;
+                    if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                }
+                cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
+            }
+            // the group's K best: least cost bits, then least decode index,
+            // i.e. the lowest lane holding the minimum in the first column
+            // that holds it
+            const uint32_t slot = i - g0;
+#pragma unroll
+            for (int r = 0; r < K; ++r) {
+                uint32_t lm = cb[0];
+#pragma unroll
+                for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
+                const uint32_t mn = wave_min_u32_dpp(lm);
+                if (mn == 0xFFFFFFFFu) break;  // no feasible candidate left (uniform)
+                uint32_t dm = 0;
+#pragma unroll
+                for (int q = 0; q < C; ++q) {
+                    const lmask m = ballot(cb[q] == mn);
+                    if (m) {
+                        const uint32_t l = (uint32_t)__builtin_ctzll(m);
+                        dm = base + q * kWave + l;
+                        if (r + 1 < K && lane == l) cb[q] = 0xFFFFFFFFu;
+                        break;
+                    }
+                }
+                if (lane == slot * K + (uint32_t)r) {
+                    pc_bits = mn;
+                    pc_idx = dm;
+                }
+            }
+            if (nl) {
+#pragma unroll
+                for (int q = 0; q < C; ++q) laml[q] = c1.slot < kLeadOver ? stg[q] : 0u;
+            }
+            c0 = c1;
+            c1 = c2;
         }
         if (lane < (g1 - g0) * K)
             partial[((uint64_t)grp * n_req + g0) * K + lane] = ((uint64_t)pc_bits << 32) | (uint64_t)pc_idx;
@@ -833,18 +959,18 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(Snap s, Table t, const Hot
     }
 }
 
-// Merge the per-chunk keys of every sorted request into its top-k
+// Merge the per-group keys of every scoring-order request into its top-k
 // (ascending (score, index)) and write it at the request's own position;
-// invalid requests (sorted last) get index -1 and score NaN.
+// invalid requests (ordered last) get index -1 and score NaN.
 template <int K>
 __global__ __launch_bounds__(256) void reduce_kernel(uint32_t n_req, uint32_t nchunk, uint32_t k,
                                                      const uint64_t *__restrict__ partial,
-                                                     const uint32_t *__restrict__ perm,
+                                                     const Cold *__restrict__ cold,
                                                      const uint32_t *__restrict__ n_valid,
                                                      int32_t *__restrict__ out_idx, float *__restrict__ out_score) {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n_req) return;
-    const uint64_t o = (uint64_t)perm[i] * k;
+    const uint64_t o = (uint64_t)cold[i].r * k;
     if (i >= *n_valid) {
         for (uint32_t q = 0; q < k; ++q) {
             out_idx[o + q] = -1;
@@ -1478,9 +1604,15 @@ struct netkv_ctx {
     Hot *hot = nullptr;   // sorted request records, the part every scan step reads
     Cold *cold = nullptr; // and the part read by probing requests
     uint32_t *n_valid = nullptr;
-    uint32_t *hv = nullptr;                  // holder values of the blocks probing positions test
+    uint32_t *hv = nullptr;                  // holder values of the leaders' blocks
     uint64_t hv_cap = 0;
     unsigned long long *hv_used = nullptr;
+    uint64_t *seg = nullptr, *scanned = nullptr;   // segmented-scan elements, hash order
+    uint32_t *pkey = nullptr, *pkey_out = nullptr, *pval = nullptr, *pord = nullptr;   // prefill order
+    Lead *lead = nullptr;                    // leader table
+    uint32_t *lead_lam = nullptr;            // [lead_cap][D] B_tok * prefix length of each leader
+    uint32_t lead_cap = 0, lead_D = 0;
+    unsigned int *n_lead = nullptr;
     void *sort_tmp = nullptr;
     size_t sort_tmp_bytes = 0;
     uint64_t *partial = nullptr;
@@ -1647,46 +1779,81 @@ netkv_status ready(netkv_handle h) {
 }
 
 constexpr int kSpec = 4;            // blocks looked up together per extension step
-constexpr uint32_t kLcpLanes = 8;   // lanes per sorted position in lcp_kernel
+constexpr uint32_t kLcpLanes = 8;   // lanes per hash-order position in order_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
 // Radix sort configuration of the batch-order keys (rocPRIM's own choice of
 // algorithm by size).
 using SortConfig = rocprim::default_config;
 
+// Leader table capacity: prefix lengths of at most 256 MiB (u32 per decode),
+// and no more leaders than requests.  Leaders beyond it (and the requests
+// that follow them) are matched on their own by the scoring kernel.
+constexpr uint64_t kLeadBytes = 256ull << 20;
+
+uint32_t lead_capacity(uint64_t R, uint32_t D) {
+    const uint64_t c = std::min<uint64_t>(std::max<uint64_t>(R, 1), kLeadBytes / (4ull * D));
+    return (uint32_t)std::max<uint64_t>(c, 1);
+}
+
+uint32_t bits_for(uint64_t v) {   // bits to hold 0..v
+    uint32_t b = 1;
+    while (b < 64 && (v >> b)) ++b;
+    return b;
+}
+
 netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, uint64_t n_hashes,
                                   hipStream_t st) {
     if (R > h->order_cap) {
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
+        dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
         dfree(h->sort_tmp);
         h->order_cap = 0;
         h->sort_tmp_bytes = 0;
         if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
             dalloc(h->vals_in, R) != hipSuccess || dalloc(h->perm, R) != hipSuccess ||
-            dalloc(h->hot, R + kHotPad) != hipSuccess || dalloc(h->cold, R) != hipSuccess)
+            dalloc(h->hot, R + kHotPad) != hipSuccess || dalloc(h->cold, R) != hipSuccess ||
+            dalloc(h->seg, R) != hipSuccess || dalloc(h->scanned, R) != hipSuccess ||
+            dalloc(h->pkey, R) != hipSuccess || dalloc(h->pkey_out, R) != hipSuccess ||
+            dalloc(h->pval, R) != hipSuccess || dalloc(h->pord, R) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
-        size_t bytes = 0;
-        if (rocprim::radix_sort_pairs<SortConfig>(nullptr, bytes, h->keys_in, h->keys_out, h->vals_in, h->perm,
-                                                  (uint32_t)R, 0, 32, st) != hipSuccess)
-            return fail(h, NETKV_EDEVICE, "sort size query failed");
+        // one temporary buffer for the two sorts and the scan
+        size_t b1 = 0, b2 = 0, b3 = 0;
+        if (rocprim::radix_sort_pairs<SortConfig>(nullptr, b1, h->keys_in, h->keys_out, h->vals_in, h->perm,
+                                                  (uint32_t)R, 0, 32, st) != hipSuccess ||
+            rocprim::radix_sort_pairs<SortConfig>(nullptr, b2, h->pkey, h->pkey_out, h->pval, h->pord, (uint32_t)R,
+                                                  0, 32, st) != hipSuccess ||
+            rocprim::inclusive_scan(nullptr, b3, h->seg, h->scanned, (size_t)R, SegOp(), st) != hipSuccess)
+            return fail(h, NETKV_EDEVICE, "sort / scan size query failed");
+        const size_t bytes = std::max<size_t>(std::max(b1, std::max(b2, b3)), 16);
         uint8_t *tmp = nullptr;
-        if (dalloc(tmp, std::max<size_t>(bytes, 16)) != hipSuccess)
-            return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
+        if (dalloc(tmp, bytes) != hipSuccess) return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
         h->sort_tmp = tmp;
-        h->sort_tmp_bytes = std::max<size_t>(bytes, 16);
+        h->sort_tmp_bytes = bytes;
         h->order_cap = R;
     }
     if (!h->n_valid && dalloc(h->n_valid, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
     if (!h->hv_used && dalloc(h->hv_used, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
-    // holder values of probing positions: at most one per block of the batch
-    // (fewer if runs overlap in the hash array; positions that do not fit
-    // look their blocks up during the scan)
+    if (!h->n_lead && dalloc(h->n_lead, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    // holder values of the leaders' blocks: at most one per block of the
+    // batch (fewer if runs overlap in the hash array; leaders that do not
+    // fit look their blocks up in the leader kernel)
     if (n_hashes > h->hv_cap || !h->hv) {
         dfree(h->hv);
         h->hv_cap = 0;
         if (dalloc(h->hv, std::max<uint64_t>(n_hashes, 1)) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "holder value scratch allocation failed");
         h->hv_cap = std::max<uint64_t>(n_hashes, 1);
+    }
+    const uint32_t lc = lead_capacity(R, h->D);
+    if (lc > h->lead_cap || h->lead_D != h->D || !h->lead) {
+        dfree(h->lead);
+        dfree(h->lead_lam);
+        h->lead_cap = 0;
+        if (dalloc(h->lead, lc) != hipSuccess || dalloc(h->lead_lam, (uint64_t)lc * h->D) != hipSuccess)
+            return fail(h, NETKV_ENOMEM, "leader table allocation failed");
+        h->lead_cap = lc;
+        h->lead_D = h->D;
     }
     if (partial_elems > h->partial_cap) {
         dfree(h->partial);
@@ -1723,52 +1890,65 @@ inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
     return D >= 4u * kWave ? 2u : 1u;
 }
 
+// Leader kernel, then the scoring kernel: one workgroup per
+// (kWavesPerBlock runs, group) when the groups split evenly over the XCDs
+// (see score_kernel), else per kWavesPerBlock waves.
 template <int K, int C>
-void launch_scan(const Snap &sn, const Table &t, const Reqs &rq, const Order &ord, uint32_t run_len,
-                 uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po, bool pairs,
-                 hipStream_t st) {
+void launch_score(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
+                  uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po,
+                  bool pairs, hipStream_t st) {
     constexpr int W = kSpec;
-    // one workgroup per (kWavesPerBlock runs, group) when the groups split
-    // evenly over the XCDs (see scan_kernel), else per kWavesPerBlock waves
+    const uint64_t lw = std::min<uint64_t>((uint64_t)h->lead_cap * ngroup, 65536);
+    hipLaunchKernelGGL((lead_kernel<W, C>), dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
+                       dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)h->lead,
+                       (const unsigned int *)h->n_lead, h->lead_cap, ord.hv, rq.hashes, ngroup, h->lead_lam);
     const uint64_t grid64 = ngroup % kXcds == 0
                                 ? (uint64_t)((n_runs + kWavesPerBlock - 1) / kWavesPerBlock) * ngroup
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
     const uint32_t grid = (uint32_t)grid64;
+    // a request that matches on its own (its leader did not fit the leader
+    // table) looks blocks up one at a time: rare, and a short loop keeps the
+    // kernel's registers for the common path
     if (pairs)
-        hipLaunchKernelGGL((scan_kernel<K, W, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, ord.hv,
-                           rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
+        hipLaunchKernelGGL((score_kernel<K, 1, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
+                           ord.lam, h->lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
+                           po);
     else
-        hipLaunchKernelGGL((scan_kernel<K, W, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, ord.hv,
-                           rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial, po);
+        hipLaunchKernelGGL((score_kernel<K, 1, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
+                           ord.lam, h->lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
+                           po);
 }
 
-// Scan, bracketed by the handle's timing events when enabled, then merge.
+// Leader and scoring kernels, bracketed by the handle's timing events when
+// enabled, then the merge.
 template <int K>
-hipError_t launch_scan_reduce(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
-                              uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C,
-                              uint64_t *partial, const PairOut &po, bool pairs, uint32_t k, int32_t *idx,
-                              float *score, hipStream_t st) {
+hipError_t launch_score_reduce(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
+                               uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C, uint64_t *partial,
+                               const PairOut &po, bool pairs, uint32_t k, int32_t *idx, float *score,
+                               hipStream_t st) {
     hipError_t e = hipSuccess;
     if ((e = time_begin(h, st)) != hipSuccess) return e;
     if (C == 6)
-        launch_scan<K, 6>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        launch_score<K, 6>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 4)
-        launch_scan<K, 4>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        launch_score<K, 4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 3)
-        launch_scan<K, 3>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        launch_score<K, 3>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 2)
-        launch_scan<K, 2>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        launch_score<K, 2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else
-        launch_scan<K, 1>(sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        launch_score<K, 1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = time_end(h, st)) != hipSuccess) return e;
     hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
-                       (const uint64_t *)partial, ord.perm, ord.n_valid, idx, score);
+                       (const uint64_t *)partial, (const Cold *)ord.cold, ord.n_valid, idx, score);
     return hipGetLastError();
 }
 
-// The whole selection of one batch on `st`: validate + order, sort, common
-// prefixes, scan, merge.
+// The whole selection of one batch on `st`: validate and key the requests,
+// hash order (sort), common runs and leaders, the segmented scan, prefill
+// order (stable sort), scoring records, leaders' prefix lengths, scoring,
+// merge.
 netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
                         const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st) {
     const uint64_t R = req->n_req;
@@ -1784,7 +1964,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
                        h->dxlim);
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
-                       h->vals_in, h->errword, h->zflag, h->hv_used);
+                       h->vals_in, h->errword, h->zflag, h->hv_used, h->n_lead);
     if (rq.n_hashes)
         hipLaunchKernelGGL(count_zero_kernel, dim3(grid_for(rq.n_hashes, 256, 8192)), dim3(256), 0, st, rq.hashes,
                            rq.n_hashes, h->zflag);
@@ -1794,26 +1974,34 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     size_t tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                     (uint32_t)R, 0, 32, st));
+    hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
+                       h->P, (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg,
+                       h->pkey, h->pval, h->lead, h->lead_cap, h->n_lead, h->hv, h->hv_cap, h->hv_used, h->n_valid);
+    HIPCHK(h, hipGetLastError());
+    tb = h->sort_tmp_bytes;
+    HIPCHK(h, rocprim::inclusive_scan(h->sort_tmp, tb, (const uint64_t *)h->seg, h->scanned, (size_t)R, SegOp(), st));
+    tb = h->sort_tmp_bytes;
+    HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
+                                                    (uint32_t)R, 0, bits_for(h->P), st));
+    hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st, rq,
+                       sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm, (const uint32_t *)h->pord,
+                       (const uint64_t *)h->scanned, (const uint32_t *)h->n_valid, h->hot, h->cold);
+    HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
-    hipLaunchKernelGGL(lcp_kernel<kLcpLanes>, dim3((uint32_t)(((R + kHotPad) * kLcpLanes + 255) / 256)), dim3(256), 0,
-                       st, rq, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->keys_out, t, h->reuse_opt, run_len, h->hot, h->cold, h->hv, h->hv_cap,
-                       h->hv_used, h->n_valid);
-    HIPCHK(h, hipGetLastError());
-    Order ord{h->perm, h->hot, h->cold, h->hv, h->n_valid};
+    Order ord{h->hot, h->cold, h->lead_lam, h->hv, h->n_valid};
     if (K == 1)
-        HIPCHK(h, launch_scan_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
-                                        pairs, k, idx, score, st));
+        HIPCHK(h, launch_score_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+                                         score, st));
     else if (K == 2)
-        HIPCHK(h, launch_scan_reduce<2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
-                                        pairs, k, idx, score, st));
+        HIPCHK(h, launch_score_reduce<2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+                                         score, st));
     else if (K == 4)
-        HIPCHK(h, launch_scan_reduce<4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
-                                        pairs, k, idx, score, st));
+        HIPCHK(h, launch_score_reduce<4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+                                         score, st));
     else
-        HIPCHK(h, launch_scan_reduce<8>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po,
-                                        pairs, k, idx, score, st));
+        HIPCHK(h, launch_score_reduce<8>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+                                         score, st));
     return NETKV_OK;
 }
 
@@ -1872,6 +2060,8 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->bytes);
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial); dfree(h->hv); dfree(h->hv_used);
+        dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
+        dfree(h->lead); dfree(h->lead_lam); dfree(h->n_lead);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
         for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
