@@ -444,20 +444,22 @@ __global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint3
 // Per hash-order position i (G lanes, G divides 64): the common leading run
 // L with the previous position (G blocks compared per step, their loads
 // issued together), whether the position is a leader (some decode holds its
-// block L), and for a leader a slot of the leader table and the holder
-// values of its blocks from block 0 (into hv, from a shared counter).
-// Writes the segmented-scan element and the prefill sort key of i, and the
-// number of valid requests (valid keys sort first): the last valid position
-// writes it, or position 0 writes 0.  Invalid positions sort after every
-// prefill (key P).
+// block L), and for a leader a slot of the leader table and room for the
+// holder values of its blocks (in hv, from a shared counter; filled by
+// lead_holder_kernel).  Writes the segmented-scan element, the prefill sort
+// key and the scoring record of i, and the number of valid requests (valid
+// keys sort first): the last valid position writes it, or position 0 writes
+// 0.  Invalid positions sort after every prefill (key P).
 template <uint32_t G>
-__global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, const uint32_t *__restrict__ perm,
+__global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_t slp, uint32_t bt,
+                                                    const uint32_t *__restrict__ perm,
                                                     const uint32_t *__restrict__ sorted_keys, Table t,
                                                     uint32_t reuse, uint64_t *__restrict__ seg,
                                                     uint32_t *__restrict__ pkey, uint32_t *__restrict__ pval,
+                                                    Hot *__restrict__ hrec, Cold *__restrict__ crec,
                                                     Lead *__restrict__ lead, uint32_t lead_cap,
-                                                    unsigned int *__restrict__ n_lead, uint32_t *__restrict__ hv,
-                                                    uint64_t hv_cap, unsigned long long *__restrict__ hv_used,
+                                                    unsigned int *__restrict__ n_lead, uint64_t hv_cap,
+                                                    unsigned long long *__restrict__ hv_used,
                                                     uint32_t *__restrict__ n_valid) {
     const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t sub = threadIdx.x % G;
@@ -465,6 +467,7 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, const u
     const uint64_t i = tid / G;
     if (i >= (uint64_t)rq.n_req) return;
     const bool valid = sorted_keys[i] < kKeyInvalid;
+    const uint32_t r = perm[i];
     if (sub == 0) {
         if (valid && (i + 1 == rq.n_req || sorted_keys[i + 1] >= kKeyInvalid)) *n_valid = (uint32_t)(i + 1);
         if (i == 0 && !valid) *n_valid = 0;
@@ -474,10 +477,11 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, const u
         if (sub == 0) {
             seg[i] = seg_elem(kNoLead, 0);
             pkey[i] = P;
+            hrec[i] = Hot{0, kNoLead, 0, 0};
+            crec[i] = Cold{0, r, 0};
         }
         return;
     }
-    const uint32_t r = perm[i];
     const uint64_t a = rq.off[r];
     const uint64_t nr = rq.off[r + 1] - a;
     uint64_t l = 0;
@@ -498,96 +502,87 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, const u
             }
         }
     }
+    if (sub != 0) return;
     // a leader if some decode holds block L
-    uint32_t vl = kNoHolder;
-    if (sub == 0 && l < nr) vl = holder_lane(t, rq.hashes[a + l]);
-    vl = __shfl(vl, (int)seg0, kWave);
+    const uint32_t vl = l < nr ? holder_lane(t, rq.hashes[a + l]) : kNoHolder;
     uint64_t e = seg_elem(kNoLead, (uint32_t)l);
     if (vl != kNoHolder) {
-        unsigned int slot = 0;
-        if (sub == 0) slot = atomicAdd(n_lead, 1u);
-        slot = __shfl(slot, (int)seg0, kWave);
+        const unsigned int slot = atomicAdd(n_lead, 1u);
         if (slot >= lead_cap) {
             e = seg_elem(kLeadOver, kNoCap);
         } else {
             e = seg_elem(slot, kNoCap);
-            // holder values of blocks 0, 1, ... up to the first block no decode holds
-            unsigned long long o = 0;
-            if (sub == 0) o = atomicAdd(hv_used, (unsigned long long)nr);
-            const uint64_t hoff = __shfl(o, (int)seg0, kWave);
-            uint32_t m = kNoPre;
-            if (hoff + nr <= hv_cap) {
-                m = (uint32_t)nr;
-                for (uint64_t k0 = 0; k0 < nr; k0 += G) {
-                    const uint64_t k = k0 + sub;
-                    uint32_t hk = kNoHolder;
-                    if (k < nr) {
-                        hk = k == l ? vl : holder_lane(t, rq.hashes[a + k]);
-                        hv[hoff + k] = hk;
-                    }
-                    const uint32_t none = (uint32_t)(__ballot(k < nr && hk == kNoHolder) >> seg0) &
-                                          (uint32_t)((1ull << G) - 1);
-                    if (none) {
-                        m = (uint32_t)(k0 + (uint64_t)__builtin_ctz(none));
-                        break;
-                    }
-                }
-            }
-            if (sub == 0) {
-                Lead ld;
-                ld.a = a;
-                ld.hoff = hoff;
-                ld.n = (uint32_t)nr;
-                ld.m = m;
-                ld.pad[0] = ld.pad[1] = 0;
-                lead[slot] = ld;
-            }
+            const unsigned long long o = atomicAdd(hv_used, (unsigned long long)nr);
+            Lead ld;
+            ld.a = a;
+            ld.hoff = o;
+            ld.n = (uint32_t)nr;
+            ld.m = o + nr <= hv_cap ? 0u : kNoPre;   // filled by lead_holder_kernel
+            ld.pad[0] = ld.pad[1] = 0;
+            lead[slot] = ld;
         }
     }
-    if (sub == 0) {
-        seg[i] = e;
-        pkey[i] = rq.prefill[r];
+    seg[i] = e;
+    pkey[i] = rq.prefill[r];
+    hrec[i] = Hot{rq.prefill[r] * slp * (uint32_t)sizeof(float2),   // < 2^32 (checked at load)
+                  0, rq.len[r], 0};
+    crec[i] = Cold{a, r, (uint32_t)nr};
+}
+
+// Holder values of every leader's blocks from block 0 up to the first
+// block no decode holds: one wavefront per leader (looping over leaders,
+// whose count is read from device memory), lanes over blocks.
+__global__ __launch_bounds__(kBlock) void lead_holder_kernel(Table t, const uint64_t *__restrict__ hashes,
+                                                             Lead *__restrict__ lead,
+                                                             const unsigned int *__restrict__ n_lead,
+                                                             uint32_t lead_cap, uint32_t *__restrict__ hv) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t nl_all = *n_lead;
+    const uint32_t nl = nl_all < lead_cap ? nl_all : lead_cap;
+    const uint32_t nw = gridDim.x * kWavesPerBlock;
+    for (uint32_t slot = blockIdx.x * kWavesPerBlock + wave_index(); slot < nl; slot += nw) {
+        const Lead ld = lead[slot];
+        if (ld.m == kNoPre) continue;   // no room: the leader kernel looks its blocks up
+        uint32_t m = ld.n;
+        for (uint32_t k0 = 0; k0 < ld.n; k0 += kWave) {
+            const uint32_t k = k0 + lane;
+            uint32_t hk = kNoHolder;
+            if (k < ld.n) {
+                hk = holder_lane(t, hashes[ld.a + k]);
+                hv[ld.hoff + k] = hk;
+            }
+            const uint64_t none = __ballot(k < ld.n && hk == kNoHolder);
+            if (none) {
+                m = k0 + (uint32_t)__builtin_ctzll(none);
+                break;
+            }
+        }
+        if (lane == 0) lead[slot].m = m;
     }
 }
 
 // Scoring-order records: position k of the prefill order holds hash-order
-// position pord[k]; its leader slot and L* come from the scan.  Positions
-// past the batch (kHotPad of them) get a record that the scan may read
-// ahead but never scores (row 0, no leader).
-__global__ __launch_bounds__(256) void assemble_kernel(Reqs rq, uint32_t slp, uint32_t bt,
-                                                       const uint32_t *__restrict__ perm,
-                                                       const uint32_t *__restrict__ pord,
+// position pord[k], whose record takes its leader slot and B_tok * L* from
+// the scan.  Positions past the batch (kHotPad of them) get a record that
+// the scan may read ahead but never scores (row 0, no leader).
+__global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t bt, const uint32_t *__restrict__ pord,
                                                        const uint64_t *__restrict__ scanned,
-                                                       const uint32_t *__restrict__ n_valid,
+                                                       const Hot *__restrict__ hrec, const Cold *__restrict__ crec,
                                                        Hot *__restrict__ hot, Cold *__restrict__ cold) {
     const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= (uint64_t)rq.n_req + kHotPad) return;
-    if (k >= rq.n_req) {
+    if (k >= (uint64_t)n_req + kHotPad) return;
+    if (k >= n_req) {
         hot[k] = Hot{0, kNoLead, 0, 0};
         return;
     }
     const uint32_t i = pord[k];
-    const uint32_t r = perm[i];
-    Cold c;
-    c.r = r;
-    c.a = 0;
-    c.n = 0;
-    if (k >= *n_valid) {
-        hot[k] = Hot{0, kNoLead, 0, 0};
-        cold[k] = c;
-        return;
-    }
+    Hot o = hrec[i];
     const uint64_t e = scanned[i];
-    const uint32_t slot = (uint32_t)(e >> 32), ls = (uint32_t)e;
-    c.a = rq.off[r];
-    c.n = (uint32_t)(rq.off[r + 1] - c.a);
-    Hot o;
-    o.row = rq.prefill[r] * slp * (uint32_t)sizeof(float2);   // < 2^32 (checked at load)
-    o.slot = slot;
-    o.len = rq.len[r];
+    const uint32_t ls = (uint32_t)e;
+    o.slot = (uint32_t)(e >> 32);
     o.lams = ls == kNoCap ? kNoCap : bt * ls;   // ls <= n_r, so bt * ls <= len
     hot[k] = o;
-    cold[k] = c;
+    cold[k] = crec[i];
 }
 
 // Read-only data that is uniform across a wavefront (request records, hash
@@ -699,78 +694,80 @@ __device__ inline void probe_from(const Table &t, uint32_t base, cptr<uint64_t> 
     }
 }
 
-// The same scan over holder values looked up beforehand: hv[0..m) are the
-// holders of consecutive blocks from the first tested one, and the block
-// after them (if any) is held by no decode, so every lane still alive there
-// stops.  W values are read per step, then their bitmap words.
-template <int W, int C>
-__device__ inline void probe_pre(const Table &t, uint32_t base, cptr<uint32_t> hv, uint32_t m, lmask (&alive)[C],
-                                 uint32_t (&lam)[C], uint32_t bt) {
-    lmask mk[C];
-    for (uint32_t k0 = 0; k0 < m; k0 += W) {
-        lmask any = 0;
-#pragma unroll
-        for (int q = 0; q < C; ++q) any |= alive[q];
-        if (!any) break;
-        uint32_t v[W];
-#pragma unroll
-        for (int w = 0; w < W; ++w) v[w] = k0 + w < m ? hv[k0 + w] : kNoHolder;
-#pragma unroll
-        for (int w = 0; w < W; ++w) {
-            if (k0 + w >= m) break;
-            holder_masks<C>(t, v[w], base, mk);
-#pragma unroll
-            for (int q = 0; q < C; ++q) {
-                alive[q] &= mk[q];
-                lam[q] += in_mask(alive[q]) ? bt : 0u;
-            }
-        }
-    }
+// Prefix lengths of every leader on every decode: one wavefront per
+// (leader, group of 64 decodes), looping over such tasks (the leader count
+// is read from device memory, so every wavefront ends after at most
+// ceil(tasks / wavefronts) of them).  A task takes the leader's blocks 64 at
+// a time, lane k block k: its holder value (looked up by lead_holder_kernel,
+// or here when there was no room), then the word of its bitmap row over
+// the task's 64 decodes (or the one-hot word of a single holder).  An
+// inclusive AND across lanes, seeded with the decodes still matching, gives
+// in lane k the decodes that hold every block up to k; it only loses bits as
+// k grows, so decode l matches exactly the blocks below the first lane whose
+// word lacks bit l, found by binary search over the words in LDS.  Writes
+// B_tok * j for the task's decodes.
+__device__ inline uint64_t shfl_up_u64(uint64_t v, uint32_t delta) {
+    const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, delta, kWave);
+    const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), delta, kWave);
+    return ((uint64_t)hi << 32) | lo;
 }
 
-// Prefix lengths of every leader on every decode: one wavefront per
-// (leader, group of 64*C decodes) runs the first-miss scan from block 0 over
-// the holder values the order kernel looked up (or over the hash run when
-// they did not fit) and writes B_tok * j for its decodes.  The wavefronts
-// loop over the (leader, group) tasks; the leader count is read from device
-// memory, so every wavefront ends after at most ceil(tasks / wavefronts)
-// tasks.
-template <int W, int C>
 __global__ __launch_bounds__(kBlock) void lead_kernel(Table t, uint32_t D, uint32_t bt, const Lead *__restrict__ lead,
                                                       const unsigned int *__restrict__ n_lead, uint32_t lead_cap,
                                                       const uint32_t *__restrict__ hv,
                                                       const uint64_t *__restrict__ hashes, uint32_t ngroup,
                                                       uint32_t *__restrict__ lam_out) {
+    __shared__ uint64_t pw[kWavesPerBlock][kWave];
     const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t wv = wave_index();
     const uint32_t nl_all = *n_lead;
     const uint32_t nl = nl_all < lead_cap ? nl_all : lead_cap;
     const uint64_t tasks = (uint64_t)nl * ngroup;
     const uint64_t nw = (uint64_t)gridDim.x * kWavesPerBlock;
-    const cptr<uint64_t> chash = as_const(hashes);
-    const cptr<uint32_t> chv = as_const(hv);
-    for (uint64_t task = (uint64_t)blockIdx.x * kWavesPerBlock + wave_index(); task < tasks; task += nw) {
+    for (uint64_t task = (uint64_t)blockIdx.x * kWavesPerBlock + wv; task < tasks; task += nw) {
         const uint32_t slot = (uint32_t)(task / ngroup), g = (uint32_t)(task % ngroup);
-        const uint32_t base = g * (kWave * C);
+        const uint32_t base = g * kWave;
         const cptr<uint32_t> w = as_const((const uint32_t *)(lead + slot));
         const uint64_t a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
         const uint64_t hoff = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
         const uint32_t n = w[4], m = w[5];
-        uint32_t lam[C];
-        lmask alive[C];
+        const bool pre = m != kNoPre;
+        const uint32_t nb = pre ? m : n;   // blocks to take (held by someone before block m)
+        uint64_t alive = ~0ull;            // decodes (lanes) holding every block so far
+        uint32_t j = 0;                    // this lane's decode: leading blocks held
+        for (uint32_t k0 = 0; k0 < nb && alive; k0 += kWave) {
+            const uint32_t k = k0 + lane;
+            const uint32_t nk = nb - k0 < (uint32_t)kWave ? nb - k0 : (uint32_t)kWave;
+            uint32_t v = kNoHolder;
+            if (k < nb) v = pre ? hv[hoff + k] : holder_lane(t, hashes[a + k]);
+            uint64_t word = 0;
+            if (v < kHeldOne) {
+                word = t.bits[(uint64_t)v * t.bpitch + g];
+            } else if (v != kNoHolder) {
+                const uint32_t o = (v & ~kHeldOne) - base;
+                word = o < (uint32_t)kWave ? 1ull << o : 0ull;
+            }
+            uint64_t pref = word & alive;
 #pragma unroll
-        for (int q = 0; q < C; ++q) {
-            lam[q] = 0;
-            alive[q] = ~0ull;
+            for (uint32_t off = 1; off < (uint32_t)kWave; off <<= 1) {
+                const uint64_t up = shfl_up_u64(pref, off);
+                if (lane >= off) pref &= up;
+            }
+            pw[wv][lane] = pref;
+            __builtin_amdgcn_wave_barrier();
+            // lane l: the number of leading words (of nk) holding bit l
+            uint32_t lo = 0, hi = nk;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi) / 2;
+                if ((pw[wv][mid] >> lane) & 1ull) lo = mid + 1;
+                else hi = mid;
+            }
+            j += lo;
+            alive = pw[wv][nk - 1];
+            __builtin_amdgcn_wave_barrier();
         }
-        if (m != kNoPre)
-            probe_pre<W, C>(t, base, chv + hoff, m, alive, lam, bt);
-        else if (n)
-            probe_from<W, C>(t, base, chash + a, n, 0, alive, lam, bt, holder_uniform(t, chash[a]));
-#pragma unroll
-        for (int q = 0; q < C; ++q) {
-            const uint32_t d = base + q * kWave + lane;
-            if (d < D) lam_out[(uint64_t)slot * D + d] = lam[q];
-        }
+        const uint32_t d = base + lane;
+        if (d < D) lam_out[(uint64_t)slot * D + d] = bt * j;
     }
 }
 
@@ -1608,6 +1605,8 @@ struct netkv_ctx {
     uint64_t hv_cap = 0;
     unsigned long long *hv_used = nullptr;
     uint64_t *seg = nullptr, *scanned = nullptr;   // segmented-scan elements, hash order
+    Hot *hrec = nullptr;                     // scoring records by hash-order position
+    Cold *crec = nullptr;
     uint32_t *pkey = nullptr, *pkey_out = nullptr, *pval = nullptr, *pord = nullptr;   // prefill order
     Lead *lead = nullptr;                    // leader table
     uint32_t *lead_lam = nullptr;            // [lead_cap][D] B_tok * prefix length of each leader
@@ -1778,7 +1777,6 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-constexpr int kSpec = 4;            // blocks looked up together per extension step
 constexpr uint32_t kLcpLanes = 8;   // lanes per hash-order position in order_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
@@ -1807,6 +1805,7 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
     if (R > h->order_cap) {
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
+        dfree(h->hrec); dfree(h->crec);
         dfree(h->sort_tmp);
         h->order_cap = 0;
         h->sort_tmp_bytes = 0;
@@ -1815,7 +1814,8 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
             dalloc(h->hot, R + kHotPad) != hipSuccess || dalloc(h->cold, R) != hipSuccess ||
             dalloc(h->seg, R) != hipSuccess || dalloc(h->scanned, R) != hipSuccess ||
             dalloc(h->pkey, R) != hipSuccess || dalloc(h->pkey_out, R) != hipSuccess ||
-            dalloc(h->pval, R) != hipSuccess || dalloc(h->pord, R) != hipSuccess)
+            dalloc(h->pval, R) != hipSuccess || dalloc(h->pord, R) != hipSuccess ||
+            dalloc(h->hrec, R) != hipSuccess || dalloc(h->crec, R) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
         // one temporary buffer for the two sorts and the scan
         size_t b1 = 0, b2 = 0, b3 = 0;
@@ -1897,11 +1897,12 @@ template <int K, int C>
 void launch_score(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
                   uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po,
                   bool pairs, hipStream_t st) {
-    constexpr int W = kSpec;
-    const uint64_t lw = std::min<uint64_t>((uint64_t)h->lead_cap * ngroup, 65536);
-    hipLaunchKernelGGL((lead_kernel<W, C>), dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
+    // leaders: 64 decodes per wavefront, 64 blocks per step
+    const uint32_t lgroup = (sn.D + kWave - 1) / kWave;
+    const uint64_t lw = std::min<uint64_t>((uint64_t)h->lead_cap * lgroup, 65536);
+    hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
                        dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)h->lead,
-                       (const unsigned int *)h->n_lead, h->lead_cap, ord.hv, rq.hashes, ngroup, h->lead_lam);
+                       (const unsigned int *)h->n_lead, h->lead_cap, ord.hv, rq.hashes, lgroup, h->lead_lam);
     const uint64_t grid64 = ngroup % kXcds == 0
                                 ? (uint64_t)((n_runs + kWavesPerBlock - 1) / kWavesPerBlock) * ngroup
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
@@ -1975,17 +1976,22 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                     (uint32_t)R, 0, 32, st));
     hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
-                       h->P, (const uint32_t *)h->perm, (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg,
-                       h->pkey, h->pval, h->lead, h->lead_cap, h->n_lead, h->hv, h->hv_cap, h->hv_used, h->n_valid);
+                       h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
+                       (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg, h->pkey, h->pval, h->hrec, h->crec,
+                       h->lead, h->lead_cap, h->n_lead, h->hv_cap, h->hv_used, h->n_valid);
+    hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((h->lead_cap + kWavesPerBlock - 1) /
+                                                                             kWavesPerBlock, 4096)),
+                       dim3(kBlock), 0, st, t, rq.hashes, h->lead, (const unsigned int *)h->n_lead, h->lead_cap,
+                       h->hv);
     HIPCHK(h, hipGetLastError());
     tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::inclusive_scan(h->sort_tmp, tb, (const uint64_t *)h->seg, h->scanned, (size_t)R, SegOp(), st));
     tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
                                                     (uint32_t)R, 0, bits_for(h->P), st));
-    hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st, rq,
-                       sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm, (const uint32_t *)h->pord,
-                       (const uint64_t *)h->scanned, (const uint32_t *)h->n_valid, h->hot, h->cold);
+    hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st, (uint32_t)R,
+                       h->block_tokens, (const uint32_t *)h->pord, (const uint64_t *)h->scanned,
+                       (const Hot *)h->hrec, (const Cold *)h->crec, h->hot, h->cold);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
@@ -2061,7 +2067,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial); dfree(h->hv); dfree(h->hv_used);
         dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
-        dfree(h->lead); dfree(h->lead_lam); dfree(h->n_lead);
+        dfree(h->lead); dfree(h->lead_lam); dfree(h->n_lead); dfree(h->hrec); dfree(h->crec);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
         for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
