@@ -220,9 +220,10 @@ netkv_status netkv_state_get(netkv_handle h, uint16_t *n_inflight, uint32_t *que
 netkv_status netkv_sync_errors(netkv_handle h, void *stream);
 
 /* Kernel timing: when enabled, the library records HIP events on `stream`
- * around the one scoring kernel of each call -- the fused match / score /
- * per-group top-k scan of netkv_select_batch (not the ordering or merge
- * kernels), the sweep kernel of netkv_rank_sweep, the per-prefill kernel of
+ * around the one scoring kernel of each call -- the kernel of
+ * netkv_select_batch that scores every pair and keeps each decode group's
+ * top-k (not the ordering, prefix-length or merge kernels), the sweep
+ * kernel of netkv_rank_sweep, the per-prefill kernel of
  * netkv_select_sequential -- without synchronising.  netkv_kernel_ms waits
  * for the last of them and returns the mean milliseconds over the launches
  * timed since timing was last enabled (the latest 256 when there were more);

@@ -1894,15 +1894,17 @@ inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
 // (kWavesPerBlock runs, group) when the groups split evenly over the XCDs
 // (see score_kernel), else per kWavesPerBlock waves.
 template <int K, int C>
-void launch_score(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
-                  uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po,
-                  bool pairs, hipStream_t st) {
+hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
+                        uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po,
+                        bool pairs, hipStream_t st) {
     // leaders: 64 decodes per wavefront, 64 blocks per step
     const uint32_t lgroup = (sn.D + kWave - 1) / kWave;
     const uint64_t lw = std::min<uint64_t>((uint64_t)h->lead_cap * lgroup, 65536);
     hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
                        dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)h->lead,
                        (const unsigned int *)h->n_lead, h->lead_cap, ord.hv, rq.hashes, lgroup, h->lead_lam);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || (e = time_begin(h, st)) != hipSuccess) return e;
     const uint64_t grid64 = ngroup % kXcds == 0
                                 ? (uint64_t)((n_runs + kWavesPerBlock - 1) / kWavesPerBlock) * ngroup
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
@@ -1918,29 +1920,29 @@ void launch_score(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq
         hipLaunchKernelGGL((score_kernel<K, 1, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
                            ord.lam, h->lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
                            po);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return time_end(h, st);
 }
 
-// Leader and scoring kernels, bracketed by the handle's timing events when
-// enabled, then the merge.
+// Leader kernel, the scoring kernel (bracketed by the handle's timing events
+// when enabled), then the merge.
 template <int K>
 hipError_t launch_score_reduce(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
                                uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C, uint64_t *partial,
                                const PairOut &po, bool pairs, uint32_t k, int32_t *idx, float *score,
                                hipStream_t st) {
     hipError_t e = hipSuccess;
-    if ((e = time_begin(h, st)) != hipSuccess) return e;
     if (C == 6)
-        launch_score<K, 6>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 6>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 4)
-        launch_score<K, 4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 3)
-        launch_score<K, 3>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 3>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else if (C == 2)
-        launch_score<K, 2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
     else
-        launch_score<K, 1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = time_end(h, st)) != hipSuccess) return e;
+        e = launch_score<K, 1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
                        (const uint64_t *)partial, (const Cold *)ord.cold, ord.n_valid, idx, score);
     return hipGetLastError();
