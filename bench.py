@@ -1,15 +1,15 @@
 """Benchmark: batched NetKV decode-instance selection on one MI355X.
 
 One step = one netkv_select_batch call over the whole batch: for every
-(request, decode) pair the first-miss prefix match against the decode's
-resident-set table, the non-cached bytes, feasibility, the Eq. (5) cost,
+(request, decode) pair the prefix length (leading blocks resident on the
+decode, Sec. III-B), the non-cached bytes, feasibility, the Eq. (5) cost,
 and the per-request argmin (k = 1).  Inputs are resident in device memory
 before timing starts.
 
 Default workload: 4,096-GPU fat-tree (512 nodes, 64 leaves, 8 pods), 1,024
 prefill and 3,072 decode instances, 1,048,576 requests in one snapshot
-(3.2e9 scored pairs), 65,536 resident block hashes per decode in tables at
-load factor 0.5.
+(3.2e9 scored pairs), 65,536 resident block hashes per decode in one holder
+index at load factor 0.5.
 
 Prints one JSON line: scored pairs/s (value), selections/s, per-launch time
 of the scoring kernel from HIP events on the launch stream, that kernel's
@@ -60,7 +60,7 @@ def kernel_source_digest() -> str:
 
 
 def counter_summary(workload: str, digest: str):
-    """Per-launch rocprofv3 counter figures of the scan kernel (HBM bytes,
+    """Per-launch rocprofv3 counter figures of the scoring kernel (HBM bytes,
     instruction counts) from the committed summary, if they were taken on
     this exact kernel source; else an empty dict."""
     path = os.path.join(ROOT, "profiles", f"score_kernel_{workload}_counters.json")
@@ -83,9 +83,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-reuse", action="store_true",
-                    help="scan every pair from block 0 (no first-miss carry along the batch order)")
+                    help="no prefix sharing along the batch order: every request whose block 0 "
+                         "is resident somewhere is matched from block 0")
     ap.add_argument("--run-len", type=int, default=0, help="requests per wavefront run (0 = auto)")
-    ap.add_argument("--cols", type=int, default=0, help="decodes per lane (0 = auto, 1, 2, 4)")
+    ap.add_argument("--cols", type=int, default=0, help="decodes per lane (0 = auto, 1, 2, 3, 4, 6)")
     ap.add_argument("--policy", type=int, default=0,
                     help="cost rung: 0 full, 1 without live congestion, 2 topology only")
     ap.add_argument("--sequential", action="store_true",
@@ -163,7 +164,7 @@ def main():
 
     # Events on the launch stream (torch's current stream, which the library
     # launches on): the whole step, and the library's own pair around the
-    # scan kernel (match + score + per-group top-k) of the same launch.
+    # scoring kernel (prefix lengths + score + per-group top-k) of the same launch.
     stream = torch.cuda.current_stream(dev)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
@@ -284,7 +285,7 @@ def main():
             "requests": R, "decodes": D, "prefills": P, "gpus_modelled": cfg.cluster.n_gpus,
             "resident_hashes_per_decode": cfg.cache_per_decode, "index": ci,
             "block_tokens": cfg.block_tokens, "mean_blocks_per_request": float(nblk.mean()),
-            "k": k, "parallelism": "single-gpu", "first_miss_carry": not args.no_reuse,
+            "k": k, "parallelism": "single-gpu", "prefix_sharing": not args.no_reuse,
             "run_len": args.run_len or "auto", "policy": args.policy,
             "selection": "sequential (in-batch in-flight increments)" if args.sequential else "snapshot",
         },

@@ -235,24 +235,38 @@ netkv_status netkv_kernel_ms(netkv_handle h, float *ms);
 /* Tuning options (results never depend on them):
  *   NETKV_OPT_RUN_LEN -- requests per wavefront run in the batch order
  *                        (0 = automatic, else 1..2^20);
- *   NETKV_OPT_REUSE   -- 1 (default): a request's first-miss index on a
- *                        decode is taken from the preceding request of the
- *                        batch order when it lies inside their common
- *                        leading blocks (an exact identity, no probe);
- *                        0: nothing is carried, every pair is scanned
- *                        from block 0;
- *   NETKV_OPT_COLS    -- decodes per lane of a scanning wavefront: 0 =
+ *   NETKV_OPT_REUSE   -- 1 (default): prefix lengths are shared along an
+ *                        order of the batch that makes requests with equal
+ *                        leading blocks neighbours.  Only a "leader" -- a
+ *                        request whose first block past the run it shares
+ *                        with its predecessor is resident on some decode --
+ *                        is matched from block 0; any other request takes,
+ *                        on every decode, the smaller of its last leader's
+ *                        prefix length and the shortest common run since
+ *                        that leader (an exact identity);
+ *                        0: common runs are taken as empty, so every
+ *                        request whose block 0 is resident somewhere is
+ *                        matched from block 0;
+ *   NETKV_OPT_COLS    -- decodes per lane of a scoring wavefront: 0 =
  *                        automatic (the widest of 6, 3, 2 whose groups of
  *                        64 per lane-column split evenly over the 8 XCDs,
  *                        else 2 on pools of 256+ decodes, else 1), 1, 2,
- *                        3, 4, 6.
+ *                        3, 4, 6;
+ *   NETKV_OPT_LEAD_CAP -- 0 (default): the leader table is sized by memory
+ *                        (prefix lengths of at most 256 MiB); else at most
+ *                        `value` leaders, and holder values of at most
+ *                        `value` of their blocks, are kept per call.  A
+ *                        request whose leader is not kept is matched from
+ *                        block 0 on its own, and a leader whose blocks'
+ *                        holder values are not kept looks them up itself.
  * and one option that does change results, selecting the rung of the
  * method's ablation (Sec. VI, Experiment 6) the costs use:
  *   NETKV_OPT_POLICY  -- 0 (default): the full cost; 1: static tier map and
  *                        self-contention counter, live congestion taken as 0;
  *                        2: static tier map only (congestion and in-flight
  *                        counters taken as 0). */
-enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3, NETKV_OPT_POLICY = 4 };
+enum { NETKV_OPT_RUN_LEN = 1, NETKV_OPT_REUSE = 2, NETKV_OPT_COLS = 3, NETKV_OPT_POLICY = 4,
+       NETKV_OPT_LEAD_CAP = 5 };
 netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 
 /* Geometry of the loaded cache's holder index (any pointer may be NULL):

@@ -6,32 +6,42 @@
 // of requests against one telemetry snapshot.
 //
 // Data layout in device memory (all owned by the handle):
-//   * resident-set tables: one bucketized cuckoo table per decode (two
-//     candidate buckets per hash, two 8-byte slots per bucket), all with the
-//     same power-of-two bucket count and the same bucket functions, stored
-//     bucket-major: table[(bucket * pitch + d) * 2 + slot] (pitch = D rounded
-//     up to 16).  A membership test is exactly two independent 16-byte loads
-//     (no data-dependent continuation), and a wavefront testing one hash on
-//     64 consecutive decodes reads two contiguous 1 KiB row segments.
-//     Empty slots hold 0 (hash value 0 is reserved).
+//   * holder index of the resident block hashes of all decodes: every
+//     distinct resident hash once in a two-choice bucketized cuckoo set
+//     (two 8-byte slots per bucket, 0 = empty; hash value 0 is reserved),
+//     with a 32-bit holder value per slot -- one decode, or a row of a
+//     holder bitmap pool (one bit per decode).  One lookup answers a
+//     membership test for every decode at once.
 //   * snapshot: tier_map u8[P*D], util f32[P*D] (row-major by prefill),
 //     n_inflight u16[4*P] (tier-major), free_mem u64[D], queue u32[D],
-//     batch u32[D], plus the admitted bytes of the previous batch u64[D].
+//     batch u32[D], plus the admitted bytes of the previous batch u64[D];
+//     derived per call: (seconds per token, constant part) float2 rows per
+//     prefill, and per decode the load term and feasibility limit.
 //
-// Kernels:
-//   prep / sort / lcp -- validate requests, order the batch so requests with
-//                     equal leading blocks are neighbours (rocPRIM radix
-//                     sort), and measure each one's common leading run with
-//                     its predecessor.
-//   scan_kernel    -- prefix match (Sec. III-B) + Eqs. (2)-(7) + feasibility
-//                     + per-chunk top-k, fused; one wavefront per (run of
-//                     sorted requests, 64 decodes); optional per-pair outputs.
-//   reduce_kernel  -- merges the per-chunk keys into each request's top-k.
-//   sweep_kernel   -- re-scoring under congestion scenarios with the prefix
-//                     lengths reused; lanes over requests.
-//   insert_kernel  -- builds the tables (cuckoo insertion with 64-bit CAS and
-//                     atomic exchange).
-//   commit kernels -- between-batch counter / queue / memory update.
+// Kernels of one selection (netkv_select_batch), in launch order:
+//   derive_kernel      -- per-call cost factors (Eqs. (3)-(7) split by what
+//                         they depend on).
+//   prep / count_zero / zero_fix -- validate requests, build hash-order keys.
+//   (rocPRIM radix sort into hash order)
+//   order_kernel       -- common leading run with the previous position,
+//                         leaders (positions whose next block some decode
+//                         holds), segmented-scan elements, records.
+//   lead_holder_kernel -- holder values of every leader's blocks.
+//   (rocPRIM segmented scan; stable radix sort into prefill order)
+//   assemble_kernel    -- scoring records in prefill order.
+//   lead_kernel        -- prefix lengths of every leader on every decode.
+//   score_kernel       -- per pair: prefix length min(leader's, L*),
+//                         feasibility and cost (Eqs. (2)-(7)), then the
+//                         group's top-k; one wavefront per (run of requests,
+//                         group of 64*C decodes); optional per-pair outputs.
+//   reduce_kernel      -- merges the groups' keys into each request's top-k.
+// Other calls:
+//   sweep_kernel       -- re-scoring under congestion scenarios with the
+//                         prefix lengths reused; lanes over requests.
+//   sequential kernels -- Algorithm 1's per-request in-flight increments,
+//                         one workgroup per prefill instance.
+//   owner / classify / index_insert / index_value -- build the holder index.
+//   commit kernels     -- between-batch counter / queue / memory update.
 #include <hip/hip_runtime.h>
 #include <rocprim/device/device_radix_sort.hpp>
 #include <rocprim/device/device_scan.hpp>
@@ -371,6 +381,7 @@ struct Order {
     const uint32_t *lam;      // [leaders][D] B_tok * prefix length of each leader on each decode
     const uint32_t *hv;       // holder values of the leaders' blocks
     const uint32_t *n_valid;  // valid requests (they sort first)
+    uint32_t lead_cap;        // leaders the table takes in this call
 };
 
 // Validate each request and build its sort key, one thread per request.
@@ -1618,7 +1629,8 @@ struct netkv_ctx {
     uint64_t partial_cap = 0;
     // options
     uint32_t run_len_opt = 0;   // 0 = automatic
-    uint32_t reuse_opt = 1;     // carry first-miss indices along sorted runs
+    uint32_t reuse_opt = 1;     // share prefix lengths along the hash order
+    uint32_t lead_cap_opt = 0;  // leader table limit (0 = by memory)
     uint32_t cols_opt = 0;      // decodes per lane (0 = automatic)
     uint32_t policy_opt = 0;    // 0 full, 1 without live congestion, 2 topology only
     // sequential-selection scratch
@@ -1780,9 +1792,15 @@ netkv_status ready(netkv_handle h) {
 constexpr uint32_t kLcpLanes = 8;   // lanes per hash-order position in order_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
-// Radix sort configuration of the batch-order keys (rocPRIM's own choice of
-// algorithm by size).
-using SortConfig = rocprim::default_config;
+// Radix sort configuration of the batch-order keys: rocPRIM's tuned kernels,
+// with its merge-sort path limited to batches of at most 2^16 requests
+// (rocPRIM's own limit is 2^20).  Above the limit the onesweep radix sort
+// takes one pass per 8 key bits, so the prefill order (11 bits for 1,024
+// prefills) takes two; measured on MI355X at 2^20 requests, 91 us against
+// 150 us for the block sort and twenty merge passes, while the 32-bit hash
+// order takes about 165 us either way.
+using SortConfig = rocprim::radix_sort_config<rocprim::default_config, rocprim::default_config,
+                                              rocprim::default_config, (size_t)1 << 16>;
 
 // Leader table capacity: prefix lengths of at most 256 MiB (u32 per decode),
 // and no more leaders than requests.  Leaders beyond it (and the requests
@@ -1899,10 +1917,10 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
                         bool pairs, hipStream_t st) {
     // leaders: 64 decodes per wavefront, 64 blocks per step
     const uint32_t lgroup = (sn.D + kWave - 1) / kWave;
-    const uint64_t lw = std::min<uint64_t>((uint64_t)h->lead_cap * lgroup, 65536);
+    const uint64_t lw = std::min<uint64_t>((uint64_t)ord.lead_cap * lgroup, 65536);
     hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
                        dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)h->lead,
-                       (const unsigned int *)h->n_lead, h->lead_cap, ord.hv, rq.hashes, lgroup, h->lead_lam);
+                       (const unsigned int *)h->n_lead, ord.lead_cap, ord.hv, rq.hashes, lgroup, h->lead_lam);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || (e = time_begin(h, st)) != hipSuccess) return e;
     const uint64_t grid64 = ngroup % kXcds == 0
@@ -1914,11 +1932,11 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
     // kernel's registers for the common path
     if (pairs)
         hipLaunchKernelGGL((score_kernel<K, 1, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, h->lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
+                           ord.lam, ord.lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
                            po);
     else
         hipLaunchKernelGGL((score_kernel<K, 1, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, h->lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
+                           ord.lam, ord.lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
                            po);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return time_end(h, st);
@@ -1977,14 +1995,16 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     size_t tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                     (uint32_t)R, 0, 32, st));
+    // leaders (and holder values of their blocks) the table takes this call
+    const uint32_t lcap = h->lead_cap_opt ? std::min(h->lead_cap, h->lead_cap_opt) : h->lead_cap;
+    const uint64_t hvcap = h->lead_cap_opt ? std::min<uint64_t>(h->hv_cap, h->lead_cap_opt) : h->hv_cap;
     hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
                        h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
                        (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg, h->pkey, h->pval, h->hrec, h->crec,
-                       h->lead, h->lead_cap, h->n_lead, h->hv_cap, h->hv_used, h->n_valid);
-    hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((h->lead_cap + kWavesPerBlock - 1) /
+                       h->lead, lcap, h->n_lead, hvcap, h->hv_used, h->n_valid);
+    hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((lcap + kWavesPerBlock - 1) /
                                                                              kWavesPerBlock, 4096)),
-                       dim3(kBlock), 0, st, t, rq.hashes, h->lead, (const unsigned int *)h->n_lead, h->lead_cap,
-                       h->hv);
+                       dim3(kBlock), 0, st, t, rq.hashes, h->lead, (const unsigned int *)h->n_lead, lcap, h->hv);
     HIPCHK(h, hipGetLastError());
     tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::inclusive_scan(h->sort_tmp, tb, (const uint64_t *)h->seg, h->scanned, (size_t)R, SegOp(), st));
@@ -1997,7 +2017,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
-    Order ord{h->hot, h->cold, h->lead_lam, h->hv, h->n_valid};
+    Order ord{h->hot, h->cold, h->lead_lam, h->hv, h->n_valid, lcap};
     if (K == 1)
         HIPCHK(h, launch_score_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
                                          score, st));
@@ -2639,7 +2659,7 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
                        (const uint32_t *)h->keys_in, h->seq_keys, h->seq_vals);
     size_t tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals,
-                                                    h->seq_perm, (uint32_t)R, 0, 32, s));
+                                                    h->seq_perm, (uint32_t)R, 0, bits_for(P), s));
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_start, P, 0u);
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_end, P, 0u);
     hipLaunchKernelGGL(segment_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s,
@@ -2680,6 +2700,9 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value) {
     case NETKV_OPT_POLICY:
         if (value > 2) return fail(h, NETKV_EINVAL, "policy must be 0 (full), 1 (no congestion) or 2 (topology only)");
         h->policy_opt = value;
+        return NETKV_OK;
+    case NETKV_OPT_LEAD_CAP:
+        h->lead_cap_opt = value;
         return NETKV_OK;
     case NETKV_OPT_COLS:
         if (value != 0 && value != 1 && value != 2 && value != 3 && value != 4 && value != 6)

@@ -89,6 +89,7 @@ NETKV_OPT_RUN_LEN = 1
 NETKV_OPT_REUSE = 2
 NETKV_OPT_COLS = 3
 NETKV_OPT_POLICY = 4
+NETKV_OPT_LEAD_CAP = 5
 
 
 def load_library(path: str = LIB_PATH):

@@ -113,7 +113,8 @@ def test_ragged_decodes_long_runs_and_empty_runs(nk):
 
 def test_tuning_options_leave_results_unchanged(nk):
     """Decodes per lane (1, 2, 3, 4, 6), run lengths (1, 7, automatic, longer
-    than the batch) and first-miss reuse on/off are layout choices only:
+    than the batch), prefix sharing on/off and the leader table's size are
+    layout choices only:
     every pair and every top-k entry is bit-identical across them, and the
     first matches the oracle.  270 decodes leave a partial last group of
     decodes at every width."""
@@ -141,6 +142,19 @@ def test_tuning_options_leave_results_unchanged(nk):
                     continue
                 for key in base:
                     assert np.array_equal(g[key], base[key]), (cols, rl, reuse, key)
+    # a leader table that takes 1, 13 or 200 leaders (and as many blocks'
+    # holder values): leaders past it, and the requests that follow them,
+    # are matched on their own; leaders without holder room look up their
+    # blocks themselves
+    nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, 0)
+    for cap in (1, 13, 200):
+        for reuse in (1, 0):
+            nk.netkv_set_option(sel.h, nk.NETKV_OPT_LEAD_CAP, cap)
+            nk.netkv_set_option(sel.h, nk.NETKV_OPT_REUSE, reuse)
+            nk.netkv_set_option(sel.h, nk.NETKV_OPT_RUN_LEN, 7 if reuse else 0)
+            g = _run(nk, sel, req, 3)
+            for key in base:
+                assert np.array_equal(g[key], base[key]), (cap, reuse, key)
     sel.close()
 
 
