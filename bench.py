@@ -34,10 +34,12 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak, GB/s
 # VALU lane-operations per second: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one
 # wave64 VALU instruction per CU per cycle, packed fp32 not counted)
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
-# lane-operations per (request, decode) pair that scoring itself needs, given
-# the prefix length: non-cached tokens x = l - B_tok j, the feasibility test,
-# the int-to-float conversion, the fused multiply-add x * spt + (L + load),
-# the feasible-or-infinity select, and the minimum (Eqs. (2)-(5), Algorithm 1)
+# lane-operations per (request, decode) pair that scoring needs once the
+# leader's prefix length is known: the cap lambda = min(B_tok j_leader,
+# B_tok L*), non-cached tokens x = l - lambda, the fused multiply-add
+# x * spt + (L + load), the feasibility test x <= xm_d, the feasible-or-
+# infinity select, and one comparison of the per-request minimum
+# (Eqs. (2)-(5), Algorithm 1)
 OPS_PER_PAIR = 6
 
 

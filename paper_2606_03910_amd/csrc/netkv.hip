@@ -357,13 +357,26 @@ struct alignas(16) Lead {
 };
 constexpr uint32_t kNoPre = 0xFFFFFFFFu;
 
+// Token counts below 2^24 are integers that fp32 holds exactly: requests
+// shorter than that are scored in fp32 with results identical to integer
+// arithmetic, longer ones in integers.
+constexpr uint32_t kExactTok = 1u << 24;
+
+// A request by hash-order position: its prefill row and length.
+struct Pre {
+    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * slp * 8
+    uint32_t len;    // input tokens
+};
+
 // One request in scoring order: the part every scoring step reads (one
 // 16-byte scalar load) ...
 struct alignas(16) Hot {
-    uint32_t row;    // byte offset of the request's row of derived (p, d) values, p * slp * 8
-    uint32_t slot;   // leader slot, kNoLead (prefix length 0 everywhere) or kLeadOver
-    uint32_t len;    // input tokens
-    uint32_t lams;   // B_tok * L* (kNoCap for a leader)
+    uint32_t row;    // byte offset of the prefill row, as in Pre
+    uint32_t lrow;   // byte offset of the leader's row of B_tok * j in the leader
+                     // table; the all-zero row when there is no leader
+    uint32_t len;    // input tokens, fp32 bits
+    uint32_t lams;   // B_tok * L* (+inf for a leader itself), fp32 bits; negative:
+                     // match this request on its own, in integers
 };
 constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead by the scan
 
@@ -378,7 +391,7 @@ struct alignas(16) Cold {
 struct Order {
     const Hot *hot;           // [n_valid + kHotPad] scoring-order request records
     const Cold *cold;         // [n_req]
-    const uint32_t *lam;      // [leaders][D] B_tok * prefix length of each leader on each decode
+    const float *lam;         // [leader rows][D] B_tok * prefix length of each leader on each decode
     const uint32_t *hv;       // holder values of the leaders' blocks
     const uint32_t *n_valid;  // valid requests (they sort first)
     uint32_t lead_cap;        // leaders the table takes in this call
@@ -467,7 +480,7 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
                                                     const uint32_t *__restrict__ sorted_keys, Table t,
                                                     uint32_t reuse, uint64_t *__restrict__ seg,
                                                     uint32_t *__restrict__ pkey, uint32_t *__restrict__ pval,
-                                                    Hot *__restrict__ hrec, Cold *__restrict__ crec,
+                                                    Pre *__restrict__ hrec, Cold *__restrict__ crec,
                                                     Lead *__restrict__ lead, uint32_t lead_cap,
                                                     unsigned int *__restrict__ n_lead, uint64_t hv_cap,
                                                     unsigned long long *__restrict__ hv_used,
@@ -488,7 +501,7 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
         if (sub == 0) {
             seg[i] = seg_elem(kNoLead, 0);
             pkey[i] = P;
-            hrec[i] = Hot{0, kNoLead, 0, 0};
+            hrec[i] = Pre{0, 0};
             crec[i] = Cold{0, r, 0};
         }
         return;
@@ -535,8 +548,8 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
     }
     seg[i] = e;
     pkey[i] = rq.prefill[r];
-    hrec[i] = Hot{rq.prefill[r] * slp * (uint32_t)sizeof(float2),   // < 2^32 (checked at load)
-                  0, rq.len[r], 0};
+    hrec[i] = Pre{rq.prefill[r] * slp * (uint32_t)sizeof(float2),   // < 2^32 (checked at load)
+                  rq.len[r]};
     crec[i] = Cold{a, r, (uint32_t)nr};
 }
 
@@ -573,25 +586,34 @@ __global__ __launch_bounds__(kBlock) void lead_holder_kernel(Table t, const uint
 }
 
 // Scoring-order records: position k of the prefill order holds hash-order
-// position pord[k], whose record takes its leader slot and B_tok * L* from
-// the scan.  Positions past the batch (kHotPad of them) get a record that
-// the scan may read ahead but never scores (row 0, no leader).
-__global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t bt, const uint32_t *__restrict__ pord,
+// position pord[k], whose record takes its leader row and B_tok * L* from
+// the scan (lstride: bytes per leader row; zrow: byte offset of the
+// all-zero row).  A request whose leader did not fit the leader table, or
+// of 2^24 tokens or more, is marked to be matched on its own.  Positions
+// past the batch (kHotPad of them) get a record that the scoring kernel
+// may read ahead but never scores (row 0, no leader).
+__global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t bt, uint32_t lstride, uint32_t zrow,
+                                                       const uint32_t *__restrict__ pord,
                                                        const uint64_t *__restrict__ scanned,
-                                                       const Hot *__restrict__ hrec, const Cold *__restrict__ crec,
+                                                       const Pre *__restrict__ hrec, const Cold *__restrict__ crec,
                                                        Hot *__restrict__ hot, Cold *__restrict__ cold) {
     const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= (uint64_t)n_req + kHotPad) return;
     if (k >= n_req) {
-        hot[k] = Hot{0, kNoLead, 0, 0};
+        hot[k] = Hot{0, zrow, 0, 0};
         return;
     }
     const uint32_t i = pord[k];
-    Hot o = hrec[i];
+    const Pre pr = hrec[i];
     const uint64_t e = scanned[i];
-    const uint32_t ls = (uint32_t)e;
-    o.slot = (uint32_t)(e >> 32);
-    o.lams = ls == kNoCap ? kNoCap : bt * ls;   // ls <= n_r, so bt * ls <= len
+    const uint32_t ls = (uint32_t)e, slot = (uint32_t)(e >> 32);
+    const bool own = slot == kLeadOver || pr.len >= kExactTok;
+    Hot o;
+    o.row = pr.row;
+    o.lrow = (slot < kLeadOver && !own) ? slot * lstride : zrow;
+    o.len = __float_as_uint((float)pr.len);
+    // ls <= n_r, so bt * ls <= len
+    o.lams = own ? __float_as_uint(-1.0f) : ls == kNoCap ? __float_as_uint(__builtin_inff()) : __float_as_uint((float)(bt * ls));
     hot[k] = o;
     cold[k] = crec[i];
 }
@@ -611,7 +633,7 @@ __device__ inline Hot load_hot(const Hot *base, uint32_t i) {
     const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
     Hot x;
     x.row = w[0];
-    x.slot = w[1];
+    x.lrow = w[1];
     x.len = w[2];
     x.lams = w[3];
     return x;
@@ -716,7 +738,8 @@ __device__ inline void probe_from(const Table &t, uint32_t base, cptr<uint64_t> 
 // in lane k the decodes that hold every block up to k; it only loses bits as
 // k grows, so decode l matches exactly the blocks below the first lane whose
 // word lacks bit l, found by binary search over the words in LDS.  Writes
-// B_tok * j for the task's decodes.
+// B_tok * j for the task's decodes, in fp32 (exact below 2^24; only
+// requests shorter than that read it, capped by their own length).
 __device__ inline uint64_t shfl_up_u64(uint64_t v, uint32_t delta) {
     const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, delta, kWave);
     const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), delta, kWave);
@@ -727,7 +750,7 @@ __global__ __launch_bounds__(kBlock) void lead_kernel(Table t, uint32_t D, uint3
                                                       const unsigned int *__restrict__ n_lead, uint32_t lead_cap,
                                                       const uint32_t *__restrict__ hv,
                                                       const uint64_t *__restrict__ hashes, uint32_t ngroup,
-                                                      uint32_t *__restrict__ lam_out) {
+                                                      float *__restrict__ lam_out) {
     __shared__ uint64_t pw[kWavesPerBlock][kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t wv = wave_index();
@@ -778,7 +801,7 @@ __global__ __launch_bounds__(kBlock) void lead_kernel(Table t, uint32_t D, uint3
             __builtin_amdgcn_wave_barrier();
         }
         const uint32_t d = base + lane;
-        if (d < D) lam_out[(uint64_t)slot * D + d] = bt * j;
+        if (d < D) lam_out[(uint64_t)slot * D + d] = (float)(bt * j);
     }
 }
 
@@ -795,20 +818,26 @@ __device__ inline uint32_t load_lam(__amdgpu_buffer_rsrc_t r, uint32_t lane_off,
 
 // One wavefront per (run of scoring-order requests, group of 64*C decodes);
 // lane l holds decodes g*64*C + q*64 + l, q < C.  For each request of the
-// run: prefix lengths min(leader's, L*) (matched on its own when its leader
-// did not fit the leader table), non-cached tokens, feasibility and cost
-// (Eqs. (2)-(7)), then the group's K best feasible (score, index) keys into
-// partial[group][position][0..K).  Requests of one prefill are consecutive,
-// so the snapshot row stays in registers and is reloaded only when the
-// prefill changes; the leader's prefix lengths are kept too, and the next
-// request's are fetched during the current step only when its leader
+// run: prefix lengths min(leader's, L*), non-cached tokens, feasibility and
+// cost (Eqs. (2)-(7)), then the group's K best feasible (score, index) keys
+// into partial[group][position][0..K).  Token counts are below 2^24 here,
+// so x = l - lambda and the feasibility test x <= xm_d are exact in fp32
+// and give the costs of integer arithmetic; a request no longer than every
+// limit xm_d of the group is feasible on all of them and skips the test.
+// A request marked in its record (its leader did not fit the leader table,
+// or it has 2^24 tokens or more) is matched from block 0 on its own and
+// scored in integers.  Requests of one prefill are consecutive, so the
+// snapshot row stays in registers and is reloaded only when the prefill
+// changes; the leader's prefix lengths are kept too, and the next
+// request's are fetched during the current step only when its leader row
 // differs.  Records are read two requests ahead.  Requests are taken in
 // chunks of 64/K whose keys are gathered one per lane and stored together.
 template <int K, int W, int C, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Hot *__restrict__ hot,
                                                        const Cold *__restrict__ cold,
-                                                       const uint32_t *__restrict__ lead_lam, uint32_t lead_cap,
+                                                       const float *__restrict__ lead_lam, uint32_t lead_rows,
                                                        const uint64_t *__restrict__ hashes,
+                                                       const uint32_t *__restrict__ len_tokens,
                                                        const uint32_t *__restrict__ n_valid, uint32_t n_req,
                                                        uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
                                                        uint64_t *__restrict__ partial, PairOut po) {
@@ -833,43 +862,50 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
     const uint32_t base = grp * (kWave * C);
     const uint32_t bt = s.block_tokens;
-    uint32_t d[C], voff[C], loff[C], xm[C];
+    uint32_t d[C], voff[C], loff[C];
+    float xmf[C];
     bool act[C];
-    lmask okm[C];
+    // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
+    // xlim >= 1; xlim = 0 never is (limit -1).  Limits above 2^24 are taken
+    // as 2^24, which every x scored in fp32 is below.  xlo: the least limit
+    // of the lane's decodes as fp32 bits, 0 when one is never feasible.
+    uint32_t xlo = 0xFFFFFFFFu;
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
         act[q] = d[q] < s.D;
         const uint32_t pc = act[q] ? d[q] : 0;
         voff[q] = pc * (uint32_t)sizeof(float2);
-        loff[q] = pc * (uint32_t)sizeof(uint32_t);
-        // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
-        // xlim >= 1 (capped to 32 bits, as x is); xlim = 0 never is
+        loff[q] = pc * (uint32_t)sizeof(float);
         const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
-        okm[q] = ballot(xlim != 0);
-        xm[q] = xlim == 0 ? 0u : xlim - 1 > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)(xlim - 1);
+        xmf[q] = xlim == 0 ? -1.0f : (float)(xlim - 1 < kExactTok ? xlim - 1 : (uint64_t)kExactTok);
+        xlo = min(xlo, xlim == 0 ? 0u : __float_as_uint(xmf[q]));
     }
+    // a request of at most xall tokens (fp32 bits) is feasible on every
+    // decode of the group
+    const uint32_t xall = wave_min_u32_dpp(xlo);
     const cptr<uint64_t> chash = as_const(hashes);
     // rows of (seconds per token, constant part) and the leaders' prefix
     // lengths through buffer resources: a row's byte offset is the scalar
     // offset, the column's the lane offset
-    const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);        // < 2^32 (checked at load)
-    const uint64_t ll_bytes = (uint64_t)lead_cap * s.D * sizeof(uint32_t);   // < 2^32 (capacity is capped)
+    const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);      // < 2^32 (checked at load)
+    const uint64_t ll_bytes = (uint64_t)lead_rows * s.D * sizeof(float);   // < 2^32 (capacity is capped)
     const __amdgpu_buffer_rsrc_t slr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)s.sl, (short)0, (int)(uint32_t)(sl_bytes < 0xFFFFFFFFull ? sl_bytes : 0xFFFFFFFFull), kBufferFlags);
     const __amdgpu_buffer_rsrc_t llr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)lead_lam, (short)0, (int)(uint32_t)(ll_bytes < 0xFFFFFFFFull ? ll_bytes : 0xFFFFFFFFull),
         kBufferFlags);
-    const uint32_t lstride = s.D * (uint32_t)sizeof(uint32_t);
     Hot c0 = load_hot(hot, i0);
     Hot c1 = load_hot(hot, i0 + 1);
     float2 rowv[C];           // the current prefill's row
     uint32_t rowcur = c0.row;
-    uint32_t laml[C], stg[C]; // the current leader's B_tok * j, and the next one's while it loads
+    // the current leader's B_tok * j, and the next one's while it loads, as
+    // fp32 bits: non-negative, so their order is that of the unsigned bits
+    uint32_t laml[C], stg[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         rowv[q] = load_row(slr, voff[q], c0.row);
-        laml[q] = c0.slot < kLeadOver ? load_lam(llr, loff[q], c0.slot * lstride) : 0u;
+        laml[q] = load_lam(llr, loff[q], c0.lrow);
         stg[q] = 0;
     }
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
@@ -879,26 +915,26 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
         const uint32_t g1 = (g0 + kPer < i1) ? g0 + kPer : i1;
         for (uint32_t i = g0; i < g1; ++i) {
             const Hot c2 = load_hot(hot, i + 2);
-            // the next request's leader values, if they differ
-            const bool nl = c1.slot != c0.slot;
-            if (nl && c1.slot < kLeadOver) {
+            // the next request's leader values, if its leader row differs
+            const bool nl = c1.lrow != c0.lrow;
+            if (nl) {
 #pragma unroll
-                for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, loff[q], c1.slot * lstride);
+                for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, loff[q], c1.lrow);
             }
             if (c0.row != rowcur) {
 #pragma unroll
                 for (int q = 0; q < C; ++q) rowv[q] = load_row(slr, voff[q], c0.row);
                 rowcur = c0.row;
             }
-            // prefix lengths (as B_tok * j): the leader's, capped by L*
-            uint32_t lam[C];
-#pragma unroll
-            for (int q = 0; q < C; ++q) lam[q] = min(laml[q], c0.lams);
-            if (c0.slot == kLeadOver) {
-                // the leader did not fit the leader table: match this request
-                // on its own from block 0 (exact)
+            uint32_t r_out = 0;
+            if (PAIRS) r_out = load_cold(cold, i).r;
+            uint32_t cb[C];
+            if ((int32_t)c0.lams < 0) {
+                // matched on its own from block 0, in integers (exact)
                 const Cold k = load_cold(cold, i);
+                const uint32_t len = as_const(len_tokens)[k.r];
                 lmask alive[C];
+                uint32_t lam[C];
 #pragma unroll
                 for (int q = 0; q < C; ++q) {
                     lam[q] = 0;
@@ -906,25 +942,49 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
                 }
                 if (k.n)
                     probe_from<W, C>(t, base, chash + k.a, k.n, 0, alive, lam, bt, holder_uniform(t, chash[k.a]));
-            }
-            // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
-            uint32_t r_out = 0;
-            if (PAIRS) r_out = load_cold(cold, i).r;
-            uint32_t cb[C];
 #pragma unroll
-            for (int q = 0; q < C; ++q) {
-                const uint32_t x = c0.len - lam[q];
-                const bool feas = in_mask(okm[q]) && x <= xm[q];
-                const float cost = fmaf((float)x, rowv[q].x, rowv[q].y);
-                if (PAIRS && act[q]) {
-                    const uint64_t o = (uint64_t)r_out * s.D + d[q];
-                    const uint32_t jq = lam[q] / bt;
-                    if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
-                    if (po.feas) po.feas[o] = feas ? 1 : 0;
-                    if (po.score) po.score[o] = cost;
-                    if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                for (int q = 0; q < C; ++q) {
+                    const uint32_t x = len - lam[q];
+                    const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
+                    const bool feas = (uint64_t)x < xlim;
+                    const float cost = fmaf((float)x, rowv[q].x, rowv[q].y);
+                    if (PAIRS && act[q]) {
+                        const uint64_t o = (uint64_t)r_out * s.D + d[q];
+                        const uint32_t jq = lam[q] / bt;
+                        if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                        if (po.feas) po.feas[o] = feas ? 1 : 0;
+                        if (po.score) po.score[o] = cost;
+                        if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                    }
+                    cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
                 }
-                cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
+            } else {
+                // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
+                const float lenf = __uint_as_float(c0.len);
+                if (!PAIRS && c0.len <= xall) {
+#pragma unroll
+                    for (int q = 0; q < C; ++q)
+                        cb[q] = __float_as_uint(
+                            fmaf(lenf - __uint_as_float(min(laml[q], c0.lams)), rowv[q].x, rowv[q].y));
+                } else {
+#pragma unroll
+                    for (int q = 0; q < C; ++q) {
+                        const float lam = __uint_as_float(min(laml[q], c0.lams));
+                        const float x = lenf - lam;
+                        const bool feas = x <= xmf[q];
+                        const float cost = fmaf(x, rowv[q].x, rowv[q].y);
+                        if (PAIRS && act[q]) {
+                            const uint64_t o = (uint64_t)r_out * s.D + d[q];
+                            const uint32_t jq = (uint32_t)lam / bt;
+                            if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                            if (po.feas) po.feas[o] = feas ? 1 : 0;
+                            if (po.score) po.score[o] = cost;
+                            if (po.jT)
+                                po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                        }
+                        cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
+                    }
+                }
             }
             // the group's K best: least cost bits, then least decode index,
             // i.e. the lowest lane holding the minimum in the first column
@@ -955,7 +1015,7 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
             }
             if (nl) {
 #pragma unroll
-                for (int q = 0; q < C; ++q) laml[q] = c1.slot < kLeadOver ? stg[q] : 0u;
+                for (int q = 0; q < C; ++q) laml[q] = stg[q];
             }
             c0 = c1;
             c1 = c2;
@@ -1616,11 +1676,12 @@ struct netkv_ctx {
     uint64_t hv_cap = 0;
     unsigned long long *hv_used = nullptr;
     uint64_t *seg = nullptr, *scanned = nullptr;   // segmented-scan elements, hash order
-    Hot *hrec = nullptr;                     // scoring records by hash-order position
+    Pre *hrec = nullptr;                     // prefill row and length by hash-order position
     Cold *crec = nullptr;
     uint32_t *pkey = nullptr, *pkey_out = nullptr, *pval = nullptr, *pord = nullptr;   // prefill order
     Lead *lead = nullptr;                    // leader table
-    uint32_t *lead_lam = nullptr;            // [lead_cap][D] B_tok * prefix length of each leader
+    float *lead_lam = nullptr;               // [lead_cap + 1][D] B_tok * prefix length of each
+                                             // leader; row lead_cap is all zero (no leader)
     uint32_t lead_cap = 0, lead_D = 0;
     unsigned int *n_lead = nullptr;
     void *sort_tmp = nullptr;
@@ -1868,8 +1929,12 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         dfree(h->lead);
         dfree(h->lead_lam);
         h->lead_cap = 0;
-        if (dalloc(h->lead, lc) != hipSuccess || dalloc(h->lead_lam, (uint64_t)lc * h->D) != hipSuccess)
+        if (dalloc(h->lead, lc) != hipSuccess || dalloc(h->lead_lam, (uint64_t)(lc + 1) * h->D) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "leader table allocation failed");
+        // the all-zero row of requests without a leader (no leader writes it)
+        hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(h->D, 256)), dim3(256), 0, st,
+                           (uint32_t *)(h->lead_lam + (uint64_t)lc * h->D), (uint64_t)h->D, 0u);
+        if (hipGetLastError() != hipSuccess) return fail(h, NETKV_EDEVICE, "leader table initialisation failed");
         h->lead_cap = lc;
         h->lead_D = h->D;
     }
@@ -1928,16 +1993,16 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
     const uint32_t grid = (uint32_t)grid64;
     // a request that matches on its own (its leader did not fit the leader
-    // table) looks blocks up one at a time: rare, and a short loop keeps the
-    // kernel's registers for the common path
+    // table, or 2^24 tokens or more) looks blocks up one at a time: rare,
+    // and a short loop keeps the kernel's registers for the common path
     if (pairs)
         hipLaunchKernelGGL((score_kernel<K, 1, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, ord.lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
-                           po);
+                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, ord.n_valid, rq.n_req, run_len, n_runs,
+                           ngroup, partial, po);
     else
         hipLaunchKernelGGL((score_kernel<K, 1, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, ord.lead_cap, rq.hashes, ord.n_valid, rq.n_req, run_len, n_runs, ngroup, partial,
-                           po);
+                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, ord.n_valid, rq.n_req, run_len, n_runs,
+                           ngroup, partial, po);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return time_end(h, st);
 }
@@ -2011,9 +2076,10 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
                                                     (uint32_t)R, 0, bits_for(h->P), st));
+    const uint32_t lstride = h->D * (uint32_t)sizeof(float);
     hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st, (uint32_t)R,
-                       h->block_tokens, (const uint32_t *)h->pord, (const uint64_t *)h->scanned,
-                       (const Hot *)h->hrec, (const Cold *)h->crec, h->hot, h->cold);
+                       h->block_tokens, lstride, h->lead_cap * lstride, (const uint32_t *)h->pord,
+                       (const uint64_t *)h->scanned, (const Pre *)h->hrec, (const Cold *)h->crec, h->hot, h->cold);
     HIPCHK(h, hipGetLastError());
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);

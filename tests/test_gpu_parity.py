@@ -64,6 +64,9 @@ def test_c0_full_parity(nk, inflight, k):
     check_pairs(g["j"], g["feas"], g["cost"], o)
     n, near = check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
     assert n > 0.99 * cfg.n_requests * k
+    g2 = _run(nk, sel, req, k, pairs=False)
+    assert np.array_equal(g2["idx"], g["idx"])
+    assert np.array_equal(g2["score"].view(np.uint32), g["score"].view(np.uint32))
     sel.close()
 
 
@@ -155,6 +158,36 @@ def test_tuning_options_leave_results_unchanged(nk):
             g = _run(nk, sel, req, 3)
             for key in base:
                 assert np.array_equal(g[key], base[key]), (cap, reuse, key)
+            g2 = _run(nk, sel, req, 3, pairs=False)
+            assert np.array_equal(g2["idx"], base["idx"]), (cap, reuse)
+            assert np.array_equal(g2["score"].view(np.uint32), base["score"].view(np.uint32)), (cap, reuse)
+    sel.close()
+
+
+def test_all_feasible_path_matches_general_path(nk):
+    """A pool of whole wavefronts of decodes (384), where a request no
+    longer than every feasibility limit of a decode group is scored without
+    per-pair feasibility tests: the top-k-only kernel must match the
+    per-pair kernel bit for bit, and the oracle, under every decodes-per-lane
+    choice, with requests on both sides of the limits."""
+    _say("all-feasible path")
+    cl = W.Cluster(8, 8, 4, 2)
+    cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=4000, cache_per_decode=4096)
+    assert cfg.n_decode == 384
+    snap, req, cache = _inputs(cfg, 11, "random")
+    snap["m_min"] = 15 * 10 ** 9
+    sel = _gpu(nk, snap, cache)
+    o = oracle.select(snap, cache, req, k=2, pairs=True, n_threads=8)
+    allf = o["feasible"].all(axis=1)
+    assert 0.05 < allf.mean() < 0.95, allf.mean()
+    for cols in (0, 1, 2, 3, 6):
+        nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, cols)
+        g = _run(nk, sel, req, 2)
+        check_pairs(g["j"], g["feas"], g["cost"], o)
+        check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+        g2 = _run(nk, sel, req, 2, pairs=False)
+        assert np.array_equal(g2["idx"], g["idx"]), cols
+        assert np.array_equal(g2["score"].view(np.uint32), g["score"].view(np.uint32)), cols
     sel.close()
 
 
@@ -370,6 +403,48 @@ def test_kernel_timing_mean_over_launches(nk):
     nk.netkv_select_batch(sel.h, rd, 1, idx, sc, None, sel.device)
     with pytest.raises(nk.NetKVError):
         nk.netkv_kernel_ms(sel.h)
+    sel.close()
+
+
+def test_requests_across_2_pow_24_tokens(nk):
+    """Token counts below 2^24 are scored in fp32, longer requests are
+    matched on their own and scored in integers; a request of 2^25 tokens
+    leads the shorter ones that share its chain, so those read its prefix
+    lengths capped by their own.  Both kernels (per-pair outputs and
+    top-k only) must equal the oracle across the boundary."""
+    _say("requests across 2^24 tokens")
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=8)
+    bt = cfg.block_tokens
+    snap = W.make_snapshot(cfg, 23)
+    D = cfg.n_decode
+    rng = np.random.default_rng(23)
+    lens = np.array([2**25 - 1000, 2**24 - 1, 2**24, 2**24 + 300, 2**24 + 5 * bt + 7, 1000, 2**24 - bt, 70000],
+                    dtype=np.uint32)
+    nb = (lens // bt).astype(np.int64)
+    chain = (np.arange(1, nb.max() + 1, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15)) | np.uint64(1)
+    # decode 0 holds the whole chain, decodes 1 and 2 its first 20000 and 100 blocks
+    sets = [chain, chain[:20000], chain[:100]] + [rng.integers(1, 2**63, 500, dtype=np.uint64)
+                                                  for _ in range(D - 3)]
+    cache = dict(n_decode=D, hash_off=np.concatenate([[0], np.cumsum([len(x) for x in sets])]).astype(np.uint64),
+                 hashes=np.concatenate(sets).astype(np.uint64))
+    runs = [chain[:n] for n in nb]
+    runs[3] = np.concatenate([chain[:nb[3] - 10], rng.integers(1, 2**63, 10, dtype=np.uint64)])
+    runs[7] = rng.integers(1, 2**63, nb[7], dtype=np.uint64)
+    req = dict(n_req=len(lens), prefill=rng.integers(0, cfg.n_prefill, len(lens)).astype(np.uint32),
+               len_tokens=lens, hash_off=np.concatenate([[0], np.cumsum(nb)]).astype(np.uint64),
+               hashes=np.concatenate(runs).astype(np.uint64))
+    assert nb.max() < 65535
+    sel = _gpu(nk, snap, cache)
+    o = oracle.select(snap, cache, req, k=2, pairs=True)
+    # the long requests fit only where their whole run is resident
+    long = [0, 1, 2, 3, 4, 6]
+    assert o["feasible"][long, 0].all() and not o["feasible"][long, 1:].any()
+    g = _run(nk, sel, req, 2)
+    check_pairs(g["j"], g["feas"], g["cost"], o)
+    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    g2 = _run(nk, sel, req, 2, pairs=False)
+    assert np.array_equal(g2["idx"], g["idx"])
+    assert np.array_equal(g2["score"].view(np.uint32), g["score"].view(np.uint32))
     sel.close()
 
 
