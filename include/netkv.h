@@ -127,7 +127,9 @@ typedef struct {
     const uint32_t *prefill;        /* [n_req] */
     const uint32_t *len_tokens;     /* [n_req] */
     const uint64_t *hash_off;       /* [n_req + 1] */
-    const uint64_t *hashes;         /* [n_hashes], nonzero */
+    const uint64_t *hashes;         /* [n_hashes]; a block hash 0 is resident
+                                       on no decode (resident sets cannot
+                                       hold 0), so a run's match ends there */
     uint64_t n_hashes;
 } netkv_requests_t;
 

@@ -21,14 +21,17 @@
 // Kernels of one selection (netkv_select_batch), in launch order:
 //   derive_kernel      -- per-call cost factors (Eqs. (3)-(7) split by what
 //                         they depend on).
-//   prep / count_zero / zero_fix -- validate requests, build hash-order keys.
-//   (rocPRIM radix sort into hash order)
+//   prep_kernel        -- validate requests, build hash-order keys.
+//   sort kernels       -- stable radix sort into hash order (rocPRIM's for
+//                         small and very large batches).
 //   order_kernel       -- common leading run with the previous position,
 //                         leaders (positions whose next block some decode
 //                         holds), segmented-scan elements, records.
 //   lead_holder_kernel -- holder values of every leader's blocks.
-//   (rocPRIM segmented scan; stable radix sort into prefill order)
-//   assemble_kernel    -- scoring records in prefill order.
+//   (rocPRIM segmented scan)
+//   sort kernels       -- stable sort into prefill order, writing the
+//                         scoring records (or rocPRIM's sort and
+//                         assemble_kernel).
 //   lead_kernel        -- prefix lengths of every leader on every decode.
 //   score_kernel       -- per pair: prefix length min(leader's, L*),
 //                         feasibility and cost (Eqs. (2)-(7)), then the
@@ -380,12 +383,10 @@ struct alignas(16) Hot {
 };
 constexpr uint32_t kHotPad = 2;   // records past the last position, read ahead by the scan
 
-// ... and the rest (output index; hash run, read only when a request has
-// to be matched on its own).
-struct alignas(16) Cold {
-    uint64_t a;      // offset of the hash run
-    uint32_t r;      // request index in the caller's batch
-    uint32_t n;      // hashed blocks
+// ... and its index in the caller's batch (where its result goes, and its
+// hash run and length when it is matched on its own).
+struct Cold {
+    uint32_t r;
 };
 
 struct Order {
@@ -399,20 +400,16 @@ struct Order {
 
 // Validate each request and build its sort key, one thread per request.
 // A request of more than max_blocks blocks is invalid (calls that keep
-// per-pair prefix lengths in 16 bits pass 65535).
-// The reserved hash value 0 is looked for separately: a flat scan of the
-// batch's hash array (count_zero_kernel) raises `zflag`, and only then does
-// zero_fix_kernel check each request's run and invalidate those holding it.
-// Thread 0 clears zflag for that scan, and the holder-value and leader
-// counters of the order kernel.
+// per-pair prefix lengths in 16 bits pass 65535).  A block hash 0 needs no
+// check: no resident set holds it (cache loads reject it), so it is a miss
+// on every decode, as the prefix definition gives.  Thread 0 clears the
+// holder-value and leader counters of the order kernel.
 __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max_blocks, uint32_t *__restrict__ keys,
                                                    uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
-                                                   uint32_t *__restrict__ zflag,
                                                    unsigned long long *__restrict__ hv_used,
                                                    unsigned int *__restrict__ n_lead) {
     const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
     if (r == 0) {
-        *zflag = 0;
         *hv_used = 0;
         *n_lead = 0;
     }
@@ -435,34 +432,6 @@ __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max
         bad = !ok;
     }
     if (__ballot(bad) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrRequest);
-}
-
-// Requests whose run holds the value 0 become invalid (only when the flat
-// scan found a 0 somewhere; otherwise every wavefront returns at once).
-// Wavefronts take 16 requests at a time, lanes stride over each run.
-__global__ __launch_bounds__(kBlock) void zero_fix_kernel(Snap s, Reqs rq, uint32_t *__restrict__ keys,
-                                                          const uint32_t *__restrict__ zflag,
-                                                          uint32_t *__restrict__ err) {
-    if (*zflag == 0) return;
-    const uint32_t lane = threadIdx.x % kWave;
-    const uint32_t nw = gridDim.x * kWavesPerBlock;
-    bool found = false;
-    for (uint32_t w = blockIdx.x * kWavesPerBlock + wave_index(); w * 16 < rq.n_req; w += nw) {
-        for (uint32_t q = 0; q < 16; ++q) {
-            const uint32_t r = w * 16 + q;
-            if (r >= rq.n_req) break;
-            uint32_t p, len, n;
-            uint64_t a;
-            if (!request_ok(rq, s, r, p, len, a, n)) continue;
-            bool zero = false;
-            for (uint32_t i = lane; i < n; i += kWave) zero |= rq.hashes[a + i] == 0;
-            if (__any(zero)) {
-                if (lane == 0) keys[r] = kKeyInvalid;
-                found = true;
-            }
-        }
-    }
-    if (found && lane == 0) atomicOr(err, kErrZeroHash);
 }
 
 // Per hash-order position i (G lanes, G divides 64): the common leading run
@@ -502,7 +471,7 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
             seg[i] = seg_elem(kNoLead, 0);
             pkey[i] = P;
             hrec[i] = Pre{0, 0};
-            crec[i] = Cold{0, r, 0};
+            crec[i] = Cold{r};
         }
         return;
     }
@@ -550,7 +519,7 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
     pkey[i] = rq.prefill[r];
     hrec[i] = Pre{rq.prefill[r] * slp * (uint32_t)sizeof(float2),   // < 2^32 (checked at load)
                   rq.len[r]};
-    crec[i] = Cold{a, r, (uint32_t)nr};
+    crec[i] = Cold{r};
 }
 
 // Holder values of every leader's blocks from block 0 up to the first
@@ -585,6 +554,21 @@ __global__ __launch_bounds__(kBlock) void lead_holder_kernel(Table t, const uint
     }
 }
 
+// The scoring record of a request from its prefill row and length and its
+// scan element (leader slot, L*).
+__device__ inline Hot make_hot(Pre pr, uint64_t e, uint32_t bt, uint32_t lstride, uint32_t zrow) {
+    const uint32_t ls = (uint32_t)e, slot = (uint32_t)(e >> 32);
+    const bool own = slot == kLeadOver || pr.len >= kExactTok;
+    Hot o;
+    o.row = pr.row;
+    o.lrow = (slot < kLeadOver && !own) ? slot * lstride : zrow;
+    o.len = __float_as_uint((float)pr.len);
+    // ls <= n_r, so bt * ls <= len
+    o.lams = own ? __float_as_uint(-1.0f)
+                 : ls == kNoCap ? __float_as_uint(__builtin_inff()) : __float_as_uint((float)(bt * ls));
+    return o;
+}
+
 // Scoring-order records: position k of the prefill order holds hash-order
 // position pord[k], whose record takes its leader row and B_tok * L* from
 // the scan (lstride: bytes per leader row; zrow: byte offset of the
@@ -604,18 +588,209 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
         return;
     }
     const uint32_t i = pord[k];
-    const Pre pr = hrec[i];
-    const uint64_t e = scanned[i];
-    const uint32_t ls = (uint32_t)e, slot = (uint32_t)(e >> 32);
-    const bool own = slot == kLeadOver || pr.len >= kExactTok;
-    Hot o;
-    o.row = pr.row;
-    o.lrow = (slot < kLeadOver && !own) ? slot * lstride : zrow;
-    o.len = __float_as_uint((float)pr.len);
-    // ls <= n_r, so bt * ls <= len
-    o.lams = own ? __float_as_uint(-1.0f) : ls == kNoCap ? __float_as_uint(__builtin_inff()) : __float_as_uint((float)(bt * ls));
-    hot[k] = o;
+    hot[k] = make_hot(hrec[i], scanned[i], bt, lstride, zrow);
     cold[k] = crec[i];
+}
+
+// ---------------------------------------------------------------- batch sorts
+//
+// Stable LSD radix sort for the batch orders (batches of up to kSortMaxN):
+// tiles of kSortTile positions, one wavefront each, four per workgroup.
+// A pass over `bits` digit bits (at most 11) takes four kernels:
+// sort_count_kernel counts each tile's digits into cnt[tile][digit];
+// sort_segsum_kernel and sort_offsets_kernel turn every digit's column into
+// exclusive offsets over the tiles (in place; the column is cut into at
+// most kSortSegs segments, summed first) and write the digit totals;
+// sort_scatter_kernel adds the digit bases (an exclusive scan of the
+// totals) and each tile writes its elements in order, 64 at a time,
+// ranking equal digits within the 64 by lane masks.  Equal keys keep
+// their order (stable), which the prefill order relies on.
+constexpr uint32_t kSortTile = 1024;
+constexpr uint32_t kSortMaxBits = 11;
+constexpr uint32_t kSortMaxBins = 1u << kSortMaxBits;
+constexpr uint64_t kSortMaxN = 1ull << 24;
+constexpr uint64_t kSortMinN = 1ull << 16;   // smaller batches: rocPRIM (fewer launches)
+constexpr uint32_t kSortSegs = 32;
+constexpr uint32_t kSortSteps = kSortTile / kWave;   // 64-element steps of a tile
+
+__global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__restrict__ keys, uint32_t n,
+                                                            uint32_t shift, uint32_t bits, uint32_t ntile,
+                                                            uint32_t *__restrict__ cnt) {
+    __shared__ uint32_t hs[kWavesPerBlock * kSortMaxBins];
+    const uint32_t bins = 1u << bits, mask = bins - 1;
+    for (uint32_t b = threadIdx.x; b < kWavesPerBlock * bins; b += blockDim.x) hs[b] = 0;
+    __syncthreads();
+    const uint32_t w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const uint32_t tile = blockIdx.x * kWavesPerBlock + w;
+    uint32_t *h = hs + w * bins;
+    if (tile < ntile) {
+        const uint64_t e0 = (uint64_t)tile * kSortTile + lane;
+        uint32_t kr[kSortSteps];   // the lane's keys, all loads issued first
+#pragma unroll
+        for (uint32_t x = 0; x < kSortSteps; ++x) {
+            const uint64_t e = e0 + (uint64_t)x * kWave;
+            kr[x] = e < n ? keys[e] : 0u;
+        }
+#pragma unroll
+        for (uint32_t x = 0; x < kSortSteps; ++x)
+            if (e0 + (uint64_t)x * kWave < n) atomicAdd(h + ((kr[x] >> shift) & mask), 1u);
+    }
+    __syncthreads();
+    if (tile < ntile)
+        for (uint32_t b = lane; b < bins; b += kWave) cnt[(uint64_t)tile * bins + b] = h[b];
+}
+
+// One thread per (segment, digit): the segment's sum of the digit's
+// column (segments of seglen tiles).
+__global__ __launch_bounds__(256) void sort_segsum_kernel(const uint32_t *__restrict__ cnt, uint32_t ntile,
+                                                          uint32_t bits, uint32_t nseg, uint32_t seglen,
+                                                          uint32_t *__restrict__ segsum) {
+    const uint32_t bins = 1u << bits;
+    const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t b = g & (bins - 1), sg = g >> bits;
+    if (sg >= nseg) return;
+    const uint32_t t0 = sg * seglen, t1 = t0 + seglen < ntile ? t0 + seglen : ntile;
+    uint32_t sum = 0;
+#pragma unroll 16
+    for (uint32_t t = t0; t < t1; ++t) sum += cnt[(uint64_t)t * bins + b];
+    segsum[sg * bins + b] = sum;
+}
+
+// One thread per (segment, digit): the exclusive offsets of the segment's
+// tiles (in place), starting from the sums of the earlier segments; the
+// last segment's thread writes the digit total.
+__global__ __launch_bounds__(256) void sort_offsets_kernel(uint32_t *__restrict__ cnt, uint32_t ntile, uint32_t bits,
+                                                           uint32_t nseg, uint32_t seglen,
+                                                           const uint32_t *__restrict__ segsum,
+                                                           uint32_t *__restrict__ tot) {
+    const uint32_t bins = 1u << bits;
+    const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t b = g & (bins - 1), sg = g >> bits;
+    if (sg >= nseg) return;
+    uint32_t run = 0;
+#pragma unroll 8
+    for (uint32_t q = 0; q < sg; ++q) run += segsum[q * bins + b];
+    const uint32_t t0 = sg * seglen, t1 = t0 + seglen < ntile ? t0 + seglen : ntile;
+    // loads of 16 tiles first, then their offsets
+    for (uint32_t ta = t0; ta < t1; ta += 16) {
+        uint32_t c[16];
+#pragma unroll
+        for (uint32_t u = 0; u < 16; ++u) c[u] = ta + u < t1 ? cnt[(uint64_t)(ta + u) * bins + b] : 0u;
+#pragma unroll
+        for (uint32_t u = 0; u < 16; ++u) {
+            if (ta + u < t1) cnt[(uint64_t)(ta + u) * bins + b] = run;
+            run += c[u];
+        }
+    }
+    if (sg == nseg - 1) tot[b] = run;
+}
+
+// Exclusive scan of the digit totals into LDS (bins <= kSortMaxBins, a
+// block of kBlock threads, kSortMaxBins / kBlock digits each).
+__device__ inline void digit_bases(const uint32_t *__restrict__ tot, uint32_t bins, uint32_t *bb) {
+    __shared__ uint32_t part[kBlock];
+    constexpr uint32_t kPer = kSortMaxBins / kBlock;
+    const uint32_t t = threadIdx.x;
+    uint32_t v[kPer], sum = 0;
+#pragma unroll
+    for (uint32_t q = 0; q < kPer; ++q) {
+        const uint32_t b = t * kPer + q;
+        v[q] = b < bins ? tot[b] : 0u;
+        sum += v[q];
+    }
+    part[t] = sum;
+    __syncthreads();
+    for (uint32_t off = 1; off < kBlock; off <<= 1) {   // inclusive scan of the partial sums
+        const uint32_t add = t >= off ? part[t - off] : 0u;
+        __syncthreads();
+        part[t] += add;
+        __syncthreads();
+    }
+    uint32_t run = part[t] - sum;
+#pragma unroll
+    for (uint32_t q = 0; q < kPer; ++q) {
+        const uint32_t b = t * kPer + q;
+        if (b < bins) bb[b] = run;
+        run += v[q];
+    }
+    __syncthreads();
+}
+
+// Lanes of the calling wavefront in `valid` whose digit equals this lane's
+// (the digit's bits compared one ballot at a time).
+__device__ inline uint64_t digit_peers(uint32_t d, uint32_t bits, uint64_t valid) {
+    uint64_t m = valid;
+    for (uint32_t j = 0; j < bits; ++j) {
+        const bool bit = (d >> j) & 1u;
+        const uint64_t b = __builtin_amdgcn_ballot_w64(bit);
+        m &= bit ? b : ~b;
+    }
+    return m;
+}
+
+// Scatter of one pass.  ASSEMBLE: the keys are the prefill-order keys of
+// the hash-order positions; each element writes its scoring records (from
+// hrec, scanned and crec at its position) at its output position, and the
+// kHotPad records past the batch are written too.  Otherwise (key, value)
+// pairs move to kout / vout.
+template <bool ASSEMBLE>
+__global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__restrict__ kin,
+                                                              const uint32_t *__restrict__ vin, uint32_t n,
+                                                              uint32_t shift, uint32_t bits, uint32_t ntile,
+                                                              const uint32_t *__restrict__ cnt,
+                                                              const uint32_t *__restrict__ tot,
+                                                              uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
+                                                              const Pre *__restrict__ hrec,
+                                                              const uint64_t *__restrict__ scanned,
+                                                              const Cold *__restrict__ crec, uint32_t bt,
+                                                              uint32_t lstride, uint32_t zrow, Hot *__restrict__ hot,
+                                                              Cold *__restrict__ cold) {
+    __shared__ uint32_t bases[kWavesPerBlock * kSortMaxBins];
+    __shared__ uint32_t bb[kSortMaxBins];
+    const uint32_t bins = 1u << bits, mask = bins - 1;
+    digit_bases(tot, bins, bb);
+    const uint32_t w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const uint32_t tile = blockIdx.x * kWavesPerBlock + w;
+    uint32_t *base = bases + w * bins;
+    if (tile < ntile)
+        for (uint32_t b = lane; b < bins; b += kWave) base[b] = bb[b] + cnt[(uint64_t)tile * bins + b];
+    if (ASSEMBLE && blockIdx.x == 0 && threadIdx.x < kHotPad) hot[(uint64_t)n + threadIdx.x] = Hot{0, zrow, 0, 0};
+    __syncthreads();
+    if (tile >= ntile) return;
+    const uint64_t e0 = (uint64_t)tile * kSortTile + lane;
+    uint32_t kr[kSortSteps], dst[kSortSteps];
+#pragma unroll
+    for (uint32_t x = 0; x < kSortSteps; ++x) {
+        const uint64_t e = e0 + (uint64_t)x * kWave;
+        kr[x] = e < n ? kin[e] : 0u;
+    }
+    // output positions, step by step (the digit bases carry over)
+#pragma unroll
+    for (uint32_t x = 0; x < kSortSteps; ++x) {
+        const bool valid = e0 + (uint64_t)x * kWave < n;
+        const uint32_t d = (kr[x] >> shift) & mask;
+        const uint64_t peers = digit_peers(d, bits, __builtin_amdgcn_ballot_w64(valid));
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+        const uint32_t at = base[d];
+        if (valid && lane == (uint32_t)__builtin_ctzll(peers)) base[d] = at + (uint32_t)__builtin_popcountll(peers);
+        dst[x] = at + rank;
+    }
+    // the moves, independent of each other
+#pragma unroll
+    for (uint32_t x = 0; x < kSortSteps; ++x) {
+        const uint64_t e = e0 + (uint64_t)x * kWave;
+        if (e < n) {
+            const uint32_t o = dst[x];
+            if (ASSEMBLE) {
+                hot[o] = make_hot(hrec[e], scanned[e], bt, lstride, zrow);
+                cold[o] = crec[e];
+            } else {
+                kout[o] = kr[x];
+                vout[o] = vin[e];
+            }
+        }
+    }
 }
 
 // Read-only data that is uniform across a wavefront (request records, hash
@@ -640,12 +815,7 @@ __device__ inline Hot load_hot(const Hot *base, uint32_t i) {
 }
 
 __device__ inline Cold load_cold(const Cold *base, uint32_t i) {
-    const cptr<uint32_t> w = as_const((const uint32_t *)(base + i));
-    Cold x;
-    x.a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
-    x.r = w[2];
-    x.n = w[3];
-    return x;
+    return Cold{as_const((const uint32_t *)base)[i]};
 }
 
 // Lane masks of a wavefront: ballot turns a per-lane predicate into a
@@ -838,6 +1008,7 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
                                                        const float *__restrict__ lead_lam, uint32_t lead_rows,
                                                        const uint64_t *__restrict__ hashes,
                                                        const uint32_t *__restrict__ len_tokens,
+                                                       const uint64_t *__restrict__ hash_off,
                                                        const uint32_t *__restrict__ n_valid, uint32_t n_req,
                                                        uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
                                                        uint64_t *__restrict__ partial, PairOut po) {
@@ -931,8 +1102,10 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
             uint32_t cb[C];
             if ((int32_t)c0.lams < 0) {
                 // matched on its own from block 0, in integers (exact)
-                const Cold k = load_cold(cold, i);
-                const uint32_t len = as_const(len_tokens)[k.r];
+                const uint32_t r = load_cold(cold, i).r;
+                const uint32_t len = as_const(len_tokens)[r];
+                const uint64_t ha = as_const(hash_off)[r];
+                const uint32_t hn = (uint32_t)(as_const(hash_off)[r + 1] - ha);
                 lmask alive[C];
                 uint32_t lam[C];
 #pragma unroll
@@ -940,8 +1113,8 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
                     lam[q] = 0;
                     alive[q] = ~0ull;
                 }
-                if (k.n)
-                    probe_from<W, C>(t, base, chash + k.a, k.n, 0, alive, lam, bt, holder_uniform(t, chash[k.a]));
+                if (hn)
+                    probe_from<W, C>(t, base, chash + ha, hn, 0, alive, lam, bt, holder_uniform(t, chash[ha]));
 #pragma unroll
                 for (int q = 0; q < C; ++q) {
                     const uint32_t x = len - lam[q];
@@ -1657,7 +1830,6 @@ struct netkv_ctx {
     // scratch
     uint32_t *errword = nullptr;          // request / selection errors (sticky)
     uint32_t *loadword = nullptr;         // validation flags of the load calls
-    uint32_t *zflag = nullptr;            // a batch hash array holds the value 0
     uint16_t *jT = nullptr;
     uint64_t jT_bytes = 0;
     int32_t *base_idx = nullptr;
@@ -1686,6 +1858,11 @@ struct netkv_ctx {
     unsigned int *n_lead = nullptr;
     void *sort_tmp = nullptr;
     size_t sort_tmp_bytes = 0;
+    // the batch sorts' own scratch (batches of up to kSortMaxN requests)
+    uint32_t *sort_cnt = nullptr;   // [tiles][kSortMaxBins] digit counts, then offsets
+    uint32_t *sort_seg = nullptr;   // [kSortSegs][kSortMaxBins] segment sums
+    uint32_t *sort_tot = nullptr;   // [kSortMaxBins] digit totals
+    uint32_t *keys_tmp = nullptr, *vals_tmp = nullptr;   // ping-pong buffers of the passes
     uint64_t *partial = nullptr;
     uint64_t partial_cap = 0;
     // options
@@ -1853,13 +2030,12 @@ netkv_status ready(netkv_handle h) {
 constexpr uint32_t kLcpLanes = 8;   // lanes per hash-order position in order_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
-// Radix sort configuration of the batch-order keys: rocPRIM's tuned kernels,
-// with its merge-sort path limited to batches of at most 2^16 requests
-// (rocPRIM's own limit is 2^20).  Above the limit the onesweep radix sort
-// takes one pass per 8 key bits, so the prefill order (11 bits for 1,024
-// prefills) takes two; measured on MI355X at 2^20 requests, 91 us against
-// 150 us for the block sort and twenty merge passes, while the 32-bit hash
-// order takes about 165 us either way.
+// rocPRIM's radix sorts of the batch-order keys (batches outside the range
+// of the own batch sort): its tuned kernels, with the merge-sort path
+// limited to 2^16 items (rocPRIM's own limit is 2^20).  Above the limit
+// the onesweep radix sort takes one pass per 8 key bits; measured on
+// MI355X at 2^20 requests, 91 us for the 11-bit prefill order against
+// 150 us for the block sort and twenty merge passes.
 using SortConfig = rocprim::radix_sort_config<rocprim::default_config, rocprim::default_config,
                                               rocprim::default_config, (size_t)1 << 16>;
 
@@ -1886,6 +2062,7 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
         dfree(h->hrec); dfree(h->crec);
         dfree(h->sort_tmp);
+        dfree(h->sort_cnt); dfree(h->sort_seg); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
         h->order_cap = 0;
         h->sort_tmp_bytes = 0;
         if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
@@ -1909,6 +2086,14 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         if (dalloc(tmp, bytes) != hipSuccess) return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
         h->sort_tmp = tmp;
         h->sort_tmp_bytes = bytes;
+        if (R <= kSortMaxN) {
+            const uint64_t ntile = (R + kSortTile - 1) / kSortTile;
+            if (dalloc(h->sort_cnt, ntile * kSortMaxBins) != hipSuccess ||
+                dalloc(h->sort_seg, (uint64_t)kSortSegs * kSortMaxBins) != hipSuccess ||
+                dalloc(h->sort_tot, kSortMaxBins) != hipSuccess || dalloc(h->keys_tmp, R) != hipSuccess ||
+                dalloc(h->vals_tmp, R) != hipSuccess)
+                return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
+        }
         h->order_cap = R;
     }
     if (!h->n_valid && dalloc(h->n_valid, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
@@ -1946,6 +2131,52 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         h->partial_cap = partial_elems;
     }
     return NETKV_OK;
+}
+
+// One pass of the batch sort over key bits [shift, shift + bits): counts,
+// offsets, scatter (ASSEMBLE: the prefill order's scoring records).
+template <bool ASSEMBLE>
+hipError_t sort_pass(netkv_handle h, const uint32_t *kin, const uint32_t *vin, uint32_t *kout, uint32_t *vout,
+                     uint32_t n, uint32_t shift, uint32_t bits, const Pre *hrec, const uint64_t *scanned,
+                     const Cold *crec, uint32_t lstride, uint32_t zrow, Hot *hot, Cold *cold, hipStream_t st) {
+    if (n == 0) return hipSuccess;
+    const uint32_t ntile = (n + kSortTile - 1) / kSortTile;
+    const uint32_t nseg = std::min(kSortSegs, ntile), seglen = (ntile + nseg - 1) / nseg;
+    const uint32_t wg = (ntile + kWavesPerBlock - 1) / kWavesPerBlock;
+    const uint32_t cols = (nseg << bits);
+    hipLaunchKernelGGL(sort_count_kernel, dim3(wg), dim3(kBlock), 0, st, kin, n, shift, bits, ntile, h->sort_cnt);
+    hipLaunchKernelGGL(sort_segsum_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint32_t *)h->sort_cnt,
+                       ntile, bits, nseg, seglen, h->sort_seg);
+    hipLaunchKernelGGL(sort_offsets_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, h->sort_cnt, ntile, bits,
+                       nseg, seglen, (const uint32_t *)h->sort_seg, h->sort_tot);
+    hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(wg), dim3(kBlock), 0, st, kin, vin, n, shift, bits, ntile,
+                       (const uint32_t *)h->sort_cnt, (const uint32_t *)h->sort_tot, kout, vout, hrec, scanned, crec,
+                       h->block_tokens, lstride, zrow, hot, cold);
+    return hipGetLastError();
+}
+
+// Stable sort of n (key, value) pairs on key bits [0, nbits), in passes of
+// at most kSortMaxBits through the handle's ping-pong buffers; the result
+// lands in kout / vout (n <= kSortMaxN).
+hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
+                            uint32_t *vout, uint32_t n, uint32_t nbits, hipStream_t st) {
+    if (n == 0) return hipSuccess;
+    const uint32_t passes = std::max(1u, (nbits + kSortMaxBits - 1) / kSortMaxBits);
+    uint32_t shift = 0;
+    const uint32_t *sk = kin, *sv = vin;
+    for (uint32_t p = 0; p < passes; ++p) {
+        const uint32_t bits = (nbits - shift + (passes - p) - 1) / (passes - p);   // even split of the rest
+        // the last pass writes kout, the one before the ping-pong buffer, ...
+        const bool to_out = ((passes - 1 - p) % 2) == 0;
+        uint32_t *dk = to_out ? kout : h->keys_tmp, *dv = to_out ? vout : h->vals_tmp;
+        const hipError_t e = sort_pass<false>(h, sk, sv, dk, dv, n, shift, std::max(bits, 1u), nullptr, nullptr,
+                                              nullptr, 0, 0, nullptr, nullptr, st);
+        if (e != hipSuccess) return e;
+        shift += bits;
+        sk = dk;
+        sv = dv;
+    }
+    return hipSuccess;
 }
 
 uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
@@ -1997,12 +2228,12 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
     // and a short loop keeps the kernel's registers for the common path
     if (pairs)
         hipLaunchKernelGGL((score_kernel<K, 1, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, ord.n_valid, rq.n_req, run_len, n_runs,
-                           ngroup, partial, po);
+                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len,
+                           n_runs, ngroup, partial, po);
     else
         hipLaunchKernelGGL((score_kernel<K, 1, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, ord.n_valid, rq.n_req, run_len, n_runs,
-                           ngroup, partial, po);
+                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len,
+                           n_runs, ngroup, partial, po);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return time_end(h, st);
 }
@@ -2050,16 +2281,15 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
                        h->dxlim);
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
-                       h->vals_in, h->errword, h->zflag, h->hv_used, h->n_lead);
-    if (rq.n_hashes)
-        hipLaunchKernelGGL(count_zero_kernel, dim3(grid_for(rq.n_hashes, 256, 8192)), dim3(256), 0, st, rq.hashes,
-                           rq.n_hashes, h->zflag);
-    hipLaunchKernelGGL(zero_fix_kernel, dim3(grid_for((R + 15) / 16, kWavesPerBlock, 2048)), dim3(kBlock), 0, st,
-                       sn, rq, h->keys_in, (const uint32_t *)h->zflag, h->errword);
+                       h->vals_in, h->errword, h->hv_used, h->n_lead);
     HIPCHK(h, hipGetLastError());
     size_t tb = h->sort_tmp_bytes;
-    HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
-                                                    (uint32_t)R, 0, 32, st));
+    const bool own_sort = R > kSortMinN && R <= kSortMaxN;
+    if (own_sort)
+        HIPCHK(h, batch_sort_pairs(h, h->keys_in, h->vals_in, h->keys_out, h->perm, (uint32_t)R, 32, st));
+    else
+        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
+                                                        (uint32_t)R, 0, 32, st));
     // leaders (and holder values of their blocks) the table takes this call
     const uint32_t lcap = h->lead_cap_opt ? std::min(h->lead_cap, h->lead_cap_opt) : h->lead_cap;
     const uint64_t hvcap = h->lead_cap_opt ? std::min<uint64_t>(h->hv_cap, h->lead_cap_opt) : h->hv_cap;
@@ -2073,14 +2303,23 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     HIPCHK(h, hipGetLastError());
     tb = h->sort_tmp_bytes;
     HIPCHK(h, rocprim::inclusive_scan(h->sort_tmp, tb, (const uint64_t *)h->seg, h->scanned, (size_t)R, SegOp(), st));
-    tb = h->sort_tmp_bytes;
-    HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
-                                                    (uint32_t)R, 0, bits_for(h->P), st));
+    // prefill order (stable: the hash order within each prefill) and the
+    // scoring records in it
     const uint32_t lstride = h->D * (uint32_t)sizeof(float);
-    hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st, (uint32_t)R,
-                       h->block_tokens, lstride, h->lead_cap * lstride, (const uint32_t *)h->pord,
-                       (const uint64_t *)h->scanned, (const Pre *)h->hrec, (const Cold *)h->crec, h->hot, h->cold);
-    HIPCHK(h, hipGetLastError());
+    const uint32_t pbits = bits_for(h->P);
+    if (own_sort && pbits <= kSortMaxBits) {
+        HIPCHK(h, sort_pass<true>(h, h->pkey, nullptr, nullptr, nullptr, (uint32_t)R, 0, pbits, h->hrec,
+                                  h->scanned, h->crec, lstride, h->lead_cap * lstride, h->hot, h->cold, st));
+    } else {
+        tb = h->sort_tmp_bytes;
+        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
+                                                        (uint32_t)R, 0, pbits, st));
+        hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st,
+                           (uint32_t)R, h->block_tokens, lstride, h->lead_cap * lstride, (const uint32_t *)h->pord,
+                           (const uint64_t *)h->scanned, (const Pre *)h->hrec, (const Cold *)h->crec, h->hot,
+                           h->cold);
+        HIPCHK(h, hipGetLastError());
+    }
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{h->hot, h->cold, h->lead_lam, h->hv, h->n_valid, lcap};
@@ -2116,7 +2355,6 @@ netkv_status netkv_create(netkv_handle *out, int device) {
     h->device = device;
     DeviceGuard g(device);
     if (dalloc(h->errword, 1) != hipSuccess || dalloc(h->loadword, 1) != hipSuccess ||
-        dalloc(h->zflag, 1) != hipSuccess ||
         hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess) {
         netkv_destroy(h);
         return NETKV_EDEVICE;
@@ -2145,7 +2383,6 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->bits);
         dfree(h->errword);
         dfree(h->loadword);
-        dfree(h->zflag);
         dfree(h->jT);
         dfree(h->base_idx);
         dfree(h->base_score);
@@ -2154,6 +2391,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->bytes);
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial); dfree(h->hv); dfree(h->hv_used);
+        dfree(h->sort_cnt); dfree(h->sort_seg); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
         dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
         dfree(h->lead); dfree(h->lead_lam); dfree(h->n_lead); dfree(h->hrec); dfree(h->crec);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
@@ -2724,8 +2962,12 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     hipLaunchKernelGGL(prefill_key_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s, rq, (uint32_t)P,
                        (const uint32_t *)h->keys_in, h->seq_keys, h->seq_vals);
     size_t tb = h->sort_tmp_bytes;
-    HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals,
-                                                    h->seq_perm, (uint32_t)R, 0, bits_for(P), s));
+    if (R > kSortMinN && R <= kSortMaxN)
+        HIPCHK(h, batch_sort_pairs(h, h->seq_keys, h->seq_vals, h->seq_keys_out, h->seq_perm, (uint32_t)R,
+                                   bits_for(P), s));
+    else
+        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals,
+                                                        h->seq_perm, (uint32_t)R, 0, bits_for(P), s));
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_start, P, 0u);
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_end, P, 0u);
     hipLaunchKernelGGL(segment_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s,

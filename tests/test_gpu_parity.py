@@ -286,6 +286,9 @@ def test_subset_batches_match_full_batch(nk):
 
 
 def test_invalid_requests_are_flagged(nk):
+    """Requests with no such prefill instance or a run length inconsistent
+    with l_r are answered with -1 / NaN and reported; a block hash 0 (which
+    no resident set can hold) is an ordinary miss."""
     _say("invalid requests")
     cfg = W.scaled(W.CONFIGS["c0"], n_requests=64)
     snap, req, cache = _inputs(cfg, 15)
@@ -293,9 +296,11 @@ def test_invalid_requests_are_flagged(nk):
     bad = {k: v.copy() for k, v in req.items() if k in ("prefill", "len_tokens", "hash_off", "hashes")}
     bad["prefill"][3] = 999            # no such prefill instance
     bad["len_tokens"][7] += 512 * 3    # run length inconsistent with l_r
-    i = int(bad["hash_off"][10])
-    if int(bad["hash_off"][11]) > i:
-        bad["hashes"][i] = 0           # reserved hash value
+    # a hash 0 inside the longest run that some decode matches past it
+    o0 = oracle.select(snap, cache, req, k=1, pairs=True)
+    r0 = int(np.argmax(o0["j"].max(axis=1)))
+    assert r0 not in (3, 7) and o0["j"][r0].max() >= 2
+    bad["hashes"][int(bad["hash_off"][r0]) + 1] = 0
     rd = nk.requests_to_device(bad, sel.device)
     out = sel.select(rd, k=2)
     with pytest.raises(nk.NetKVError) as e:
@@ -305,8 +310,9 @@ def test_invalid_requests_are_flagged(nk):
     sc = nk.to_numpy(out["score"]).reshape(-1, 2)
     for r in (3, 7):
         assert (idx[r] == -1).all() and np.isnan(sc[r]).all()
-    good = [r for r in range(64) if r not in (3, 7, 10)]
-    o = oracle.select(snap, cache, subset_requests(req, good), k=2, pairs=True)
+    good = [r for r in range(64) if r not in (3, 7)]
+    o = oracle.select(snap, cache, subset_requests(bad, good), k=2, pairs=True)
+    assert o["j"][good.index(r0)].max() == 1
     check_topk(idx[good], sc[good], o["idx"], o["cost"], o["feasible"])
     sel.sync_errors()  # cleared
     sel.close()
@@ -452,8 +458,8 @@ def test_long_runs_and_invalid_requests_in_every_mode(nk):
     """Runs longer than 65535 blocks (B_tok = 1): the batch selection scores
     them exactly and writes prefix lengths saturated at 65535; the ranking
     sweep and the sequential form, which keep prefix lengths in 16 bits,
-    answer them (and a request holding the reserved hash 0) with -1 / NaN
-    and report them."""
+    answer them (and a request whose run length contradicts l_r, in every
+    mode) with -1 / NaN and report them.  A block hash 0 ends a match."""
     _say("long runs, B_tok 1")
     cfg = W.scaled(W.CONFIGS["c0"], n_requests=6, block_tokens=1)
     snap = W.make_snapshot(cfg, 21)
@@ -468,7 +474,9 @@ def test_long_runs_and_invalid_requests_in_every_mode(nk):
     runs = [chain, np.concatenate([chain, rng.integers(1, 2**63, 500, dtype=np.uint64)]),
             chain[:1000], rng.integers(1, 2**63, 900, dtype=np.uint64), chain[:40],
             np.concatenate([chain[:50], rng.integers(1, 2**63, 65950, dtype=np.uint64)])]
-    runs[3][17] = 0   # reserved value: request 3 is invalid everywhere
+    lens[3] += 1        # run length != l_r / B_tok: request 3 is invalid everywhere
+    runs[2] = runs[2].copy()
+    runs[2][500] = 0    # resident nowhere: request 2 matches 500 blocks on decode 0
     req = dict(n_req=6, prefill=rng.integers(0, cfg.n_prefill, 6).astype(np.uint32), len_tokens=lens,
                hash_off=np.concatenate([[0], np.cumsum([len(x) for x in runs])]).astype(np.uint64),
                hashes=np.concatenate(runs).astype(np.uint64))
@@ -481,7 +489,7 @@ def test_long_runs_and_invalid_requests_in_every_mode(nk):
     sc = nk.to_numpy(out["score"]).reshape(-1, 2)
     good = [0, 1, 2, 4, 5]
     o = oracle.select(snap, cache, subset_requests(req, good), k=2, pairs=True)
-    assert int(o["j"][0, 0]) == 70000 and int(o["j"][1, 0]) == 70000
+    assert int(o["j"][0, 0]) == 70000 and int(o["j"][1, 0]) == 70000 and int(o["j"][2, 0]) == 500
     check_topk(idx[good], sc[good], o["idx"], o["cost"], o["feasible"])
     j = nk.to_numpy(out["pairs"]["prefix_blocks"]).reshape(6, D)[good].astype(np.int64)
     assert np.array_equal(j, np.minimum(o["j"], 65535))
@@ -497,7 +505,7 @@ def test_long_runs_and_invalid_requests_in_every_mode(nk):
     si = nk.to_numpy(sw["idx"]).reshape(-1, 2)
     ss = nk.to_numpy(sw["score"]).reshape(-1, 2)
     qi, qs = nk.to_numpy(sq["idx"]), nk.to_numpy(sq["score"])
-    for r in (0, 1, 3, 5):   # more than 65535 blocks, or a zero hash
+    for r in (0, 1, 3, 5):   # more than 65535 blocks, or an invalid run length
         assert (si[r] == -1).all() and np.isnan(ss[r]).all()
         assert qi[r] == -1 and np.isnan(qs[r])
     for r in (2, 4):
