@@ -827,6 +827,14 @@ using lmask = uint64_t;
 __device__ inline lmask ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 __device__ inline bool in_mask(lmask m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
 
+// v_writelane: lane `l` (uniform) of `old` takes the uniform value `v`, the
+// other lanes keep theirs.  The compiler offers no builtin for it, so the
+// intrinsic is declared by its name.
+extern "C" __device__ int amdgcn_writelane(int v, int l, int old) __asm("llvm.amdgcn.writelane.i32");
+__device__ inline uint32_t write_lane(uint32_t v, uint32_t l, uint32_t old) {
+    return (uint32_t)amdgcn_writelane((int)v, (int)l, (int)old);
+}
+
 // Holder value of a hash that is the same on every lane (scalar loads of
 // both candidate buckets' keys and values).
 __device__ inline uint32_t holder_uniform(const Table &t, uint64_t h) {
@@ -1181,10 +1189,8 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
                         break;
                     }
                 }
-                if (lane == slot * K + (uint32_t)r) {
-                    pc_bits = mn;
-                    pc_idx = dm;
-                }
+                pc_bits = write_lane(mn, slot * K + (uint32_t)r, pc_bits);
+                pc_idx = write_lane(dm, slot * K + (uint32_t)r, pc_idx);
             }
             if (nl) {
 #pragma unroll
