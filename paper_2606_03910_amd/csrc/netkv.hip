@@ -594,50 +594,49 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
 
 // ---------------------------------------------------------------- batch sorts
 //
-// Stable LSD radix sort for the batch orders (batches of up to kSortMaxN):
-// tiles of kSortTile positions, one wavefront each, four per workgroup.
-// A pass over `bits` digit bits (at most 11) takes four kernels:
+// Stable LSD radix sort for the batch orders (batches of kSortMinN + 1 to
+// kSortMaxN): tiles of kSortTile positions, one workgroup each, in passes
+// of at most kSortMaxBits digit bits.  A pass takes four kernels:
 // sort_count_kernel counts each tile's digits into cnt[tile][digit];
 // sort_segsum_kernel and sort_offsets_kernel turn every digit's column into
 // exclusive offsets over the tiles (in place; the column is cut into at
 // most kSortSegs segments, summed first) and write the digit totals;
-// sort_scatter_kernel adds the digit bases (an exclusive scan of the
-// totals) and each tile writes its elements in order, 64 at a time,
-// ranking equal digits within the 64 by lane masks.  Equal keys keep
+// sort_scatter_kernel ranks the tile's elements (each wavefront a quarter
+// of the tile, 64 at a time, equal digits ranked by lane masks), stages
+// them in LDS in output order and writes them out in that order, so that
+// the elements of one digit leave as a contiguous run.  Equal keys keep
 // their order (stable), which the prefill order relies on.
-constexpr uint32_t kSortTile = 1024;
-constexpr uint32_t kSortMaxBits = 11;
+constexpr uint32_t kSortTile = 4096;
+constexpr uint32_t kSortPer = kSortTile / kBlock;                          // positions per thread
+constexpr uint32_t kSortQuarter = kSortTile / kWavesPerBlock;              // positions per wavefront
+constexpr uint32_t kSortSteps = kSortQuarter / kWave;                      // 64-position steps of a wavefront
+constexpr uint32_t kSortMaxBits = 8;
 constexpr uint32_t kSortMaxBins = 1u << kSortMaxBits;
 constexpr uint64_t kSortMaxN = 1ull << 24;
 constexpr uint64_t kSortMinN = 1ull << 16;   // smaller batches: rocPRIM (fewer launches)
 constexpr uint32_t kSortSegs = 32;
-constexpr uint32_t kSortSteps = kSortTile / kWave;   // 64-element steps of a tile
+static_assert(kSortMaxBins <= kBlock, "one thread per digit");
 
 __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__restrict__ keys, uint32_t n,
-                                                            uint32_t shift, uint32_t bits, uint32_t ntile,
+                                                            uint32_t shift, uint32_t bits,
                                                             uint32_t *__restrict__ cnt) {
-    __shared__ uint32_t hs[kWavesPerBlock * kSortMaxBins];
+    __shared__ uint32_t h[kSortMaxBins];
     const uint32_t bins = 1u << bits, mask = bins - 1;
-    for (uint32_t b = threadIdx.x; b < kWavesPerBlock * bins; b += blockDim.x) hs[b] = 0;
+    const uint32_t tid = threadIdx.x;
+    if (tid < bins) h[tid] = 0;
     __syncthreads();
-    const uint32_t w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const uint32_t tile = blockIdx.x * kWavesPerBlock + w;
-    uint32_t *h = hs + w * bins;
-    if (tile < ntile) {
-        const uint64_t e0 = (uint64_t)tile * kSortTile + lane;
-        uint32_t kr[kSortSteps];   // the lane's keys, all loads issued first
+    const uint64_t e0 = (uint64_t)blockIdx.x * kSortTile + tid;
+    uint32_t kr[kSortPer];   // the thread's keys, all loads issued first
 #pragma unroll
-        for (uint32_t x = 0; x < kSortSteps; ++x) {
-            const uint64_t e = e0 + (uint64_t)x * kWave;
-            kr[x] = e < n ? keys[e] : 0u;
-        }
-#pragma unroll
-        for (uint32_t x = 0; x < kSortSteps; ++x)
-            if (e0 + (uint64_t)x * kWave < n) atomicAdd(h + ((kr[x] >> shift) & mask), 1u);
+    for (uint32_t x = 0; x < kSortPer; ++x) {
+        const uint64_t e = e0 + (uint64_t)x * kBlock;
+        kr[x] = e < n ? keys[e] : 0u;
     }
+#pragma unroll
+    for (uint32_t x = 0; x < kSortPer; ++x)
+        if (e0 + (uint64_t)x * kBlock < n) atomicAdd(h + ((kr[x] >> shift) & mask), 1u);
     __syncthreads();
-    if (tile < ntile)
-        for (uint32_t b = lane; b < bins; b += kWave) cnt[(uint64_t)tile * bins + b] = h[b];
+    if (tid < bins) cnt[(uint64_t)blockIdx.x * bins + tid] = h[tid];
 }
 
 // One thread per (segment, digit): the segment's sum of the digit's
@@ -685,34 +684,21 @@ __global__ __launch_bounds__(256) void sort_offsets_kernel(uint32_t *__restrict_
     if (sg == nseg - 1) tot[b] = run;
 }
 
-// Exclusive scan of the digit totals into LDS (bins <= kSortMaxBins, a
-// block of kBlock threads, kSortMaxBins / kBlock digits each).
+// Exclusive scan of the digit totals into bb (bins <= kBlock, one digit
+// per thread).
 __device__ inline void digit_bases(const uint32_t *__restrict__ tot, uint32_t bins, uint32_t *bb) {
     __shared__ uint32_t part[kBlock];
-    constexpr uint32_t kPer = kSortMaxBins / kBlock;
     const uint32_t t = threadIdx.x;
-    uint32_t v[kPer], sum = 0;
-#pragma unroll
-    for (uint32_t q = 0; q < kPer; ++q) {
-        const uint32_t b = t * kPer + q;
-        v[q] = b < bins ? tot[b] : 0u;
-        sum += v[q];
-    }
-    part[t] = sum;
+    const uint32_t v = t < bins ? tot[t] : 0u;
+    part[t] = v;
     __syncthreads();
-    for (uint32_t off = 1; off < kBlock; off <<= 1) {   // inclusive scan of the partial sums
+    for (uint32_t off = 1; off < kBlock; off <<= 1) {   // inclusive scan
         const uint32_t add = t >= off ? part[t - off] : 0u;
         __syncthreads();
         part[t] += add;
         __syncthreads();
     }
-    uint32_t run = part[t] - sum;
-#pragma unroll
-    for (uint32_t q = 0; q < kPer; ++q) {
-        const uint32_t b = t * kPer + q;
-        if (b < bins) bb[b] = run;
-        run += v[q];
-    }
+    if (t < bins) bb[t] = part[t] - v;
     __syncthreads();
 }
 
@@ -728,15 +714,15 @@ __device__ inline uint64_t digit_peers(uint32_t d, uint32_t bits, uint64_t valid
     return m;
 }
 
-// Scatter of one pass.  ASSEMBLE: the keys are the prefill-order keys of
-// the hash-order positions; each element writes its scoring records (from
-// hrec, scanned and crec at its position) at its output position, and the
-// kHotPad records past the batch are written too.  Otherwise (key, value)
-// pairs move to kout / vout.
+// Scatter of one pass.  The values are vin's, or the input positions when
+// vin is null.  ASSEMBLE: the values are hash-order positions and each
+// element writes its scoring records (from hrec, scanned and crec at that
+// position) at its output position; the kHotPad records past the batch
+// are written too.  Otherwise (key, value) pairs go to kout / vout.
 template <bool ASSEMBLE>
 __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__restrict__ kin,
                                                               const uint32_t *__restrict__ vin, uint32_t n,
-                                                              uint32_t shift, uint32_t bits, uint32_t ntile,
+                                                              uint32_t shift, uint32_t bits,
                                                               const uint32_t *__restrict__ cnt,
                                                               const uint32_t *__restrict__ tot,
                                                               uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
@@ -745,49 +731,89 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
                                                               const Cold *__restrict__ crec, uint32_t bt,
                                                               uint32_t lstride, uint32_t zrow, Hot *__restrict__ hot,
                                                               Cold *__restrict__ cold) {
-    __shared__ uint32_t bases[kWavesPerBlock * kSortMaxBins];
-    __shared__ uint32_t bb[kSortMaxBins];
+    __shared__ uint32_t bb[kSortMaxBins];                     // the tile's first output position per digit
+    __shared__ uint32_t hist[kWavesPerBlock][kSortMaxBins];   // per-wavefront counts, then their prefixes
+    __shared__ uint32_t toff[kSortMaxBins];                   // first staging slot per digit
+    __shared__ uint32_t sk[kSortTile], sv[kSortTile];         // keys and values in output order
     const uint32_t bins = 1u << bits, mask = bins - 1;
+    const uint32_t tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const uint64_t t0 = (uint64_t)blockIdx.x * kSortTile;
     digit_bases(tot, bins, bb);
-    const uint32_t w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const uint32_t tile = blockIdx.x * kWavesPerBlock + w;
-    uint32_t *base = bases + w * bins;
-    if (tile < ntile)
-        for (uint32_t b = lane; b < bins; b += kWave) base[b] = bb[b] + cnt[(uint64_t)tile * bins + b];
-    if (ASSEMBLE && blockIdx.x == 0 && threadIdx.x < kHotPad) hot[(uint64_t)n + threadIdx.x] = Hot{0, zrow, 0, 0};
-    __syncthreads();
-    if (tile >= ntile) return;
-    const uint64_t e0 = (uint64_t)tile * kSortTile + lane;
-    uint32_t kr[kSortSteps], dst[kSortSteps];
+    if (tid < bins) bb[tid] += cnt[(uint64_t)blockIdx.x * bins + tid];
+    for (uint32_t b = lane; b < bins; b += kWave) hist[w][b] = 0;
+    if (ASSEMBLE && blockIdx.x == 0 && tid < kHotPad) hot[(uint64_t)n + tid] = Hot{0, zrow, 0, 0};
+    // this wavefront's quarter of the tile: keys and values, loads first
+    const uint64_t e0 = t0 + (uint64_t)w * kSortQuarter + lane;
+    uint32_t kr[kSortSteps], vr[kSortSteps], rk[kSortSteps];
 #pragma unroll
     for (uint32_t x = 0; x < kSortSteps; ++x) {
         const uint64_t e = e0 + (uint64_t)x * kWave;
         kr[x] = e < n ? kin[e] : 0u;
+        vr[x] = e < n ? (vin ? vin[e] : (uint32_t)e) : 0u;
     }
-    // output positions, step by step (the digit bases carry over)
+    __syncthreads();
+    // rank within the wavefront's quarter, step by step
 #pragma unroll
     for (uint32_t x = 0; x < kSortSteps; ++x) {
         const bool valid = e0 + (uint64_t)x * kWave < n;
         const uint32_t d = (kr[x] >> shift) & mask;
         const uint64_t peers = digit_peers(d, bits, __builtin_amdgcn_ballot_w64(valid));
-        const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
-                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
-        const uint32_t at = base[d];
-        if (valid && lane == (uint32_t)__builtin_ctzll(peers)) base[d] = at + (uint32_t)__builtin_popcountll(peers);
-        dst[x] = at + rank;
+        const uint32_t at = hist[w][d];
+        if (valid && lane == (uint32_t)__builtin_ctzll(peers)) hist[w][d] = at + (uint32_t)__builtin_popcountll(peers);
+        rk[x] = at + __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
     }
-    // the moves, independent of each other
+    __syncthreads();
+    // per digit: the wavefronts' prefixes (in place) and the tile count
+    if (tid < bins) {
+        uint32_t run = 0;
+#pragma unroll
+        for (uint32_t q = 0; q < kWavesPerBlock; ++q) {
+            const uint32_t c = hist[q][tid];
+            hist[q][tid] = run;
+            run += c;
+        }
+        toff[tid] = run;
+    }
+    __syncthreads();
+    // exclusive scan of the tile counts over the digits
+    {
+        const uint32_t v = tid < bins ? toff[tid] : 0u;
+        for (uint32_t off = 1; off < bins; off <<= 1) {
+            const uint32_t add = (tid < bins && tid >= off) ? toff[tid - off] : 0u;
+            __syncthreads();
+            if (tid < bins) toff[tid] += add;
+            __syncthreads();
+        }
+        if (tid < bins) toff[tid] -= v;
+        __syncthreads();
+    }
+    // stage in output order
 #pragma unroll
     for (uint32_t x = 0; x < kSortSteps; ++x) {
-        const uint64_t e = e0 + (uint64_t)x * kWave;
-        if (e < n) {
-            const uint32_t o = dst[x];
+        if (e0 + (uint64_t)x * kWave < n) {
+            const uint32_t d = (kr[x] >> shift) & mask;
+            const uint32_t pos = toff[d] + hist[w][d] + rk[x];
+            sk[pos] = kr[x];
+            sv[pos] = vr[x];
+        }
+    }
+    __syncthreads();
+    // write out in output order: one digit's elements are consecutive
+    const uint32_t nt = n - t0 < (uint64_t)kSortTile ? (uint32_t)(n - t0) : kSortTile;
+#pragma unroll
+    for (uint32_t x = 0; x < kSortPer; ++x) {
+        const uint32_t j = x * kBlock + tid;
+        if (j < nt) {
+            const uint32_t k = sk[j];
+            const uint32_t d = (k >> shift) & mask;
+            const uint32_t o = bb[d] + (j - toff[d]);
             if (ASSEMBLE) {
+                const uint32_t e = sv[j];
                 hot[o] = make_hot(hrec[e], scanned[e], bt, lstride, zrow);
                 cold[o] = crec[e];
             } else {
-                kout[o] = kr[x];
-                vout[o] = vin[e];
+                kout[o] = k;
+                vout[o] = sv[j];
             }
         }
     }
@@ -2148,39 +2174,75 @@ hipError_t sort_pass(netkv_handle h, const uint32_t *kin, const uint32_t *vin, u
     if (n == 0) return hipSuccess;
     const uint32_t ntile = (n + kSortTile - 1) / kSortTile;
     const uint32_t nseg = std::min(kSortSegs, ntile), seglen = (ntile + nseg - 1) / nseg;
-    const uint32_t wg = (ntile + kWavesPerBlock - 1) / kWavesPerBlock;
-    const uint32_t cols = (nseg << bits);
-    hipLaunchKernelGGL(sort_count_kernel, dim3(wg), dim3(kBlock), 0, st, kin, n, shift, bits, ntile, h->sort_cnt);
+    const uint32_t cols = nseg << bits;
+    hipLaunchKernelGGL(sort_count_kernel, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits, h->sort_cnt);
     hipLaunchKernelGGL(sort_segsum_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint32_t *)h->sort_cnt,
                        ntile, bits, nseg, seglen, h->sort_seg);
     hipLaunchKernelGGL(sort_offsets_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, h->sort_cnt, ntile, bits,
                        nseg, seglen, (const uint32_t *)h->sort_seg, h->sort_tot);
-    hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(wg), dim3(kBlock), 0, st, kin, vin, n, shift, bits, ntile,
+    hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(ntile), dim3(kBlock), 0, st, kin, vin, n, shift, bits,
                        (const uint32_t *)h->sort_cnt, (const uint32_t *)h->sort_tot, kout, vout, hrec, scanned, crec,
                        h->block_tokens, lstride, zrow, hot, cold);
     return hipGetLastError();
 }
 
-// Stable sort of n (key, value) pairs on key bits [0, nbits), in passes of
-// at most kSortMaxBits through the handle's ping-pong buffers; the result
-// lands in kout / vout (n <= kSortMaxN).
+// Bits of pass p of `passes` even passes over nbits key bits, and its shift.
+inline void pass_bits(uint32_t nbits, uint32_t passes, uint32_t p, uint32_t &shift, uint32_t &bits) {
+    shift = 0;
+    for (uint32_t q = 0; q <= p; ++q) {
+        bits = (nbits - shift + (passes - q) - 1) / (passes - q);
+        if (q < p) shift += bits;
+    }
+    bits = std::max(bits, 1u);
+}
+
+// Stable sort of n (key, value) pairs on key bits [0, nbits) (values: vin,
+// or the input positions when vin is null), in passes of at most
+// kSortMaxBits through the handle's ping-pong buffers; the result lands in
+// kout / vout (kSortMinN < n <= kSortMaxN).
 hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
                             uint32_t *vout, uint32_t n, uint32_t nbits, hipStream_t st) {
     if (n == 0) return hipSuccess;
     const uint32_t passes = std::max(1u, (nbits + kSortMaxBits - 1) / kSortMaxBits);
-    uint32_t shift = 0;
     const uint32_t *sk = kin, *sv = vin;
     for (uint32_t p = 0; p < passes; ++p) {
-        const uint32_t bits = (nbits - shift + (passes - p) - 1) / (passes - p);   // even split of the rest
-        // the last pass writes kout, the one before the ping-pong buffer, ...
+        uint32_t shift, bits;
+        pass_bits(nbits, passes, p, shift, bits);
+        // the last pass writes kout, the one before the ping-pong buffers, ...
         const bool to_out = ((passes - 1 - p) % 2) == 0;
         uint32_t *dk = to_out ? kout : h->keys_tmp, *dv = to_out ? vout : h->vals_tmp;
-        const hipError_t e = sort_pass<false>(h, sk, sv, dk, dv, n, shift, std::max(bits, 1u), nullptr, nullptr,
-                                              nullptr, 0, 0, nullptr, nullptr, st);
+        const hipError_t e = sort_pass<false>(h, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0, 0,
+                                              nullptr, nullptr, st);
         if (e != hipSuccess) return e;
-        shift += bits;
         sk = dk;
         sv = dv;
+    }
+    return hipSuccess;
+}
+
+// The prefill order: a stable sort of the hash-order positions by the
+// prefill key (pbits <= 2 * kSortMaxBits), whose last pass writes the
+// scoring records at their output positions; earlier passes go through
+// buf_k / buf_v (free at this point of a selection).
+hipError_t prefill_order(netkv_handle h, uint32_t n, uint32_t pbits, uint32_t *buf_k, uint32_t *buf_v,
+                         uint32_t lstride, uint32_t zrow, hipStream_t st) {
+    const uint32_t passes = std::max(1u, (pbits + kSortMaxBits - 1) / kSortMaxBits);
+    const uint32_t *sk = h->pkey, *sv = nullptr;
+    for (uint32_t p = 0; p < passes; ++p) {
+        uint32_t shift, bits;
+        pass_bits(pbits, passes, p, shift, bits);
+        hipError_t e;
+        if (p + 1 == passes) {
+            e = sort_pass<true>(h, sk, sv, nullptr, nullptr, n, shift, bits, h->hrec, h->scanned, h->crec, lstride,
+                                zrow, h->hot, h->cold, st);
+        } else {
+            uint32_t *dk = (p % 2) ? buf_k : h->keys_tmp, *dv = (p % 2) ? buf_v : h->vals_tmp;
+            e = sort_pass<false>(h, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0, 0, nullptr,
+                                 nullptr, st);
+            sk = dk;
+            sv = dv;
+        }
+        if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
@@ -2292,7 +2354,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     size_t tb = h->sort_tmp_bytes;
     const bool own_sort = R > kSortMinN && R <= kSortMaxN;
     if (own_sort)
-        HIPCHK(h, batch_sort_pairs(h, h->keys_in, h->vals_in, h->keys_out, h->perm, (uint32_t)R, 32, st));
+        HIPCHK(h, batch_sort_pairs(h, h->keys_in, nullptr, h->keys_out, h->perm, (uint32_t)R, 32, st));
     else
         HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
                                                         (uint32_t)R, 0, 32, st));
@@ -2313,9 +2375,9 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     // scoring records in it
     const uint32_t lstride = h->D * (uint32_t)sizeof(float);
     const uint32_t pbits = bits_for(h->P);
-    if (own_sort && pbits <= kSortMaxBits) {
-        HIPCHK(h, sort_pass<true>(h, h->pkey, nullptr, nullptr, nullptr, (uint32_t)R, 0, pbits, h->hrec,
-                                  h->scanned, h->crec, lstride, h->lead_cap * lstride, h->hot, h->cold, st));
+    if (own_sort && pbits <= 2 * kSortMaxBits) {
+        // (the hash order's keys and permutation are no longer needed)
+        HIPCHK(h, prefill_order(h, (uint32_t)R, pbits, h->keys_out, h->perm, lstride, h->lead_cap * lstride, st));
     } else {
         tb = h->sort_tmp_bytes;
         HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
