@@ -329,6 +329,7 @@ __global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict_
 // prefill, a stable radix sort): consecutive requests share their row of
 // the snapshot and often their leader, so both are re-read from L1.
 
+constexpr uint32_t kKeyLenBits = 12;             // low key bits: 4095 - min(blocks, 4095)
 constexpr uint32_t kKeyEmptyRun = 0x80000000u;   // valid request without blocks
 constexpr uint32_t kKeyInvalid = 0xFFFFFFFFu;
 constexpr uint32_t kNoLead = 0xFFFFFFFFu;        // no leader before the position
@@ -424,7 +425,7 @@ __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max
                 key = kKeyEmptyRun;
             } else {
                 const uint32_t top = (uint32_t)((rq.hashes[a] * kGolden) >> 32);
-                key = ((top >> 13) << 12) | (4095u - (n < 4095u ? n : 4095u));
+                key = ((top >> 13) << kKeyLenBits) | (4095u - (n < 4095u ? n : 4095u));
             }
         }
         keys[r] = key;
@@ -464,7 +465,7 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
     if (sub == 0) {
         if (valid && (i + 1 == rq.n_req || sorted_keys[i + 1] >= kKeyInvalid)) *n_valid = (uint32_t)(i + 1);
         if (i == 0 && !valid) *n_valid = 0;
-        pval[i] = (uint32_t)i;
+        if (pval) pval[i] = (uint32_t)i;
     }
     if (!valid) {
         if (sub == 0) {
@@ -478,7 +479,9 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
     const uint64_t a = rq.off[r];
     const uint64_t nr = rq.off[r + 1] - a;
     uint64_t l = 0;
-    if (i > 0 && reuse) {
+    // keys that differ in their first-block hash bits have different first
+    // blocks: nothing in common
+    if (i > 0 && reuse && (sorted_keys[i] >> kKeyLenBits) == (sorted_keys[i - 1] >> kKeyLenBits)) {
         const uint32_t q = perm[i - 1];
         const uint64_t b = rq.off[q];
         const uint64_t nq = rq.off[q + 1] - b;
@@ -2361,10 +2364,14 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     // leaders (and holder values of their blocks) the table takes this call
     const uint32_t lcap = h->lead_cap_opt ? std::min(h->lead_cap, h->lead_cap_opt) : h->lead_cap;
     const uint64_t hvcap = h->lead_cap_opt ? std::min<uint64_t>(h->hv_cap, h->lead_cap_opt) : h->hv_cap;
+    // the prefill order: the own sort (positions as its values), or rocPRIM's on pval
+    const uint32_t pbits = bits_for(h->P);
+    const bool own_prefill = own_sort && pbits <= 2 * kSortMaxBits;
     hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
                        h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg, h->pkey, h->pval, h->hrec, h->crec,
-                       h->lead, lcap, h->n_lead, hvcap, h->hv_used, h->n_valid);
+                       (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg, h->pkey,
+                       own_prefill ? nullptr : h->pval, h->hrec, h->crec, h->lead, lcap, h->n_lead, hvcap,
+                       h->hv_used, h->n_valid);
     hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((lcap + kWavesPerBlock - 1) /
                                                                              kWavesPerBlock, 4096)),
                        dim3(kBlock), 0, st, t, rq.hashes, h->lead, (const unsigned int *)h->n_lead, lcap, h->hv);
@@ -2374,8 +2381,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     // prefill order (stable: the hash order within each prefill) and the
     // scoring records in it
     const uint32_t lstride = h->D * (uint32_t)sizeof(float);
-    const uint32_t pbits = bits_for(h->P);
-    if (own_sort && pbits <= 2 * kSortMaxBits) {
+    if (own_prefill) {
         // (the hash order's keys and permutation are no longer needed)
         HIPCHK(h, prefill_order(h, (uint32_t)R, pbits, h->keys_out, h->perm, lstride, h->lead_cap * lstride, st));
     } else {
