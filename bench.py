@@ -93,6 +93,11 @@ def main():
                     help="cost rung: 0 full, 1 without live congestion, 2 topology only")
     ap.add_argument("--sequential", action="store_true",
                     help="time the request-by-request form (in-batch in-flight increments, cap 16)")
+    ap.add_argument("--forecast", type=float, default=0.0, metavar="BETA",
+                    help="c1: fold each batch's (stale) congestion observation into the forecast by "
+                         "exponential smoothing with this factor instead of replacing the snapshot's")
+    ap.add_argument("--smooth-bench", action="store_true",
+                    help="only time the congestion smoothing kernel on the workload's P x D matrix")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (K launches) and exit: the "
                          "reference kernel for scaling HBM byte counters")
@@ -121,6 +126,8 @@ def main():
 
     cfg = W.CONFIGS[args.workload]
     dev = torch.device("cuda", 0)
+    if args.smooth_bench:
+        return bench_smooth(args, cfg, dev)
     if args.workload == "c3":
         return bench_sweep(args, cfg, dev)
     if args.workload == "c1":
@@ -437,7 +444,10 @@ def bench_stream(args, cfg, dev):
     def step():
         sel.load_snapshot(snap)
         for t in range(B):
-            netkv.netkv_oracle_set_util(sel.h, utils[max(0, t - 1)], dev)
+            if args.forecast:
+                netkv.netkv_congestion_smooth(sel.h, utils[max(0, t - 1)], args.forecast, dev)
+            else:
+                netkv.netkv_oracle_set_util(sel.h, utils[max(0, t - 1)], dev)
             netkv.netkv_select_batch(sel.h, reqs[t], 1, idx, sc, None, dev)
             netkv.netkv_commit_batch(sel.h, reqs[t], idx, 16, mu, dev)
 
@@ -459,10 +469,59 @@ def bench_stream(args, cfg, dev):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32+u64",
         "data": "synthetic (seeded; AR(1) congestion, staleness 1 batch)",
         "config": {"workload": cfg.name, "requests_per_batch": R, "batches": B, "decodes": D,
-                   "prefills": cfg.n_prefill, "staleness": 1, "parallelism": "single-gpu"},
+                   "prefills": cfg.n_prefill, "staleness": 1, "parallelism": "single-gpu",
+                   "congestion": (f"exponential smoothing, beta {args.forecast}" if args.forecast
+                                  else "replaced by each observation")},
         "roofline": None, "cpu_baseline": None,
         "note": "wall time of the whole stream (snapshot load, per-batch congestion refresh, "
                 "selection and update); small batches are launch- and latency-bound",
+    }
+    print(json.dumps(rec), flush=True)
+    sel.close()
+
+
+def bench_smooth(args, cfg, dev):
+    """Predictive congestion: one step = one smoothing of the P x D
+    congestion matrix towards an observation (12 B per entry: read the
+    forecast and the observation, write the forecast), HBM-bound."""
+    import torch
+
+    from paper_2606_03910_amd import netkv
+    from paper_2606_03910_amd import workload as W
+    snap = W.make_snapshot(cfg, args.seed)
+    sel = netkv.Selector(0)
+    sel.load_snapshot(snap)
+    npd = cfg.n_prefill * cfg.n_decode
+    rng = np.random.default_rng(args.seed)
+    obs = [netkv.to_device(rng.uniform(0, 0.99, npd).astype(np.float32), dev) for _ in range(4)]
+    beta = args.forecast or 0.2
+    for i in range(args.warmup):
+        netkv.netkv_congestion_smooth(sel.h, obs[i % 4], beta, dev)
+    sel.sync_errors()
+    netkv.netkv_set_timing(sel.h, True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        netkv.netkv_congestion_smooth(sel.h, obs[i % 4], beta, dev)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    kern_ms = netkv.netkv_kernel_ms(sel.h)
+    netkv.netkv_set_timing(sel.h, False)
+    sel.sync_errors()
+    nbytes = 12 * npd
+    gbs = nbytes / (kern_ms * 1e-3) / 1e9
+    rec = {
+        "metric": "congestion entries smoothed/s (predictive congestion)",
+        "value": npd / (kern_ms * 1e-3), "unit": "entries/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "kernel_ms": kern_ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded uniform observations)",
+        "config": {"workload": cfg.name + "-congestion-smoothing", "prefills": cfg.n_prefill,
+                   "decodes": cfg.n_decode, "entries": npd, "beta": beta},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": nbytes, "bytes_per_entry": 12},
+        "cpu_baseline": None,
     }
     print(json.dumps(rec), flush=True)
     sel.close()

@@ -96,6 +96,26 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
  * no snapshot loaded. */
 netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stream);
 
+/* Predictive congestion (Sec. VIII, future work: a lightweight time-series
+ * prediction over the telemetry history in place of the instantaneous
+ * snapshot, relying on the staleness tolerance of Proposition 2).  Reading:
+ * simple exponential smoothing.  Each call folds one observation into the
+ * handle's congestion matrix, which later selections use as their
+ * forecast:
+ *     c(p,d) <- c(p,d) + beta * (obs(p,d) - c(p,d)),   0 < beta <= 1,
+ * in fp32; the first forecast is the loaded snapshot's (or the last
+ * netkv_oracle_set_util) matrix, and beta = 1 takes the observation as is.
+ * obs: DEVICE f32[n_prefill * n_decode], row-major by prefill.
+ * Asynchronous on `stream`; allocates nothing.  An observation outside
+ * [0, 1) or NaN leaves its entry unchanged and is reported by
+ * netkv_sync_errors.  EINVAL: NULL obs, beta outside (0, 1]; ENOTREADY: no
+ * snapshot loaded. */
+netkv_status netkv_congestion_smooth(netkv_handle h, const float *obs, float beta, void *stream);
+
+/* Copy the congestion matrix the selections currently use (snapshot, set,
+ * or smoothed) to out: DEVICE f32[n_prefill * n_decode].  Asynchronous. */
+netkv_status netkv_congestion_get(netkv_handle h, float *out, void *stream);
+
 /* Load the resident block-hash sets K_d (Sec. III-B, III-C) of n_decode
  * decode instances as CSR: the hashes of decode d are
  * hashes[hash_off[d] .. hash_off[d+1]), n_hashes = hash_off[n_decode].
@@ -226,7 +246,8 @@ netkv_status netkv_sync_errors(netkv_handle h, void *stream);
  * netkv_select_batch that scores every pair and keeps each decode group's
  * top-k (not the ordering, prefix-length or merge kernels), the sweep
  * kernel of netkv_rank_sweep, the per-prefill kernel of
- * netkv_select_sequential -- without synchronising.  netkv_kernel_ms waits
+ * netkv_select_sequential, the smoothing kernel of netkv_congestion_smooth
+ * -- without synchronising.  netkv_kernel_ms waits
  * for the last of them and returns the mean milliseconds over the launches
  * timed since timing was last enabled (the latest 256 when there were more);
  * ENOTREADY when there were none.  Enabling creates the events (EDEVICE if

@@ -73,6 +73,8 @@ def _load():
         lib.orc_tier_counts.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         lib.orc_prefix_len.restype = C.c_uint32
         lib.orc_prefix_len.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint32]
+        lib.orc_smooth.restype = C.c_uint64
+        lib.orc_smooth.argtypes = [C.c_void_p, C.c_void_p, C.c_uint64, C.c_double]
         lib.orc_max_threads.restype = C.c_int
         _lib = lib
     return _lib
@@ -245,3 +247,14 @@ def tier_counts(snap, req, sel: np.ndarray) -> np.ndarray:
     out = np.empty(5, dtype=np.uint64)
     lib.orc_tier_counts(C.byref(s.s), C.byref(q.r), sel.ctypes.data, out.ctypes.data)
     return out
+
+
+def smooth(c: np.ndarray, obs: np.ndarray, beta: float):
+    """One step of the predictive-congestion smoothing (Sec. VIII): returns
+    (the new fp64 congestion, the number of observations outside [0, 1))."""
+    lib = _load()
+    out = np.array(c, dtype=np.float64, copy=True).reshape(-1)
+    o = _arr(np.asarray(obs, np.float32).reshape(-1), np.float32)
+    assert o.size == out.size
+    bad = lib.orc_smooth(out.ctypes.data, o.ctypes.data, C.c_uint64(out.size), C.c_double(beta))
+    return out, int(bad)

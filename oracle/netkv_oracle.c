@@ -404,6 +404,23 @@ void orc_tier_counts(const orc_snapshot *s, const orc_requests *q, const int32_t
     }
 }
 
+/* Predictive congestion (Sec. VIII, reading: simple exponential smoothing
+ * of the congestion telemetry): one step c <- c + beta (obs - c) per entry,
+ * in fp64.  An observation outside [0, 1) or NaN leaves its entry as it
+ * was.  Returns the number of such observations. */
+uint64_t orc_smooth(double *c, const float *obs, uint64_t n, double beta) {
+    uint64_t bad = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        const double o = (double)obs[i];
+        if (!(o >= 0.0 && o < 1.0)) {
+            bad += 1;
+            continue;
+        }
+        c[i] = c[i] + beta * (o - c[i]);
+    }
+    return bad;
+}
+
 /* The first-miss prefix length of one hash run against one decode's set
  * (exposed for tests). */
 uint32_t orc_prefix_len(const orc_cache *c, uint32_t d, const uint64_t *h, uint32_t n) {

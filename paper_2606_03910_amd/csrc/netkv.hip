@@ -72,7 +72,7 @@ constexpr uint64_t kEmptyKey = ~0ull; // empty top-k entry (sorts last)
 
 enum : uint32_t {
     kErrRequest = 1u,    // request header inconsistent
-    kErrZeroHash = 2u,   // request carries hash 0
+    kErrObservation = 2u,   // congestion observation outside [0, 1) or NaN
     kErrSelection = 4u,  // selection index out of range
     kErrTableFull = 8u,  // insertion found no free slot
 };
@@ -1338,12 +1338,13 @@ __global__ __launch_bounds__(256) void sweep_kernel(Snap s, Reqs rq, const float
 
 // ------------------------------------------------------------------ table build
 
-__global__ void count_zero_kernel(const uint64_t *__restrict__ h, uint64_t n, uint32_t *__restrict__ err) {
+// Sets *flag when the resident hashes hold the reserved value 0.
+__global__ void count_zero_kernel(const uint64_t *__restrict__ h, uint64_t n, uint32_t *__restrict__ flag) {
     uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     bool z = false;
     for (; i < n; i += stride) z |= h[i] == 0;
-    if (__any(z) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrZeroHash);
+    if (__any(z) && (threadIdx.x % kWave) == 0) atomicOr(flag, 1u);
 }
 
 // ---- holder index build (once per cache load)
@@ -1512,6 +1513,46 @@ __global__ void fill_u32_kernel(uint32_t *__restrict__ p, uint64_t n, uint32_t v
 }
 
 // ------------------------------------------------------------------ snapshot checks
+
+// Predictive congestion (Sec. VIII): one step of simple exponential
+// smoothing of the congestion matrix towards an observation,
+// c <- c + beta (obs - c), in fp32.  Both lie in [0, 1) and the result is
+// their convex combination, rounded between them, so it stays in [0, 1).
+// An observation outside [0, 1) or NaN leaves its entry unchanged and
+// raises kErrObservation.
+__device__ inline float smooth_one(float u, float o, float beta, bool &bad) {
+    if (!(o >= 0.0f && o < 1.0f)) {
+        bad = true;
+        return u;
+    }
+    return fmaf(beta, o - u, u);
+}
+
+// VEC4: both arrays 16-byte aligned; four entries per thread and step,
+// the n % 4 tail by the first threads.
+template <bool VEC4>
+__global__ __launch_bounds__(256) void smooth_kernel(float *__restrict__ util, const float *__restrict__ obs,
+                                                     uint64_t n, float beta, uint32_t *__restrict__ err) {
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    bool bad = false;
+    if (VEC4) {
+        const uint64_t n4 = n / 4;
+        for (uint64_t v = i; v < n4; v += stride) {
+            const float4 o = ((const float4 *)obs)[v];
+            float4 u = ((const float4 *)util)[v];
+            u.x = smooth_one(u.x, o.x, beta, bad);
+            u.y = smooth_one(u.y, o.y, beta, bad);
+            u.z = smooth_one(u.z, o.z, beta, bad);
+            u.w = smooth_one(u.w, o.w, beta, bad);
+            ((float4 *)util)[v] = u;
+        }
+        i += n4 * 4;
+        if (i >= n4 * 4 + 4) i = n;   // only the first threads take the tail
+    }
+    for (; i < n; i += stride) util[i] = smooth_one(util[i], obs[i], beta, bad);
+    if (__ballot(bad) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrObservation);
+}
 
 __global__ void check_snapshot_kernel(const uint8_t *__restrict__ tier, const float *__restrict__ util,
                                       uint64_t npd, const uint32_t *__restrict__ batch, uint32_t D,
@@ -2602,6 +2643,38 @@ netkv_status netkv_oracle_set_util(netkv_handle h, const float *util, void *stre
     return NETKV_OK;
 }
 
+netkv_status netkv_congestion_smooth(netkv_handle h, const float *obs, float beta, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    if (!h->have_snap) return fail(h, NETKV_ENOTREADY, "no snapshot loaded");
+    if (!obs) return fail(h, NETKV_EINVAL, "obs is NULL");
+    if (!(beta > 0.0f && beta <= 1.0f)) return fail(h, NETKV_EINVAL, "beta must be in (0, 1]");
+    DeviceGuard g(h->device);
+    hipStream_t st = (hipStream_t)stream;
+    const uint64_t npd = (uint64_t)h->P * h->D;
+    HIPCHK(h, time_begin(h, st));
+    if (((uintptr_t)obs & 15) == 0 && ((uintptr_t)h->util & 15) == 0)
+        hipLaunchKernelGGL(smooth_kernel<true>, dim3(grid_for((npd + 3) / 4, 256, 8192)), dim3(256), 0, st, h->util,
+                           obs, npd, beta, h->errword);
+    else
+        hipLaunchKernelGGL(smooth_kernel<false>, dim3(grid_for(npd, 256, 8192)), dim3(256), 0, st, h->util, obs,
+                           npd, beta, h->errword);
+    HIPCHK(h, hipGetLastError());
+    HIPCHK(h, time_end(h, st));
+    return NETKV_OK;
+}
+
+netkv_status netkv_congestion_get(netkv_handle h, float *out, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    if (!h->have_snap) return fail(h, NETKV_ENOTREADY, "no snapshot loaded");
+    if (!out) return fail(h, NETKV_EINVAL, "out is NULL");
+    DeviceGuard g(h->device);
+    HIPCHK(h, hipMemcpyAsync(out, h->util, (uint64_t)h->P * h->D * sizeof(float), hipMemcpyDeviceToDevice,
+                             (hipStream_t)stream));
+    return NETKV_OK;
+}
+
 netkv_status netkv_cache_load(netkv_handle h, uint32_t n_decode, const uint64_t *hash_off, const uint64_t *hashes,
                               uint64_t n_hashes, float max_load_factor, void *stream) {
     if (!h) return NETKV_EINVAL;
@@ -2935,7 +3008,8 @@ netkv_status netkv_sync_errors(netkv_handle h, void *stream) {
     HIPCHK(h, hipMemset(h->errword, 0, 4));
     if (e)
         return fail(h, NETKV_EINVAL, "input errors:%s%s%s%s", (e & kErrRequest) ? " inconsistent request header" : "",
-                    (e & kErrZeroHash) ? " request hash 0" : "", (e & kErrSelection) ? " selection index >= D" : "",
+                    (e & kErrObservation) ? " congestion observation outside [0,1)" : "",
+                    (e & kErrSelection) ? " selection index >= D" : "",
                     (e & kErrTableFull) ? " table full" : "");
     return NETKV_OK;
 }

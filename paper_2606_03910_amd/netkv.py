@@ -61,6 +61,8 @@ _SIGS = {
     "netkv_last_error": (C.c_char_p, [C.c_void_p]),
     "netkv_oracle_load": (C.c_int32, [C.c_void_p, C.POINTER(netkv_oracle_t), C.c_void_p]),
     "netkv_oracle_set_util": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p]),
+    "netkv_congestion_smooth": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_float, C.c_void_p]),
+    "netkv_congestion_get": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p]),
     "netkv_cache_load": (C.c_int32, [C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p, C.c_uint64,
                                      C.c_float, C.c_void_p]),
     "netkv_select_batch": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
@@ -189,6 +191,15 @@ def netkv_oracle_load(h: int, snap: Dict[str, object], device) -> None:
 def netkv_oracle_set_util(h: int, util: torch.Tensor, device) -> None:
     _check(h, load_library().netkv_oracle_set_util(h, _dptr(util, torch.float32, name="util"),
                                                    _stream(device)))
+
+
+def netkv_congestion_smooth(h: int, obs: torch.Tensor, beta: float, device) -> None:
+    _check(h, load_library().netkv_congestion_smooth(h, _dptr(obs, torch.float32, name="obs"), float(beta),
+                                                     _stream(device)))
+
+
+def netkv_congestion_get(h: int, out: torch.Tensor, device) -> None:
+    _check(h, load_library().netkv_congestion_get(h, _dptr(out, torch.float32, name="out"), _stream(device)))
 
 
 def netkv_cache_load(h: int, n_decode: int, hash_off: torch.Tensor, hashes: torch.Tensor,
@@ -363,6 +374,19 @@ class Selector:
     def set_util(self, util: np.ndarray) -> None:
         netkv_oracle_set_util(self.h, to_device(np.asarray(util, np.float32), self.device),
                               self.device)
+
+    def smooth_congestion(self, obs, beta: float) -> None:
+        """Fold one congestion observation [P*D] (numpy or device tensor)
+        into the forecast the selections use."""
+        if not isinstance(obs, torch.Tensor):
+            obs = to_device(np.asarray(obs, np.float32), self.device)
+        netkv_congestion_smooth(self.h, obs, beta, self.device)
+
+    def congestion(self) -> np.ndarray:
+        """The congestion matrix the selections currently use [P*D]."""
+        out = torch.empty(self.P * self.D, dtype=torch.float32, device=self.device)
+        netkv_congestion_get(self.h, out, self.device)
+        return to_numpy(out)
 
     def load_cache(self, cache: Dict[str, np.ndarray], max_load_factor: float = 0.5) -> None:
         dev = self.device

@@ -188,3 +188,80 @@ def test_sequential_pool_sizes(nk, shape):
     near = _check_sequential(g_idx, g_sc, ref)
     assert near < 0.01 * cfg.n_requests
     sel.close()
+
+
+def test_congestion_smoothing_matches_oracle(nk):
+    """Predictive congestion (Sec. VIII; reading: simple exponential
+    smoothing): a series of observations folded in with beta 1, 0.5 and
+    0.1 gives the oracle's fp64 forecast within the fp32 rounding of the
+    steps (at most ~1.2e-7 per step), an invalid observation leaves its entry
+    unchanged and is reported, and a selection under the forecast matches
+    the oracle's under the same forecast."""
+    _say("congestion smoothing")
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=W.Cluster(8, 2, 2, 2), n_requests=1500)
+    snap, req, cache = _inputs(cfg, 43)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    npd = cfg.n_prefill * cfg.n_decode
+    rng = np.random.default_rng(43)
+    c = np.asarray(snap["util"], np.float32).astype(np.float64).reshape(-1)
+    assert np.array_equal(sel.congestion(), np.asarray(snap["util"], np.float32).reshape(-1))
+    steps = [1.0, 0.5, 0.5, 0.1, 0.1, 0.1]
+    for s, beta in enumerate(steps):
+        obs = rng.uniform(0, 0.99, npd).astype(np.float32)
+        if s == 2:
+            obs[[0, 7, npd - 1]] = [np.nan, 1.0, -0.5]
+        sel.smooth_congestion(obs, beta)
+        c, bad = oracle.smooth(c, obs, beta)
+        if s == 2:
+            assert bad == 3
+            with pytest.raises(nk.NetKVError):
+                sel.sync_errors()
+        else:
+            sel.sync_errors()
+        g = sel.congestion().astype(np.float64)
+        assert ((g >= 0) & (g < 1)).all()
+        np.testing.assert_allclose(g, c, rtol=0, atol=1.2e-7 * (s + 1) + 1e-9)
+    # selection under the forecast
+    fsnap = dict(snap)
+    fsnap["util"] = sel.congestion().reshape(np.asarray(snap["util"]).shape)
+    out = sel.select(nk.requests_to_device(req, sel.device), k=2, pairs=True)
+    sel.sync_errors()
+    o = oracle.select(fsnap, cache, req, k=2, pairs=True, n_threads=8)
+    check_pairs(nk.to_numpy(out["pairs"]["prefix_blocks"]), nk.to_numpy(out["pairs"]["feasible"]),
+                nk.to_numpy(out["pairs"]["score"]), o)
+    check_topk(nk.to_numpy(out["idx"]).reshape(-1, 2), nk.to_numpy(out["score"]).reshape(-1, 2),
+               o["idx"], o["cost"], o["feasible"])
+    # contract: beta outside (0, 1] is rejected and changes nothing
+    before = sel.congestion()
+    for beta in (0.0, 1.5, float("nan")):
+        with pytest.raises(nk.NetKVError):
+            sel.smooth_congestion(np.zeros(npd, np.float32), beta)
+    assert np.array_equal(sel.congestion(), before)
+    sel.close()
+
+
+def test_congestion_smoothing_odd_sizes_and_unaligned_observations(nk):
+    """The vectorised smoothing path's tail (P * D = 21, not a multiple of 4)
+    and the scalar path (an observation that is not 16-byte aligned)."""
+    _say("congestion smoothing, odd sizes")
+    from tests.test_oracle_pins import tiny_snapshot
+    rng = np.random.default_rng(44)
+    P, D = 3, 7
+    util = rng.uniform(0, 0.99, P * D).astype(np.float32)
+    snap = tiny_snapshot(P, D, rng.integers(0, 4, P * D), util)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    c = util.astype(np.float64)
+    for beta, offset in ((0.25, 0), (0.6, 1), (1.0, 3)):
+        obs = rng.uniform(0, 0.99, P * D).astype(np.float32)
+        buf = torch.zeros(P * D + 4, dtype=torch.float32, device=sel.device)
+        buf[offset:offset + P * D] = torch.from_numpy(obs).to(sel.device)
+        view = buf[offset:offset + P * D]
+        assert (view.data_ptr() % 16 == 0) == (offset == 0)
+        sel.smooth_congestion(view, beta)
+        sel.sync_errors()
+        c, _ = oracle.smooth(c, obs, beta)
+        np.testing.assert_allclose(sel.congestion().astype(np.float64), c, rtol=0, atol=4e-7)
+    sel.close()

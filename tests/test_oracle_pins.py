@@ -625,3 +625,43 @@ def test_tier_counts_closed_form():
     cnt = oracle.tier_counts(snap, rq, np.array([2, 2, 3, -1, 0], np.int32))
     # p0->d2 tier 2, p1->d2 tier 1, p1->d3 tier 0, rejected, p1->d0 tier 3
     assert cnt.tolist() == [1, 1, 1, 1, 1]
+
+
+# ---- predictive congestion (Sec. VIII; reading: simple exponential smoothing)
+
+def test_smoothing_with_beta_one_takes_the_observation():
+    rng = np.random.default_rng(5)
+    c0 = rng.uniform(0, 0.99, 50)
+    obs = rng.uniform(0, 0.99, 50).astype(np.float32)
+    c1, bad = oracle.smooth(c0, obs, 1.0)
+    assert bad == 0
+    np.testing.assert_array_equal(c1, obs.astype(np.float64))
+
+
+def test_smoothing_constant_observation_closed_form():
+    """A constant observation o, k times from c0: c_k = o + (1 - beta)^k (c0 - o)."""
+    rng = np.random.default_rng(6)
+    c0 = rng.uniform(0, 0.99, 40)
+    o = rng.uniform(0, 0.99, 40).astype(np.float32)
+    for beta in (0.05, 0.3, 0.7):
+        c = c0.copy()
+        for k in range(1, 25):
+            c, _ = oracle.smooth(c, o, beta)
+            expect = o.astype(np.float64) + (1 - beta) ** k * (c0 - o.astype(np.float64))
+            np.testing.assert_allclose(c, expect, rtol=0, atol=1e-14)
+
+
+def test_smoothing_stays_between_forecast_and_observation_and_skips_invalid():
+    rng = np.random.default_rng(7)
+    c0 = rng.uniform(0, 0.99, 64)
+    obs = rng.uniform(0, 0.99, 64).astype(np.float32)
+    obs[[3, 9, 20, 41]] = [np.nan, 1.0, -0.25, np.inf]
+    c1, bad = oracle.smooth(c0, obs, 0.4)
+    assert bad == 4
+    keep = np.isin(np.arange(64), [3, 9, 20, 41])
+    np.testing.assert_array_equal(c1[keep], c0[keep])
+    o = obs.astype(np.float64)
+    lo, hi = np.minimum(c0, o), np.maximum(c0, o)
+    assert ((c1[~keep] >= lo[~keep]) & (c1[~keep] <= hi[~keep])).all()
+    # the step moves 40 % of the way: c1 - c0 = 0.4 (obs - c0)
+    np.testing.assert_allclose((c1 - c0)[~keep], 0.4 * (o - c0)[~keep], rtol=1e-12, atol=1e-15)
