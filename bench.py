@@ -41,6 +41,9 @@ ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 # infinity select, and one comparison of the per-request minimum
 # (Eqs. (2)-(5), Algorithm 1)
 OPS_PER_PAIR = 6
+# with staged routes: a second fused multiply-add for the staged cost and the
+# minimum of the two route costs (Sec. VIII)
+OPS_PER_PAIR_TWO_HOP = 8
 
 
 def log(*a):
@@ -96,6 +99,9 @@ def main():
     ap.add_argument("--forecast", type=float, default=0.0, metavar="BETA",
                     help="c1: fold each batch's (stale) congestion observation into the forecast by "
                          "exponential smoothing with this factor instead of replacing the snapshot's")
+    ap.add_argument("--two-hop", action="store_true",
+                    help="load a staged (two-hop) route for every (prefill, decode) pair: each pair "
+                         "scores the faster of its direct and staged routes")
     ap.add_argument("--smooth-bench", action="store_true",
                     help="only time the congestion smoothing kernel on the workload's P x D matrix")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -148,6 +154,11 @@ def main():
     t0 = time.time()
     sel.load_snapshot(snap)
     sel.load_cache(cache, 0.5)
+    routes = None
+    if args.two_hop:
+        routes = W.make_routes(cfg, args.seed)
+        sel.load_routes(routes["route_tier1"], routes["route_util1"], routes["route_tier2"],
+                        routes["route_util2"])
     torch.cuda.synchronize()
     ci = netkv.netkv_cache_info(sel.h)
     log(f"snapshot + holder index loaded in {time.time() - t0:.1f}s: {ci['distinct_hashes']} distinct "
@@ -223,10 +234,16 @@ def main():
     b_dec = D * (8 + 4 + 4)
     b_nco = P * D * (1 + 4) + 4 * P * 2
     b_alg = b_tests + b_req + b_dec + b_nco
-    ops = OPS_PER_PAIR * R * D
+    ops_pair = OPS_PER_PAIR_TWO_HOP if args.two_hop else OPS_PER_PAIR
+    ops = ops_pair * R * D
+    staged = None
+    if args.two_hop:
+        rt = sel.routes_of(rd, out["idx"], k)
+        staged = float((rt == 1).sum()) / max(1, int((rt >= 0).sum()))
+        log(f"selections taking the staged route: {staged:.4f}")
     achieved = ops / (kern_ms * 1e-3) / 1e12
     digest = kernel_source_digest()
-    cs = counter_summary(args.workload, digest)
+    cs = counter_summary(args.workload + ("_two_hop" if args.two_hop else ""), digest)
     traffic = cs.get("hbm_bytes_per_launch")
     issue = None
     if "valu_insts_per_launch" in cs:
@@ -252,7 +269,7 @@ def main():
         log(f"oracle resident sets sorted in {time.time() - t0:.1f}s ({threads} threads)")
         rng = np.random.default_rng(7)
         order = rng.permutation(R)
-        osnap = oracle.Snapshot(snap)
+        osnap = oracle.Snapshot(dict(snap, **routes) if routes else snap)
         # chunks of seeded-random requests, doubling, until the sample has
         # taken the requested CPU time (or the batch is used up)
         n_s, dt, o_tests, chunk, agree_n = 0, 0.0, 0, 64, 0
@@ -297,6 +314,8 @@ def main():
             "k": k, "parallelism": "single-gpu", "prefix_sharing": not args.no_reuse,
             "run_len": args.run_len or "auto", "policy": args.policy,
             "selection": "sequential (in-batch in-flight increments)" if args.sequential else "snapshot",
+            "routes": "direct + staged (two-hop)" if args.two_hop else "direct",
+            "staged_fraction": staged,
         },
         "roofline": {
             "bound": "alu", "achieved": achieved, "peak": ALU_PEAK_TOPS, "unit": "TOP/s",
@@ -305,8 +324,9 @@ def main():
             "traffic_unit": "GB/s",
             "traffic_bytes_per_launch": traffic,
             "algorithmic_ops_per_launch": ops,
-            "ops_per_pair": OPS_PER_PAIR,
-            "kernel": "score_kernel (k=1; %d decodes per lane)" % (args.cols or cols_per_lane(D)),
+            "ops_per_pair": ops_pair,
+            "kernel": "score_kernel (k=1; %d decodes per lane%s)" % (
+                args.cols or cols_per_lane(D), "; two routes per pair" if args.two_hop else ""),
             "kernel_source_sha256_16": digest,
             "issue": issue,
             "hbm_algorithmic": {

@@ -177,6 +177,39 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
                                 int32_t *out_idx, float *out_score, netkv_pairs_t *pairs,
                                 void *stream);
 
+/* Two-hop KV routing (Sec. VIII, future work: KV state staged through an
+ * intermediate cache in CPU DRAM or SSD; the oracle exposes both hops'
+ * tiers and the cost sums the two transfer times).  Reading: every pair
+ * (p, d) has, besides its direct route, a staged route p -> staging store
+ * -> d whose hops have tiers tier1 / tier2 and congestion util1 / util2
+ * (row-major [n_prefill * n_decode], like the snapshot's maps).  Its
+ * transfer time is
+ *     s_eff / B_eff(tier1, util1, n_inflight[tier1][p]) + L(tier1)
+ *   + s_eff / B_eff(tier2, util2, 0) + L(tier2)
+ * (the staging store's own transfers are not the prefill's in-flight ones;
+ * Eqs. (3)-(4) per hop), and each pair's cost takes the faster of its two
+ * routes (ties: direct).  Feasibility and the load term are unchanged, and
+ * the policy rungs apply to both hops.  Only netkv_select_batch uses the
+ * staged routes; the ranking sweep and the sequential form keep the direct
+ * ones.  Synchronous; host or device pointers; the handle keeps copies
+ * while the snapshot keeps its shape (a snapshot of another shape drops
+ * them).  EINVAL: NULL map, tier > 3, util outside [0,1) or NaN (nothing is
+ * changed); ENOTREADY: no snapshot loaded. */
+netkv_status netkv_route2_load(netkv_handle h, const uint8_t *tier1, const float *util1,
+                               const uint8_t *tier2, const float *util2, void *stream);
+
+/* Drop the staged routes: selections score direct routes only again. */
+netkv_status netkv_route2_clear(netkv_handle h);
+
+/* The route of each selection under the current snapshot and route maps:
+ * for idx[r*k + q] (DEVICE, as written by netkv_select_batch), out_route
+ * (DEVICE int8[n_req * k]) = 1 when the staged route is strictly faster,
+ * 0 when the direct one is (the scoring kernel's arithmetic), -1 for no
+ * selection or an invalid request.  Asynchronous.  ENOTREADY: no route
+ * maps, snapshot or cache loaded; EINVAL: k outside [1, 8], NULL arrays. */
+netkv_status netkv_route2_of(netkv_handle h, const netkv_requests_t *req, uint32_t k,
+                             const int32_t *idx, int8_t *out_route, void *stream);
+
 /* Stale-telemetry ranking sweep (Sec. V-D, Proposition 2): re-rank the
  * batch under n_scen congestion scenarios util_scen [n_scen][P*D] (DEVICE,
  * each value in [0,1)).  Prefix matches do not depend on telemetry and are

@@ -42,6 +42,8 @@ class _Snap(C.Structure):
         ("t_iter_a", C.c_double), ("t_iter_b", C.c_double), ("beta_max", C.c_uint32),
         ("alpha", C.c_double), ("m_min", C.c_uint64), ("kv_bytes_per_token", C.c_uint64),
         ("block_tokens", C.c_uint32),
+        ("route_tier1", C.c_void_p), ("route_util1", C.c_void_p),
+        ("route_tier2", C.c_void_p), ("route_util2", C.c_void_p),
     ]
 
 
@@ -73,6 +75,7 @@ def _load():
         lib.orc_tier_counts.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         lib.orc_prefix_len.restype = C.c_uint32
         lib.orc_prefix_len.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint32]
+        lib.orc_route_of.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p]
         lib.orc_smooth.restype = C.c_uint64
         lib.orc_smooth.argtypes = [C.c_void_p, C.c_void_p, C.c_uint64, C.c_double]
         lib.orc_max_threads.restype = C.c_int
@@ -113,6 +116,11 @@ class Snapshot:
         s.m_min = int(snap["m_min"])
         s.kv_bytes_per_token = int(snap["kv_bytes_per_token"])
         s.block_tokens = int(snap["block_tokens"])
+        if snap.get("route_tier1") is not None:   # two-hop routing (Sec. VIII)
+            for f, dt in (("route_tier1", np.uint8), ("route_util1", np.float32),
+                          ("route_tier2", np.uint8), ("route_util2", np.float32)):
+                self.keep[f] = _arr(np.asarray(snap[f]).reshape(-1), dt)
+                setattr(s, f, self.keep[f].ctypes.data)
         self.s = s
         self.n_prefill, self.n_decode = s.n_prefill, s.n_decode
 
@@ -258,3 +266,16 @@ def smooth(c: np.ndarray, obs: np.ndarray, beta: float):
     assert o.size == out.size
     bad = lib.orc_smooth(out.ctypes.data, o.ctypes.data, C.c_uint64(out.size), C.c_double(beta))
     return out, int(bad)
+
+
+def route_of(snap, cache, req, idx: np.ndarray, k: int) -> np.ndarray:
+    """Two-hop routing (Sec. VIII): 1 where a selection's staged route is
+    strictly faster, 0 direct, -1 no selection."""
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    q = req if isinstance(req, Requests) else Requests(req)
+    cc = cache if isinstance(cache, Cache) else Cache(cache)
+    idx = _arr(np.asarray(idx).reshape(-1), np.int32)
+    out = np.empty(idx.size, dtype=np.int8)
+    lib.orc_route_of(C.byref(s.s), cc.h, C.byref(q.r), int(k), idx.ctypes.data, out.ctypes.data)
+    return out

@@ -56,6 +56,12 @@ typedef struct {
     uint64_t m_min;
     uint64_t kv_bytes_per_token;
     uint32_t block_tokens;
+    /* two-hop routing (Sec. VIII): the staged route p -> store -> d of every
+     * pair, hop tiers and congestion [n_prefill * n_decode]; NULL: none */
+    const uint8_t *route_tier1;
+    const float *route_util1;
+    const uint8_t *route_tier2;
+    const float *route_util2;
 } orc_snapshot;
 
 typedef struct {
@@ -150,6 +156,28 @@ static double eff_bandwidth(const orc_snapshot *s, uint32_t p, uint32_t d) {
     return s->tier_bw[tau] * (1.0 - c) / (1.0 + n);
 }
 
+/* Transfer time of s_eff bytes from p to d (Eq. (3)): the direct route, or
+ * with staged routes the faster of the direct one and the sum of the two
+ * hops' transfer times (Sec. VIII; the staging store's transfers carry no
+ * in-flight count of the prefill).  *staged tells which (ties: direct). */
+static double transfer_time(const orc_snapshot *s, uint32_t p, uint32_t d, uint64_t s_eff, int *staged) {
+    uint64_t pd = (uint64_t)p * s->n_decode + d;
+    int tau = s->tier_map[pd];
+    double direct = (double)s_eff / eff_bandwidth(s, p, d) + s->tier_lat[tau];
+    *staged = 0;
+    if (!s->route_tier1) return direct;
+    int t1 = s->route_tier1[pd], t2 = s->route_tier2[pd];
+    double n1 = (double)s->n_inflight[(uint64_t)t1 * s->n_prefill + p];
+    double b1 = s->tier_bw[t1] * (1.0 - (double)s->route_util1[pd]) / (1.0 + n1);
+    double b2 = s->tier_bw[t2] * (1.0 - (double)s->route_util2[pd]);
+    double two = (double)s_eff / b1 + s->tier_lat[t1] + (double)s_eff / b2 + s->tier_lat[t2];
+    if (two < direct) {
+        *staged = 1;
+        return two;
+    }
+    return direct;
+}
+
 typedef struct {
     double cost;
     int32_t d;
@@ -189,8 +217,8 @@ static void score_request(const orc_snapshot *s, const float *util, const orc_ca
         uint64_t s_eff = s->kv_bytes_per_token * (len - lambda);       /* Eq. (2) */
         uint64_t m = s->free_mem[d];
         int feas = (m >= s->m_min) && (m - s->m_min >= s_eff);         /* m >= s_eff + m_min */
-        int tau = s->tier_map[(uint64_t)p * s->n_decode + d];
-        double t_x = (double)s_eff / eff_bandwidth(&sv, p, d) + s->tier_lat[tau];   /* Eq. (3) */
+        int staged;
+        double t_x = transfer_time(&sv, p, d, s_eff, &staged);              /* Eq. (3) */
         double cost = t_x + s->alpha * load_time(s, d);
         if (pj) pj[d] = j;
         if (pf) pf[d] = (uint8_t)feas;
@@ -245,9 +273,12 @@ uint64_t orc_select(const orc_snapshot *s, const orc_cache *c, const orc_request
  * decode's tier differs from the tier selected under the snapshot's own
  * congestion, out_flips[2*s+1] those whose selected decode differs
  * (a rejection counts as its own tier and index). */
-void orc_rank_sweep(const orc_snapshot *s, const orc_cache *c, const orc_requests *q,
+void orc_rank_sweep(const orc_snapshot *s_in, const orc_cache *c, const orc_requests *q,
                     uint32_t n_scen, const float *util_scen, uint32_t k, int32_t *out_idx,
                     double *out_score, uint64_t *out_flips, int n_threads) {
+    orc_snapshot sd = *s_in;
+    sd.route_tier1 = NULL;   /* the ranking sweep scores direct routes */
+    const orc_snapshot *s = &sd;
     const uint32_t D = s->n_decode, R = q->n_req;
     uint32_t *jm = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)R * (D ? D : 1));
     int32_t *base = (int32_t *)malloc(sizeof(int32_t) * (R ? R : 1));
@@ -373,6 +404,7 @@ void orc_select_sequential(const orc_snapshot *s, const orc_cache *c, const orc_
     double *cost = (double *)malloc(sizeof(double) * (D ? D : 1));
     orc_snapshot sv = *s;
     sv.n_inflight = n;
+    sv.route_tier1 = NULL;   /* the sequential form scores direct routes */
     for (uint32_t r = 0; r < q->n_req; ++r) {
         uint64_t tests = 0;
         score_request(&sv, s->util, c, q, r, NULL, buf, 1, out_idx + r, out_score + r, NULL, feas, cost, &tests);
@@ -393,6 +425,30 @@ void orc_select_sequential(const orc_snapshot *s, const orc_cache *c, const orc_
     free(buf);
     free(feas);
     free(cost);
+}
+
+/* Two-hop routing: for each selection idx[r*k+q] >= 0, out[r*k+q] = 1 when
+ * its staged route is strictly faster than the direct one, else 0; -1 for
+ * no selection. */
+void orc_route_of(const orc_snapshot *s, const orc_cache *c, const orc_requests *q, uint32_t k,
+                  const int32_t *idx, int8_t *out) {
+    for (uint32_t r = 0; r < q->n_req; ++r) {
+        uint64_t a = q->hash_off[r];
+        uint32_t n = (uint32_t)(q->hash_off[r + 1] - a);
+        for (uint32_t i = 0; i < k; ++i) {
+            int32_t d = idx[(uint64_t)r * k + i];
+            if (d < 0) {
+                out[(uint64_t)r * k + i] = -1;
+                continue;
+            }
+            uint32_t t;
+            uint32_t j = prefix_blocks(c, (uint32_t)d, q->hashes + a, n, &t);
+            uint64_t s_eff = s->kv_bytes_per_token * (q->len_tokens[r] - (uint64_t)s->block_tokens * j);
+            int staged;
+            (void)transfer_time(s, q->prefill[r], (uint32_t)d, s_eff, &staged);
+            out[(uint64_t)r * k + i] = (int8_t)staged;
+        }
+    }
 }
 
 /* Requests per tier of the selected decode; counts[4] = rejected. */

@@ -99,6 +99,7 @@ struct Snap {
     const float2 *sl;        // [P][slp] per (p, d): seconds per non-cached token, and the
                              // constant part L_tau + alpha (T_queue + T_decode)
     uint32_t slp;            // row pitch of sl in elements (an odd number of 128-byte lines)
+    const float2 *sr;        // like sl, for the staged (two-hop) route; null without one
     const float *dbase;      // [D] alpha (T_queue + T_decode)
     const uint64_t *dxlim;   // [D] x = l - lambda is feasible iff x < dxlim
 };
@@ -301,6 +302,27 @@ __global__ __launch_bounds__(256) void derive_kernel(Snap s, float2 *__restrict_
         dbase[i] = load_term(s, (uint32_t)i);
         dxlim[i] = feasible_limit(s, s.free_mem[i]);
     }
+}
+
+// Two-hop routing (Sec. VIII): the staged route p -> staging store -> d of
+// every pair, with hop tiers t1, t2 and congestion u1, u2.  Its transfer
+// time is the sum of the hops' (Eqs. (3)-(4) each): seconds per token
+// bpt (1 + n_inflight[t1][p]) / (B_t1 (1 - u1)) + bpt / (B_t2 (1 - u2)) (the
+// staging store's transfers are not the prefill's in-flight ones) and the
+// constant part L_t1 + L_t2 plus the decode's load term.
+__global__ __launch_bounds__(256) void derive_route_kernel(Snap s, const uint8_t *__restrict__ t1,
+                                                           const float *__restrict__ u1,
+                                                           const uint8_t *__restrict__ t2,
+                                                           const float *__restrict__ u2, float2 *__restrict__ sr) {
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t npd = (uint64_t)s.P * s.D;
+    if (i >= npd) return;
+    const uint32_t p = (uint32_t)(i / s.D);
+    const uint32_t d = (uint32_t)(i - (uint64_t)p * s.D);
+    const uint32_t a = t1[i] & 3u, b = t2[i] & 3u;
+    const float spt = sec_per_token(s, a, p, u1[i]) + sec_per_token_n(s, b, 0.0f, u2[i]);
+    sr[(uint64_t)p * s.slp + d] =
+        make_float2(spt, __fadd_rn(__fadd_rn(tier_latency(s, a), tier_latency(s, b)), load_term(s, d)));
 }
 
 // ---------------------------------------------------------------- batch order
@@ -1039,7 +1061,18 @@ __device__ inline uint32_t load_lam(__amdgpu_buffer_rsrc_t r, uint32_t lane_off,
 // request's are fetched during the current step only when its leader row
 // differs.  Records are read two requests ahead.  Requests are taken in
 // chunks of 64/K whose keys are gathered one per lane and stored together.
-template <int K, int W, int C, bool PAIRS>
+// The cost of a pair with x non-cached tokens from its derived row(s), as
+// fp32 bits: the direct route, or the cheaper of the direct and the staged
+// route (costs are non-negative, so the smaller bits are the smaller cost;
+// ties keep the direct route's value, which is the same).
+template <bool TWO>
+__device__ inline uint32_t route_cost(float x, float2 r1, float2 r2) {
+    const uint32_t c1 = __float_as_uint(fmaf(x, r1.x, r1.y));
+    if (!TWO) return c1;
+    return min(c1, __float_as_uint(fmaf(x, r2.x, r2.y)));
+}
+
+template <int K, int W, int C, bool PAIRS, bool TWO>
 __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Hot *__restrict__ hot,
                                                        const Cold *__restrict__ cold,
                                                        const float *__restrict__ lead_lam, uint32_t lead_rows,
@@ -1103,9 +1136,12 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
     const __amdgpu_buffer_rsrc_t llr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)lead_lam, (short)0, (int)(uint32_t)(ll_bytes < 0xFFFFFFFFull ? ll_bytes : 0xFFFFFFFFull),
         kBufferFlags);
+    const __amdgpu_buffer_rsrc_t srr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(TWO ? s.sr : s.sl), (short)0,
+        (int)(uint32_t)(sl_bytes < 0xFFFFFFFFull ? sl_bytes : 0xFFFFFFFFull), kBufferFlags);
     Hot c0 = load_hot(hot, i0);
     Hot c1 = load_hot(hot, i0 + 1);
-    float2 rowv[C];           // the current prefill's row
+    float2 rowv[C], rowv2[C];   // the current prefill's row (and its staged-route row)
     uint32_t rowcur = c0.row;
     // the current leader's B_tok * j, and the next one's while it loads, as
     // fp32 bits: non-negative, so their order is that of the unsigned bits
@@ -1113,6 +1149,7 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         rowv[q] = load_row(slr, voff[q], c0.row);
+        rowv2[q] = TWO ? load_row(srr, voff[q], c0.row) : rowv[q];
         laml[q] = load_lam(llr, loff[q], c0.lrow);
         stg[q] = 0;
     }
@@ -1131,7 +1168,10 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
             }
             if (c0.row != rowcur) {
 #pragma unroll
-                for (int q = 0; q < C; ++q) rowv[q] = load_row(slr, voff[q], c0.row);
+                for (int q = 0; q < C; ++q) {
+                    rowv[q] = load_row(slr, voff[q], c0.row);
+                    if (TWO) rowv2[q] = load_row(srr, voff[q], c0.row);
+                }
                 rowcur = c0.row;
             }
             uint32_t r_out = 0;
@@ -1157,7 +1197,7 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
                     const uint32_t x = len - lam[q];
                     const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
                     const bool feas = (uint64_t)x < xlim;
-                    const float cost = fmaf((float)x, rowv[q].x, rowv[q].y);
+                    const float cost = __uint_as_float(route_cost<TWO>((float)x, rowv[q], rowv2[q]));
                     if (PAIRS && act[q]) {
                         const uint64_t o = (uint64_t)r_out * s.D + d[q];
                         const uint32_t jq = lam[q] / bt;
@@ -1174,15 +1214,14 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
                 if (!PAIRS && c0.len <= xall) {
 #pragma unroll
                     for (int q = 0; q < C; ++q)
-                        cb[q] = __float_as_uint(
-                            fmaf(lenf - __uint_as_float(min(laml[q], c0.lams)), rowv[q].x, rowv[q].y));
+                        cb[q] = route_cost<TWO>(lenf - __uint_as_float(min(laml[q], c0.lams)), rowv[q], rowv2[q]);
                 } else {
 #pragma unroll
                     for (int q = 0; q < C; ++q) {
                         const float lam = __uint_as_float(min(laml[q], c0.lams));
                         const float x = lenf - lam;
                         const bool feas = x <= xmf[q];
-                        const float cost = fmaf(x, rowv[q].x, rowv[q].y);
+                        const float cost = __uint_as_float(route_cost<TWO>(x, rowv[q], rowv2[q]));
                         if (PAIRS && act[q]) {
                             const uint64_t o = (uint64_t)r_out * s.D + d[q];
                             const uint32_t jq = (uint32_t)lam / bt;
@@ -1625,6 +1664,30 @@ __global__ void commit_apply_kernel(uint32_t P, uint32_t D, uint32_t cap, uint32
 
 // ---------------------------------------------------------------- tier counts
 
+// Two-hop routing: the route each selection takes (1: staged, 0: direct,
+// -1: no selection or an invalid request): the selected pair's prefix
+// length (first miss of the run on that decode), then its direct and
+// staged costs from the derived rows, in the scoring kernel's arithmetic.
+__global__ __launch_bounds__(256) void route_of_kernel(Snap s, Table t, Reqs rq, uint32_t k,
+                                                       const int32_t *__restrict__ idx, int8_t *__restrict__ out) {
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (uint64_t)rq.n_req * k) return;
+    const uint32_t r = (uint32_t)(i / k);
+    const int32_t d = idx[i];
+    uint32_t p, len, n;
+    uint64_t a;
+    if (d < 0 || (uint32_t)d >= s.D || !request_ok(rq, s, r, p, len, a, n)) {
+        out[i] = -1;
+        return;
+    }
+    uint32_t j = 0;
+    while (j < n && holds(t, rq.hashes[a + j], (uint32_t)d)) ++j;
+    const float x = (float)(len - s.block_tokens * j);
+    const uint64_t o = (uint64_t)p * s.slp + (uint32_t)d;
+    const float2 r1 = s.sl[o], r2 = s.sr[o];
+    out[i] = fmaf(x, r2.x, r2.y) < fmaf(x, r1.x, r1.y) ? 1 : 0;
+}
+
 // Requests per tier of the selected decode (index 4: rejected), the tier
 // shift statistic.  Invalid selections are flagged and not counted.
 __global__ __launch_bounds__(256) void tier_count_kernel(Snap s, Reqs rq, const int32_t *__restrict__ sel,
@@ -1956,6 +2019,12 @@ struct netkv_ctx {
     uint32_t seq_P = 0;
     // timing
     bool timing = false;
+    // two-hop routing: the staged route's hop tiers and congestion per (p, d),
+    // and its derived rows (like sl)
+    uint8_t *rt1 = nullptr, *rt2 = nullptr;
+    float *ru1 = nullptr, *ru2 = nullptr;
+    float2 *sr = nullptr;
+    bool have_route = false;
     // kernel timing: begin/end event pairs in a ring, created on first enable
     std::vector<hipEvent_t> tev;
     uint32_t tcount = 0;    // launches timed since timing was enabled
@@ -2059,6 +2128,7 @@ Snap make_snap(netkv_handle h) {
     s.D = h->D;
     s.sl = h->sl;
     s.slp = sl_pitch(h->D);
+    s.sr = nullptr;
     s.dbase = h->dbase;
     s.dxlim = h->dxlim;
     s.policy = h->policy_opt;
@@ -2338,14 +2408,19 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
     // a request that matches on its own (its leader did not fit the leader
     // table, or 2^24 tokens or more) looks blocks up one at a time: rare,
     // and a short loop keeps the kernel's registers for the common path
-    if (pairs)
-        hipLaunchKernelGGL((score_kernel<K, 1, C, true>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len,
-                           n_runs, ngroup, partial, po);
-    else
-        hipLaunchKernelGGL((score_kernel<K, 1, C, false>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold,
-                           ord.lam, h->lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len,
-                           n_runs, ngroup, partial, po);
+    const bool two = sn.sr != nullptr;
+#define NETKV_SCORE(P2, T2)                                                                                      \
+    hipLaunchKernelGGL((score_kernel<K, 1, C, P2, T2>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, \
+                       ord.lam, h->lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len, n_runs, \
+                       ngroup, partial, po)
+    if (pairs) {
+        if (two) NETKV_SCORE(true, true);
+        else NETKV_SCORE(true, false);
+    } else {
+        if (two) NETKV_SCORE(false, true);
+        else NETKV_SCORE(false, false);
+    }
+#undef NETKV_SCORE
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return time_end(h, st);
 }
@@ -2379,19 +2454,25 @@ hipError_t launch_score_reduce(netkv_handle h, const Snap &sn, const Table &t, c
 // order (stable sort), scoring records, leaders' prefix lengths, scoring,
 // merge.
 netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
-                        const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st) {
+                        const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false) {
     const uint64_t R = req->n_req;
     const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
     const uint32_t C = cols_per_lane(h->D, h->cols_opt);
     const uint32_t ngroup = (h->D + kWave * C - 1) / (kWave * C);
     netkv_status e = ensure_order_scratch(h, R, R * ngroup * K, req->n_hashes, st);
     if (e) return e;
-    const Snap sn = make_snap(h);
+    Snap sn = make_snap(h);
     const Table t = make_table(h);
     const Reqs rq = make_reqs(req);
     const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
     hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
                        h->dxlim);
+    if (route2 && h->have_route) {
+        hipLaunchKernelGGL(derive_route_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn,
+                           (const uint8_t *)h->rt1, (const float *)h->ru1, (const uint8_t *)h->rt2,
+                           (const float *)h->ru2, h->sr);
+        sn.sr = h->sr;
+    }
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
                        h->vals_in, h->errword, h->hv_used, h->n_lead);
     HIPCHK(h, hipGetLastError());
@@ -2512,6 +2593,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
         for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
+        dfree(h->rt1); dfree(h->rt2); dfree(h->ru1); dfree(h->ru2); dfree(h->sr);
     }
     delete h;
 }
@@ -2585,6 +2667,11 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
     }
     if (!h->have_snap || h->P != P || h->D != D) {
         dfree(h->sl); dfree(h->dbase); dfree(h->dxlim);
+        // route maps and rows of another shape no longer apply
+        dfree(h->rt1); dfree(h->rt2); dfree(h->ru1); dfree(h->ru2); dfree(h->sr);
+        h->rt1 = h->rt2 = nullptr;
+        h->ru1 = h->ru2 = nullptr;
+        h->have_route = false;
         h->have_snap = false;
         if (dalloc(h->sl, (uint64_t)P * sl_pitch(D)) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
             dalloc(h->dxlim, D) != hipSuccess) {
@@ -2672,6 +2759,100 @@ netkv_status netkv_congestion_get(netkv_handle h, float *out, void *stream) {
     DeviceGuard g(h->device);
     HIPCHK(h, hipMemcpyAsync(out, h->util, (uint64_t)h->P * h->D * sizeof(float), hipMemcpyDeviceToDevice,
                              (hipStream_t)stream));
+    return NETKV_OK;
+}
+
+netkv_status netkv_route2_load(netkv_handle h, const uint8_t *tier1, const float *util1, const uint8_t *tier2,
+                               const float *util2, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    if (!h->have_snap) return fail(h, NETKV_ENOTREADY, "no snapshot loaded");
+    if (!tier1 || !util1 || !tier2 || !util2) return fail(h, NETKV_EINVAL, "a route map is NULL");
+    DeviceGuard g(h->device);
+    hipStream_t st = (hipStream_t)stream;
+    const uint64_t npd = (uint64_t)h->P * h->D;
+    uint8_t *a = nullptr, *b = nullptr;
+    float *ua = nullptr, *ub = nullptr;
+    auto drop = [&]() { dfree(a); dfree(b); dfree(ua); dfree(ub); };
+    if (dalloc(a, npd) != hipSuccess || dalloc(b, npd) != hipSuccess || dalloc(ua, npd) != hipSuccess ||
+        dalloc(ub, npd) != hipSuccess || (!h->sr && dalloc(h->sr, (uint64_t)h->P * sl_pitch(h->D)) != hipSuccess)) {
+        drop();
+        return fail(h, NETKV_ENOMEM, "route map allocation failed");
+    }
+    uint32_t bad = 0;
+    hipError_t e = hipMemcpyAsync(a, tier1, npd, hipMemcpyDefault, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(b, tier2, npd, hipMemcpyDefault, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(ua, util1, npd * 4, hipMemcpyDefault, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(ub, util2, npd * 4, hipMemcpyDefault, st);
+    if (e == hipSuccess) e = hipMemsetAsync(h->loadword, 0, 4, st);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(check_snapshot_kernel, dim3(grid_for(npd, 256, 4096)), dim3(256), 0, st,
+                           (const uint8_t *)a, (const float *)ua, npd, (const uint32_t *)nullptr, 0u, 0u,
+                           h->loadword);
+        hipLaunchKernelGGL(check_snapshot_kernel, dim3(grid_for(npd, 256, 4096)), dim3(256), 0, st,
+                           (const uint8_t *)b, (const float *)ub, npd, (const uint32_t *)nullptr, 0u, 0u,
+                           h->loadword);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = hipMemcpyAsync(&bad, h->loadword, 4, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess || bad) {
+        drop();
+        return e != hipSuccess ? fail(h, NETKV_EDEVICE, "route map upload failed: %s", hipGetErrorString(e))
+                               : fail(h, NETKV_EINVAL, "invalid route map:%s%s", (bad & 1) ? " tier value > 3" : "",
+                                      (bad & 2) ? " util outside [0,1) or NaN" : "");
+    }
+    dfree(h->rt1);
+    dfree(h->rt2);
+    dfree(h->ru1);
+    dfree(h->ru2);
+    h->rt1 = a;
+    h->rt2 = b;
+    h->ru1 = ua;
+    h->ru2 = ub;
+    h->have_route = true;
+    return NETKV_OK;
+}
+
+netkv_status netkv_route2_clear(netkv_handle h) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    DeviceGuard g(h->device);
+    dfree(h->rt1);
+    dfree(h->rt2);
+    dfree(h->ru1);
+    dfree(h->ru2);
+    h->rt1 = h->rt2 = nullptr;
+    h->ru1 = h->ru2 = nullptr;
+    h->have_route = false;
+    return NETKV_OK;
+}
+
+netkv_status netkv_route2_of(netkv_handle h, const netkv_requests_t *req, uint32_t k, const int32_t *idx,
+                             int8_t *out_route, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    netkv_status st = check_requests(h, req);
+    if (st) return st;
+    if (k < 1 || k > 8) return fail(h, NETKV_EINVAL, "k must be in [1, 8]");
+    if (req->n_req && (!idx || !out_route)) return fail(h, NETKV_EINVAL, "idx and out_route must not be NULL");
+    if ((st = ready(h))) return st;
+    if (!h->have_route) return fail(h, NETKV_ENOTREADY, "no route maps loaded (netkv_route2_load)");
+    if (req->n_req == 0) return NETKV_OK;
+    DeviceGuard g(h->device);
+    hipStream_t s = (hipStream_t)stream;
+    Snap sn = make_snap(h);
+    const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
+    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, s, sn, h->sl, h->dbase,
+                       h->dxlim);
+    hipLaunchKernelGGL(derive_route_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, s, sn,
+                       (const uint8_t *)h->rt1, (const float *)h->ru1, (const uint8_t *)h->rt2,
+                       (const float *)h->ru2, h->sr);
+    sn.sr = h->sr;
+    const uint64_t n = (uint64_t)req->n_req * k;
+    hipLaunchKernelGGL(route_of_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, sn, make_table(h),
+                       make_reqs(req), k, idx, out_route);
+    HIPCHK(h, hipGetLastError());
     return NETKV_OK;
 }
 
@@ -2877,7 +3058,7 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
         po.score = pairs->score;
         want_pairs = po.j || po.feas || po.score;
     }
-    return run_select(h, req, k, out_idx, out_score, po, want_pairs, 0xFFFFFFFFu, s);
+    return run_select(h, req, k, out_idx, out_score, po, want_pairs, 0xFFFFFFFFu, s, true);
 }
 
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen, const float *util_scen,

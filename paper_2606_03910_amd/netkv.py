@@ -63,6 +63,11 @@ _SIGS = {
     "netkv_oracle_set_util": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p]),
     "netkv_congestion_smooth": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_float, C.c_void_p]),
     "netkv_congestion_get": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p]),
+    "netkv_route2_load": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                      C.c_void_p]),
+    "netkv_route2_clear": (C.c_int32, [C.c_void_p]),
+    "netkv_route2_of": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32, C.c_void_p,
+                                    C.c_void_p, C.c_void_p]),
     "netkv_cache_load": (C.c_int32, [C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p, C.c_uint64,
                                      C.c_float, C.c_void_p]),
     "netkv_select_batch": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
@@ -200,6 +205,26 @@ def netkv_congestion_smooth(h: int, obs: torch.Tensor, beta: float, device) -> N
 
 def netkv_congestion_get(h: int, out: torch.Tensor, device) -> None:
     _check(h, load_library().netkv_congestion_get(h, _dptr(out, torch.float32, name="out"), _stream(device)))
+
+
+def netkv_route2_load(h: int, tier1: torch.Tensor, util1: torch.Tensor, tier2: torch.Tensor,
+                      util2: torch.Tensor, device) -> None:
+    _check(h, load_library().netkv_route2_load(
+        h, _dptr(tier1, torch.uint8, name="tier1"), _dptr(util1, torch.float32, name="util1"),
+        _dptr(tier2, torch.uint8, name="tier2"), _dptr(util2, torch.float32, name="util2"), _stream(device)))
+
+
+def netkv_route2_clear(h: int) -> None:
+    _check(h, load_library().netkv_route2_clear(h))
+
+
+def netkv_route2_of(h: int, req: Dict[str, torch.Tensor], k: int, idx: torch.Tensor, out_route: torch.Tensor,
+                    device) -> None:
+    r = _requests(req)
+    _check(h, load_library().netkv_route2_of(h, C.byref(r), int(k),
+                                             _dptr(idx, torch.int32, r.n_req * k, "idx"),
+                                             _dptr(out_route, torch.int8, r.n_req * k, "out_route"),
+                                             _stream(device)))
 
 
 def netkv_cache_load(h: int, n_decode: int, hash_off: torch.Tensor, hashes: torch.Tensor,
@@ -411,6 +436,24 @@ class Selector:
             out.update(pairs=pp)
         netkv_select_batch(self.h, req_dev, k, out["idx"], out["score"], pp, dev)
         return out
+
+    def load_routes(self, tier1, util1, tier2, util2) -> None:
+        """Staged (two-hop) routes per (p, d): hop tiers and congestion [P*D]."""
+        dev = self.device
+        netkv_route2_load(self.h, to_device(np.asarray(tier1, np.uint8).reshape(-1), dev),
+                          to_device(np.asarray(util1, np.float32).reshape(-1), dev),
+                          to_device(np.asarray(tier2, np.uint8).reshape(-1), dev),
+                          to_device(np.asarray(util2, np.float32).reshape(-1), dev), dev)
+
+    def clear_routes(self) -> None:
+        netkv_route2_clear(self.h)
+
+    def routes_of(self, req_dev, idx: torch.Tensor, k: int) -> np.ndarray:
+        """1 where a selection takes its staged route, 0 direct, -1 none."""
+        n = int(req_dev["prefill"].numel())
+        out = torch.empty(n * k, dtype=torch.int8, device=self.device)
+        netkv_route2_of(self.h, req_dev, k, idx, out, self.device)
+        return to_numpy(out)
 
     def rank_sweep(self, req_dev, util_scen: torch.Tensor, k: int = 3):
         n = int(req_dev["prefill"].numel())

@@ -475,3 +475,22 @@ def scenario_utils(cfg: Config, seed: int, links: Dict[str, np.ndarray],
             noisy[key] = np.minimum(u * np.exp(sg * rng.standard_normal(len(u))), 0.99)
         out[s] = pair_util(cfg.cluster, noisy).reshape(-1)
     return out, sig
+
+
+# --------------------------------------------------------------------------
+# staged (two-hop) routes
+# --------------------------------------------------------------------------
+
+def make_routes(cfg: Config, seed: int) -> Dict[str, np.ndarray]:
+    """A staged route p -> staging store -> d for every pair, as maps of the
+    snapshot's shape [P*D]: the first hop (prefill to a host-memory or SSD
+    store) on a leaf, pod or cross-pod link (tier 1..3), the second (store
+    to decode) on a same-node or same-leaf link (tier 0..1), and each hop's
+    congestion uniform on [0, 0.9).  Staged routes then beat congested
+    direct ones on the slow tiers and lose on the fast ones."""
+    rng = _rng(seed, 71)
+    n = cfg.n_prefill * cfg.n_decode
+    return dict(route_tier1=rng.integers(1, 4, n).astype(np.uint8),
+                route_util1=rng.uniform(0.0, 0.9, n).astype(np.float32),
+                route_tier2=rng.integers(0, 2, n).astype(np.uint8),
+                route_util2=rng.uniform(0.0, 0.9, n).astype(np.float32))

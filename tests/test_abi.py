@@ -11,7 +11,7 @@ def _declared():
     with open(os.path.join(ROOT, "include", "netkv.h")) as f:
         src = f.read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(netkv_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(netkv_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_declares_the_boundary():

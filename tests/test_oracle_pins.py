@@ -665,3 +665,128 @@ def test_smoothing_stays_between_forecast_and_observation_and_skips_invalid():
     assert ((c1[~keep] >= lo[~keep]) & (c1[~keep] <= hi[~keep])).all()
     # the step moves 40 % of the way: c1 - c0 = 0.4 (obs - c0)
     np.testing.assert_allclose((c1 - c0)[~keep], 0.4 * (o - c0)[~keep], rtol=1e-12, atol=1e-15)
+
+
+# ---- two-hop routing (Sec. VIII; reading: the staged route's transfer time
+# is the sum of its hops' Eq. (3) times, the pair takes the faster route)
+
+def _routes(t1, u1, t2, u2):
+    return dict(route_tier1=np.asarray(t1, np.uint8), route_util1=np.asarray(u1, np.float32),
+                route_tier2=np.asarray(t2, np.uint8), route_util2=np.asarray(u2, np.float32))
+
+
+def test_two_hop_hand_worked_example():
+    """10 GB to move (10 tokens of 1 GB, nothing cached).  d0: direct on the
+    1 GB/s tier, 10 s + 0.03 s; staged over a 10 GB/s hop at half load with
+    one transfer in flight (2.5 GB/s: 4 s + 0.01 s) and a 5 GB/s hop at 20 %
+    load (4 GB/s: 2.5 s + 0.02 s) = 6.53 s, so it goes staged.  d1: direct
+    on the 5 GB/s tier, 2 s + 0.02 s; its staged route is d0's, slower."""
+    snap = tiny_snapshot(1, 2, [3, 2], [0.0, 0.0], bw=(1e12, 1e10, 5e9, 1e9),
+                         lat=(0.0, 0.01, 0.02, 0.03), n_inflight=[0, 1, 0, 0], alpha=0.0,
+                         bpt=10 ** 9)
+    snap.update(_routes([1, 1], [0.5, 0.5], [2, 2], [0.2, 0.2]))
+    rq = requests([(0, 10, list(range(31, 41)))])
+    out = oracle.select(snap, caches([[], []]), rq, k=2, pairs=True)
+    assert out["idx"][0].tolist() == [1, 0]
+    np.testing.assert_allclose(out["cost"][0], [6.53, 2.02], rtol=1e-7)
+    np.testing.assert_allclose(out["score"][0], [2.02, 6.53], rtol=1e-7)
+    assert oracle.route_of(snap, caches([[], []]), rq, out["idx"], 2).tolist() == [0, 1]
+
+
+def test_two_hop_exact_tie_goes_direct():
+    """Direct at 5 GB/s (2 s) against two 10 GB/s hops (1 s + 1 s): equal in
+    binary floating point, so the direct route is kept."""
+    snap = tiny_snapshot(1, 1, [2], [0.0], bw=(1e10, 1e10, 5e9, 1e9), alpha=0.0, bpt=10 ** 9)
+    snap.update(_routes([0], [0.0], [1], [0.0]))
+    rq = requests([(0, 10, list(range(31, 41)))])
+    out = oracle.select(snap, caches([[]]), rq, k=1, pairs=True)
+    assert out["cost"][0, 0] == 2.0
+    assert oracle.route_of(snap, caches([[]]), rq, out["idx"], 1).tolist() == [0]
+    # one byte per second faster on the second hop: staged, strictly cheaper
+    snap["tier_bw"] = np.array([1e10, 1e10 + 1, 5e9, 1e9])
+    out = oracle.select(snap, caches([[]]), rq, k=1, pairs=True)
+    assert out["cost"][0, 0] < 2.0
+    assert oracle.route_of(snap, caches([[]]), rq, out["idx"], 1).tolist() == [1]
+
+
+def _random_cluster(seed, P=3, D=7, n_req=40):
+    rng = np.random.default_rng(seed)
+    snap = tiny_snapshot(P, D, rng.integers(0, 4, P * D), rng.uniform(0, 0.9, P * D),
+                         lat=(2e-6, 5e-6, 1e-5, 2e-5), n_inflight=rng.integers(0, 5, 4 * P),
+                         free_mem=rng.integers(0, 40, D) * 10 ** 6, alpha=0.3, bpt=10 ** 5,
+                         block_tokens=4)
+    pool = list(range(1000, 1040))
+    sets = [sorted(rng.choice(pool, rng.integers(0, 30), replace=False).tolist()) for _ in range(D)]
+    rows = []
+    for _ in range(n_req):
+        nb = int(rng.integers(1, 12))
+        rows.append((int(rng.integers(0, P)), 4 * nb - int(rng.integers(0, 4)), pool[:nb]))
+    return snap, caches(sets), requests(rows)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_two_hop_never_raises_a_cost_and_keeps_feasibility(seed):
+    snap, cache, rq = _random_cluster(seed)
+    base = oracle.select(snap, cache, rq, k=3, pairs=True)
+    rng = np.random.default_rng(100 + seed)
+    n = snap["n_prefill"] * snap["n_decode"]
+    snap2 = dict(snap)
+    snap2.update(_routes(rng.integers(0, 4, n), rng.uniform(0, 0.9, n),
+                         rng.integers(0, 4, n), rng.uniform(0, 0.9, n)))
+    two = oracle.select(snap2, cache, rq, k=3, pairs=True)
+    np.testing.assert_array_equal(two["j"], base["j"])
+    np.testing.assert_array_equal(two["feasible"], base["feasible"])
+    assert (two["cost"] <= base["cost"]).all()
+    # the pair cost is the direct one wherever the chosen route is direct
+    full = np.tile(np.arange(snap["n_decode"], dtype=np.int32), (rq["prefill"].size, 1))
+    route = oracle.route_of(snap2, cache, rq, full, snap["n_decode"]).reshape(full.shape)
+    assert set(np.unique(route).tolist()) == {0, 1}
+    np.testing.assert_array_equal(two["cost"][route == 0], base["cost"][route == 0])
+    assert (two["cost"][route == 1] < base["cost"][route == 1]).all()
+    # rejections and the empty top-k slots have no route
+    r = oracle.route_of(snap2, cache, rq, two["idx"], 3)
+    np.testing.assert_array_equal(r < 0, two["idx"].reshape(-1) < 0)
+
+
+def test_two_hop_staged_cost_is_additive_over_hops():
+    """Doubling the bytes to move doubles both hops' serialisation terms:
+    staged(2s) - staged(s) = s (1/b1 + 1/b2) while the latencies cancel; a
+    staging store that replicates the direct route on both hops costs the
+    direct time twice over, so it never wins."""
+    P, D = 1, 4
+    tmap = [0, 1, 2, 3]
+    util = [0.1, 0.3, 0.5, 0.7]
+    lat = (1e-3, 2e-3, 3e-3, 4e-3)
+    snap = tiny_snapshot(P, D, tmap, util, lat=lat, n_inflight=[2, 0, 1, 3], alpha=0.0, bpt=10 ** 6)
+    snap.update(_routes(tmap, util, tmap, util))
+    sizes = [(0, 8, list(range(1, 9))), (0, 16, list(range(1, 17)))]
+    out = oracle.select(snap, caches([[]] * D), requests(sizes), k=4, pairs=True)
+    full = np.tile(np.arange(D, dtype=np.int32), (2, 1))
+    assert (oracle.route_of(snap, caches([[]] * D), requests(sizes), full, D) == 0).all()
+    # staged over two hops, the second without the prefill's in-flight count
+    snap.update(_routes([1, 1, 1, 1], [0.5] * 4, [0, 0, 0, 0], [0.0] * 4))
+    two = oracle.select(snap, caches([[]] * D), requests(sizes), k=4, pairs=True)
+    b1 = 50e9 * 0.5 / (1 + 0)
+    b2 = 900e9
+    hop = lambda s: s / b1 + lat[1] + s / b2 + lat[0]
+    staged = np.array([hop(8e6), hop(16e6)])
+    direct = out["cost"]
+    expect = np.minimum(direct, staged[:, None])
+    np.testing.assert_allclose(two["cost"], expect, rtol=1e-12)
+    assert two["cost"][1, 3] - two["cost"][0, 3] == pytest.approx(8e6 * (1 / b1 + 1 / b2), rel=1e-12)
+
+
+def test_two_hop_leaves_sweep_and_sequential_direct():
+    snap, cache, rq = _random_cluster(9)
+    n = snap["n_prefill"] * snap["n_decode"]
+    snap2 = dict(snap)
+    snap2.update(_routes(np.ones(n), np.zeros(n), np.zeros(n), np.zeros(n)))
+    scen = np.random.default_rng(3).uniform(0, 0.9, (3, n)).astype(np.float32)
+    a = oracle.rank_sweep(snap, cache, rq, scen, k=2)
+    b = oracle.rank_sweep(snap2, cache, rq, scen, k=2)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    s1 = oracle.select_sequential(snap, oracle.Cache(cache), rq, cap=4)
+    s2 = oracle.select_sequential(snap2, oracle.Cache(cache), rq, cap=4)
+    for key in s1:
+        np.testing.assert_array_equal(s1[key], s2[key])
