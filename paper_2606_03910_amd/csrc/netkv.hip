@@ -621,11 +621,10 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
 //
 // Stable LSD radix sort for the batch orders (batches of kSortMinN + 1 to
 // kSortMaxN): tiles of kSortTile positions, one workgroup each, in passes
-// of at most kSortMaxBits digit bits.  A pass takes four kernels:
+// of at most kSortMaxBits digit bits.  A pass takes three kernels:
 // sort_count_kernel counts each tile's digits into cnt[tile][digit];
-// sort_segsum_kernel and sort_offsets_kernel turn every digit's column into
-// exclusive offsets over the tiles (in place; the column is cut into at
-// most kSortSegs segments, summed first) and write the digit totals;
+// sort_colscan_kernel turns every digit's column into exclusive offsets
+// over the tiles (in place) and writes the digit totals;
 // sort_scatter_kernel ranks the tile's elements (each wavefront a quarter
 // of the tile, 64 at a time, equal digits ranked by lane masks), stages
 // them in LDS in output order and writes them out in that order, so that
@@ -639,7 +638,6 @@ constexpr uint32_t kSortMaxBits = 8;
 constexpr uint32_t kSortMaxBins = 1u << kSortMaxBits;
 constexpr uint64_t kSortMaxN = 1ull << 24;
 constexpr uint64_t kSortMinN = 1ull << 16;   // smaller batches: rocPRIM (fewer launches)
-constexpr uint32_t kSortSegs = 32;
 static_assert(kSortMaxBins <= kBlock, "one thread per digit");
 
 __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__restrict__ keys, uint32_t n,
@@ -664,49 +662,47 @@ __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__re
     if (tid < bins) cnt[(uint64_t)blockIdx.x * bins + tid] = h[tid];
 }
 
-// One thread per (segment, digit): the segment's sum of the digit's
-// column (segments of seglen tiles).
-__global__ __launch_bounds__(256) void sort_segsum_kernel(const uint32_t *__restrict__ cnt, uint32_t ntile,
-                                                          uint32_t bits, uint32_t nseg, uint32_t seglen,
-                                                          uint32_t *__restrict__ segsum) {
-    const uint32_t bins = 1u << bits;
-    const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
-    const uint32_t b = g & (bins - 1), sg = g >> bits;
-    if (sg >= nseg) return;
-    const uint32_t t0 = sg * seglen, t1 = t0 + seglen < ntile ? t0 + seglen : ntile;
-    uint32_t sum = 0;
-#pragma unroll 16
-    for (uint32_t t = t0; t < t1; ++t) sum += cnt[(uint64_t)t * bins + b];
-    segsum[sg * bins + b] = sum;
+// Inclusive prefix sum over the 64 lanes of a wavefront.
+__device__ inline uint32_t wave_incl_scan(uint32_t v) {
+    const uint32_t lane = threadIdx.x % kWave;
+#pragma unroll
+    for (uint32_t off = 1; off < (uint32_t)kWave; off <<= 1) {
+        const uint32_t u = __shfl_up(v, off, kWave);
+        if (lane >= off) v += u;
+    }
+    return v;
 }
 
-// One thread per (segment, digit): the exclusive offsets of the segment's
-// tiles (in place), starting from the sums of the earlier segments; the
-// last segment's thread writes the digit total.
-__global__ __launch_bounds__(256) void sort_offsets_kernel(uint32_t *__restrict__ cnt, uint32_t ntile, uint32_t bits,
-                                                           uint32_t nseg, uint32_t seglen,
-                                                           const uint32_t *__restrict__ segsum,
-                                                           uint32_t *__restrict__ tot) {
-    const uint32_t bins = 1u << bits;
-    const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
-    const uint32_t b = g & (bins - 1), sg = g >> bits;
-    if (sg >= nseg) return;
-    uint32_t run = 0;
-#pragma unroll 8
-    for (uint32_t q = 0; q < sg; ++q) run += segsum[q * bins + b];
-    const uint32_t t0 = sg * seglen, t1 = t0 + seglen < ntile ? t0 + seglen : ntile;
-    // loads of 16 tiles first, then their offsets
-    for (uint32_t ta = t0; ta < t1; ta += 16) {
-        uint32_t c[16];
+// One workgroup per digit: the exclusive offsets of the digit's column
+// over the tiles (in place) and the digit total.  Thread t takes kColPer
+// consecutive tiles (fewer at the end), sums them, and the workgroup scans
+// the sums.
+constexpr uint32_t kColPer = (uint32_t)(kSortMaxN / kSortTile / kBlock);
+static_assert(kColPer * kBlock * kSortTile == kSortMaxN, "column scan covers the largest batch");
+__global__ __launch_bounds__(kBlock) void sort_colscan_kernel(uint32_t *__restrict__ cnt, uint32_t ntile,
+                                                              uint32_t bits, uint32_t *__restrict__ tot) {
+    __shared__ uint32_t wsum[kWavesPerBlock];
+    const uint32_t bins = 1u << bits, b = blockIdx.x, t = threadIdx.x;
+    const uint32_t per = (ntile + kBlock - 1) / kBlock;   // <= kColPer
+    const uint32_t t0 = t * per;
+    uint32_t c[kColPer];
+    uint32_t sum = 0;
 #pragma unroll
-        for (uint32_t u = 0; u < 16; ++u) c[u] = ta + u < t1 ? cnt[(uint64_t)(ta + u) * bins + b] : 0u;
-#pragma unroll
-        for (uint32_t u = 0; u < 16; ++u) {
-            if (ta + u < t1) cnt[(uint64_t)(ta + u) * bins + b] = run;
-            run += c[u];
-        }
+    for (uint32_t u = 0; u < kColPer; ++u) {
+        c[u] = (u < per && t0 + u < ntile) ? cnt[(uint64_t)(t0 + u) * bins + b] : 0u;
+        sum += c[u];
     }
-    if (sg == nseg - 1) tot[b] = run;
+    const uint32_t incl = wave_incl_scan(sum);
+    if (t % kWave == kWave - 1) wsum[t / kWave] = incl;
+    __syncthreads();
+    uint32_t run = incl - sum;
+    for (uint32_t q = 0; q < t / kWave; ++q) run += wsum[q];
+#pragma unroll
+    for (uint32_t u = 0; u < kColPer; ++u) {
+        if (u < per && t0 + u < ntile) cnt[(uint64_t)(t0 + u) * bins + b] = run;
+        run += c[u];
+    }
+    if (t == kBlock - 1) tot[b] = run;
 }
 
 // Exclusive scan of the digit totals into bb (bins <= kBlock, one digit
@@ -1999,7 +1995,6 @@ struct netkv_ctx {
     size_t sort_tmp_bytes = 0;
     // the batch sorts' own scratch (batches of up to kSortMaxN requests)
     uint32_t *sort_cnt = nullptr;   // [tiles][kSortMaxBins] digit counts, then offsets
-    uint32_t *sort_seg = nullptr;   // [kSortSegs][kSortMaxBins] segment sums
     uint32_t *sort_tot = nullptr;   // [kSortMaxBins] digit totals
     uint32_t *keys_tmp = nullptr, *vals_tmp = nullptr;   // ping-pong buffers of the passes
     uint64_t *partial = nullptr;
@@ -2208,7 +2203,7 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
         dfree(h->hrec); dfree(h->crec);
         dfree(h->sort_tmp);
-        dfree(h->sort_cnt); dfree(h->sort_seg); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
+        dfree(h->sort_cnt); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
         h->order_cap = 0;
         h->sort_tmp_bytes = 0;
         if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
@@ -2235,7 +2230,6 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
         if (R <= kSortMaxN) {
             const uint64_t ntile = (R + kSortTile - 1) / kSortTile;
             if (dalloc(h->sort_cnt, ntile * kSortMaxBins) != hipSuccess ||
-                dalloc(h->sort_seg, (uint64_t)kSortSegs * kSortMaxBins) != hipSuccess ||
                 dalloc(h->sort_tot, kSortMaxBins) != hipSuccess || dalloc(h->keys_tmp, R) != hipSuccess ||
                 dalloc(h->vals_tmp, R) != hipSuccess)
                 return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
@@ -2286,14 +2280,10 @@ hipError_t sort_pass(netkv_handle h, const uint32_t *kin, const uint32_t *vin, u
                      uint32_t n, uint32_t shift, uint32_t bits, const Pre *hrec, const uint64_t *scanned,
                      const Cold *crec, uint32_t lstride, uint32_t zrow, Hot *hot, Cold *cold, hipStream_t st) {
     if (n == 0) return hipSuccess;
-    const uint32_t ntile = (n + kSortTile - 1) / kSortTile;
-    const uint32_t nseg = std::min(kSortSegs, ntile), seglen = (ntile + nseg - 1) / nseg;
-    const uint32_t cols = nseg << bits;
+    const uint32_t ntile = (n + kSortTile - 1) / kSortTile;   // <= kColPer * kBlock (n <= kSortMaxN)
     hipLaunchKernelGGL(sort_count_kernel, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits, h->sort_cnt);
-    hipLaunchKernelGGL(sort_segsum_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint32_t *)h->sort_cnt,
-                       ntile, bits, nseg, seglen, h->sort_seg);
-    hipLaunchKernelGGL(sort_offsets_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, h->sort_cnt, ntile, bits,
-                       nseg, seglen, (const uint32_t *)h->sort_seg, h->sort_tot);
+    hipLaunchKernelGGL(sort_colscan_kernel, dim3(1u << bits), dim3(kBlock), 0, st, h->sort_cnt, ntile, bits,
+                       h->sort_tot);
     hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(ntile), dim3(kBlock), 0, st, kin, vin, n, shift, bits,
                        (const uint32_t *)h->sort_cnt, (const uint32_t *)h->sort_tot, kout, vout, hrec, scanned, crec,
                        h->block_tokens, lstride, zrow, hot, cold);
@@ -2587,7 +2577,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->bytes);
         dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
         dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial); dfree(h->hv); dfree(h->hv_used);
-        dfree(h->sort_cnt); dfree(h->sort_seg); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
+        dfree(h->sort_cnt); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
         dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
         dfree(h->lead); dfree(h->lead_lam); dfree(h->n_lead); dfree(h->hrec); dfree(h->crec);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
