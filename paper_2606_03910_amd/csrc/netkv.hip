@@ -2168,7 +2168,7 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-constexpr uint32_t kLcpLanes = 8;   // lanes per hash-order position in order_kernel
+constexpr uint32_t kLcpLanes = 4;   // lanes per hash-order position in order_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
 // rocPRIM's radix sorts of the batch-order keys (batches outside the range
