@@ -1152,114 +1152,134 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
     uint32_t pc_bits = 0xFFFFFFFFu, pc_idx = 0xFFFFFFFFu;   // gathered keys (empty = ~0)
 
-    for (uint32_t g0 = i0; g0 < i1; g0 += kPer) {
-        const uint32_t g1 = (g0 + kPer < i1) ? g0 + kPer : i1;
-        for (uint32_t i = g0; i < g1; ++i) {
-            const Hot c2 = load_hot(hot, i + 2);
-            // the next request's leader values, if its leader row differs
-            const bool nl = c1.lrow != c0.lrow;
-            if (nl) {
+    // one request: scoring-order position i, its record and the next one's
+    // (whose leader values are fetched while i is scored)
+    auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt) {
+        // the next request's leader values, if its leader row differs
+        const bool nl = nxt.lrow != cur.lrow;
+        if (nl) {
 #pragma unroll
-                for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, loff[q], c1.lrow);
+            for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, loff[q], nxt.lrow);
+        }
+        if (cur.row != rowcur) {
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                rowv[q] = load_row(slr, voff[q], cur.row);
+                if (TWO) rowv2[q] = load_row(srr, voff[q], cur.row);
             }
-            if (c0.row != rowcur) {
+            rowcur = cur.row;
+        }
+        uint32_t r_out = 0;
+        if (PAIRS) r_out = load_cold(cold, i).r;
+        uint32_t cb[C];
+        if ((int32_t)cur.lams < 0) {
+            // matched on its own from block 0, in integers (exact)
+            const uint32_t r = load_cold(cold, i).r;
+            const uint32_t len = as_const(len_tokens)[r];
+            const uint64_t ha = as_const(hash_off)[r];
+            const uint32_t hn = (uint32_t)(as_const(hash_off)[r + 1] - ha);
+            lmask alive[C];
+            uint32_t lam[C];
 #pragma unroll
-                for (int q = 0; q < C; ++q) {
-                    rowv[q] = load_row(slr, voff[q], c0.row);
-                    if (TWO) rowv2[q] = load_row(srr, voff[q], c0.row);
-                }
-                rowcur = c0.row;
+            for (int q = 0; q < C; ++q) {
+                lam[q] = 0;
+                alive[q] = ~0ull;
             }
-            uint32_t r_out = 0;
-            if (PAIRS) r_out = load_cold(cold, i).r;
-            uint32_t cb[C];
-            if ((int32_t)c0.lams < 0) {
-                // matched on its own from block 0, in integers (exact)
-                const uint32_t r = load_cold(cold, i).r;
-                const uint32_t len = as_const(len_tokens)[r];
-                const uint64_t ha = as_const(hash_off)[r];
-                const uint32_t hn = (uint32_t)(as_const(hash_off)[r + 1] - ha);
-                lmask alive[C];
-                uint32_t lam[C];
+            if (hn)
+                probe_from<W, C>(t, base, chash + ha, hn, 0, alive, lam, bt, holder_uniform(t, chash[ha]));
 #pragma unroll
-                for (int q = 0; q < C; ++q) {
-                    lam[q] = 0;
-                    alive[q] = ~0ull;
+            for (int q = 0; q < C; ++q) {
+                const uint32_t x = len - lam[q];
+                const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
+                const bool feas = (uint64_t)x < xlim;
+                const float cost = __uint_as_float(route_cost<TWO>((float)x, rowv[q], rowv2[q]));
+                if (PAIRS && act[q]) {
+                    const uint64_t o = (uint64_t)r_out * s.D + d[q];
+                    const uint32_t jq = lam[q] / bt;
+                    if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                    if (po.feas) po.feas[o] = feas ? 1 : 0;
+                    if (po.score) po.score[o] = cost;
+                    if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                 }
-                if (hn)
-                    probe_from<W, C>(t, base, chash + ha, hn, 0, alive, lam, bt, holder_uniform(t, chash[ha]));
+                cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
+            }
+        } else {
+            // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
+            const float lenf = __uint_as_float(cur.len);
+            if (!PAIRS && cur.len <= xall) {
+#pragma unroll
+                for (int q = 0; q < C; ++q)
+                    cb[q] = route_cost<TWO>(lenf - __uint_as_float(min(laml[q], cur.lams)), rowv[q], rowv2[q]);
+            } else {
 #pragma unroll
                 for (int q = 0; q < C; ++q) {
-                    const uint32_t x = len - lam[q];
-                    const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
-                    const bool feas = (uint64_t)x < xlim;
-                    const float cost = __uint_as_float(route_cost<TWO>((float)x, rowv[q], rowv2[q]));
+                    const float lam = __uint_as_float(min(laml[q], cur.lams));
+                    const float x = lenf - lam;
+                    const bool feas = x <= xmf[q];
+                    const float cost = __uint_as_float(route_cost<TWO>(x, rowv[q], rowv2[q]));
                     if (PAIRS && act[q]) {
                         const uint64_t o = (uint64_t)r_out * s.D + d[q];
-                        const uint32_t jq = lam[q] / bt;
+                        const uint32_t jq = (uint32_t)lam / bt;
                         if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                         if (po.feas) po.feas[o] = feas ? 1 : 0;
                         if (po.score) po.score[o] = cost;
-                        if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
+                        if (po.jT)
+                            po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                     }
                     cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
                 }
-            } else {
-                // non-cached tokens (Eq. (2) / bpt), feasibility and the cost of Eq. (5)
-                const float lenf = __uint_as_float(c0.len);
-                if (!PAIRS && c0.len <= xall) {
+            }
+        }
+        // the group's K best: least cost bits, then least decode index,
+        // i.e. the lowest lane holding the minimum in the first column
+        // that holds it
+        const uint32_t slot = i - g0;
 #pragma unroll
-                    for (int q = 0; q < C; ++q)
-                        cb[q] = route_cost<TWO>(lenf - __uint_as_float(min(laml[q], c0.lams)), rowv[q], rowv2[q]);
-                } else {
+        for (int r = 0; r < K; ++r) {
+            uint32_t lm = cb[0];
 #pragma unroll
-                    for (int q = 0; q < C; ++q) {
-                        const float lam = __uint_as_float(min(laml[q], c0.lams));
-                        const float x = lenf - lam;
-                        const bool feas = x <= xmf[q];
-                        const float cost = __uint_as_float(route_cost<TWO>(x, rowv[q], rowv2[q]));
-                        if (PAIRS && act[q]) {
-                            const uint64_t o = (uint64_t)r_out * s.D + d[q];
-                            const uint32_t jq = (uint32_t)lam / bt;
-                            if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
-                            if (po.feas) po.feas[o] = feas ? 1 : 0;
-                            if (po.score) po.score[o] = cost;
-                            if (po.jT)
-                                po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
-                        }
-                        cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
-                    }
+            for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
+            const uint32_t mn = wave_min_u32_dpp(lm);
+            if (mn == 0xFFFFFFFFu) break;  // no feasible candidate left (uniform)
+            uint32_t dm = 0;
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                const lmask m = ballot(cb[q] == mn);
+                if (m) {
+                    const uint32_t l = (uint32_t)__builtin_ctzll(m);
+                    dm = base + q * kWave + l;
+                    if (r + 1 < K && lane == l) cb[q] = 0xFFFFFFFFu;
+                    break;
                 }
             }
-            // the group's K best: least cost bits, then least decode index,
-            // i.e. the lowest lane holding the minimum in the first column
-            // that holds it
-            const uint32_t slot = i - g0;
+            pc_bits = write_lane(mn, slot * K + (uint32_t)r, pc_bits);
+            pc_idx = write_lane(dm, slot * K + (uint32_t)r, pc_idx);
+        }
+        if (nl) {
 #pragma unroll
-            for (int r = 0; r < K; ++r) {
-                uint32_t lm = cb[0];
-#pragma unroll
-                for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
-                const uint32_t mn = wave_min_u32_dpp(lm);
-                if (mn == 0xFFFFFFFFu) break;  // no feasible candidate left (uniform)
-                uint32_t dm = 0;
-#pragma unroll
-                for (int q = 0; q < C; ++q) {
-                    const lmask m = ballot(cb[q] == mn);
-                    if (m) {
-                        const uint32_t l = (uint32_t)__builtin_ctzll(m);
-                        dm = base + q * kWave + l;
-                        if (r + 1 < K && lane == l) cb[q] = 0xFFFFFFFFu;
-                        break;
-                    }
-                }
-                pc_bits = write_lane(mn, slot * K + (uint32_t)r, pc_bits);
-                pc_idx = write_lane(dm, slot * K + (uint32_t)r, pc_idx);
-            }
-            if (nl) {
-#pragma unroll
-                for (int q = 0; q < C; ++q) laml[q] = stg[q];
-            }
+            for (int q = 0; q < C; ++q) laml[q] = stg[q];
+        }
+    };
+
+    for (uint32_t g0 = i0; g0 < i1; g0 += kPer) {
+        const uint32_t g1 = (g0 + kPer < i1) ? g0 + kPer : i1;
+        uint32_t i = g0;
+        // three requests per trip: each record is loaded into the registers
+        // of the one whose step has just ended, so the records rotate
+        // without copies
+        for (; i + 3 <= g1; i += 3) {
+            const Hot c2 = load_hot(hot, i + 2);
+            step(i, g0, c0, c1);
+            const Hot c3 = load_hot(hot, i + 3);
+            step(i + 1, g0, c1, c2);
+            const Hot c4 = load_hot(hot, i + 4);
+            step(i + 2, g0, c2, c3);
+            c0 = c3;
+            c1 = c4;
+        }
+        for (; i < g1; ++i) {
+            const Hot c2 = load_hot(hot, i + 2);
+            step(i, g0, c0, c1);
             c0 = c1;
             c1 = c2;
         }
