@@ -1154,7 +1154,7 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
 
     // one request: scoring-order position i, its record and the next one's
     // (whose leader values are fetched while i is scored)
-    auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt) {
+    auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt, Hot &ahead) {
         // the next request's leader values, if its leader row differs
         const bool nl = nxt.lrow != cur.lrow;
         if (nl) {
@@ -1169,6 +1169,11 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
             }
             rowcur = cur.row;
         }
+        // the record two ahead, issued after the last use of the loaded
+        // records' fields (scalar loads complete out of order, so a use
+        // after it would wait for it)
+        __builtin_amdgcn_sched_barrier(0);
+        ahead = load_hot(hot, i + 2);
         uint32_t r_out = 0;
         if (PAIRS) r_out = load_cold(cold, i).r;
         uint32_t cb[C];
@@ -1268,18 +1273,16 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
         // of the one whose step has just ended, so the records rotate
         // without copies
         for (; i + 3 <= g1; i += 3) {
-            const Hot c2 = load_hot(hot, i + 2);
-            step(i, g0, c0, c1);
-            const Hot c3 = load_hot(hot, i + 3);
-            step(i + 1, g0, c1, c2);
-            const Hot c4 = load_hot(hot, i + 4);
-            step(i + 2, g0, c2, c3);
+            Hot c2, c3, c4;
+            step(i, g0, c0, c1, c2);
+            step(i + 1, g0, c1, c2, c3);
+            step(i + 2, g0, c2, c3, c4);
             c0 = c3;
             c1 = c4;
         }
         for (; i < g1; ++i) {
-            const Hot c2 = load_hot(hot, i + 2);
-            step(i, g0, c0, c1);
+            Hot c2;
+            step(i, g0, c0, c1, c2);
             c0 = c1;
             c1 = c2;
         }
