@@ -634,11 +634,14 @@ constexpr uint32_t kSortTile = 4096;
 constexpr uint32_t kSortPer = kSortTile / kBlock;                          // positions per thread
 constexpr uint32_t kSortQuarter = kSortTile / kWavesPerBlock;              // positions per wavefront
 constexpr uint32_t kSortSteps = kSortQuarter / kWave;                      // 64-position steps of a wavefront
-constexpr uint32_t kSortMaxBits = 8;
+constexpr uint32_t kSortMaxBits = 11;   // widest pass: the prefill order of up to 2,047 prefills in one
 constexpr uint32_t kSortMaxBins = 1u << kSortMaxBits;
+constexpr uint32_t kSortPassBits = 8;   // passes of the hash order and the general pair sort (faster per bit)
+constexpr uint32_t kSortBinsPer = kSortMaxBins / kBlock;   // digits per thread at the widest pass
+constexpr uint32_t kPrefillMaxBits = 16;   // prefill keys of more bits: rocPRIM's sort and a gather
 constexpr uint64_t kSortMaxN = 1ull << 24;
 constexpr uint64_t kSortMinN = 1ull << 16;   // smaller batches: rocPRIM (fewer launches)
-static_assert(kSortMaxBins <= kBlock, "one thread per digit");
+static_assert(kSortBinsPer * kBlock == kSortMaxBins, "digits split evenly over the threads");
 
 __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__restrict__ keys, uint32_t n,
                                                             uint32_t shift, uint32_t bits,
@@ -646,7 +649,7 @@ __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__re
     __shared__ uint32_t h[kSortMaxBins];
     const uint32_t bins = 1u << bits, mask = bins - 1;
     const uint32_t tid = threadIdx.x;
-    if (tid < bins) h[tid] = 0;
+    for (uint32_t b = tid; b < bins; b += kBlock) h[b] = 0;
     __syncthreads();
     const uint64_t e0 = (uint64_t)blockIdx.x * kSortTile + tid;
     uint32_t kr[kSortPer];   // the thread's keys, all loads issued first
@@ -659,7 +662,7 @@ __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__re
     for (uint32_t x = 0; x < kSortPer; ++x)
         if (e0 + (uint64_t)x * kBlock < n) atomicAdd(h + ((kr[x] >> shift) & mask), 1u);
     __syncthreads();
-    if (tid < bins) cnt[(uint64_t)blockIdx.x * bins + tid] = h[tid];
+    for (uint32_t b = tid; b < bins; b += kBlock) cnt[(uint64_t)blockIdx.x * bins + b] = h[b];
 }
 
 // Inclusive prefix sum over the 64 lanes of a wavefront.
@@ -705,21 +708,32 @@ __global__ __launch_bounds__(kBlock) void sort_colscan_kernel(uint32_t *__restri
     if (t == kBlock - 1) tot[b] = run;
 }
 
-// Exclusive scan of the digit totals into bb (bins <= kBlock, one digit
-// per thread).
-__device__ inline void digit_bases(const uint32_t *__restrict__ tot, uint32_t bins, uint32_t *bb) {
-    __shared__ uint32_t part[kBlock];
+// Exclusive prefix sum of v[0, bins) in LDS, in place, by the whole
+// workgroup: thread t takes consecutive digits t*per .. t*per + per - 1
+// (per = bins / kBlock, at least 1), the wavefronts scan the threads' sums
+// with lane shuffles, then the four wavefront totals are added.
+__device__ inline void lds_exclusive_scan(uint32_t *v, uint32_t bins) {
+    __shared__ uint32_t wsum[kWavesPerBlock];
     const uint32_t t = threadIdx.x;
-    const uint32_t v = t < bins ? tot[t] : 0u;
-    part[t] = v;
-    __syncthreads();
-    for (uint32_t off = 1; off < kBlock; off <<= 1) {   // inclusive scan
-        const uint32_t add = t >= off ? part[t - off] : 0u;
-        __syncthreads();
-        part[t] += add;
-        __syncthreads();
+    const uint32_t per = bins > (uint32_t)kBlock ? bins / kBlock : 1u;
+    const uint32_t b0 = t * per;
+    uint32_t loc[kSortBinsPer];
+    uint32_t sum = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kSortBinsPer; ++u) {
+        loc[u] = (u < per && b0 + u < bins) ? v[b0 + u] : 0u;
+        sum += loc[u];
     }
-    if (t < bins) bb[t] = part[t] - v;
+    const uint32_t incl = wave_incl_scan(sum);
+    if (t % kWave == kWave - 1) wsum[t / kWave] = incl;
+    __syncthreads();
+    uint32_t run = incl - sum;
+    for (uint32_t q = 0; q < t / kWave; ++q) run += wsum[q];
+#pragma unroll
+    for (uint32_t u = 0; u < kSortBinsPer; ++u) {
+        if (u < per && b0 + u < bins) v[b0 + u] = run;
+        run += loc[u];
+    }
     __syncthreads();
 }
 
@@ -759,9 +773,11 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
     const uint32_t bins = 1u << bits, mask = bins - 1;
     const uint32_t tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
     const uint64_t t0 = (uint64_t)blockIdx.x * kSortTile;
-    digit_bases(tot, bins, bb);
-    if (tid < bins) bb[tid] += cnt[(uint64_t)blockIdx.x * bins + tid];
+    for (uint32_t b = tid; b < bins; b += kBlock) bb[b] = tot[b];
     for (uint32_t b = lane; b < bins; b += kWave) hist[w][b] = 0;
+    __syncthreads();
+    lds_exclusive_scan(bb, bins);   // the digits' first output positions
+    for (uint32_t b = tid; b < bins; b += kBlock) bb[b] += cnt[(uint64_t)blockIdx.x * bins + b];
     if (ASSEMBLE && blockIdx.x == 0 && tid < kHotPad) hot[(uint64_t)n + tid] = Hot{0, zrow, 0, 0};
     // this wavefront's quarter of the tile: keys and values, loads first
     const uint64_t e0 = t0 + (uint64_t)w * kSortQuarter + lane;
@@ -785,29 +801,18 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
     }
     __syncthreads();
     // per digit: the wavefronts' prefixes (in place) and the tile count
-    if (tid < bins) {
+    for (uint32_t b = tid; b < bins; b += kBlock) {
         uint32_t run = 0;
 #pragma unroll
         for (uint32_t q = 0; q < kWavesPerBlock; ++q) {
-            const uint32_t c = hist[q][tid];
-            hist[q][tid] = run;
+            const uint32_t c = hist[q][b];
+            hist[q][b] = run;
             run += c;
         }
-        toff[tid] = run;
+        toff[b] = run;
     }
     __syncthreads();
-    // exclusive scan of the tile counts over the digits
-    {
-        const uint32_t v = tid < bins ? toff[tid] : 0u;
-        for (uint32_t off = 1; off < bins; off <<= 1) {
-            const uint32_t add = (tid < bins && tid >= off) ? toff[tid - off] : 0u;
-            __syncthreads();
-            if (tid < bins) toff[tid] += add;
-            __syncthreads();
-        }
-        if (tid < bins) toff[tid] -= v;
-        __syncthreads();
-    }
+    lds_exclusive_scan(toff, bins);   // the digits' first staging slots
     // stage in output order
 #pragma unroll
     for (uint32_t x = 0; x < kSortSteps; ++x) {
@@ -2325,12 +2330,12 @@ inline void pass_bits(uint32_t nbits, uint32_t passes, uint32_t p, uint32_t &shi
 
 // Stable sort of n (key, value) pairs on key bits [0, nbits) (values: vin,
 // or the input positions when vin is null), in passes of at most
-// kSortMaxBits through the handle's ping-pong buffers; the result lands in
+// kSortPassBits through the handle's ping-pong buffers; the result lands in
 // kout / vout (kSortMinN < n <= kSortMaxN).
 hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
                             uint32_t *vout, uint32_t n, uint32_t nbits, hipStream_t st) {
     if (n == 0) return hipSuccess;
-    const uint32_t passes = std::max(1u, (nbits + kSortMaxBits - 1) / kSortMaxBits);
+    const uint32_t passes = std::max(1u, (nbits + kSortPassBits - 1) / kSortPassBits);
     const uint32_t *sk = kin, *sv = vin;
     for (uint32_t p = 0; p < passes; ++p) {
         uint32_t shift, bits;
@@ -2348,7 +2353,7 @@ hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t 
 }
 
 // The prefill order: a stable sort of the hash-order positions by the
-// prefill key (pbits <= 2 * kSortMaxBits), whose last pass writes the
+// prefill key (pbits <= kPrefillMaxBits), whose last pass writes the
 // scoring records at their output positions; earlier passes go through
 // buf_k / buf_v (free at this point of a selection).
 hipError_t prefill_order(netkv_handle h, uint32_t n, uint32_t pbits, uint32_t *buf_k, uint32_t *buf_v,
@@ -2501,7 +2506,7 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
     const uint64_t hvcap = h->lead_cap_opt ? std::min<uint64_t>(h->hv_cap, h->lead_cap_opt) : h->hv_cap;
     // the prefill order: the own sort (positions as its values), or rocPRIM's on pval
     const uint32_t pbits = bits_for(h->P);
-    const bool own_prefill = own_sort && pbits <= 2 * kSortMaxBits;
+    const bool own_prefill = own_sort && pbits <= kPrefillMaxBits;
     hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
                        h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
                        (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg, h->pkey,
