@@ -76,3 +76,64 @@ def test_full_size_sampled(nk, name, n_sample):
                 nk.to_numpy(p["score"]), o)
     assert o["j"].max() > 0
     sel.close()
+
+
+def _sentinel_select(nk, sel, req, k):
+    """Top-k of every request into outputs pre-filled with a sentinel: a
+    request that the batch orders lost or duplicated would keep it."""
+    n = len(req["prefill"])
+    out = dict(idx=torch.full((n * k,), -7, dtype=torch.int32, device=sel.device),
+               score=torch.full((n * k,), -7.0, dtype=torch.float32, device=sel.device))
+    sel.select(nk.requests_to_device(req, sel.device), k=k, out=out)
+    sel.sync_errors()
+    idx = nk.to_numpy(out["idx"]).reshape(-1, k)
+    sc = nk.to_numpy(out["score"]).reshape(-1, k)
+    assert not (idx == -7).any() and not (sc == -7.0).any(), "a request's result was never written"
+    return idx, sc
+
+
+def test_batch_sort_path_every_request(nk):
+    """150,000 requests (above the 65,536 where the library's own batch
+    sorts take over, 37 tiles with a ragged last one) on 48 decodes: every
+    request against the oracle."""
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=150000)
+    snap = W.make_snapshot(cfg, 21, inflight="random")
+    ch = W.prefix_chains(cfg, 21)
+    req = W.make_requests(cfg, 21, chains=ch)
+    cache = W.make_caches(cfg, 21, chains=ch)
+    _say("own-sort batch: 150,000 x 48")
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    idx, sc = _sentinel_select(nk, sel, req, 3)
+    o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=16)
+    n, near = check_topk(idx, sc, o["idx"], o["cost"], o["feasible"])
+    assert n > 0.99 * 3 * cfg.n_requests and near <= max(2, n // 1000)
+    sel.close()
+
+
+@pytest.mark.timeout(900)
+def test_two_pass_prefill_order(nk):
+    """2,048 prefill instances (8,192 GPUs): the prefill key takes 12 bits,
+    so the prefill order takes two sort passes; 70,000 requests over 6,144
+    decodes, every result written, a seeded sample against the oracle."""
+    cl = W.Cluster(8, 16, 16, 4)
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=cl, n_requests=70000, cache_per_decode=1024)
+    assert cfg.n_prefill == 2048 and cfg.n_decode == 6144
+    snap = W.make_snapshot(cfg, 23)
+    ch = W.prefix_chains(cfg, 23)
+    req = W.make_requests(cfg, 23, chains=ch)
+    cache = W.make_caches(cfg, 23, chains=ch)
+    _say("two-pass prefill order: 70,000 x 6,144")
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    idx, sc = _sentinel_select(nk, sel, req, 1)
+    ok = idx[:, 0] >= 0
+    assert ((idx[:, 0] >= -1) & (idx[:, 0] < cfg.n_decode)).all() and ok.mean() > 0.9
+    assert np.isfinite(sc[ok]).all() and np.isinf(sc[~ok]).all()
+    rows = np.sort(np.random.default_rng(102).choice(cfg.n_requests, 256, replace=False))
+    o = oracle.select(snap, cache, subset_requests(req, rows), k=1, pairs=True, n_threads=16)
+    n, near = check_topk(idx[rows], sc[rows], o["idx"], o["cost"], o["feasible"])
+    assert near <= 2
+    sel.close()
