@@ -970,9 +970,23 @@ __device__ inline void probe_from(const Table &t, uint32_t base, cptr<uint64_t> 
 // word lacks bit l, found by binary search over the words in LDS.  Writes
 // B_tok * j for the task's decodes, in fp32 (exact below 2^24; only
 // requests shorter than that read it, capped by their own length).
-__device__ inline uint64_t shfl_up_u64(uint64_t v, uint32_t delta) {
-    const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, delta, kWave);
-    const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), delta, kWave);
+// Inclusive AND over lanes 0..l of a 32-bit value, in lane l, with DPP:
+// shifts right by 1, 2, 4 and 8 within each row of 16 lanes (a lane with
+// no source takes all ones), then the last lane of row 0 into row 1 and of
+// row 2 into row 3, then the last lane of row 1 into rows 2 and 3.  Every
+// lane must be active.
+__device__ inline uint32_t wave_and_prefix_u32(uint32_t v) {
+    v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x111, 0xF, 0xF, false);   // row_shr 1
+    v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x112, 0xF, 0xF, false);   // row_shr 2
+    v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x114, 0xF, 0xF, false);   // row_shr 4
+    v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x118, 0xF, 0xF, false);   // row_shr 8
+    v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x142, 0xA, 0xF, false);   // row_bcast 15
+    v &= (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, 0x143, 0xC, 0xF, false);   // row_bcast 31
+    return v;
+}
+
+__device__ inline uint64_t wave_and_prefix_u64(uint64_t v) {
+    const uint32_t lo = wave_and_prefix_u32((uint32_t)v), hi = wave_and_prefix_u32((uint32_t)(v >> 32));
     return ((uint64_t)hi << 32) | lo;
 }
 
@@ -1011,12 +1025,7 @@ __global__ __launch_bounds__(kBlock) void lead_kernel(Table t, uint32_t D, uint3
                 const uint32_t o = (v & ~kHeldOne) - base;
                 word = o < (uint32_t)kWave ? 1ull << o : 0ull;
             }
-            uint64_t pref = word & alive;
-#pragma unroll
-            for (uint32_t off = 1; off < (uint32_t)kWave; off <<= 1) {
-                const uint64_t up = shfl_up_u64(pref, off);
-                if (lane >= off) pref &= up;
-            }
+            const uint64_t pref = wave_and_prefix_u64(word & alive);
             pw[wv][lane] = pref;
             __builtin_amdgcn_wave_barrier();
             // lane l: the number of leading words (of nk) holding bit l
