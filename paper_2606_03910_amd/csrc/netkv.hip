@@ -509,12 +509,28 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
         const uint64_t nq = rq.off[q + 1] - b;
         const uint64_t m = nr < nq ? nr : nq;
         l = m;
-        for (uint64_t base = 0; base < m; base += G) {
-            const uint64_t x = base + sub;
-            const bool stop = x >= m || rq.hashes[a + x] != rq.hashes[b + x];
-            const uint32_t bits = (uint32_t)(__ballot(stop) >> seg0) & (uint32_t)((1ull << G) - 1);
+        // each lane compares U consecutive blocks per step, their loads
+        // issued together; the first differing block is the lowest lane's
+        // first stop
+        constexpr uint32_t U = 2;
+        for (uint64_t base = 0; base < m; base += (uint64_t)G * U) {
+            const uint64_t x0 = base + (uint64_t)sub * U;
+            uint64_t hr[U], hq[U];
+#pragma unroll
+            for (uint32_t u = 0; u < U; ++u) {
+                const bool in = x0 + u < m;
+                hr[u] = in ? rq.hashes[a + x0 + u] : 0ull;
+                hq[u] = in ? rq.hashes[b + x0 + u] : 1ull;
+            }
+            uint32_t ls = U;   // this lane's first stop (U: none)
+#pragma unroll
+            for (int u = (int)U - 1; u >= 0; --u)
+                if (hr[u] != hq[u]) ls = (uint32_t)u;
+            const uint32_t bits = (uint32_t)(__ballot(ls < U) >> seg0) & (uint32_t)((1ull << G) - 1);
             if (bits) {
-                const uint64_t first = base + (uint64_t)__builtin_ctz(bits);
+                const uint32_t fl = (uint32_t)__builtin_ctz(bits);
+                const uint32_t lsf = (uint32_t)__shfl((int)ls, (int)(seg0 + fl), kWave);
+                const uint64_t first = base + (uint64_t)fl * U + lsf;
                 l = first < m ? first : m;
                 break;
             }
