@@ -425,7 +425,8 @@ struct Order {
 // A request of more than max_blocks blocks is invalid (calls that keep
 // per-pair prefix lengths in 16 bits pass 65535).  A block hash 0 needs no
 // check: no resident set holds it (cache loads reject it), so it is a miss
-// on every decode, as the prefix definition gives.  Thread 0 clears the
+// on every decode, as the prefix definition gives.  vals (the input
+// positions, for rocPRIM's sort) may be null.  Thread 0 clears the
 // holder-value and leader counters of the order kernel.
 __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max_blocks, uint32_t *__restrict__ keys,
                                                    uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
@@ -451,7 +452,7 @@ __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max
             }
         }
         keys[r] = key;
-        vals[r] = r;
+        if (vals) vals[r] = r;
         bad = !ok;
     }
     if (__ballot(bad) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrRequest);
@@ -2516,11 +2517,11 @@ netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k,
                            (const float *)h->ru2, h->sr);
         sn.sr = h->sr;
     }
+    const bool own_sort = R > kSortMinN && R <= kSortMaxN;   // its first pass takes positions as values
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
-                       h->vals_in, h->errword, h->hv_used, h->n_lead);
+                       own_sort ? nullptr : h->vals_in, h->errword, h->hv_used, h->n_lead);
     HIPCHK(h, hipGetLastError());
     size_t tb = h->sort_tmp_bytes;
-    const bool own_sort = R > kSortMinN && R <= kSortMaxN;
     if (own_sort)
         HIPCHK(h, batch_sort_pairs(h, h->keys_in, nullptr, h->keys_out, h->perm, (uint32_t)R, 32, st));
     else
