@@ -232,3 +232,33 @@ def test_two_hop_full_size_sampled(nk):
     o_route = _check_routes(g_route.reshape(-1, 1)[rows], g["idx"][rows], snap, routes, ocache, sub, 1)
     assert 0 < (o_route == 1).sum() < o_route.size
     sel.close()
+
+
+def test_two_hop_leaves_sweep_and_sequential_direct(nk):
+    """Only the batch selection takes staged routes: the ranking sweep and
+    the sequential form give the same bits with and without route maps."""
+    _say("two-hop: sweep and sequential unchanged")
+    cfg = W.scaled(W.CONFIGS["c0"], cluster=W.Cluster(8, 2, 2, 2), n_requests=1000)
+    snap, req, cache, routes = _inputs(cfg, 59)
+    plain = nk.Selector(0)
+    plain.load_snapshot(snap)
+    plain.load_cache(cache, 0.5)
+    sel = _selector(nk, snap, cache, routes)
+    scen = torch.from_numpy(np.random.default_rng(5).uniform(0, 0.9, (4, cfg.n_prefill * cfg.n_decode))
+                            .astype(np.float32)).to(sel.device)
+    outs = []
+    for s_ in (plain, sel):
+        rd = nk.requests_to_device(req, s_.device)
+        sw = s_.rank_sweep(rd, scen, k=2)
+        sq = s_.select_sequential(rd, cap=4)
+        s_.sync_errors()
+        outs.append([nk.to_numpy(sw["idx"]), nk.to_numpy(sw["score"]).view(np.uint32), nk.to_numpy(sw["flips"]),
+                     nk.to_numpy(sq["idx"]), nk.to_numpy(sq["score"]).view(np.uint32)])
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
+    # the batch selection itself does change
+    g0 = _select(nk, plain, req, 1, pairs=True)
+    g1 = _select(nk, sel, req, 1, pairs=True)
+    assert (g1["cost"] < g0["cost"]).any()
+    sel.close()
+    plain.close()
