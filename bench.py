@@ -120,9 +120,8 @@ def main():
                           "launches": args.steps}), flush=True)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(requests or decodes would be sharded across GPUs; see the design notes). "
-              "Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(requests or decodes would be sharded across GPUs). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -431,7 +430,7 @@ def bench_sweep(args, cfg, dev):
                      "algorithmic_flops_per_launch": flops,
                      "kernel": "sweep_kernel<4> (k=3)",
                      "note": "7 fp32 operations per scenario-pair of Eqs. (3)-(5); the peak counts "
-                             "packed fp32, which this build does not emit"},
+                             "packed fp32, which the library is compiled without"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -27,9 +27,9 @@
  *   Every request is scored against the same snapshot (the in-flight counter
  *   update of Algorithm 1 happens between batches, see orc_commit).
  *
- * Readings where the paper is silent are listed in the design notes of the
- * repository: congestion is given per (p, d) pair; the block size is a
- * parameter; all decodes are matched before the feasibility filter.
+ * Readings where the paper is silent: congestion is given per (p, d) pair;
+ * the block size is a parameter; all decodes are matched before the
+ * feasibility filter.
  */
 #include <math.h>
 #include <stdint.h>
