@@ -5,7 +5,7 @@ import pytest
 
 import oracle
 from paper_2606_03910_amd import workload as W
-from tests.parity import check_pairs, check_topk, subset_requests
+from tests.parity import check_pairs, check_self_topk, check_topk, subset_requests
 
 pytestmark = pytest.mark.gpu
 
@@ -52,6 +52,19 @@ def _run(nk, sel, req, k, pairs=True):
     return res
 
 
+def _check_all(g, o):
+    """Per-pair outputs against the oracle, the selections against the
+    oracle (near-tie rule, exact ties to the lowest index), and the
+    selections against the exact top-k of the GPU's own per-pair scores."""
+    err = check_pairs(g["j"], g["feas"], g["cost"], o)
+    R, k = g["idx"].shape
+    D = o["j"].shape[1]
+    res = check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"],
+                     g_cost=g["cost"].reshape(R, D))
+    check_self_topk(g["idx"], g["score"], g["cost"].reshape(R, D), g["feas"].reshape(R, D))
+    return res, err
+
+
 @pytest.mark.parametrize("inflight", ["zero", "random"])
 @pytest.mark.parametrize("k", [1, 3, 8])
 def test_c0_full_parity(nk, inflight, k):
@@ -61,8 +74,7 @@ def test_c0_full_parity(nk, inflight, k):
     sel = _gpu(nk, snap, cache)
     g = _run(nk, sel, req, k)
     o = oracle.select(snap, cache, req, k=k, pairs=True, n_threads=8)
-    check_pairs(g["j"], g["feas"], g["cost"], o)
-    n, near = check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    (n, near), _ = _check_all(g, o)
     assert n > 0.99 * cfg.n_requests * k
     g2 = _run(nk, sel, req, k, pairs=False)
     assert np.array_equal(g2["idx"], g["idx"])
@@ -82,15 +94,14 @@ def test_c0_load_terms_and_memory_pressure(nk):
     g = _run(nk, sel, req, 4)
     o = oracle.select(snap, cache, req, k=4, pairs=True, n_threads=8)
     assert 0.05 < 1 - o["feasible"].mean() < 0.9
-    check_pairs(g["j"], g["feas"], g["cost"], o)
-    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    _check_all(g, o)
     sel.close()
 
 
 def test_ragged_decodes_long_runs_and_empty_runs(nk):
     """90 decodes (a full and a partial wavefront of decodes), 16-token
-    blocks so runs exceed the LDS staging length, and requests shorter than
-    one block (empty runs)."""
+    blocks so that runs exceed 256 blocks (several 64-block steps of the
+    leader kernel), and requests shorter than one block (empty runs)."""
     _say("ragged decodes / long runs")
     cl = W.Cluster(8, 5, 1, 3)
     cfg = W.scaled(W.CONFIGS["c0"], cluster=cl, block_tokens=16, n_requests=700,
@@ -108,8 +119,7 @@ def test_ragged_decodes_long_runs_and_empty_runs(nk):
     sel = _gpu(nk, snap, cache)
     g = _run(nk, sel, req, 3)
     o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
-    check_pairs(g["j"], g["feas"], g["cost"], o)
-    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    _check_all(g, o)
     assert o["j"].max() > 256
     sel.close()
 
@@ -140,8 +150,7 @@ def test_tuning_options_leave_results_unchanged(nk):
                 if base is None:
                     base = g
                     o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
-                    check_pairs(g["j"], g["feas"], g["cost"], o)
-                    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+                    _check_all(g, o)
                     continue
                 for key in base:
                     assert np.array_equal(g[key], base[key]), (cols, rl, reuse, key)
@@ -183,8 +192,7 @@ def test_all_feasible_path_matches_general_path(nk):
     for cols in (0, 1, 2, 3, 6):
         nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, cols)
         g = _run(nk, sel, req, 2)
-        check_pairs(g["j"], g["feas"], g["cost"], o)
-        check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+        _check_all(g, o)
         g2 = _run(nk, sel, req, 2, pairs=False)
         assert np.array_equal(g2["idx"], g["idx"]), cols
         assert np.array_equal(g2["score"].view(np.uint32), g["score"].view(np.uint32)), cols
@@ -214,8 +222,7 @@ def test_dense_tables(nk, lf):
     assert ci["index_slots"] in (2 * buckets, 4 * buckets, 8 * buckets)
     g = _run(nk, sel, req, 2)
     o = oracle.select(snap, cache, req, k=2, pairs=True, n_threads=8)
-    check_pairs(g["j"], g["feas"], g["cost"], o)
-    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    _check_all(g, o)
     sel.close()
 
 
@@ -239,8 +246,7 @@ def test_all_infeasible_and_full_hits(nk):
     o = oracle.select(snap, cache2, req, k=2, pairs=True, n_threads=8)
     n10 = (np.diff(off)[:10])
     assert (o["j"][:10] == n10[:, None]).all()
-    check_pairs(g["j"], g["feas"], g["cost"], o)
-    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    _check_all(g, o)
     # a reserve larger than any free memory rejects every request
     snap2 = dict(snap)
     snap2["m_min"] = 2 ** 63
@@ -446,8 +452,7 @@ def test_requests_across_2_pow_24_tokens(nk):
     long = [0, 1, 2, 3, 4, 6]
     assert o["feasible"][long, 0].all() and not o["feasible"][long, 1:].any()
     g = _run(nk, sel, req, 2)
-    check_pairs(g["j"], g["feas"], g["cost"], o)
-    check_topk(g["idx"], g["score"], o["idx"], o["cost"], o["feasible"])
+    _check_all(g, o)
     g2 = _run(nk, sel, req, 2, pairs=False)
     assert np.array_equal(g2["idx"], g["idx"])
     assert np.array_equal(g2["score"].view(np.uint32), g["score"].view(np.uint32))
@@ -511,4 +516,225 @@ def test_long_runs_and_invalid_requests_in_every_mode(nk):
     for r in (2, 4):
         assert np.array_equal(si[r], idx[r]) and np.array_equal(ss[r], sc[r])
         assert qi[r] == idx[r, 0] and qs[r] == sc[r, 0]
+    sel.close()
+
+
+def _uniform_snapshot(cfg, queue=6, tier=2, util=0.3):
+    """A snapshot on which every decode is identical from every prefill: one
+    tier, one congestion value, one queue depth, batch size and free memory."""
+    P, D = cfg.n_prefill, cfg.n_decode
+    snap = dict(W.params_of(cfg))
+    snap.update(n_prefill=P, n_decode=D, tier_map=np.full(P * D, tier, np.uint8),
+                util=np.full(P * D, util, np.float32), n_inflight=np.zeros(4 * P, np.uint16),
+                free_mem=np.full(D, 100 * 10 ** 9, np.uint64), queue_depth=np.full(D, queue, np.uint32),
+                batch_size=np.full(D, 60, np.uint32))
+    return snap
+
+
+def test_exact_ties_go_to_the_lowest_index(nk):
+    """Algorithm 1's argmin with ties to the lowest decode index, on exact
+    ties spread over lanes, decode columns and decode groups (3,072 decodes,
+    every decodes-per-lane choice, k = 1, 3, 8):
+      * every decode identical: the top-k is decodes 0..k-1;
+      * the decodes of S one queue slot shorter (identical among
+        themselves): S in ascending order, then 0, 1, ...;
+      * S plus decodes of S2 that also hold a request's whole run: the
+        oracle's order, which the GPU must reproduce exactly.
+    The expected lists of the first two cases are written out here; every
+    case is also checked against the oracle and against the exact top-k of
+    the GPU's own per-pair scores."""
+    cfg = W.scaled(W.CONFIGS["c2"], n_requests=200, cache_per_decode=64)
+    D = cfg.n_decode
+    assert D == 3072
+    S = np.array([5, 64 + 5, 3 * 64 + 7, 384 + 2, 2 * 384 + 3 * 64 + 1, 1000, 2047, 3071])
+    S2 = np.array([7, 64 + 9, 700, 3000])
+    ch = W.prefix_chains(cfg, 31)
+    req = W.make_requests(cfg, 31, chains=ch)
+    n_r = np.diff(req["hash_off"].astype(np.int64))
+    rng = np.random.default_rng(31)
+    base_sets = [rng.integers(1, 2 ** 63, 64, dtype=np.uint64) for _ in range(D)]
+    runs = np.unique(np.concatenate([req["hashes"][int(req["hash_off"][r]):int(req["hash_off"][r + 1])]
+                                     for r in range(20)]))
+    rows = np.arange(cfg.n_requests)
+
+    def cache_of(extra):
+        sets = [np.union1d(base_sets[d], runs) if d in extra else base_sets[d] for d in range(D)]
+        return dict(n_decode=D, hash_off=np.concatenate([[0], np.cumsum([len(x) for x in sets])]).astype(np.uint64),
+                    hashes=np.concatenate(sets).astype(np.uint64))
+
+    cases = []
+    snap_a = _uniform_snapshot(cfg)
+    exp_a = np.tile(np.arange(8), (cfg.n_requests, 1))
+    cases.append(("all identical", snap_a, cache_of(set()), exp_a))
+    snap_b = _uniform_snapshot(cfg)
+    snap_b["queue_depth"] = snap_b["queue_depth"].copy()
+    snap_b["queue_depth"][S] = 5   # one blocked request fewer (4 free batch slots)
+    exp_b = np.tile(np.concatenate([np.sort(S), [0, 1, 2, 3]])[:8], (cfg.n_requests, 1))
+    cases.append(("S shorter queues", snap_b, cache_of(set()), exp_b))
+    cases.append(("S and S2 with cached runs", snap_b, cache_of(set(S2.tolist())), None))
+    for name, snap, cache, exp in cases:
+        o = oracle.select(snap, cache, req, k=8, pairs=True, n_threads=8)
+        if exp is not None:
+            assert np.array_equal(o["idx"], exp), name
+        else:
+            # requests 0..19 hold their whole run on S2 (when they have blocks)
+            assert (o["j"][:20][:, S2] == n_r[:20, None]).all()
+        sel = _gpu(nk, snap, cache)
+        for cols in (0, 1, 2, 3, 4, 6):
+            nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, cols)
+            for k in (1, 3, 8):
+                _say("exact ties:", name, "cols", cols, "k", k)
+                g = _run(nk, sel, req, k)
+                ok = o["idx"][:, :k]
+                assert np.array_equal(g["idx"], ok), (name, cols, k)
+                oo = dict(o, idx=ok)
+                _check_all(g, oo)
+                g2 = _run(nk, sel, req, k, pairs=False)
+                assert np.array_equal(g2["idx"], g["idx"]), (name, cols, k)
+        sel.close()
+    del rows
+
+
+def _holed_cache(cfg, ch, wl_seed, seed):
+    """Resident sets that are not prefix-closed: for each decode, segments of
+    the shared chains with holes -- blocks a+1..a+5 without block a, a
+    chain without its block 0, every other block, Bernoulli(0.6) scatter --
+    next to ordinary leading segments, plus private filler."""
+    rng = np.random.default_rng(seed)
+    D = cfg.n_decode
+    S = ch["blocks"]
+    top = np.argsort(-ch["weights"])[:60]
+    sets = []
+    for d in range(D):
+        parts = [rng.integers(1, 2 ** 63, 300, dtype=np.uint64)]
+        for k in top:
+            n = int(S[k])
+            if n == 0 or rng.random() < 0.3:
+                continue
+            kind = rng.integers(0, 5)
+            if kind == 0:      # blocks [0, a) and a+1 .. a+5, hole at a
+                a = int(rng.integers(0, n))
+                blk = np.concatenate([np.arange(0, a), np.arange(a + 1, min(n, a + 6))])
+            elif kind == 1:    # everything but block 0
+                blk = np.arange(1, n)
+            elif kind == 2:    # every other block
+                blk = np.arange(int(rng.integers(0, 2)), n, 2)
+            elif kind == 3:    # scattered
+                blk = np.nonzero(rng.random(n) < 0.6)[0]
+            else:              # an ordinary leading segment
+                blk = np.arange(0, int(rng.integers(1, n + 1)))
+            if blk.size:
+                parts.append(W.block_hash(wl_seed, int(ch["domain"]), np.full(blk.size, k), blk))
+        sets.append(np.unique(np.concatenate(parts)))
+    return dict(n_decode=D, hash_off=np.concatenate([[0], np.cumsum([len(x) for x in sets])]).astype(np.uint64),
+                hashes=np.concatenate(sets).astype(np.uint64))
+
+
+def test_holed_resident_sets(nk):
+    """Resident sets with holes (Sec. III-B: the block LCP is the leading run
+    up to the first miss, and K_d need not be prefix-closed).  Prefix
+    lengths, feasibility and scores bit-exact against the oracle on 270
+    decodes, with and without the batch order's sharing, under every
+    decodes-per-lane choice and a leader table of 3."""
+    cl = W.Cluster(8, 5, 3, 3)
+    cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=3000, cache_per_decode=4096, n_prefixes=80)
+    assert cfg.n_decode == 270
+    seed = 3
+    snap = W.make_snapshot(cfg, seed, inflight="random")
+    ch = W.prefix_chains(cfg, seed)
+    req = W.make_requests(cfg, seed, chains=ch)
+    cache = _holed_cache(cfg, ch, seed, 77)
+    o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
+    # holes matter: some decode holds block j (and beyond) of a request
+    # without holding all blocks before it
+    assert o["j"].max() > 3
+    sel = _gpu(nk, snap, cache)
+    for cols in (0, 1, 3, 6):
+        for reuse in (1, 0):
+            for cap in (0, 3):
+                _say("holed sets cols", cols, "reuse", reuse, "lead cap", cap)
+                nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, cols)
+                nk.netkv_set_option(sel.h, nk.NETKV_OPT_REUSE, reuse)
+                nk.netkv_set_option(sel.h, nk.NETKV_OPT_LEAD_CAP, cap)
+                g = _run(nk, sel, req, 3)
+                _check_all(g, o)
+    sel.close()
+
+
+_GOLDEN = 0x9E3779B97F4A7C15
+_GOLDEN_INV = pow(_GOLDEN, -1, 1 << 64)
+
+
+def _colliding_hashes(rng, n, bucket_bits=19):
+    """n distinct nonzero 64-bit hashes whose Fibonacci products agree in the
+    top bucket_bits bits -- the bits of the first block that the batch
+    order groups requests by -- so that different chains share one group."""
+    y0 = int(rng.integers(0, 1 << 63)) << 1
+    top = (y0 >> (64 - bucket_bits)) << (64 - bucket_bits)
+    out = set()
+    while len(out) < n:
+        y = top | int(rng.integers(0, 1 << (64 - bucket_bits)))
+        h = (y * _GOLDEN_INV) % (1 << 64)
+        if h:
+            out.add(h)
+    hs = np.array(sorted(out), dtype=np.uint64)
+    prods = (hs.astype(object) * _GOLDEN) % (1 << 64)
+    assert len({int(p) >> (64 - bucket_bits) for p in prods}) == 1
+    return hs
+
+
+def test_first_block_key_collisions(nk):
+    """Chains whose first blocks differ but fall in the same group of the
+    batch order (their sort keys agree in the first-block bits): the
+    requests of the chains interleave by length in the hash order, so
+    neighbours share no leading run and every switch starts a leader.  A
+    batch of 70,000 requests (the library's own batch sorts) on 48 decodes:
+    every pair bit-exact against the oracle, every top-3 within the rules."""
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=70000, block_tokens=64)
+    rng = np.random.default_rng(41)
+    snap = W.make_snapshot(cfg, 41, inflight="random")
+    ch = W.prefix_chains(cfg, 41)
+    req = W.make_requests(cfg, 41, chains=ch)
+    D = cfg.n_decode
+    nch, clen = 6, 300
+    firsts = _colliding_hashes(rng, nch)
+    chains = [np.concatenate([[firsts[c]], rng.integers(1, 2 ** 63, clen - 1, dtype=np.uint64)])
+              for c in range(nch)]
+    # 40 % of the requests switch to one of the colliding chains
+    off = req["hash_off"].astype(np.int64)
+    n_r = np.diff(off)
+    pick = np.nonzero((rng.random(cfg.n_requests) < 0.4) & (n_r > 0))[0]
+    hs = req["hashes"].copy()
+    for r in pick:
+        c = chains[int(rng.integers(0, nch))]
+        m = min(int(n_r[r]), clen)
+        hs[off[r]:off[r] + m] = c[:m]
+    req = dict(req, hashes=hs)
+    # decodes hold leading segments of the colliding chains (and some holes)
+    base = W.make_caches(cfg, 41, chains=ch)
+    coff = base["hash_off"].astype(np.int64)
+    sets = []
+    for d in range(D):
+        parts = [base["hashes"][coff[d]:coff[d + 1]]]
+        for c in range(nch):
+            if rng.random() < 0.5:
+                a = int(rng.integers(1, clen + 1))
+                blk = np.arange(a)
+                if rng.random() < 0.3 and a > 3:
+                    blk = np.delete(blk, int(rng.integers(1, a)))
+                parts.append(chains[c][blk])
+        sets.append(np.unique(np.concatenate(parts)))
+    cache = dict(n_decode=D, hash_off=np.concatenate([[0], np.cumsum([len(x) for x in sets])]).astype(np.uint64),
+                 hashes=np.concatenate(sets).astype(np.uint64))
+    o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
+    assert o["j"][pick].max() > 100
+    sel = _gpu(nk, snap, cache)
+    for reuse in (1, 0):
+        _say("first-block key collisions, 70,000 x 48, reuse", reuse)
+        nk.netkv_set_option(sel.h, nk.NETKV_OPT_REUSE, reuse)
+        g = _run(nk, sel, req, 3)
+        _check_all(g, o)
+        g2 = _run(nk, sel, req, 3, pairs=False)
+        assert np.array_equal(g2["idx"], g["idx"])
+        assert np.array_equal(g2["score"].view(np.uint32), g["score"].view(np.uint32))
     sel.close()
