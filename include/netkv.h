@@ -169,13 +169,27 @@ typedef struct {
  * rejects a request with no feasible decode).  out_idx, out_score: [n_req * k] DEVICE arrays.  `pairs` may be
  * NULL.  Asynchronous on `stream`: inputs must stay valid and outputs are
  * defined once the stream completes.  Allocates only when a batch is
- * larger than every earlier one on the handle (its ordering and per-chunk
- * work buffers grow; about 21 + 8*k*ceil(D/64) bytes per request).
+ * larger than the handle's work buffers hold -- every earlier batch's, or
+ * what netkv_reserve sized them for -- and then grows them (about
+ * 100 + 8*K*ceil(D/(64*C)) bytes per request, K the next power of two >= k
+ * and C the decodes per lane, plus 4 bytes per block hash and the leader
+ * table).
  * EINVAL: NULL pointers, k out of range; ENOTREADY: snapshot or cache
  * missing; n_req = 0 is a no-op. */
 netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uint32_t k,
                                 int32_t *out_idx, float *out_score, netkv_pairs_t *pairs,
                                 void *stream);
+
+/* Size the handle's selection work buffers ahead for batches of up to
+ * max_req requests with up to max_hashes block hashes and 1 <= k <= max_k,
+ * so that netkv_select_batch, netkv_rank_sweep and netkv_select_sequential
+ * allocate no selection buffers for such batches afterwards (they grow
+ * them otherwise, when a batch exceeds every earlier one).  Needs a loaded
+ * snapshot (ENOTREADY) and is redone after a snapshot with another decode
+ * count; synchronous with respect to allocation.  ENOMEM when the device
+ * cannot hold them. */
+netkv_status netkv_reserve(netkv_handle h, uint32_t max_req, uint64_t max_hashes, uint32_t max_k,
+                           void *stream);
 
 /* Two-hop KV routing (Sec. VIII, future work: KV state staged through an
  * intermediate cache in CPU DRAM or SSD; the oracle exposes both hops'

@@ -1981,6 +1981,38 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, uint32_t c
     }
 }
 
+// Work buffers of one selection: per-request ordering buffers and records,
+// the leader table, the leaders' holder values, per-group partial top-k
+// keys and the sort / scan temporaries, owned by the handle (grown on
+// demand, or sized ahead by netkv_reserve).
+struct Scratch {
+    uint64_t order_cap = 0;   // requests the per-request buffers hold
+    uint32_t *keys_in = nullptr, *keys_out = nullptr, *vals_in = nullptr, *perm = nullptr;
+    Hot *hot = nullptr;       // [order_cap + kHotPad] scoring-order records, the part every step reads
+    Cold *cold = nullptr;     // and the request's index in the batch
+    uint64_t *seg = nullptr, *scanned = nullptr;   // segmented-scan elements, hash order
+    Pre *hrec = nullptr;      // prefill row and length by hash-order position
+    Cold *crec = nullptr;
+    uint32_t *pkey = nullptr, *pkey_out = nullptr, *pval = nullptr, *pord = nullptr;   // prefill order
+    uint32_t *n_valid = nullptr;
+    unsigned long long *hv_used = nullptr;
+    unsigned int *n_lead = nullptr;
+    uint32_t *hv = nullptr;   // holder values of the leaders' blocks
+    uint64_t hv_cap = 0;
+    Lead *lead = nullptr;     // leader table
+    float *lead_lam = nullptr;   // [lead_cap + 1][D] B_tok * prefix length of each leader;
+                                 // row lead_cap is all zero (no leader)
+    uint32_t lead_cap = 0, lead_D = 0;
+    bool zero_row_set = false;   // row lead_cap has been cleared
+    void *sort_tmp = nullptr;    // rocPRIM sort / scan temporary storage
+    size_t sort_tmp_bytes = 0;
+    // the batch sorts' own buffers: digit counts, totals and the ping-pong
+    // pair (null when the per-request buffers hold no more than kSortMinN)
+    uint32_t *sort_cnt = nullptr, *sort_tot = nullptr, *keys_tmp = nullptr, *vals_tmp = nullptr;
+    uint64_t *partial = nullptr;   // [groups][R][K] per-group top-k keys
+    uint64_t partial_cap = 0;
+};
+
 }  // namespace
 
 // ====================================================================== host side
@@ -2027,32 +2059,8 @@ struct netkv_ctx {
     uint32_t *cnt = nullptr, *adm = nullptr;
     unsigned long long *bytes = nullptr;
     uint32_t commit_P = 0, commit_D = 0;
-    // batch-order scratch (grows to the largest batch seen)
-    uint64_t order_cap = 0;
-    uint32_t *keys_in = nullptr, *keys_out = nullptr, *vals_in = nullptr, *perm = nullptr;
-    Hot *hot = nullptr;   // sorted request records, the part every scan step reads
-    Cold *cold = nullptr; // and the part read by probing requests
-    uint32_t *n_valid = nullptr;
-    uint32_t *hv = nullptr;                  // holder values of the leaders' blocks
-    uint64_t hv_cap = 0;
-    unsigned long long *hv_used = nullptr;
-    uint64_t *seg = nullptr, *scanned = nullptr;   // segmented-scan elements, hash order
-    Pre *hrec = nullptr;                     // prefill row and length by hash-order position
-    Cold *crec = nullptr;
-    uint32_t *pkey = nullptr, *pkey_out = nullptr, *pval = nullptr, *pord = nullptr;   // prefill order
-    Lead *lead = nullptr;                    // leader table
-    float *lead_lam = nullptr;               // [lead_cap + 1][D] B_tok * prefix length of each
-                                             // leader; row lead_cap is all zero (no leader)
-    uint32_t lead_cap = 0, lead_D = 0;
-    unsigned int *n_lead = nullptr;
-    void *sort_tmp = nullptr;
-    size_t sort_tmp_bytes = 0;
-    // the batch sorts' own scratch (batches of up to kSortMaxN requests)
-    uint32_t *sort_cnt = nullptr;   // [tiles][kSortMaxBins] digit counts, then offsets
-    uint32_t *sort_tot = nullptr;   // [kSortMaxBins] digit totals
-    uint32_t *keys_tmp = nullptr, *vals_tmp = nullptr;   // ping-pong buffers of the passes
-    uint64_t *partial = nullptr;
-    uint64_t partial_cap = 0;
+    // work buffers of the selection (grow to the largest batch seen)
+    Scratch sc;
     // options
     uint32_t run_len_opt = 0;   // 0 = automatic
     uint32_t reuse_opt = 1;     // share prefix lengths along the hash order
@@ -2250,79 +2258,99 @@ uint32_t bits_for(uint64_t v) {   // bits to hold 0..v
     return b;
 }
 
-netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_elems, uint64_t n_hashes,
-                                  hipStream_t st) {
-    if (R > h->order_cap) {
-        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
-        dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
-        dfree(h->hrec); dfree(h->crec);
-        dfree(h->sort_tmp);
-        dfree(h->sort_cnt); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
-        h->order_cap = 0;
-        h->sort_tmp_bytes = 0;
-        if (dalloc(h->keys_in, R) != hipSuccess || dalloc(h->keys_out, R) != hipSuccess ||
-            dalloc(h->vals_in, R) != hipSuccess || dalloc(h->perm, R) != hipSuccess ||
-            dalloc(h->hot, R + kHotPad) != hipSuccess || dalloc(h->cold, R) != hipSuccess ||
-            dalloc(h->seg, R) != hipSuccess || dalloc(h->scanned, R) != hipSuccess ||
-            dalloc(h->pkey, R) != hipSuccess || dalloc(h->pkey_out, R) != hipSuccess ||
-            dalloc(h->pval, R) != hipSuccess || dalloc(h->pord, R) != hipSuccess ||
-            dalloc(h->hrec, R) != hipSuccess || dalloc(h->crec, R) != hipSuccess)
+void free_scratch(Scratch &sc) {
+    dfree(sc.keys_in); dfree(sc.keys_out); dfree(sc.vals_in); dfree(sc.perm); dfree(sc.hot); dfree(sc.cold);
+    dfree(sc.seg); dfree(sc.scanned); dfree(sc.hrec); dfree(sc.crec);
+    dfree(sc.pkey); dfree(sc.pkey_out); dfree(sc.pval); dfree(sc.pord);
+    dfree(sc.n_valid); dfree(sc.hv_used); dfree(sc.n_lead); dfree(sc.hv); dfree(sc.lead); dfree(sc.lead_lam);
+    dfree(sc.sort_tmp); dfree(sc.sort_cnt); dfree(sc.sort_tot); dfree(sc.keys_tmp); dfree(sc.vals_tmp);
+    dfree(sc.partial);
+    sc = Scratch();
+}
+
+// rocPRIM temporary storage for the batch orders of R requests (both sorts
+// and the segmented scan share one buffer); a size query only.
+hipError_t sort_tmp_bytes_for(uint64_t R, size_t &bytes) {
+    size_t b1 = 0, b2 = 0, b3 = 0;
+    uint32_t *k = nullptr;
+    uint64_t *e = nullptr;
+    hipError_t err = rocprim::radix_sort_pairs<SortConfig>(nullptr, b1, k, k, k, k, (uint32_t)R, 0, 32, nullptr);
+    if (err == hipSuccess)
+        err = rocprim::radix_sort_pairs<SortConfig>(nullptr, b2, k, k, k, k, (uint32_t)R, 0, 32, nullptr);
+    if (err == hipSuccess) err = rocprim::inclusive_scan(nullptr, b3, e, e, (size_t)R, SegOp(), nullptr);
+    bytes = std::max<size_t>(std::max(b1, std::max(b2, b3)), 16);
+    return err;
+}
+
+// The handle's work buffers for a batch of R requests with n_hashes block
+// hashes and partial_elems per-group keys: grown (never shrunk) when a batch
+// needs more than any earlier one or than netkv_reserve provided.
+netkv_status ensure_scratch(netkv_handle h, Scratch &sc, uint64_t R, uint64_t partial_elems, uint64_t n_hashes,
+                            hipStream_t st) {
+    if (R > sc.order_cap) {
+        dfree(sc.keys_in); dfree(sc.keys_out); dfree(sc.vals_in); dfree(sc.perm); dfree(sc.hot); dfree(sc.cold);
+        dfree(sc.seg); dfree(sc.scanned); dfree(sc.pkey); dfree(sc.pkey_out); dfree(sc.pval); dfree(sc.pord);
+        dfree(sc.hrec); dfree(sc.crec);
+        dfree(sc.sort_tmp);
+        dfree(sc.sort_cnt); dfree(sc.sort_tot); dfree(sc.keys_tmp); dfree(sc.vals_tmp);
+        sc.order_cap = 0;
+        sc.sort_tmp_bytes = 0;
+        if (dalloc(sc.keys_in, R) != hipSuccess || dalloc(sc.keys_out, R) != hipSuccess ||
+            dalloc(sc.vals_in, R) != hipSuccess || dalloc(sc.perm, R) != hipSuccess ||
+            dalloc(sc.hot, R + kHotPad) != hipSuccess || dalloc(sc.cold, R) != hipSuccess ||
+            dalloc(sc.seg, R) != hipSuccess || dalloc(sc.scanned, R) != hipSuccess ||
+            dalloc(sc.pkey, R) != hipSuccess || dalloc(sc.pkey_out, R) != hipSuccess ||
+            dalloc(sc.pval, R) != hipSuccess || dalloc(sc.pord, R) != hipSuccess ||
+            dalloc(sc.hrec, R) != hipSuccess || dalloc(sc.crec, R) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "batch scratch allocation failed");
         // one temporary buffer for the two sorts and the scan
-        size_t b1 = 0, b2 = 0, b3 = 0;
-        if (rocprim::radix_sort_pairs<SortConfig>(nullptr, b1, h->keys_in, h->keys_out, h->vals_in, h->perm,
-                                                  (uint32_t)R, 0, 32, st) != hipSuccess ||
-            rocprim::radix_sort_pairs<SortConfig>(nullptr, b2, h->pkey, h->pkey_out, h->pval, h->pord, (uint32_t)R,
-                                                  0, 32, st) != hipSuccess ||
-            rocprim::inclusive_scan(nullptr, b3, h->seg, h->scanned, (size_t)R, SegOp(), st) != hipSuccess)
-            return fail(h, NETKV_EDEVICE, "sort / scan size query failed");
-        const size_t bytes = std::max<size_t>(std::max(b1, std::max(b2, b3)), 16);
+        size_t bytes = 0;
+        if (sort_tmp_bytes_for(R, bytes) != hipSuccess) return fail(h, NETKV_EDEVICE, "sort / scan size query failed");
         uint8_t *tmp = nullptr;
         if (dalloc(tmp, bytes) != hipSuccess) return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
-        h->sort_tmp = tmp;
-        h->sort_tmp_bytes = bytes;
-        if (R <= kSortMaxN) {
-            const uint64_t ntile = (R + kSortTile - 1) / kSortTile;
-            if (dalloc(h->sort_cnt, ntile * kSortMaxBins) != hipSuccess ||
-                dalloc(h->sort_tot, kSortMaxBins) != hipSuccess || dalloc(h->keys_tmp, R) != hipSuccess ||
-                dalloc(h->vals_tmp, R) != hipSuccess)
+        sc.sort_tmp = tmp;
+        sc.sort_tmp_bytes = bytes;
+        if (R > kSortMinN) {
+            // the own batch sorts run for kSortMinN < n <= kSortMaxN
+            const uint64_t n = std::min<uint64_t>(R, kSortMaxN);
+            const uint64_t ntile = (n + kSortTile - 1) / kSortTile;
+            if (dalloc(sc.sort_cnt, ntile * kSortMaxBins) != hipSuccess ||
+                dalloc(sc.sort_tot, kSortMaxBins) != hipSuccess || dalloc(sc.keys_tmp, n) != hipSuccess ||
+                dalloc(sc.vals_tmp, n) != hipSuccess)
                 return fail(h, NETKV_ENOMEM, "sort scratch allocation failed");
         }
-        h->order_cap = R;
+        sc.order_cap = R;
     }
-    if (!h->n_valid && dalloc(h->n_valid, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
-    if (!h->hv_used && dalloc(h->hv_used, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
-    if (!h->n_lead && dalloc(h->n_lead, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    if (!sc.n_valid && dalloc(sc.n_valid, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    if (!sc.hv_used && dalloc(sc.hv_used, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
+    if (!sc.n_lead && dalloc(sc.n_lead, 1) != hipSuccess) return fail(h, NETKV_ENOMEM, "allocation failed");
     // holder values of the leaders' blocks: at most one per block of the
     // batch (fewer if runs overlap in the hash array; leaders that do not
     // fit look their blocks up in the leader kernel)
-    if (n_hashes > h->hv_cap || !h->hv) {
-        dfree(h->hv);
-        h->hv_cap = 0;
-        if (dalloc(h->hv, std::max<uint64_t>(n_hashes, 1)) != hipSuccess)
+    if (n_hashes > sc.hv_cap || !sc.hv) {
+        dfree(sc.hv);
+        sc.hv_cap = 0;
+        if (dalloc(sc.hv, std::max<uint64_t>(n_hashes, 1)) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "holder value scratch allocation failed");
-        h->hv_cap = std::max<uint64_t>(n_hashes, 1);
+        sc.hv_cap = std::max<uint64_t>(n_hashes, 1);
     }
     const uint32_t lc = lead_capacity(R, h->D);
-    if (lc > h->lead_cap || h->lead_D != h->D || !h->lead) {
-        dfree(h->lead);
-        dfree(h->lead_lam);
-        h->lead_cap = 0;
-        if (dalloc(h->lead, lc) != hipSuccess || dalloc(h->lead_lam, (uint64_t)(lc + 1) * h->D) != hipSuccess)
+    if (lc > sc.lead_cap || sc.lead_D != h->D || !sc.lead) {
+        dfree(sc.lead);
+        dfree(sc.lead_lam);
+        sc.lead_cap = 0;
+        sc.zero_row_set = false;
+        if (dalloc(sc.lead, lc) != hipSuccess || dalloc(sc.lead_lam, (uint64_t)(lc + 1) * h->D) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "leader table allocation failed");
-        // the all-zero row of requests without a leader (no leader writes it)
-        hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(h->D, 256)), dim3(256), 0, st,
-                           (uint32_t *)(h->lead_lam + (uint64_t)lc * h->D), (uint64_t)h->D, 0u);
-        if (hipGetLastError() != hipSuccess) return fail(h, NETKV_EDEVICE, "leader table initialisation failed");
-        h->lead_cap = lc;
-        h->lead_D = h->D;
+        sc.lead_cap = lc;
+        sc.lead_D = h->D;
     }
-    if (partial_elems > h->partial_cap) {
-        dfree(h->partial);
-        h->partial_cap = 0;
-        if (dalloc(h->partial, partial_elems) != hipSuccess)
+    if (partial_elems > sc.partial_cap) {
+        dfree(sc.partial);
+        sc.partial_cap = 0;
+        if (dalloc(sc.partial, partial_elems) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "partial top-k scratch allocation failed");
-        h->partial_cap = partial_elems;
+        sc.partial_cap = partial_elems;
     }
     return NETKV_OK;
 }
@@ -2330,17 +2358,18 @@ netkv_status ensure_order_scratch(netkv_handle h, uint64_t R, uint64_t partial_e
 // One pass of the batch sort over key bits [shift, shift + bits): counts,
 // offsets, scatter (ASSEMBLE: the prefill order's scoring records).
 template <bool ASSEMBLE>
-hipError_t sort_pass(netkv_handle h, const uint32_t *kin, const uint32_t *vin, uint32_t *kout, uint32_t *vout,
-                     uint32_t n, uint32_t shift, uint32_t bits, const Pre *hrec, const uint64_t *scanned,
-                     const Cold *crec, uint32_t lstride, uint32_t zrow, Hot *hot, Cold *cold, hipStream_t st) {
+hipError_t sort_pass(netkv_handle h, Scratch &sc, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
+                     uint32_t *vout, uint32_t n, uint32_t shift, uint32_t bits, const Pre *hrec,
+                     const uint64_t *scanned, const Cold *crec, uint32_t lstride, uint32_t zrow, Hot *hot,
+                     Cold *cold, hipStream_t st) {
     if (n == 0) return hipSuccess;
     const uint32_t ntile = (n + kSortTile - 1) / kSortTile;   // <= kColPer * kBlock (n <= kSortMaxN)
-    hipLaunchKernelGGL(sort_count_kernel, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits, h->sort_cnt);
-    hipLaunchKernelGGL(sort_colscan_kernel, dim3(1u << bits), dim3(kBlock), 0, st, h->sort_cnt, ntile, bits,
-                       h->sort_tot);
+    hipLaunchKernelGGL(sort_count_kernel, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits, sc.sort_cnt);
+    hipLaunchKernelGGL(sort_colscan_kernel, dim3(1u << bits), dim3(kBlock), 0, st, sc.sort_cnt, ntile, bits,
+                       sc.sort_tot);
     hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(ntile), dim3(kBlock), 0, st, kin, vin, n, shift, bits,
-                       (const uint32_t *)h->sort_cnt, (const uint32_t *)h->sort_tot, kout, vout, hrec, scanned, crec,
-                       h->block_tokens, lstride, zrow, hot, cold);
+                       (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout, vout, hrec, scanned,
+                       crec, h->block_tokens, lstride, zrow, hot, cold);
     return hipGetLastError();
 }
 
@@ -2358,7 +2387,7 @@ inline void pass_bits(uint32_t nbits, uint32_t passes, uint32_t p, uint32_t &shi
 // or the input positions when vin is null), in passes of at most
 // kSortPassBits through the handle's ping-pong buffers; the result lands in
 // kout / vout (kSortMinN < n <= kSortMaxN).
-hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
+hipError_t batch_sort_pairs(netkv_handle h, Scratch &sc, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
                             uint32_t *vout, uint32_t n, uint32_t nbits, hipStream_t st) {
     if (n == 0) return hipSuccess;
     const uint32_t passes = std::max(1u, (nbits + kSortPassBits - 1) / kSortPassBits);
@@ -2368,9 +2397,9 @@ hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t 
         pass_bits(nbits, passes, p, shift, bits);
         // the last pass writes kout, the one before the ping-pong buffers, ...
         const bool to_out = ((passes - 1 - p) % 2) == 0;
-        uint32_t *dk = to_out ? kout : h->keys_tmp, *dv = to_out ? vout : h->vals_tmp;
-        const hipError_t e = sort_pass<false>(h, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0, 0,
-                                              nullptr, nullptr, st);
+        uint32_t *dk = to_out ? kout : sc.keys_tmp, *dv = to_out ? vout : sc.vals_tmp;
+        const hipError_t e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0,
+                                              0, nullptr, nullptr, st);
         if (e != hipSuccess) return e;
         sk = dk;
         sv = dv;
@@ -2382,20 +2411,20 @@ hipError_t batch_sort_pairs(netkv_handle h, const uint32_t *kin, const uint32_t 
 // prefill key (pbits <= kPrefillMaxBits), whose last pass writes the
 // scoring records at their output positions; earlier passes go through
 // buf_k / buf_v (free at this point of a selection).
-hipError_t prefill_order(netkv_handle h, uint32_t n, uint32_t pbits, uint32_t *buf_k, uint32_t *buf_v,
-                         uint32_t lstride, uint32_t zrow, hipStream_t st) {
+hipError_t prefill_order(netkv_handle h, Scratch &sc, uint32_t n, uint32_t pbits, uint32_t *buf_k,
+                         uint32_t *buf_v, uint32_t lstride, uint32_t zrow, hipStream_t st) {
     const uint32_t passes = std::max(1u, (pbits + kSortMaxBits - 1) / kSortMaxBits);
-    const uint32_t *sk = h->pkey, *sv = nullptr;
+    const uint32_t *sk = sc.pkey, *sv = nullptr;
     for (uint32_t p = 0; p < passes; ++p) {
         uint32_t shift, bits;
         pass_bits(pbits, passes, p, shift, bits);
         hipError_t e;
         if (p + 1 == passes) {
-            e = sort_pass<true>(h, sk, sv, nullptr, nullptr, n, shift, bits, h->hrec, h->scanned, h->crec, lstride,
-                                zrow, h->hot, h->cold, st);
+            e = sort_pass<true>(h, sc, sk, sv, nullptr, nullptr, n, shift, bits, sc.hrec, sc.scanned, sc.crec,
+                                lstride, zrow, sc.hot, sc.cold, st);
         } else {
-            uint32_t *dk = (p % 2) ? buf_k : h->keys_tmp, *dv = (p % 2) ? buf_v : h->vals_tmp;
-            e = sort_pass<false>(h, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0, 0, nullptr,
+            uint32_t *dk = (p % 2) ? buf_k : sc.keys_tmp, *dv = (p % 2) ? buf_v : sc.vals_tmp;
+            e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0, 0, nullptr,
                                  nullptr, st);
             sk = dk;
             sv = dv;
@@ -2434,15 +2463,15 @@ inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
 // (kWavesPerBlock runs, group) when the groups split evenly over the XCDs
 // (see score_kernel), else per kWavesPerBlock waves.
 template <int K, int C>
-hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
-                        uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint64_t *partial, const PairOut &po,
+hipError_t launch_score(netkv_handle h, Scratch &sc, const Snap &sn, const Table &t, const Reqs &rq,
+                        const Order &ord, uint32_t run_len, uint32_t n_runs, uint32_t ngroup, const PairOut &po,
                         bool pairs, hipStream_t st) {
     // leaders: 64 decodes per wavefront, 64 blocks per step
     const uint32_t lgroup = (sn.D + kWave - 1) / kWave;
     const uint64_t lw = std::min<uint64_t>((uint64_t)ord.lead_cap * lgroup, 65536);
     hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
-                       dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)h->lead,
-                       (const unsigned int *)h->n_lead, ord.lead_cap, ord.hv, rq.hashes, lgroup, h->lead_lam);
+                       dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)sc.lead,
+                       (const unsigned int *)sc.n_lead, ord.lead_cap, ord.hv, rq.hashes, lgroup, sc.lead_lam);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || (e = time_begin(h, st)) != hipSuccess) return e;
     const uint64_t grid64 = ngroup % kXcds == 0
@@ -2455,8 +2484,8 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
     const bool two = sn.sr != nullptr;
 #define NETKV_SCORE(P2, T2)                                                                                      \
     hipLaunchKernelGGL((score_kernel<K, 1, C, P2, T2>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, \
-                       ord.lam, h->lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len, n_runs, \
-                       ngroup, partial, po)
+                       ord.lam, sc.lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len, n_runs, \
+                       ngroup, sc.partial, po)
     if (pairs) {
         if (two) NETKV_SCORE(true, true);
         else NETKV_SCORE(true, false);
@@ -2472,110 +2501,144 @@ hipError_t launch_score(netkv_handle h, const Snap &sn, const Table &t, const Re
 // Leader kernel, the scoring kernel (bracketed by the handle's timing events
 // when enabled), then the merge.
 template <int K>
-hipError_t launch_score_reduce(netkv_handle h, const Snap &sn, const Table &t, const Reqs &rq, const Order &ord,
-                               uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C, uint64_t *partial,
+hipError_t launch_score_reduce(netkv_handle h, Scratch &sc, const Snap &sn, const Table &t, const Reqs &rq,
+                               const Order &ord, uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C,
                                const PairOut &po, bool pairs, uint32_t k, int32_t *idx, float *score,
                                hipStream_t st) {
     hipError_t e = hipSuccess;
     if (C == 6)
-        e = launch_score<K, 6>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 6>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
     else if (C == 4)
-        e = launch_score<K, 4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 4>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
     else if (C == 3)
-        e = launch_score<K, 3>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 3>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
     else if (C == 2)
-        e = launch_score<K, 2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 2>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
     else
-        e = launch_score<K, 1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, partial, po, pairs, st);
+        e = launch_score<K, 1>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
-                       (const uint64_t *)partial, (const Cold *)ord.cold, ord.n_valid, idx, score);
+                       (const uint64_t *)sc.partial, (const Cold *)ord.cold, ord.n_valid, idx, score);
     return hipGetLastError();
 }
 
-// The whole selection of one batch on `st`: validate and key the requests,
-// hash order (sort), common runs and leaders, the segmented scan, prefill
-// order (stable sort), scoring records, leaders' prefix lengths, scoring,
-// merge.
-netkv_status run_select(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
-                        const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false) {
+// Top-k width K of the kernels for k, decodes per lane C and decode groups.
+struct Geometry {
+    uint32_t K, C, ngroup;
+};
+
+Geometry geometry(netkv_handle h, uint32_t k) {
+    Geometry g;
+    g.K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
+    g.C = cols_per_lane(h->D, h->cols_opt);
+    g.ngroup = (h->D + kWave * g.C - 1) / (kWave * g.C);
+    return g;
+}
+
+// The whole selection of one batch on `st` with the work buffers of sc
+// (which must hold the batch: R <= order_cap, R * ngroup * K <= partial_cap):
+// validate and key the requests, hash order (sort), common runs and
+// leaders, the segmented scan, prefill order (stable sort), scoring
+// records, leaders' prefix lengths, scoring, merge.  Launches kernels only.
+netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req, uint32_t k, int32_t *idx,
+                        float *score, const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st,
+                        bool route2 = false, bool derive = true) {
     const uint64_t R = req->n_req;
-    const uint32_t K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8;
-    const uint32_t C = cols_per_lane(h->D, h->cols_opt);
-    const uint32_t ngroup = (h->D + kWave * C - 1) / (kWave * C);
-    netkv_status e = ensure_order_scratch(h, R, R * ngroup * K, req->n_hashes, st);
-    if (e) return e;
+    const Geometry geo = geometry(h, k);
+    const uint32_t K = geo.K, C = geo.C, ngroup = geo.ngroup;
     Snap sn = make_snap(h);
     const Table t = make_table(h);
     const Reqs rq = make_reqs(req);
+    if (!sc.zero_row_set) {
+        // the all-zero row of requests without a leader (no leader writes it)
+        hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(h->D, 256)), dim3(256), 0, st,
+                           (uint32_t *)(sc.lead_lam + (uint64_t)sc.lead_cap * h->D), (uint64_t)h->D, 0u);
+        HIPCHK(h, hipGetLastError());
+        sc.zero_row_set = true;
+    }
     const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
-    hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
-                       h->dxlim);
+    if (derive)
+        hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
+                           h->dxlim);
     if (route2 && h->have_route) {
-        hipLaunchKernelGGL(derive_route_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn,
-                           (const uint8_t *)h->rt1, (const float *)h->ru1, (const uint8_t *)h->rt2,
-                           (const float *)h->ru2, h->sr);
+        if (derive)
+            hipLaunchKernelGGL(derive_route_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn,
+                               (const uint8_t *)h->rt1, (const float *)h->ru1, (const uint8_t *)h->rt2,
+                               (const float *)h->ru2, h->sr);
         sn.sr = h->sr;
     }
-    const bool own_sort = R > kSortMinN && R <= kSortMaxN;   // its first pass takes positions as values
-    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks, h->keys_in,
-                       own_sort ? nullptr : h->vals_in, h->errword, h->hv_used, h->n_lead);
+    // the own batch sort (its first pass takes positions as values) where
+    // its buffers are there and the batch is in its range
+    const bool own_sort = R > kSortMinN && R <= kSortMaxN && sc.sort_cnt != nullptr;
+    hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks,
+                       sc.keys_in, own_sort ? nullptr : sc.vals_in, h->errword, sc.hv_used, sc.n_lead);
     HIPCHK(h, hipGetLastError());
-    size_t tb = h->sort_tmp_bytes;
+    size_t tb = sc.sort_tmp_bytes;
     if (own_sort)
-        HIPCHK(h, batch_sort_pairs(h, h->keys_in, nullptr, h->keys_out, h->perm, (uint32_t)R, 32, st));
+        HIPCHK(h, batch_sort_pairs(h, sc, sc.keys_in, nullptr, sc.keys_out, sc.perm, (uint32_t)R, 32, st));
     else
-        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->keys_in, h->keys_out, h->vals_in, h->perm,
-                                                        (uint32_t)R, 0, 32, st));
+        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(sc.sort_tmp, tb, sc.keys_in, sc.keys_out, sc.vals_in,
+                                                        sc.perm, (uint32_t)R, 0, 32, st));
     // leaders (and holder values of their blocks) the table takes this call
-    const uint32_t lcap = h->lead_cap_opt ? std::min(h->lead_cap, h->lead_cap_opt) : h->lead_cap;
-    const uint64_t hvcap = h->lead_cap_opt ? std::min<uint64_t>(h->hv_cap, h->lead_cap_opt) : h->hv_cap;
+    const uint32_t lcap = h->lead_cap_opt ? std::min(sc.lead_cap, h->lead_cap_opt) : sc.lead_cap;
+    const uint64_t hvcap = h->lead_cap_opt ? std::min<uint64_t>(sc.hv_cap, h->lead_cap_opt) : sc.hv_cap;
     // the prefill order: the own sort (positions as its values), or rocPRIM's on pval
     const uint32_t pbits = bits_for(h->P);
     const bool own_prefill = own_sort && pbits <= kPrefillMaxBits;
     hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
-                       h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)h->perm,
-                       (const uint32_t *)h->keys_out, t, h->reuse_opt, h->seg, h->pkey,
-                       own_prefill ? nullptr : h->pval, h->hrec, h->crec, h->lead, lcap, h->n_lead, hvcap,
-                       h->hv_used, h->n_valid);
+                       h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)sc.perm,
+                       (const uint32_t *)sc.keys_out, t, h->reuse_opt, sc.seg, sc.pkey,
+                       own_prefill ? nullptr : sc.pval, sc.hrec, sc.crec, sc.lead, lcap, sc.n_lead, hvcap,
+                       sc.hv_used, sc.n_valid);
     hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((lcap + kWavesPerBlock - 1) /
                                                                              kWavesPerBlock, 4096)),
-                       dim3(kBlock), 0, st, t, rq.hashes, h->lead, (const unsigned int *)h->n_lead, lcap, h->hv);
+                       dim3(kBlock), 0, st, t, rq.hashes, sc.lead, (const unsigned int *)sc.n_lead, lcap, sc.hv);
     HIPCHK(h, hipGetLastError());
-    tb = h->sort_tmp_bytes;
-    HIPCHK(h, rocprim::inclusive_scan(h->sort_tmp, tb, (const uint64_t *)h->seg, h->scanned, (size_t)R, SegOp(), st));
+    tb = sc.sort_tmp_bytes;
+    HIPCHK(h, rocprim::inclusive_scan(sc.sort_tmp, tb, (const uint64_t *)sc.seg, sc.scanned, (size_t)R, SegOp(), st));
     // prefill order (stable: the hash order within each prefill) and the
     // scoring records in it
     const uint32_t lstride = h->D * (uint32_t)sizeof(float);
     if (own_prefill) {
         // (the hash order's keys and permutation are no longer needed)
-        HIPCHK(h, prefill_order(h, (uint32_t)R, pbits, h->keys_out, h->perm, lstride, h->lead_cap * lstride, st));
+        HIPCHK(h, prefill_order(h, sc, (uint32_t)R, pbits, sc.keys_out, sc.perm, lstride, sc.lead_cap * lstride,
+                                st));
     } else {
-        tb = h->sort_tmp_bytes;
-        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->pkey, h->pkey_out, h->pval, h->pord,
+        tb = sc.sort_tmp_bytes;
+        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(sc.sort_tmp, tb, sc.pkey, sc.pkey_out, sc.pval, sc.pord,
                                                         (uint32_t)R, 0, pbits, st));
         hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st,
-                           (uint32_t)R, h->block_tokens, lstride, h->lead_cap * lstride, (const uint32_t *)h->pord,
-                           (const uint64_t *)h->scanned, (const Pre *)h->hrec, (const Cold *)h->crec, h->hot,
-                           h->cold);
+                           (uint32_t)R, h->block_tokens, lstride, sc.lead_cap * lstride, (const uint32_t *)sc.pord,
+                           (const uint64_t *)sc.scanned, (const Pre *)sc.hrec, (const Cold *)sc.crec, sc.hot,
+                           sc.cold);
         HIPCHK(h, hipGetLastError());
     }
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
-    Order ord{h->hot, h->cold, h->lead_lam, h->hv, h->n_valid, lcap};
+    Order ord{sc.hot, sc.cold, sc.lead_lam, sc.hv, sc.n_valid, lcap};
     if (K == 1)
-        HIPCHK(h, launch_score_reduce<1>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+        HIPCHK(h, launch_score_reduce<1>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, C, po, pairs, k, idx,
                                          score, st));
     else if (K == 2)
-        HIPCHK(h, launch_score_reduce<2>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+        HIPCHK(h, launch_score_reduce<2>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, C, po, pairs, k, idx,
                                          score, st));
     else if (K == 4)
-        HIPCHK(h, launch_score_reduce<4>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+        HIPCHK(h, launch_score_reduce<4>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, C, po, pairs, k, idx,
                                          score, st));
     else
-        HIPCHK(h, launch_score_reduce<8>(h, sn, t, rq, ord, run_len, n_runs, ngroup, C, h->partial, po, pairs, k, idx,
+        HIPCHK(h, launch_score_reduce<8>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, C, po, pairs, k, idx,
                                          score, st));
     return NETKV_OK;
+}
+
+// The handle's buffers for the batch, then the selection.
+netkv_status select_owned(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
+                          const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false) {
+    const Geometry geo = geometry(h, k);
+    netkv_status e = ensure_scratch(h, h->sc, req->n_req, (uint64_t)req->n_req * geo.ngroup * geo.K,
+                                    req->n_hashes, st);
+    if (e) return e;
+    return run_select(h, h->sc, req, k, idx, score, po, pairs, max_blocks, st, route2);
 }
 
 bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
@@ -2629,11 +2692,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->cnt);
         dfree(h->adm);
         dfree(h->bytes);
-        dfree(h->keys_in); dfree(h->keys_out); dfree(h->vals_in); dfree(h->perm); dfree(h->hot); dfree(h->cold);
-        dfree(h->n_valid); dfree(h->sort_tmp); dfree(h->partial); dfree(h->hv); dfree(h->hv_used);
-        dfree(h->sort_cnt); dfree(h->sort_tot); dfree(h->keys_tmp); dfree(h->vals_tmp);
-        dfree(h->seg); dfree(h->scanned); dfree(h->pkey); dfree(h->pkey_out); dfree(h->pval); dfree(h->pord);
-        dfree(h->lead); dfree(h->lead_lam); dfree(h->n_lead); dfree(h->hrec); dfree(h->crec);
+        free_scratch(h->sc);
         dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
         for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
@@ -3102,7 +3161,23 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
         po.score = pairs->score;
         want_pairs = po.j || po.feas || po.score;
     }
-    return run_select(h, req, k, out_idx, out_score, po, want_pairs, 0xFFFFFFFFu, s, true);
+    return select_owned(h, req, k, out_idx, out_score, po, want_pairs, 0xFFFFFFFFu, s, true);
+}
+
+netkv_status netkv_reserve(netkv_handle h, uint32_t max_req, uint64_t max_hashes, uint32_t max_k, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    if (max_k < 1 || max_k > 8) return fail(h, NETKV_EINVAL, "max_k must be in [1, 8]");
+    if (max_req > (1u << 31)) return fail(h, NETKV_EINVAL, "max_req too large");
+    if (!h->have_snap) return fail(h, NETKV_ENOTREADY, "no snapshot loaded (netkv_oracle_load)");
+    if (max_req == 0) return NETKV_OK;
+    DeviceGuard g(h->device);
+    uint64_t elems = 0;
+    for (uint32_t k = 1; k <= max_k; ++k) {
+        const Geometry geo = geometry(h, k);
+        elems = std::max<uint64_t>(elems, (uint64_t)max_req * geo.ngroup * geo.K);
+    }
+    return ensure_scratch(h, h->sc, max_req, elems, max_hashes, (hipStream_t)stream);
 }
 
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen, const float *util_scen,
@@ -3140,7 +3215,7 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
     PairOut po{nullptr, nullptr, nullptr, h->jT};
     {
         TimingOff off(h);  // only the sweep kernel is timed
-        if ((st = run_select(h, req, 1, h->base_idx, h->base_score, po, true, kMaxBlocks16, s))) return st;
+        if ((st = select_owned(h, req, 1, h->base_idx, h->base_score, po, true, kMaxBlocks16, s))) return st;
     }
     if (out_flips) {
         hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(2ull * n_scen, 256)), dim3(256), 0, s, out_flips,
@@ -3328,19 +3403,19 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     PairOut po{h->seq_j, nullptr, nullptr, nullptr};
     {
         TimingOff off(h);  // only the sequential kernel is timed
-        if ((st = run_select(h, req, 1, out_idx, out_score, po, true, kMaxBlocks16, s))) return st;
+        if ((st = select_owned(h, req, 1, out_idx, out_score, po, true, kMaxBlocks16, s))) return st;
     }
     // requests grouped by prefill instance, batch order kept inside a group
     const Reqs rq = make_reqs(req);
     hipLaunchKernelGGL(prefill_key_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s, rq, (uint32_t)P,
-                       (const uint32_t *)h->keys_in, h->seq_keys, h->seq_vals);
-    size_t tb = h->sort_tmp_bytes;
-    if (R > kSortMinN && R <= kSortMaxN)
-        HIPCHK(h, batch_sort_pairs(h, h->seq_keys, h->seq_vals, h->seq_keys_out, h->seq_perm, (uint32_t)R,
+                       (const uint32_t *)h->sc.keys_in, h->seq_keys, h->seq_vals);
+    size_t tb = h->sc.sort_tmp_bytes;
+    if (R > kSortMinN && R <= kSortMaxN && h->sc.sort_cnt)
+        HIPCHK(h, batch_sort_pairs(h, h->sc, h->seq_keys, h->seq_vals, h->seq_keys_out, h->seq_perm, (uint32_t)R,
                                    bits_for(P), s));
     else
-        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sort_tmp, tb, h->seq_keys, h->seq_keys_out, h->seq_vals,
-                                                        h->seq_perm, (uint32_t)R, 0, bits_for(P), s));
+        HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(h->sc.sort_tmp, tb, h->seq_keys, h->seq_keys_out,
+                                                        h->seq_vals, h->seq_perm, (uint32_t)R, 0, bits_for(P), s));
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_start, P, 0u);
     hipLaunchKernelGGL(fill_u32_kernel, dim3(grid_for(P, 256)), dim3(256), 0, s, h->seq_end, P, 0u);
     hipLaunchKernelGGL(segment_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, s,
