@@ -180,6 +180,26 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
                                 int32_t *out_idx, float *out_score, netkv_pairs_t *pairs,
                                 void *stream);
 
+/* netkv_select_batch in throughput mode (no per-pair outputs) without any
+ * device allocation, for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, results and errors as netkv_select_batch with
+ * pairs = NULL; the selections and scores are bit-identical to it.  Its
+ * work buffers come from one static array of 64 MiB per device, part of the
+ * library's device code, held from the device's first netkv_create until
+ * the process ends.  A batch larger than the array holds (more than 65,536
+ * requests, or fewer when k * ceil(n_decode / 64) is large) is processed
+ * in consecutive sub-batches on `stream`, which is exact: every request's
+ * result depends only on that request.  Leaders beyond the table the
+ * array leaves room for are matched on their own (slower, same results).
+ * Every call on a device shares that device's array and leaves its last
+ * contents there: calls that overlap on one device (different streams or
+ * threads, with no ordering between them) race and give undefined
+ * results.  ECAPACITY when not even a sub-batch of 256 requests fits (a
+ * pool of several million decodes); otherwise as netkv_select_batch. */
+netkv_status netkv_select_batch_noalloc(netkv_handle h, const netkv_requests_t *req, uint32_t k,
+                                        int32_t *out_idx, float *out_score, void *stream);
+
 /* Size the handle's selection work buffers ahead for batches of up to
  * max_req requests with up to max_hashes block hashes and 1 <= k <= max_k,
  * so that netkv_select_batch, netkv_rank_sweep and netkv_select_sequential

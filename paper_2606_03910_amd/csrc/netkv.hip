@@ -55,6 +55,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -69,6 +70,8 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kMix64 = 0xBF58476D1CE4E5B9ull;
 constexpr uint64_t kEmptyKey = ~0ull; // empty top-k entry (sorts last)
+// bytes of the static scratch array of the no-allocation selection (per device)
+constexpr uint64_t kScratchBytes = 64ull << 20;
 
 enum : uint32_t {
     kErrRequest = 1u,    // request header inconsistent
@@ -1983,8 +1986,9 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, uint32_t c
 
 // Work buffers of one selection: per-request ordering buffers and records,
 // the leader table, the leaders' holder values, per-group partial top-k
-// keys and the sort / scan temporaries, owned by the handle (grown on
-// demand, or sized ahead by netkv_reserve).
+// keys and the sort / scan temporaries.  Owned by the handle (grown on
+// demand, or sized ahead by netkv_reserve) or carved from the library's
+// static scratch array (netkv_select_batch_noalloc).
 struct Scratch {
     uint64_t order_cap = 0;   // requests the per-request buffers hold
     uint32_t *keys_in = nullptr, *keys_out = nullptr, *vals_in = nullptr, *perm = nullptr;
@@ -2641,8 +2645,127 @@ netkv_status select_owned(netkv_handle h, const netkv_requests_t *req, uint32_t 
     return run_select(h, h->sc, req, k, idx, score, po, pairs, max_blocks, st, route2);
 }
 
+// ---- work buffers carved from the static scratch array (no allocation)
+
+constexpr uint64_t kAlign = 256;
+inline uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Lay out the buffers of a selection of at most r requests (no own-sort
+// buffers: r <= kSortMinN), lead_cap leaders and hv_cap holder values in
+// the bytes at base; with base null only the size is computed.  Returns
+// the bytes used.
+uint64_t carve(uint8_t *base, uint64_t r, uint32_t D, uint64_t partial_elems, uint32_t lead_cap, uint64_t hv_cap,
+               size_t tmp_bytes, Scratch *sc) {
+    uint64_t used = 0;
+    auto take = [&](uint64_t bytes) -> uint8_t * {
+        uint8_t *p = base ? base + used : nullptr;
+        used = align_up(used + std::max<uint64_t>(bytes, 1));
+        return p;
+    };
+    Scratch t;
+    t.n_valid = (uint32_t *)take(4);
+    t.hv_used = (unsigned long long *)take(8);
+    t.n_lead = (unsigned int *)take(4);
+    t.sort_tmp = take(tmp_bytes);
+    t.sort_tmp_bytes = tmp_bytes;
+    t.keys_in = (uint32_t *)take(4 * r);
+    t.keys_out = (uint32_t *)take(4 * r);
+    t.vals_in = (uint32_t *)take(4 * r);
+    t.perm = (uint32_t *)take(4 * r);
+    t.hot = (Hot *)take(sizeof(Hot) * (r + kHotPad));
+    t.cold = (Cold *)take(sizeof(Cold) * r);
+    t.seg = (uint64_t *)take(8 * r);
+    t.scanned = (uint64_t *)take(8 * r);
+    t.hrec = (Pre *)take(sizeof(Pre) * r);
+    t.crec = (Cold *)take(sizeof(Cold) * r);
+    t.pkey = (uint32_t *)take(4 * r);
+    t.pkey_out = (uint32_t *)take(4 * r);
+    t.pval = (uint32_t *)take(4 * r);
+    t.pord = (uint32_t *)take(4 * r);
+    t.partial = (uint64_t *)take(8 * partial_elems);
+    t.partial_cap = partial_elems;
+    t.lead = (Lead *)take(sizeof(Lead) * (uint64_t)lead_cap);
+    t.lead_lam = (float *)take(4ull * ((uint64_t)lead_cap + 1) * D);
+    t.lead_cap = lead_cap;
+    t.lead_D = D;
+    t.hv = (uint32_t *)take(4 * hv_cap);
+    t.hv_cap = hv_cap;
+    t.order_cap = r;
+    t.zero_row_set = false;
+    if (sc) *sc = t;
+    return used;
+}
+
+// Sub-batch size and buffers for a no-allocation selection of R requests:
+// the largest r (at most kSortMinN, halved down to 256) whose per-request
+// buffers and per-group keys fit with one leader row; what is left goes
+// half to leader rows, half to leaders' holder values.
+netkv_status carve_static(netkv_handle h, uint8_t *base, uint64_t R, uint32_t k, Scratch &sc, uint64_t &r_sub) {
+    const Geometry geo = geometry(h, k);
+    const uint32_t D = h->D;
+    uint64_t r = std::min<uint64_t>(R, kSortMinN);
+    size_t tmp = 0;
+    for (;;) {
+        if (sort_tmp_bytes_for(r, tmp) != hipSuccess) return fail(h, NETKV_EDEVICE, "sort / scan size query failed");
+        if (carve(nullptr, r, D, r * geo.ngroup * geo.K, 1, 1, tmp, nullptr) <= kScratchBytes) break;
+        if (r <= 256)
+            return fail(h, NETKV_ECAPACITY,
+                        "the no-allocation scratch (%llu MiB) cannot hold a sub-batch of %llu requests on %u decodes "
+                        "with k = %u",
+                        (unsigned long long)(kScratchBytes >> 20), (unsigned long long)r, D, k);
+        r = std::max<uint64_t>(256, r / 2);
+    }
+    const uint64_t base_bytes = carve(nullptr, r, D, r * geo.ngroup * geo.K, 1, 1, tmp, nullptr);
+    const uint64_t rest = kScratchBytes - base_bytes;
+    const uint64_t row = 4ull * D + sizeof(Lead);
+    const uint64_t slack = 4 * kAlign;
+    uint64_t extra = rest > slack ? std::min<uint64_t>(r - 1, (rest - slack) / 2 / row) : 0;
+    uint64_t hv_cap = 1 + (rest > slack + extra * row ? (rest - slack - extra * row) / 4 : 0);
+    while (carve(nullptr, r, D, r * geo.ngroup * geo.K, (uint32_t)(1 + extra), hv_cap, tmp, nullptr) > kScratchBytes) {
+        if (hv_cap > 1024) hv_cap -= 1024;
+        else if (extra > 0) --extra;
+        else break;   // one leader row and one holder value: fits (checked above)
+    }
+    carve(base, r, D, r * geo.ngroup * geo.K, (uint32_t)(1 + extra), hv_cap, tmp, &sc);
+    r_sub = r;
+    return NETKV_OK;
+}
+
 bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
 
+}  // namespace
+
+// ------------------------------------------------------------------ no-allocation scratch
+//
+// Work buffers of netkv_select_batch_noalloc: one array per device in the
+// code object's zero-initialised data, held until the process ends.  In
+// host code its name stands for a host-side shadow, not a device address:
+// the address on each device is resolved once, with that device current
+// (netkv_create), and only that address is used.
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t *g_scratch_dev[kMaxDevices] = {};
+
+// Called with `device` current.
+hipError_t resolve_scratch(int device) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dev[device]) return hipSuccess;
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_dev[device] = (uint8_t *)p;
+    return hipSuccess;
+}
+
+uint8_t *scratch_of(int device) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_dev[device];
+}
 }  // namespace
 
 // ------------------------------------------------------------------ API
@@ -2654,10 +2777,12 @@ netkv_status netkv_create(netkv_handle *out, int device) {
     *out = nullptr;
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) return NETKV_EINVAL;
+    if (device >= kMaxDevices) return NETKV_EINVAL;
     netkv_handle h = new netkv_ctx();
     h->device = device;
     DeviceGuard g(device);
-    if (dalloc(h->errword, 1) != hipSuccess || dalloc(h->loadword, 1) != hipSuccess ||
+    if (resolve_scratch(device) != hipSuccess || dalloc(h->errword, 1) != hipSuccess ||
+        dalloc(h->loadword, 1) != hipSuccess ||
         hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess) {
         netkv_destroy(h);
         return NETKV_EDEVICE;
@@ -3162,6 +3287,38 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
         want_pairs = po.j || po.feas || po.score;
     }
     return select_owned(h, req, k, out_idx, out_score, po, want_pairs, 0xFFFFFFFFu, s, true);
+}
+
+netkv_status netkv_select_batch_noalloc(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *out_idx,
+                                        float *out_score, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    netkv_status st = check_requests(h, req);
+    if (st) return st;
+    if (k < 1 || k > 8) return fail(h, NETKV_EINVAL, "k must be in [1, 8]");
+    if (req->n_req && (!out_idx || !out_score))
+        return fail(h, NETKV_EINVAL, "out_idx and out_score must not be NULL");
+    if ((st = ready(h))) return st;
+    if (req->n_req == 0) return NETKV_OK;
+    uint8_t *base = scratch_of(h->device);
+    if (!base) return fail(h, NETKV_EDEVICE, "no-allocation scratch not resolved on device %d", h->device);
+    DeviceGuard g(h->device);
+    hipStream_t s = (hipStream_t)stream;
+    Scratch sc;
+    uint64_t r_sub = 0;
+    if ((st = carve_static(h, base, req->n_req, k, sc, r_sub))) return st;
+    const PairOut po{nullptr, nullptr, nullptr, nullptr};
+    for (uint64_t r0 = 0; r0 < req->n_req; r0 += r_sub) {
+        netkv_requests_t sub = *req;
+        sub.n_req = (uint32_t)std::min<uint64_t>(r_sub, req->n_req - r0);
+        sub.prefill += r0;
+        sub.len_tokens += r0;
+        sub.hash_off += r0;   // absolute offsets into the same hash array
+        if ((st = run_select(h, sc, &sub, k, out_idx + r0 * k, out_score + r0 * k, po, false, 0xFFFFFFFFu, s, true,
+                             r0 == 0)))
+            return st;
+    }
+    return NETKV_OK;
 }
 
 netkv_status netkv_reserve(netkv_handle h, uint32_t max_req, uint64_t max_hashes, uint32_t max_k, void *stream) {

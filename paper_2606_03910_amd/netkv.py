@@ -73,6 +73,8 @@ _SIGS = {
     "netkv_select_batch": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
                                        C.c_void_p, C.c_void_p, C.POINTER(netkv_pairs_t),
                                        C.c_void_p]),
+    "netkv_select_batch_noalloc": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
+                                               C.c_void_p, C.c_void_p, C.c_void_p]),
     "netkv_reserve": (C.c_int32, [C.c_void_p, C.c_uint32, C.c_uint64, C.c_uint32, C.c_void_p]),
     "netkv_rank_sweep": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
                                      C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -264,6 +266,15 @@ def netkv_select_batch(h: int, req: Dict[str, torch.Tensor], k: int, out_idx: to
         h, C.byref(r), int(k), _dptr(out_idx, torch.int32, n * k, "out_idx"),
         _dptr(out_score, torch.float32, n * k, "out_score"),
         C.byref(pp) if pp is not None else None, _stream(device)))
+
+
+def netkv_select_batch_noalloc(h: int, req: Dict[str, torch.Tensor], k: int, out_idx: torch.Tensor,
+                               out_score: torch.Tensor, device) -> None:
+    r = _requests(req)
+    n = r.n_req
+    _check(h, load_library().netkv_select_batch_noalloc(
+        h, C.byref(r), int(k), _dptr(out_idx, torch.int32, n * k, "out_idx"),
+        _dptr(out_score, torch.float32, n * k, "out_score"), _stream(device)))
 
 
 def netkv_reserve(h: int, max_req: int, max_hashes: int, max_k: int, device) -> None:
