@@ -154,22 +154,28 @@ def cpu_baseline(args, snap, cache, req, routes, gidx, gscore, D):
 
 
 def stream_ceiling(dev, mib=2048, reps=10):
-    """Achieved read bandwidth of a plain read-only streaming kernel (a sum
-    over 2 GiB of int32): the practical ceiling for HBM-bound kernels."""
+    """Achieved bandwidth of plain streaming kernels over 2 GiB: a read-only
+    one (torch's fp32 sum) and a device copy (read + write): the practical
+    ceiling for HBM-bound kernels."""
     import torch
-    x = torch.ones(mib * (1 << 20) // 4, dtype=torch.int32, device=dev)
-    for _ in range(3):
-        x.sum()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
-        x.sum()
-    b.record()
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / reps
-    del x
-    return dict(gbs=mib * (1 << 20) / (ms * 1e-3) / 1e9, kernel="torch.sum over 2 GiB int32 (reads only)",
-                ms=ms)
+    x = torch.ones(mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    res = {}
+    for name, fn, mult in (("read", lambda: x.sum(), 1), ("copy", lambda: y.copy_(x), 2)):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        res[name] = dict(gbs=mult * mib * (1 << 20) / (ms * 1e-3) / 1e9, ms=ms)
+    del x, y
+    return dict(gbs=max(v["gbs"] for v in res.values()), read_only_gbs=res["read"]["gbs"],
+                copy_gbs=res["copy"]["gbs"],
+                kernels="torch fp32 sum over 2 GiB (reads only); device copy of 2 GiB (read + write)")
 
 
 def main():
@@ -180,6 +186,9 @@ def main():
     ap.add_argument("--workload", default="c2", choices=["c0", "c1", "c2", "c3", "c4"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile", action="store_true",
+                    help="timed steps only (no algorithmic-byte pass, streaming ceiling or CPU baseline): "
+                         "for kernel traces and counters")
     ap.add_argument("--cpu-seconds", type=float, default=45.0,
                     help="cap on the all-threads oracle timing of the 65,536-request slice")
     ap.add_argument("--no-reuse", action="store_true",
@@ -304,6 +313,11 @@ def main():
     # the same kernel (bit-identical to the oracle's in the parity tests), plus
     # the bytes every launch must read once and write.
     nblk = np.diff(req["hash_off"].astype(np.int64))
+    if args.profile:
+        print(json.dumps({"profile_run": True, "workload": cfg.name, "step_ms_events": step_ms,
+                          "kernel_ms": kern_ms}), flush=True)
+        sel.close()
+        return
     tests = 0
     chunk = 65536
     jbuf = torch.empty(chunk * D, dtype=torch.uint16, device=dev)
@@ -353,7 +367,7 @@ def main():
         }
 
     stream = stream_ceiling(dev)
-    log(f"read-only streaming ceiling {stream['gbs']:.0f} GB/s")
+    log(f"streaming ceiling: read {stream['read_only_gbs']:.0f} GB/s, copy {stream['copy_gbs']:.0f} GB/s")
 
     # ---- CPU oracle baseline on a bounded sample of the same workload
     cpu = None

@@ -47,7 +47,6 @@
 //   commit kernels     -- between-batch counter / queue / memory update.
 #include <hip/hip_runtime.h>
 #include <rocprim/device/device_radix_sort.hpp>
-#include <rocprim/device/device_scan.hpp>
 
 #include <algorithm>
 #include <cmath>
@@ -374,6 +373,10 @@ struct SegOp {
     }
 };
 
+// The identity of SegOp: no leader, no cap.
+constexpr uint64_t kSegIdentity = ((uint64_t)kNoLead << 32) | kNoCap;
+__device__ inline uint64_t seg_op(uint64_t a, uint64_t b) { return SegOp()(a, b); }
+
 // A leader: where its blocks' holder values start in hv (from block 0, up
 // to the first block no decode holds; m = kNoPre if they did not fit), and
 // its hash run for lookups otherwise.
@@ -466,105 +469,201 @@ __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max
 // issued together), whether the position is a leader (some decode holds its
 // block L), and for a leader a slot of the leader table and room for the
 // holder values of its blocks (in hv, from a shared counter; filled by
-// lead_holder_kernel).  Writes the segmented-scan element, the prefill sort
-// key and the scoring record of i, and the number of valid requests (valid
-// keys sort first): the last valid position writes it, or position 0 writes
-// 0.  Invalid positions sort after every prefill (key P).
+// lead_holder_kernel).  Writes the prefill sort key and the scoring record
+// of i, and the number of valid requests (valid keys sort first): the last
+// valid position writes it, or position 0 writes 0.  Invalid positions sort
+// after every prefill (key P).
+//
+// The segmented scan of the positions' elements (leader slot, L) is fused
+// here, in two levels: each workgroup (kOrderPos positions, one tile) scans
+// its own elements and writes, for each position, the inclusive combination
+// within the tile (seg) and the tile's total (agg[tile]).
+// tile_prefix_kernel turns the totals into exclusive tile prefixes, and the
+// record writers combine a position's tile prefix with its in-tile value.
+// (A single-pass look-back over tiles was slower here: a tile's prefix can
+// be published only a device-scope load round-trip after its predecessor's,
+// far slower than tiles complete.)
+constexpr uint32_t kLcpLanes = 4;                  // lanes per hash-order position
+constexpr uint32_t kOrderPos = 256 / kLcpLanes;    // hash-order positions per order workgroup
+
+// 64-bit lane shuffle up by `off` lanes (within the wavefront).
+__device__ inline uint64_t shfl_up_u64(uint64_t v, uint32_t off) {
+    const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, off, kWave);
+    const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), off, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 template <uint32_t G>
 __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_t slp, uint32_t bt,
                                                     const uint32_t *__restrict__ perm,
                                                     const uint32_t *__restrict__ sorted_keys, Table t,
                                                     uint32_t reuse, uint64_t *__restrict__ seg,
+                                                    uint64_t *__restrict__ agg,
                                                     uint32_t *__restrict__ pkey, uint32_t *__restrict__ pval,
                                                     Pre *__restrict__ hrec, Cold *__restrict__ crec,
                                                     Lead *__restrict__ lead, uint32_t lead_cap,
                                                     unsigned int *__restrict__ n_lead, uint64_t hv_cap,
                                                     unsigned long long *__restrict__ hv_used,
                                                     uint32_t *__restrict__ n_valid) {
-    const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    static_assert(G * kOrderPos == 256, "positions per workgroup");
+    __shared__ uint64_t wtot[kWavesPerBlock];
     const uint32_t sub = threadIdx.x % G;
-    const uint32_t seg0 = (threadIdx.x % kWave) - sub;   // first lane of this position's lanes
-    const uint64_t i = tid / G;
-    if (i >= (uint64_t)rq.n_req) return;
-    const bool valid = sorted_keys[i] < kKeyInvalid;
-    const uint32_t r = perm[i];
-    if (sub == 0) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint32_t seg0 = lane - sub;   // first lane of this position's lanes
+    const uint64_t i = (uint64_t)blockIdx.x * kOrderPos + threadIdx.x / G;
+    const bool inb = i < (uint64_t)rq.n_req;
+    const bool valid = inb && sorted_keys[i] < kKeyInvalid;
+    const uint32_t r = inb ? perm[i] : 0u;
+    uint64_t e = kSegIdentity;   // this position's scan element (lane sub == 0)
+    if (inb && sub == 0) {
         if (valid && (i + 1 == rq.n_req || sorted_keys[i + 1] >= kKeyInvalid)) *n_valid = (uint32_t)(i + 1);
         if (i == 0 && !valid) *n_valid = 0;
         if (pval) pval[i] = (uint32_t)i;
-    }
-    if (!valid) {
-        if (sub == 0) {
-            seg[i] = seg_elem(kNoLead, 0);
+        if (!valid) {
+            e = seg_elem(kNoLead, 0);
             pkey[i] = P;
             hrec[i] = Pre{0, 0};
             crec[i] = Cold{r};
         }
-        return;
     }
-    const uint64_t a = rq.off[r];
-    const uint64_t nr = rq.off[r + 1] - a;
-    uint64_t l = 0;
-    // keys that differ in their first-block hash bits have different first
-    // blocks: nothing in common
-    if (i > 0 && reuse && (sorted_keys[i] >> kKeyLenBits) == (sorted_keys[i - 1] >> kKeyLenBits)) {
-        const uint32_t q = perm[i - 1];
-        const uint64_t b = rq.off[q];
-        const uint64_t nq = rq.off[q + 1] - b;
-        const uint64_t m = nr < nq ? nr : nq;
-        l = m;
-        // each lane compares U consecutive blocks per step, their loads
-        // issued together; the first differing block is the lowest lane's
-        // first stop
-        constexpr uint32_t U = 2;
-        for (uint64_t base = 0; base < m; base += (uint64_t)G * U) {
-            const uint64_t x0 = base + (uint64_t)sub * U;
-            uint64_t hr[U], hq[U];
+    if (valid) {
+        const uint64_t a = rq.off[r];
+        const uint64_t nr = rq.off[r + 1] - a;
+        uint64_t l = 0;
+        // keys that differ in their first-block hash bits have different
+        // first blocks: nothing in common
+        if (i > 0 && reuse && (sorted_keys[i] >> kKeyLenBits) == (sorted_keys[i - 1] >> kKeyLenBits)) {
+            const uint32_t q = perm[i - 1];
+            const uint64_t b = rq.off[q];
+            const uint64_t nq = rq.off[q + 1] - b;
+            const uint64_t m = nr < nq ? nr : nq;
+            l = m;
+            // each lane compares U consecutive blocks per step, their loads
+            // issued together; the first differing block is the lowest
+            // lane's first stop
+            constexpr uint32_t U = 2;
+            for (uint64_t base = 0; base < m; base += (uint64_t)G * U) {
+                const uint64_t x0 = base + (uint64_t)sub * U;
+                uint64_t hr[U], hq[U];
 #pragma unroll
-            for (uint32_t u = 0; u < U; ++u) {
-                const bool in = x0 + u < m;
-                hr[u] = in ? rq.hashes[a + x0 + u] : 0ull;
-                hq[u] = in ? rq.hashes[b + x0 + u] : 1ull;
-            }
-            uint32_t ls = U;   // this lane's first stop (U: none)
+                for (uint32_t u = 0; u < U; ++u) {
+                    const bool in = x0 + u < m;
+                    hr[u] = in ? rq.hashes[a + x0 + u] : 0ull;
+                    hq[u] = in ? rq.hashes[b + x0 + u] : 1ull;
+                }
+                uint32_t ls = U;   // this lane's first stop (U: none)
 #pragma unroll
-            for (int u = (int)U - 1; u >= 0; --u)
-                if (hr[u] != hq[u]) ls = (uint32_t)u;
-            const uint32_t bits = (uint32_t)(__ballot(ls < U) >> seg0) & (uint32_t)((1ull << G) - 1);
-            if (bits) {
-                const uint32_t fl = (uint32_t)__builtin_ctz(bits);
-                const uint32_t lsf = (uint32_t)__shfl((int)ls, (int)(seg0 + fl), kWave);
-                const uint64_t first = base + (uint64_t)fl * U + lsf;
-                l = first < m ? first : m;
-                break;
+                for (int u = (int)U - 1; u >= 0; --u)
+                    if (hr[u] != hq[u]) ls = (uint32_t)u;
+                const uint32_t bits = (uint32_t)(__ballot(ls < U) >> seg0) & (uint32_t)((1ull << G) - 1);
+                if (bits) {
+                    const uint32_t fl = (uint32_t)__builtin_ctz(bits);
+                    const uint32_t lsf = (uint32_t)__shfl((int)ls, (int)(seg0 + fl), kWave);
+                    const uint64_t first = base + (uint64_t)fl * U + lsf;
+                    l = first < m ? first : m;
+                    break;
+                }
             }
         }
-    }
-    if (sub != 0) return;
-    // a leader if some decode holds block L
-    const uint32_t vl = l < nr ? holder_lane(t, rq.hashes[a + l]) : kNoHolder;
-    uint64_t e = seg_elem(kNoLead, (uint32_t)l);
-    if (vl != kNoHolder) {
-        const unsigned int slot = atomicAdd(n_lead, 1u);
-        if (slot >= lead_cap) {
-            e = seg_elem(kLeadOver, kNoCap);
-        } else {
-            e = seg_elem(slot, kNoCap);
-            const unsigned long long o = atomicAdd(hv_used, (unsigned long long)nr);
-            Lead ld;
-            ld.a = a;
-            ld.hoff = o;
-            ld.n = (uint32_t)nr;
-            ld.m = o + nr <= hv_cap ? 0u : kNoPre;   // filled by lead_holder_kernel
-            ld.pad[0] = ld.pad[1] = 0;
-            lead[slot] = ld;
+        if (sub == 0) {
+            // a leader if some decode holds block L
+            const uint32_t vl = l < nr ? holder_lane(t, rq.hashes[a + l]) : kNoHolder;
+            e = seg_elem(kNoLead, (uint32_t)l);
+            if (vl != kNoHolder) {
+                const unsigned int slot = atomicAdd(n_lead, 1u);
+                if (slot >= lead_cap) {
+                    e = seg_elem(kLeadOver, kNoCap);
+                } else {
+                    e = seg_elem(slot, kNoCap);
+                    const unsigned long long o = atomicAdd(hv_used, (unsigned long long)nr);
+                    Lead ld;
+                    ld.a = a;
+                    ld.hoff = o;
+                    ld.n = (uint32_t)nr;
+                    ld.m = o + nr <= hv_cap ? 0u : kNoPre;   // filled by lead_holder_kernel
+                    ld.pad[0] = ld.pad[1] = 0;
+                    lead[slot] = ld;
+                }
+            }
+            pkey[i] = rq.prefill[r];
+            hrec[i] = Pre{rq.prefill[r] * slp * (uint32_t)sizeof(float2),   // < 2^32 (checked at load)
+                          rq.len[r]};
+            crec[i] = Cold{r};
         }
     }
-    seg[i] = e;
-    pkey[i] = rq.prefill[r];
-    hrec[i] = Pre{rq.prefill[r] * slp * (uint32_t)sizeof(float2),   // < 2^32 (checked at load)
-                  rq.len[r]};
-    crec[i] = Cold{r};
+    // the tile's scan: the wavefront's positions (lanes sub == 0, G apart)
+    // by shuffles, then the wavefronts' totals in order
+#pragma unroll
+    for (uint32_t off = G; off < (uint32_t)kWave; off <<= 1) {
+        const uint64_t prev = shfl_up_u64(e, off);
+        if (lane >= off) e = seg_op(prev, e);
+    }
+    const uint32_t w = threadIdx.x / kWave;
+    if (lane == kWave - G) wtot[w] = e;
+    __syncthreads();
+    uint64_t pre = kSegIdentity;
+    for (uint32_t q = 0; q < w; ++q) pre = seg_op(pre, wtot[q]);
+    e = seg_op(pre, e);
+    if (inb && sub == 0) seg[i] = e;
+    if (threadIdx.x == 0) {
+        uint64_t tot = kSegIdentity;
+#pragma unroll
+        for (uint32_t q = 0; q < kWavesPerBlock; ++q) tot = seg_op(tot, wtot[q]);
+        agg[blockIdx.x] = tot;
+    }
+}
+
+// Exclusive prefixes of the order workgroups' tile totals, in place: one
+// workgroup of kPrefixThreads, kPrefixThreads * kPrefixPer totals per round
+// (one round up to 2^24 requests), each thread combining its consecutive
+// totals, the threads' results scanned by shuffles and then across the
+// wavefronts, with the running prefix of earlier rounds.
+constexpr uint32_t kPrefixThreads = 1024;
+constexpr uint32_t kPrefixWaves = kPrefixThreads / kWave;
+constexpr uint32_t kPrefixPer = 16;
+__global__ __launch_bounds__(kPrefixThreads) void tile_prefix_kernel(uint64_t *__restrict__ agg, uint32_t n) {
+    __shared__ uint64_t wtot[kPrefixWaves];
+    __shared__ uint64_t carry_s;
+    const uint32_t tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+    uint64_t carry = kSegIdentity;
+    for (uint64_t r0 = 0; r0 < n; r0 += (uint64_t)kPrefixThreads * kPrefixPer) {
+        const uint64_t b0 = r0 + (uint64_t)tid * kPrefixPer;
+        uint64_t v[kPrefixPer];
+#pragma unroll
+        for (uint32_t u = 0; u < kPrefixPer; ++u) v[u] = b0 + u < n ? agg[b0 + u] : kSegIdentity;
+        uint64_t tot = kSegIdentity;
+#pragma unroll
+        for (uint32_t u = 0; u < kPrefixPer; ++u) tot = seg_op(tot, v[u]);
+        // inclusive scan of the threads' totals within the wavefront
+        uint64_t inc = tot;
+#pragma unroll
+        for (uint32_t off = 1; off < (uint32_t)kWave; off <<= 1) {
+            const uint64_t prev = shfl_up_u64(inc, off);
+            if (lane >= off) inc = seg_op(prev, inc);
+        }
+        const uint64_t prev1 = shfl_up_u64(inc, 1);
+        if (lane == kWave - 1) wtot[w] = inc;
+        __syncthreads();
+        uint64_t pre = carry;
+        for (uint32_t q = 0; q < w; ++q) pre = seg_op(pre, wtot[q]);
+        // this thread's first total's exclusive prefix
+        uint64_t run = lane > 0 ? seg_op(pre, prev1) : pre;
+#pragma unroll
+        for (uint32_t u = 0; u < kPrefixPer; ++u) {
+            if (b0 + u < n) agg[b0 + u] = run;
+            run = seg_op(run, v[u]);
+        }
+        if (tid == kPrefixThreads - 1) carry_s = run;
+        __syncthreads();
+        carry = carry_s;
+        __syncthreads();
+    }
+}
+
+// The scanned element (last leader slot, L*) of hash-order position i: its
+// tile's exclusive prefix combined with its inclusive value in the tile.
+__device__ inline uint64_t scanned_at(const uint64_t *seg, const uint64_t *tpre, uint64_t i) {
+    return seg_op(tpre[i / kOrderPos], seg[i]);
 }
 
 // Holder values of every leader's blocks from block 0 up to the first
@@ -623,7 +722,8 @@ __device__ inline Hot make_hot(Pre pr, uint64_t e, uint32_t bt, uint32_t lstride
 // may read ahead but never scores (row 0, no leader).
 __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t bt, uint32_t lstride, uint32_t zrow,
                                                        const uint32_t *__restrict__ pord,
-                                                       const uint64_t *__restrict__ scanned,
+                                                       const uint64_t *__restrict__ seg,
+                                                       const uint64_t *__restrict__ tpre,
                                                        const Pre *__restrict__ hrec, const Cold *__restrict__ crec,
                                                        Hot *__restrict__ hot, Cold *__restrict__ cold) {
     const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -633,7 +733,7 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
         return;
     }
     const uint32_t i = pord[k];
-    hot[k] = make_hot(hrec[i], scanned[i], bt, lstride, zrow);
+    hot[k] = make_hot(hrec[i], scanned_at(seg, tpre, i), bt, lstride, zrow);
     cold[k] = crec[i];
 }
 
@@ -771,7 +871,7 @@ __device__ inline uint64_t digit_peers(uint32_t d, uint32_t bits, uint64_t valid
 
 // Scatter of one pass.  The values are vin's, or the input positions when
 // vin is null.  ASSEMBLE: the values are hash-order positions and each
-// element writes its scoring records (from hrec, scanned and crec at that
+// element writes its scoring records (from hrec, the scan and crec at that
 // position) at its output position; the kHotPad records past the batch
 // are written too.  Otherwise (key, value) pairs go to kout / vout.
 template <bool ASSEMBLE>
@@ -782,7 +882,8 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
                                                               const uint32_t *__restrict__ tot,
                                                               uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
                                                               const Pre *__restrict__ hrec,
-                                                              const uint64_t *__restrict__ scanned,
+                                                              const uint64_t *__restrict__ seg,
+                                                              const uint64_t *__restrict__ tpre,
                                                               const Cold *__restrict__ crec, uint32_t bt,
                                                               uint32_t lstride, uint32_t zrow, Hot *__restrict__ hot,
                                                               Cold *__restrict__ cold) {
@@ -855,7 +956,7 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
             const uint32_t o = bb[d] + (j - toff[d]);
             if (ASSEMBLE) {
                 const uint32_t e = sv[j];
-                hot[o] = make_hot(hrec[e], scanned[e], bt, lstride, zrow);
+                hot[o] = make_hot(hrec[e], scanned_at(seg, tpre, e), bt, lstride, zrow);
                 cold[o] = crec[e];
             } else {
                 kout[o] = k;
@@ -1994,7 +2095,8 @@ struct Scratch {
     uint32_t *keys_in = nullptr, *keys_out = nullptr, *vals_in = nullptr, *perm = nullptr;
     Hot *hot = nullptr;       // [order_cap + kHotPad] scoring-order records, the part every step reads
     Cold *cold = nullptr;     // and the request's index in the batch
-    uint64_t *seg = nullptr, *scanned = nullptr;   // segmented-scan elements, hash order
+    uint64_t *seg = nullptr;    // in-tile inclusive scan of the positions' (leader, L) elements, hash order
+    uint64_t *tpre = nullptr;   // per order tile: its total, then the exclusive prefix of the tiles before it
     Pre *hrec = nullptr;      // prefill row and length by hash-order position
     Cold *crec = nullptr;
     uint32_t *pkey = nullptr, *pkey_out = nullptr, *pval = nullptr, *pord = nullptr;   // prefill order
@@ -2234,7 +2336,6 @@ netkv_status ready(netkv_handle h) {
     return NETKV_OK;
 }
 
-constexpr uint32_t kLcpLanes = 4;   // lanes per hash-order position in order_kernel
 constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
 // rocPRIM's radix sorts of the batch-order keys (batches outside the range
@@ -2264,7 +2365,7 @@ uint32_t bits_for(uint64_t v) {   // bits to hold 0..v
 
 void free_scratch(Scratch &sc) {
     dfree(sc.keys_in); dfree(sc.keys_out); dfree(sc.vals_in); dfree(sc.perm); dfree(sc.hot); dfree(sc.cold);
-    dfree(sc.seg); dfree(sc.scanned); dfree(sc.hrec); dfree(sc.crec);
+    dfree(sc.seg); dfree(sc.tpre); dfree(sc.hrec); dfree(sc.crec);
     dfree(sc.pkey); dfree(sc.pkey_out); dfree(sc.pval); dfree(sc.pord);
     dfree(sc.n_valid); dfree(sc.hv_used); dfree(sc.n_lead); dfree(sc.hv); dfree(sc.lead); dfree(sc.lead_lam);
     dfree(sc.sort_tmp); dfree(sc.sort_cnt); dfree(sc.sort_tot); dfree(sc.keys_tmp); dfree(sc.vals_tmp);
@@ -2273,16 +2374,14 @@ void free_scratch(Scratch &sc) {
 }
 
 // rocPRIM temporary storage for the batch orders of R requests (both sorts
-// and the segmented scan share one buffer); a size query only.
+// share one buffer); a size query only.
 hipError_t sort_tmp_bytes_for(uint64_t R, size_t &bytes) {
-    size_t b1 = 0, b2 = 0, b3 = 0;
+    size_t b1 = 0, b2 = 0;
     uint32_t *k = nullptr;
-    uint64_t *e = nullptr;
     hipError_t err = rocprim::radix_sort_pairs<SortConfig>(nullptr, b1, k, k, k, k, (uint32_t)R, 0, 32, nullptr);
     if (err == hipSuccess)
         err = rocprim::radix_sort_pairs<SortConfig>(nullptr, b2, k, k, k, k, (uint32_t)R, 0, 32, nullptr);
-    if (err == hipSuccess) err = rocprim::inclusive_scan(nullptr, b3, e, e, (size_t)R, SegOp(), nullptr);
-    bytes = std::max<size_t>(std::max(b1, std::max(b2, b3)), 16);
+    bytes = std::max<size_t>(std::max(b1, b2), 16);
     return err;
 }
 
@@ -2293,7 +2392,7 @@ netkv_status ensure_scratch(netkv_handle h, Scratch &sc, uint64_t R, uint64_t pa
                             hipStream_t st) {
     if (R > sc.order_cap) {
         dfree(sc.keys_in); dfree(sc.keys_out); dfree(sc.vals_in); dfree(sc.perm); dfree(sc.hot); dfree(sc.cold);
-        dfree(sc.seg); dfree(sc.scanned); dfree(sc.pkey); dfree(sc.pkey_out); dfree(sc.pval); dfree(sc.pord);
+        dfree(sc.seg); dfree(sc.tpre); dfree(sc.pkey); dfree(sc.pkey_out); dfree(sc.pval); dfree(sc.pord);
         dfree(sc.hrec); dfree(sc.crec);
         dfree(sc.sort_tmp);
         dfree(sc.sort_cnt); dfree(sc.sort_tot); dfree(sc.keys_tmp); dfree(sc.vals_tmp);
@@ -2302,7 +2401,7 @@ netkv_status ensure_scratch(netkv_handle h, Scratch &sc, uint64_t R, uint64_t pa
         if (dalloc(sc.keys_in, R) != hipSuccess || dalloc(sc.keys_out, R) != hipSuccess ||
             dalloc(sc.vals_in, R) != hipSuccess || dalloc(sc.perm, R) != hipSuccess ||
             dalloc(sc.hot, R + kHotPad) != hipSuccess || dalloc(sc.cold, R) != hipSuccess ||
-            dalloc(sc.seg, R) != hipSuccess || dalloc(sc.scanned, R) != hipSuccess ||
+            dalloc(sc.seg, R) != hipSuccess || dalloc(sc.tpre, R / kOrderPos + 1) != hipSuccess ||
             dalloc(sc.pkey, R) != hipSuccess || dalloc(sc.pkey_out, R) != hipSuccess ||
             dalloc(sc.pval, R) != hipSuccess || dalloc(sc.pord, R) != hipSuccess ||
             dalloc(sc.hrec, R) != hipSuccess || dalloc(sc.crec, R) != hipSuccess)
@@ -2364,7 +2463,8 @@ netkv_status ensure_scratch(netkv_handle h, Scratch &sc, uint64_t R, uint64_t pa
 template <bool ASSEMBLE>
 hipError_t sort_pass(netkv_handle h, Scratch &sc, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
                      uint32_t *vout, uint32_t n, uint32_t shift, uint32_t bits, const Pre *hrec,
-                     const uint64_t *scanned, const Cold *crec, uint32_t lstride, uint32_t zrow, Hot *hot,
+                     const uint64_t *seg, const uint64_t *tpre, const Cold *crec, uint32_t lstride, uint32_t zrow,
+                     Hot *hot,
                      Cold *cold, hipStream_t st) {
     if (n == 0) return hipSuccess;
     const uint32_t ntile = (n + kSortTile - 1) / kSortTile;   // <= kColPer * kBlock (n <= kSortMaxN)
@@ -2372,7 +2472,7 @@ hipError_t sort_pass(netkv_handle h, Scratch &sc, const uint32_t *kin, const uin
     hipLaunchKernelGGL(sort_colscan_kernel, dim3(1u << bits), dim3(kBlock), 0, st, sc.sort_cnt, ntile, bits,
                        sc.sort_tot);
     hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(ntile), dim3(kBlock), 0, st, kin, vin, n, shift, bits,
-                       (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout, vout, hrec, scanned,
+                       (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout, vout, hrec, seg, tpre,
                        crec, h->block_tokens, lstride, zrow, hot, cold);
     return hipGetLastError();
 }
@@ -2402,8 +2502,8 @@ hipError_t batch_sort_pairs(netkv_handle h, Scratch &sc, const uint32_t *kin, co
         // the last pass writes kout, the one before the ping-pong buffers, ...
         const bool to_out = ((passes - 1 - p) % 2) == 0;
         uint32_t *dk = to_out ? kout : sc.keys_tmp, *dv = to_out ? vout : sc.vals_tmp;
-        const hipError_t e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0,
-                                              0, nullptr, nullptr, st);
+        const hipError_t e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr,
+                                              nullptr, 0, 0, nullptr, nullptr, st);
         if (e != hipSuccess) return e;
         sk = dk;
         sv = dv;
@@ -2424,12 +2524,12 @@ hipError_t prefill_order(netkv_handle h, Scratch &sc, uint32_t n, uint32_t pbits
         pass_bits(pbits, passes, p, shift, bits);
         hipError_t e;
         if (p + 1 == passes) {
-            e = sort_pass<true>(h, sc, sk, sv, nullptr, nullptr, n, shift, bits, sc.hrec, sc.scanned, sc.crec,
+            e = sort_pass<true>(h, sc, sk, sv, nullptr, nullptr, n, shift, bits, sc.hrec, sc.seg, sc.tpre, sc.crec,
                                 lstride, zrow, sc.hot, sc.cold, st);
         } else {
             uint32_t *dk = (p % 2) ? buf_k : sc.keys_tmp, *dv = (p % 2) ? buf_v : sc.vals_tmp;
-            e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, 0, 0, nullptr,
-                                 nullptr, st);
+            e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, nullptr, 0, 0,
+                                 nullptr, nullptr, st);
             sk = dk;
             sv = dv;
         }
@@ -2591,15 +2691,17 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
     const bool own_prefill = own_sort && pbits <= kPrefillMaxBits;
     hipLaunchKernelGGL(order_kernel<kLcpLanes>, dim3((uint32_t)((R * kLcpLanes + 255) / 256)), dim3(256), 0, st, rq,
                        h->P, sl_pitch(h->D), h->block_tokens, (const uint32_t *)sc.perm,
-                       (const uint32_t *)sc.keys_out, t, h->reuse_opt, sc.seg, sc.pkey,
+                       (const uint32_t *)sc.keys_out, t, h->reuse_opt, sc.seg, sc.tpre, sc.pkey,
                        own_prefill ? nullptr : sc.pval, sc.hrec, sc.crec, sc.lead, lcap, sc.n_lead, hvcap,
                        sc.hv_used, sc.n_valid);
     hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((lcap + kWavesPerBlock - 1) /
                                                                              kWavesPerBlock, 4096)),
                        dim3(kBlock), 0, st, t, rq.hashes, sc.lead, (const unsigned int *)sc.n_lead, lcap, sc.hv);
+    // the exclusive prefixes of the order tiles' totals (the second level of
+    // the segmented scan; the first is in order_kernel)
+    hipLaunchKernelGGL(tile_prefix_kernel, dim3(1), dim3(kPrefixThreads), 0, st, sc.tpre,
+                       (uint32_t)((R + kOrderPos - 1) / kOrderPos));
     HIPCHK(h, hipGetLastError());
-    tb = sc.sort_tmp_bytes;
-    HIPCHK(h, rocprim::inclusive_scan(sc.sort_tmp, tb, (const uint64_t *)sc.seg, sc.scanned, (size_t)R, SegOp(), st));
     // prefill order (stable: the hash order within each prefill) and the
     // scoring records in it
     const uint32_t lstride = h->D * (uint32_t)sizeof(float);
@@ -2613,8 +2715,8 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
                                                         (uint32_t)R, 0, pbits, st));
         hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st,
                            (uint32_t)R, h->block_tokens, lstride, sc.lead_cap * lstride, (const uint32_t *)sc.pord,
-                           (const uint64_t *)sc.scanned, (const Pre *)sc.hrec, (const Cold *)sc.crec, sc.hot,
-                           sc.cold);
+                           (const uint64_t *)sc.seg, (const uint64_t *)sc.tpre, (const Pre *)sc.hrec,
+                           (const Cold *)sc.crec, sc.hot, sc.cold);
         HIPCHK(h, hipGetLastError());
     }
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
@@ -2675,7 +2777,7 @@ uint64_t carve(uint8_t *base, uint64_t r, uint32_t D, uint64_t partial_elems, ui
     t.hot = (Hot *)take(sizeof(Hot) * (r + kHotPad));
     t.cold = (Cold *)take(sizeof(Cold) * r);
     t.seg = (uint64_t *)take(8 * r);
-    t.scanned = (uint64_t *)take(8 * r);
+    t.tpre = (uint64_t *)take(8 * (r / kOrderPos + 1));
     t.hrec = (Pre *)take(sizeof(Pre) * r);
     t.crec = (Cold *)take(sizeof(Cold) * r);
     t.pkey = (uint32_t *)take(4 * r);
