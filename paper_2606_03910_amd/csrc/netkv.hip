@@ -433,11 +433,14 @@ struct Order {
 // check: no resident set holds it (cache loads reject it), so it is a miss
 // on every decode, as the prefix definition gives.  vals (the input
 // positions, for rocPRIM's sort) may be null.  Thread 0 clears the
-// holder-value and leader counters of the order kernel.
+// holder-value and leader counters of the order kernel.  An invalid
+// request's outputs (index -1, score NaN) are written here when out_idx is
+// given.
 __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max_blocks, uint32_t *__restrict__ keys,
                                                    uint32_t *__restrict__ vals, uint32_t *__restrict__ err,
                                                    unsigned long long *__restrict__ hv_used,
-                                                   unsigned int *__restrict__ n_lead) {
+                                                   unsigned int *__restrict__ n_lead, uint32_t k_out,
+                                                   int32_t *__restrict__ out_idx, float *__restrict__ out_score) {
     const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
     if (r == 0) {
         *hv_used = 0;
@@ -460,6 +463,13 @@ __global__ __launch_bounds__(256) void prep_kernel(Snap s, Reqs rq, uint32_t max
         keys[r] = key;
         if (vals) vals[r] = r;
         bad = !ok;
+        if (bad && out_idx) {
+            // an invalid request is answered here (the scoring kernel skips it)
+            for (uint32_t q = 0; q < k_out; ++q) {
+                out_idx[(uint64_t)r * k_out + q] = -1;
+                out_score[(uint64_t)r * k_out + q] = __builtin_nanf("");
+            }
+        }
     }
     if (__ballot(bad) && (threadIdx.x % kWave) == 0) atomicOr(err, kErrRequest);
 }
@@ -1203,19 +1213,34 @@ __device__ inline uint32_t route_cost(float x, float2 r1, float2 r2) {
     return min(c1, __float_as_uint(fmaf(x, r2.x, r2.y)));
 }
 
-template <int K, int W, int C, bool PAIRS, bool TWO>
-__global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Hot *__restrict__ hot,
-                                                       const Cold *__restrict__ cold,
-                                                       const float *__restrict__ lead_lam, uint32_t lead_rows,
-                                                       const uint64_t *__restrict__ hashes,
-                                                       const uint32_t *__restrict__ len_tokens,
-                                                       const uint64_t *__restrict__ hash_off,
-                                                       const uint32_t *__restrict__ n_valid, uint32_t n_req,
-                                                       uint32_t run_len, uint32_t n_runs, uint32_t ngroup,
-                                                       uint64_t *__restrict__ partial, PairOut po) {
+// Merged mode (MERGE, at most kMaxMergeGroups groups; used for a pool of
+// one group, where it saves the merge kernel): a workgroup is one run,
+// its wavefront w the decode group w; at the end of each chunk of requests
+// the wavefronts put their top-k keys in LDS (two buffers, alternating by
+// chunk), and after one barrier each wavefront merges a share of the
+// chunk's requests over all groups and writes their outputs.  A buffer is
+// written again only two chunks later, after the next barrier, which every
+// wavefront reaches only once its merge of the buffer is done.  Workgroups
+// go to the XCDs in turn, and XCD x takes the x-th contiguous eighth of the
+// runs, so its L2 holds the snapshot rows of its own prefills.
+constexpr uint32_t kMaxMergeGroups = 8;
+
+template <int K, int W, int C, bool PAIRS, bool TWO, bool MERGE>
+__global__ __launch_bounds__(MERGE ? kWave * kMaxMergeGroups : kBlock)
+void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__restrict__ cold,
+                  const float *__restrict__ lead_lam, uint32_t lead_rows, const uint64_t *__restrict__ hashes,
+                  const uint32_t *__restrict__ len_tokens, const uint64_t *__restrict__ hash_off,
+                  const uint32_t *__restrict__ n_valid, uint32_t n_req, uint32_t run_len, uint32_t n_runs,
+                  uint32_t ngroup, uint64_t *__restrict__ partial, PairOut po, uint32_t k_out,
+                  int32_t *__restrict__ out_idx, float *__restrict__ out_score) {
+    __shared__ uint64_t mkeys[MERGE ? 2 : 1][MERGE ? kMaxMergeGroups : 1][kWave];
     const uint32_t lane = threadIdx.x % kWave;
     uint32_t run, grp;
-    if (ngroup % kXcds == 0) {
+    if (MERGE) {
+        const uint32_t rpx = (n_runs + kXcds - 1) / kXcds;
+        run = (blockIdx.x % kXcds) * rpx + blockIdx.x / kXcds;
+        grp = wave_index();
+    } else if (ngroup % kXcds == 0) {
         // workgroups go to the XCDs in turn: XCD x takes groups
         // [x*gx, (x+1)*gx), so its decodes' snapshot columns stay in its
         // own L2; the waves of a workgroup take consecutive runs of one group
@@ -1421,8 +1446,36 @@ __global__ __launch_bounds__(kBlock) void score_kernel(Snap s, Table t, const Ho
             c0 = c1;
             c1 = c2;
         }
-        if (lane < (g1 - g0) * K)
-            partial[((uint64_t)grp * n_req + g0) * K + lane] = ((uint64_t)pc_bits << 32) | (uint64_t)pc_idx;
+        const uint64_t key = ((uint64_t)pc_bits << 32) | (uint64_t)pc_idx;
+        if (MERGE) {
+            const uint32_t buf = ((g0 - i0) / kPer) & 1u;
+            mkeys[buf][grp][lane] = key;
+            __syncthreads();
+            // request slot sl of the chunk (its keys in lanes sl*K ..
+            // sl*K+K-1 of every group) is merged by lane sl / ngroup of
+            // wavefront sl % ngroup
+            const uint32_t sl = grp + lane * ngroup;
+            if (sl < g1 - g0) {
+                uint64_t best[K];
+#pragma unroll
+                for (int q = 0; q < K; ++q) best[q] = kEmptyKey;
+                for (uint32_t g = 0; g < ngroup; ++g) {
+#pragma unroll
+                    for (int q = 0; q < K; ++q) {
+                        const uint64_t x = mkeys[buf][g][sl * K + q];
+                        if (x < best[K - 1]) topk_insert<K>(best, x);
+                    }
+                }
+                const uint64_t o = (uint64_t)cold[g0 + sl].r * k_out;
+                for (uint32_t q = 0; q < k_out; ++q) {
+                    const uint64_t m = best[q];
+                    out_idx[o + q] = m == kEmptyKey ? -1 : (int32_t)(uint32_t)m;
+                    out_score[o + q] = m == kEmptyKey ? __builtin_inff() : __uint_as_float((uint32_t)(m >> 32));
+                }
+            }
+        } else if (lane < (g1 - g0) * K) {
+            partial[((uint64_t)grp * n_req + g0) * K + lane] = key;
+        }
         pc_bits = 0xFFFFFFFFu;
         pc_idx = 0xFFFFFFFFu;
     }
@@ -2553,7 +2606,9 @@ uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
 // and 2 whose groups of 64 * C decodes split evenly over the XCDs (at least
 // one each), so that every XCD's L2 keeps its own slice of the snapshot
 // rows; else 2 on pools of 256+ decodes, else 1 (measured on MI355X: wider
-// groups share each request's scalar work over more decodes)
+// groups share each request's scalar work over more decodes; 12 per lane
+// spills registers, and merging the groups of 3,072 decodes in one
+// workgroup was slower than XCD-sliced groups and a merge kernel)
 inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
     if (opt == 1 || opt == 2 || opt == 3 || opt == 4 || opt == 6) return opt;
     for (uint32_t c : {6u, 3u, 2u}) {
@@ -2563,13 +2618,17 @@ inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
     return D >= 4u * kWave ? 2u : 1u;
 }
 
-// Leader kernel, then the scoring kernel: one workgroup per
+// Leader kernel, then the scoring kernel.  A pool of one group of one
+// decode per lane (up to 64 decodes) is scored in merged mode: one
+// wavefront per run, writing its requests' outputs itself.  Otherwise one
+// workgroup per
 // (kWavesPerBlock runs, group) when the groups split evenly over the XCDs
-// (see score_kernel), else per kWavesPerBlock waves.
+// (see score_kernel), else per kWavesPerBlock waves, writing per-group keys
+// that reduce_kernel merges.
 template <int K, int C>
 hipError_t launch_score(netkv_handle h, Scratch &sc, const Snap &sn, const Table &t, const Reqs &rq,
                         const Order &ord, uint32_t run_len, uint32_t n_runs, uint32_t ngroup, const PairOut &po,
-                        bool pairs, hipStream_t st) {
+                        bool pairs, uint32_t k, int32_t *idx, float *score, hipStream_t st) {
     // leaders: 64 decodes per wavefront, 64 blocks per step
     const uint32_t lgroup = (sn.D + kWave - 1) / kWave;
     const uint64_t lw = std::min<uint64_t>((uint64_t)ord.lead_cap * lgroup, 65536);
@@ -2578,52 +2637,61 @@ hipError_t launch_score(netkv_handle h, Scratch &sc, const Snap &sn, const Table
                        (const unsigned int *)sc.n_lead, ord.lead_cap, ord.hv, rq.hashes, lgroup, sc.lead_lam);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || (e = time_begin(h, st)) != hipSuccess) return e;
-    const uint64_t grid64 = ngroup % kXcds == 0
+    constexpr bool kMergeable = C == 1;
+    const bool merge = kMergeable && ngroup == 1;
+    const uint64_t grid64 = merge ? (uint64_t)(n_runs + kXcds - 1) / kXcds * kXcds
+                            : ngroup % kXcds == 0
                                 ? (uint64_t)((n_runs + kWavesPerBlock - 1) / kWavesPerBlock) * ngroup
                                 : ((uint64_t)n_runs * ngroup + kWavesPerBlock - 1) / kWavesPerBlock;
     const uint32_t grid = (uint32_t)grid64;
+    const uint32_t block = merge ? ngroup * kWave : kBlock;
     // a request that matches on its own (its leader did not fit the leader
     // table, or 2^24 tokens or more) looks blocks up one at a time: rare,
     // and a short loop keeps the kernel's registers for the common path
     const bool two = sn.sr != nullptr;
-#define NETKV_SCORE(P2, T2)                                                                                      \
-    hipLaunchKernelGGL((score_kernel<K, 1, C, P2, T2>), dim3(grid), dim3(kBlock), 0, st, sn, t, ord.hot, ord.cold, \
-                       ord.lam, sc.lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req, run_len, n_runs, \
-                       ngroup, sc.partial, po)
-    if (pairs) {
-        if (two) NETKV_SCORE(true, true);
-        else NETKV_SCORE(true, false);
+#define NETKV_SCORE(P2, T2, M2)                                                                                  \
+    hipLaunchKernelGGL((score_kernel<K, 1, C, P2, T2, M2>), dim3(grid), dim3(block), 0, st, sn, t, ord.hot,     \
+                       ord.cold, ord.lam, sc.lead_cap + 1, rq.hashes, rq.len, rq.off, ord.n_valid, rq.n_req,      \
+                       run_len, n_runs, ngroup, sc.partial, po, k, idx, score)
+    if (merge) {
+        if (pairs) {
+            if (two) NETKV_SCORE(true, true, kMergeable);
+            else NETKV_SCORE(true, false, kMergeable);
+        } else {
+            if (two) NETKV_SCORE(false, true, kMergeable);
+            else NETKV_SCORE(false, false, kMergeable);
+        }
     } else {
-        if (two) NETKV_SCORE(false, true);
-        else NETKV_SCORE(false, false);
+        if (pairs) {
+            if (two) NETKV_SCORE(true, true, false);
+            else NETKV_SCORE(true, false, false);
+        } else {
+            if (two) NETKV_SCORE(false, true, false);
+            else NETKV_SCORE(false, false, false);
+        }
     }
 #undef NETKV_SCORE
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return time_end(h, st);
+    if ((e = time_end(h, st)) != hipSuccess || merge) return e;
+    hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
+                       (const uint64_t *)sc.partial, (const Cold *)ord.cold, ord.n_valid, idx, score);
+    return hipGetLastError();
 }
 
 // Leader kernel, the scoring kernel (bracketed by the handle's timing events
-// when enabled), then the merge.
+// when enabled), then, outside merged mode, the merge.
 template <int K>
 hipError_t launch_score_reduce(netkv_handle h, Scratch &sc, const Snap &sn, const Table &t, const Reqs &rq,
                                const Order &ord, uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C,
                                const PairOut &po, bool pairs, uint32_t k, int32_t *idx, float *score,
                                hipStream_t st) {
-    hipError_t e = hipSuccess;
-    if (C == 6)
-        e = launch_score<K, 6>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
-    else if (C == 4)
-        e = launch_score<K, 4>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
-    else if (C == 3)
-        e = launch_score<K, 3>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
-    else if (C == 2)
-        e = launch_score<K, 2>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
-    else
-        e = launch_score<K, 1>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, st);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((reduce_kernel<K>), dim3((rq.n_req + 255) / 256), dim3(256), 0, st, rq.n_req, ngroup, k,
-                       (const uint64_t *)sc.partial, (const Cold *)ord.cold, ord.n_valid, idx, score);
-    return hipGetLastError();
+    switch (C) {
+    case 6: return launch_score<K, 6>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, k, idx, score, st);
+    case 4: return launch_score<K, 4>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, k, idx, score, st);
+    case 3: return launch_score<K, 3>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, k, idx, score, st);
+    case 2: return launch_score<K, 2>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, k, idx, score, st);
+    default: return launch_score<K, 1>(h, sc, sn, t, rq, ord, run_len, n_runs, ngroup, po, pairs, k, idx, score, st);
+    }
 }
 
 // Top-k width K of the kernels for k, decodes per lane C and decode groups.
@@ -2675,7 +2743,7 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
     // its buffers are there and the batch is in its range
     const bool own_sort = R > kSortMinN && R <= kSortMaxN && sc.sort_cnt != nullptr;
     hipLaunchKernelGGL(prep_kernel, dim3((uint32_t)((R + 255) / 256)), dim3(256), 0, st, sn, rq, max_blocks,
-                       sc.keys_in, own_sort ? nullptr : sc.vals_in, h->errword, sc.hv_used, sc.n_lead);
+                       sc.keys_in, own_sort ? nullptr : sc.vals_in, h->errword, sc.hv_used, sc.n_lead, k, idx, score);
     HIPCHK(h, hipGetLastError());
     size_t tb = sc.sort_tmp_bytes;
     if (own_sort)
