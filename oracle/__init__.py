@@ -67,6 +67,7 @@ def _load():
         lib.orc_rank_sweep.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32,
                                        C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p,
                                        C.c_void_p, C.c_int]
+        lib.orc_tier_inversions.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p, C.c_int]
         lib.orc_commit.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p,
                                    C.c_void_p, C.c_void_p]
@@ -203,6 +204,20 @@ def rank_sweep(snap, cache, req, util_scen: np.ndarray, k: int = 3, n_threads: i
     lib.orc_rank_sweep(C.byref(s.s), c.h, C.byref(q.r), S, u.ctypes.data, k, idx.ctypes.data,
                        score.ctypes.data, flips.ctypes.data, int(n_threads))
     return dict(idx=idx, score=score, flips=flips)
+
+
+def tier_inversions(snap, util_scen: np.ndarray, n_threads: int = 1) -> np.ndarray:
+    """Proposition 2's quantity per congestion scenario (netkv_oracle.c):
+    [S, 3] = (pairs the sufficient condition covers, inverted pairs among
+    them, all inverted pairs), over pairs of decodes on different tiers."""
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    u = _arr(util_scen, np.float32)
+    S = u.shape[0]
+    assert u.size == S * s.n_prefill * s.n_decode
+    out = np.empty((S, 3), dtype=np.uint64)
+    lib.orc_tier_inversions(C.byref(s.s), S, u.ctypes.data, out.ctypes.data, int(n_threads))
+    return out
 
 
 def commit(snap, cache, req, sel: np.ndarray, cap: int, mu: int, state: Dict[str, np.ndarray]):

@@ -337,6 +337,67 @@ void orc_rank_sweep(const orc_snapshot *s_in, const orc_cache *c, const orc_requ
     free(base);
 }
 
+/* Proposition 2 (Sec. V-D): tier-ranking inversions under a congestion
+ * scenario.  For every prefill instance p and every pair of decodes d, d'
+ * on different tiers from p, the bandwidths of Eq. (4) are compared under
+ * the loaded snapshot's congestion c and under the scenario's c^:
+ *     X = B'_tau (1 - c),  B'_tau = B_tau / (1 + n_inflight[tau][p])
+ * (the proposition states n = 0; the in-flight count is the same in both,
+ * so it scales B_tau only).  A pair whose snapshot values differ is
+ * inverted when the scenario does not keep that strict order.  The
+ * proposition's sufficient condition, taken per pair: with
+ *     eps = max(|c^(p,d) - c(p,d)|, |c^(p,d') - c(p,d')|),
+ * the order is kept when eps < |X - X'| / (B'_tau + B'_tau').  Per scenario
+ * out[3s + 0] = pairs the condition covers, out[3s + 1] = inverted pairs
+ * among them (0 by the proposition), out[3s + 2] = all inverted pairs.
+ * Every quantity is evaluated in fp64 in exactly this order:
+ *     b = tier_bw[tau] / (1.0 + n);  X = b * (1.0 - (double)c);
+ *     bound = |X - X'| / (b + b');   eps from the exact float differences. */
+static double share_bw(const orc_snapshot *s, uint32_t p, int tau) {
+    return s->tier_bw[tau] / (1.0 + (double)s->n_inflight[(uint64_t)tau * s->n_prefill + p]);
+}
+
+void orc_tier_inversions(const orc_snapshot *s, uint32_t n_scen, const float *util_scen, uint64_t *out,
+                         int n_threads) {
+    const uint32_t P = s->n_prefill, D = s->n_decode;
+    for (uint32_t sn = 0; sn < n_scen; ++sn) {
+        const float *u = util_scen + (uint64_t)sn * P * D;
+        uint64_t covered = 0, inv_covered = 0, inverted = 0;
+#ifdef _OPENMP
+        if (n_threads < 1) n_threads = 1;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads) reduction(+ : covered, inv_covered, inverted)
+#endif
+        for (int64_t p = 0; p < (int64_t)P; ++p) {
+            for (uint32_t d = 0; d < D; ++d) {
+                const uint64_t a = (uint64_t)p * D + d;
+                const int ta = s->tier_map[a];
+                const double ba = share_bw(s, (uint32_t)p, ta);
+                const double ca = (double)s->util[a], ha = (double)u[a];
+                const double xa = ba * (1.0 - ca), ya = ba * (1.0 - ha);
+                for (uint32_t e = d + 1; e < D; ++e) {
+                    const uint64_t b = (uint64_t)p * D + e;
+                    const int tb = s->tier_map[b];
+                    if (tb == ta) continue;   /* only pairs across tiers */
+                    const double bb = share_bw(s, (uint32_t)p, tb);
+                    const double cb = (double)s->util[b], hb = (double)u[b];
+                    const double xb = bb * (1.0 - cb), yb = bb * (1.0 - hb);
+                    if (xa == xb) continue;   /* no strict order to keep */
+                    const int inv = xa > xb ? !(ya > yb) : !(ya < yb);
+                    const double eps = fmax(fabs(ha - ca), fabs(hb - cb));
+                    const int cov = eps < fabs(xa - xb) / (ba + bb);
+                    covered += (uint64_t)cov;
+                    inv_covered += (uint64_t)(cov && inv);
+                    inverted += (uint64_t)inv;
+                }
+            }
+        }
+        out[3 * (uint64_t)sn] = covered;
+        out[3 * (uint64_t)sn + 1] = inv_covered;
+        out[3 * (uint64_t)sn + 2] = inverted;
+    }
+    (void)n_threads;
+}
+
 /* State carried from one batch to the next (streaming workload).
  * Algorithm 1 increments n_inflight[tau(p, d*)][p] after each selection and
  * the paper caps the counter (default 16); the transfer-complete callback

@@ -239,6 +239,84 @@ def test_prop2_no_inversion_below_bound(seed):
     assert inverted > 10
 
 
+def _two_tier_snapshot(c_fast, c_slow, ratio=4.0, n=(0, 0)):
+    """One prefill, a decode on a fast tier (1) and one on a slow tier (3)
+    with B_1 = ratio * B_3 (the 4:1 oversubscription of Proposition 2's
+    example)."""
+    nf = np.zeros(4, np.uint16)
+    nf[1], nf[3] = n
+    return tiny_snapshot(1, 2, [1, 3], [c_fast, c_slow], bw=(1, ratio * 1e9, 1, 1e9), n_inflight=nf)
+
+
+def test_prop2_count_on_the_papers_example():
+    """Sec. V-D's example: B_1 / B_3 = 4 and c* = 0.3 on both tiers give the
+    bound 0.42.  An error of 0.41 on the fast tier is covered and keeps the
+    order; 0.43 is beyond the bound (not covered) but, one-sided, still
+    keeps it; 0.53 inverts it (4 * 0.17 < 0.7)."""
+    g = _gold("paper_constants.json")["prop2_example"]
+    snap = _two_tier_snapshot(g["c_fast"], g["c_slow"], ratio=g["bw_ratio"])
+    c = g["c_fast"]
+    scen = np.array([[c + 0.41, c], [c + 0.43, c], [c + 0.53, c], [c, c]], np.float32)
+    out = oracle.tier_inversions(snap, scen)
+    assert out.tolist() == [[1, 0, 0], [0, 0, 0], [0, 0, 1], [1, 0, 0]]
+
+
+def test_prop2_count_worst_case_around_the_bound():
+    """The proof's worst case -- the faster tier's congestion raised and the
+    slower one's lowered by the same error -- on c_fast = 0.3, c_slow = 0.5
+    (bound (4 * 0.7 - 0.5) / 5 = 0.46): 0.45 is covered and keeps the order,
+    0.47 inverts it; with 3 transfers in flight on the fast tier (B_1 / 4 vs
+    B_3: 0.7 < 0.5 fails, so the slow tier leads) the roles swap."""
+    snap = _two_tier_snapshot(0.3, 0.5)
+    scen = np.array([[0.3 + 0.45, 0.5 - 0.45], [0.3 + 0.47, 0.5 - 0.47]], np.float32)
+    assert oracle.tier_inversions(snap, scen).tolist() == [[1, 0, 0], [0, 0, 1]]
+    # B'_1 = B_1 / 4 = B_3: X_fast = 0.7 B_3 > X_slow = 0.5 B_3 still, bound (0.7 - 0.5) / 2 = 0.1
+    snap_n = _two_tier_snapshot(0.3, 0.5, n=(3, 0))
+    scen_n = np.array([[0.3 + 0.09, 0.5 - 0.09], [0.3 + 0.11, 0.5 - 0.11]], np.float32)
+    assert oracle.tier_inversions(snap_n, scen_n).tolist() == [[1, 0, 0], [0, 0, 1]]
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_prop2_no_covered_pair_ever_inverts(seed):
+    """Proposition 2 on random clusters: whatever the scenario, no pair the
+    sufficient condition covers is inverted; noisier scenarios invert more
+    pairs; a noise-free scenario inverts none and covers every ordered pair
+    across tiers; pairs on one tier are never counted."""
+    rng = np.random.default_rng(200 + seed)
+    P, D = 3, 12
+    tm = rng.integers(0, 4, (P, D))
+    snap = tiny_snapshot(P, D, tm, rng.uniform(0, 0.9, (P, D)), bw=(900e9, 50e9, 25e9, 12.5e9),
+                         n_inflight=rng.integers(0, 5, 4 * P))
+    u = snap["util"].reshape(P, D).astype(np.float64)
+    scen = [u]
+    for sg in (0.05, 0.2, 0.8, 2.0):
+        for _ in range(25):
+            scen.append(np.minimum(u * np.exp(sg * rng.standard_normal((P, D))), 0.99))
+    out = oracle.tier_inversions(snap, np.array(scen, np.float32).reshape(len(scen), -1))
+    assert (out[:, 1] == 0).all()
+    across = sum(int(tm[p, a] != tm[p, b]) for p in range(P) for a in range(D) for b in range(a + 1, D))
+    assert out[0].tolist() == [across, 0, 0]
+    by_sigma = out[1:, 2].reshape(4, 25).mean(axis=1)
+    assert by_sigma[0] <= by_sigma[-1] and by_sigma[-1] > 0
+    one = tiny_snapshot(1, D, np.full(D, 2), rng.uniform(0, 0.9, D))
+    assert oracle.tier_inversions(one, np.array(scen, np.float32)[:, 0, :]).sum() == 0
+
+
+def test_prop2_count_is_invariant_to_decode_order():
+    """Counts are over unordered pairs: permuting the decodes (with their
+    tiers and congestion) leaves them unchanged."""
+    rng = np.random.default_rng(7)
+    P, D = 2, 10
+    tm = rng.integers(0, 4, (P, D))
+    u = rng.uniform(0, 0.9, (P, D))
+    scen = np.minimum(u[None] * np.exp(0.5 * rng.standard_normal((6, P, D))), 0.99)
+    a = oracle.tier_inversions(tiny_snapshot(P, D, tm, u), scen.reshape(6, -1).astype(np.float32))
+    perm = rng.permutation(D)
+    b = oracle.tier_inversions(tiny_snapshot(P, D, tm[:, perm], u[:, perm]),
+                               scen[:, :, perm].reshape(6, -1).astype(np.float32))
+    assert np.array_equal(a, b) and a[:, 2].sum() > 0
+
+
 # ---------------------------------------------------------------- tiers
 
 def test_tier_ordering_at_equal_load():
