@@ -454,8 +454,11 @@ def main():
     sel.close()
 
 
-FP32_PEAK_TFLOPS = 157.3   # MI355X published fp32 vector peak (counts packed fp32)
-SWEEP_FLOPS_PER_PAIR = 7    # (1 - c), B (1 - c), s_eff (1 + n), the division, + L, + load, (1 + n)
+# lane-operations per (scenario, request, decode) of the ranking sweep with
+# k = 3, once the pair's non-cached tokens are known: the FMA x * spt + (L +
+# load), three comparisons with the running top-3, one minimum and two
+# medians that update its values, and five selects that update its indices
+SWEEP_OPS_PER_PAIR = 12
 
 
 def bench_sweep(args, cfg, dev):
@@ -468,7 +471,7 @@ def bench_sweep(args, cfg, dev):
     ch = W.prefix_chains(cfg, args.seed)
     req = W.make_requests(cfg, args.seed, chains=ch)
     cache = W.make_caches(cfg, args.seed, chains=ch)
-    util_s, _ = W.scenario_utils(cfg, args.seed, snap["links"])
+    util_s, sig = W.scenario_utils(cfg, args.seed, snap["links"])
     S, R, D, P, k = cfg.n_scenarios, cfg.n_requests, cfg.n_decode, cfg.n_prefill, 3
     sel = netkv.Selector(0)
     sel.load_snapshot(snap)
@@ -477,10 +480,12 @@ def bench_sweep(args, cfg, dev):
     us = netkv.to_device(util_s.reshape(-1), dev)
     out = dict(idx=torch.empty(S * R * k, dtype=torch.int32, device=dev),
                score=torch.empty(S * R * k, dtype=torch.float32, device=dev),
-               flips=torch.empty(2 * S, dtype=torch.uint64, device=dev))
+               flips=torch.empty(2 * S, dtype=torch.uint64, device=dev),
+               inversions=torch.empty(3 * S, dtype=torch.uint64, device=dev))
 
     def step():
-        netkv.netkv_rank_sweep(sel.h, rd, S, us, k, out["idx"], out["score"], out["flips"], dev, P * D)
+        netkv.netkv_rank_sweep(sel.h, rd, S, us, k, out["idx"], out["score"], out["flips"], dev, P * D,
+                               out["inversions"])
 
     for _ in range(args.warmup):
         step()
@@ -503,22 +508,28 @@ def bench_sweep(args, cfg, dev):
     step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     log(f"sweep: step {step_ms:.3f} ms, sweep kernel {kern_ms:.3f} ms")
     pairs = S * R * D
-    flops = SWEEP_FLOPS_PER_PAIR * pairs
-    achieved = flops / (kern_ms * 1e-3) / 1e12
+    ops = SWEEP_OPS_PER_PAIR * pairs
+    achieved = ops / (kern_ms * 1e-3) / 1e12
+    inv = netkv.to_numpy(out["inversions"]).reshape(S, 3)
+    fl = netkv.to_numpy(out["flips"]).reshape(S, 2)
+    prop2 = {"covered_pairs_mean": float(inv[:, 0].mean()), "covered_inverted_total": int(inv[:, 1].sum()),
+             "inverted_pairs_mean_by_sigma": {str(sg): float(inv[sig == sg, 2].mean()) for sg in cfg.noise_sigmas},
+             "selected_tier_flip_rate_by_sigma": {str(sg): float(fl[sig == sg, 0].mean() / R)
+                                                  for sg in cfg.noise_sigmas}}
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.profile:
         import oracle
         threads = oracle.max_threads()
-        # scenario count doubled until one run takes about the requested time
+        # scenario count doubled until one run takes about 10 s
         ns = 4
         while True:
             t0 = time.perf_counter()
             oracle.rank_sweep(snap, cache, req, util_s[:ns], k=k, n_threads=threads)
             dt = time.perf_counter() - t0
-            if dt >= args.cpu_seconds / 2 or ns >= S:
+            if dt >= 5.0 or ns >= S:
                 break
             ns = min(S, ns * 2)
-        cpu = dict(value=ns * R * D / dt, unit="pairs/s", cores=threads, kind="oracle",
+        cpu = dict(value=ns * R * D / dt, unit="pairs/s", cores=threads, kind="oracle", cpu_model=cpu_model(),
                    sample=f"{ns} scenarios x {R} requests x {D} decodes (prefix match once, "
                           f"then rescoring), {dt:.1f} s")
     rec = {
@@ -532,12 +543,15 @@ def bench_sweep(args, cfg, dev):
         "config": {"workload": cfg.name, "requests": R, "decodes": D, "prefills": P,
                    "scenarios": S, "sigmas": list(cfg.noise_sigmas), "k": k,
                    "parallelism": "single-gpu"},
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": FP32_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / FP32_PEAK_TFLOPS, "traffic": None,
-                     "algorithmic_flops_per_launch": flops,
-                     "kernel": "sweep_kernel<4> (k=3)",
-                     "note": "7 fp32 operations per scenario-pair of Eqs. (3)-(5); the peak counts "
-                             "packed fp32, which the library is compiled without"},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK_TOPS, "unit": "TOP/s",
+                     "frac": achieved / ALU_PEAK_TOPS, "traffic": None,
+                     "algorithmic_ops_per_launch": ops, "ops_per_pair": SWEEP_OPS_PER_PAIR,
+                     "step_frac": ops / (step_ms * 1e-3) / 1e12 / ALU_PEAK_TOPS,
+                     "kernel": "sweep_kernel<3, 48, LDS, full>",
+                     "note": "12 lane-operations per scenario-pair (the FMA and the running top-3's "
+                             "compares, minimum, medians and index selects) against one wave64 VALU "
+                             "instruction per CU per cycle, the same peak as the selection's"},
+        "prop2": prop2,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

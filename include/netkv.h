@@ -247,20 +247,35 @@ netkv_status netkv_route2_of(netkv_handle h, const netkv_requests_t *req, uint32
 /* Stale-telemetry ranking sweep (Sec. V-D, Proposition 2): re-rank the
  * batch under n_scen congestion scenarios util_scen [n_scen][P*D] (DEVICE,
  * each value in [0,1)).  Prefix matches do not depend on telemetry and are
- * computed once.  Writes the top-k (1 <= k <= 8) of every scenario to
- * out_idx / out_score [n_scen][n_req][k] and, if out_flips is not NULL,
+ * computed once (the batch selection under the loaded snapshot, whose
+ * leader rows give every pair's non-cached tokens).  Writes the top-k
+ * (1 <= k <= 8) of every scenario to out_idx / out_score
+ * [n_scen][n_req][k]; a scenario equal to the loaded congestion reproduces
+ * netkv_select_batch's results bit for bit.  If out_flips is not NULL,
  * out_flips[2*s] = number of requests whose selected decode lies on a
  * different tier than the one selected under the loaded snapshot's own
  * congestion, out_flips[2*s+1] = number whose selected decode differs (a
- * rejection counts as its own tier and index).  Asynchronous; grows an
- * internal work buffer (n_req * n_decode * 2 bytes) on first use.  Prefix
- * lengths are kept in 16 bits: a request of more than 65535 blocks is
- * invalid here (index -1, score NaN, reported by netkv_sync_errors).
- * Scenario values are not validated (values >= 1 give non-positive
- * bandwidth and meaningless costs). */
+ * rejection counts as its own tier and index).  If out_inversions is not
+ * NULL, Proposition 2's quantity: over pairs of decodes on different tiers
+ * from one prefill instance, with X = B'(1 - c), B' = B_tau / (1 +
+ * n_inflight[tau][p]), under the snapshot's congestion and the scenario's,
+ *   out_inversions[3*s]   = pairs the proposition covers: the larger of the
+ *                           two pairs' congestion errors is below
+ *                           |X - X'| / (B'_tau + B'_tau');
+ *   out_inversions[3*s+1] = covered pairs whose order is inverted (0 by the
+ *                           proposition);
+ *   out_inversions[3*s+2] = all pairs whose strict snapshot order the
+ *                           scenario does not keep;
+ * evaluated in fp64 (the policy option does not apply to them).
+ * Asynchronous; grows internal buffers on first use (n_scen * P * D * 4
+ * bytes of per-scenario factors, 16 bytes per request of records, and the
+ * selection's buffers, see netkv_reserve).  Invalid requests get index -1
+ * and score NaN in every scenario.  Scenario values are not validated
+ * (values >= 1 give non-positive bandwidth and meaningless costs). */
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen,
                               const float *util_scen, uint32_t k, int32_t *out_idx,
-                              float *out_score, uint64_t *out_flips, void *stream);
+                              float *out_score, uint64_t *out_flips, uint64_t *out_inversions,
+                              void *stream);
 
 /* Between-batch update after the selections sel[n_req] (DEVICE; -1 =
  * rejected) of a batch (the in-flight increment of Algorithm 1 and the counter cap of

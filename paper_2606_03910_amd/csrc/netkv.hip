@@ -139,7 +139,6 @@ struct PairOut {
     uint16_t *j;        // [R][D]
     uint8_t *feas;      // [R][D]
     float *score;       // [R][D]
-    uint16_t *jT;       // [D][R] (internal, for the sweep)
 };
 
 // The two candidate buckets of hash h in a set of 2^b buckets (shift =
@@ -229,10 +228,6 @@ __device__ inline uint64_t feasible_limit(const Snap &s, uint64_t m) {
 
 __device__ inline float pair_score(uint32_t x, float spt, float lat, float base) {
     return fmaf((float)x, spt, lat + base);
-}
-
-__device__ inline uint64_t pack_key(float cost, uint32_t d) {
-    return ((uint64_t)__float_as_uint(cost) << 32) | (uint64_t)d;
 }
 
 template <int K>
@@ -729,13 +724,16 @@ __device__ inline Hot make_hot(Pre pr, uint64_t e, uint32_t bt, uint32_t lstride
 // all-zero row).  A request whose leader did not fit the leader table, or
 // of 2^24 tokens or more, is marked to be matched on its own.  Positions
 // past the batch (kHotPad of them) get a record that the scoring kernel
-// may read ahead but never scores (row 0, no leader).
+// may read ahead but never scores (row 0, no leader).  With hotr, each
+// request's record is also written at its index in the batch (the ranking
+// sweep reads records in batch order).
 __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t bt, uint32_t lstride, uint32_t zrow,
                                                        const uint32_t *__restrict__ pord,
                                                        const uint64_t *__restrict__ seg,
                                                        const uint64_t *__restrict__ tpre,
                                                        const Pre *__restrict__ hrec, const Cold *__restrict__ crec,
-                                                       Hot *__restrict__ hot, Cold *__restrict__ cold) {
+                                                       Hot *__restrict__ hot, Cold *__restrict__ cold,
+                                                       Hot *__restrict__ hotr) {
     const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= (uint64_t)n_req + kHotPad) return;
     if (k >= n_req) {
@@ -743,8 +741,11 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
         return;
     }
     const uint32_t i = pord[k];
-    hot[k] = make_hot(hrec[i], scanned_at(seg, tpre, i), bt, lstride, zrow);
-    cold[k] = crec[i];
+    const Hot rec = make_hot(hrec[i], scanned_at(seg, tpre, i), bt, lstride, zrow);
+    const Cold c = crec[i];
+    hot[k] = rec;
+    cold[k] = c;
+    if (hotr) hotr[c.r] = rec;
 }
 
 // ---------------------------------------------------------------- batch sorts
@@ -882,8 +883,9 @@ __device__ inline uint64_t digit_peers(uint32_t d, uint32_t bits, uint64_t valid
 // Scatter of one pass.  The values are vin's, or the input positions when
 // vin is null.  ASSEMBLE: the values are hash-order positions and each
 // element writes its scoring records (from hrec, the scan and crec at that
-// position) at its output position; the kHotPad records past the batch
-// are written too.  Otherwise (key, value) pairs go to kout / vout.
+// position) at its output position (and, with hotr, at the request's index
+// in the batch); the kHotPad records past the batch are written too.
+// Otherwise (key, value) pairs go to kout / vout.
 template <bool ASSEMBLE>
 __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__restrict__ kin,
                                                               const uint32_t *__restrict__ vin, uint32_t n,
@@ -896,7 +898,7 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
                                                               const uint64_t *__restrict__ tpre,
                                                               const Cold *__restrict__ crec, uint32_t bt,
                                                               uint32_t lstride, uint32_t zrow, Hot *__restrict__ hot,
-                                                              Cold *__restrict__ cold) {
+                                                              Cold *__restrict__ cold, Hot *__restrict__ hotr) {
     __shared__ uint32_t bb[kSortMaxBins];                     // the tile's first output position per digit
     __shared__ uint32_t hist[kWavesPerBlock][kSortMaxBins];   // per-wavefront counts, then their prefixes
     __shared__ uint32_t toff[kSortMaxBins];                   // first staging slot per digit
@@ -966,8 +968,11 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
             const uint32_t o = bb[d] + (j - toff[d]);
             if (ASSEMBLE) {
                 const uint32_t e = sv[j];
-                hot[o] = make_hot(hrec[e], scanned_at(seg, tpre, e), bt, lstride, zrow);
-                cold[o] = crec[e];
+                const Hot rec = make_hot(hrec[e], scanned_at(seg, tpre, e), bt, lstride, zrow);
+                const Cold c = crec[e];
+                hot[o] = rec;
+                cold[o] = c;
+                if (hotr) hotr[c.r] = rec;
             } else {
                 kout[o] = k;
                 vout[o] = sv[j];
@@ -1364,7 +1369,6 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
                     if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                     if (po.feas) po.feas[o] = feas ? 1 : 0;
                     if (po.score) po.score[o] = cost;
-                    if (po.jT) po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                 }
                 cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
             }
@@ -1388,8 +1392,6 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
                         if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                         if (po.feas) po.feas[o] = feas ? 1 : 0;
                         if (po.score) po.score[o] = cost;
-                        if (po.jT)
-                            po.jT[(uint64_t)d[q] * n_req + r_out] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                     }
                     cb[q] = feas ? __float_as_uint(cost) : 0xFFFFFFFFu;
                 }
@@ -1521,64 +1523,272 @@ __global__ __launch_bounds__(256) void reduce_kernel(uint32_t n_req, uint32_t nc
     }
 }
 
-// Ranking sweep: one thread per (request, scenario); decodes looped.
+// ---------------------------------------------------------------- ranking sweep
+//
+// Re-ranking of a batch under congestion scenarios (Sec. V-D).  Prefix
+// lengths do not depend on congestion: every request's non-cached tokens on
+// every decode come from its scoring record (leader row and cap, as in
+// score_kernel) once, and only seconds per token change per scenario.
+// Under scenario s the pair costs x * spt_s(p, d) + (L + load term), with
+// spt_s from the scenario's congestion by the same expression as the
+// snapshot's derived rows, so a scenario equal to the snapshot reproduces
+// the selection bit for bit.
+
+// Seconds per non-cached token of every (scenario, p, d).
+__global__ __launch_bounds__(256) void derive_scen_kernel(Snap s, const float *__restrict__ util_scen, uint64_t n,
+                                                          float *__restrict__ spt) {
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint64_t pd = i % ((uint64_t)s.P * s.D);
+    const uint32_t p = (uint32_t)(pd / s.D);
+    spt[i] = sec_per_token(s, s.tier_map[pd] & 3u, p, util_scen[i]);
+}
+
+constexpr uint32_t kSweepThreads = 256;   // requests per workgroup, one per thread, in batch order
+constexpr uint32_t kSweepScen = 32;       // scenarios per workgroup
+constexpr uint32_t kSweepMaxTab = 8192;   // largest P * Dp kept in LDS (two fp32 tables)
+
+// Ascending top-K list of fp32 cost bits (unsigned order) and decodes:
+// insert (key, d) by min / median-of-three on the values and selects on the
+// indices; decodes come in ascending order and only a strictly smaller key
+// moves ahead, so equal costs keep the lower index first.
 template <int K>
-__global__ __launch_bounds__(256) void sweep_kernel(Snap s, Reqs rq, const float *__restrict__ util_scen,
-                                                    const uint16_t *__restrict__ jT,
-                                                    const int32_t *__restrict__ base_idx,
-                                                    const float *__restrict__ base_score, uint32_t k,
-                                                    int32_t *__restrict__ out_idx,
-                                                    float *__restrict__ out_score,
-                                                    unsigned long long *__restrict__ flips) {
-    const uint32_t sc = blockIdx.y;
-    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
-    const bool act = r < rq.n_req;
-    uint32_t tier_flip = 0, idx_flip = 0;
-    if (act) {
-        uint32_t p, len, n;
-        uint64_t a;
-        uint64_t o = ((uint64_t)sc * rq.n_req + r) * k;
-        // invalid requests (also those the batch selection found invalid:
-        // a zero hash, a run too long for 16-bit prefix lengths) have a NaN
-        // selection score
-        if (!request_ok(rq, s, r, p, len, a, n) || __builtin_isnan(base_score[r])) {
-            for (uint32_t i = 0; i < k; ++i) {
-                out_idx[o + i] = -1;
-                out_score[o + i] = __builtin_nanf("");
-            }
-        } else {
-            const float *u = util_scen + (uint64_t)sc * s.P * s.D + (uint64_t)p * s.D;
-            uint64_t best[K];
+__device__ inline void topk_ins32(uint32_t (&t)[K], uint32_t (&ix)[K], uint32_t key, uint32_t d) {
+    bool c[K];
 #pragma unroll
-            for (int i = 0; i < K; ++i) best[i] = kEmptyKey;
-            for (uint32_t d = 0; d < s.D; ++d) {
-                uint32_t j = jT[(uint64_t)d * rq.n_req + r];
-                const uint32_t tau = s.tier_map[(uint64_t)p * s.D + d] & 3u;
-                const uint32_t x = len - s.block_tokens * j;
-                if ((uint64_t)x < s.dxlim[d]) {
-                    const float cost = pair_score(x, sec_per_token(s, tau, p, u[d]), s.lat[tau], s.dbase[d]);
-                    topk_insert<K>(best, pack_key(cost, d));
+    for (int q = 0; q < K; ++q) c[q] = key < t[q];
+#pragma unroll
+    for (int q = K - 1; q >= 1; --q) {
+        ix[q] = c[q - 1] ? ix[q - 1] : (c[q] ? d : ix[q]);
+        // the median of t[q-1], t[q] and key, in the form the compiler
+        // turns into one median-of-three instruction
+        t[q] = max(min(t[q - 1], t[q]), min(max(t[q - 1], t[q]), key));
+    }
+    ix[0] = c[0] ? d : ix[0];
+    t[0] = min(t[0], key);
+}
+
+// Decodes db .. db+63 holding a hash with holder value v, as a bit mask
+// (db a multiple of 64, or 0).
+__device__ inline uint64_t held_mask(const Table &t, uint32_t v, uint32_t db) {
+    if (v == kNoHolder) return 0;
+    if (v & kHeldOne) {
+        const uint32_t o = (v & ~kHeldOne) - db;
+        return o < (uint32_t)kWave ? 1ull << o : 0ull;
+    }
+    return t.bits[(uint64_t)v * t.bpitch + db / kWave];
+}
+
+// Non-cached tokens x of the lane's request on decodes db .. db+NX-1, as
+// fp32, -inf where infeasible.  From the leader row (min with the cap), or
+// for a request marked to match on its own, a first-miss scan of its run in
+// integers (x then rounded to fp32, as the scoring kernel does).
+template <int NX>
+__device__ inline void sweep_x(const Snap &s, const Table &t, const Reqs &rq, const Hot &rec, uint32_t r,
+                               const float *lead_lam, uint32_t db, float (&xf)[NX]) {
+    if ((int32_t)rec.lams >= 0) {
+        const float lenf = __uint_as_float(rec.len);
+        const float *row = lead_lam + rec.lrow / sizeof(float);
+#pragma unroll
+        for (int u = 0; u < NX; ++u) {
+            const uint32_t d = db + u;
+            float x = -__builtin_inff();
+            if (d < s.D) {
+                const uint64_t xlim = s.dxlim[d];
+                const float xm = xlim == 0 ? -1.0f : (float)(xlim - 1 < kExactTok ? xlim - 1 : (uint64_t)kExactTok);
+                const float lam = __uint_as_float(min(__float_as_uint(row[d]), rec.lams));
+                const float xx = lenf - lam;
+                x = xx <= xm ? xx : -__builtin_inff();
+            }
+            xf[u] = x;
+        }
+        return;
+    }
+    uint32_t p, len, n;
+    uint64_t a;
+    request_ok(rq, s, r, p, len, a, n);   // validated by the selection
+    uint32_t jx[NX];
+#pragma unroll
+    for (int u = 0; u < NX; ++u) jx[u] = n;
+    uint64_t alive = ~0ull;
+    for (uint32_t b = 0; b < n && alive; ++b) {
+        const uint64_t dead = alive & ~held_mask(t, holder_lane(t, rq.hashes[a + b]), db);
+#pragma unroll
+        for (int u = 0; u < NX; ++u) jx[u] = (dead >> u) & 1ull ? b : jx[u];
+        alive &= ~dead;
+    }
+#pragma unroll
+    for (int u = 0; u < NX; ++u) {
+        const uint32_t d = db + u;
+        float x = -__builtin_inff();
+        if (d < s.D) {
+            const uint32_t xi = len - s.block_tokens * jx[u];
+            x = (uint64_t)xi < s.dxlim[d] ? (float)xi : -__builtin_inff();
+        }
+        xf[u] = x;
+    }
+}
+
+// One thread per request (batch order), kSweepScen scenarios per
+// workgroup.  LDS: the (L + load term) constants of every (p, d) and the
+// current scenario's seconds per token, rows of Dp = D | 1 (an odd pitch,
+// so lanes of different prefills read different banks).  NX decodes'
+// tokens are held in registers; a pool of more decodes is taken NX at a
+// time and its tokens recomputed per scenario.  FULL: exactly NX decodes,
+// every decode index a compile-time constant (no bounds test per pair).
+// Writes the top-k of every scenario and counts, per scenario, the requests
+// whose selected tier / decode differs from the loaded snapshot's selection.
+template <int K, int NX, bool LDS, bool FULL>
+__global__ __launch_bounds__(kSweepThreads) void sweep_kernel(Snap s, Table t, Reqs rq, const Hot *__restrict__ hotr,
+                                                             const float *__restrict__ lead_lam,
+                                                             const float *__restrict__ spt_scen, uint32_t n_scen,
+                                                             const int32_t *__restrict__ base_idx,
+                                                             const float *__restrict__ base_score, uint32_t k_out,
+                                                             int32_t *__restrict__ out_idx,
+                                                             float *__restrict__ out_score,
+                                                             unsigned long long *__restrict__ flips) {
+    extern __shared__ float tab[];   // LDS: [P][Dp] constants, then [P][Dp] seconds per token
+    const uint32_t P = s.P, D = FULL ? (uint32_t)NX : s.D, Dp = D | 1u;
+    const uint32_t r = blockIdx.x * kSweepThreads + threadIdx.x;
+    const uint32_t s0 = blockIdx.y * kSweepScen;
+    const uint32_t s1 = min(s0 + kSweepScen, n_scen);
+    const bool act = r < rq.n_req;
+    const bool valid = act && !__builtin_isnan(base_score[r]);
+    Hot rec = Hot{0, 0, 0, 0};
+    uint32_t p = 0;
+    if (valid) {
+        rec = hotr[r];
+        p = rec.row / (s.slp * (uint32_t)sizeof(float2));
+    }
+    float *tc = tab, *ts = tab + (uint64_t)P * Dp;
+    if (LDS)
+        for (uint32_t i = threadIdx.x; i < P * D; i += kSweepThreads) {
+            const uint32_t pp = i / D, d = i - pp * D;
+            tc[pp * Dp + d] = s.sl[(uint64_t)pp * s.slp + d].y;
+        }
+    const bool one = FULL || D <= (uint32_t)NX;
+    float xf[NX];
+    if (valid && one) sweep_x<NX>(s, t, rq, rec, r, lead_lam, 0, xf);
+    const int32_t bsel = valid ? base_idx[r] : -1;
+    const int btier = bsel < 0 ? -1 : (int)(s.tier_map[(uint64_t)p * D + (uint32_t)bsel] & 3u);
+    const uint32_t lrow = p * Dp;
+    for (uint32_t sc = s0; sc < s1; ++sc) {
+        const float *sp = spt_scen + (uint64_t)sc * P * D;
+        if (LDS) {
+            __syncthreads();   // the previous scenario's table is no longer read
+            for (uint32_t i = threadIdx.x; i < P * D; i += kSweepThreads) {
+                const uint32_t pp = i / D;
+                ts[pp * Dp + (i - pp * D)] = sp[i];
+            }
+            __syncthreads();
+        }
+        uint32_t tk[K], ti[K];
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            tk[q] = 0xFFFFFFFFu;
+            ti[q] = 0xFFFFFFFFu;
+        }
+        if (valid) {
+            if (FULL) {
+#pragma unroll
+                for (int u = 0; u < NX; ++u) {
+                    const float spt = LDS ? ts[lrow + u] : sp[(uint64_t)p * D + u];
+                    const float cst = LDS ? tc[lrow + u] : s.sl[(uint64_t)p * s.slp + u].y;
+                    topk_ins32<K>(tk, ti, __float_as_uint(fmaf(xf[u], spt, cst)), (uint32_t)u);
+                }
+            } else {
+                for (uint32_t db = 0; db < D; db += NX) {
+                    if (!one) sweep_x<NX>(s, t, rq, rec, r, lead_lam, db, xf);
+#pragma unroll
+                    for (int u = 0; u < NX; ++u) {
+                        const uint32_t d = db + u;
+                        if (d < D) {
+                            const float spt = LDS ? ts[lrow + d] : sp[(uint64_t)p * D + d];
+                            const float cst = LDS ? tc[lrow + d] : s.sl[(uint64_t)p * s.slp + d].y;
+                            topk_ins32<K>(tk, ti, __float_as_uint(fmaf(xf[u], spt, cst)), d);
+                        }
+                    }
                 }
             }
-            for (uint32_t i = 0; i < k; ++i) {
-                uint64_t m = i < (uint32_t)K ? best[i] : kEmptyKey;
-                out_idx[o + i] = m == kEmptyKey ? -1 : (int32_t)(uint32_t)m;
-                out_score[o + i] = m == kEmptyKey ? __builtin_inff() : __uint_as_float((uint32_t)(m >> 32));
+        }
+        uint32_t tier_flip = 0, idx_flip = 0;
+        if (act) {
+            const uint64_t o = ((uint64_t)sc * rq.n_req + r) * k_out;
+#pragma unroll
+            for (int q = 0; q < K; ++q) {
+                if ((uint32_t)q < k_out) {
+                    // a key with its sign bit set is an infeasible pair (cost -inf)
+                    const bool none = !valid || tk[q] >= 0x80000000u;
+                    out_idx[o + q] = none ? -1 : (int32_t)ti[q];
+                    out_score[o + q] = !valid ? __builtin_nanf("") : none ? __builtin_inff() : __uint_as_float(tk[q]);
+                }
             }
-            int32_t sel = best[0] == kEmptyKey ? -1 : (int32_t)(uint32_t)best[0];
-            int32_t ref = base_idx[r];
-            int ts = sel < 0 ? -1 : (int)s.tier_map[(uint64_t)p * s.D + (uint32_t)sel];
-            int tr = ref < 0 ? -1 : (int)s.tier_map[(uint64_t)p * s.D + (uint32_t)ref];
-            tier_flip = ts != tr;
-            idx_flip = sel != ref;
+            if (valid) {
+                const int32_t sel = tk[0] >= 0x80000000u ? -1 : (int32_t)ti[0];
+                const int ts_ = sel < 0 ? -1 : (int)(s.tier_map[(uint64_t)p * D + (uint32_t)sel] & 3u);
+                tier_flip = ts_ != btier;
+                idx_flip = sel != bsel;
+            }
+        }
+        if (flips) {
+            const uint32_t fa = wave_sum_u32(tier_flip), fb = wave_sum_u32(idx_flip);
+            if ((threadIdx.x % kWave) == 0) {
+                if (fa) atomicAdd(flips + 2 * sc, (unsigned long long)fa);
+                if (fb) atomicAdd(flips + 2 * sc + 1, (unsigned long long)fb);
+            }
         }
     }
-    if (flips) {
-        uint32_t a = wave_sum_u32(tier_flip), b = wave_sum_u32(idx_flip);
-        if ((threadIdx.x % kWave) == 0) {
-            if (a) atomicAdd(flips + 2 * sc, (unsigned long long)a);
-            if (b) atomicAdd(flips + 2 * sc + 1, (unsigned long long)b);
+}
+
+// Proposition 2 (Sec. V-D) per scenario: pairs of decodes on different
+// tiers from one prefill instance, their bandwidths X = B'(1 - c) with
+// B' = B_tau / (1 + n_inflight[tau][p]) under the snapshot's congestion and
+// under the scenario's, counted into out[3 s + 0..2]: pairs the
+// proposition's sufficient condition covers (the larger of the two
+// congestion errors below |X - X'| / (B'_tau + B'_tau')), inverted pairs
+// among them, all inverted pairs (the snapshot's strict order not kept).
+// fp64, every operation in a fixed order, so the counts are exact.  One
+// thread per (p, d), pairs with the decodes after d.
+struct Bw64 {
+    double b[4];
+};
+
+__global__ __launch_bounds__(256) void tier_inv_kernel(Snap s, Bw64 bw, const float *__restrict__ util_scen,
+                                                       unsigned long long *__restrict__ out) {
+    const uint32_t sc = blockIdx.y;
+    const uint64_t pd = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint64_t npd = (uint64_t)s.P * s.D;
+    uint32_t covered = 0, inv_cov = 0, inverted = 0;
+    if (pd < npd) {
+        const uint32_t p = (uint32_t)(pd / s.D), d = (uint32_t)(pd - (uint64_t)p * s.D);
+        const float *u = util_scen + (uint64_t)sc * npd;
+        const uint32_t ta = s.tier_map[pd] & 3u;
+        const double ba = bw.b[ta] / (1.0 + (double)s.n_inflight[ta * s.P + p]);
+        const double ca = (double)s.util[pd], ha = (double)u[pd];
+        const double xa = ba * (1.0 - ca), ya = ba * (1.0 - ha);
+        for (uint32_t e = d + 1; e < s.D; ++e) {
+            const uint64_t q = (uint64_t)p * s.D + e;
+            const uint32_t tb = s.tier_map[q] & 3u;
+            if (tb == ta) continue;
+            const double bb = bw.b[tb] / (1.0 + (double)s.n_inflight[tb * s.P + p]);
+            const double cb = (double)s.util[q], hb = (double)u[q];
+            const double xb = bb * (1.0 - cb), yb = bb * (1.0 - hb);
+            if (xa == xb) continue;
+            const bool inv = xa > xb ? !(ya > yb) : !(ya < yb);
+            const double eps = fmax(fabs(ha - ca), fabs(hb - cb));
+            const bool cov = eps < fabs(xa - xb) / (ba + bb);
+            covered += cov;
+            inv_cov += cov && inv;
+            inverted += inv;
         }
+    }
+    covered = wave_sum_u32(covered);
+    inv_cov = wave_sum_u32(inv_cov);
+    inverted = wave_sum_u32(inverted);
+    if ((threadIdx.x % kWave) == 0) {
+        if (covered) atomicAdd(out + 3 * (uint64_t)sc, (unsigned long long)covered);
+        if (inv_cov) atomicAdd(out + 3 * (uint64_t)sc + 1, (unsigned long long)inv_cov);
+        if (inverted) atomicAdd(out + 3 * (uint64_t)sc + 2, (unsigned long long)inverted);
     }
 }
 
@@ -2170,6 +2380,8 @@ struct Scratch {
     uint32_t *sort_cnt = nullptr, *sort_tot = nullptr, *keys_tmp = nullptr, *vals_tmp = nullptr;
     uint64_t *partial = nullptr;   // [groups][R][K] per-group top-k keys
     uint64_t partial_cap = 0;
+    Hot *hotr = nullptr;           // scoring records by batch index (ranking sweep, sequential form)
+    uint64_t hotr_cap = 0;
 };
 
 }  // namespace
@@ -2195,6 +2407,7 @@ struct netkv_ctx {
     float *dbase = nullptr;      // [D]
     uint64_t *dxlim = nullptr;   // [D]
     float bw[4] = {0, 0, 0, 0}, lat[4] = {0, 0, 0, 0};
+    double bw64[4] = {0, 0, 0, 0};   // the snapshot's bandwidths as given (Proposition 2's counts)
     float t_a = 0, t_b = 0, alpha = 0;
     uint32_t beta_max = 0, bpt = 0, block_tokens = 1;
     uint64_t m_min = 0;
@@ -2210,8 +2423,8 @@ struct netkv_ctx {
     // scratch
     uint32_t *errword = nullptr;          // request / selection errors (sticky)
     uint32_t *loadword = nullptr;         // validation flags of the load calls
-    uint16_t *jT = nullptr;
-    uint64_t jT_bytes = 0;
+    float *spt_scen = nullptr;    // ranking sweep: seconds per token of every (scenario, p, d)
+    uint64_t spt_cap = 0;
     int32_t *base_idx = nullptr;
     float *base_score = nullptr;
     uint64_t base_n = 0;
@@ -2423,6 +2636,7 @@ void free_scratch(Scratch &sc) {
     dfree(sc.n_valid); dfree(sc.hv_used); dfree(sc.n_lead); dfree(sc.hv); dfree(sc.lead); dfree(sc.lead_lam);
     dfree(sc.sort_tmp); dfree(sc.sort_cnt); dfree(sc.sort_tot); dfree(sc.keys_tmp); dfree(sc.vals_tmp);
     dfree(sc.partial);
+    dfree(sc.hotr);
     sc = Scratch();
 }
 
@@ -2517,8 +2731,7 @@ template <bool ASSEMBLE>
 hipError_t sort_pass(netkv_handle h, Scratch &sc, const uint32_t *kin, const uint32_t *vin, uint32_t *kout,
                      uint32_t *vout, uint32_t n, uint32_t shift, uint32_t bits, const Pre *hrec,
                      const uint64_t *seg, const uint64_t *tpre, const Cold *crec, uint32_t lstride, uint32_t zrow,
-                     Hot *hot,
-                     Cold *cold, hipStream_t st) {
+                     Hot *hot, Cold *cold, Hot *hotr, hipStream_t st) {
     if (n == 0) return hipSuccess;
     const uint32_t ntile = (n + kSortTile - 1) / kSortTile;   // <= kColPer * kBlock (n <= kSortMaxN)
     hipLaunchKernelGGL(sort_count_kernel, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits, sc.sort_cnt);
@@ -2526,7 +2739,7 @@ hipError_t sort_pass(netkv_handle h, Scratch &sc, const uint32_t *kin, const uin
                        sc.sort_tot);
     hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(ntile), dim3(kBlock), 0, st, kin, vin, n, shift, bits,
                        (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout, vout, hrec, seg, tpre,
-                       crec, h->block_tokens, lstride, zrow, hot, cold);
+                       crec, h->block_tokens, lstride, zrow, hot, cold, hotr);
     return hipGetLastError();
 }
 
@@ -2556,7 +2769,7 @@ hipError_t batch_sort_pairs(netkv_handle h, Scratch &sc, const uint32_t *kin, co
         const bool to_out = ((passes - 1 - p) % 2) == 0;
         uint32_t *dk = to_out ? kout : sc.keys_tmp, *dv = to_out ? vout : sc.vals_tmp;
         const hipError_t e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr,
-                                              nullptr, 0, 0, nullptr, nullptr, st);
+                                              nullptr, 0, 0, nullptr, nullptr, nullptr, st);
         if (e != hipSuccess) return e;
         sk = dk;
         sv = dv;
@@ -2569,7 +2782,7 @@ hipError_t batch_sort_pairs(netkv_handle h, Scratch &sc, const uint32_t *kin, co
 // scoring records at their output positions; earlier passes go through
 // buf_k / buf_v (free at this point of a selection).
 hipError_t prefill_order(netkv_handle h, Scratch &sc, uint32_t n, uint32_t pbits, uint32_t *buf_k,
-                         uint32_t *buf_v, uint32_t lstride, uint32_t zrow, hipStream_t st) {
+                         uint32_t *buf_v, uint32_t lstride, uint32_t zrow, Hot *hotr, hipStream_t st) {
     const uint32_t passes = std::max(1u, (pbits + kSortMaxBits - 1) / kSortMaxBits);
     const uint32_t *sk = sc.pkey, *sv = nullptr;
     for (uint32_t p = 0; p < passes; ++p) {
@@ -2578,11 +2791,11 @@ hipError_t prefill_order(netkv_handle h, Scratch &sc, uint32_t n, uint32_t pbits
         hipError_t e;
         if (p + 1 == passes) {
             e = sort_pass<true>(h, sc, sk, sv, nullptr, nullptr, n, shift, bits, sc.hrec, sc.seg, sc.tpre, sc.crec,
-                                lstride, zrow, sc.hot, sc.cold, st);
+                                lstride, zrow, sc.hot, sc.cold, hotr, st);
         } else {
             uint32_t *dk = (p % 2) ? buf_k : sc.keys_tmp, *dv = (p % 2) ? buf_v : sc.vals_tmp;
             e = sort_pass<false>(h, sc, sk, sv, dk, dv, n, shift, bits, nullptr, nullptr, nullptr, nullptr, 0, 0,
-                                 nullptr, nullptr, st);
+                                 nullptr, nullptr, nullptr, st);
             sk = dk;
             sv = dv;
         }
@@ -2714,7 +2927,7 @@ Geometry geometry(netkv_handle h, uint32_t k) {
 // records, leaders' prefix lengths, scoring, merge.  Launches kernels only.
 netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req, uint32_t k, int32_t *idx,
                         float *score, const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st,
-                        bool route2 = false, bool derive = true) {
+                        bool route2 = false, bool derive = true, Hot *hotr = nullptr) {
     const uint64_t R = req->n_req;
     const Geometry geo = geometry(h, k);
     const uint32_t K = geo.K, C = geo.C, ngroup = geo.ngroup;
@@ -2776,7 +2989,7 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
     if (own_prefill) {
         // (the hash order's keys and permutation are no longer needed)
         HIPCHK(h, prefill_order(h, sc, (uint32_t)R, pbits, sc.keys_out, sc.perm, lstride, sc.lead_cap * lstride,
-                                st));
+                                hotr, st));
     } else {
         tb = sc.sort_tmp_bytes;
         HIPCHK(h, rocprim::radix_sort_pairs<SortConfig>(sc.sort_tmp, tb, sc.pkey, sc.pkey_out, sc.pval, sc.pord,
@@ -2784,7 +2997,7 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
         hipLaunchKernelGGL(assemble_kernel, dim3((uint32_t)((R + kHotPad + 255) / 256)), dim3(256), 0, st,
                            (uint32_t)R, h->block_tokens, lstride, sc.lead_cap * lstride, (const uint32_t *)sc.pord,
                            (const uint64_t *)sc.seg, (const uint64_t *)sc.tpre, (const Pre *)sc.hrec,
-                           (const Cold *)sc.crec, sc.hot, sc.cold);
+                           (const Cold *)sc.crec, sc.hot, sc.cold, hotr);
         HIPCHK(h, hipGetLastError());
     }
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
@@ -2806,13 +3019,24 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
 }
 
 // The handle's buffers for the batch, then the selection.
+// With want_hotr, every request's scoring record is also kept by batch
+// index in sc.hotr (grown to the batch).
 netkv_status select_owned(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
-                          const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false) {
+                          const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false,
+                          bool want_hotr = false) {
     const Geometry geo = geometry(h, k);
     netkv_status e = ensure_scratch(h, h->sc, req->n_req, (uint64_t)req->n_req * geo.ngroup * geo.K,
                                     req->n_hashes, st);
     if (e) return e;
-    return run_select(h, h->sc, req, k, idx, score, po, pairs, max_blocks, st, route2);
+    if (want_hotr && req->n_req > h->sc.hotr_cap) {
+        dfree(h->sc.hotr);
+        h->sc.hotr_cap = 0;
+        if (dalloc(h->sc.hotr, req->n_req) != hipSuccess)
+            return fail(h, NETKV_ENOMEM, "record scratch allocation failed");
+        h->sc.hotr_cap = req->n_req;
+    }
+    return run_select(h, h->sc, req, k, idx, score, po, pairs, max_blocks, st, route2, true,
+                      want_hotr ? h->sc.hotr : nullptr);
 }
 
 // ---- work buffers carved from the static scratch array (no allocation)
@@ -2905,6 +3129,40 @@ bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
 
 }  // namespace
 
+namespace {
+
+template <int K, int NX, bool LDS, bool FULL>
+void launch_sweep(dim3 grid, size_t lds, hipStream_t st, const Snap &sn, const Table &t, const Reqs &rq,
+                  const Hot *hotr, const float *lead_lam, const float *spt, uint32_t n_scen, const int32_t *bidx,
+                  const float *bsc, uint32_t k, int32_t *out_idx, float *out_score, unsigned long long *fl) {
+    hipLaunchKernelGGL((sweep_kernel<K, NX, LDS, FULL>), grid, dim3(kSweepThreads), lds, st, sn, t, rq, hotr,
+                       lead_lam, spt, n_scen, bidx, bsc, k, out_idx, out_score, fl);
+}
+
+// 48 decodes (the 64-GPU pools) with compile-time decode indices, up to 48
+// with a bounds test, more 64 at a time; the per-(p, d) tables in LDS when
+// they fit, else read from memory.
+template <int K>
+void launch_sweep_k(uint32_t D, bool lds, dim3 grid, size_t lds_bytes, hipStream_t st, const Snap &sn, const Table &t,
+                    const Reqs &rq, const Hot *hotr, const float *lead_lam, const float *spt, uint32_t n_scen,
+                    const int32_t *bidx, const float *bsc, uint32_t k, int32_t *out_idx, float *out_score,
+                    unsigned long long *fl) {
+    if (lds && D == 48)
+        launch_sweep<K, 48, true, true>(grid, lds_bytes, st, sn, t, rq, hotr, lead_lam, spt, n_scen, bidx, bsc, k,
+                                        out_idx, out_score, fl);
+    else if (lds && D < 48)
+        launch_sweep<K, 48, true, false>(grid, lds_bytes, st, sn, t, rq, hotr, lead_lam, spt, n_scen, bidx, bsc, k,
+                                         out_idx, out_score, fl);
+    else if (lds)
+        launch_sweep<K, 64, true, false>(grid, lds_bytes, st, sn, t, rq, hotr, lead_lam, spt, n_scen, bidx, bsc, k,
+                                         out_idx, out_score, fl);
+    else
+        launch_sweep<K, 64, false, false>(grid, 0, st, sn, t, rq, hotr, lead_lam, spt, n_scen, bidx, bsc, k, out_idx,
+                                          out_score, fl);
+}
+
+}  // namespace
+
 // ------------------------------------------------------------------ no-allocation scratch
 //
 // Work buffers of netkv_select_batch_noalloc: one array per device in the
@@ -2981,7 +3239,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->bits);
         dfree(h->errword);
         dfree(h->loadword);
-        dfree(h->jT);
+        dfree(h->spt_scen);
         dfree(h->base_idx);
         dfree(h->base_score);
         dfree(h->cnt);
@@ -3085,6 +3343,7 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
     h->D = D;
     for (int i = 0; i < 4; ++i) {
         h->bw[i] = (float)o->tier_bw[i];
+        h->bw64[i] = o->tier_bw[i];
         h->lat[i] = (float)o->tier_lat[i];
     }
     h->t_a = (float)o->t_iter_a;
@@ -3448,7 +3707,7 @@ netkv_status netkv_select_batch(netkv_handle h, const netkv_requests_t *req, uin
     if (req->n_req == 0) return NETKV_OK;
     DeviceGuard g(h->device);
     hipStream_t s = (hipStream_t)stream;
-    PairOut po{nullptr, nullptr, nullptr, nullptr};
+    PairOut po{nullptr, nullptr, nullptr};
     bool want_pairs = false;
     if (pairs) {
         po.j = pairs->prefix_blocks;
@@ -3477,7 +3736,7 @@ netkv_status netkv_select_batch_noalloc(netkv_handle h, const netkv_requests_t *
     Scratch sc;
     uint64_t r_sub = 0;
     if ((st = carve_static(h, base, req->n_req, k, sc, r_sub))) return st;
-    const PairOut po{nullptr, nullptr, nullptr, nullptr};
+    const PairOut po{nullptr, nullptr, nullptr};
     for (uint64_t r0 = 0; r0 < req->n_req; r0 += r_sub) {
         netkv_requests_t sub = *req;
         sub.n_req = (uint32_t)std::min<uint64_t>(r_sub, req->n_req - r0);
@@ -3508,26 +3767,39 @@ netkv_status netkv_reserve(netkv_handle h, uint32_t max_req, uint64_t max_hashes
 }
 
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen, const float *util_scen,
-                              uint32_t k, int32_t *out_idx, float *out_score, uint64_t *out_flips, void *stream) {
+                              uint32_t k, int32_t *out_idx, float *out_score, uint64_t *out_flips,
+                              uint64_t *out_inversions, void *stream) {
     if (!h) return NETKV_EINVAL;
     h->err.clear();
     netkv_status st = check_requests(h, req);
     if (st) return st;
     if (k < 1 || k > 8) return fail(h, NETKV_EINVAL, "k must be in [1, 8]");
     if (n_scen > 65535) return fail(h, NETKV_EINVAL, "n_scen must be <= 65535");
-    if (n_scen && req->n_req && (!util_scen || !out_idx || !out_score))
-        return fail(h, NETKV_EINVAL, "util_scen, out_idx and out_score must not be NULL");
+    if (n_scen && !util_scen) return fail(h, NETKV_EINVAL, "util_scen must not be NULL");
+    if (n_scen && req->n_req && (!out_idx || !out_score))
+        return fail(h, NETKV_EINVAL, "out_idx and out_score must not be NULL");
     if ((st = ready(h))) return st;
-    if (req->n_req == 0 || n_scen == 0) return NETKV_OK;
+    if (n_scen == 0) return NETKV_OK;
     DeviceGuard g(h->device);
     hipStream_t s = (hipStream_t)stream;
-    const uint64_t R = req->n_req, D = h->D;
-    if (h->jT_bytes < R * D * 2) {
-        dfree(h->jT);
-        h->jT_bytes = 0;
-        HIPCHK(h, dalloc(h->jT, R * D));
-        h->jT_bytes = R * D * 2;
+    const uint64_t R = req->n_req, P = h->P, D = h->D;
+    Snap sn = make_snap(h);
+    if (out_flips) {
+        hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(2ull * n_scen, 256)), dim3(256), 0, s, out_flips,
+                           2ull * n_scen, 0ull);
+        HIPCHK(h, hipGetLastError());
     }
+    if (out_inversions) {
+        // Proposition 2's counts depend on the snapshot and the scenarios only
+        hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(3ull * n_scen, 256)), dim3(256), 0, s, out_inversions,
+                           3ull * n_scen, 0ull);
+        Bw64 bw;
+        for (int i = 0; i < 4; ++i) bw.b[i] = h->bw64[i];
+        hipLaunchKernelGGL(tier_inv_kernel, dim3((uint32_t)((P * D + 255) / 256), n_scen), dim3(256), 0, s, sn, bw,
+                           util_scen, (unsigned long long *)out_inversions);
+        HIPCHK(h, hipGetLastError());
+    }
+    if (R == 0) return NETKV_OK;
     if (h->base_n < R) {
         dfree(h->base_idx);
         dfree(h->base_score);
@@ -3536,34 +3808,41 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
         HIPCHK(h, dalloc(h->base_score, R));
         h->base_n = R;
     }
-    Snap sn = make_snap(h);
-    Reqs rq = make_reqs(req);
-    // prefix lengths (transposed) and the selection under the loaded congestion
-    PairOut po{nullptr, nullptr, nullptr, h->jT};
+    const uint64_t nspt = (uint64_t)n_scen * P * D;
+    if (h->spt_cap < nspt) {
+        dfree(h->spt_scen);
+        h->spt_cap = 0;
+        HIPCHK(h, dalloc(h->spt_scen, nspt));
+        h->spt_cap = nspt;
+    }
+    // the selection under the loaded congestion, keeping every request's
+    // scoring record by batch index and the leaders' prefix lengths
     {
         TimingOff off(h);  // only the sweep kernel is timed
-        if ((st = select_owned(h, req, 1, h->base_idx, h->base_score, po, true, kMaxBlocks16, s))) return st;
+        const PairOut po{nullptr, nullptr, nullptr};
+        if ((st = select_owned(h, req, 1, h->base_idx, h->base_score, po, false, 0xFFFFFFFFu, s, false, true)))
+            return st;
     }
-    if (out_flips) {
-        hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(2ull * n_scen, 256)), dim3(256), 0, s, out_flips,
-                           2ull * n_scen, 0ull);
-        HIPCHK(h, hipGetLastError());
-    }
-    HIPCHK(h, time_begin(h, s));
-    dim3 grid((uint32_t)((R + 255) / 256), n_scen);
+    hipLaunchKernelGGL(derive_scen_kernel, dim3((uint32_t)((nspt + 255) / 256)), dim3(256), 0, s, sn, util_scen, nspt,
+                       h->spt_scen);
+    HIPCHK(h, hipGetLastError());
+    const Reqs rq = make_reqs(req);
+    const Table t = make_table(h);
+    const uint32_t Dp = (uint32_t)D | 1u;
+    const bool lds = P * Dp <= kSweepMaxTab;
+    const size_t lds_bytes = lds ? 2 * P * Dp * sizeof(float) : 0;
+    const dim3 grid((uint32_t)((R + kSweepThreads - 1) / kSweepThreads), (n_scen + kSweepScen - 1) / kSweepScen);
     unsigned long long *fl = (unsigned long long *)out_flips;
-    if (k <= 1)
-        hipLaunchKernelGGL(sweep_kernel<1>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
-                           out_score, fl);
-    else if (k <= 2)
-        hipLaunchKernelGGL(sweep_kernel<2>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
-                           out_score, fl);
-    else if (k <= 4)
-        hipLaunchKernelGGL(sweep_kernel<4>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
-                           out_score, fl);
-    else
-        hipLaunchKernelGGL(sweep_kernel<8>, grid, dim3(256), 0, s, sn, rq, util_scen, h->jT, h->base_idx, h->base_score, k, out_idx,
-                           out_score, fl);
+    HIPCHK(h, time_begin(h, s));
+#define NETKV_SWEEP(KK)                                                                                            \
+    launch_sweep_k<KK>((uint32_t)D, lds, grid, lds_bytes, s, sn, t, rq, h->sc.hotr, h->sc.lead_lam, h->spt_scen,    \
+                       n_scen, h->base_idx, h->base_score, k, out_idx, out_score, fl)
+    if (k == 1) NETKV_SWEEP(1);
+    else if (k == 2) NETKV_SWEEP(2);
+    else if (k == 3) NETKV_SWEEP(3);
+    else if (k == 4) NETKV_SWEEP(4);
+    else NETKV_SWEEP(8);
+#undef NETKV_SWEEP
     HIPCHK(h, hipGetLastError());
     HIPCHK(h, time_end(h, s));
     return NETKV_OK;
@@ -3727,7 +4006,7 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
         h->seq_P = (uint32_t)P;
     }
     // prefix lengths of every pair (and validation) by the batch scan
-    PairOut po{h->seq_j, nullptr, nullptr, nullptr};
+    PairOut po{h->seq_j, nullptr, nullptr};
     {
         TimingOff off(h);  // only the sequential kernel is timed
         if ((st = select_owned(h, req, 1, out_idx, out_score, po, true, kMaxBlocks16, s))) return st;

@@ -78,7 +78,7 @@ _SIGS = {
     "netkv_reserve": (C.c_int32, [C.c_void_p, C.c_uint32, C.c_uint64, C.c_uint32, C.c_void_p]),
     "netkv_rank_sweep": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
                                      C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p, C.c_void_p,
-                                     C.c_void_p]),
+                                     C.c_void_p, C.c_void_p]),
     "netkv_commit_batch": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_void_p,
                                        C.c_uint32, C.c_uint32, C.c_void_p]),
     "netkv_state_get": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -283,14 +283,16 @@ def netkv_reserve(h: int, max_req: int, max_hashes: int, max_k: int, device) -> 
 
 def netkv_rank_sweep(h: int, req: Dict[str, torch.Tensor], n_scen: int, util_scen: torch.Tensor,
                      k: int, out_idx: torch.Tensor, out_score: torch.Tensor,
-                     out_flips: Optional[torch.Tensor], device, n_cells: int) -> None:
+                     out_flips: Optional[torch.Tensor], device, n_cells: int,
+                     out_inversions: Optional[torch.Tensor] = None) -> None:
     r = _requests(req)
     n = r.n_req
     _check(h, load_library().netkv_rank_sweep(
         h, C.byref(r), int(n_scen), _dptr(util_scen, torch.float32, n_scen * n_cells, "util_scen"),
         int(k), _dptr(out_idx, torch.int32, n_scen * n * k, "out_idx"),
         _dptr(out_score, torch.float32, n_scen * n * k, "out_score"),
-        _dptr(out_flips, torch.uint64, 2 * n_scen, "out_flips"), _stream(device)))
+        _dptr(out_flips, torch.uint64, 2 * n_scen, "out_flips"),
+        _dptr(out_inversions, torch.uint64, 3 * n_scen, "out_inversions"), _stream(device)))
 
 
 def netkv_commit_batch(h: int, req: Dict[str, torch.Tensor], sel: torch.Tensor, cap: int, mu: int,
@@ -480,9 +482,10 @@ class Selector:
         dev = self.device
         out = dict(idx=torch.empty(S * n * k, dtype=torch.int32, device=dev),
                    score=torch.empty(S * n * k, dtype=torch.float32, device=dev),
-                   flips=torch.empty(2 * S, dtype=torch.uint64, device=dev))
+                   flips=torch.empty(2 * S, dtype=torch.uint64, device=dev),
+                   inversions=torch.empty(3 * S, dtype=torch.uint64, device=dev))
         netkv_rank_sweep(self.h, req_dev, S, util_scen, k, out["idx"], out["score"],
-                         out["flips"], dev, self.P * self.D)
+                         out["flips"], dev, self.P * self.D, out["inversions"])
         return out
 
     def commit(self, req_dev, sel: torch.Tensor, cap: int, mu: int) -> None:

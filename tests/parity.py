@@ -29,9 +29,10 @@ def classify(g_idx, o_idx, o_cost, near=NEAR_TIE, g_cost=None):
     g_cost [R, D] (the GPU's fp32 per-pair scores).
 
     Returns dict(positions, mismatches, near_ties, exact_ties_fp32_split,
-    exact_ties, beyond, max_rel_gap), where exact_ties counts mismatches at
-    an exact fp64 tie that the GPU's fp32 scores do not separate (a
-    tie-break error), exact_ties_fp32_split those that they do, and beyond
+    exact_ties, beyond, max_rel_gap), where exact_ties counts rows whose
+    first difference is at an exact fp64 tie that the GPU's fp32 scores do
+    not separate (a tie-break error: the oracle's choice is the lowest index
+    among the tied), exact_ties_fp32_split those that they do, and beyond
     the mismatches further apart than the near-tie rule allows."""
     g_idx = np.asarray(g_idx).reshape(np.asarray(o_idx).shape)
     R = g_idx.shape[0]
@@ -42,14 +43,18 @@ def classify(g_idx, o_idx, o_cost, near=NEAR_TIE, g_cost=None):
     cg = o_cost[rows, gi]
     co = o_cost[rows, oi]
     mism = ok & (g_idx != o_idx)
-    tie = mism & (cg == co)
+    # the exact-tie rule applies at a row's first difference: after it, a
+    # near-tie substitution shifts the rest of a top-k list, so later
+    # positions may pair up equal costs of different decodes
+    first = mism & (np.cumsum(mism, axis=1) == 1)
+    tie = first & (cg == co)
     split = np.zeros_like(tie)
     if g_cost is not None and tie.any():
         gc = np.asarray(g_cost, dtype=np.float32).reshape(R, -1)
         gb = _bits(gc[rows, gi])
         ob = _bits(gc[rows, oi])
         split = tie & (gb < ob)
-    near_m = mism & ~tie & (np.abs(cg - co) <= near * np.abs(co))
+    near_m = mism & ~tie & (np.abs(cg - co) <= near * np.abs(co))   # includes later equal costs
     beyond = mism & ~tie & ~near_m
     gap = np.abs(cg - co)[mism] / np.abs(co[mism]) if mism.any() else np.zeros(0)
     return dict(positions=int(ok.sum()), mismatches=int(mism.sum()), near_ties=int(near_m.sum()),
