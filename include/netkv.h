@@ -203,8 +203,10 @@ netkv_status netkv_select_batch_noalloc(netkv_handle h, const netkv_requests_t *
 /* Size the handle's selection work buffers ahead for batches of up to
  * max_req requests with up to max_hashes block hashes and 1 <= k <= max_k,
  * so that netkv_select_batch, netkv_rank_sweep and netkv_select_sequential
- * allocate no selection buffers for such batches afterwards (they grow
- * them otherwise, when a batch exceeds every earlier one).  Needs a loaded
+ * allocate no work buffers for such batches afterwards (they grow them
+ * otherwise, when a batch exceeds every earlier one) -- except the ranking
+ * sweep's per-scenario factors (4 * n_scen * P * D bytes), which depend on
+ * the scenario count.  Needs a loaded
  * snapshot (ENOTREADY) and is redone after a snapshot with another decode
  * count; synchronous with respect to allocation.  ENOMEM when the device
  * cannot hold them. */
@@ -305,10 +307,12 @@ netkv_status netkv_tier_counts(netkv_handle h, const netkv_requests_t *req, cons
  * instances do not interact.  Writes the argmin (index, score) per request
  * to out_idx / out_score ([n_req] DEVICE); invalid requests get -1 / NaN.
  * The handle's between-batch state is not changed (netkv_commit_batch
- * applies the batch).  Asynchronous; grows an internal buffer of
- * n_req * n_decode * 2 bytes (per-pair prefix lengths) on first use; a
- * request of more than 65535 blocks is invalid here, as for
- * netkv_rank_sweep. */
+ * applies the batch).  Asynchronous.  The prefix lengths come from the
+ * batch selection's per-request records and leader rows (no per-pair
+ * buffer): the work buffers are netkv_select_batch's at k = 1 plus
+ * 16 bytes per request (records by batch index) and 16 bytes per request
+ * for the per-prefill ordering, grown when a batch exceeds every earlier
+ * one (netkv_reserve sizes them ahead).  Runs of any length are valid. */
 netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req, uint32_t cap,
                                      int32_t *out_idx, float *out_score, void *stream);
 

@@ -20,6 +20,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "netkv_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle_netkv.so")
+# a checking build (build_sanitized) loaded instead of the default one
+_LIB_OVERRIDE = os.environ.get("NETKV_ORACLE_LIB")
 _lib = None
 
 
@@ -31,6 +33,17 @@ def build(force: bool = True) -> str:
                                "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
+
+
+def build_sanitized(path: str) -> str:
+    """Compile the oracle with AddressSanitizer and UndefinedBehaviorSanitizer
+    (every report fatal) into `path`.  A process loads it by setting
+    NETKV_ORACLE_LIB=path and preloading gcc's libasan (the ASan runtime must
+    come first)."""
+    subprocess.check_call(["gcc", "-O1", "-g", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+                           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                           "-fno-omit-frame-pointer", "-o", path, _SRC, "-lm"])
+    return path
 
 
 class _Snap(C.Structure):
@@ -55,8 +68,11 @@ class _Req(C.Structure):
 def _load():
     global _lib
     if _lib is None:
-        build(force=False)
-        lib = C.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            lib = C.CDLL(_LIB_OVERRIDE)
+        else:
+            build(force=False)
+            lib = C.CDLL(_LIB)
         lib.orc_cache_build.restype = C.c_void_p
         lib.orc_cache_build.argtypes = [C.c_uint32, C.c_void_p, C.c_void_p, C.c_int]
         lib.orc_cache_free.argtypes = [C.c_void_p]

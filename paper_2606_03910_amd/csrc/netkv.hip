@@ -1904,7 +1904,10 @@ __global__ __launch_bounds__(256) void index_insert_kernel(uint64_t *__restrict_
                 done = true;
                 break;
             }
-            // displace from the bucket the key did not just leave
+            // displace from the bucket the key did not just leave; the walk's
+            // choices come from the full-period 32-bit LCG of Knuth and Lewis
+            // (multiplier 1664525, increment 1013904223; Press et al.,
+            // Numerical Recipes, "quick and dirty" generator)
             rnd = rnd * 1664525u + 1013904223u;
             const uint32_t b = (b1 == from) ? b2 : (b2 == from) ? b1 : ((rnd >> 31) ? b2 : b1);
             const unsigned long long old = atomicExch(tab + 2 * (uint64_t)b + ((rnd >> 30) & 1u),
@@ -2135,8 +2138,10 @@ __global__ __launch_bounds__(256) void tier_count_kernel(Snap s, Reqs rq, const 
 // counter of the chosen tier grows by one (up to the cap) before the next
 // request from the same prefill instance is scored.  Requests of different
 // prefill instances do not interact, so each prefill instance's requests are
-// a sequential chain run by one workgroup, over prefix lengths computed
-// beforehand by the batch scan.
+// a sequential chain run by one workgroup.  The prefix lengths come from the
+// batch selection's scoring records (by batch index) and leader rows: the
+// chain reads min(leader row, B_tok * L*) per decode, as the scoring kernel
+// does, and no per-pair buffer is written.
 
 // start/end of each prefill instance's run in the order sorted by prefill
 __global__ void segment_kernel(const uint32_t *__restrict__ keys, uint32_t n, uint32_t P, uint32_t *__restrict__ start,
@@ -2157,11 +2162,60 @@ __global__ void prefill_key_kernel(Reqs rq, uint32_t P, const uint32_t *__restri
     vals[r] = r;
 }
 
+// Non-cached tokens x (Eq. (2)) of request r on decodes d0 + stride * k,
+// k < M, from its scoring record: the leader row capped by B_tok * L*, or,
+// for a request marked to match on its own, a first-miss scan of its hash
+// run over the holder index.  Integers throughout (a record's fp32 values
+// are integers below 2^24, so exact).  Decodes at or past D get len; the
+// caller never finds them feasible.
+template <int M>
+__device__ inline void seq_tokens(const Snap &s, const Table &t, const Reqs &rq, const Hot *__restrict__ hotr,
+                                  const float *__restrict__ lead_lam, uint32_t r, uint32_t d0, uint32_t stride,
+                                  uint32_t (&x)[M]) {
+    const Hot rec = hotr[r];
+    if ((int32_t)rec.lams >= 0) {
+        const uint32_t len = (uint32_t)__uint_as_float(rec.len);
+        const float *row = lead_lam + rec.lrow / sizeof(float);
+#pragma unroll
+        for (int k = 0; k < M; ++k) {
+            const uint32_t d = d0 + stride * k;
+            const uint32_t lam = d < s.D ? min(__float_as_uint(row[d]), rec.lams) : 0u;
+            x[k] = len - (uint32_t)__uint_as_float(lam);
+        }
+        return;
+    }
+    uint32_t p, len, n;
+    uint64_t a;
+    request_ok(rq, s, r, p, len, a, n);   // validated by the selection
+    uint32_t j[M];
+    uint32_t alive = 0;
+#pragma unroll
+    for (int k = 0; k < M; ++k) {
+        j[k] = n;
+        alive |= (d0 + stride * k < s.D ? 1u : 0u) << k;
+    }
+    for (uint32_t b = 0; b < n && alive; ++b) {
+        const uint32_t v = holder_lane(t, rq.hashes[a + b]);
+#pragma unroll
+        for (int k = 0; k < M; ++k) {
+            const uint32_t d = d0 + stride * k;
+            if (((alive >> k) & 1u) && !((held_mask(t, v, d & ~(uint32_t)(kWave - 1)) >> (d % kWave)) & 1ull)) {
+                j[k] = b;
+                alive &= ~(1u << k);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < M; ++k) x[k] = len - s.block_tokens * j[k];
+}
+
 constexpr int kSeqThreads = 256;
 
-__global__ __launch_bounds__(kSeqThreads) void sequential_kernel(Snap s, uint32_t n_req, uint32_t cap,
-                                                                 const uint16_t *__restrict__ jm,
-                                                                 const uint32_t *__restrict__ len,
+constexpr int kSeqChunk = 8;   // decodes per thread per pass of the general chain
+
+__global__ __launch_bounds__(kSeqThreads) void sequential_kernel(Snap s, Table t, Reqs rq, uint32_t cap,
+                                                                 const Hot *__restrict__ hotr,
+                                                                 const float *__restrict__ lead_lam,
                                                                  const uint32_t *__restrict__ order,
                                                                  const uint32_t *__restrict__ start,
                                                                  const uint32_t *__restrict__ end,
@@ -2178,19 +2232,23 @@ __global__ __launch_bounds__(kSeqThreads) void sequential_kernel(Snap s, uint32_
     __syncthreads();
     for (uint32_t i = i0; i < i1; ++i) {
         const uint32_t r = order[i];
-        const uint32_t l = len[r];
         uint32_t lb = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
-        for (uint32_t d = threadIdx.x; d < s.D; d += kSeqThreads) {
-            const uint32_t x = l - s.block_tokens * jm[(uint64_t)r * s.D + d];
-            if ((uint64_t)x < s.dxlim[d]) {
-                const uint64_t o = (uint64_t)p * s.D + d;
-                const uint32_t tau = s.tier_map[o] & 3u;
-                const float cost = pair_score(x, sec_per_token_n(s, tau, n_tier[tau], s.util[o]), s.lat[tau],
-                                              s.dbase[d]);
-                const uint32_t cbits = __float_as_uint(cost);
-                if (cbits < lb) {   // d grows within a thread: first strict minimum wins ties
-                    lb = cbits;
-                    ld = d;
+        for (uint32_t d0 = threadIdx.x; d0 < s.D; d0 += kSeqThreads * kSeqChunk) {
+            uint32_t xc[kSeqChunk];
+            seq_tokens<kSeqChunk>(s, t, rq, hotr, lead_lam, r, d0, kSeqThreads, xc);
+#pragma unroll
+            for (int k = 0; k < kSeqChunk; ++k) {
+                const uint32_t d = d0 + kSeqThreads * k, x = xc[k];
+                if (d < s.D && (uint64_t)x < s.dxlim[d]) {
+                    const uint64_t o = (uint64_t)p * s.D + d;
+                    const uint32_t tau = s.tier_map[o] & 3u;
+                    const float cost = pair_score(x, sec_per_token_n(s, tau, n_tier[tau], s.util[o]), s.lat[tau],
+                                                  s.dbase[d]);
+                    const uint32_t cbits = __float_as_uint(cost);
+                    if (cbits < lb) {   // d grows within a thread: first strict minimum wins ties
+                        lb = cbits;
+                        ld = d;
+                    }
                 }
             }
         }
@@ -2232,16 +2290,30 @@ __device__ inline float pick4(const float (&v)[4], uint32_t t) {
 // The same chain with each thread's decodes (d = thread + T*k, k < MAXC)
 // held in registers: tier (2 bits each in one word), seconds per token,
 // tier latency plus load term, and the feasibility limit (32 bits, with a
-// bit for limits of 2^32 and more, which every x meets).  Between requests
-// only the factors of the tier whose counter grew change, and they are
-// recomputed with the same expression.  The next request's prefix lengths
-// are loaded a request ahead into the other of two buffers; the waves'
+// bit for limits of 2^32 and more, which every x meets); the prefill row's
+// congestion sits in LDS.  Between requests only the factors of the tier
+// whose counter grew change, and they are recomputed with the same
+// expression.
+//
+// Pipeline: the chain's scoring records (and batch indices) are staged in
+// LDS T at a time, two chunks deep, so a request's record is an LDS read;
+// the leader-row values of the next request are loaded while the current
+// one is scored (raw bits, into the other of two buffers).  Each wave's
+// minimum carries the winner's decode and tier (d << 2 | tier), the waves'
 // minima go to alternating LDS slots and every thread picks the winner, so
-// one barrier per request suffices (a wave can write a slot again only after
-// the barrier that follows every wave's reading of it).
+// one barrier per request suffices (a wave can write a slot again only
+// after the barrier that follows every wave's reading of it) and the
+// counter update needs no memory read.
+template <int MAXC>
+struct SeqBuf {
+    uint32_t raw[MAXC];   // leader-row bits B_tok * j, or B_tok * j itself (own scan)
+    uint32_t len, lams, own, r;
+};
+
 template <int T, int MAXC>
-__global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, uint32_t cap, const uint16_t *__restrict__ jm,
-                                                              const uint32_t *__restrict__ len,
+__global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, Table t, Reqs rq, uint32_t cap,
+                                                              const Hot *__restrict__ hotr,
+                                                              const float *__restrict__ lead_lam,
                                                               const uint32_t *__restrict__ order,
                                                               const uint32_t *__restrict__ start,
                                                               const uint32_t *__restrict__ end,
@@ -2250,6 +2322,13 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, uint32_t c
     static_assert(MAXC <= 16, "two tier bits per decode in one word");
     constexpr int NW = T / kWave;
     __shared__ uint32_t slot_c[2][NW], slot_d[2][NW];
+    __shared__ Hot crec[2][T];
+    __shared__ uint32_t cr[2][T];
+    // per thread-decode (index k * T + thread), each entry only ever used by
+    // its own thread: the congestion, and a staging area for seconds per
+    // token (set-up, counter updates) or an own scan's B_tok * j
+    __shared__ float urow[T * MAXC];
+    __shared__ uint32_t stage[T * MAXC];
     const uint32_t p = blockIdx.x;
     const uint32_t i0 = start[p], i1 = end[p];
     if (i0 >= i1) return;
@@ -2257,94 +2336,156 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, uint32_t c
     const uint64_t row = (uint64_t)p * s.D;
     float n_tier[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) n_tier[t] = (float)s.n_inflight[t * s.P + p];
+    for (int q = 0; q < 4; ++q) n_tier[q] = (float)s.n_inflight[q * s.P + p];
     uint32_t tmask = 0, big = 0;
     float sk[MAXC], lk[MAXC];
     uint32_t xk[MAXC];
+    // the factors, one decode at a time through LDS (keeps the divisions'
+    // temporaries out of the register budget)
+#pragma unroll 1
+    for (int k = 0; k < MAXC; ++k) {
+        const uint32_t d = threadIdx.x + T * k;
+        const uint32_t dd = d < s.D ? d : 0;
+        const uint32_t tq = s.tier_map[row + dd] & 3u;
+        const float u = s.util[row + dd];
+        urow[k * T + threadIdx.x] = u;
+        stage[k * T + threadIdx.x] = __float_as_uint(sec_per_token_n(s, tq, pick4(n_tier, tq), u));
+        tmask |= tq << (2 * k);
+    }
 #pragma unroll
     for (int k = 0; k < MAXC; ++k) {
         const uint32_t d = threadIdx.x + T * k;
         const bool ok = d < s.D;
         const uint32_t dd = ok ? d : 0;
-        const uint32_t t = s.tier_map[row + dd] & 3u;
-        tmask |= t << (2 * k);
-        sk[k] = sec_per_token_n(s, t, pick4(n_tier, t), s.util[row + dd]);
-        lk[k] = tier_latency(s, t) + s.dbase[dd];
+        sk[k] = __uint_as_float(stage[k * T + threadIdx.x]);
+        lk[k] = tier_latency(s, (tmask >> (2 * k)) & 3u) + s.dbase[dd];
         const uint64_t xl = ok ? s.dxlim[dd] : 0;   // 0: never feasible, so never chosen
         xk[k] = xl > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)xl;
         big |= (xl > 0xFFFFFFFFull ? 1u : 0u) << k;
     }
-    auto load_j = [&](uint32_t r, uint16_t (&jj)[MAXC]) {
-#pragma unroll
-        for (int k = 0; k < MAXC; ++k) {
-            const uint32_t d = threadIdx.x + T * k;
-            jj[k] = d < s.D ? jm[(uint64_t)r * s.D + d] : 0;
+    // stage chunk c (positions i0 + c*T ...) of the chain's records in LDS
+    auto fill = [&](uint32_t c) {
+        const uint32_t i = i0 + c * T + threadIdx.x;
+        if (i < i1) {
+            const uint32_t r = order[i];
+            crec[c & 1u][threadIdx.x] = hotr[r];
+            cr[c & 1u][threadIdx.x] = r;
         }
     };
-    // score request r (prefix lengths jc), choose, count the choice
-    auto step = [&](uint32_t i, uint32_t r, const uint16_t (&jc)[MAXC]) {
-        const uint32_t l = len[r];
+    // read position i's record and start loading its leader-row values
+    auto issue = [&](uint32_t i, SeqBuf<MAXC> &b) {
+        const uint32_t o = i - i0, c = o / T;
+        if (o % T == 0 && c >= 1) fill(c + 1);   // chunk c-1's last record was read before the last barrier
+        const Hot &h = crec[c & 1u][o % T];
+        const uint32_t r = __builtin_amdgcn_readfirstlane(cr[c & 1u][o % T]);
+        const uint32_t lams = __builtin_amdgcn_readfirstlane(h.lams);
+        b.r = r;
+        if ((int32_t)lams >= 0) {
+            const float *lrow = lead_lam + __builtin_amdgcn_readfirstlane(h.lrow) / sizeof(float);
+            b.len = (uint32_t)__uint_as_float(__builtin_amdgcn_readfirstlane(h.len));
+            b.lams = lams;
+            b.own = 0;
+#pragma unroll
+            for (int k = 0; k < MAXC; ++k) {
+                // decodes past D read decode 0's value; their limit 0 makes them infeasible
+                const uint32_t d = threadIdx.x + T * k;
+                b.raw[k] = __float_as_uint(lrow[d < s.D ? d : 0u]);
+            }
+        } else {
+            // matched on its own: a first-miss scan of its run per decode, in
+            // integers, B_tok * j through LDS
+            uint32_t pp, len, n;
+            uint64_t a;
+            request_ok(rq, s, r, pp, len, a, n);   // validated by the selection
+#pragma unroll 1
+            for (int k = 0; k < MAXC; ++k) {
+                const uint32_t d = threadIdx.x + T * k;
+                uint32_t j = n;
+                if (d < s.D) {
+                    const uint32_t db = d & ~(uint32_t)(kWave - 1), bit = d % kWave;
+                    for (uint32_t bk = 0; bk < n; ++bk)
+                        if (!((held_mask(t, holder_lane(t, rq.hashes[a + bk]), db) >> bit) & 1ull)) {
+                            j = bk;
+                            break;
+                        }
+                }
+                stage[k * T + threadIdx.x] = s.block_tokens * j;
+            }
+            b.len = len;
+            b.lams = 0xFFFFFFFFu;
+            b.own = 1;
+#pragma unroll
+            for (int k = 0; k < MAXC; ++k) b.raw[k] = stage[k * T + threadIdx.x];
+        }
+    };
+    // score the buffered request, choose, count the choice
+    auto step = [&](uint32_t i, const SeqBuf<MAXC> &b) {
         uint32_t lb = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
 #pragma unroll
         for (int k = 0; k < MAXC; ++k) {
-            const uint32_t x = l - s.block_tokens * jc[k];
+            const uint32_t lam = b.own ? b.raw[k] : (uint32_t)__uint_as_float(min(b.raw[k], b.lams));
+            const uint32_t x = b.len - lam;
             if (x < xk[k] || ((big >> k) & 1u)) {
                 const uint32_t cbits = __float_as_uint(fmaf((float)x, sk[k], lk[k]));
                 if (cbits < lb) {   // d grows with k: the first strict minimum wins ties
                     lb = cbits;
-                    ld = threadIdx.x + T * k;
+                    ld = ((threadIdx.x + T * k) << 2) | ((tmask >> (2 * k)) & 3u);
                 }
             }
         }
         const uint32_t mn = wave_min_u32_dpp(lb);
         const uint32_t dm = wave_min_u32_dpp(lb == mn ? ld : 0xFFFFFFFFu);
-        const uint32_t b = i & 1u;
+        const uint32_t sl = i & 1u;
         if (lane == 0) {
-            slot_c[b][wave] = mn;
-            slot_d[b][wave] = dm;
+            slot_c[sl][wave] = mn;
+            slot_d[sl][wave] = dm;
         }
         __syncthreads();
-        uint32_t bc = slot_c[b][0], bd = slot_d[b][0];
+        uint32_t bc = slot_c[sl][0], bd = slot_d[sl][0];
 #pragma unroll
         for (int w = 1; w < NW; ++w) {
-            const uint32_t c = slot_c[b][w], dw = slot_d[b][w];
+            const uint32_t c = slot_c[sl][w], dw = slot_d[sl][w];
             if (c < bc || (c == bc && dw < bd)) {
                 bc = c;
                 bd = dw;
             }
         }
         if (threadIdx.x == 0) {
-            out_idx[r] = bc == 0xFFFFFFFFu ? -1 : (int32_t)bd;
-            out_score[r] = bc == 0xFFFFFFFFu ? __builtin_inff() : __uint_as_float(bc);
+            out_idx[b.r] = bc == 0xFFFFFFFFu ? -1 : (int32_t)(bd >> 2);
+            out_score[b.r] = bc == 0xFFFFFFFFu ? __builtin_inff() : __uint_as_float(bc);
         }
         if (bc != 0xFFFFFFFFu) {
-            const uint32_t tw = s.tier_map[row + bd] & 3u;
+            const uint32_t tw = bd & 3u;
             const float nw = pick4(n_tier, tw);
             if (nw < (float)cap) {
+                // at most cap times per tier: the tier's factors again, with
+                // the same expression, through LDS
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    if ((uint32_t)t == tw) n_tier[t] = nw + 1.0f;
+                for (int q = 0; q < 4; ++q)
+                    if ((uint32_t)q == tw) n_tier[q] = nw + 1.0f;
 #pragma unroll
-                for (int k = 0; k < MAXC; ++k) {
-                    const uint32_t d = threadIdx.x + T * k;
-                    if (((tmask >> (2 * k)) & 3u) == tw && d < s.D)
-                        sk[k] = sec_per_token_n(s, tw, nw + 1.0f, s.util[row + d]);
-                }
+                for (int k = 0; k < MAXC; ++k) stage[k * T + threadIdx.x] = __float_as_uint(sk[k]);
+#pragma unroll 1
+                for (int k = 0; k < MAXC; ++k)
+                    if (((tmask >> (2 * k)) & 3u) == tw)
+                        stage[k * T + threadIdx.x] =
+                            __float_as_uint(sec_per_token_n(s, tw, nw + 1.0f, urow[k * T + threadIdx.x]));
+#pragma unroll
+                for (int k = 0; k < MAXC; ++k) sk[k] = __uint_as_float(stage[k * T + threadIdx.x]);
             }
         }
     };
-    uint16_t ja[MAXC], jb[MAXC];
-    uint32_t r = order[i0];
-    load_j(r, ja);
+    fill(0);
+    fill(1);
+    __syncthreads();
+    SeqBuf<MAXC> ba, bb;
+    issue(i0, ba);
     for (uint32_t i = i0; i < i1; i += 2) {
-        const uint32_t r1 = i + 1 < i1 ? order[i + 1] : r;
-        if (i + 1 < i1) load_j(r1, jb);
-        step(i, r, ja);
+        if (i + 1 < i1) issue(i + 1, bb);
+        step(i, ba);
         if (i + 1 >= i1) break;
-        const uint32_t r2 = i + 2 < i1 ? order[i + 2] : r1;
-        if (i + 2 < i1) load_j(r2, ja);
-        step(i + 1, r1, jb);
-        r = r2;
+        if (i + 2 < i1) issue(i + 2, ba);
+        step(i + 1, bb);
     }
 }
 
@@ -2440,8 +2581,6 @@ struct netkv_ctx {
     uint32_t cols_opt = 0;      // decodes per lane (0 = automatic)
     uint32_t policy_opt = 0;    // 0 full, 1 without live congestion, 2 topology only
     // sequential-selection scratch
-    uint16_t *seq_j = nullptr;
-    uint64_t seq_j_cap = 0;
     uint32_t *seq_keys = nullptr, *seq_vals = nullptr, *seq_keys_out = nullptr, *seq_perm = nullptr;
     uint32_t *seq_start = nullptr, *seq_end = nullptr;
     uint64_t seq_cap = 0;
@@ -2601,8 +2740,6 @@ netkv_status ready(netkv_handle h) {
         return fail(h, NETKV_EINVAL, "cache has %u decodes, snapshot %u", h->cache_D, h->D);
     return NETKV_OK;
 }
-
-constexpr uint32_t kMaxBlocks16 = 0xFFFFu;   // longest run whose prefix lengths fit 16 bits
 
 // rocPRIM's radix sorts of the batch-order keys (batches outside the range
 // of the own batch sort): its tuned kernels, with the merge-sort path
@@ -3021,6 +3158,47 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
 // The handle's buffers for the batch, then the selection.
 // With want_hotr, every request's scoring record is also kept by batch
 // index in sc.hotr (grown to the batch).
+// Scoring records by batch index for n requests (ranking sweep, sequential form).
+netkv_status ensure_hotr(netkv_handle h, uint64_t n) {
+    if (n <= h->sc.hotr_cap) return NETKV_OK;
+    dfree(h->sc.hotr);
+    h->sc.hotr_cap = 0;
+    if (dalloc(h->sc.hotr, n) != hipSuccess) return fail(h, NETKV_ENOMEM, "record scratch allocation failed");
+    h->sc.hotr_cap = n;
+    return NETKV_OK;
+}
+
+// The sequential form's per-prefill ordering of R requests over P prefill
+// instances (seq), and the ranking sweep's selection under the loaded
+// snapshot (base).
+netkv_status ensure_seq(netkv_handle h, uint64_t R, uint64_t P, bool seq, bool base) {
+    if (seq && h->seq_cap < R) {
+        dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
+        h->seq_cap = 0;
+        HIPCHK(h, dalloc(h->seq_keys, R));
+        HIPCHK(h, dalloc(h->seq_vals, R));
+        HIPCHK(h, dalloc(h->seq_keys_out, R));
+        HIPCHK(h, dalloc(h->seq_perm, R));
+        h->seq_cap = R;
+    }
+    if (seq && h->seq_P != P) {
+        dfree(h->seq_start); dfree(h->seq_end);
+        h->seq_P = 0;
+        HIPCHK(h, dalloc(h->seq_start, P));
+        HIPCHK(h, dalloc(h->seq_end, P));
+        h->seq_P = (uint32_t)P;
+    }
+    if (base && h->base_n < R) {
+        dfree(h->base_idx);
+        dfree(h->base_score);
+        h->base_n = 0;
+        HIPCHK(h, dalloc(h->base_idx, R));
+        HIPCHK(h, dalloc(h->base_score, R));
+        h->base_n = R;
+    }
+    return NETKV_OK;
+}
+
 netkv_status select_owned(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
                           const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false,
                           bool want_hotr = false) {
@@ -3028,13 +3206,7 @@ netkv_status select_owned(netkv_handle h, const netkv_requests_t *req, uint32_t 
     netkv_status e = ensure_scratch(h, h->sc, req->n_req, (uint64_t)req->n_req * geo.ngroup * geo.K,
                                     req->n_hashes, st);
     if (e) return e;
-    if (want_hotr && req->n_req > h->sc.hotr_cap) {
-        dfree(h->sc.hotr);
-        h->sc.hotr_cap = 0;
-        if (dalloc(h->sc.hotr, req->n_req) != hipSuccess)
-            return fail(h, NETKV_ENOMEM, "record scratch allocation failed");
-        h->sc.hotr_cap = req->n_req;
-    }
+    if (want_hotr && (e = ensure_hotr(h, req->n_req))) return e;
     return run_select(h, h->sc, req, k, idx, score, po, pairs, max_blocks, st, route2, true,
                       want_hotr ? h->sc.hotr : nullptr);
 }
@@ -3246,7 +3418,7 @@ void netkv_destroy(netkv_handle h) {
         dfree(h->adm);
         dfree(h->bytes);
         free_scratch(h->sc);
-        dfree(h->seq_j); dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
+        dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
         dfree(h->seq_start); dfree(h->seq_end);
         for (hipEvent_t ev : h->tev) (void)hipEventDestroy(ev);
         dfree(h->rt1); dfree(h->rt2); dfree(h->ru1); dfree(h->ru2); dfree(h->sr);
@@ -3763,7 +3935,10 @@ netkv_status netkv_reserve(netkv_handle h, uint32_t max_req, uint64_t max_hashes
         const Geometry geo = geometry(h, k);
         elems = std::max<uint64_t>(elems, (uint64_t)max_req * geo.ngroup * geo.K);
     }
-    return ensure_scratch(h, h->sc, max_req, elems, max_hashes, (hipStream_t)stream);
+    netkv_status st = ensure_scratch(h, h->sc, max_req, elems, max_hashes, (hipStream_t)stream);
+    if (!st) st = ensure_hotr(h, max_req);
+    if (!st) st = ensure_seq(h, max_req, h->P, true, true);
+    return st;
 }
 
 netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint32_t n_scen, const float *util_scen,
@@ -3800,14 +3975,7 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
         HIPCHK(h, hipGetLastError());
     }
     if (R == 0) return NETKV_OK;
-    if (h->base_n < R) {
-        dfree(h->base_idx);
-        dfree(h->base_score);
-        h->base_n = 0;
-        HIPCHK(h, dalloc(h->base_idx, R));
-        HIPCHK(h, dalloc(h->base_score, R));
-        h->base_n = R;
-    }
+    if ((st = ensure_seq(h, R, P, false, true))) return st;
     const uint64_t nspt = (uint64_t)n_scen * P * D;
     if (h->spt_cap < nspt) {
         dfree(h->spt_scen);
@@ -3982,34 +4150,15 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     if (req->n_req == 0) return NETKV_OK;
     DeviceGuard g(h->device);
     hipStream_t s = (hipStream_t)stream;
-    const uint64_t R = req->n_req, D = h->D, P = h->P;
-    if (h->seq_j_cap < R * D) {
-        dfree(h->seq_j);
-        h->seq_j_cap = 0;
-        HIPCHK(h, dalloc(h->seq_j, R * D));
-        h->seq_j_cap = R * D;
-    }
-    if (h->seq_cap < R) {
-        dfree(h->seq_keys); dfree(h->seq_vals); dfree(h->seq_keys_out); dfree(h->seq_perm);
-        h->seq_cap = 0;
-        HIPCHK(h, dalloc(h->seq_keys, R));
-        HIPCHK(h, dalloc(h->seq_vals, R));
-        HIPCHK(h, dalloc(h->seq_keys_out, R));
-        HIPCHK(h, dalloc(h->seq_perm, R));
-        h->seq_cap = R;
-    }
-    if (h->seq_P != P) {
-        dfree(h->seq_start); dfree(h->seq_end);
-        h->seq_P = 0;
-        HIPCHK(h, dalloc(h->seq_start, P));
-        HIPCHK(h, dalloc(h->seq_end, P));
-        h->seq_P = (uint32_t)P;
-    }
-    // prefix lengths of every pair (and validation) by the batch scan
-    PairOut po{h->seq_j, nullptr, nullptr};
+    const uint64_t R = req->n_req, P = h->P;
+    if ((st = ensure_seq(h, R, P, true, false))) return st;
+    // validation, every request's scoring record by batch index and the
+    // leaders' prefix lengths, by the batch selection (its outputs are then
+    // overwritten by the chain; invalid requests keep -1 / NaN)
     {
         TimingOff off(h);  // only the sequential kernel is timed
-        if ((st = select_owned(h, req, 1, out_idx, out_score, po, true, kMaxBlocks16, s))) return st;
+        const PairOut po{nullptr, nullptr, nullptr};
+        if ((st = select_owned(h, req, 1, out_idx, out_score, po, false, 0xFFFFFFFFu, s, false, true))) return st;
     }
     // requests grouped by prefill instance, batch order kept inside a group
     const Reqs rq = make_reqs(req);
@@ -4029,20 +4178,29 @@ netkv_status netkv_select_sequential(netkv_handle h, const netkv_requests_t *req
     HIPCHK(h, hipGetLastError());
     HIPCHK(h, time_begin(h, s));
     const Snap sn = make_snap(h);
-    const uint16_t *jm = h->seq_j;
+    const Table t = make_table(h);
+    const Hot *hr = h->sc.hotr;
+    const float *ll = h->sc.lead_lam;
     const uint32_t *ord = h->seq_perm, *b0 = h->seq_start, *b1 = h->seq_end;
-    if (h->D <= 512u * 4)
-        hipLaunchKernelGGL((sequential_cached_kernel<512, 4>), dim3((uint32_t)P), dim3(512), 0, s, sn, cap, jm,
-                           req->len_tokens, ord, b0, b1, out_idx, out_score);
-    else if (h->D <= 512u * 6)
-        hipLaunchKernelGGL((sequential_cached_kernel<512, 6>), dim3((uint32_t)P), dim3(512), 0, s, sn, cap, jm,
-                           req->len_tokens, ord, b0, b1, out_idx, out_score);
-    else if (h->D <= 512u * 8)
-        hipLaunchKernelGGL((sequential_cached_kernel<512, 8>), dim3((uint32_t)P), dim3(512), 0, s, sn, cap, jm,
-                           req->len_tokens, ord, b0, b1, out_idx, out_score);
+    // one workgroup per prefill instance, all of them resident at once on
+    // 256 CUs up to 1,024 prefills (256 threads: four workgroups per CU
+    // within the register budget); a thread holds MAXC decodes
+#define NETKV_SEQ(TT, MC)                                                                                       \
+    hipLaunchKernelGGL((sequential_cached_kernel<TT, MC>), dim3((uint32_t)P), dim3(TT), 0, s, sn, t, rq, cap, hr, ll, \
+                       ord, b0, b1, out_idx, out_score)
+    const uint32_t Dn = h->D;
+    if (Dn <= 64) NETKV_SEQ(64, 1);
+    else if (Dn <= 256) NETKV_SEQ(256, 1);
+    else if (Dn <= 512) NETKV_SEQ(256, 2);
+    else if (Dn <= 1024) NETKV_SEQ(256, 4);
+    else if (Dn <= 1536) NETKV_SEQ(256, 6);
+    else if (Dn <= 2048) NETKV_SEQ(256, 8);
+    else if (Dn <= 3072) NETKV_SEQ(256, 12);
+    else if (Dn <= 4096) NETKV_SEQ(256, 16);
     else
-        hipLaunchKernelGGL(sequential_kernel, dim3((uint32_t)P), dim3(kSeqThreads), 0, s, sn, (uint32_t)R, cap, jm,
-                           req->len_tokens, ord, b0, b1, out_idx, out_score);
+        hipLaunchKernelGGL(sequential_kernel, dim3((uint32_t)P), dim3(kSeqThreads), 0, s, sn, t, rq, cap, hr, ll, ord,
+                           b0, b1, out_idx, out_score);
+#undef NETKV_SEQ
     HIPCHK(h, hipGetLastError());
     HIPCHK(h, time_end(h, s));
     return NETKV_OK;

@@ -166,12 +166,15 @@ def test_sequential_full_size_two_prefill_instances(nk):
     sel.close()
 
 
-@pytest.mark.parametrize("shape", [(8, 8, 8, 4), (8, 8, 8, 6), (8, 8, 10, 8), (8, 8, 12, 8)])
+@pytest.mark.parametrize("shape", [(8, 8, 4, 4), (8, 8, 8, 4), (8, 8, 8, 5), (8, 8, 8, 6), (8, 8, 10, 8),
+                                   (8, 8, 12, 8)])
 def test_sequential_pool_sizes(nk, shape):
-    """Pools of 1,536 / 2,304 / 3,840 / 4,608 decodes (each register layout
-    of the sequential kernel and the general form beyond them), with 6,000
+    """Pools of 768 / 1,536 / 1,920 / 2,304 / 3,840 / 4,608 decodes (4, 6,
+    8, 12 and 16 decodes per thread of the register-held chain, and the
+    general form beyond them), with 6,000
     requests from three prefill instances so that the counters of every
-    tier grow and saturate within the batch."""
+    tier grow and saturate within the batch; then the same batch with the
+    prefix lengths taken by each request's own scan."""
     cl = W.Cluster(*shape)
     cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=6000, cache_per_decode=512)
     _say("sequential pool", cfg.n_decode)
@@ -187,6 +190,15 @@ def test_sequential_pool_sizes(nk, shape):
     ref = oracle.select_sequential(snap, oracle.Cache(cache, n_threads=8), req, cap=16, follow=g_idx)
     near = _check_sequential(g_idx, g_sc, ref)
     assert near < 0.01 * cfg.n_requests
+    # a leader table of two rows: nearly every request is matched on its own
+    # (first-miss scan of its run) instead of from a leader row; the chain's
+    # prefix lengths, and so its selections, are the same bits
+    nk.netkv_set_option(sel.h, nk.NETKV_OPT_LEAD_CAP, 2)
+    own = sel.select_sequential(rd, cap=16)
+    sel.sync_errors()
+    nk.netkv_set_option(sel.h, nk.NETKV_OPT_LEAD_CAP, 0)
+    np.testing.assert_array_equal(nk.to_numpy(own["idx"]), g_idx)
+    np.testing.assert_array_equal(nk.to_numpy(own["score"]).view(np.uint32), g_sc.view(np.uint32))
     sel.close()
 
 

@@ -462,10 +462,11 @@ def test_requests_across_2_pow_24_tokens(nk):
 def test_long_runs_and_invalid_requests_in_every_mode(nk):
     """Runs longer than 65535 blocks (B_tok = 1): the batch selection scores
     them exactly and writes prefix lengths saturated at 65535; the ranking
-    sweep under the snapshot's own congestion reproduces the selection for
-    them; the sequential form, which keeps prefix lengths in 16 bits,
-    answers them (and a request whose run length contradicts l_r, in every
-    mode) with -1 / NaN and reports them.  A block hash 0 ends a match."""
+    sweep under the snapshot's own congestion and the sequential form with
+    no counter growth (cap 0) reproduce the selection for them, from leader
+    rows and from each request's own scan; a request whose run length
+    contradicts l_r is answered with -1 / NaN in every mode and reported.
+    A block hash 0 ends a match."""
     _say("long runs, B_tok 1")
     cfg = W.scaled(W.CONFIGS["c0"], n_requests=6, block_tokens=1)
     snap = W.make_snapshot(cfg, 21)
@@ -508,18 +509,23 @@ def test_long_runs_and_invalid_requests_in_every_mode(nk):
     sq = sel.select_sequential(rd, cap=0)
     with pytest.raises(nk.NetKVError):
         sel.sync_errors()
+    nk.netkv_set_option(sel.h, nk.NETKV_OPT_LEAD_CAP, 1)   # one leader row: the rest match on their own
+    sq1 = sel.select_sequential(rd, cap=0)
+    with pytest.raises(nk.NetKVError):
+        sel.sync_errors()
     si = nk.to_numpy(sw["idx"]).reshape(-1, 2)
     ss = nk.to_numpy(sw["score"]).reshape(-1, 2)
-    qi, qs = nk.to_numpy(sq["idx"]), nk.to_numpy(sq["score"])
-    # the sweep takes prefix lengths from leader rows: every valid request,
-    # long runs included, reproduces the selection; the invalid one is -1/NaN
+    # the sweep and the sequential form take prefix lengths from leader rows
+    # (or own scans): every valid request, long runs included, reproduces
+    # the selection; the invalid one is -1/NaN
     assert (si[3] == -1).all() and np.isnan(ss[3]).all()
     for r in (0, 1, 2, 4, 5):
         assert np.array_equal(si[r], idx[r]) and np.array_equal(ss[r].view(np.uint32), sc[r].view(np.uint32))
-    for r in (0, 1, 3, 5):   # the sequential form: more than 65535 blocks, or an invalid run length
-        assert qi[r] == -1 and np.isnan(qs[r])
-    for r in (2, 4):
-        assert qi[r] == idx[r, 0] and qs[r] == sc[r, 0]
+    for q in (sq, sq1):
+        qi, qs = nk.to_numpy(q["idx"]), nk.to_numpy(q["score"])
+        assert qi[3] == -1 and np.isnan(qs[3])
+        for r in (0, 1, 2, 4, 5):
+            assert qi[r] == idx[r, 0] and qs[r].view(np.uint32) == sc[r, 0].view(np.uint32)
     sel.close()
 
 
