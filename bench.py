@@ -70,11 +70,11 @@ def kernel_source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def counter_summary(workload: str, digest: str):
+def counter_summary(workload: str, digest: str, kernel: str = "score_kernel"):
     """Per-launch rocprofv3 counter figures of the scoring kernel (HBM bytes,
     instruction counts) from the committed summary, if they were taken on
     this exact kernel source; else an empty dict."""
-    path = os.path.join(ROOT, "profiles", f"score_kernel_{workload}_counters.json")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.json")
     if not os.path.exists(path):
         return {}
     with open(path) as f:
@@ -532,6 +532,14 @@ def bench_sweep(args, cfg, dev):
         cpu = dict(value=ns * R * D / dt, unit="pairs/s", cores=threads, kind="oracle", cpu_model=cpu_model(),
                    sample=f"{ns} scenarios x {R} requests x {D} decodes (prefix match once, "
                           f"then rescoring), {dt:.1f} s")
+    cs = counter_summary(args.workload, kernel_source_digest(), "sweep_kernel")
+    traffic = cs.get("hbm_bytes_per_launch")
+    issue = None
+    if "valu_insts_per_launch" in cs:
+        issue = {"valu_frac": cs["valu_insts_per_launch"] / (kern_ms * 1e-3 * ISSUE_PEAK_PER_S),
+                 "salu_frac": cs["salu_insts_per_launch"] / (kern_ms * 1e-3 * ISSUE_PEAK_PER_S),
+                 "model": "one VALU and one SALU wave64 instruction issued per CU per cycle "
+                          "(256 CUs x 2.4 GHz); counters from the committed profile of this source"}
     rec = {
         "metric": "scored (request,decode) pairs/sec + selections/sec; achieved HBM GB/s vs peak",
         "value": pairs / (step_ms * 1e-3), "unit": "pairs/s",
@@ -544,7 +552,9 @@ def bench_sweep(args, cfg, dev):
                    "scenarios": S, "sigmas": list(cfg.noise_sigmas), "k": k,
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK_TOPS, "unit": "TOP/s",
-                     "frac": achieved / ALU_PEAK_TOPS, "traffic": None,
+                     "frac": achieved / ALU_PEAK_TOPS,
+                     "traffic": (traffic / (kern_ms * 1e-3) / 1e9) if traffic else None,
+                     "traffic_unit": "GB/s", "traffic_bytes_per_launch": traffic, "issue": issue,
                      "algorithmic_ops_per_launch": ops, "ops_per_pair": SWEEP_OPS_PER_PAIR,
                      "step_frac": ops / (step_ms * 1e-3) / 1e12 / ALU_PEAK_TOPS,
                      "kernel": "sweep_kernel<3, 48, LDS, full>",
