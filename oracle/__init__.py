@@ -60,6 +60,11 @@ class _Snap(C.Structure):
     ]
 
 
+class _Flows(C.Structure):
+    _fields_ = [("n_links", C.c_uint32), ("cap", C.c_void_p), ("n_flows", C.c_uint32),
+                ("path_off", C.c_void_p), ("path", C.c_void_p), ("bytes", C.c_void_p), ("start", C.c_void_p)]
+
+
 class _Req(C.Structure):
     _fields_ = [("n_req", C.c_uint32), ("prefill", C.c_void_p), ("len_tokens", C.c_void_p),
                 ("hash_off", C.c_void_p), ("hashes", C.c_void_p)]
@@ -96,6 +101,10 @@ def _load():
         lib.orc_smooth.restype = C.c_uint64
         lib.orc_smooth.argtypes = [C.c_void_p, C.c_void_p, C.c_uint64, C.c_double]
         lib.orc_max_threads.restype = C.c_int
+        lib.orc_maxmin.restype = C.c_uint32
+        lib.orc_maxmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
+        lib.orc_flow_sim.restype = C.c_uint64
+        lib.orc_flow_sim.argtypes = [C.c_void_p, C.c_void_p]
         _lib = lib
     return _lib
 
@@ -310,3 +319,44 @@ def route_of(snap, cache, req, idx: np.ndarray, k: int) -> np.ndarray:
     out = np.empty(idx.size, dtype=np.int8)
     lib.orc_route_of(C.byref(s.s), cc.h, C.byref(q.r), int(k), idx.ctypes.data, out.ctypes.data)
     return out
+
+
+class Flows:
+    """A flow set for the transfer simulation: link capacities cap [L]
+    (bytes/s), per flow a path (CSR path_off [N+1], path: link ids), bytes
+    [N] and start [N] (s)."""
+
+    def __init__(self, f):
+        self.keep = dict(cap=_arr(f["cap"], np.float64), path_off=_arr(f["path_off"], np.uint64),
+                         path=_arr(f["path"], np.uint32), bytes=_arr(f["bytes"], np.float64),
+                         start=_arr(f["start"], np.float64))
+        k = self.keep
+        self.n = len(k["bytes"])
+        assert len(k["path_off"]) == self.n + 1 and len(k["start"]) == self.n
+        assert (k["cap"] > 0).all() and (np.diff(k["path_off"].astype(np.int64)) > 0).all()
+        if len(k["path"]):
+            assert int(k["path"].max()) < len(k["cap"])
+        self.s = _Flows(len(k["cap"]), k["cap"].ctypes.data, self.n, k["path_off"].ctypes.data,
+                        k["path"].ctypes.data if len(k["path"]) else None, k["bytes"].ctypes.data,
+                        k["start"].ctypes.data)
+
+
+def maxmin(flows, active=None):
+    """Max-min fair rates (progressive filling) of the active flows
+    (default: all).  Returns (rates [N] float64, filling rounds)."""
+    lib = _load()
+    fl = flows if isinstance(flows, Flows) else Flows(flows)
+    act = np.ones(fl.n, np.uint8) if active is None else _arr(np.asarray(active, np.uint8), np.uint8)
+    rate = np.empty(fl.n, np.float64)
+    rounds = lib.orc_maxmin(C.byref(fl.s), act.ctypes.data, rate.ctypes.data)
+    return rate, int(rounds)
+
+
+def flow_sim(flows):
+    """Event-driven transfer simulation under max-min fair link sharing.
+    Returns (finish times [N] float64, number of allocations computed)."""
+    lib = _load()
+    fl = flows if isinstance(flows, Flows) else Flows(flows)
+    fin = np.empty(fl.n, np.float64)
+    ev = lib.orc_flow_sim(C.byref(fl.s), fin.ctypes.data)
+    return fin, int(ev)

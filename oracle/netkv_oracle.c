@@ -552,3 +552,161 @@ int orc_max_threads(void) {
     return 1;
 #endif
 }
+
+/* ------------------------------------------------------------------------
+ * Flow-level transfer simulation (Sec. VI-B, the evaluation simulator's
+ * network model): KV transfers are flows over the links of their path; the
+ * links are shared max-min fairly among the flows crossing them, and every
+ * flow arrival or completion re-evaluates the allocation of all flows in
+ * progress.  Background traffic is a steady utilisation already taken out
+ * of each link's capacity by the caller (the mean-field model).  The paper
+ * gives no algorithm; the allocation is the max-min fair one, computed by
+ * progressive filling (Bertsekas & Gallager, "Data Networks", Sec. 6.5.2):
+ * all unfrozen flows' rates rise together until some link is full; the
+ * flows crossing a full link are frozen at that rate; repeat.  fp64, with
+ * every operation written out in order (no contraction: the file is built
+ * without FMA), so that a second implementation doing the same operations
+ * gets the same bits.
+ * ------------------------------------------------------------------------ */
+
+typedef struct {
+    uint32_t n_links;
+    const double *cap;          /* [n_links] bytes/s available to the flows, > 0 */
+    uint32_t n_flows;
+    const uint64_t *path_off;   /* [n_flows + 1] */
+    const uint32_t *path;       /* links of each flow (distinct within a flow, at least one) */
+    const double *bytes;        /* [n_flows] bytes to move, >= 0 */
+    const double *start;        /* [n_flows] arrival time, s */
+} orc_flows;
+
+/* Max-min fair rates of the flows with active[f] != 0 (others get 0).
+ * Returns the number of filling rounds. */
+uint32_t orc_maxmin(const orc_flows *F, const uint8_t *active, double *rate) {
+    const uint32_t L = F->n_links, N = F->n_flows;
+    double *rem = (double *)malloc(sizeof(double) * (L ? L : 1));
+    uint32_t *cnt = (uint32_t *)calloc(L ? L : 1, sizeof(uint32_t));
+    uint8_t *sat = (uint8_t *)malloc(L ? L : 1);
+    uint8_t *frozen = (uint8_t *)calloc(N ? N : 1, 1);
+    uint32_t unfrozen = 0, rounds = 0;
+    for (uint32_t l = 0; l < L; ++l) rem[l] = F->cap[l];
+    for (uint32_t f = 0; f < N; ++f) {
+        rate[f] = 0.0;
+        if (!active[f]) continue;
+        ++unfrozen;
+        for (uint64_t q = F->path_off[f]; q < F->path_off[f + 1]; ++q) cnt[F->path[q]] += 1;
+    }
+    double level = 0.0;
+    while (unfrozen > 0) {
+        /* the largest equal raise every link still allows */
+        double inc = INFINITY;
+        for (uint32_t l = 0; l < L; ++l)
+            if (cnt[l] > 0) {
+                const double share = rem[l] / (double)cnt[l];
+                if (share < inc) inc = share;
+            }
+        /* links that the raise fills, and the capacity left on each */
+        for (uint32_t l = 0; l < L; ++l) {
+            sat[l] = 0;
+            if (cnt[l] > 0) {
+                sat[l] = rem[l] / (double)cnt[l] == inc;
+                const double used = inc * (double)cnt[l];
+                const double left = rem[l] - used;
+                rem[l] = left > 0.0 ? left : 0.0;
+            }
+        }
+        level = level + inc;
+        /* flows crossing a filled link stop at the current level */
+        for (uint32_t f = 0; f < N; ++f) {
+            if (!active[f] || frozen[f]) continue;
+            int hit = 0;
+            for (uint64_t q = F->path_off[f]; q < F->path_off[f + 1]; ++q) hit |= sat[F->path[q]];
+            if (hit) {
+                frozen[f] = 2;   /* frozen this round */
+                rate[f] = level;
+                --unfrozen;
+            }
+        }
+        for (uint32_t f = 0; f < N; ++f)
+            if (frozen[f] == 2) {
+                frozen[f] = 1;
+                for (uint64_t q = F->path_off[f]; q < F->path_off[f + 1]; ++q) cnt[F->path[q]] -= 1;
+            }
+        ++rounds;
+    }
+    free(rem);
+    free(cnt);
+    free(sat);
+    free(frozen);
+    return rounds;
+}
+
+/* Event-driven simulation: flows start at their arrival time; between
+ * events every flow in progress moves at its max-min fair rate; the next
+ * event is the earliest completion (remaining / rate) or the next arrival.
+ * finish[f] = the completion time of flow f.  Returns the number of
+ * events (allocations computed). */
+uint64_t orc_flow_sim(const orc_flows *F, double *finish) {
+    const uint32_t N = F->n_flows;
+    uint8_t *state = (uint8_t *)calloc(N ? N : 1, 1);   /* 0 waiting, 1 in progress, 2 done */
+    uint8_t *active = (uint8_t *)calloc(N ? N : 1, 1);
+    double *remaining = (double *)malloc(sizeof(double) * (N ? N : 1));
+    double *rate = (double *)malloc(sizeof(double) * (N ? N : 1));
+    uint64_t events = 0;
+    uint32_t left = N;
+    for (uint32_t f = 0; f < N; ++f) remaining[f] = F->bytes[f];
+    double t = INFINITY;
+    for (uint32_t f = 0; f < N; ++f)
+        if (F->start[f] < t) t = F->start[f];
+    while (left > 0) {
+        uint32_t n_act = 0;
+        for (uint32_t f = 0; f < N; ++f) {
+            if (state[f] == 0 && F->start[f] <= t) state[f] = 1;
+            active[f] = state[f] == 1;
+            n_act += active[f];
+        }
+        double next = INFINITY;   /* the next arrival */
+        for (uint32_t f = 0; f < N; ++f)
+            if (state[f] == 0 && F->start[f] < next) next = F->start[f];
+        if (n_act == 0) {
+            t = next;
+            continue;
+        }
+        orc_maxmin(F, active, rate);
+        ++events;
+        double dtc = INFINITY;    /* the earliest completion from t */
+        for (uint32_t f = 0; f < N; ++f)
+            if (active[f]) {
+                const double tf = remaining[f] / rate[f];
+                if (tf < dtc) dtc = tf;
+            }
+        if (dtc <= next - t) {
+            for (uint32_t f = 0; f < N; ++f) {
+                if (!active[f]) continue;
+                if (remaining[f] / rate[f] == dtc) {
+                    state[f] = 2;
+                    finish[f] = t + dtc;
+                    --left;
+                } else {
+                    const double moved = rate[f] * dtc;
+                    const double r = remaining[f] - moved;
+                    remaining[f] = r > 0.0 ? r : 0.0;
+                }
+            }
+            t = t + dtc;
+        } else {
+            const double dt = next - t;
+            for (uint32_t f = 0; f < N; ++f) {
+                if (!active[f]) continue;
+                const double moved = rate[f] * dt;
+                const double r = remaining[f] - moved;
+                remaining[f] = r > 0.0 ? r : 0.0;
+            }
+            t = next;
+        }
+    }
+    free(state);
+    free(active);
+    free(remaining);
+    free(rate);
+    return events;
+}

@@ -868,3 +868,127 @@ def test_two_hop_leaves_sweep_and_sequential_direct():
     s2 = oracle.select_sequential(snap2, oracle.Cache(cache), rq, cap=4)
     for key in s1:
         np.testing.assert_array_equal(s1[key], s2[key])
+
+
+# ---------------------------------------------------------------- flow-level transfer simulation (Sec. VI-B)
+
+def _flows(cap, paths, nbytes, start):
+    off = np.zeros(len(paths) + 1, np.uint64)
+    off[1:] = np.cumsum([len(p) for p in paths])
+    return dict(cap=np.asarray(cap, np.float64), path_off=off,
+                path=np.asarray([l for p in paths for l in p], np.uint32),
+                bytes=np.asarray(nbytes, np.float64), start=np.asarray(start, np.float64))
+
+
+def test_flowsim_single_flow_moves_at_its_bottleneck():
+    """Sec. VI-B's first validation: one flow on an uncontested path runs at
+    the bandwidth of its slowest link (here a 25 GB/s link between two of
+    50 GB/s; 10 GB arriving at t = 1 s)."""
+    f = _flows([50e9, 25e9, 50e9, 900e9], [[0, 1, 2]], [10e9], [1.0])
+    rate, rounds = oracle.maxmin(f)
+    assert rate[0] == 25e9 and rounds == 1
+    fin, ev = oracle.flow_sim(f)
+    assert fin[0] == 1.0 + 10e9 / 25e9 and ev == 1
+
+
+def test_flowsim_n_flows_share_a_bottleneck_equally():
+    """Sec. VI-B's second validation: N flows through one bottleneck each get
+    1/N of it (private access links are faster); equal flows starting
+    together finish together at N * bytes / capacity."""
+    for n in (1, 2, 5, 16):
+        cap = [10.0] + [100.0] * n
+        f = _flows(cap, [[0, 1 + i] for i in range(n)], [4.0] * n, [0.0] * n)
+        rate, _ = oracle.maxmin(f)
+        assert np.all(rate == 10.0 / n)
+        fin, ev = oracle.flow_sim(f)
+        np.testing.assert_allclose(fin, n * 4.0 / 10.0, rtol=1e-15)
+        assert ev == 1
+
+
+def test_flowsim_reallocation_after_completion_and_arrival():
+    """Sec. VI-B's third validation: when a flow completes (or arrives) the
+    others' shares are re-evaluated at once.  On one link of capacity C,
+    flows sharing it form a processor-sharing queue: with sizes b1 <= ... <=
+    bN starting together, flow k finishes at (b1 + ... + bk + (N - k) bk) / C.
+    A late arrival: flow a (2 bytes) alone at rate 2 until t = 0.5, then
+    both at 1 until a finishes at 1.5, then b alone at 2 until 2.0."""
+    b = np.array([1.0, 2.0, 2.0, 5.0, 9.0])
+    n = len(b)
+    f = _flows([3.0] + [50.0] * n, [[0, 1 + i] for i in range(n)], b, np.zeros(n))
+    fin, ev = oracle.flow_sim(f)
+    want = np.array([(b[:k + 1].sum() + (n - k - 1) * b[k]) / 3.0 for k in range(n)])
+    np.testing.assert_allclose(fin, want, rtol=1e-14)
+    assert ev == 4   # the two flows of 2 bytes finish at the same event
+    f = _flows([2.0, 10.0, 10.0], [[0, 1], [0, 2]], [2.0, 2.0], [0.0, 0.5])
+    fin, ev = oracle.flow_sim(f)
+    np.testing.assert_allclose(fin, [1.5, 2.0], rtol=1e-15)
+    assert ev == 3
+
+
+def test_maxmin_parking_lot():
+    """The textbook case: flow 0 crosses links 0 (capacity 1) and 1
+    (capacity 2), flow 1 only link 0, flow 2 only link 1.  Link 0 fills
+    first at 1/2 each; flow 2 then takes the rest of link 1: 3/2."""
+    f = _flows([1.0, 2.0], [[0, 1], [0], [1]], [1.0] * 3, [0.0] * 3)
+    rate, rounds = oracle.maxmin(f)
+    assert rate.tolist() == [0.5, 0.5, 1.5] and rounds == 2
+    fin, _ = oracle.flow_sim(f)
+    # flow 2 ends at 2/3; flows 0 and 1 then share link 0 until 2
+    np.testing.assert_allclose(fin, [2.0, 2.0, 2.0 / 3.0], rtol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_maxmin_allocation_has_a_bottleneck_for_every_flow(seed):
+    """Max-min fairness by its characterisation (Bertsekas & Gallager,
+    Prop. 6.5.1): a feasible allocation is max-min fair iff every flow
+    crosses a saturated link on which no other flow has a larger rate.
+    Checked directly on random paths and capacities, with a random subset
+    of flows active."""
+    rng = np.random.default_rng(seed)
+    L, N = int(rng.integers(3, 12)), int(rng.integers(1, 30))
+    cap = rng.uniform(1.0, 10.0, L)
+    paths = [sorted(rng.choice(L, int(rng.integers(1, min(L, 4) + 1)), replace=False).tolist()) for _ in range(N)]
+    active = (rng.uniform(size=N) < 0.8).astype(np.uint8)
+    f = _flows(cap, paths, np.ones(N), np.zeros(N))
+    rate, _ = oracle.maxmin(f, active)
+    assert (rate[active == 0] == 0).all()
+    load = np.zeros(L)
+    for i, p in enumerate(paths):
+        load[p] += rate[i]
+    assert (load <= cap * (1 + 1e-12)).all()
+    for i, p in enumerate(paths):
+        if not active[i]:
+            continue
+        ok = False
+        for l in p:
+            others = [rate[j] for j, q in enumerate(paths) if l in q and active[j]]
+            if load[l] >= cap[l] * (1 - 1e-12) and rate[i] >= max(others) * (1 - 1e-12):
+                ok = True
+        assert ok, f"flow {i} has no bottleneck link"
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_flowsim_never_beats_the_path_alone_and_matches_it_without_sharing(seed):
+    """A flow can never finish earlier than alone on its path; flows whose
+    paths share no link with any other finish exactly as alone; and the
+    link carrying every flow (a common bottleneck) is never idle while
+    flows are in progress, so with all flows starting together the last
+    one finishes at sum(bytes) / capacity."""
+    rng = np.random.default_rng(100 + seed)
+    N = 20
+    L = 2 * N + 1
+    cap = rng.uniform(1.0, 10.0, L)
+    nbytes = rng.uniform(0.5, 5.0, N)
+    start = rng.uniform(0.0, 2.0, N)
+    # disjoint paths: flow i on links 2i, 2i+1
+    f = _flows(cap, [[2 * i, 2 * i + 1] for i in range(N)], nbytes, start)
+    fin, _ = oracle.flow_sim(f)
+    alone = start + nbytes / np.minimum(cap[0:2 * N:2], cap[1:2 * N:2])
+    np.testing.assert_allclose(fin, alone, rtol=1e-14)
+    # one common link (index L-1), slower than every private link
+    cap2 = cap.copy()
+    cap2[-1] = 0.5
+    f = _flows(cap2, [[2 * i, L - 1] for i in range(N)], nbytes, np.zeros(N))
+    fin, _ = oracle.flow_sim(f)
+    assert (fin >= nbytes / np.minimum(cap2[0:2 * N:2], 0.5) * (1 - 1e-14)).all()
+    np.testing.assert_allclose(fin.max(), nbytes.sum() / 0.5, rtol=1e-12)

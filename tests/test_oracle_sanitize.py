@@ -58,6 +58,16 @@ r2 = oracle.select(rs, c, req, k=2, n_threads=2)
 out["route_of"] = dig(r2["idx"], oracle.route_of(rs, c, req, r2["idx"], 2))
 off = np.asarray(req["hash_off"], np.int64)
 out["prefix_len"] = [c.prefix_len(d, req["hashes"][off[0]:off[1]]) for d in range(4)]
+rng = np.random.default_rng(9)
+L, N = 40, 200
+plen = rng.integers(1, 5, N)
+poff = np.concatenate([[0], np.cumsum(plen)]).astype(np.uint64)
+path = np.concatenate([rng.choice(L, k, replace=False) for k in plen]).astype(np.uint32)
+fl = dict(cap=rng.uniform(1.0, 9.0, L), path_off=poff, path=path, bytes=rng.uniform(0.0, 4.0, N),
+          start=rng.uniform(0.0, 1.0, N))
+rt, nr = oracle.maxmin(fl)
+fin, ev = oracle.flow_sim(fl)
+out["flows"] = dig(rt, fin) + str(nr) + str(ev)
 import os
 if os.environ.get("NETKV_ORACLE_LIB"):   # the checking build and the ASan runtime are the ones mapped
     maps = open("/proc/self/maps").read()
