@@ -772,6 +772,7 @@ constexpr uint32_t kSortBinsPer = kSortMaxBins / kBlock;   // digits per thread 
 constexpr uint32_t kPrefillMaxBits = 16;   // prefill keys of more bits: rocPRIM's sort and a gather
 constexpr uint64_t kSortMaxN = 1ull << 24;
 constexpr uint64_t kSortMinN = 1ull << 16;   // smaller batches: rocPRIM (fewer launches)
+constexpr uint64_t kForkMinN = 1ull << 16;   // batches from which a selection forks its second stream
 static_assert(kSortBinsPer * kBlock == kSortMaxBins, "digits split evenly over the threads");
 
 __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__restrict__ keys, uint32_t n,
@@ -2549,6 +2550,12 @@ struct netkv_ctx {
     uint64_t *dxlim = nullptr;   // [D]
     float bw[4] = {0, 0, 0, 0}, lat[4] = {0, 0, 0, 0};
     double bw64[4] = {0, 0, 0, 0};   // the snapshot's bandwidths as given (Proposition 2's counts)
+    // a second stream (default priority, non-blocking) on which a large
+    // selection runs the derivation and the leader kernels beside the
+    // ordering kernels, forked from and joined to the caller's stream by
+    // events (so a caller's graph capture takes both branches)
+    hipStream_t side = nullptr;
+    hipEvent_t ev_fork0 = nullptr, ev_fork1 = nullptr, ev_join = nullptr;
     float t_a = 0, t_b = 0, alpha = 0;
     uint32_t beta_max = 0, bpt = 0, block_tokens = 1;
     uint64_t m_min = 0;
@@ -2968,7 +2975,7 @@ inline uint32_t cols_per_lane(uint32_t D, uint32_t opt) {
     return D >= 4u * kWave ? 2u : 1u;
 }
 
-// Leader kernel, then the scoring kernel.  A pool of one group of one
+// The scoring kernel.  A pool of one group of one
 // decode per lane (up to 64 decodes) is scored in merged mode: one
 // wavefront per run, writing its requests' outputs itself.  Otherwise one
 // workgroup per
@@ -2979,14 +2986,8 @@ template <int K, int C>
 hipError_t launch_score(netkv_handle h, Scratch &sc, const Snap &sn, const Table &t, const Reqs &rq,
                         const Order &ord, uint32_t run_len, uint32_t n_runs, uint32_t ngroup, const PairOut &po,
                         bool pairs, uint32_t k, int32_t *idx, float *score, hipStream_t st) {
-    // leaders: 64 decodes per wavefront, 64 blocks per step
-    const uint32_t lgroup = (sn.D + kWave - 1) / kWave;
-    const uint64_t lw = std::min<uint64_t>((uint64_t)ord.lead_cap * lgroup, 65536);
-    hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
-                       dim3(kBlock), 0, st, t, sn.D, sn.block_tokens, (const Lead *)sc.lead,
-                       (const unsigned int *)sc.n_lead, ord.lead_cap, ord.hv, rq.hashes, lgroup, sc.lead_lam);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || (e = time_begin(h, st)) != hipSuccess) return e;
+    hipError_t e = time_begin(h, st);
+    if (e != hipSuccess) return e;
     constexpr bool kMergeable = C == 1;
     const bool merge = kMergeable && ngroup == 1;
     const uint64_t grid64 = merge ? (uint64_t)(n_runs + kXcds - 1) / kXcds * kXcds
@@ -3028,8 +3029,8 @@ hipError_t launch_score(netkv_handle h, Scratch &sc, const Snap &sn, const Table
     return hipGetLastError();
 }
 
-// Leader kernel, the scoring kernel (bracketed by the handle's timing events
-// when enabled), then, outside merged mode, the merge.
+// The scoring kernel (bracketed by the handle's timing events when
+// enabled), then, outside merged mode, the merge.
 template <int K>
 hipError_t launch_score_reduce(netkv_handle h, Scratch &sc, const Snap &sn, const Table &t, const Reqs &rq,
                                const Order &ord, uint32_t run_len, uint32_t n_runs, uint32_t ngroup, uint32_t C,
@@ -3078,13 +3079,23 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
         HIPCHK(h, hipGetLastError());
         sc.zero_row_set = true;
     }
+    // a large batch forks a second stream: the derivation (independent of
+    // the ordering), then after the order kernel the leaders' holder values
+    // and prefix lengths, beside the tile prefixes and the prefill order;
+    // joined before the scoring kernel
+    const bool fork = R >= kForkMinN;
+    hipStream_t s2 = fork ? h->side : st;
+    if (fork) {
+        HIPCHK(h, hipEventRecord(h->ev_fork0, st));
+        HIPCHK(h, hipStreamWaitEvent(s2, h->ev_fork0, 0));
+    }
     const uint64_t nd = std::max<uint64_t>((uint64_t)h->P * h->D, h->D);
     if (derive)
-        hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn, h->sl, h->dbase,
+        hipLaunchKernelGGL(derive_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, s2, sn, h->sl, h->dbase,
                            h->dxlim);
     if (route2 && h->have_route) {
         if (derive)
-            hipLaunchKernelGGL(derive_route_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, st, sn,
+            hipLaunchKernelGGL(derive_route_kernel, dim3((uint32_t)((nd + 255) / 256)), dim3(256), 0, s2, sn,
                                (const uint8_t *)h->rt1, (const float *)h->ru1, (const uint8_t *)h->rt2,
                                (const float *)h->ru2, h->sr);
         sn.sr = h->sr;
@@ -3112,9 +3123,24 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
                        (const uint32_t *)sc.keys_out, t, h->reuse_opt, sc.seg, sc.tpre, sc.pkey,
                        own_prefill ? nullptr : sc.pval, sc.hrec, sc.crec, sc.lead, lcap, sc.n_lead, hvcap,
                        sc.hv_used, sc.n_valid);
+    HIPCHK(h, hipGetLastError());
+    if (fork) {
+        HIPCHK(h, hipEventRecord(h->ev_fork1, st));
+        HIPCHK(h, hipStreamWaitEvent(s2, h->ev_fork1, 0));
+    }
     hipLaunchKernelGGL(lead_holder_kernel, dim3((uint32_t)std::min<uint64_t>((lcap + kWavesPerBlock - 1) /
                                                                              kWavesPerBlock, 4096)),
-                       dim3(kBlock), 0, st, t, rq.hashes, sc.lead, (const unsigned int *)sc.n_lead, lcap, sc.hv);
+                       dim3(kBlock), 0, s2, t, rq.hashes, sc.lead, (const unsigned int *)sc.n_lead, lcap, sc.hv);
+    {
+        // leaders' prefix lengths: 64 decodes per wavefront, 64 blocks per step
+        const uint32_t lgroup = (h->D + kWave - 1) / kWave;
+        const uint64_t lw = std::min<uint64_t>((uint64_t)lcap * lgroup, 65536);
+        hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
+                           dim3(kBlock), 0, s2, t, h->D, h->block_tokens, (const Lead *)sc.lead,
+                           (const unsigned int *)sc.n_lead, lcap, (const uint32_t *)sc.hv, rq.hashes, lgroup,
+                           sc.lead_lam);
+    }
+    HIPCHK(h, hipGetLastError());
     // the exclusive prefixes of the order tiles' totals (the second level of
     // the segmented scan; the first is in order_kernel)
     hipLaunchKernelGGL(tile_prefix_kernel, dim3(1), dim3(kPrefixThreads), 0, st, sc.tpre,
@@ -3137,6 +3163,10 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
                            (const Cold *)sc.crec, sc.hot, sc.cold, hotr);
         HIPCHK(h, hipGetLastError());
     }
+    if (fork) {
+        HIPCHK(h, hipEventRecord(h->ev_join, s2));
+        HIPCHK(h, hipStreamWaitEvent(st, h->ev_join, 0));
+    }
     const uint32_t run_len = h->run_len_opt ? h->run_len_opt : auto_run_len(R, ngroup);
     const uint32_t n_runs = (uint32_t)((R + run_len - 1) / run_len);
     Order ord{sc.hot, sc.cold, sc.lead_lam, sc.hv, sc.n_valid, lcap};
@@ -3155,9 +3185,6 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
     return NETKV_OK;
 }
 
-// The handle's buffers for the batch, then the selection.
-// With want_hotr, every request's scoring record is also kept by batch
-// index in sc.hotr (grown to the batch).
 // Scoring records by batch index for n requests (ranking sweep, sequential form).
 netkv_status ensure_hotr(netkv_handle h, uint64_t n) {
     if (n <= h->sc.hotr_cap) return NETKV_OK;
@@ -3199,6 +3226,9 @@ netkv_status ensure_seq(netkv_handle h, uint64_t R, uint64_t P, bool seq, bool b
     return NETKV_OK;
 }
 
+// The handle's buffers for the batch, then the selection.
+// With want_hotr, every request's scoring record is also kept by batch
+// index in sc.hotr (grown to the batch).
 netkv_status select_owned(netkv_handle h, const netkv_requests_t *req, uint32_t k, int32_t *idx, float *score,
                           const PairOut &po, bool pairs, uint32_t max_blocks, hipStream_t st, bool route2 = false,
                           bool want_hotr = false) {
@@ -3382,7 +3412,10 @@ netkv_status netkv_create(netkv_handle *out, int device) {
     h->device = device;
     DeviceGuard g(device);
     if (resolve_scratch(device) != hipSuccess || dalloc(h->errword, 1) != hipSuccess ||
-        dalloc(h->loadword, 1) != hipSuccess ||
+        dalloc(h->loadword, 1) != hipSuccess || hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&h->ev_fork0, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&h->ev_fork1, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming) != hipSuccess ||
         hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess) {
         netkv_destroy(h);
         return NETKV_EDEVICE;
@@ -3396,6 +3429,10 @@ void netkv_destroy(netkv_handle h) {
     {
         DeviceGuard g(h->device);
         (void)hipDeviceSynchronize();
+        if (h->side) (void)hipStreamDestroy(h->side);
+        if (h->ev_fork0) (void)hipEventDestroy(h->ev_fork0);
+        if (h->ev_fork1) (void)hipEventDestroy(h->ev_fork1);
+        if (h->ev_join) (void)hipEventDestroy(h->ev_join);
         dfree(h->tier_map);
         dfree(h->util);
         dfree(h->n_inflight);
