@@ -386,6 +386,47 @@ netkv_status netkv_set_option(netkv_handle h, int option, uint32_t value);
 netkv_status netkv_cache_info(netkv_handle h, uint64_t *index_slots, uint64_t *distinct_hashes,
                               uint64_t *shared_hashes, uint64_t *index_bytes);
 
+/* Non-cached bytes of each selection (Eq. (2), s_eff = bpt * (l_r -
+ * B_tok * j) with j the selected pair's block prefix length, Sec. III-B):
+ * for idx[r*k + q] (DEVICE, as written by netkv_select_batch) out_bytes
+ * (DEVICE u64[n_req * k]) gets the bytes the transfer moves, 0 for no
+ * selection or an invalid request.  The sizes of the KV transfers that
+ * netkv_flow_sim takes.  Asynchronous; an index >= D is reported by
+ * netkv_sync_errors.  ENOTREADY: no snapshot or cache; EINVAL: k outside
+ * [1, 8], NULL arrays. */
+netkv_status netkv_selection_bytes(netkv_handle h, const netkv_requests_t *req, uint32_t k,
+                                   const int32_t *idx, uint64_t *out_bytes, void *stream);
+
+/* Flow-level transfer simulation (Sec. VI-B, the evaluation simulator's
+ * network model): KV transfers are flows over the links of their paths;
+ * each link is shared max-min fairly among the flows crossing it, and every
+ * flow arrival or completion re-evaluates the allocation of all flows in
+ * progress.  Background traffic is a steady utilisation the caller takes
+ * out of each link's capacity (the section's mean-field model).  The
+ * allocation is computed by progressive filling: all unfrozen flows' rates
+ * rise together until a link is full, and the flows crossing it stop
+ * there.  fp64 throughout; results are bit-identical to a sequential
+ * implementation of the same operations.
+ *
+ * n_inst independent instances, one workgroup each: instance i holds flows
+ * flow_off[i] .. flow_off[i+1]-1 (n_flows = flow_off[n_inst] in all) on
+ * links 0 .. n_links-1 with capacities cap[i * n_links + l] (bytes/s,
+ * finite and > 0).  Flow f crosses the links path[path_off[f] ..
+ * path_off[f+1]) (at least one, each < n_links, distinct within the flow;
+ * n_path = path_off[n_flows]), moves bytes[f] >= 0 bytes and arrives at
+ * start[f] (s, finite).  Writes finish[f], its completion time (s), and,
+ * if stats is not NULL, stats[3i .. 3i+2] = the instance's allocations
+ * computed (one per event), filling rounds over all of them, and flows in
+ * progress summed over all of them.  All arrays DEVICE.  Asynchronous.  An instance with an invalid flow or capacity
+ * gets finish = NaN for all its flows and is reported by netkv_sync_errors
+ * (as is one that reached an iteration bound, which valid input never
+ * does).  Grows a work buffer of the handle to 13 B per link and instance
+ * plus 18 B per flow, rounded up.  EINVAL: NULL arrays, n_links = 0. */
+netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t n_links, const double *cap,
+                            const uint64_t *flow_off, uint64_t n_flows, const uint64_t *path_off,
+                            const uint32_t *path, uint64_t n_path, const double *bytes, const double *start,
+                            double *finish, uint64_t *stats, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -101,10 +101,12 @@ def _load():
         lib.orc_smooth.restype = C.c_uint64
         lib.orc_smooth.argtypes = [C.c_void_p, C.c_void_p, C.c_uint64, C.c_double]
         lib.orc_max_threads.restype = C.c_int
+        lib.orc_selection_bytes.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32, C.c_void_p,
+                                            C.c_void_p]
         lib.orc_maxmin.restype = C.c_uint32
         lib.orc_maxmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
         lib.orc_flow_sim.restype = C.c_uint64
-        lib.orc_flow_sim.argtypes = [C.c_void_p, C.c_void_p]
+        lib.orc_flow_sim.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
         _lib = lib
     return _lib
 
@@ -321,6 +323,18 @@ def route_of(snap, cache, req, idx: np.ndarray, k: int) -> np.ndarray:
     return out
 
 
+def selection_bytes(snap, cache, req, idx: np.ndarray, k: int) -> np.ndarray:
+    """Eq. (2)'s non-cached bytes of each selection idx [R*k] (0 for none)."""
+    lib = _load()
+    s = snap if isinstance(snap, Snapshot) else Snapshot(snap)
+    q = req if isinstance(req, Requests) else Requests(req)
+    cc = cache if isinstance(cache, Cache) else Cache(cache)
+    idx = _arr(np.asarray(idx).reshape(-1), np.int32)
+    out = np.empty(idx.size, dtype=np.uint64)
+    lib.orc_selection_bytes(C.byref(s.s), cc.h, C.byref(q.r), int(k), idx.ctypes.data, out.ctypes.data)
+    return out
+
+
 class Flows:
     """A flow set for the transfer simulation: link capacities cap [L]
     (bytes/s), per flow a path (CSR path_off [N+1], path: link ids), bytes
@@ -352,11 +366,16 @@ def maxmin(flows, active=None):
     return rate, int(rounds)
 
 
-def flow_sim(flows):
+def flow_sim(flows, stats: bool = False):
     """Event-driven transfer simulation under max-min fair link sharing.
-    Returns (finish times [N] float64, number of allocations computed)."""
+    Returns (finish times [N] float64, number of allocations computed), and
+    with stats also (allocations, filling rounds, flows in progress summed
+    over the allocations)."""
     lib = _load()
     fl = flows if isinstance(flows, Flows) else Flows(flows)
     fin = np.empty(fl.n, np.float64)
-    ev = lib.orc_flow_sim(C.byref(fl.s), fin.ctypes.data)
+    st = np.zeros(3, np.uint64)
+    ev = lib.orc_flow_sim(C.byref(fl.s), fin.ctypes.data, st.ctypes.data)
+    if stats:
+        return fin, int(ev), tuple(int(x) for x in st)
     return fin, int(ev)

@@ -512,6 +512,27 @@ void orc_route_of(const orc_snapshot *s, const orc_cache *c, const orc_requests 
     }
 }
 
+/* Eq. (2): the non-cached bytes s_eff = bpt * (l_r - B_tok * j) of each
+ * selection idx[r*k + i] (0 for no selection): the size of the KV transfer
+ * it starts. */
+void orc_selection_bytes(const orc_snapshot *s, const orc_cache *c, const orc_requests *q, uint32_t k,
+                         const int32_t *idx, uint64_t *out) {
+    for (uint32_t r = 0; r < q->n_req; ++r) {
+        uint64_t a = q->hash_off[r];
+        uint32_t n = (uint32_t)(q->hash_off[r + 1] - a);
+        for (uint32_t i = 0; i < k; ++i) {
+            int32_t d = idx[(uint64_t)r * k + i];
+            if (d < 0) {
+                out[(uint64_t)r * k + i] = 0;
+                continue;
+            }
+            uint32_t t;
+            uint32_t j = prefix_blocks(c, (uint32_t)d, q->hashes + a, n, &t);
+            out[(uint64_t)r * k + i] = s->kv_bytes_per_token * (q->len_tokens[r] - (uint64_t)s->block_tokens * j);
+        }
+    }
+}
+
 /* Requests per tier of the selected decode; counts[4] = rejected. */
 void orc_tier_counts(const orc_snapshot *s, const orc_requests *q, const int32_t *sel, uint64_t *counts) {
     for (int t = 0; t < 5; ++t) counts[t] = 0;
@@ -643,15 +664,16 @@ uint32_t orc_maxmin(const orc_flows *F, const uint8_t *active, double *rate) {
 /* Event-driven simulation: flows start at their arrival time; between
  * events every flow in progress moves at its max-min fair rate; the next
  * event is the earliest completion (remaining / rate) or the next arrival.
- * finish[f] = the completion time of flow f.  Returns the number of
- * events (allocations computed). */
-uint64_t orc_flow_sim(const orc_flows *F, double *finish) {
+ * finish[f] = the completion time of flow f.  stats (may be NULL) =
+ * {allocations computed, filling rounds over all of them, flows in
+ * progress summed over all of them}.  Returns the number of allocations. */
+uint64_t orc_flow_sim(const orc_flows *F, double *finish, uint64_t *stats) {
     const uint32_t N = F->n_flows;
     uint8_t *state = (uint8_t *)calloc(N ? N : 1, 1);   /* 0 waiting, 1 in progress, 2 done */
     uint8_t *active = (uint8_t *)calloc(N ? N : 1, 1);
     double *remaining = (double *)malloc(sizeof(double) * (N ? N : 1));
     double *rate = (double *)malloc(sizeof(double) * (N ? N : 1));
-    uint64_t events = 0;
+    uint64_t events = 0, rounds = 0, moving = 0;
     uint32_t left = N;
     for (uint32_t f = 0; f < N; ++f) remaining[f] = F->bytes[f];
     double t = INFINITY;
@@ -671,7 +693,8 @@ uint64_t orc_flow_sim(const orc_flows *F, double *finish) {
             t = next;
             continue;
         }
-        orc_maxmin(F, active, rate);
+        rounds += orc_maxmin(F, active, rate);
+        moving += n_act;
         ++events;
         double dtc = INFINITY;    /* the earliest completion from t */
         for (uint32_t f = 0; f < N; ++f)
@@ -708,5 +731,10 @@ uint64_t orc_flow_sim(const orc_flows *F, double *finish) {
     free(active);
     free(remaining);
     free(rate);
+    if (stats) {
+        stats[0] = events;
+        stats[1] = rounds;
+        stats[2] = moving;
+    }
     return events;
 }

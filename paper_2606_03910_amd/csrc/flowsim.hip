@@ -1,0 +1,363 @@
+// Flow-level transfer simulation (Sec. VI-B, the evaluation simulator's
+// network model) for MI355X (gfx950).
+//
+// KV transfers are flows over the links of their paths.  Each link is
+// shared max-min fairly among the flows crossing it, and every flow arrival
+// or completion re-evaluates the allocation of all flows in progress;
+// background traffic is a steady utilisation already taken out of each
+// link's capacity (the section's mean-field model).  The allocation is the
+// max-min fair one, computed by progressive filling: all unfrozen flows'
+// rates rise together by the largest amount every link still allows; the
+// flows crossing a link that this fills stop there; repeat.
+//
+// One workgroup runs one instance (a flow set on its links) through all its
+// events; the instances of a call are independent (other congestion draws,
+// other batches).  Inside a workgroup, threads take links and flows in
+// strides, and workgroup reductions give the minimum raise, the next event
+// and the counts.  Every quantity is fp64 and every operation is written
+// out in order with contraction off, so the results equal those of a
+// sequential implementation of the same steps bit for bit (minima do not
+// depend on the reduction order; link counts are integers).
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "netkv.h"
+#include "netkv_internal.h"
+
+namespace {
+
+constexpr int kSimThreads = 256;
+constexpr int kSimWaves = kSimThreads / 64;
+constexpr uint32_t kSimLdsLinks = 2048;   // instances with at most this many links keep them in LDS
+
+// flow states
+constexpr uint8_t kWaiting = 0, kMoving = 1, kDone = 2;
+// freeze marks of a moving flow within one allocation
+constexpr uint8_t kFree = 0, kFrozen = 1, kJustFrozen = 2;
+
+struct SimArgs {
+    uint32_t n_links;
+    const double *cap;          // [n_inst][n_links]
+    const uint64_t *flow_off;   // [n_inst + 1]
+    uint64_t n_flows;
+    const uint64_t *path_off;   // [n_flows + 1]
+    const uint32_t *path;
+    uint64_t n_path;
+    const double *bytes, *start;
+    double *finish;
+    uint64_t *stats;   // [n_inst][3]: allocations, filling rounds, moving flows summed over allocations
+    // work: per flow, and per link of every instance (when not in LDS)
+    double *remaining, *rate;
+    uint8_t *state, *frz;
+    double *g_rem;
+    uint32_t *g_cnt;
+    uint8_t *g_sat;
+    uint32_t *err;
+};
+
+__device__ inline double dmin(double a, double b) { return b < a ? b : a; }
+
+__device__ inline double wave_min_f64(double v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = dmin(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ inline uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+template <bool LDS>
+__global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
+#pragma clang fp contract(off)
+    __shared__ double red_d[2][kSimWaves];
+    __shared__ uint32_t red_u[2][kSimWaves];
+    __shared__ double l_rem[LDS ? kSimLdsLinks : 1];
+    __shared__ uint32_t l_cnt[LDS ? kSimLdsLinks : 1];
+    __shared__ uint8_t l_sat[LDS ? kSimLdsLinks : 1];
+    const uint32_t tid = threadIdx.x, lane = tid % 64, w = tid / 64;
+    const uint32_t inst = blockIdx.x;
+    const uint32_t L = a.n_links;
+    const uint64_t f0 = a.flow_off[inst], f1 = a.flow_off[inst + 1];
+    const double *cap = a.cap + (uint64_t)inst * L;
+    double *rem = LDS ? l_rem : a.g_rem + (uint64_t)inst * L;
+    uint32_t *cnt = LDS ? l_cnt : a.g_cnt + (uint64_t)inst * L;
+    uint8_t *sat = LDS ? l_sat : a.g_sat + (uint64_t)inst * L;
+    // workgroup reductions: one barrier each; two buffers used in turn, so a
+    // buffer is written again only after the next reduction's barrier,
+    // which every thread reaches after reading it
+    uint32_t par = 0;
+    auto bmin = [&](double v) {
+        v = wave_min_f64(v);
+        if (lane == 0) red_d[par][w] = v;
+        __syncthreads();
+        double m = red_d[par][0];
+#pragma unroll
+        for (int q = 1; q < kSimWaves; ++q) m = dmin(m, red_d[par][q]);
+        par ^= 1u;
+        return m;
+    };
+    auto bsum = [&](uint32_t v) {
+        v = wave_sum_u32(v);
+        if (lane == 0) red_u[par][w] = v;
+        __syncthreads();
+        uint32_t m = red_u[par][0];
+#pragma unroll
+        for (int q = 1; q < kSimWaves; ++q) m += red_u[par][q];
+        par ^= 1u;
+        return m;
+    };
+    // the instance's input, checked before any simulation
+    const bool range_ok = f0 <= f1 && f1 <= a.n_flows;
+    uint32_t bad = range_ok ? 0u : 1u;
+    for (uint32_t l = tid; l < L; l += kSimThreads) {
+        const double c = cap[l];
+        if (!(c > 0.0) || !isfinite(c)) bad = 1;
+    }
+    for (uint64_t f = f0 + tid; range_ok && f < f1; f += kSimThreads) {
+        const uint64_t p0 = a.path_off[f], p1 = a.path_off[f + 1];
+        if (!(p1 > p0) || p1 > a.n_path) {
+            bad = 1;
+        } else {
+            for (uint64_t q = p0; q < p1; ++q)
+                if (a.path[q] >= L) bad = 1;
+        }
+        const double b = a.bytes[f], s = a.start[f];
+        if (!(b >= 0.0) || !isfinite(b) || !isfinite(s)) bad = 1;
+    }
+    if (bsum(bad)) {
+        for (uint64_t f = f0 + tid; range_ok && f < f1; f += kSimThreads) a.finish[f] = NAN;
+        if (tid == 0) {
+            atomicOr(a.err, kErrFlowBit);
+            if (a.stats)
+                for (int q = 0; q < 3; ++q) a.stats[3ull * inst + q] = 0;
+        }
+        return;
+    }
+    // flows wait for their arrival; the clock starts at the first one
+    double t0 = INFINITY;
+    for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+        a.state[f] = kWaiting;
+        a.frz[f] = kFree;
+        a.remaining[f] = a.bytes[f];
+        t0 = dmin(t0, a.start[f]);
+    }
+    double t = bmin(t0);
+    const uint64_t nf = f1 - f0;
+    uint64_t left = nf;
+    uint64_t events = 0, rounds = 0, moving = 0;
+    bool stall = false;
+    // each pass starts a flow or completes one (or both), so 2 nf + 1 passes
+    // end every valid instance
+    for (uint64_t pass = 0; left > 0; ++pass) {
+        if (pass > 2 * nf + 4) {
+            stall = true;
+            break;
+        }
+        // start the flows that have arrived; the next arrival
+        uint32_t na = 0;
+        double nx = INFINITY;
+        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+            uint8_t st = a.state[f];
+            const double s = a.start[f];
+            if (st == kWaiting && s <= t) {
+                st = kMoving;
+                a.state[f] = st;
+            }
+            na += st == kMoving ? 1u : 0u;
+            if (st == kWaiting) nx = dmin(nx, s);
+        }
+        na = bsum(na);
+        nx = bmin(nx);
+        if (na == 0) {
+            t = nx;
+            continue;
+        }
+        // the max-min fair allocation of the moving flows
+        for (uint32_t l = tid; l < L; l += kSimThreads) {
+            rem[l] = cap[l];
+            cnt[l] = 0;
+        }
+        __syncthreads();
+        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+            if (a.state[f] != kMoving) continue;
+            a.frz[f] = kFree;
+            for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) atomicAdd(&cnt[a.path[q]], 1u);
+        }
+        __syncthreads();
+        double level = 0.0;
+        uint32_t unfrozen = na;
+        for (uint32_t round = 0; unfrozen > 0; ++round) {
+            if (round > na) {   // every round freezes at least one flow
+                stall = true;
+                break;
+            }
+            // the largest equal raise every link still allows
+            double sh = INFINITY;
+            for (uint32_t l = tid; l < L; l += kSimThreads) {
+                const uint32_t c = cnt[l];
+                if (c > 0) sh = dmin(sh, rem[l] / (double)c);
+            }
+            const double inc = bmin(sh);
+            // links that the raise fills, and the capacity left on each
+            for (uint32_t l = tid; l < L; l += kSimThreads) {
+                const uint32_t c = cnt[l];
+                uint8_t full = 0;
+                if (c > 0) {
+                    const double r = rem[l];
+                    full = r / (double)c == inc ? 1 : 0;
+                    const double used = inc * (double)c;
+                    const double lf = r - used;
+                    rem[l] = lf > 0.0 ? lf : 0.0;
+                }
+                sat[l] = full;
+            }
+            level = level + inc;
+            __syncthreads();
+            // flows crossing a filled link stop at the current level
+            uint32_t nfz = 0;
+            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+                if (a.state[f] != kMoving || a.frz[f] != kFree) continue;
+                uint8_t hit = 0;
+                for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) hit |= sat[a.path[q]];
+                if (hit) {
+                    a.frz[f] = kJustFrozen;
+                    a.rate[f] = level;
+                    ++nfz;
+                }
+            }
+            nfz = bsum(nfz);
+            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+                if (a.state[f] != kMoving || a.frz[f] != kJustFrozen) continue;
+                a.frz[f] = kFrozen;
+                for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) atomicSub(&cnt[a.path[q]], 1u);
+            }
+            __syncthreads();
+            unfrozen -= nfz;
+            ++rounds;
+        }
+        if (stall) break;
+        ++events;
+        moving += na;
+        // the next event: the earliest completion, or the next arrival
+        double tc = INFINITY;
+        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads)
+            if (a.state[f] == kMoving) tc = dmin(tc, a.remaining[f] / a.rate[f]);
+        const double dtc = bmin(tc);
+        uint32_t nd = 0;
+        if (dtc <= nx - t) {
+            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+                if (a.state[f] != kMoving) continue;
+                const double rm = a.remaining[f], rt = a.rate[f];
+                if (rm / rt == dtc) {
+                    a.state[f] = kDone;
+                    a.finish[f] = t + dtc;
+                    ++nd;
+                } else {
+                    const double moved = rt * dtc;
+                    const double r = rm - moved;
+                    a.remaining[f] = r > 0.0 ? r : 0.0;
+                }
+            }
+            t = t + dtc;
+        } else {
+            const double dt = nx - t;
+            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
+                if (a.state[f] != kMoving) continue;
+                const double moved = a.rate[f] * dt;
+                const double r = a.remaining[f] - moved;
+                a.remaining[f] = r > 0.0 ? r : 0.0;
+            }
+            t = nx;
+        }
+        left -= bsum(nd);
+    }
+    if (stall) {
+        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads)
+            if (a.state[f] != kDone) a.finish[f] = NAN;
+        if (tid == 0) atomicOr(a.err, kErrFlowStallBit);
+    }
+    if (tid == 0 && a.stats) {
+        a.stats[3ull * inst + 0] = events;
+        a.stats[3ull * inst + 1] = rounds;
+        a.stats[3ull * inst + 2] = moving;
+    }
+}
+
+inline uint64_t align256(uint64_t x) { return (x + 255) / 256 * 256; }
+
+}  // namespace
+
+extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t n_links, const double *cap,
+                                       const uint64_t *flow_off, uint64_t n_flows, const uint64_t *path_off,
+                                       const uint32_t *path, uint64_t n_path, const double *bytes,
+                                       const double *start, double *finish, uint64_t *stats, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    netkv_internal_clear(h);
+    if (n_inst == 0) return NETKV_OK;
+    if (n_links == 0) return netkv_internal_fail(h, NETKV_EINVAL, "n_links must be >= 1");
+    if (n_inst > 0x7FFFFFFFu) return netkv_internal_fail(h, NETKV_EINVAL, "n_inst must be < 2^31");
+    if (!cap || !flow_off || !path_off || (n_flows && (!bytes || !start || !finish)) || (n_path && !path))
+        return netkv_internal_fail(h, NETKV_EINVAL, "NULL array");
+    if (n_flows > (1ull << 40) || n_path > (1ull << 40))
+        return netkv_internal_fail(h, NETKV_EINVAL, "n_flows and n_path must be <= 2^40");
+    const int dev = netkv_internal_device(h);
+    int prev = -1;
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+    const bool lds = n_links <= kSimLdsLinks;
+    const uint64_t per_flow = align256(8 * n_flows) * 2 + align256(n_flows) * 2;
+    const uint64_t per_link = lds ? 0 : align256(8ull * n_inst * n_links) + align256(4ull * n_inst * n_links) +
+                                            align256((uint64_t)n_inst * n_links);
+    void *buf = nullptr;
+    netkv_status st = NETKV_OK;
+    hipError_t e = netkv_internal_flow_buffer(h, per_flow + per_link + 256, &buf);
+    if (e != hipSuccess) {
+        st = netkv_internal_fail(h, e == hipErrorOutOfMemory ? NETKV_ENOMEM : NETKV_EDEVICE,
+                                 "flow simulation work buffer allocation failed");
+    } else {
+        uint8_t *p = (uint8_t *)buf;
+        SimArgs a{};
+        a.n_links = n_links;
+        a.cap = cap;
+        a.flow_off = flow_off;
+        a.n_flows = n_flows;
+        a.path_off = path_off;
+        a.path = path;
+        a.n_path = n_path;
+        a.bytes = bytes;
+        a.start = start;
+        a.finish = finish;
+        a.stats = stats;
+        a.remaining = (double *)p;
+        p += align256(8 * n_flows);
+        a.rate = (double *)p;
+        p += align256(8 * n_flows);
+        a.state = p;
+        p += align256(n_flows);
+        a.frz = p;
+        p += align256(n_flows);
+        if (!lds) {
+            a.g_rem = (double *)p;
+            p += align256(8ull * n_inst * n_links);
+            a.g_cnt = (uint32_t *)p;
+            p += align256(4ull * n_inst * n_links);
+            a.g_sat = p;
+        }
+        a.err = netkv_internal_errword(h);
+        hipStream_t s = (hipStream_t)stream;
+        if (lds)
+            hipLaunchKernelGGL(flow_sim_kernel<true>, dim3(n_inst), dim3(kSimThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL(flow_sim_kernel<false>, dim3(n_inst), dim3(kSimThreads), 0, s, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) st = netkv_internal_fail(h, NETKV_EDEVICE, hipGetErrorString(e));
+    }
+    if (prev >= 0 && prev != dev) (void)hipSetDevice(prev);
+    return st;
+}

@@ -59,6 +59,7 @@
 #include <vector>
 
 #include "netkv.h"
+#include "netkv_internal.h"
 
 namespace {
 
@@ -77,6 +78,8 @@ enum : uint32_t {
     kErrObservation = 2u,   // congestion observation outside [0, 1) or NaN
     kErrSelection = 4u,  // selection index out of range
     kErrTableFull = 8u,  // insertion found no free slot
+    kErrFlow = kErrFlowBit,           // flow simulation: invalid flow set
+    kErrFlowStall = kErrFlowStallBit,   // flow simulation: an iteration bound was reached
 };
 
 // ------------------------------------------------------------------ device data
@@ -2109,6 +2112,29 @@ __global__ __launch_bounds__(256) void route_of_kernel(Snap s, Table t, Reqs rq,
     out[i] = fmaf(x, r2.x, r2.y) < fmaf(x, r1.x, r1.y) ? 1 : 0;
 }
 
+// Non-cached bytes of each selection (Eq. (2) in the integer form
+// bpt * (l_r - B_tok * j)): the selected pair's prefix length by the first
+// miss of the run on that decode.  0 for no selection or an invalid
+// request; a selection index >= D is flagged.
+__global__ __launch_bounds__(256) void selection_bytes_kernel(Snap s, Table t, Reqs rq, uint32_t k,
+                                                              const int32_t *__restrict__ idx,
+                                                              uint64_t *__restrict__ out, uint32_t *__restrict__ err) {
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (uint64_t)rq.n_req * k) return;
+    const uint32_t r = (uint32_t)(i / k);
+    const int32_t d = idx[i];
+    uint32_t p, len, n;
+    uint64_t a;
+    if (d >= 0 && (uint32_t)d >= s.D) atomicOr(err, kErrSelection);
+    if (d < 0 || (uint32_t)d >= s.D || !request_ok(rq, s, r, p, len, a, n)) {
+        out[i] = 0;
+        return;
+    }
+    uint32_t j = 0;
+    while (j < n && holds(t, rq.hashes[a + j], (uint32_t)d)) ++j;
+    out[i] = (uint64_t)s.bpt * (uint64_t)(len - s.block_tokens * j);
+}
+
 // Requests per tier of the selected decode (index 4: rejected), the tier
 // shift statistic.  Invalid selections are flagged and not counted.
 __global__ __launch_bounds__(256) void tier_count_kernel(Snap s, Reqs rq, const int32_t *__restrict__ sel,
@@ -2556,6 +2582,9 @@ struct netkv_ctx {
     // events (so a caller's graph capture takes both branches)
     hipStream_t side = nullptr;
     hipEvent_t ev_fork0 = nullptr, ev_fork1 = nullptr, ev_join = nullptr;
+    // the flow simulation's work buffer (flowsim.hip)
+    void *flow_buf = nullptr;
+    uint64_t flow_buf_bytes = 0;
     float t_a = 0, t_b = 0, alpha = 0;
     uint32_t beta_max = 0, bpt = 0, block_tokens = 1;
     uint64_t m_min = 0;
@@ -3400,6 +3429,29 @@ uint8_t *scratch_of(int device) {
 
 // ------------------------------------------------------------------ API
 
+// ---- for the library's other translation units (netkv_internal.h)
+
+netkv_status netkv_internal_fail(netkv_handle h, netkv_status st, const char *msg) { return fail(h, st, "%s", msg); }
+
+void netkv_internal_clear(netkv_handle h) { h->err.clear(); }
+
+int netkv_internal_device(netkv_handle h) { return h->device; }
+
+uint32_t *netkv_internal_errword(netkv_handle h) { return h->errword; }
+
+hipError_t netkv_internal_flow_buffer(netkv_handle h, uint64_t bytes, void **out) {
+    if (bytes > h->flow_buf_bytes) {
+        if (h->flow_buf) (void)hipFree(h->flow_buf);
+        h->flow_buf = nullptr;
+        h->flow_buf_bytes = 0;
+        const hipError_t e = hipMalloc(&h->flow_buf, bytes);
+        if (e != hipSuccess) return e;
+        h->flow_buf_bytes = bytes;
+    }
+    *out = h->flow_buf;
+    return hipSuccess;
+}
+
 extern "C" {
 
 netkv_status netkv_create(netkv_handle *out, int device) {
@@ -3430,6 +3482,7 @@ void netkv_destroy(netkv_handle h) {
         DeviceGuard g(h->device);
         (void)hipDeviceSynchronize();
         if (h->side) (void)hipStreamDestroy(h->side);
+        if (h->flow_buf) (void)hipFree(h->flow_buf);
         if (h->ev_fork0) (void)hipEventDestroy(h->ev_fork0);
         if (h->ev_fork1) (void)hipEventDestroy(h->ev_fork1);
         if (h->ev_join) (void)hipEventDestroy(h->ev_join);
@@ -3718,6 +3771,24 @@ netkv_status netkv_route2_of(netkv_handle h, const netkv_requests_t *req, uint32
     const uint64_t n = (uint64_t)req->n_req * k;
     hipLaunchKernelGGL(route_of_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, sn, make_table(h),
                        make_reqs(req), k, idx, out_route);
+    HIPCHK(h, hipGetLastError());
+    return NETKV_OK;
+}
+
+netkv_status netkv_selection_bytes(netkv_handle h, const netkv_requests_t *req, uint32_t k, const int32_t *idx,
+                                   uint64_t *out_bytes, void *stream) {
+    if (!h) return NETKV_EINVAL;
+    h->err.clear();
+    netkv_status st = check_requests(h, req);
+    if (st) return st;
+    if (k < 1 || k > 8) return fail(h, NETKV_EINVAL, "k must be in [1, 8]");
+    if (req->n_req && (!idx || !out_bytes)) return fail(h, NETKV_EINVAL, "idx and out_bytes must not be NULL");
+    if ((st = ready(h))) return st;
+    if (req->n_req == 0) return NETKV_OK;
+    DeviceGuard g(h->device);
+    const uint64_t n = (uint64_t)req->n_req * k;
+    hipLaunchKernelGGL(selection_bytes_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream,
+                       make_snap(h), make_table(h), make_reqs(req), k, idx, out_bytes, h->errword);
     HIPCHK(h, hipGetLastError());
     return NETKV_OK;
 }
@@ -4118,10 +4189,12 @@ netkv_status netkv_sync_errors(netkv_handle h, void *stream) {
     HIPCHK(h, hipMemcpy(&e, h->errword, 4, hipMemcpyDeviceToHost));
     HIPCHK(h, hipMemset(h->errword, 0, 4));
     if (e)
-        return fail(h, NETKV_EINVAL, "input errors:%s%s%s%s", (e & kErrRequest) ? " inconsistent request header" : "",
+        return fail(h, NETKV_EINVAL, "input errors:%s%s%s%s%s%s",
+                    (e & kErrRequest) ? " inconsistent request header" : "",
                     (e & kErrObservation) ? " congestion observation outside [0,1)" : "",
-                    (e & kErrSelection) ? " selection index >= D" : "",
-                    (e & kErrTableFull) ? " table full" : "");
+                    (e & kErrSelection) ? " selection index >= D" : "", (e & kErrTableFull) ? " table full" : "",
+                    (e & kErrFlow) ? " invalid flow set" : "",
+                    (e & kErrFlowStall) ? " flow simulation reached its iteration bound" : "");
     return NETKV_OK;
 }
 

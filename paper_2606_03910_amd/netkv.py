@@ -93,6 +93,11 @@ _SIGS = {
                                       C.c_void_p]),
     "netkv_select_sequential": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32,
                                             C.c_void_p, C.c_void_p, C.c_void_p]),
+    "netkv_selection_bytes": (C.c_int32, [C.c_void_p, C.POINTER(netkv_requests_t), C.c_uint32, C.c_void_p,
+                                          C.c_void_p, C.c_void_p]),
+    "netkv_flow_sim": (C.c_int32, [C.c_void_p, C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p, C.c_uint64,
+                                   C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p, C.c_void_p, C.c_void_p,
+                                   C.c_void_p, C.c_void_p]),
 }
 
 NETKV_OPT_RUN_LEN = 1
@@ -228,6 +233,29 @@ def netkv_route2_of(h: int, req: Dict[str, torch.Tensor], k: int, idx: torch.Ten
                                              _dptr(idx, torch.int32, r.n_req * k, "idx"),
                                              _dptr(out_route, torch.int8, r.n_req * k, "out_route"),
                                              _stream(device)))
+
+
+def netkv_selection_bytes(h: int, req: Dict[str, torch.Tensor], k: int, idx: torch.Tensor,
+                          out_bytes: torch.Tensor, device) -> None:
+    r = _requests(req)
+    _check(h, load_library().netkv_selection_bytes(h, C.byref(r), int(k),
+                                                   _dptr(idx, torch.int32, r.n_req * k, "idx"),
+                                                   _dptr(out_bytes, torch.uint64, r.n_req * k, "out_bytes"),
+                                                   _stream(device)))
+
+
+def netkv_flow_sim(h: int, n_inst: int, n_links: int, cap: torch.Tensor, flow_off: torch.Tensor,
+                   path_off: torch.Tensor, path: torch.Tensor, nbytes: torch.Tensor, start: torch.Tensor,
+                   finish: torch.Tensor, stats: Optional[torch.Tensor], device) -> None:
+    n_flows = int(nbytes.numel())
+    n_path = int(path.numel())
+    _check(h, load_library().netkv_flow_sim(
+        h, int(n_inst), int(n_links), _dptr(cap, torch.float64, n_inst * n_links, "cap"),
+        _dptr(flow_off, torch.uint64, n_inst + 1, "flow_off"), n_flows,
+        _dptr(path_off, torch.uint64, n_flows + 1, "path_off"), _dptr(path, torch.uint32, name="path"), n_path,
+        _dptr(nbytes, torch.float64, n_flows, "bytes"), _dptr(start, torch.float64, n_flows, "start"),
+        _dptr(finish, torch.float64, n_flows, "finish"),
+        _dptr(stats, torch.uint64, 3 * n_inst, "stats") if stats is not None else None, _stream(device)))
 
 
 def netkv_cache_load(h: int, n_decode: int, hash_off: torch.Tensor, hashes: torch.Tensor,
@@ -472,6 +500,25 @@ class Selector:
         out = torch.empty(n * k, dtype=torch.int8, device=self.device)
         netkv_route2_of(self.h, req_dev, k, idx, out, self.device)
         return to_numpy(out)
+
+    def selection_bytes(self, req_dev, idx: torch.Tensor, k: int) -> torch.Tensor:
+        """Non-cached bytes (Eq. (2)) of each selection; 0 for none."""
+        n = int(req_dev["prefill"].numel())
+        out = torch.empty(n * k, dtype=torch.uint64, device=self.device)
+        netkv_selection_bytes(self.h, req_dev, k, idx, out, self.device)
+        return out
+
+    def flow_sim(self, fl: Dict[str, torch.Tensor], n_inst: int, n_links: int):
+        """Flow-level transfer simulation of n_inst instances (device
+        tensors cap [n_inst * n_links] f64, flow_off [n_inst + 1] u64,
+        path_off u64, path u32, bytes f64, start f64): finish times [n_flows]
+        and per instance (allocations, filling rounds, moving flows summed
+        over the allocations) [n_inst, 3]."""
+        fin = torch.empty(int(fl["bytes"].numel()), dtype=torch.float64, device=self.device)
+        st = torch.empty(3 * n_inst, dtype=torch.uint64, device=self.device)
+        netkv_flow_sim(self.h, n_inst, n_links, fl["cap"], fl["flow_off"], fl["path_off"], fl["path"],
+                       fl["bytes"], fl["start"], fin, st, self.device)
+        return fin, st
 
     def rank_sweep(self, req_dev, util_scen: torch.Tensor, k: int = 3):
         n = int(req_dev["prefill"].numel())

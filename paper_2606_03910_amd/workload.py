@@ -494,3 +494,88 @@ def make_routes(cfg: Config, seed: int) -> Dict[str, np.ndarray]:
                 route_util1=rng.uniform(0.0, 0.9, n).astype(np.float32),
                 route_tier2=rng.integers(0, 2, n).astype(np.uint8),
                 route_util2=rng.uniform(0.0, 0.9, n).astype(np.float32))
+
+
+# --------------------------------------------------------------------------
+# fat-tree links and KV-transfer flows (the transfer simulation's input)
+# --------------------------------------------------------------------------
+
+def fat_tree_links(cfg: Config, links: Dict[str, np.ndarray], spines: int = 4, cores: int = 4):
+    """The cluster's links for the flow-level transfer simulation, with
+    capacities after background load (bytes/s): per GPU an egress and an
+    ingress port on its node's fabric (tier-0 bandwidth, the node's u0) and
+    a NIC uplink and downlink (tier 1, the node's u1); per leaf `spines`
+    uplinks and downlinks (tier 2, the leaf's u2); per pod `cores` uplinks
+    and downlinks (tier 3, the pod's u3).  A flow alone on a path of tier tau
+    with no background load moves at exactly B_tau.  Returns (cap [L],
+    layout dict of the index bases)."""
+    cl = cfg.cluster
+    G, NL, NP = cl.n_gpus, cl.n_leaves, cl.pods
+    node, leaf, pod = cl.coords()
+    bw = np.asarray(cfg.tier_bw, dtype=np.float64)
+    u = {t: np.asarray(links[f"u{t}"], dtype=np.float64) for t in range(4)}
+    lay = dict(node_out=0, node_in=G, nic_up=2 * G, nic_down=3 * G, leaf_up=4 * G,
+               leaf_down=4 * G + NL * spines, pod_up=4 * G + 2 * NL * spines,
+               pod_down=4 * G + 2 * NL * spines + NP * cores, spines=spines, cores=cores)
+    L = 4 * G + 2 * NL * spines + 2 * NP * cores
+    cap = np.empty(L, dtype=np.float64)
+    g = np.arange(G)
+    cap[lay["node_out"] + g] = bw[0] * (1.0 - u[0][node])
+    cap[lay["node_in"] + g] = bw[0] * (1.0 - u[0][node])
+    cap[lay["nic_up"] + g] = bw[1] * (1.0 - u[1][node])
+    cap[lay["nic_down"] + g] = bw[1] * (1.0 - u[1][node])
+    lf = np.repeat(np.arange(NL), spines)
+    cap[lay["leaf_up"]:lay["leaf_up"] + NL * spines] = bw[2] * (1.0 - u[2][lf])
+    cap[lay["leaf_down"]:lay["leaf_down"] + NL * spines] = bw[2] * (1.0 - u[2][lf])
+    pd = np.repeat(np.arange(NP), cores)
+    cap[lay["pod_up"]:lay["pod_up"] + NP * cores] = bw[3] * (1.0 - u[3][pd])
+    cap[lay["pod_down"]:lay["pod_down"] + NP * cores] = bw[3] * (1.0 - u[3][pd])
+    return cap, lay
+
+
+def transfer_paths(cfg: Config, seed: int, p_inst: np.ndarray, d_inst: np.ndarray, lay: Dict[str, int]):
+    """The path of the KV transfer from prefill instance p_inst[i] to decode
+    instance d_inst[i]: same node, the two fabric ports; same leaf, the two
+    NICs; same pod, NIC, a leaf uplink, the matching downlink of the other
+    leaf, NIC; across pods, NIC, a leaf uplink, a pod uplink, the matching
+    pod downlink, a leaf downlink, NIC.  ECMP picks the spine and core
+    uniformly at random per flow (seeded).  Returns (path_off [N+1] u64,
+    path u32)."""
+    cl = cfg.cluster
+    node, leaf, pod = cl.coords()
+    a = cl.prefill_gpus()[np.asarray(p_inst, dtype=np.int64)]
+    b = cl.decode_gpus()[np.asarray(d_inst, dtype=np.int64)]
+    rng = _rng(seed, 81)
+    S, Cc = lay["spines"], lay["cores"]
+    n = len(a)
+    s1 = rng.integers(0, S, n)
+    s2 = rng.integers(0, S, n)
+    cc = rng.integers(0, Cc, n)
+    tier = np.where(node[a] == node[b], 0, np.where(leaf[a] == leaf[b], 1, np.where(pod[a] == pod[b], 2, 3)))
+    plen = np.array([2, 2, 4, 6])[tier]
+    off = np.zeros(n + 1, dtype=np.uint64)
+    off[1:] = np.cumsum(plen)
+    cols = np.full((n, 6), -1, dtype=np.int64)
+    t0, t1, t2, t3 = (tier == 0), (tier == 1), (tier == 2), (tier == 3)
+    cols[t0, 0] = lay["node_out"] + a[t0]
+    cols[t0, 1] = lay["node_in"] + b[t0]
+    cols[t1, 0] = lay["nic_up"] + a[t1]
+    cols[t1, 1] = lay["nic_down"] + b[t1]
+    cols[t2, 0] = lay["nic_up"] + a[t2]
+    cols[t2, 1] = lay["leaf_up"] + leaf[a[t2]] * S + s1[t2]
+    cols[t2, 2] = lay["leaf_down"] + leaf[b[t2]] * S + s1[t2]
+    cols[t2, 3] = lay["nic_down"] + b[t2]
+    cols[t3, 0] = lay["nic_up"] + a[t3]
+    cols[t3, 1] = lay["leaf_up"] + leaf[a[t3]] * S + s1[t3]
+    cols[t3, 2] = lay["pod_up"] + pod[a[t3]] * Cc + cc[t3]
+    cols[t3, 3] = lay["pod_down"] + pod[b[t3]] * Cc + cc[t3]
+    cols[t3, 4] = lay["leaf_down"] + leaf[b[t3]] * S + s2[t3]
+    cols[t3, 5] = lay["nic_down"] + b[t3]
+    path = cols[cols >= 0].astype(np.uint32)   # row-major: each flow's links in order
+    return off, path
+
+
+def transfer_starts(seed: int, n: int, window: float = 0.05) -> np.ndarray:
+    """Arrival times of n transfers (the moments their prefills complete),
+    uniform over a window of `window` seconds."""
+    return np.sort(_rng(seed, 91).uniform(0.0, window, n))

@@ -992,3 +992,19 @@ def test_flowsim_never_beats_the_path_alone_and_matches_it_without_sharing(seed)
     fin, _ = oracle.flow_sim(f)
     assert (fin >= nbytes / np.minimum(cap2[0:2 * N:2], 0.5) * (1 - 1e-14)).all()
     np.testing.assert_allclose(fin.max(), nbytes.sum() / 0.5, rtol=1e-12)
+
+
+def test_selection_bytes_is_eq2_on_a_hand_built_case():
+    """Eq. (2) for the flows the transfer simulation takes: a request of
+    1,000 tokens in blocks of 100 (10 hashed blocks), whose first three
+    blocks are resident on decode 0 and whose first block is missing on
+    decode 1 (a later block resident there does not count: Sec. III-B's
+    leading run).  With Eq. (1)'s 327,680 bytes per token: decode 0 moves
+    700 tokens, decode 1 all 1,000; no selection moves nothing."""
+    bpt = 327680
+    snap = tiny_snapshot(1, 2, [1, 1], [0.0, 0.0], bpt=bpt, block_tokens=100)
+    h = [11, 12, 13, 14, 15, 16, 17, 18, 19, 20]
+    cache = caches([[11, 12, 13, 15], [12, 13]])
+    req = requests([(0, 1000, h), (0, 1000, h), (0, 1000, h)])
+    out = oracle.selection_bytes(snap, cache, req, np.array([0, 1, -1], np.int32), 1)
+    assert out.tolist() == [700 * bpt, 1000 * bpt, 0]
