@@ -103,6 +103,10 @@ def _load():
         lib.orc_max_threads.restype = C.c_int
         lib.orc_selection_bytes.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint32, C.c_void_p,
                                             C.c_void_p]
+        lib.orc_pair_congestion.argtypes = [C.c_uint32, C.c_uint32] + [C.c_void_p] * 12
+        lib.orc_ar1_step.argtypes = [C.c_uint64, C.c_void_p, C.c_void_p, C.c_void_p, C.c_double, C.c_double,
+                                     C.c_void_p]
+        lib.orc_link_noise.argtypes = [C.c_uint64, C.c_void_p, C.c_void_p, C.c_double, C.c_void_p]
         lib.orc_maxmin.restype = C.c_uint32
         lib.orc_maxmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
         lib.orc_flow_sim.restype = C.c_uint64
@@ -379,3 +383,42 @@ def flow_sim(flows, stats: bool = False):
     if stats:
         return fin, int(ev), tuple(int(x) for x in st)
     return fin, int(ev)
+
+
+# ---------------------------------------------------------------- telemetry derivations
+
+def pair_congestion(p_coords, d_coords, links):
+    """Per-pair tier and congestion from per-link utilisation (netkv_oracle.c,
+    orc_pair_congestion).  p_coords / d_coords: (node, leaf, pod) index
+    arrays of each prefill / decode instance's GPU; links: dict u0..u3.
+    Returns (tier [P, D] uint8, util [P, D] float32)."""
+    lib = _load()
+    pn, pl, pp = (_arr(x, np.uint32) for x in p_coords)
+    dn, dl, dp = (_arr(x, np.uint32) for x in d_coords)
+    u = [_arr(links[f"u{t}"], np.float64) for t in range(4)]
+    P, D = len(pn), len(dn)
+    tier = np.empty((P, D), np.uint8)
+    util = np.empty((P, D), np.float32)
+    lib.orc_pair_congestion(P, D, pn.ctypes.data, pl.ctypes.data, pp.ctypes.data, dn.ctypes.data,
+                            dl.ctypes.data, dp.ctypes.data, *[x.ctypes.data for x in u], tier.ctypes.data,
+                            util.ctypes.data)
+    return tier, util
+
+
+def ar1_step(cur, mean, eps, rho: float, sigma: float) -> np.ndarray:
+    """One AR(1) step of link utilisations (orc_ar1_step)."""
+    lib = _load()
+    c, m, e = (_arr(x, np.float64) for x in (cur, mean, eps))
+    out = np.empty(len(c), np.float64)
+    lib.orc_ar1_step(len(c), c.ctypes.data, m.ctypes.data, e.ctypes.data, float(rho), float(sigma),
+                     out.ctypes.data)
+    return out
+
+
+def link_noise(u, z, sigma: float) -> np.ndarray:
+    """Lognormal telemetry noise on link utilisations (orc_link_noise)."""
+    lib = _load()
+    a, b = _arr(u, np.float64), _arr(z, np.float64)
+    out = np.empty(len(a), np.float64)
+    lib.orc_link_noise(len(a), a.ctypes.data, b.ctypes.data, float(sigma), out.ctypes.data)
+    return out

@@ -738,3 +738,78 @@ uint64_t orc_flow_sim(const orc_flows *F, double *finish, uint64_t *stats) {
     }
     return events;
 }
+
+/* ------------------------------------------------------------------------
+ * Telemetry derivations (the operator's side of the interface): what the
+ * snapshot's congestion map is made of.  These restate the readings that
+ * the synthetic inputs follow, so that the inputs can be checked against
+ * them.
+ * ------------------------------------------------------------------------ */
+
+/* Per-link utilisation to one congestion value per (p, d) pair (Sec. III-E
+ * gives one congestion value per tier; reading: the snapshot carries one per
+ * pair).  The pair's tier is the lowest level its two GPUs share: 0 same
+ * node, 1 same leaf, 2 same pod, 3 otherwise.  Its congestion is the larger
+ * utilisation of the two tier-level links at its ends: u0 per node (the
+ * node's fabric), u1 per node (its NIC uplink), u2 per leaf (leaf-spine),
+ * u3 per pod (pod-core); domain of tier 0 and 1 = node, 2 = leaf, 3 = pod.
+ * Coordinates per prefill and per decode: node, leaf, pod indices.  Writes
+ * tier [P*D] and util [P*D] (fp32 of the fp64 maximum). */
+void orc_pair_congestion(uint32_t P, uint32_t D, const uint32_t *p_node, const uint32_t *p_leaf,
+                         const uint32_t *p_pod, const uint32_t *d_node, const uint32_t *d_leaf,
+                         const uint32_t *d_pod, const double *u0, const double *u1, const double *u2,
+                         const double *u3, uint8_t *tier, float *util) {
+    for (uint32_t p = 0; p < P; ++p)
+        for (uint32_t d = 0; d < D; ++d) {
+            uint8_t t;
+            double a, b;
+            if (p_node[p] == d_node[d]) {
+                t = 0;
+                a = u0[p_node[p]];
+                b = u0[d_node[d]];
+            } else if (p_leaf[p] == d_leaf[d]) {
+                t = 1;
+                a = u1[p_node[p]];
+                b = u1[d_node[d]];
+            } else if (p_pod[p] == d_pod[d]) {
+                t = 2;
+                a = u2[p_leaf[p]];
+                b = u2[d_leaf[d]];
+            } else {
+                t = 3;
+                a = u3[p_pod[p]];
+                b = u3[d_pod[d]];
+            }
+            tier[(uint64_t)p * D + d] = t;
+            util[(uint64_t)p * D + d] = (float)(a > b ? a : b);
+        }
+}
+
+/* One AR(1) step of n link utilisations (reading of the streaming
+ * workload's telemetry): next = clamp(mean + rho (cur - mean) + sigma eps,
+ * 0, 0.99), with mean the link's initial utilisation and eps a standard
+ * normal draw per link (given). */
+void orc_ar1_step(uint64_t n, const double *cur, const double *mean, const double *eps, double rho,
+                  double sigma, double *next) {
+    for (uint64_t i = 0; i < n; ++i) {
+        const double dev = cur[i] - mean[i];
+        const double pull = rho * dev;
+        const double shock = sigma * eps[i];
+        double v = mean[i] + pull;
+        v = v + shock;
+        if (v < 0.0) v = 0.0;
+        if (v > 0.99) v = 0.99;
+        next[i] = v;
+    }
+}
+
+/* Noisy telemetry of one scenario (Sec. V-D's stale congestion, reading:
+ * lognormal noise): each link utilisation times exp(sigma z), z a standard
+ * normal draw per link (given), capped at 0.99. */
+void orc_link_noise(uint64_t n, const double *u, const double *z, double sigma, double *out) {
+    for (uint64_t i = 0; i < n; ++i) {
+        const double m = exp(sigma * z[i]);
+        const double v = u[i] * m;
+        out[i] = v < 0.99 ? v : 0.99;
+    }
+}

@@ -1008,3 +1008,77 @@ def test_selection_bytes_is_eq2_on_a_hand_built_case():
     req = requests([(0, 1000, h), (0, 1000, h), (0, 1000, h)])
     out = oracle.selection_bytes(snap, cache, req, np.array([0, 1, -1], np.int32), 1)
     assert out.tolist() == [700 * bpt, 1000 * bpt, 0]
+
+
+# ---------------------------------------------------------------- telemetry derivations
+
+def _two_pod_coords():
+    """8 GPUs: 2 per node, 2 nodes per leaf, 1 leaf per pod, 2 pods.  Prefill
+    on GPU 0; decodes on GPUs 1 (same node), 2 (same leaf), 4 and 6 (other
+    pod)."""
+    node = np.array([0, 0, 1, 1, 2, 2, 3, 3])
+    leaf = node // 2
+    pod = leaf
+    pg, dg = [0], [1, 2, 4, 6]
+    return (node[pg], leaf[pg], pod[pg]), (node[dg], leaf[dg], pod[dg])
+
+
+def test_pair_congestion_constant_per_tier_is_the_papers_c_tau():
+    """Sec. III-E gives one congestion value c_tau per tier.  With every link
+    of tier tau at the same utilisation, each pair of tier tau gets exactly
+    c_tau, and the tiers follow the topology (same node 0, same leaf 1,
+    other pod 3)."""
+    pc, dc = _two_pod_coords()
+    c = [0.125, 0.25, 0.5, 0.75]
+    links = {f"u{t}": np.full(4, c[t]) for t in range(4)}
+    tier, util = oracle.pair_congestion(pc, dc, links)
+    assert tier.tolist() == [[0, 1, 3, 3]]
+    assert util.tolist() == [[0.125, 0.25, 0.75, 0.75]]
+
+
+def test_pair_congestion_takes_the_busier_end():
+    """With per-link values, a pair reads the tier-level links at both of its
+    ends and takes the larger: node 0's fabric (0.1) against itself; NIC
+    uplinks of nodes 0 and 1 (0.2, 0.6); the pod uplinks of pods 0 and 1
+    (0.3, 0.05) for the cross-pod pairs."""
+    pc, dc = _two_pod_coords()
+    links = dict(u0=np.array([0.1, 0.9, 0.9, 0.9]), u1=np.array([0.2, 0.6, 0.0, 0.0]),
+                 u2=np.array([0.7, 0.7]), u3=np.array([0.3, 0.05]))
+    _, util = oracle.pair_congestion(pc, dc, links)
+    np.testing.assert_array_equal(util, np.float32([[0.1, 0.6, 0.3, 0.3]]))
+
+
+def test_ar1_step_closed_forms():
+    """The AR(1) telemetry step: rho = 1 and sigma = 0 keep the value; sigma
+    = 0 contracts the deviation from the mean by rho per step (k steps:
+    mean + rho^k (u0 - mean)); rho = 0 gives mean + sigma eps; the result is
+    clamped to [0, 0.99]."""
+    rng = np.random.default_rng(3)
+    mean = rng.uniform(0.1, 0.8, 50)
+    u = rng.uniform(0.0, 0.9, 50)
+    eps = rng.standard_normal(50)
+    np.testing.assert_allclose(oracle.ar1_step(u, mean, eps, 1.0, 0.0), u, rtol=0, atol=2e-16)
+    x = u.copy()
+    for _ in range(5):
+        x = oracle.ar1_step(x, mean, eps, 0.5, 0.0)
+    np.testing.assert_allclose(x, mean + 0.5 ** 5 * (u - mean), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(oracle.ar1_step(u, mean, eps, 0.0, 0.05),
+                               np.clip(mean + 0.05 * eps, 0.0, 0.99), rtol=0, atol=1e-16)
+    hi = oracle.ar1_step(np.full(3, 0.98), np.full(3, 0.98), np.array([10.0, -100.0, 0.0]), 0.9, 0.05)
+    assert hi.tolist() == [0.99, 0.0, 0.98]
+
+
+def test_link_noise_closed_forms():
+    """Lognormal telemetry noise: sigma = 0 or z = 0 leaves the utilisation
+    unchanged; z = 1 multiplies by e^sigma; the result is capped at 0.99;
+    the multiplier's median over many draws is 1."""
+    u = np.array([0.1, 0.3, 0.5, 0.9])
+    z = np.array([1.0, -2.0, 0.5, 3.0])
+    np.testing.assert_array_equal(oracle.link_noise(u, z, 0.0), u)
+    np.testing.assert_array_equal(oracle.link_noise(u, np.zeros(4), 0.4), u)
+    np.testing.assert_allclose(oracle.link_noise(u, np.ones(4), 0.2), np.minimum(u * np.e ** 0.2, 0.99),
+                               rtol=1e-15)
+    assert oracle.link_noise(np.array([0.9]), np.array([3.0]), 0.4)[0] == 0.99
+    zz = np.random.default_rng(4).standard_normal(20001)
+    m = oracle.link_noise(np.full(zz.size, 0.001), zz, 0.4) / 0.001
+    assert abs(np.median(m) - 1.0) < 0.02

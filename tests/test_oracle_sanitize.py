@@ -68,6 +68,12 @@ fl = dict(cap=rng.uniform(1.0, 9.0, L), path_off=poff, path=path, bytes=rng.unif
 rt, nr = oracle.maxmin(fl)
 fin, ev = oracle.flow_sim(fl)
 out["flows"] = dig(rt, fin) + str(nr) + str(ev)
+nd, lf, pd = cfg.cluster.coords()
+pg, dg = cfg.cluster.prefill_gpus(), cfg.cluster.decode_gpus()
+tr, pu = oracle.pair_congestion((nd[pg], lf[pg], pd[pg]), (nd[dg], lf[dg], pd[dg]), links)
+ar = oracle.ar1_step(links["u1"], links["u1"], rng.standard_normal(len(links["u1"])), 0.9, 0.05)
+nz = oracle.link_noise(links["u2"], rng.standard_normal(len(links["u2"])), 0.4)
+out["telemetry"] = dig(tr, pu, ar, nz)
 import os
 if os.environ.get("NETKV_ORACLE_LIB"):   # the checking build and the ASan runtime are the ones mapped
     maps = open("/proc/self/maps").read()

@@ -107,3 +107,66 @@ def test_ar1_stays_in_range_and_starts_at_draw():
     for s in seq:
         for v in s.values():
             assert v.min() >= 0 and v.max() <= 0.99
+
+
+def _coords(cfg):
+    node, leaf, pod = cfg.cluster.coords()
+    pg, dg = cfg.cluster.prefill_gpus(), cfg.cluster.decode_gpus()
+    return (node[pg], leaf[pg], pod[pg]), (node[dg], leaf[dg], pod[dg])
+
+
+@pytest.mark.parametrize("name", ["c0", "c2"])
+def test_generator_congestion_matches_the_oracles_derivation(name):
+    """The snapshots' tier and congestion maps are what the oracle derives
+    from the same link draws (one congestion value per pair from the
+    tier-level links at both ends), bit for bit."""
+    import oracle
+    cfg = W.CONFIGS[name]
+    links = W.draw_links(cfg, 7)
+    tier, util = oracle.pair_congestion(*_coords(cfg), links)
+    np.testing.assert_array_equal(tier, W.pair_tiers(cfg.cluster))
+    np.testing.assert_array_equal(util, W.pair_util(cfg.cluster, links))
+    snap = W.make_snapshot(cfg, 7)
+    np.testing.assert_array_equal(snap["tier_map"].reshape(tier.shape), tier)
+
+
+def test_generator_ar1_matches_the_oracles_step():
+    """The streaming workload's per-batch link utilisations are the oracle's
+    AR(1) steps from the initial draw, with the generator's normal draws
+    (the same seeded stream, links in key order, batch after batch)."""
+    import oracle
+    cfg = W.CONFIGS["c1"]
+    links0 = W.draw_links(cfg, 5)
+    seq = W.ar1_links(cfg, 5, links0, 6)
+    rng = W._rng(5, 51)
+    cur = {k: np.asarray(v, np.float64) for k, v in links0.items()}
+    for t in range(1, 6):
+        nxt = {}
+        for key in sorted(cur):
+            eps = rng.standard_normal(len(cur[key]))
+            nxt[key] = oracle.ar1_step(cur[key], links0[key], eps, cfg.ar1_rho, cfg.ar1_sigma)
+            np.testing.assert_array_equal(nxt[key], seq[t][key])
+        cur = nxt
+
+
+def test_generator_scenarios_match_the_oracles_noise():
+    """The ranking sweep's scenarios are the oracle's lognormal noise on every
+    link (the generator's normal draws), collapsed to pairs as in the
+    snapshot; equal to within one fp32 ulp (the two sides' exp may round
+    differently in the last bit)."""
+    import oracle
+    cfg = W.CONFIGS["c3"]
+    links = W.draw_links(cfg, 9)
+    S = 16
+    util, sig = W.scenario_utils(cfg, 9, links, n_scen=S)
+    rng = W._rng(9, 61)
+    pc, dc = _coords(cfg)
+    for s in range(S):
+        noisy = {}
+        for key in sorted(links):
+            z = rng.standard_normal(len(links[key]))
+            noisy[key] = oracle.link_noise(links[key], z, sig[s])
+        _, u = oracle.pair_congestion(pc, dc, noisy)
+        a = u.reshape(-1).view(np.int32).astype(np.int64)
+        b = util[s].view(np.int32).astype(np.int64)
+        assert np.abs(a - b).max() <= 1
