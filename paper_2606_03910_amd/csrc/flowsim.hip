@@ -52,8 +52,9 @@ struct SimArgs {
     // work: per flow, and per link of every instance (when not in LDS)
     double *remaining, *rate;
     uint8_t *state, *frz;
+    uint32_t *mlist;   // [n_flows] the moving flows of each instance (its own range)
     double *g_rem;
-    uint32_t *g_cnt;
+    uint32_t *g_cnt, *g_lk;
     uint8_t *g_sat;
     uint32_t *err;
 };
@@ -80,6 +81,8 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     __shared__ double l_rem[LDS ? kSimLdsLinks : 1];
     __shared__ uint32_t l_cnt[LDS ? kSimLdsLinks : 1];
     __shared__ uint8_t l_sat[LDS ? kSimLdsLinks : 1];
+    __shared__ uint32_t l_lk[LDS ? kSimLdsLinks : 1];
+    __shared__ uint32_t n_mv, n_lk;
     const uint32_t tid = threadIdx.x, lane = tid % 64, w = tid / 64;
     const uint32_t inst = blockIdx.x;
     const uint32_t L = a.n_links;
@@ -139,7 +142,10 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
         }
         return;
     }
-    // flows wait for their arrival; the clock starts at the first one
+    // flows wait for their arrival; the clock starts at the first one.
+    // Link counts start at 0 and return to 0 at the end of every allocation
+    // (every flow counted on a link is frozen and uncounted again).
+    for (uint32_t l = tid; l < L; l += kSimThreads) cnt[l] = 0;
     double t0 = INFINITY;
     for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
         a.state[f] = kWaiting;
@@ -152,6 +158,8 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     uint64_t left = nf;
     uint64_t events = 0, rounds = 0, moving = 0;
     bool stall = false;
+    uint32_t *mv = a.mlist + f0;   // the moving flows (offsets from f0), rebuilt each pass
+    uint32_t *lk = LDS ? l_lk : a.g_lk + (uint64_t)inst * L;   // the links they cross
     // each pass starts a flow or completes one (or both), so 2 nf + 1 passes
     // end every valid instance
     for (uint64_t pass = 0; left > 0; ++pass) {
@@ -159,7 +167,12 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
             stall = true;
             break;
         }
-        // start the flows that have arrived; the next arrival
+        if (tid == 0) {
+            n_mv = 0;
+            n_lk = 0;
+        }
+        __syncthreads();   // the list counters' previous uses all precede the last barrier
+        // start the flows that have arrived and list the moving ones; the next arrival
         uint32_t na = 0;
         double nx = INFINITY;
         for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
@@ -169,7 +182,10 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
                 st = kMoving;
                 a.state[f] = st;
             }
-            na += st == kMoving ? 1u : 0u;
+            if (st == kMoving) {
+                mv[atomicAdd(&n_mv, 1u)] = (uint32_t)(f - f0);
+                ++na;
+            }
             if (st == kWaiting) nx = dmin(nx, s);
         }
         na = bsum(na);
@@ -178,18 +194,21 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
             t = nx;
             continue;
         }
-        // the max-min fair allocation of the moving flows
-        for (uint32_t l = tid; l < L; l += kSimThreads) {
-            rem[l] = cap[l];
-            cnt[l] = 0;
-        }
-        __syncthreads();
-        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
-            if (a.state[f] != kMoving) continue;
+        // the max-min fair allocation of the moving flows: count them on
+        // their links (a link's first count lists it and resets its capacity)
+        for (uint32_t i = tid; i < na; i += kSimThreads) {
+            const uint64_t f = f0 + mv[i];
             a.frz[f] = kFree;
-            for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) atomicAdd(&cnt[a.path[q]], 1u);
+            for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) {
+                const uint32_t l = a.path[q];
+                if (atomicAdd(&cnt[l], 1u) == 0) {
+                    rem[l] = cap[l];
+                    lk[atomicAdd(&n_lk, 1u)] = l;
+                }
+            }
         }
         __syncthreads();
+        const uint32_t nl = n_lk;
         double level = 0.0;
         uint32_t unfrozen = na;
         for (uint32_t round = 0; unfrozen > 0; ++round) {
@@ -199,13 +218,15 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
             }
             // the largest equal raise every link still allows
             double sh = INFINITY;
-            for (uint32_t l = tid; l < L; l += kSimThreads) {
+            for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                const uint32_t l = lk[i];
                 const uint32_t c = cnt[l];
                 if (c > 0) sh = dmin(sh, rem[l] / (double)c);
             }
             const double inc = bmin(sh);
             // links that the raise fills, and the capacity left on each
-            for (uint32_t l = tid; l < L; l += kSimThreads) {
+            for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                const uint32_t l = lk[i];
                 const uint32_t c = cnt[l];
                 uint8_t full = 0;
                 if (c > 0) {
@@ -221,8 +242,9 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
             __syncthreads();
             // flows crossing a filled link stop at the current level
             uint32_t nfz = 0;
-            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
-                if (a.state[f] != kMoving || a.frz[f] != kFree) continue;
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint64_t f = f0 + mv[i];
+                if (a.frz[f] != kFree) continue;
                 uint8_t hit = 0;
                 for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) hit |= sat[a.path[q]];
                 if (hit) {
@@ -232,8 +254,9 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
                 }
             }
             nfz = bsum(nfz);
-            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
-                if (a.state[f] != kMoving || a.frz[f] != kJustFrozen) continue;
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint64_t f = f0 + mv[i];
+                if (a.frz[f] != kJustFrozen) continue;
                 a.frz[f] = kFrozen;
                 for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) atomicSub(&cnt[a.path[q]], 1u);
             }
@@ -246,13 +269,15 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
         moving += na;
         // the next event: the earliest completion, or the next arrival
         double tc = INFINITY;
-        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads)
-            if (a.state[f] == kMoving) tc = dmin(tc, a.remaining[f] / a.rate[f]);
+        for (uint32_t i = tid; i < na; i += kSimThreads) {
+            const uint64_t f = f0 + mv[i];
+            tc = dmin(tc, a.remaining[f] / a.rate[f]);
+        }
         const double dtc = bmin(tc);
         uint32_t nd = 0;
         if (dtc <= nx - t) {
-            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
-                if (a.state[f] != kMoving) continue;
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint64_t f = f0 + mv[i];
                 const double rm = a.remaining[f], rt = a.rate[f];
                 if (rm / rt == dtc) {
                     a.state[f] = kDone;
@@ -267,8 +292,8 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
             t = t + dtc;
         } else {
             const double dt = nx - t;
-            for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
-                if (a.state[f] != kMoving) continue;
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint64_t f = f0 + mv[i];
                 const double moved = a.rate[f] * dt;
                 const double r = a.remaining[f] - moved;
                 a.remaining[f] = r > 0.0 ? r : 0.0;
@@ -311,8 +336,8 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
     if (hipGetDevice(&prev) != hipSuccess) prev = -1;
     if (prev != dev) (void)hipSetDevice(dev);
     const bool lds = n_links <= kSimLdsLinks;
-    const uint64_t per_flow = align256(8 * n_flows) * 2 + align256(n_flows) * 2;
-    const uint64_t per_link = lds ? 0 : align256(8ull * n_inst * n_links) + align256(4ull * n_inst * n_links) +
+    const uint64_t per_flow = align256(8 * n_flows) * 2 + align256(n_flows) * 2 + align256(4 * n_flows);
+    const uint64_t per_link = lds ? 0 : align256(8ull * n_inst * n_links) + 2 * align256(4ull * n_inst * n_links) +
                                             align256((uint64_t)n_inst * n_links);
     void *buf = nullptr;
     netkv_status st = NETKV_OK;
@@ -342,10 +367,14 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         p += align256(n_flows);
         a.frz = p;
         p += align256(n_flows);
+        a.mlist = (uint32_t *)p;
+        p += align256(4 * n_flows);
         if (!lds) {
             a.g_rem = (double *)p;
             p += align256(8ull * n_inst * n_links);
             a.g_cnt = (uint32_t *)p;
+            p += align256(4ull * n_inst * n_links);
+            a.g_lk = (uint32_t *)p;
             p += align256(4ull * n_inst * n_links);
             a.g_sat = p;
         }
