@@ -210,7 +210,7 @@ def main():
                     help="only time the flow-level transfer simulation: the workload's batch selected "
                          "(k = 1), its transfers simulated on the cluster's fat tree under "
                          "--flow-instances background-load draws")
-    ap.add_argument("--flow-instances", type=int, default=256,
+    ap.add_argument("--flow-instances", type=int, default=1024,
                     help="independent simulation instances per call (background-load draws)")
     ap.add_argument("--flow-window", type=float, default=5.0,
                     help="seconds over which the batch's transfers arrive")
