@@ -18,7 +18,9 @@
 //     derived per call: (seconds per token, constant part) float2 rows per
 //     prefill, and per decode the load term and feasibility limit.
 //
-// Kernels of one selection (netkv_select_batch), in launch order:
+// Kernels of one selection (netkv_select_batch), in launch order (a batch
+// of 2^16 requests or more runs derive_kernel, then lead_holder_kernel and
+// lead_kernel, on a second stream beside the others):
 //   derive_kernel      -- per-call cost factors (Eqs. (3)-(7) split by what
 //                         they depend on).
 //   prep_kernel        -- validate requests, build hash-order keys.
@@ -26,9 +28,11 @@
 //                         small and very large batches).
 //   order_kernel       -- common leading run with the previous position,
 //                         leaders (positions whose next block some decode
-//                         holds), segmented-scan elements, records.
+//                         holds), segmented-scan elements within each tile
+//                         of positions, records.
+//   tile_prefix_kernel -- the tiles' exclusive prefixes (the scan's second
+//                         level).
 //   lead_holder_kernel -- holder values of every leader's blocks.
-//   (rocPRIM segmented scan)
 //   sort kernels       -- stable sort into prefill order, writing the
 //                         scoring records (or rocPRIM's sort and
 //                         assemble_kernel).
@@ -37,13 +41,18 @@
 //                         feasibility and cost (Eqs. (2)-(7)), then the
 //                         group's top-k; one wavefront per (run of requests,
 //                         group of 64*C decodes); optional per-pair outputs.
-//   reduce_kernel      -- merges the groups' keys into each request's top-k.
+//   reduce_kernel      -- merges the groups' keys into each request's top-k
+//                         (not launched when one group covers the pool).
 // Other calls:
-//   sweep_kernel       -- re-scoring under congestion scenarios with the
-//                         prefix lengths reused; lanes over requests.
+//   derive_scen_kernel, sweep_kernel -- re-scoring under congestion
+//                         scenarios from the leader rows; lanes over requests.
+//   tier_inv_kernel    -- Proposition 2's tier-ranking inversion counts.
 //   sequential kernels -- Algorithm 1's per-request in-flight increments,
-//                         one workgroup per prefill instance.
+//                         one workgroup per prefill instance, from the
+//                         leader rows.
+//   selection_bytes_kernel -- the selections' transfer sizes (Eq. (2)).
 //   owner / classify / index_insert / index_value -- build the holder index.
+// The flow-level transfer simulation is in flowsim.hip.
 //   commit kernels     -- between-batch counter / queue / memory update.
 #include <hip/hip_runtime.h>
 #include <rocprim/device/device_radix_sort.hpp>
@@ -426,8 +435,8 @@ struct Order {
 };
 
 // Validate each request and build its sort key, one thread per request.
-// A request of more than max_blocks blocks is invalid (calls that keep
-// per-pair prefix lengths in 16 bits pass 65535).  A block hash 0 needs no
+// A request of more than max_blocks blocks is invalid (every call passes
+// 2^32 - 1: runs of any length are scored).  A block hash 0 needs no
 // check: no resident set holds it (cache loads reject it), so it is a miss
 // on every decode, as the prefix definition gives.  vals (the input
 // positions, for rocPRIM's sort) may be null.  Thread 0 clears the
