@@ -543,45 +543,68 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
             crec[i] = Cold{r};
         }
     }
+    // this position's run, and the previous position's: from the lanes G
+    // below (one wavefront holds kWave / G consecutive positions), or, for
+    // the wavefront's first position, loaded
+    uint64_t a = 0, nr = 0;
     if (valid) {
-        const uint64_t a = rq.off[r];
-        const uint64_t nr = rq.off[r + 1] - a;
-        uint64_t l = 0;
-        // keys that differ in their first-block hash bits have different
-        // first blocks: nothing in common
-        if (i > 0 && reuse && (sorted_keys[i] >> kKeyLenBits) == (sorted_keys[i - 1] >> kKeyLenBits)) {
-            const uint32_t q = perm[i - 1];
-            const uint64_t b = rq.off[q];
-            const uint64_t nq = rq.off[q + 1] - b;
-            const uint64_t m = nr < nq ? nr : nq;
-            l = m;
-            // each lane compares U consecutive blocks per step, their loads
-            // issued together; the first differing block is the lowest
-            // lane's first stop
-            constexpr uint32_t U = 2;
-            for (uint64_t base = 0; base < m; base += (uint64_t)G * U) {
-                const uint64_t x0 = base + (uint64_t)sub * U;
-                uint64_t hr[U], hq[U];
+        a = rq.off[r];
+        nr = rq.off[r + 1] - a;
+    }
+    const uint32_t pg = lane / G;
+    const uint32_t key = valid ? sorted_keys[i] : kKeyInvalid;
+    uint32_t kq = (uint32_t)__shfl_up((int)key, G, kWave);
+    uint64_t b = shfl_up_u64(a, G), nq = shfl_up_u64(nr, G);
+    if (pg == 0 && valid && i > 0) {
+        kq = sorted_keys[i - 1];
+        const uint32_t q = perm[i - 1];
+        b = rq.off[q];
+        nq = rq.off[q + 1] - b;
+    }
+    // keys that differ in their first-block hash bits have different first
+    // blocks: nothing in common
+    const bool cmp = valid && i > 0 && reuse && (key >> kKeyLenBits) == (kq >> kKeyLenBits);
+    const uint64_t m = cmp ? (nr < nq ? nr : nq) : 0;
+    uint64_t l = m;
+    {
+        // Lock-step over the wavefront: each lane loads U consecutive blocks
+        // of its own run per step (their loads issued together) while its
+        // position or the next one is still comparing, and takes the
+        // previous position's blocks from the lanes G below; the first
+        // differing block is the lowest lane's first stop.
+        constexpr uint32_t U = 2;
+        bool act = m > 0;
+        for (uint64_t base = 0;; base += (uint64_t)G * U) {
+            if (!__any(act)) break;
+            const bool act_next = (bool)__shfl_down((int)act, G, kWave) && pg + 1 < (uint32_t)kWave / G;
+            const bool need = act || act_next;
+            const uint64_t x0 = base + (uint64_t)sub * U;
+            uint64_t hr[U], hq[U];
 #pragma unroll
-                for (uint32_t u = 0; u < U; ++u) {
-                    const bool in = x0 + u < m;
-                    hr[u] = in ? rq.hashes[a + x0 + u] : 0ull;
-                    hq[u] = in ? rq.hashes[b + x0 + u] : 1ull;
-                }
-                uint32_t ls = U;   // this lane's first stop (U: none)
+            for (uint32_t u = 0; u < U; ++u) hr[u] = (need && x0 + u < nr) ? rq.hashes[a + x0 + u] : 0ull;
 #pragma unroll
-                for (int u = (int)U - 1; u >= 0; --u)
-                    if (hr[u] != hq[u]) ls = (uint32_t)u;
-                const uint32_t bits = (uint32_t)(__ballot(ls < U) >> seg0) & (uint32_t)((1ull << G) - 1);
-                if (bits) {
-                    const uint32_t fl = (uint32_t)__builtin_ctz(bits);
-                    const uint32_t lsf = (uint32_t)__shfl((int)ls, (int)(seg0 + fl), kWave);
-                    const uint64_t first = base + (uint64_t)fl * U + lsf;
-                    l = first < m ? first : m;
-                    break;
-                }
+            for (uint32_t u = 0; u < U; ++u) hq[u] = shfl_up_u64(hr[u], G);
+            if (pg == 0) {
+#pragma unroll
+                for (uint32_t u = 0; u < U; ++u) hq[u] = (act && x0 + u < m) ? rq.hashes[b + x0 + u] : 1ull;
             }
+            uint32_t ls = U;   // this lane's first stop (U: none); blocks at m and beyond stop
+#pragma unroll
+            for (int u = (int)U - 1; u >= 0; --u)
+                if (x0 + u >= m || hr[u] != hq[u]) ls = (uint32_t)u;
+            const uint32_t bits =
+                (uint32_t)(__ballot(act && ls < U) >> seg0) & (uint32_t)((1ull << G) - 1);
+            if (act && bits) {
+                const uint32_t fl = (uint32_t)__builtin_ctz(bits);
+                const uint32_t lsf = (uint32_t)__shfl((int)ls, (int)(seg0 + fl), kWave);
+                const uint64_t first = base + (uint64_t)fl * U + lsf;
+                l = first < m ? first : m;
+                act = false;
+            }
+            if (base + (uint64_t)G * U >= m) act = false;
         }
+    }
+    if (valid) {
         if (sub == 0) {
             // a leader if some decode holds block L
             const uint32_t vl = l < nr ? holder_lane(t, rq.hashes[a + l]) : kNoHolder;
