@@ -2396,9 +2396,8 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, Table t, R
     float n_tier[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) n_tier[q] = (float)s.n_inflight[q * s.P + p];
-    uint32_t tmask = 0, big = 0;
-    float sk[MAXC], lk[MAXC];
-    uint32_t xk[MAXC];
+    uint32_t tmask = 0;
+    float sk[MAXC], lk[MAXC], xm[MAXC];
     // the factors, one decode at a time through LDS (keeps the divisions'
     // temporaries out of the register budget)
 #pragma unroll 1
@@ -2418,9 +2417,11 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, Table t, R
         const uint32_t dd = ok ? d : 0;
         sk[k] = __uint_as_float(stage[k * T + threadIdx.x]);
         lk[k] = tier_latency(s, (tmask >> (2 * k)) & 3u) + s.dbase[dd];
-        const uint64_t xl = ok ? s.dxlim[dd] : 0;   // 0: never feasible, so never chosen
-        xk[k] = xl > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)xl;
-        big |= (xl > 0xFFFFFFFFull ? 1u : 0u) << k;
+        // the largest feasible token count, as fp32 (exact: capped at 2^24,
+        // beyond every count of the fp32 path); -1 when nothing is feasible
+        // (and for decodes past D, never chosen)
+        const uint64_t xl = ok ? s.dxlim[dd] : 0;
+        xm[k] = xl == 0 ? -1.0f : (float)(xl - 1 < kExactTok ? xl - 1 : (uint64_t)kExactTok);
     }
     // stage chunk c (positions i0 + c*T ...) of the chain's records in LDS
     auto fill = [&](uint32_t c) {
@@ -2479,19 +2480,37 @@ __global__ __launch_bounds__(T) void sequential_cached_kernel(Snap s, Table t, R
     };
     // score the buffered request, choose, count the choice
     auto step = [&](uint32_t i, const SeqBuf<MAXC> &b) {
-        uint32_t lb = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
+        // the lane's least cost bits and the k of its decode: from the leader
+        // row in fp32 (token counts below 2^24 are exact, as in the scoring
+        // kernel), or for a request matched on its own in integers
+        uint32_t lb = 0xFFFFFFFFu, kf = 0;
+        if (!b.own) {
+            const float lenf = (float)b.len;
 #pragma unroll
-        for (int k = 0; k < MAXC; ++k) {
-            const uint32_t lam = b.own ? b.raw[k] : (uint32_t)__uint_as_float(min(b.raw[k], b.lams));
-            const uint32_t x = b.len - lam;
-            if (x < xk[k] || ((big >> k) & 1u)) {
-                const uint32_t cbits = __float_as_uint(fmaf((float)x, sk[k], lk[k]));
-                if (cbits < lb) {   // d grows with k: the first strict minimum wins ties
-                    lb = cbits;
-                    ld = ((threadIdx.x + T * k) << 2) | ((tmask >> (2 * k)) & 3u);
+            for (int k = 0; k < MAXC; ++k) {
+                const float x = lenf - __uint_as_float(min(b.raw[k], b.lams));
+                const uint32_t c = __float_as_uint(fmaf(x, sk[k], lk[k]));
+                if (x <= xm[k] && c < lb) {   // d grows with k: the first strict minimum wins ties
+                    lb = c;
+                    kf = (uint32_t)k;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < MAXC; ++k) {
+                const uint32_t d = threadIdx.x + T * k;
+                const uint32_t x = b.len - b.raw[k];
+                if (d < s.D && (uint64_t)x < s.dxlim[d < s.D ? d : 0]) {
+                    const uint32_t c = __float_as_uint(fmaf((float)x, sk[k], lk[k]));
+                    if (c < lb) {
+                        lb = c;
+                        kf = (uint32_t)k;
+                    }
                 }
             }
         }
+        const uint32_t ld = lb == 0xFFFFFFFFu ? 0xFFFFFFFFu
+                                              : ((threadIdx.x + T * kf) << 2) | ((tmask >> (2 * kf)) & 3u);
         const uint32_t mn = wave_min_u32_dpp(lb);
         const uint32_t dm = wave_min_u32_dpp(lb == mn ? ld : 0xFFFFFFFFu);
         const uint32_t sl = i & 1u;
