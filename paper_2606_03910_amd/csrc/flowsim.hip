@@ -30,8 +30,11 @@
 namespace {
 
 constexpr int kSimThreads = 256;
-constexpr int kSimWaves = kSimThreads / 64;
+constexpr int kWave = 64;
+constexpr int kSimWaves = kSimThreads / kWave;
 constexpr uint32_t kSimLdsLinks = 2048;   // instances with at most this many links keep them in LDS
+constexpr uint32_t kPathRegs = 6;         // path links a wavefront-path lane keeps in registers
+constexpr uint32_t kScanUnroll = 4;       // flows per thread whose state the arrival scan loads at once
 
 // flow states
 constexpr uint8_t kWaiting = 0, kMoving = 1, kDone = 2;
@@ -73,6 +76,133 @@ __device__ inline uint32_t wave_sum_u32(uint32_t v) {
     return v;
 }
 
+// What the wavefront path of one pass hands to the workgroup.
+struct WavePassOut {
+    double t;          // the clock after the event
+    uint32_t rounds;   // filling rounds of the allocation
+    uint32_t done;     // flows completed at the event
+    uint32_t stall;    // the round bound was reached
+};
+
+// Ordering of one wavefront's LDS and memory accesses between the phases
+// of a filling round (lanes read what other lanes of the wavefront wrote).
+__device__ inline void wave_phase() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup"); }
+
+// One pass with at most one wavefront of moving flows (lane i holds the
+// moving flow mv[i]): the max-min fair allocation by progressive filling
+// and the next event, in exactly the operations of the workgroup path.
+// Called by wavefront 0 only; lane 0 writes the results to `out`.
+__device__ void wave_pass(const SimArgs &a, uint64_t f0, const uint32_t *mv, const uint32_t *lk, double *rem,
+                          uint32_t *cnt, uint8_t *sat, const double *cap, uint32_t na, uint32_t nl, double nx,
+                          double t, uint32_t lane, WavePassOut &out) {
+#pragma clang fp contract(off)
+    (void)cap;
+    const bool mine = lane < na;
+    const uint64_t f = mine ? f0 + mv[lane] : 0;
+    const uint64_t p0 = mine ? a.path_off[f] : 0, p1 = mine ? a.path_off[f + 1] : 0;
+    // the flow's first kPathRegs links in registers (a fat-tree path has at
+    // most 6); longer paths read the rest from memory
+    const uint32_t plen = (uint32_t)(p1 - p0);
+    uint32_t pl[kPathRegs];
+#pragma unroll
+    for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = u < plen ? a.path[p0 + u] : 0u;
+    bool frozen = !mine;
+    double level = 0.0;
+    uint32_t rd = 0, stl = 0;
+    double rt = 0.0;
+    for (;;) {
+        if (!__any(!frozen)) break;
+        if (rd > na) {   // every round freezes at least one flow
+            stl = 1;
+            break;
+        }
+        // the largest equal raise every link still allows
+        double sh = INFINITY;
+        for (uint32_t i = lane; i < nl; i += kWave) {
+            const uint32_t l = lk[i];
+            const uint32_t c = cnt[l];
+            if (c > 0) sh = dmin(sh, rem[l] / (double)c);
+        }
+        const double inc = wave_min_f64(sh);
+        // links that the raise fills, and the capacity left on each
+        for (uint32_t i = lane; i < nl; i += kWave) {
+            const uint32_t l = lk[i];
+            const uint32_t c = cnt[l];
+            uint8_t full = 0;
+            if (c > 0) {
+                const double r = rem[l];
+                full = r / (double)c == inc ? 1 : 0;
+                const double used = inc * (double)c;
+                const double lf = r - used;
+                rem[l] = lf > 0.0 ? lf : 0.0;
+            }
+            sat[l] = full;
+        }
+        level = level + inc;
+        wave_phase();
+        // flows crossing a filled link stop at the current level
+        bool just = false;
+        if (!frozen) {
+            uint8_t hit = 0;
+#pragma unroll
+            for (uint32_t u = 0; u < kPathRegs; ++u)
+                if (u < plen) hit |= sat[pl[u]];
+            for (uint64_t q = p0 + kPathRegs; q < p1; ++q) hit |= sat[a.path[q]];
+            if (hit) {
+                just = true;
+                frozen = true;
+                rt = level;
+                a.rate[f] = level;
+            }
+        }
+        wave_phase();
+        if (just) {
+#pragma unroll
+            for (uint32_t u = 0; u < kPathRegs; ++u)
+                if (u < plen) atomicSub(&cnt[pl[u]], 1u);
+            for (uint64_t q = p0 + kPathRegs; q < p1; ++q) atomicSub(&cnt[a.path[q]], 1u);
+        }
+        wave_phase();
+        ++rd;
+    }
+    double tn = t;
+    uint32_t nd = 0;
+    if (!stl) {
+        // the next event: the earliest completion, or the next arrival
+        const double rm = mine ? a.remaining[f] : 0.0;
+        const double dtc = wave_min_f64(mine ? rm / rt : INFINITY);
+        if (dtc <= nx - t) {
+            if (mine) {
+                if (rm / rt == dtc) {
+                    a.state[f] = kDone;
+                    a.finish[f] = t + dtc;
+                    nd = 1;
+                } else {
+                    const double moved = rt * dtc;
+                    const double r = rm - moved;
+                    a.remaining[f] = r > 0.0 ? r : 0.0;
+                }
+            }
+            tn = t + dtc;
+        } else {
+            const double dt = nx - t;
+            if (mine) {
+                const double moved = rt * dt;
+                const double r = rm - moved;
+                a.remaining[f] = r > 0.0 ? r : 0.0;
+            }
+            tn = nx;
+        }
+    }
+    nd = wave_sum_u32(nd);
+    if (lane == 0) {
+        out.t = tn;
+        out.rounds = rd;
+        out.done = nd;
+        out.stall = stl;
+    }
+}
+
 template <bool LDS>
 __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
 #pragma clang fp contract(off)
@@ -83,6 +213,7 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     __shared__ uint8_t l_sat[LDS ? kSimLdsLinks : 1];
     __shared__ uint32_t l_lk[LDS ? kSimLdsLinks : 1];
     __shared__ uint32_t n_mv, n_lk;
+    __shared__ WavePassOut s_out;
     const uint32_t tid = threadIdx.x, lane = tid % 64, w = tid / 64;
     const uint32_t inst = blockIdx.x;
     const uint32_t L = a.n_links;
@@ -175,18 +306,30 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
         // start the flows that have arrived and list the moving ones; the next arrival
         uint32_t na = 0;
         double nx = INFINITY;
-        for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
-            uint8_t st = a.state[f];
-            const double s = a.start[f];
-            if (st == kWaiting && s <= t) {
-                st = kMoving;
-                a.state[f] = st;
+        // kScanUnroll flows per thread at a time, their loads issued together
+        for (uint64_t fb = f0 + tid; fb < f1; fb += (uint64_t)kScanUnroll * kSimThreads) {
+            uint8_t sts[kScanUnroll];
+            double sv[kScanUnroll];
+#pragma unroll
+            for (uint32_t u = 0; u < kScanUnroll; ++u) {
+                const uint64_t f = fb + (uint64_t)u * kSimThreads;
+                sts[u] = f < f1 ? a.state[f] : kDone;
+                sv[u] = f < f1 ? a.start[f] : 0.0;
             }
-            if (st == kMoving) {
-                mv[atomicAdd(&n_mv, 1u)] = (uint32_t)(f - f0);
-                ++na;
+#pragma unroll
+            for (uint32_t u = 0; u < kScanUnroll; ++u) {
+                const uint64_t f = fb + (uint64_t)u * kSimThreads;
+                uint8_t st = sts[u];
+                if (st == kWaiting && sv[u] <= t) {
+                    st = kMoving;
+                    a.state[f] = st;
+                }
+                if (st == kMoving) {
+                    mv[atomicAdd(&n_mv, 1u)] = (uint32_t)(f - f0);
+                    ++na;
+                }
+                if (st == kWaiting) nx = dmin(nx, sv[u]);
             }
-            if (st == kWaiting) nx = dmin(nx, s);
         }
         na = bsum(na);
         nx = bmin(nx);
@@ -209,6 +352,23 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
         }
         __syncthreads();
         const uint32_t nl = n_lk;
+        if (na <= (uint32_t)kWave) {
+            // few moving flows: one wavefront runs the allocation and the
+            // event (a flow per lane; wavefront reductions, no barriers) with
+            // the same operations as the workgroup path below
+            if (w == 0) wave_pass(a, f0, mv, lk, rem, cnt, sat, cap, na, nl, nx, t, lane, s_out);
+            __syncthreads();
+            t = s_out.t;
+            rounds += s_out.rounds;
+            if (s_out.stall) {
+                stall = true;
+                break;
+            }
+            ++events;
+            moving += na;
+            left -= s_out.done;
+            continue;   // s_out is written again only after the next pass's first barrier
+        }
         double level = 0.0;
         uint32_t unfrozen = na;
         for (uint32_t round = 0; unfrozen > 0; ++round) {
