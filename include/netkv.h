@@ -166,9 +166,13 @@ typedef struct {
  * (1 <= k <= 8) feasible decodes of lowest cost in ascending (score, index)
  * order (the argmin of Algorithm 1 generalised to top-k); fewer than k
  * feasible decodes are padded with index -1 and score +inf (Algorithm 1
- * rejects a request with no feasible decode).  out_idx, out_score: [n_req * k] DEVICE arrays.  `pairs` may be
- * NULL.  Asynchronous on `stream`: inputs must stay valid and outputs are
- * defined once the stream completes.  Allocates only when a batch is
+ * rejects a request with no feasible decode).  out_idx, out_score:
+ * [n_req * k] DEVICE arrays.  `pairs` may be NULL.  Asynchronous on
+ * `stream`: inputs must stay valid and outputs are defined once the stream
+ * completes.  A batch of 2^16 requests or more also runs work on a second
+ * stream of the handle, forked from `stream` and joined back to it by
+ * events within the call, so ordering on `stream` (and a graph capture of
+ * it) covers all of it.  Allocates only when a batch is
  * larger than the handle's work buffers hold -- every earlier batch's, or
  * what netkv_reserve sized them for -- and then grows them (about
  * 100 + 8*K*ceil(D/(64*C)) bytes per request, K the next power of two >= k
@@ -420,8 +424,10 @@ netkv_status netkv_selection_bytes(netkv_handle h, const netkv_requests_t *req, 
  * progress summed over all of them.  All arrays DEVICE.  Asynchronous.  An instance with an invalid flow or capacity
  * gets finish = NaN for all its flows and is reported by netkv_sync_errors
  * (as is one that reached an iteration bound, which valid input never
- * does).  Grows a work buffer of the handle to 13 B per link and instance
- * plus 18 B per flow, rounded up.  EINVAL: NULL arrays, n_links = 0. */
+ * does).  Grows a work buffer of the handle to 22 B per flow, plus, for
+ * more than 2,048 links (whose state then lives in device memory instead
+ * of LDS), 17 B per link and instance.  EINVAL: NULL arrays, n_links = 0,
+ * n_inst >= 2^31. */
 netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t n_links, const double *cap,
                             const uint64_t *flow_off, uint64_t n_flows, const uint64_t *path_off,
                             const uint32_t *path, uint64_t n_path, const double *bytes, const double *start,
