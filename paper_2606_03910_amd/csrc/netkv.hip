@@ -786,8 +786,11 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
 // ---------------------------------------------------------------- batch sorts
 //
 // Stable LSD radix sort for the batch orders (batches of kSortMinN + 1 to
-// kSortMaxN): tiles of kSortTile positions, one workgroup each, in passes
-// of at most kSortMaxBits digit bits.  A pass takes three kernels:
+// kSortMaxN): tiles of TILE positions (sort_tile: 1,024 up to
+// kSortSmallTileN positions, so that a batch of a few hundred thousand
+// still spreads over every CU, else 4,096, whose digits leave in longer
+// runs), one workgroup each, in passes of at most kSortMaxBits digit bits.
+// A pass takes three kernels:
 // sort_count_kernel counts each tile's digits into cnt[tile][digit];
 // sort_colscan_kernel turns every digit's column into exclusive offsets
 // over the tiles (in place) and writes the digit totals;
@@ -796,10 +799,9 @@ __global__ __launch_bounds__(256) void assemble_kernel(uint32_t n_req, uint32_t 
 // them in LDS in output order and writes them out in that order, so that
 // the elements of one digit leave as a contiguous run.  Equal keys keep
 // their order (stable), which the prefill order relies on.
-constexpr uint32_t kSortTile = 4096;
-constexpr uint32_t kSortPer = kSortTile / kBlock;                          // positions per thread
-constexpr uint32_t kSortQuarter = kSortTile / kWavesPerBlock;              // positions per wavefront
-constexpr uint32_t kSortSteps = kSortQuarter / kWave;                      // 64-position steps of a wavefront
+constexpr uint32_t kSortTile = 4096;           // the large tile
+constexpr uint32_t kSortSmallTile = 1024;      // the small tile
+constexpr uint64_t kSortSmallTileN = 1ull << 19;   // largest batch sorted in small tiles (512 of them)
 constexpr uint32_t kSortMaxBits = 11;   // widest pass: the prefill order of up to 2,047 prefills in one
 constexpr uint32_t kSortMaxBins = 1u << kSortMaxBits;
 constexpr uint32_t kSortPassBits = 8;   // passes of the hash order and the general pair sort (faster per bit)
@@ -810,23 +812,28 @@ constexpr uint64_t kSortMinN = 1ull << 16;   // smaller batches: rocPRIM (fewer 
 constexpr uint64_t kForkMinN = 1ull << 16;   // batches from which a selection forks its second stream
 static_assert(kSortBinsPer * kBlock == kSortMaxBins, "digits split evenly over the threads");
 
+// Tile size of the batch sorts for n positions.
+inline uint32_t sort_tile(uint64_t n) { return n <= kSortSmallTileN ? kSortSmallTile : kSortTile; }
+
+template <uint32_t TILE>
 __global__ __launch_bounds__(kBlock) void sort_count_kernel(const uint32_t *__restrict__ keys, uint32_t n,
                                                             uint32_t shift, uint32_t bits,
                                                             uint32_t *__restrict__ cnt) {
+    constexpr uint32_t kPer = TILE / kBlock;   // positions per thread
     __shared__ uint32_t h[kSortMaxBins];
     const uint32_t bins = 1u << bits, mask = bins - 1;
     const uint32_t tid = threadIdx.x;
     for (uint32_t b = tid; b < bins; b += kBlock) h[b] = 0;
     __syncthreads();
-    const uint64_t e0 = (uint64_t)blockIdx.x * kSortTile + tid;
-    uint32_t kr[kSortPer];   // the thread's keys, all loads issued first
+    const uint64_t e0 = (uint64_t)blockIdx.x * TILE + tid;
+    uint32_t kr[kPer];   // the thread's keys, all loads issued first
 #pragma unroll
-    for (uint32_t x = 0; x < kSortPer; ++x) {
+    for (uint32_t x = 0; x < kPer; ++x) {
         const uint64_t e = e0 + (uint64_t)x * kBlock;
         kr[x] = e < n ? keys[e] : 0u;
     }
 #pragma unroll
-    for (uint32_t x = 0; x < kSortPer; ++x)
+    for (uint32_t x = 0; x < kPer; ++x)
         if (e0 + (uint64_t)x * kBlock < n) atomicAdd(h + ((kr[x] >> shift) & mask), 1u);
     __syncthreads();
     for (uint32_t b = tid; b < bins; b += kBlock) cnt[(uint64_t)blockIdx.x * bins + b] = h[b];
@@ -849,6 +856,7 @@ __device__ inline uint32_t wave_incl_scan(uint32_t v) {
 // the sums.
 constexpr uint32_t kColPer = (uint32_t)(kSortMaxN / kSortTile / kBlock);
 static_assert(kColPer * kBlock * kSortTile == kSortMaxN, "column scan covers the largest batch");
+static_assert(kSortSmallTileN / kSortSmallTile <= (uint64_t)kColPer * kBlock, "and the most small tiles");
 __global__ __launch_bounds__(kBlock) void sort_colscan_kernel(uint32_t *__restrict__ cnt, uint32_t ntile,
                                                               uint32_t bits, uint32_t *__restrict__ tot) {
     __shared__ uint32_t wsum[kWavesPerBlock];
@@ -922,7 +930,7 @@ __device__ inline uint64_t digit_peers(uint32_t d, uint32_t bits, uint64_t valid
 // position) at its output position (and, with hotr, at the request's index
 // in the batch); the kHotPad records past the batch are written too.
 // Otherwise (key, value) pairs go to kout / vout.
-template <bool ASSEMBLE>
+template <bool ASSEMBLE, uint32_t TILE>
 __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__restrict__ kin,
                                                               const uint32_t *__restrict__ vin, uint32_t n,
                                                               uint32_t shift, uint32_t bits,
@@ -935,13 +943,16 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
                                                               const Cold *__restrict__ crec, uint32_t bt,
                                                               uint32_t lstride, uint32_t zrow, Hot *__restrict__ hot,
                                                               Cold *__restrict__ cold, Hot *__restrict__ hotr) {
+    constexpr uint32_t kPer = TILE / kBlock;                  // positions per thread
+    constexpr uint32_t kQuarter = TILE / kWavesPerBlock;      // positions per wavefront
+    constexpr uint32_t kSteps = kQuarter / kWave;             // 64-position steps of a wavefront
     __shared__ uint32_t bb[kSortMaxBins];                     // the tile's first output position per digit
     __shared__ uint32_t hist[kWavesPerBlock][kSortMaxBins];   // per-wavefront counts, then their prefixes
     __shared__ uint32_t toff[kSortMaxBins];                   // first staging slot per digit
-    __shared__ uint32_t sk[kSortTile], sv[kSortTile];         // keys and values in output order
+    __shared__ uint32_t sk[TILE], sv[TILE];                   // keys and values in output order
     const uint32_t bins = 1u << bits, mask = bins - 1;
     const uint32_t tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
-    const uint64_t t0 = (uint64_t)blockIdx.x * kSortTile;
+    const uint64_t t0 = (uint64_t)blockIdx.x * TILE;
     for (uint32_t b = tid; b < bins; b += kBlock) bb[b] = tot[b];
     for (uint32_t b = lane; b < bins; b += kWave) hist[w][b] = 0;
     __syncthreads();
@@ -949,10 +960,10 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
     for (uint32_t b = tid; b < bins; b += kBlock) bb[b] += cnt[(uint64_t)blockIdx.x * bins + b];
     if (ASSEMBLE && blockIdx.x == 0 && tid < kHotPad) hot[(uint64_t)n + tid] = Hot{0, zrow, 0, 0};
     // this wavefront's quarter of the tile: keys and values, loads first
-    const uint64_t e0 = t0 + (uint64_t)w * kSortQuarter + lane;
-    uint32_t kr[kSortSteps], vr[kSortSteps], rk[kSortSteps];
+    const uint64_t e0 = t0 + (uint64_t)w * kQuarter + lane;
+    uint32_t kr[kSteps], vr[kSteps], rk[kSteps];
 #pragma unroll
-    for (uint32_t x = 0; x < kSortSteps; ++x) {
+    for (uint32_t x = 0; x < kSteps; ++x) {
         const uint64_t e = e0 + (uint64_t)x * kWave;
         kr[x] = e < n ? kin[e] : 0u;
         vr[x] = e < n ? (vin ? vin[e] : (uint32_t)e) : 0u;
@@ -960,7 +971,7 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
     __syncthreads();
     // rank within the wavefront's quarter, step by step
 #pragma unroll
-    for (uint32_t x = 0; x < kSortSteps; ++x) {
+    for (uint32_t x = 0; x < kSteps; ++x) {
         const bool valid = e0 + (uint64_t)x * kWave < n;
         const uint32_t d = (kr[x] >> shift) & mask;
         const uint64_t peers = digit_peers(d, bits, __builtin_amdgcn_ballot_w64(valid));
@@ -984,7 +995,7 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
     lds_exclusive_scan(toff, bins);   // the digits' first staging slots
     // stage in output order
 #pragma unroll
-    for (uint32_t x = 0; x < kSortSteps; ++x) {
+    for (uint32_t x = 0; x < kSteps; ++x) {
         if (e0 + (uint64_t)x * kWave < n) {
             const uint32_t d = (kr[x] >> shift) & mask;
             const uint32_t pos = toff[d] + hist[w][d] + rk[x];
@@ -994,9 +1005,9 @@ __global__ __launch_bounds__(kBlock) void sort_scatter_kernel(const uint32_t *__
     }
     __syncthreads();
     // write out in output order: one digit's elements are consecutive
-    const uint32_t nt = n - t0 < (uint64_t)kSortTile ? (uint32_t)(n - t0) : kSortTile;
+    const uint32_t nt = n - t0 < (uint64_t)TILE ? (uint32_t)(n - t0) : TILE;
 #pragma unroll
-    for (uint32_t x = 0; x < kSortPer; ++x) {
+    for (uint32_t x = 0; x < kPer; ++x) {
         const uint32_t j = x * kBlock + tid;
         if (j < nt) {
             const uint32_t k = sk[j];
@@ -2907,7 +2918,10 @@ netkv_status ensure_scratch(netkv_handle h, Scratch &sc, uint64_t R, uint64_t pa
         if (R > kSortMinN) {
             // the own batch sorts run for kSortMinN < n <= kSortMaxN
             const uint64_t n = std::min<uint64_t>(R, kSortMaxN);
-            const uint64_t ntile = (n + kSortTile - 1) / kSortTile;
+            // the most tiles of any batch up to n: small tiles up to
+            // kSortSmallTileN, large beyond
+            const uint64_t ns = std::min<uint64_t>(n, kSortSmallTileN);
+            const uint64_t ntile = std::max((ns + kSortSmallTile - 1) / kSortSmallTile, (n + kSortTile - 1) / kSortTile);
             if (dalloc(sc.sort_cnt, ntile * kSortMaxBins) != hipSuccess ||
                 dalloc(sc.sort_tot, kSortMaxBins) != hipSuccess || dalloc(sc.keys_tmp, n) != hipSuccess ||
                 dalloc(sc.vals_tmp, n) != hipSuccess)
@@ -2957,13 +2971,24 @@ hipError_t sort_pass(netkv_handle h, Scratch &sc, const uint32_t *kin, const uin
                      const uint64_t *seg, const uint64_t *tpre, const Cold *crec, uint32_t lstride, uint32_t zrow,
                      Hot *hot, Cold *cold, Hot *hotr, hipStream_t st) {
     if (n == 0) return hipSuccess;
-    const uint32_t ntile = (n + kSortTile - 1) / kSortTile;   // <= kColPer * kBlock (n <= kSortMaxN)
-    hipLaunchKernelGGL(sort_count_kernel, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits, sc.sort_cnt);
+    const uint32_t tile = sort_tile(n);
+    const uint32_t ntile = (n + tile - 1) / tile;   // <= kColPer * kBlock (n <= kSortMaxN)
+    if (tile == kSortSmallTile)
+        hipLaunchKernelGGL(sort_count_kernel<kSortSmallTile>, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits,
+                           sc.sort_cnt);
+    else
+        hipLaunchKernelGGL(sort_count_kernel<kSortTile>, dim3(ntile), dim3(kBlock), 0, st, kin, n, shift, bits,
+                           sc.sort_cnt);
     hipLaunchKernelGGL(sort_colscan_kernel, dim3(1u << bits), dim3(kBlock), 0, st, sc.sort_cnt, ntile, bits,
                        sc.sort_tot);
-    hipLaunchKernelGGL(sort_scatter_kernel<ASSEMBLE>, dim3(ntile), dim3(kBlock), 0, st, kin, vin, n, shift, bits,
-                       (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout, vout, hrec, seg, tpre,
-                       crec, h->block_tokens, lstride, zrow, hot, cold, hotr);
+    if (tile == kSortSmallTile)
+        hipLaunchKernelGGL((sort_scatter_kernel<ASSEMBLE, kSortSmallTile>), dim3(ntile), dim3(kBlock), 0, st, kin,
+                           vin, n, shift, bits, (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout,
+                           vout, hrec, seg, tpre, crec, h->block_tokens, lstride, zrow, hot, cold, hotr);
+    else
+        hipLaunchKernelGGL((sort_scatter_kernel<ASSEMBLE, kSortTile>), dim3(ntile), dim3(kBlock), 0, st, kin, vin,
+                           n, shift, bits, (const uint32_t *)sc.sort_cnt, (const uint32_t *)sc.sort_tot, kout, vout,
+                           hrec, seg, tpre, crec, h->block_tokens, lstride, zrow, hot, cold, hotr);
     return hipGetLastError();
 }
 

@@ -156,16 +156,18 @@ def _sentinel_select(nk, sel, req, k):
     return idx, sc
 
 
-def test_batch_sort_path_every_request(nk):
-    """150,000 requests (above the 65,536 where the library's own batch
-    sorts take over, 37 tiles with a ragged last one) on 48 decodes: every
-    request against the oracle."""
-    cfg = W.scaled(W.CONFIGS["c0"], n_requests=150000)
+@pytest.mark.parametrize("n_req", [150000, 530000])
+def test_batch_sort_path_every_request(nk, n_req):
+    """Batches above the 65,536 where the library's own batch sorts take
+    over, on 48 decodes, every request against the oracle: 150,000 requests
+    (147 tiles of 1,024, the last ragged) and 530,000 (just above the 2^19
+    where the sorts switch to tiles of 4,096: 130 tiles, the last ragged)."""
+    cfg = W.scaled(W.CONFIGS["c0"], n_requests=n_req)
     snap = W.make_snapshot(cfg, 21, inflight="random")
     ch = W.prefix_chains(cfg, 21)
     req = W.make_requests(cfg, 21, chains=ch)
     cache = W.make_caches(cfg, 21, chains=ch)
-    _say("own-sort batch: 150,000 x 48")
+    _say(f"own-sort batch: {n_req:,} x 48")
     sel = nk.Selector(0)
     sel.load_snapshot(snap)
     sel.load_cache(cache, 0.5)
