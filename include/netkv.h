@@ -421,13 +421,17 @@ netkv_status netkv_selection_bytes(netkv_handle h, const netkv_requests_t *req, 
  * start[f] (s, finite).  Writes finish[f], its completion time (s), and,
  * if stats is not NULL, stats[3i .. 3i+2] = the instance's allocations
  * computed (one per event), filling rounds over all of them, and flows in
- * progress summed over all of them.  All arrays DEVICE.  Asynchronous.  An instance with an invalid flow or capacity
- * gets finish = NaN for all its flows and is reported by netkv_sync_errors
- * (as is one that reached an iteration bound, which valid input never
- * does).  Grows a work buffer of the handle to 22 B per flow, plus, for
- * more than 2,048 links (whose state then lives in device memory instead
- * of LDS), 17 B per link and instance.  EINVAL: NULL arrays, n_links = 0,
- * n_inst >= 2^31. */
+ * progress summed over all of them.  All arrays DEVICE.  Asynchronous.
+ * An instance with an invalid flow or capacity gets finish = NaN for all
+ * its flows and is reported by netkv_sync_errors (as is one that reached an
+ * iteration bound, which valid input never does); offsets that are not
+ * non-decreasing, or that end past n_flows, make every instance invalid.
+ * Each instance's flows are first sorted by arrival time (rocPRIM's
+ * segmented radix sort).  Grows a work buffer of the handle to 30 B per
+ * flow, 8 B per instance and the sort's temporary storage, plus, for more
+ * than 2,048 links (whose state then lives in device memory instead of
+ * LDS), 17 B per link and instance.  EINVAL: NULL arrays, n_links = 0,
+ * n_inst >= 2^31, n_flows >= 2^32. */
 netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t n_links, const double *cap,
                             const uint64_t *flow_off, uint64_t n_flows, const uint64_t *path_off,
                             const uint32_t *path, uint64_t n_path, const double *bytes, const double *start,

@@ -14,12 +14,17 @@
 // events; the instances of a call are independent (other congestion draws,
 // other batches).  Inside a workgroup, threads take links and flows in
 // strides, and workgroup reductions give the minimum raise, the next event
-// and the counts.  Every quantity is fp64 and every operation is written
+// and the counts.  Before the simulation each instance's flows are sorted
+// by arrival time (rocPRIM's segmented radix sort, which only orders work),
+// so that a pass takes its arrivals from the head of that order and keeps
+// the list of flows in progress from pass to pass: its cost follows the
+// flows in progress, not the instance's size.  Every quantity is fp64 and every operation is written
 // out in order with contraction off, so the results equal those of a
 // sequential implementation of the same steps bit for bit (minima do not
 // depend on the reduction order; link counts are integers).
 
 #include <hip/hip_runtime.h>
+#include <rocprim/device/device_segmented_radix_sort.hpp>
 
 #include <cmath>
 #include <cstdint>
@@ -34,7 +39,6 @@ constexpr int kWave = 64;
 constexpr int kSimWaves = kSimThreads / kWave;
 constexpr uint32_t kSimLdsLinks = 2048;   // instances with at most this many links keep them in LDS
 constexpr uint32_t kPathRegs = 6;         // path links a wavefront-path lane keeps in registers
-constexpr uint32_t kScanUnroll = 4;       // flows per thread whose state the arrival scan loads at once
 
 // flow states
 constexpr uint8_t kWaiting = 0, kMoving = 1, kDone = 2;
@@ -55,7 +59,9 @@ struct SimArgs {
     // work: per flow, and per link of every instance (when not in LDS)
     double *remaining, *rate;
     uint8_t *state, *frz;
-    uint32_t *mlist;   // [n_flows] the moving flows of each instance (its own range)
+    uint32_t *mlist, *mlist2;   // [n_flows] the moving flows of each instance (its own range), in turn
+    const uint32_t *arr;        // [n_flows] each instance's flows (offsets) in order of arrival
+    const uint32_t *bad_off;    // nonzero: flow_off is not a valid partition of the flows
     double *g_rem;
     uint32_t *g_cnt, *g_lk;
     uint8_t *g_sat;
@@ -148,11 +154,10 @@ __device__ void wave_pass(const SimArgs &a, uint64_t f0, const uint32_t *mv, con
             for (uint32_t u = 0; u < kPathRegs; ++u)
                 if (u < plen) hit |= sat[pl[u]];
             for (uint64_t q = p0 + kPathRegs; q < p1; ++q) hit |= sat[a.path[q]];
-            if (hit) {
+            if (hit) {   // (the rate stays in the lane: every allocation sets all rates anew)
                 just = true;
                 frozen = true;
                 rt = level;
-                a.rate[f] = level;
             }
         }
         wave_phase();
@@ -246,9 +251,10 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
         par ^= 1u;
         return m;
     };
-    // the instance's input, checked before any simulation
+    // the instance's input, checked before any simulation (offsets that are
+    // not a partition of the flows invalidate every instance of the call)
     const bool range_ok = f0 <= f1 && f1 <= a.n_flows;
-    uint32_t bad = range_ok ? 0u : 1u;
+    uint32_t bad = range_ok && *a.bad_off == 0 ? 0u : 1u;
     for (uint32_t l = tid; l < L; l += kSimThreads) {
         const double c = cap[l];
         if (!(c > 0.0) || !isfinite(c)) bad = 1;
@@ -277,20 +283,24 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     // Link counts start at 0 and return to 0 at the end of every allocation
     // (every flow counted on a link is frozen and uncounted again).
     for (uint32_t l = tid; l < L; l += kSimThreads) cnt[l] = 0;
-    double t0 = INFINITY;
     for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
         a.state[f] = kWaiting;
         a.frz[f] = kFree;
         a.remaining[f] = a.bytes[f];
-        t0 = dmin(t0, a.start[f]);
     }
-    double t = bmin(t0);
-    const uint64_t nf = f1 - f0;
+    const uint64_t nf = f1 - f0;   // < 2^32 (the call's flows are)
+    const uint32_t *arr = a.arr + f0;
+    // the clock starts at the first arrival
+    double t = nf ? a.start[f0 + arr[0]] : INFINITY;
     uint64_t left = nf;
     uint64_t events = 0, rounds = 0, moving = 0;
     bool stall = false;
-    uint32_t *mv = a.mlist + f0;   // the moving flows (offsets from f0), rebuilt each pass
+    // the moving flows (offsets from f0): the previous pass's list in mv,
+    // this pass's built in mv2, then swapped
+    uint32_t *mv = a.mlist + f0, *mv2 = a.mlist2 + f0;
     uint32_t *lk = LDS ? l_lk : a.g_lk + (uint64_t)inst * L;   // the links they cross
+    uint32_t na = 0;   // flows in mv
+    uint64_t ap = 0;   // arrivals taken: arr[0 .. ap) have started
     // each pass starts a flow or completes one (or both), so 2 nf + 1 passes
     // end every valid instance
     for (uint64_t pass = 0; left > 0; ++pass) {
@@ -303,36 +313,35 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
             n_lk = 0;
         }
         __syncthreads();   // the list counters' previous uses all precede the last barrier
-        // start the flows that have arrived and list the moving ones; the next arrival
-        uint32_t na = 0;
-        double nx = INFINITY;
-        // kScanUnroll flows per thread at a time, their loads issued together
-        for (uint64_t fb = f0 + tid; fb < f1; fb += (uint64_t)kScanUnroll * kSimThreads) {
-            uint8_t sts[kScanUnroll];
-            double sv[kScanUnroll];
-#pragma unroll
-            for (uint32_t u = 0; u < kScanUnroll; ++u) {
-                const uint64_t f = fb + (uint64_t)u * kSimThreads;
-                sts[u] = f < f1 ? a.state[f] : kDone;
-                sv[u] = f < f1 ? a.start[f] : 0.0;
-            }
-#pragma unroll
-            for (uint32_t u = 0; u < kScanUnroll; ++u) {
-                const uint64_t f = fb + (uint64_t)u * kSimThreads;
-                uint8_t st = sts[u];
-                if (st == kWaiting && sv[u] <= t) {
-                    st = kMoving;
-                    a.state[f] = st;
-                }
-                if (st == kMoving) {
-                    mv[atomicAdd(&n_mv, 1u)] = (uint32_t)(f - f0);
-                    ++na;
-                }
-                if (st == kWaiting) nx = dmin(nx, sv[u]);
-            }
+        // this pass's moving flows: the previous list without the flows that
+        // completed, then the flows that have arrived by t (a prefix of the
+        // rest of the arrival order); the next arrival
+        for (uint32_t i = tid; i < na; i += kSimThreads) {
+            const uint32_t o = mv[i];
+            if (a.state[f0 + o] != kDone) mv2[atomicAdd(&n_mv, 1u)] = o;
         }
-        na = bsum(na);
-        nx = bmin(nx);
+        for (;;) {
+            const uint64_t q = ap + tid;
+            uint32_t in = 0;
+            if (q < nf) {
+                const uint32_t o = arr[q];
+                if (a.start[f0 + o] <= t) {
+                    a.state[f0 + o] = kMoving;
+                    mv2[atomicAdd(&n_mv, 1u)] = o;
+                    in = 1;
+                }
+            }
+            const uint32_t c = bsum(in);   // its barrier also orders the list writes before n_mv is read
+            ap += c;
+            if (c < (uint32_t)kSimThreads) break;
+        }
+        const double nx = ap < nf ? a.start[f0 + arr[ap]] : INFINITY;
+        na = n_mv;
+        {
+            uint32_t *x = mv;
+            mv = mv2;
+            mv2 = x;
+        }
         if (na == 0) {
             t = nx;
             continue;
@@ -474,6 +483,49 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     }
 }
 
+// Whether flow_off partitions the call's flows (non-decreasing, ending at
+// most at n_flows): *bad_off = 0 if so, else 1.  One workgroup.
+__global__ __launch_bounds__(kSimThreads) void flow_check_kernel(const uint64_t *__restrict__ flow_off,
+                                                                 uint32_t n_inst, uint64_t n_flows,
+                                                                 uint32_t *__restrict__ bad_off) {
+    __shared__ uint32_t any;
+    if (threadIdx.x == 0) any = 0;
+    __syncthreads();
+    uint32_t b = 0;
+    for (uint32_t i = threadIdx.x; i < n_inst; i += kSimThreads)
+        if (flow_off[i] > flow_off[i + 1] || flow_off[i + 1] > n_flows) b = 1;
+    if (b) atomicOr(&any, 1u);
+    __syncthreads();
+    if (threadIdx.x == 0) *bad_off = any;
+}
+
+// The arrival-order sort's input, one workgroup per instance: each flow's
+// arrival time as a 64-bit key whose unsigned order is that of the times
+// (the sign bit set on non-negative values, all bits inverted on negative
+// ones), its offset in the instance as the value, and the instance's
+// segment (empty for every instance when the offsets are invalid, so that
+// the sort stays inside the flows).
+__global__ __launch_bounds__(kSimThreads) void flow_keys_kernel(const uint64_t *__restrict__ flow_off,
+                                                                const double *__restrict__ start,
+                                                                const uint32_t *__restrict__ bad_off,
+                                                                uint64_t *__restrict__ keys,
+                                                                uint32_t *__restrict__ vals,
+                                                                uint32_t *__restrict__ seg_b,
+                                                                uint32_t *__restrict__ seg_e) {
+    const uint32_t inst = blockIdx.x;
+    const bool ok = *bad_off == 0;
+    const uint64_t f0 = ok ? flow_off[inst] : 0, f1 = ok ? flow_off[inst + 1] : 0;   // < 2^32 when ok
+    if (threadIdx.x == 0) {
+        seg_b[inst] = (uint32_t)f0;
+        seg_e[inst] = (uint32_t)f1;
+    }
+    for (uint64_t f = f0 + threadIdx.x; f < f1; f += kSimThreads) {
+        const uint64_t u = (uint64_t)__double_as_longlong(start[f]);
+        keys[f] = (u >> 63) ? ~u : (u | (1ull << 63));
+        vals[f] = (uint32_t)(f - f0);
+    }
+}
+
 inline uint64_t align256(uint64_t x) { return (x + 255) / 256 * 256; }
 
 }  // namespace
@@ -489,19 +541,34 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
     if (n_inst > 0x7FFFFFFFu) return netkv_internal_fail(h, NETKV_EINVAL, "n_inst must be < 2^31");
     if (!cap || !flow_off || !path_off || (n_flows && (!bytes || !start || !finish)) || (n_path && !path))
         return netkv_internal_fail(h, NETKV_EINVAL, "NULL array");
-    if (n_flows > (1ull << 40) || n_path > (1ull << 40))
-        return netkv_internal_fail(h, NETKV_EINVAL, "n_flows and n_path must be <= 2^40");
+    if (n_flows >= (1ull << 32) || n_path > (1ull << 40))
+        return netkv_internal_fail(h, NETKV_EINVAL, "n_flows must be < 2^32 and n_path <= 2^40");
     const int dev = netkv_internal_device(h);
     int prev = -1;
     if (hipGetDevice(&prev) != hipSuccess) prev = -1;
     if (prev != dev) (void)hipSetDevice(dev);
     const bool lds = n_links <= kSimLdsLinks;
-    const uint64_t per_flow = align256(8 * n_flows) * 2 + align256(n_flows) * 2 + align256(4 * n_flows);
+    hipStream_t s = (hipStream_t)stream;
+    // the arrival-order sort: keys in `remaining`, sorted keys in `rate`,
+    // values in the first moving list, the order itself in `arr` (the
+    // simulation initialises the first three itself)
+    size_t sort_bytes = 0;
+    hipError_t e = hipSuccess;
+    if (n_flows)
+        e = rocprim::segmented_radix_sort_pairs(nullptr, sort_bytes, (const uint64_t *)nullptr, (uint64_t *)nullptr,
+                                                (const uint32_t *)nullptr, (uint32_t *)nullptr, (unsigned)n_flows,
+                                                n_inst, (const uint32_t *)nullptr, (const uint32_t *)nullptr, 0, 64, s);
+    if (e != hipSuccess) {
+        if (prev >= 0 && prev != dev) (void)hipSetDevice(prev);
+        return netkv_internal_fail(h, NETKV_EDEVICE, "arrival sort size query failed");
+    }
+    const uint64_t per_flow = align256(8 * n_flows) * 2 + align256(n_flows) * 2 + align256(4 * n_flows) * 3;
+    const uint64_t per_inst = 2 * align256(4ull * n_inst) + 256 + align256(sort_bytes);
     const uint64_t per_link = lds ? 0 : align256(8ull * n_inst * n_links) + 2 * align256(4ull * n_inst * n_links) +
                                             align256((uint64_t)n_inst * n_links);
     void *buf = nullptr;
     netkv_status st = NETKV_OK;
-    hipError_t e = netkv_internal_flow_buffer(h, per_flow + per_link + 256, &buf);
+    e = netkv_internal_flow_buffer(h, per_flow + per_inst + per_link + 256, &buf);
     if (e != hipSuccess) {
         st = netkv_internal_fail(h, e == hipErrorOutOfMemory ? NETKV_ENOMEM : NETKV_EDEVICE,
                                  "flow simulation work buffer allocation failed");
@@ -529,6 +596,20 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         p += align256(n_flows);
         a.mlist = (uint32_t *)p;
         p += align256(4 * n_flows);
+        a.mlist2 = (uint32_t *)p;
+        p += align256(4 * n_flows);
+        uint32_t *arr = (uint32_t *)p;
+        a.arr = arr;
+        p += align256(4 * n_flows);
+        uint32_t *seg_b = (uint32_t *)p;
+        p += align256(4ull * n_inst);
+        uint32_t *seg_e = (uint32_t *)p;
+        p += align256(4ull * n_inst);
+        uint32_t *bad_off = (uint32_t *)p;
+        a.bad_off = bad_off;
+        p += 256;
+        void *sort_tmp = p;
+        p += align256(sort_bytes);
         if (!lds) {
             a.g_rem = (double *)p;
             p += align256(8ull * n_inst * n_links);
@@ -539,12 +620,20 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
             a.g_sat = p;
         }
         a.err = netkv_internal_errword(h);
-        hipStream_t s = (hipStream_t)stream;
-        if (lds)
+        hipLaunchKernelGGL(flow_check_kernel, dim3(1), dim3(kSimThreads), 0, s, flow_off, n_inst, n_flows, bad_off);
+        if (n_flows) {
+            hipLaunchKernelGGL(flow_keys_kernel, dim3(n_inst), dim3(kSimThreads), 0, s, flow_off, start,
+                               (const uint32_t *)bad_off, (uint64_t *)a.remaining, a.mlist, seg_b, seg_e);
+            size_t tb = sort_bytes;
+            e = rocprim::segmented_radix_sort_pairs(sort_tmp, tb, (const uint64_t *)a.remaining, (uint64_t *)a.rate,
+                                                    (const uint32_t *)a.mlist, arr, (unsigned)n_flows, n_inst,
+                                                    (const uint32_t *)seg_b, (const uint32_t *)seg_e, 0, 64, s);
+        }
+        if (e == hipSuccess && lds)
             hipLaunchKernelGGL(flow_sim_kernel<true>, dim3(n_inst), dim3(kSimThreads), 0, s, a);
-        else
+        else if (e == hipSuccess)
             hipLaunchKernelGGL(flow_sim_kernel<false>, dim3(n_inst), dim3(kSimThreads), 0, s, a);
-        e = hipGetLastError();
+        if (e == hipSuccess) e = hipGetLastError();
         if (e != hipSuccess) st = netkv_internal_fail(h, NETKV_EDEVICE, hipGetErrorString(e));
     }
     if (prev >= 0 && prev != dev) (void)hipSetDevice(prev);

@@ -209,3 +209,28 @@ def test_invalid_instances_are_reported_and_others_unaffected(nk):
         assert np.array_equal(fin[off[i]:off[i + 1]], o_fin) and tuple(ev[i]) == o_st
     sel.sync_errors()   # cleared by the previous report
     sel.close()
+
+
+def test_offsets_that_are_not_a_partition_invalidate_the_call(nk):
+    """Flow offsets that decrease, or end past the call's flows, make every
+    instance of the call invalid (finish times NaN on every instance whose
+    own range lies inside the flows, all counts 0, reported by
+    netkv_sync_errors); the same flows with valid offsets then match the
+    oracle."""
+    _say("flow sim offsets not a partition")
+    good = _flows([1.0, 2.0, 3.0], [[0, 1], [1, 2], [2]], [1.0, 2.0, 3.0], [0.0, 0.1, 0.2])
+    arr, L = _instances([good, good, good])
+    sel = nk.Selector(0)
+    # (offsets, flows covered by an instance whose range is inside the 9 flows)
+    for off, covered in (([0, 3, 1, 9], 9), ([0, 3, 6, 10], 6)):
+        bad = dict(arr, flow_off=np.asarray(off, np.uint64))
+        dev = {k: nk.to_device(v, sel.device) for k, v in bad.items()}
+        fin, st = sel.flow_sim(dev, 3, L)
+        with pytest.raises(nk.NetKVError):
+            sel.sync_errors()
+        assert np.isnan(nk.to_numpy(fin)[:covered]).all(), off
+        assert (nk.to_numpy(st) == 0).all(), off
+    fin, st, arr2 = _run(nk, sel, [good, good, good])
+    sel.sync_errors()
+    _check_against_oracle([good, good, good], fin, st, arr2)
+    sel.close()
