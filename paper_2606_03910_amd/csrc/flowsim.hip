@@ -61,6 +61,7 @@ struct SimArgs {
     uint8_t *state, *frz;
     uint32_t *mlist, *mlist2;   // [n_flows] the moving flows of each instance (its own range), in turn
     const uint32_t *arr;        // [n_flows] each instance's flows (offsets) in order of arrival
+    const uint64_t *skey;       // [n_flows] their arrival times as sort keys, in that order
     const uint32_t *bad_off;    // nonzero: flow_off is not a valid partition of the flows
     double *g_rem;
     uint32_t *g_cnt, *g_lk;
@@ -70,163 +71,321 @@ struct SimArgs {
 
 __device__ inline double dmin(double a, double b) { return b < a ? b : a; }
 
+// Wavefront reductions by DPP (every lane active): pairs and pairs of
+// pairs within each quad, rotations by 4 and 8 within each row of 16, then
+// the last lane of row 0 into row 1 and of row 2 into row 3, and of row 1
+// into rows 2 and 3; lane 63 then holds the result, which is read back to
+// every lane.  A lane without a source takes the operation's identity.
+// (DPP controls: quad_perm 0xB1 and 0x4E, row_ror 0x124 and 0x128,
+// row_bcast 0x142 and 0x143.)
+template <int CTRL, int ROWS>
+__device__ inline double dpp_f64(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROWS, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0x7FF00000, (int)(uint32_t)(b >> 32), CTRL, ROWS, 0xF,
+                                                              false);   // +infinity where there is no source
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 __device__ inline double wave_min_f64(double v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = dmin(v, __shfl_xor(v, off, 64));
-    return v;
+    v = dmin(v, dpp_f64<0xB1, 0xF>(v));
+    v = dmin(v, dpp_f64<0x4E, 0xF>(v));
+    v = dmin(v, dpp_f64<0x124, 0xF>(v));
+    v = dmin(v, dpp_f64<0x128, 0xF>(v));
+    v = dmin(v, dpp_f64<0x142, 0xA>(v));
+    v = dmin(v, dpp_f64<0x143, 0xC>(v));
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), 63);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
 __device__ inline uint32_t wave_sum_u32(uint32_t v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
-
-// What the wavefront path of one pass hands to the workgroup.
-struct WavePassOut {
-    double t;          // the clock after the event
-    uint32_t rounds;   // filling rounds of the allocation
-    uint32_t done;     // flows completed at the event
-    uint32_t stall;    // the round bound was reached
-};
 
 // Ordering of one wavefront's LDS and memory accesses between the phases
 // of a filling round (lanes read what other lanes of the wavefront wrote).
 __device__ inline void wave_phase() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup"); }
 
-// One pass with at most one wavefront of moving flows (lane i holds the
-// moving flow mv[i]): the max-min fair allocation by progressive filling
-// and the next event, in exactly the operations of the workgroup path.
-// Called by wavefront 0 only; lane 0 writes the results to `out`.
-__device__ void wave_pass(const SimArgs &a, uint64_t f0, const uint32_t *mv, const uint32_t *lk, double *rem,
-                          uint32_t *cnt, uint8_t *sat, const double *cap, uint32_t na, uint32_t nl, double nx,
-                          double t, uint32_t lane, WavePassOut &out) {
+// The arrival time of a key of the arrival sort (the inverse of its map).
+__device__ inline double key_time(uint64_t k) {
+    return __longlong_as_double((long long)((k >> 63) ? (k ^ (1ull << 63)) : ~k));
+}
+
+using lmask = uint64_t;
+__device__ inline lmask ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+// set bits of m below this lane
+__device__ inline uint32_t below(lmask m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+// lane i's v goes to lane dst (a permutation of the lanes)
+__device__ inline uint32_t send_u32(uint32_t v, uint32_t dst) {
+    return (uint32_t)__builtin_amdgcn_ds_permute((int)(dst * 4u), (int)v);
+}
+__device__ inline uint64_t send_u64(uint64_t v, uint32_t dst) {
+    return ((uint64_t)send_u32((uint32_t)(v >> 32), dst) << 32) | send_u32((uint32_t)v, dst);
+}
+
+// Where an instance stands when the wavefront run and the workgroup passes
+// hand over to each other (in LDS; the moving flows are then in the device
+// list `list`).
+struct SimCtl {
+    double t, nx;          // the clock; the next arrival (infinity: none left)
+    uint64_t ap;           // arrivals taken (a prefix of the arrival order)
+    uint64_t left;         // flows not completed
+    uint64_t pass;         // passes so far (bounded)
+    uint64_t events, rounds, moving;
+    uint32_t na;           // moving flows
+    uint32_t list;         // the device list that holds them: 0 mlist, 1 mlist2
+    uint32_t mode;         // kRunWave, kRunGroup or kRunEnd
+    uint32_t resume;       // the current pass has taken its arrivals already
+    uint32_t stall;        // an iteration bound was reached
+};
+constexpr uint32_t kRunWave = 0, kRunGroup = 1, kRunEnd = 2;
+
+// The instance's passes while at most one wavefront of flows moves, run by
+// wavefront 0 alone.  Lane i keeps moving flow i (its offset, path and
+// remaining size) in registers from pass to pass.  A pass takes the
+// arrivals that are due into free lanes (from the sorted arrival order),
+// counts the flows on their links, runs the filling rounds and the event,
+// and moves the flows that are still in progress to the lowest lanes.  When
+// more flows are due than lanes are free, the lanes' flows go to the device
+// list and the workgroup passes take over.  Each flow and each link goes
+// through the operations of the workgroup pass, in the same order.
+__device__ void wave_run(const SimArgs &a, uint64_t f0, uint64_t nf, const uint32_t *arr, const uint64_t *skey,
+                         double *rem, uint32_t *cnt, uint8_t *sat, uint32_t *lk, const double *lcap,
+                         uint32_t *n_lk, SimCtl &c, uint32_t lane) {
 #pragma clang fp contract(off)
-    (void)cap;
-    const bool mine = lane < na;
-    const uint64_t f = mine ? f0 + mv[lane] : 0;
-    const uint64_t p0 = mine ? a.path_off[f] : 0, p1 = mine ? a.path_off[f + 1] : 0;
-    // the flow's first kPathRegs links in registers (a fat-tree path has at
-    // most 6); longer paths read the rest from memory
-    const uint32_t plen = (uint32_t)(p1 - p0);
+    double t = c.t, nx = c.nx;
+    uint64_t ap = c.ap, left = c.left, pass = c.pass, events = c.events, rounds = c.rounds, moving = c.moving;
+    uint32_t na = c.na;
+    bool resume = c.resume != 0;
+    uint32_t *list = (c.list ? a.mlist2 : a.mlist) + f0;
+    uint32_t o = 0, plen = 0;
+    uint64_t p0 = 0;
     uint32_t pl[kPathRegs];
+    double rm = 0.0;
+    auto take = [&](uint32_t off) {   // the flow's path (its first kPathRegs links in registers)
+        const uint64_t f = f0 + off;
+        p0 = a.path_off[f];
+        plen = (uint32_t)(a.path_off[f + 1] - p0);
 #pragma unroll
-    for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = u < plen ? a.path[p0 + u] : 0u;
-    bool frozen = !mine;
-    double level = 0.0;
-    uint32_t rd = 0, stl = 0;
-    double rt = 0.0;
-    for (;;) {
-        if (!__any(!frozen)) break;
-        if (rd > na) {   // every round freezes at least one flow
-            stl = 1;
-            break;
-        }
-        // the largest equal raise every link still allows
-        double sh = INFINITY;
-        for (uint32_t i = lane; i < nl; i += kWave) {
-            const uint32_t l = lk[i];
-            const uint32_t c = cnt[l];
-            if (c > 0) sh = dmin(sh, rem[l] / (double)c);
-        }
-        const double inc = wave_min_f64(sh);
-        // links that the raise fills, and the capacity left on each
-        for (uint32_t i = lane; i < nl; i += kWave) {
-            const uint32_t l = lk[i];
-            const uint32_t c = cnt[l];
-            uint8_t full = 0;
-            if (c > 0) {
-                const double r = rem[l];
-                full = r / (double)c == inc ? 1 : 0;
-                const double used = inc * (double)c;
-                const double lf = r - used;
-                rem[l] = lf > 0.0 ? lf : 0.0;
-            }
-            sat[l] = full;
-        }
-        level = level + inc;
-        wave_phase();
-        // flows crossing a filled link stop at the current level
-        bool just = false;
-        if (!frozen) {
-            uint8_t hit = 0;
+        for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = u < plen ? a.path[p0 + u] : 0u;
+    };
+    auto link = [&](uint32_t u) { return u < kPathRegs ? pl[u] : a.path[p0 + u]; };
 #pragma unroll
-            for (uint32_t u = 0; u < kPathRegs; ++u)
-                if (u < plen) hit |= sat[pl[u]];
-            for (uint64_t q = p0 + kPathRegs; q < p1; ++q) hit |= sat[a.path[q]];
-            if (hit) {   // (the rate stays in the lane: every allocation sets all rates anew)
-                just = true;
-                frozen = true;
-                rt = level;
-            }
-        }
-        wave_phase();
-        if (just) {
-#pragma unroll
-            for (uint32_t u = 0; u < kPathRegs; ++u)
-                if (u < plen) atomicSub(&cnt[pl[u]], 1u);
-            for (uint64_t q = p0 + kPathRegs; q < p1; ++q) atomicSub(&cnt[a.path[q]], 1u);
-        }
-        wave_phase();
-        ++rd;
+    for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = 0u;
+    bool has = lane < na;
+    if (has) {
+        o = list[lane];
+        take(o);
+        rm = a.remaining[f0 + o];
     }
-    double tn = t;
-    uint32_t nd = 0;
-    if (!stl) {
+    uint32_t mode = kRunEnd, stall = 0;
+    for (;; ++pass) {
+        if (left == 0) break;
+        if (!resume) {
+            if (pass > 2 * nf + 4) {
+                stall = 1;
+                break;
+            }
+            if (t >= nx) {
+                // the arrivals that are due: lane na + j takes arrival ap + j
+                const uint64_t q = ap + (uint64_t)(lane - na);
+                const bool cand = lane >= na && q < nf;
+                double sq = INFINITY;
+                uint32_t oq = 0;
+                if (cand) {
+                    sq = key_time(skey[f0 + q]);
+                    oq = arr[q];
+                }
+                const bool in = cand && sq <= t;   // a prefix of the free lanes (the order is sorted)
+                const uint32_t cn = (uint32_t)__builtin_popcountll(ballot(in));
+                double nx2;
+                if (na + cn < (uint32_t)kWave) nx2 = __shfl(sq, (int)(na + cn), kWave);
+                else nx2 = ap + cn < nf ? key_time(skey[f0 + ap + cn]) : INFINITY;
+                if (na + cn == (uint32_t)kWave && nx2 <= t) {
+                    mode = kRunGroup;   // more flows due than lanes: the workgroup takes this pass
+                    break;
+                }
+                if (in) {
+                    o = oq;
+                    take(o);
+                    rm = a.bytes[f0 + o];
+                    a.state[f0 + o] = kMoving;
+                }
+                ap += cn;
+                na += cn;
+                has = lane < na;
+                nx = nx2;
+            }
+        }
+        resume = false;
+        if (na == 0) {
+            t = nx;
+            continue;
+        }
+        // the flows on their links (a link's first count lists it and resets its capacity)
+        if (has) {
+            for (uint32_t u = 0; u < plen; ++u) {
+                const uint32_t l = link(u);
+                if (atomicAdd(&cnt[l], 1u) == 0) {
+                    rem[l] = lcap[l];
+                    lk[atomicAdd(n_lk, 1u)] = l;
+                }
+            }
+        }
+        wave_phase();
+        const uint32_t nl = *n_lk;
+        // progressive filling
+        bool frozen = !has;
+        double level = 0.0, rt = 0.0;
+        uint32_t rd = 0;
+        for (;;) {
+            if (!__any(!frozen)) break;
+            if (rd > na) {   // every round freezes at least one flow
+                stall = 1;
+                break;
+            }
+            // the largest equal raise every link still allows
+            double sh = INFINITY;
+            for (uint32_t i = lane; i < nl; i += kWave) {
+                const uint32_t l = lk[i];
+                const uint32_t k = cnt[l];
+                if (k > 0) sh = dmin(sh, rem[l] / (double)k);
+            }
+            const double inc = wave_min_f64(sh);
+            // links that the raise fills, and the capacity left on each
+            for (uint32_t i = lane; i < nl; i += kWave) {
+                const uint32_t l = lk[i];
+                const uint32_t k = cnt[l];
+                uint8_t full = 0;
+                if (k > 0) {
+                    const double r = rem[l];
+                    full = r / (double)k == inc ? 1 : 0;
+                    const double used = inc * (double)k;
+                    const double lf = r - used;
+                    rem[l] = lf > 0.0 ? lf : 0.0;
+                }
+                sat[l] = full;
+            }
+            level = level + inc;
+            wave_phase();
+            // flows crossing a filled link stop at the current level
+            bool just = false;
+            if (!frozen) {
+                uint8_t hit = 0;
+                for (uint32_t u = 0; u < plen; ++u) hit |= sat[link(u)];
+                if (hit) {
+                    just = true;
+                    frozen = true;
+                    rt = level;
+                }
+            }
+            wave_phase();
+            if (just)
+                for (uint32_t u = 0; u < plen; ++u) atomicSub(&cnt[link(u)], 1u);
+            wave_phase();
+            ++rd;
+        }
+        rounds += rd;
+        if (stall) break;
         // the next event: the earliest completion, or the next arrival
-        const double rm = mine ? a.remaining[f] : 0.0;
-        const double dtc = wave_min_f64(mine ? rm / rt : INFINITY);
+        bool done = false;
+        const double dtc = wave_min_f64(has ? rm / rt : INFINITY);
         if (dtc <= nx - t) {
-            if (mine) {
+            if (has) {
                 if (rm / rt == dtc) {
-                    a.state[f] = kDone;
-                    a.finish[f] = t + dtc;
-                    nd = 1;
+                    a.state[f0 + o] = kDone;
+                    a.finish[f0 + o] = t + dtc;
+                    done = true;
                 } else {
                     const double moved = rt * dtc;
                     const double r = rm - moved;
-                    a.remaining[f] = r > 0.0 ? r : 0.0;
+                    rm = r > 0.0 ? r : 0.0;
                 }
             }
-            tn = t + dtc;
+            t = t + dtc;
         } else {
             const double dt = nx - t;
-            if (mine) {
+            if (has) {
                 const double moved = rt * dt;
                 const double r = rm - moved;
-                a.remaining[f] = r > 0.0 ? r : 0.0;
+                rm = r > 0.0 ? r : 0.0;
             }
-            tn = nx;
+            t = nx;
+        }
+        ++events;
+        moving += na;
+        if (lane == 0) *n_lk = 0;   // every lane has read the link count
+        wave_phase();
+        const lmask gone = ballot(done);
+        if (gone) {
+            // the flows still in progress to the lowest lanes, the others after them
+            const lmask keep = ballot(has && !done);
+            const uint32_t ns = (uint32_t)__builtin_popcountll(keep);
+            const uint32_t dst = (has && !done) ? below(keep) : ns + below(~keep);
+            o = send_u32(o, dst);
+            plen = send_u32(plen, dst);
+            p0 = send_u64(p0, dst);
+#pragma unroll
+            for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = send_u32(pl[u], dst);
+            rm = __longlong_as_double((long long)send_u64((uint64_t)__double_as_longlong(rm), dst));
+            left -= (uint64_t)__builtin_popcountll(gone);
+            na = ns;
+            has = lane < na;
         }
     }
-    nd = wave_sum_u32(nd);
+    if (mode == kRunGroup && has) {
+        list[lane] = o;
+        a.remaining[f0 + o] = rm;
+    }
     if (lane == 0) {
-        out.t = tn;
-        out.rounds = rd;
-        out.done = nd;
-        out.stall = stl;
+        c.t = t;
+        c.nx = nx;
+        c.ap = ap;
+        c.left = left;
+        c.pass = pass;
+        c.events = events;
+        c.rounds = rounds;
+        c.moving = moving;
+        c.na = na;
+        c.mode = stall ? kRunEnd : mode;
+        c.resume = 0;
+        c.stall = stall;
     }
 }
+
+// Bytes of the link state an instance keeps in LDS: per link the capacity
+// left and the capacity (fp64), the flow count and the list entry (u32),
+// and the filled mark (u8).
+__host__ __device__ inline uint32_t lds_link_bytes(uint32_t L) { return L * (8u + 8u + 4u + 4u + 1u); }
 
 template <bool LDS>
 __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
 #pragma clang fp contract(off)
     __shared__ double red_d[2][kSimWaves];
     __shared__ uint32_t red_u[2][kSimWaves];
-    __shared__ double l_rem[LDS ? kSimLdsLinks : 1];
-    __shared__ uint32_t l_cnt[LDS ? kSimLdsLinks : 1];
-    __shared__ uint8_t l_sat[LDS ? kSimLdsLinks : 1];
-    __shared__ uint32_t l_lk[LDS ? kSimLdsLinks : 1];
     __shared__ uint32_t n_mv, n_lk;
-    __shared__ WavePassOut s_out;
+    __shared__ SimCtl ctl;
+    extern __shared__ __align__(8) unsigned char dyn[];   // the link state in LDS mode
     const uint32_t tid = threadIdx.x, lane = tid % 64, w = tid / 64;
     const uint32_t inst = blockIdx.x;
     const uint32_t L = a.n_links;
     const uint64_t f0 = a.flow_off[inst], f1 = a.flow_off[inst + 1];
     const double *cap = a.cap + (uint64_t)inst * L;
-    double *rem = LDS ? l_rem : a.g_rem + (uint64_t)inst * L;
-    uint32_t *cnt = LDS ? l_cnt : a.g_cnt + (uint64_t)inst * L;
-    uint8_t *sat = LDS ? l_sat : a.g_sat + (uint64_t)inst * L;
+    double *rem = LDS ? (double *)dyn : a.g_rem + (uint64_t)inst * L;
+    double *lcap = LDS ? (double *)dyn + L : nullptr;
+    uint32_t *cnt = LDS ? (uint32_t *)(dyn + 16u * L) : a.g_cnt + (uint64_t)inst * L;
+    uint32_t *lk = LDS ? (uint32_t *)(dyn + 20u * L) : a.g_lk + (uint64_t)inst * L;
+    uint8_t *sat = LDS ? dyn + 24u * L : a.g_sat + (uint64_t)inst * L;
     // workgroup reductions: one barrier each; two buffers used in turn, so a
     // buffer is written again only after the next reduction's barrier,
     // which every thread reaches after reading it
@@ -282,7 +441,10 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     // flows wait for their arrival; the clock starts at the first one.
     // Link counts start at 0 and return to 0 at the end of every allocation
     // (every flow counted on a link is frozen and uncounted again).
-    for (uint32_t l = tid; l < L; l += kSimThreads) cnt[l] = 0;
+    for (uint32_t l = tid; l < L; l += kSimThreads) {
+        cnt[l] = 0;
+        if (LDS) lcap[l] = cap[l];
+    }
     for (uint64_t f = f0 + tid; f < f1; f += kSimThreads) {
         a.state[f] = kWaiting;
         a.frz[f] = kFree;
@@ -290,196 +452,337 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     }
     const uint64_t nf = f1 - f0;   // < 2^32 (the call's flows are)
     const uint32_t *arr = a.arr + f0;
-    // the clock starts at the first arrival
-    double t = nf ? a.start[f0 + arr[0]] : INFINITY;
-    uint64_t left = nf;
-    uint64_t events = 0, rounds = 0, moving = 0;
-    bool stall = false;
-    // the moving flows (offsets from f0): the previous pass's list in mv,
-    // this pass's built in mv2, then swapped
-    uint32_t *mv = a.mlist + f0, *mv2 = a.mlist2 + f0;
-    uint32_t *lk = LDS ? l_lk : a.g_lk + (uint64_t)inst * L;   // the links they cross
-    uint32_t na = 0;   // flows in mv
-    uint64_t ap = 0;   // arrivals taken: arr[0 .. ap) have started
-    // each pass starts a flow or completes one (or both), so 2 nf + 1 passes
-    // end every valid instance
-    for (uint64_t pass = 0; left > 0; ++pass) {
-        if (pass > 2 * nf + 4) {
-            stall = true;
-            break;
-        }
-        if (tid == 0) {
-            n_mv = 0;
-            n_lk = 0;
-        }
-        __syncthreads();   // the list counters' previous uses all precede the last barrier
-        // this pass's moving flows: the previous list without the flows that
-        // completed, then the flows that have arrived by t (a prefix of the
-        // rest of the arrival order); the next arrival
-        for (uint32_t i = tid; i < na; i += kSimThreads) {
-            const uint32_t o = mv[i];
-            if (a.state[f0 + o] != kDone) mv2[atomicAdd(&n_mv, 1u)] = o;
-        }
-        for (;;) {
-            const uint64_t q = ap + tid;
-            uint32_t in = 0;
-            if (q < nf) {
-                const uint32_t o = arr[q];
-                if (a.start[f0 + o] <= t) {
-                    a.state[f0 + o] = kMoving;
-                    mv2[atomicAdd(&n_mv, 1u)] = o;
-                    in = 1;
-                }
-            }
-            const uint32_t c = bsum(in);   // its barrier also orders the list writes before n_mv is read
-            ap += c;
-            if (c < (uint32_t)kSimThreads) break;
-        }
-        const double nx = ap < nf ? a.start[f0 + arr[ap]] : INFINITY;
-        na = n_mv;
-        {
-            uint32_t *x = mv;
-            mv = mv2;
-            mv2 = x;
-        }
-        if (na == 0) {
-            t = nx;
+    if (tid == 0) {
+        n_lk = 0;
+        ctl.t = nf ? key_time(a.skey[f0]) : INFINITY;   // the first arrival
+        ctl.nx = ctl.t;
+        ctl.ap = 0;
+        ctl.left = nf;
+        ctl.pass = 0;
+        ctl.events = ctl.rounds = ctl.moving = 0;
+        ctl.na = 0;
+        ctl.list = 0;
+        ctl.mode = nf ? kRunWave : kRunEnd;
+        ctl.resume = 0;
+        ctl.stall = 0;
+    }
+    __syncthreads();
+    // the wavefront run while few flows move, the workgroup passes while
+    // more do, handing over through ctl (each side reads it after the
+    // barrier that follows the other side's writes)
+    for (;;) {
+        const uint32_t mode = ctl.mode;
+        __syncthreads();   // every thread has read the mode before it changes
+        if (mode == kRunEnd) break;
+        if (mode == kRunWave) {
+            if (w == 0)
+                wave_run(a, f0, nf, arr, a.skey, rem, cnt, sat, lk, LDS ? (const double *)lcap : cap, &n_lk, ctl,
+                         lane);
+            __syncthreads();
             continue;
         }
-        // the max-min fair allocation of the moving flows: count them on
-        // their links (a link's first count lists it and resets its capacity)
-        for (uint32_t i = tid; i < na; i += kSimThreads) {
-            const uint64_t f = f0 + mv[i];
-            a.frz[f] = kFree;
-            for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) {
-                const uint32_t l = a.path[q];
-                if (atomicAdd(&cnt[l], 1u) == 0) {
-                    rem[l] = cap[l];
-                    lk[atomicAdd(&n_lk, 1u)] = l;
-                }
-            }
-        }
-        __syncthreads();
-        const uint32_t nl = n_lk;
-        if (na <= (uint32_t)kWave) {
-            // few moving flows: one wavefront runs the allocation and the
-            // event (a flow per lane; wavefront reductions, no barriers) with
-            // the same operations as the workgroup path below
-            if (w == 0) wave_pass(a, f0, mv, lk, rem, cnt, sat, cap, na, nl, nx, t, lane, s_out);
-            __syncthreads();
-            t = s_out.t;
-            rounds += s_out.rounds;
-            if (s_out.stall) {
-                stall = true;
+        // workgroup passes: the moving flows in the device list mv (pass
+        // state in every thread's registers, the same in all of them)
+        double t = ctl.t;
+        uint64_t ap = ctl.ap, left = ctl.left, pass = ctl.pass;
+        uint64_t events = ctl.events, rounds = ctl.rounds, moving = ctl.moving;
+        uint32_t na = ctl.na, cur = ctl.list;
+        uint32_t *mv = (cur ? a.mlist2 : a.mlist) + f0, *mv2 = (cur ? a.mlist : a.mlist2) + f0;
+        uint32_t next = kRunEnd, stall = 0;
+        double nx = INFINITY;
+        for (;; ++pass) {
+            if (left == 0) break;
+            if (pass > 2 * nf + 4) {
+                stall = 1;
                 break;
             }
+            if (tid == 0) {
+                n_mv = 0;
+                n_lk = 0;
+            }
+            __syncthreads();   // the list counters' previous uses all precede the last barrier
+            // this pass's moving flows: the previous list without the flows
+            // that completed, then the flows that have arrived by t (a prefix
+            // of the rest of the arrival order); the next arrival
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint32_t o = mv[i];
+                if (a.state[f0 + o] != kDone) mv2[atomicAdd(&n_mv, 1u)] = o;
+            }
+            for (;;) {
+                const uint64_t q = ap + tid;
+                uint32_t in = 0;
+                if (q < nf) {
+                    const uint32_t o = arr[q];
+                    if (a.start[f0 + o] <= t) {
+                        a.state[f0 + o] = kMoving;
+                        mv2[atomicAdd(&n_mv, 1u)] = o;
+                        in = 1;
+                    }
+                }
+                const uint32_t c = bsum(in);   // its barrier also orders the list writes before n_mv is read
+                ap += c;
+                if (c < (uint32_t)kSimThreads) break;
+            }
+            nx = ap < nf ? a.start[f0 + arr[ap]] : INFINITY;
+            na = n_mv;
+            {
+                uint32_t *x = mv;
+                mv = mv2;
+                mv2 = x;
+                cur ^= 1u;
+            }
+            if (na <= (uint32_t)kWave) {
+                // few enough for the wavefront run, which finishes this pass
+                next = kRunWave;
+                break;
+            }
+            if (na <= (uint32_t)kSimThreads) {
+                // at most one flow per thread: the thread keeps its flow's
+                // path, freeze mark, rate and remaining size in registers
+                // for the pass (the operations of the general case below)
+                const bool has = tid < na;
+                uint64_t f = 0, p0 = 0;
+                uint32_t plen = 0;
+                uint32_t pl[kPathRegs];
+#pragma unroll
+                for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = 0u;
+                double rm = 0.0, rt = 0.0;
+                if (has) {
+                    f = f0 + mv[tid];
+                    p0 = a.path_off[f];
+                    plen = (uint32_t)(a.path_off[f + 1] - p0);
+#pragma unroll
+                    for (uint32_t u = 0; u < kPathRegs; ++u) pl[u] = u < plen ? a.path[p0 + u] : 0u;
+                    rm = a.remaining[f];
+                }
+                auto link = [&](uint32_t u) { return u < kPathRegs ? pl[u] : a.path[p0 + u]; };
+                if (has) {
+                    for (uint32_t u = 0; u < plen; ++u) {
+                        const uint32_t l = link(u);
+                        if (atomicAdd(&cnt[l], 1u) == 0) {
+                            rem[l] = LDS ? lcap[l] : cap[l];
+                            lk[atomicAdd(&n_lk, 1u)] = l;
+                        }
+                    }
+                }
+                __syncthreads();
+                const uint32_t nl = n_lk;
+                bool frozen = !has;
+                double level = 0.0;
+                uint32_t unfrozen = na;
+                for (uint32_t round = 0; unfrozen > 0; ++round) {
+                    if (round > na) {   // every round freezes at least one flow
+                        stall = 1;
+                        break;
+                    }
+                    // the largest equal raise every link still allows
+                    double sh = INFINITY;
+                    for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                        const uint32_t l = lk[i];
+                        const uint32_t c = cnt[l];
+                        if (c > 0) sh = dmin(sh, rem[l] / (double)c);
+                    }
+                    const double inc = bmin(sh);
+                    // links that the raise fills, and the capacity left on each
+                    for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                        const uint32_t l = lk[i];
+                        const uint32_t c = cnt[l];
+                        uint8_t full = 0;
+                        if (c > 0) {
+                            const double r = rem[l];
+                            full = r / (double)c == inc ? 1 : 0;
+                            const double used = inc * (double)c;
+                            const double lf = r - used;
+                            rem[l] = lf > 0.0 ? lf : 0.0;
+                        }
+                        sat[l] = full;
+                    }
+                    level = level + inc;
+                    __syncthreads();
+                    // flows crossing a filled link stop at the current level
+                    uint32_t just = 0;
+                    if (!frozen) {
+                        uint8_t hit = 0;
+                        for (uint32_t u = 0; u < plen; ++u) hit |= sat[link(u)];
+                        if (hit) {
+                            just = 1;
+                            frozen = true;
+                            rt = level;
+                        }
+                    }
+                    const uint32_t nfz = bsum(just);
+                    if (just)
+                        for (uint32_t u = 0; u < plen; ++u) atomicSub(&cnt[link(u)], 1u);
+                    __syncthreads();
+                    unfrozen -= nfz;
+                    ++rounds;
+                }
+                if (stall) break;
+                ++events;
+                moving += na;
+                // the next event: the earliest completion, or the next arrival
+                const double dtc = bmin(has ? rm / rt : INFINITY);
+                uint32_t nd = 0;
+                if (dtc <= nx - t) {
+                    if (has) {
+                        if (rm / rt == dtc) {
+                            a.state[f] = kDone;
+                            a.finish[f] = t + dtc;
+                            nd = 1;
+                        } else {
+                            const double moved = rt * dtc;
+                            const double r = rm - moved;
+                            a.remaining[f] = r > 0.0 ? r : 0.0;
+                        }
+                    }
+                    t = t + dtc;
+                } else {
+                    const double dt = nx - t;
+                    if (has) {
+                        const double moved = rt * dt;
+                        const double r = rm - moved;
+                        a.remaining[f] = r > 0.0 ? r : 0.0;
+                    }
+                    t = nx;
+                }
+                left -= bsum(nd);
+                continue;
+            }
+            // the max-min fair allocation of the moving flows: count them on
+            // their links (a link's first count lists it and resets its capacity)
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint64_t f = f0 + mv[i];
+                a.frz[f] = kFree;
+                for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) {
+                    const uint32_t l = a.path[q];
+                    if (atomicAdd(&cnt[l], 1u) == 0) {
+                        rem[l] = LDS ? lcap[l] : cap[l];
+                        lk[atomicAdd(&n_lk, 1u)] = l;
+                    }
+                }
+            }
+            __syncthreads();
+            const uint32_t nl = n_lk;
+            double level = 0.0;
+            uint32_t unfrozen = na;
+            for (uint32_t round = 0; unfrozen > 0; ++round) {
+                if (round > na) {   // every round freezes at least one flow
+                    stall = 1;
+                    break;
+                }
+                // the largest equal raise every link still allows
+                double sh = INFINITY;
+                for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                    const uint32_t l = lk[i];
+                    const uint32_t c = cnt[l];
+                    if (c > 0) sh = dmin(sh, rem[l] / (double)c);
+                }
+                const double inc = bmin(sh);
+                // links that the raise fills, and the capacity left on each
+                for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                    const uint32_t l = lk[i];
+                    const uint32_t c = cnt[l];
+                    uint8_t full = 0;
+                    if (c > 0) {
+                        const double r = rem[l];
+                        full = r / (double)c == inc ? 1 : 0;
+                        const double used = inc * (double)c;
+                        const double lf = r - used;
+                        rem[l] = lf > 0.0 ? lf : 0.0;
+                    }
+                    sat[l] = full;
+                }
+                level = level + inc;
+                __syncthreads();
+                // flows crossing a filled link stop at the current level
+                uint32_t nfz = 0;
+                for (uint32_t i = tid; i < na; i += kSimThreads) {
+                    const uint64_t f = f0 + mv[i];
+                    if (a.frz[f] != kFree) continue;
+                    uint8_t hit = 0;
+                    for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) hit |= sat[a.path[q]];
+                    if (hit) {
+                        a.frz[f] = kJustFrozen;
+                        a.rate[f] = level;
+                        ++nfz;
+                    }
+                }
+                nfz = bsum(nfz);
+                for (uint32_t i = tid; i < na; i += kSimThreads) {
+                    const uint64_t f = f0 + mv[i];
+                    if (a.frz[f] != kJustFrozen) continue;
+                    a.frz[f] = kFrozen;
+                    for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) atomicSub(&cnt[a.path[q]], 1u);
+                }
+                __syncthreads();
+                unfrozen -= nfz;
+                ++rounds;
+            }
+            if (stall) break;
             ++events;
             moving += na;
-            left -= s_out.done;
-            continue;   // s_out is written again only after the next pass's first barrier
-        }
-        double level = 0.0;
-        uint32_t unfrozen = na;
-        for (uint32_t round = 0; unfrozen > 0; ++round) {
-            if (round > na) {   // every round freezes at least one flow
-                stall = true;
-                break;
+            // the next event: the earliest completion, or the next arrival
+            double tc = INFINITY;
+            for (uint32_t i = tid; i < na; i += kSimThreads) {
+                const uint64_t f = f0 + mv[i];
+                tc = dmin(tc, a.remaining[f] / a.rate[f]);
             }
-            // the largest equal raise every link still allows
-            double sh = INFINITY;
-            for (uint32_t i = tid; i < nl; i += kSimThreads) {
-                const uint32_t l = lk[i];
-                const uint32_t c = cnt[l];
-                if (c > 0) sh = dmin(sh, rem[l] / (double)c);
-            }
-            const double inc = bmin(sh);
-            // links that the raise fills, and the capacity left on each
-            for (uint32_t i = tid; i < nl; i += kSimThreads) {
-                const uint32_t l = lk[i];
-                const uint32_t c = cnt[l];
-                uint8_t full = 0;
-                if (c > 0) {
-                    const double r = rem[l];
-                    full = r / (double)c == inc ? 1 : 0;
-                    const double used = inc * (double)c;
-                    const double lf = r - used;
-                    rem[l] = lf > 0.0 ? lf : 0.0;
+            const double dtc = bmin(tc);
+            uint32_t nd = 0;
+            if (dtc <= nx - t) {
+                for (uint32_t i = tid; i < na; i += kSimThreads) {
+                    const uint64_t f = f0 + mv[i];
+                    const double rm = a.remaining[f], rt = a.rate[f];
+                    if (rm / rt == dtc) {
+                        a.state[f] = kDone;
+                        a.finish[f] = t + dtc;
+                        ++nd;
+                    } else {
+                        const double moved = rt * dtc;
+                        const double r = rm - moved;
+                        a.remaining[f] = r > 0.0 ? r : 0.0;
+                    }
                 }
-                sat[l] = full;
-            }
-            level = level + inc;
-            __syncthreads();
-            // flows crossing a filled link stop at the current level
-            uint32_t nfz = 0;
-            for (uint32_t i = tid; i < na; i += kSimThreads) {
-                const uint64_t f = f0 + mv[i];
-                if (a.frz[f] != kFree) continue;
-                uint8_t hit = 0;
-                for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) hit |= sat[a.path[q]];
-                if (hit) {
-                    a.frz[f] = kJustFrozen;
-                    a.rate[f] = level;
-                    ++nfz;
-                }
-            }
-            nfz = bsum(nfz);
-            for (uint32_t i = tid; i < na; i += kSimThreads) {
-                const uint64_t f = f0 + mv[i];
-                if (a.frz[f] != kJustFrozen) continue;
-                a.frz[f] = kFrozen;
-                for (uint64_t q = a.path_off[f]; q < a.path_off[f + 1]; ++q) atomicSub(&cnt[a.path[q]], 1u);
-            }
-            __syncthreads();
-            unfrozen -= nfz;
-            ++rounds;
-        }
-        if (stall) break;
-        ++events;
-        moving += na;
-        // the next event: the earliest completion, or the next arrival
-        double tc = INFINITY;
-        for (uint32_t i = tid; i < na; i += kSimThreads) {
-            const uint64_t f = f0 + mv[i];
-            tc = dmin(tc, a.remaining[f] / a.rate[f]);
-        }
-        const double dtc = bmin(tc);
-        uint32_t nd = 0;
-        if (dtc <= nx - t) {
-            for (uint32_t i = tid; i < na; i += kSimThreads) {
-                const uint64_t f = f0 + mv[i];
-                const double rm = a.remaining[f], rt = a.rate[f];
-                if (rm / rt == dtc) {
-                    a.state[f] = kDone;
-                    a.finish[f] = t + dtc;
-                    ++nd;
-                } else {
-                    const double moved = rt * dtc;
-                    const double r = rm - moved;
+                t = t + dtc;
+            } else {
+                const double dt = nx - t;
+                for (uint32_t i = tid; i < na; i += kSimThreads) {
+                    const uint64_t f = f0 + mv[i];
+                    const double moved = a.rate[f] * dt;
+                    const double r = a.remaining[f] - moved;
                     a.remaining[f] = r > 0.0 ? r : 0.0;
                 }
+                t = nx;
             }
-            t = t + dtc;
-        } else {
-            const double dt = nx - t;
-            for (uint32_t i = tid; i < na; i += kSimThreads) {
-                const uint64_t f = f0 + mv[i];
-                const double moved = a.rate[f] * dt;
-                const double r = a.remaining[f] - moved;
-                a.remaining[f] = r > 0.0 ? r : 0.0;
-            }
-            t = nx;
+            left -= bsum(nd);
         }
-        left -= bsum(nd);
+        if (tid == 0) {
+            ctl.t = t;
+            ctl.nx = nx;
+            ctl.ap = ap;
+            ctl.left = left;
+            ctl.pass = pass;
+            ctl.events = events;
+            ctl.rounds = rounds;
+            ctl.moving = moving;
+            ctl.na = na;
+            ctl.list = cur;
+            ctl.mode = stall ? kRunEnd : next;
+            ctl.resume = next == kRunWave ? 1u : 0u;
+            ctl.stall = stall;
+            n_lk = 0;
+        }
+        __syncthreads();
     }
-    if (stall) {
+    if (ctl.stall) {
         for (uint64_t f = f0 + tid; f < f1; f += kSimThreads)
             if (a.state[f] != kDone) a.finish[f] = NAN;
         if (tid == 0) atomicOr(a.err, kErrFlowStallBit);
     }
     if (tid == 0 && a.stats) {
-        a.stats[3ull * inst + 0] = events;
-        a.stats[3ull * inst + 1] = rounds;
-        a.stats[3ull * inst + 2] = moving;
+        a.stats[3ull * inst + 0] = ctl.events;
+        a.stats[3ull * inst + 1] = ctl.rounds;
+        a.stats[3ull * inst + 2] = ctl.moving;
     }
 }
 
@@ -549,9 +852,9 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
     if (prev != dev) (void)hipSetDevice(dev);
     const bool lds = n_links <= kSimLdsLinks;
     hipStream_t s = (hipStream_t)stream;
-    // the arrival-order sort: keys in `remaining`, sorted keys in `rate`,
-    // values in the first moving list, the order itself in `arr` (the
-    // simulation initialises the first three itself)
+    // the arrival-order sort: keys in `remaining` and values in the first
+    // moving list (the simulation initialises both itself), the sorted keys
+    // in `skey`, the order in `arr`
     size_t sort_bytes = 0;
     hipError_t e = hipSuccess;
     if (n_flows)
@@ -562,7 +865,7 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         if (prev >= 0 && prev != dev) (void)hipSetDevice(prev);
         return netkv_internal_fail(h, NETKV_EDEVICE, "arrival sort size query failed");
     }
-    const uint64_t per_flow = align256(8 * n_flows) * 2 + align256(n_flows) * 2 + align256(4 * n_flows) * 3;
+    const uint64_t per_flow = align256(8 * n_flows) * 3 + align256(n_flows) * 2 + align256(4 * n_flows) * 3;
     const uint64_t per_inst = 2 * align256(4ull * n_inst) + 256 + align256(sort_bytes);
     const uint64_t per_link = lds ? 0 : align256(8ull * n_inst * n_links) + 2 * align256(4ull * n_inst * n_links) +
                                             align256((uint64_t)n_inst * n_links);
@@ -601,6 +904,9 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         uint32_t *arr = (uint32_t *)p;
         a.arr = arr;
         p += align256(4 * n_flows);
+        uint64_t *skey = (uint64_t *)p;
+        a.skey = skey;
+        p += align256(8 * n_flows);
         uint32_t *seg_b = (uint32_t *)p;
         p += align256(4ull * n_inst);
         uint32_t *seg_e = (uint32_t *)p;
@@ -625,12 +931,12 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
             hipLaunchKernelGGL(flow_keys_kernel, dim3(n_inst), dim3(kSimThreads), 0, s, flow_off, start,
                                (const uint32_t *)bad_off, (uint64_t *)a.remaining, a.mlist, seg_b, seg_e);
             size_t tb = sort_bytes;
-            e = rocprim::segmented_radix_sort_pairs(sort_tmp, tb, (const uint64_t *)a.remaining, (uint64_t *)a.rate,
+            e = rocprim::segmented_radix_sort_pairs(sort_tmp, tb, (const uint64_t *)a.remaining, skey,
                                                     (const uint32_t *)a.mlist, arr, (unsigned)n_flows, n_inst,
                                                     (const uint32_t *)seg_b, (const uint32_t *)seg_e, 0, 64, s);
         }
         if (e == hipSuccess && lds)
-            hipLaunchKernelGGL(flow_sim_kernel<true>, dim3(n_inst), dim3(kSimThreads), 0, s, a);
+            hipLaunchKernelGGL(flow_sim_kernel<true>, dim3(n_inst), dim3(kSimThreads), lds_link_bytes(n_links), s, a);
         else if (e == hipSuccess)
             hipLaunchKernelGGL(flow_sim_kernel<false>, dim3(n_inst), dim3(kSimThreads), 0, s, a);
         if (e == hipSuccess) e = hipGetLastError();
