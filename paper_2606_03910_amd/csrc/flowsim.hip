@@ -39,6 +39,8 @@ constexpr int kWave = 64;
 constexpr int kSimWaves = kSimThreads / kWave;
 constexpr uint32_t kSimLdsLinks = 2048;   // instances with at most this many links keep them in LDS
 constexpr uint32_t kPathRegs = 6;         // path links a wavefront-path lane keeps in registers
+constexpr uint32_t kLinkRegs = 2;         // links per thread whose round state the workgroup path keeps in registers
+constexpr uint32_t kWaveLinkRegs = 5;     // the same per lane of the wavefront run
 
 // flow states
 constexpr uint8_t kWaiting = 0, kMoving = 1, kDone = 2;
@@ -254,16 +256,50 @@ __device__ void wave_run(const SimArgs &a, uint64_t f0, uint64_t nf, const uint3
                 stall = 1;
                 break;
             }
-            // the largest equal raise every link still allows
+            // the largest equal raise every link still allows; the lane's
+            // first kWaveLinkRegs links keep their id, count, capacity left
+            // and share for the update
             double sh = INFINITY;
-            for (uint32_t i = lane; i < nl; i += kWave) {
+            uint32_t ll[kWaveLinkRegs], lc[kWaveLinkRegs];
+            double lr[kWaveLinkRegs], ls[kWaveLinkRegs];
+#pragma unroll
+            for (uint32_t k = 0; k < kWaveLinkRegs; ++k) {
+                const uint32_t i = lane + k * kWave;
+                ll[k] = 0;
+                lc[k] = 0;
+                lr[k] = 0.0;
+                ls[k] = INFINITY;
+                if (i < nl) {
+                    ll[k] = lk[i];
+                    lc[k] = cnt[ll[k]];
+                    if (lc[k] > 0) {
+                        lr[k] = rem[ll[k]];
+                        ls[k] = lr[k] / (double)lc[k];
+                        sh = dmin(sh, ls[k]);
+                    }
+                }
+            }
+            for (uint32_t i = lane + kWaveLinkRegs * kWave; i < nl; i += kWave) {
                 const uint32_t l = lk[i];
                 const uint32_t k = cnt[l];
                 if (k > 0) sh = dmin(sh, rem[l] / (double)k);
             }
             const double inc = wave_min_f64(sh);
             // links that the raise fills, and the capacity left on each
-            for (uint32_t i = lane; i < nl; i += kWave) {
+#pragma unroll
+            for (uint32_t k = 0; k < kWaveLinkRegs; ++k) {
+                if (lane + k * kWave < nl) {
+                    uint8_t full = 0;
+                    if (lc[k] > 0) {
+                        full = ls[k] == inc ? 1 : 0;
+                        const double used = inc * (double)lc[k];
+                        const double lf = lr[k] - used;
+                        rem[ll[k]] = lf > 0.0 ? lf : 0.0;
+                    }
+                    sat[ll[k]] = full;
+                }
+            }
+            for (uint32_t i = lane + kWaveLinkRegs * kWave; i < nl; i += kWave) {
                 const uint32_t l = lk[i];
                 const uint32_t k = cnt[l];
                 uint8_t full = 0;
@@ -569,22 +605,58 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
                 const uint32_t nl = n_lk;
                 bool frozen = !has;
                 double level = 0.0;
-                uint32_t unfrozen = na;
-                for (uint32_t round = 0; unfrozen > 0; ++round) {
-                    if (round > na) {   // every round freezes at least one flow
-                        stall = 1;
-                        break;
-                    }
-                    // the largest equal raise every link still allows
+                // every flow crosses a link, so the least share below is
+                // infinite exactly when every flow is frozen
+                for (uint32_t round = 0;; ++round) {
+                    // the largest equal raise every link still allows; the
+                    // thread's first kLinkRegs links keep their id, count,
+                    // capacity left and share for the update
                     double sh = INFINITY;
-                    for (uint32_t i = tid; i < nl; i += kSimThreads) {
+                    uint32_t ll[kLinkRegs], lc[kLinkRegs];
+                    double lr[kLinkRegs], ls[kLinkRegs];
+#pragma unroll
+                    for (uint32_t k = 0; k < kLinkRegs; ++k) {
+                        const uint32_t i = tid + k * kSimThreads;
+                        ll[k] = 0;
+                        lc[k] = 0;
+                        lr[k] = 0.0;
+                        ls[k] = INFINITY;
+                        if (i < nl) {
+                            ll[k] = lk[i];
+                            lc[k] = cnt[ll[k]];
+                            if (lc[k] > 0) {
+                                lr[k] = rem[ll[k]];
+                                ls[k] = lr[k] / (double)lc[k];
+                                sh = dmin(sh, ls[k]);
+                            }
+                        }
+                    }
+                    for (uint32_t i = tid + kLinkRegs * kSimThreads; i < nl; i += kSimThreads) {
                         const uint32_t l = lk[i];
                         const uint32_t c = cnt[l];
                         if (c > 0) sh = dmin(sh, rem[l] / (double)c);
                     }
                     const double inc = bmin(sh);
+                    if (inc == INFINITY) break;
+                    if (round > na) {   // every round freezes at least one flow
+                        stall = 1;
+                        break;
+                    }
                     // links that the raise fills, and the capacity left on each
-                    for (uint32_t i = tid; i < nl; i += kSimThreads) {
+#pragma unroll
+                    for (uint32_t k = 0; k < kLinkRegs; ++k) {
+                        if (tid + k * kSimThreads < nl) {
+                            uint8_t full = 0;
+                            if (lc[k] > 0) {
+                                full = ls[k] == inc ? 1 : 0;
+                                const double used = inc * (double)lc[k];
+                                const double lf = lr[k] - used;
+                                rem[ll[k]] = lf > 0.0 ? lf : 0.0;
+                            }
+                            sat[ll[k]] = full;
+                        }
+                    }
+                    for (uint32_t i = tid + kLinkRegs * kSimThreads; i < nl; i += kSimThreads) {
                         const uint32_t l = lk[i];
                         const uint32_t c = cnt[l];
                         uint8_t full = 0;
@@ -600,21 +672,19 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
                     level = level + inc;
                     __syncthreads();
                     // flows crossing a filled link stop at the current level
-                    uint32_t just = 0;
+                    bool just = false;
                     if (!frozen) {
                         uint8_t hit = 0;
                         for (uint32_t u = 0; u < plen; ++u) hit |= sat[link(u)];
                         if (hit) {
-                            just = 1;
+                            just = true;
                             frozen = true;
                             rt = level;
                         }
                     }
-                    const uint32_t nfz = bsum(just);
                     if (just)
                         for (uint32_t u = 0; u < plen; ++u) atomicSub(&cnt[link(u)], 1u);
                     __syncthreads();
-                    unfrozen -= nfz;
                     ++rounds;
                 }
                 if (stall) break;
