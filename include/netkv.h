@@ -427,7 +427,7 @@ netkv_status netkv_selection_bytes(netkv_handle h, const netkv_requests_t *req, 
  * iteration bound, which valid input never does); offsets that are not
  * non-decreasing, or that end past n_flows, make every instance invalid.
  * Each instance's flows are first sorted by arrival time (rocPRIM's
- * segmented radix sort).  Grows a work buffer of the handle to 30 B per
+ * segmented radix sort).  Grows a work buffer of the handle to 38 B per
  * flow, 8 B per instance and the sort's temporary storage, plus, for more
  * than 2,048 links (whose state then lives in device memory instead of
  * LDS), 17 B per link and instance.  EINVAL: NULL arrays, n_links = 0,
