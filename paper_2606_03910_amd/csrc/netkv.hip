@@ -1809,15 +1809,19 @@ __global__ __launch_bounds__(256) void tier_inv_kernel(Snap s, Bw64 bw, const fl
     if (pd < npd) {
         const uint32_t p = (uint32_t)(pd / s.D), d = (uint32_t)(pd - (uint64_t)p * s.D);
         const float *u = util_scen + (uint64_t)sc * npd;
+        // B' of each tier for this prefill (the same division for every pair)
+        double bt[4];
+#pragma unroll
+        for (uint32_t t = 0; t < 4; ++t) bt[t] = bw.b[t] / (1.0 + (double)s.n_inflight[t * s.P + p]);
         const uint32_t ta = s.tier_map[pd] & 3u;
-        const double ba = bw.b[ta] / (1.0 + (double)s.n_inflight[ta * s.P + p]);
+        const double ba = ta == 0 ? bt[0] : ta == 1 ? bt[1] : ta == 2 ? bt[2] : bt[3];
         const double ca = (double)s.util[pd], ha = (double)u[pd];
         const double xa = ba * (1.0 - ca), ya = ba * (1.0 - ha);
         for (uint32_t e = d + 1; e < s.D; ++e) {
             const uint64_t q = (uint64_t)p * s.D + e;
             const uint32_t tb = s.tier_map[q] & 3u;
             if (tb == ta) continue;
-            const double bb = bw.b[tb] / (1.0 + (double)s.n_inflight[tb * s.P + p]);
+            const double bb = tb == 0 ? bt[0] : tb == 1 ? bt[1] : tb == 2 ? bt[2] : bt[3];
             const double cb = (double)s.util[q], hb = (double)u[q];
             const double xb = bb * (1.0 - cb), yb = bb * (1.0 - hb);
             if (xa == xb) continue;
