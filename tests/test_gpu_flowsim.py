@@ -234,3 +234,33 @@ def test_offsets_that_are_not_a_partition_invalidate_the_call(nk):
     sel.sync_errors()
     _check_against_oracle([good, good, good], fin, st, arr2)
     sel.close()
+
+
+def test_bursts_cross_the_wavefront_and_workgroup_sizes(nk):
+    """Arrivals in bursts of 10, 70, 300 and 40 flows, apart and
+    overlapping, on the 64-GPU fat tree: the flows in progress cross 64
+    (one wavefront's lanes) and 256 (one flow per thread) upward and
+    downward many times, so every hand-over between the wavefront run, the
+    per-thread workgroup passes and the general workgroup passes is taken;
+    four load draws, every finish time and count against the oracle bit for
+    bit."""
+    _say("flow sim bursts")
+    cfg = W.CONFIGS["c0"]
+    rng = np.random.default_rng(17)
+    bursts = [(0.0, 10), (0.002, 70), (0.004, 300), (0.0041, 40), (0.05, 300), (0.3, 70), (0.31, 10)]
+    start = np.concatenate([np.full(n, t0) + rng.uniform(0.0, 1e-4, n) for t0, n in bursts])
+    n = len(start)
+    p_inst = rng.integers(0, cfg.n_prefill, n)
+    d_inst = rng.integers(0, cfg.n_decode, n)
+    insts = []
+    for i in range(4):
+        cap, lay = W.fat_tree_links(cfg, W.draw_links(cfg, 70 + i))
+        off, path = W.transfer_paths(cfg, 80 + i, p_inst, d_inst, lay)
+        insts.append(dict(cap=cap, path_off=off, path=path, bytes=rng.uniform(1e6, 2e9, n), start=start.copy()))
+    sel = nk.Selector(0)
+    fin, ev, arr = _run(nk, sel, insts)
+    sel.sync_errors()
+    # many flows in progress at once on average, so the larger passes ran
+    assert (ev[:, 2] / ev[:, 0] > 64).all(), ev
+    _check_against_oracle(insts, fin, ev, arr)
+    sel.close()
