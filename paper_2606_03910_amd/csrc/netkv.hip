@@ -658,9 +658,11 @@ __global__ __launch_bounds__(256) void order_kernel(Reqs rq, uint32_t P, uint32_
 // (one round up to 2^24 requests), each thread combining its consecutive
 // totals, the threads' results scanned by shuffles and then across the
 // wavefronts, with the running prefix of earlier rounds.
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 constexpr uint32_t kPrefixThreads = 1024;
 constexpr uint32_t kPrefixWaves = kPrefixThreads / kWave;
 constexpr uint32_t kPrefixPer = 16;
+static_assert(kPrefixPer % 2 == 0, "totals move in pairs");
 __global__ __launch_bounds__(kPrefixThreads) void tile_prefix_kernel(uint64_t *__restrict__ agg, uint32_t n) {
     __shared__ uint64_t wtot[kPrefixWaves];
     __shared__ uint64_t carry_s;
@@ -668,9 +670,22 @@ __global__ __launch_bounds__(kPrefixThreads) void tile_prefix_kernel(uint64_t *_
     uint64_t carry = kSegIdentity;
     for (uint64_t r0 = 0; r0 < n; r0 += (uint64_t)kPrefixThreads * kPrefixPer) {
         const uint64_t b0 = r0 + (uint64_t)tid * kPrefixPer;
+        // a thread's totals are consecutive: whole runs move in 16-byte
+        // pieces (half the requests of 8-byte ones), the tail one by one
+        const bool whole = b0 + kPrefixPer <= n;
         uint64_t v[kPrefixPer];
+        if (whole) {
+            const u64x2 *src = (const u64x2 *)(agg + b0);   // 16-byte aligned: b0 is a multiple of 16
 #pragma unroll
-        for (uint32_t u = 0; u < kPrefixPer; ++u) v[u] = b0 + u < n ? agg[b0 + u] : kSegIdentity;
+            for (uint32_t u = 0; u < kPrefixPer / 2; ++u) {
+                const u64x2 x = src[u];
+                v[2 * u] = x.x;
+                v[2 * u + 1] = x.y;
+            }
+        } else {
+#pragma unroll
+            for (uint32_t u = 0; u < kPrefixPer; ++u) v[u] = b0 + u < n ? agg[b0 + u] : kSegIdentity;
+        }
         uint64_t tot = kSegIdentity;
 #pragma unroll
         for (uint32_t u = 0; u < kPrefixPer; ++u) tot = seg_op(tot, v[u]);
@@ -688,10 +703,25 @@ __global__ __launch_bounds__(kPrefixThreads) void tile_prefix_kernel(uint64_t *_
         for (uint32_t q = 0; q < w; ++q) pre = seg_op(pre, wtot[q]);
         // this thread's first total's exclusive prefix
         uint64_t run = lane > 0 ? seg_op(pre, prev1) : pre;
+        uint64_t ex[kPrefixPer];   // the exclusive prefixes
 #pragma unroll
         for (uint32_t u = 0; u < kPrefixPer; ++u) {
-            if (b0 + u < n) agg[b0 + u] = run;
+            ex[u] = run;
             run = seg_op(run, v[u]);
+        }
+        if (whole) {
+            u64x2 *dst = (u64x2 *)(agg + b0);
+#pragma unroll
+            for (uint32_t u = 0; u < kPrefixPer / 2; ++u) {
+                u64x2 x;
+                x.x = ex[2 * u];
+                x.y = ex[2 * u + 1];
+                dst[u] = x;
+            }
+        } else {
+#pragma unroll
+            for (uint32_t u = 0; u < kPrefixPer; ++u)
+                if (b0 + u < n) agg[b0 + u] = ex[u];
         }
         if (tid == kPrefixThreads - 1) carry_s = run;
         __syncthreads();
@@ -1141,18 +1171,19 @@ __device__ inline void probe_from(const Table &t, uint32_t base, cptr<uint64_t> 
 }
 
 // Prefix lengths of every leader on every decode: one wavefront per
-// (leader, group of 64 decodes), looping over such tasks (the leader count
-// is read from device memory, so every wavefront ends after at most
-// ceil(tasks / wavefronts) of them).  A task takes the leader's blocks 64 at
-// a time, lane k block k: its holder value (looked up by lead_holder_kernel,
-// or here when there was no room), then the word of its bitmap row over
-// the task's 64 decodes (or the one-hot word of a single holder).  An
-// inclusive AND across lanes, seeded with the decodes still matching, gives
-// in lane k the decodes that hold every block up to k; it only loses bits as
-// k grows, so decode l matches exactly the blocks below the first lane whose
-// word lacks bit l, found by binary search over the words in LDS.  Writes
-// B_tok * j for the task's decodes, in fp32 (exact below 2^24; only
-// requests shorter than that read it, capped by their own length).
+// (leader, kLeadGroups groups of 64 decodes), looping over such tasks (the
+// leader count is read from device memory, so every wavefront ends after at
+// most ceil(tasks / wavefronts) of them).  A task takes the leader's blocks
+// 64 at a time, lane k block k: its holder value (looked up by
+// lead_holder_kernel, or here when there was no room), then, per group, the
+// word of its bitmap row over the group's 64 decodes (or the one-hot word of
+// a single holder).  An inclusive AND across lanes, seeded with the group's
+// decodes still matching, gives in lane k the decodes that hold every block
+// up to k; it only loses bits as k grows, so decode l matches exactly the
+// blocks below the first lane whose word lacks bit l, found by binary
+// search over the words in LDS.  Writes B_tok * j for the task's decodes,
+// in fp32 (exact below 2^24; only requests shorter than that read it,
+// capped by their own length).
 // Inclusive AND over lanes 0..l of a 32-bit value, in lane l, with DPP:
 // shifts right by 1, 2, 4 and 8 within each row of 16 lanes (a lane with
 // no source takes all ones), then the last lane of row 0 into row 1 and of
@@ -1173,57 +1204,86 @@ __device__ inline uint64_t wave_and_prefix_u64(uint64_t v) {
     return ((uint64_t)hi << 32) | lo;
 }
 
+// Groups of 64 decodes per task: the task's groups share each block's
+// holder value (and its load); their bitmap words load side by side.
+constexpr uint32_t kLeadGroups = 2;
+
 __global__ __launch_bounds__(kBlock) void lead_kernel(Table t, uint32_t D, uint32_t bt, const Lead *__restrict__ lead,
                                                       const unsigned int *__restrict__ n_lead, uint32_t lead_cap,
                                                       const uint32_t *__restrict__ hv,
                                                       const uint64_t *__restrict__ hashes, uint32_t ngroup,
                                                       float *__restrict__ lam_out) {
-    __shared__ uint64_t pw[kWavesPerBlock][kWave];
+    __shared__ uint64_t pw[kWavesPerBlock][kLeadGroups][kWave];
     const uint32_t lane = threadIdx.x % kWave;
     const uint32_t wv = wave_index();
     const uint32_t nl_all = *n_lead;
     const uint32_t nl = nl_all < lead_cap ? nl_all : lead_cap;
-    const uint64_t tasks = (uint64_t)nl * ngroup;
+    const uint32_t ntg = (ngroup + kLeadGroups - 1) / kLeadGroups;   // tasks per leader
+    const uint64_t tasks = (uint64_t)nl * ntg;
     const uint64_t nw = (uint64_t)gridDim.x * kWavesPerBlock;
     for (uint64_t task = (uint64_t)blockIdx.x * kWavesPerBlock + wv; task < tasks; task += nw) {
-        const uint32_t slot = (uint32_t)(task / ngroup), g = (uint32_t)(task % ngroup);
-        const uint32_t base = g * kWave;
+        const uint32_t slot = (uint32_t)(task / ntg), g0 = (uint32_t)(task % ntg) * kLeadGroups;
         const cptr<uint32_t> w = as_const((const uint32_t *)(lead + slot));
         const uint64_t a = ((uint64_t)w[1] << 32) | (uint64_t)w[0];
         const uint64_t hoff = ((uint64_t)w[3] << 32) | (uint64_t)w[2];
         const uint32_t n = w[4], m = w[5];
         const bool pre = m != kNoPre;
         const uint32_t nb = pre ? m : n;   // blocks to take (held by someone before block m)
-        uint64_t alive = ~0ull;            // decodes (lanes) holding every block so far
-        uint32_t j = 0;                    // this lane's decode: leading blocks held
-        for (uint32_t k0 = 0; k0 < nb && alive; k0 += kWave) {
+        // per group: the decodes (lanes) holding every block so far, and
+        // this lane's decode's leading blocks held; a group past the pool
+        // holds none
+        uint64_t alive[kLeadGroups];
+        uint32_t j[kLeadGroups];
+#pragma unroll
+        for (uint32_t q = 0; q < kLeadGroups; ++q) {
+            alive[q] = g0 + q < ngroup ? ~0ull : 0ull;
+            j[q] = 0;
+        }
+        auto live = [&]() {
+            uint64_t x = 0;
+#pragma unroll
+            for (uint32_t q = 0; q < kLeadGroups; ++q) x |= alive[q];
+            return x != 0;
+        };
+        for (uint32_t k0 = 0; k0 < nb && live(); k0 += kWave) {
             const uint32_t k = k0 + lane;
             const uint32_t nk = nb - k0 < (uint32_t)kWave ? nb - k0 : (uint32_t)kWave;
             uint32_t v = kNoHolder;
             if (k < nb) v = pre ? hv[hoff + k] : holder_lane(t, hashes[a + k]);
-            uint64_t word = 0;
-            if (v < kHeldOne) {
-                word = t.bits[(uint64_t)v * t.bpitch + g];
-            } else if (v != kNoHolder) {
-                const uint32_t o = (v & ~kHeldOne) - base;
-                word = o < (uint32_t)kWave ? 1ull << o : 0ull;
+#pragma unroll
+            for (uint32_t q = 0; q < kLeadGroups; ++q) {
+                const uint32_t g = g0 + q;
+                uint64_t word = 0;
+                if (g < ngroup) {
+                    if (v < kHeldOne) {
+                        word = t.bits[(uint64_t)v * t.bpitch + g];
+                    } else if (v != kNoHolder) {
+                        const uint32_t o = (v & ~kHeldOne) - g * kWave;
+                        word = o < (uint32_t)kWave ? 1ull << o : 0ull;
+                    }
+                }
+                pw[wv][q][lane] = wave_and_prefix_u64(word & alive[q]);
             }
-            const uint64_t pref = wave_and_prefix_u64(word & alive);
-            pw[wv][lane] = pref;
             __builtin_amdgcn_wave_barrier();
             // lane l: the number of leading words (of nk) holding bit l
-            uint32_t lo = 0, hi = nk;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi) / 2;
-                if ((pw[wv][mid] >> lane) & 1ull) lo = mid + 1;
-                else hi = mid;
+#pragma unroll
+            for (uint32_t q = 0; q < kLeadGroups; ++q) {
+                uint32_t lo = 0, hi = nk;
+                while (lo < hi) {
+                    const uint32_t mid = (lo + hi) / 2;
+                    if ((pw[wv][q][mid] >> lane) & 1ull) lo = mid + 1;
+                    else hi = mid;
+                }
+                j[q] += lo;
+                alive[q] = pw[wv][q][nk - 1];
             }
-            j += lo;
-            alive = pw[wv][nk - 1];
             __builtin_amdgcn_wave_barrier();
         }
-        const uint32_t d = base + lane;
-        if (d < D) lam_out[(uint64_t)slot * D + d] = (float)(bt * j);
+#pragma unroll
+        for (uint32_t q = 0; q < kLeadGroups; ++q) {
+            const uint32_t d = (g0 + q) * kWave + lane;
+            if (g0 + q < ngroup && d < D) lam_out[(uint64_t)slot * D + d] = (float)(bt * j[q]);
+        }
     }
 }
 
@@ -3243,7 +3303,7 @@ netkv_status run_select(netkv_handle h, Scratch &sc, const netkv_requests_t *req
     {
         // leaders' prefix lengths: 64 decodes per wavefront, 64 blocks per step
         const uint32_t lgroup = (h->D + kWave - 1) / kWave;
-        const uint64_t lw = std::min<uint64_t>((uint64_t)lcap * lgroup, 65536);
+        const uint64_t lw = std::min<uint64_t>((uint64_t)lcap * ((lgroup + kLeadGroups - 1) / kLeadGroups), 65536);
         hipLaunchKernelGGL(lead_kernel, dim3((uint32_t)((lw + kWavesPerBlock - 1) / kWavesPerBlock)),
                            dim3(kBlock), 0, s2, t, h->D, h->block_tokens, (const Lead *)sc.lead,
                            (const unsigned int *)sc.n_lead, lcap, (const uint32_t *)sc.hv, rq.hashes, lgroup,
