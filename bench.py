@@ -296,27 +296,27 @@ def main():
     log(f"warmup {args.warmup} done")
 
     # Events on the launch stream (torch's current stream, which the library
-    # launches on): the whole step, and the library's own pair around the
-    # scoring kernel (prefix lengths + score + per-group top-k) of the same launch.
+    # launches on): one pair around the timed steps (a pair per step would put
+    # two more event packets between consecutive calls), and the library's own
+    # pair around each call's scoring kernel (prefix lengths + score +
+    # per-group top-k).
     stream = torch.cuda.current_stream(dev)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     netkv.netkv_set_timing(sel.h, True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
+    ev0.record(stream)
+    for _ in range(args.steps):
         step()
-        ev[i][1].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     kern_ms = netkv.netkv_kernel_ms(sel.h)   # mean over the timed launches
     netkv.netkv_set_timing(sel.h, False)
     sel.sync_errors()
-    per = [a.elapsed_time(b) for a, b in ev]
-    step_ms = float(np.mean(per))
-    log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, step mean {step_ms:.3f} ms "
-        f"(min {min(per):.3f} max {max(per):.3f}), scoring kernel mean {kern_ms:.3f} ms")
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"timed {args.steps} steps: wall {wall * 1e3:.2f} ms, step mean {step_ms:.3f} ms, "
+        f"scoring kernel mean {kern_ms:.3f} ms")
 
     # ---- algorithmic bytes: 8 B per membership test of the first-miss scans
     # (sum over pairs of min(j + 1, n_r)), from the per-pair prefix lengths of
@@ -501,21 +501,20 @@ def bench_sweep(args, cfg, dev):
         step()
     sel.sync_errors()
     stream = torch.cuda.current_stream(dev)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     netkv.netkv_set_timing(sel.h, True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
+    ev0.record(stream)
+    for _ in range(args.steps):
         step()
-        ev[i][1].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     kern_ms = netkv.netkv_kernel_ms(sel.h)   # mean over the timed launches
     netkv.netkv_set_timing(sel.h, False)
     sel.sync_errors()
-    step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    step_ms = ev0.elapsed_time(ev1) / args.steps
     log(f"sweep: step {step_ms:.3f} ms, sweep kernel {kern_ms:.3f} ms")
     pairs = S * R * D
     ops = SWEEP_OPS_PER_PAIR * pairs
