@@ -173,6 +173,12 @@ __host__ __device__ inline uint32_t sl_pitch(uint32_t D) {
     return lines * 16u;
 }
 
+// Elements allocated after the last row of the per-(p, d) rows and of the
+// leaders' prefix-length table: one group of the widest scoring geometry
+// (64 lanes x 6 decodes), so that the scoring kernel's loads for columns
+// past the pool stay inside the allocation.
+constexpr uint32_t kRowPad = 64u * 6u;
+
 // Holder value of h, by one thread: both candidate buckets' keys, then the
 // value of the slot that holds h (most looked-up hashes are held by no
 // decode and need no value).
@@ -1371,25 +1377,35 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     const uint32_t i1 = (i0 + run_len < nv) ? i0 + run_len : nv;
     const uint32_t base = grp * (kWave * C);
     const uint32_t bt = s.block_tokens;
-    uint32_t d[C], voff[C], loff[C];
+    uint32_t d[C];
     float xmf[C];
     bool act[C];
     // x = l - lambda is feasible iff x < xlim, i.e. x <= xlim - 1 for
     // xlim >= 1; xlim = 0 never is (limit -1).  Limits above 2^24 are taken
-    // as 2^24, which every x scored in fp32 is below.  xlo: the least limit
-    // of the lane's decodes as fp32 bits, 0 when one is never feasible.
+    // as 2^24, which every x scored in fp32 is below.  A column past the
+    // pool has limit NaN, which no x passes, whatever its loads read.  xlo:
+    // the least limit of the lane's decodes as fp32 bits, 0 when one is
+    // never feasible (so a group with columns past the pool, and requests
+    // of at least one token, never take the all-feasible path).
     uint32_t xlo = 0xFFFFFFFFu;
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         d[q] = base + q * kWave + lane;
         act[q] = d[q] < s.D;
-        const uint32_t pc = act[q] ? d[q] : 0;
-        voff[q] = pc * (uint32_t)sizeof(float2);
-        loff[q] = pc * (uint32_t)sizeof(float);
         const uint64_t xlim = act[q] ? s.dxlim[d[q]] : 0;
-        xmf[q] = xlim == 0 ? -1.0f : (float)(xlim - 1 < kExactTok ? xlim - 1 : (uint64_t)kExactTok);
+        xmf[q] = !act[q] ? __builtin_nanf("")
+                 : xlim == 0 ? -1.0f
+                             : (float)(xlim - 1 < kExactTok ? xlim - 1 : (uint64_t)kExactTok);
         xlo = min(xlo, xlim == 0 ? 0u : __float_as_uint(xmf[q]));
     }
+    // column q of the lane is at lane offset (base + lane + 64 q) * size;
+    // the 64 q part is a constant that the loads carry in their offset
+    // field, so the lane needs one offset register per table.  Columns past
+    // the pool read what follows the last decode: the next row, or the
+    // kRowPad elements allocated after the last row.
+    constexpr uint32_t kRowStep = kWave * (uint32_t)sizeof(float2), kLamStep = kWave * (uint32_t)sizeof(float);
+    const uint32_t voff = (base + lane) * (uint32_t)sizeof(float2);
+    const uint32_t loff = (base + lane) * (uint32_t)sizeof(float);
     // a request of at most xall tokens (fp32 bits) is feasible on every
     // decode of the group
     const uint32_t xall = wave_min_u32_dpp(xlo);
@@ -1397,8 +1413,8 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     // rows of (seconds per token, constant part) and the leaders' prefix
     // lengths through buffer resources: a row's byte offset is the scalar
     // offset, the column's the lane offset
-    const uint64_t sl_bytes = (uint64_t)s.P * s.slp * sizeof(float2);      // < 2^32 (checked at load)
-    const uint64_t ll_bytes = (uint64_t)lead_rows * s.D * sizeof(float);   // < 2^32 (capacity is capped)
+    const uint64_t sl_bytes = ((uint64_t)s.P * s.slp + kRowPad) * sizeof(float2);   // < 2^32 (checked at load)
+    const uint64_t ll_bytes = ((uint64_t)lead_rows * s.D + kRowPad) * sizeof(float);   // < 2^32 (capped)
     const __amdgpu_buffer_rsrc_t slr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)s.sl, (short)0, (int)(uint32_t)(sl_bytes < 0xFFFFFFFFull ? sl_bytes : 0xFFFFFFFFull), kBufferFlags);
     const __amdgpu_buffer_rsrc_t llr = __builtin_amdgcn_make_buffer_rsrc(
@@ -1416,9 +1432,9 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     uint32_t laml[C], stg[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
-        rowv[q] = load_row(slr, voff[q], c0.row);
-        rowv2[q] = TWO ? load_row(srr, voff[q], c0.row) : rowv[q];
-        laml[q] = load_lam(llr, loff[q], c0.lrow);
+        rowv[q] = load_row(slr, voff + q * kRowStep, c0.row);
+        rowv2[q] = TWO ? load_row(srr, voff + q * kRowStep, c0.row) : rowv[q];
+        laml[q] = load_lam(llr, loff + q * kLamStep, c0.lrow);
         stg[q] = 0;
     }
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
@@ -1427,17 +1443,22 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     // one request: scoring-order position i, its record and the next one's
     // (whose leader values are fetched while i is scored)
     auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt, Hot &ahead) {
+        // the lane offsets, tied to the request (an empty asm, no
+        // instruction) so that the compiler keeps each column's offset
+        // in the load's offset field instead of a register of its own
+        uint32_t vo = voff, lo = loff;
+        asm("" : "+v"(vo), "+v"(lo) : "s"(i));
         // the next request's leader values, if its leader row differs
         const bool nl = nxt.lrow != cur.lrow;
         if (nl) {
 #pragma unroll
-            for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, loff[q], nxt.lrow);
+            for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, lo + q * kLamStep, nxt.lrow);
         }
         if (cur.row != rowcur) {
 #pragma unroll
             for (int q = 0; q < C; ++q) {
-                rowv[q] = load_row(slr, voff[q], cur.row);
-                if (TWO) rowv2[q] = load_row(srr, voff[q], cur.row);
+                rowv[q] = load_row(slr, vo + q * kRowStep, cur.row);
+                if (TWO) rowv2[q] = load_row(srr, vo + q * kRowStep, cur.row);
             }
             rowcur = cur.row;
         }
@@ -3012,7 +3033,7 @@ netkv_status ensure_scratch(netkv_handle h, Scratch &sc, uint64_t R, uint64_t pa
         dfree(sc.lead_lam);
         sc.lead_cap = 0;
         sc.zero_row_set = false;
-        if (dalloc(sc.lead, lc) != hipSuccess || dalloc(sc.lead_lam, (uint64_t)(lc + 1) * h->D) != hipSuccess)
+        if (dalloc(sc.lead, lc) != hipSuccess || dalloc(sc.lead_lam, (uint64_t)(lc + 1) * h->D + kRowPad) != hipSuccess)
             return fail(h, NETKV_ENOMEM, "leader table allocation failed");
         sc.lead_cap = lc;
         sc.lead_D = h->D;
@@ -3450,7 +3471,7 @@ uint64_t carve(uint8_t *base, uint64_t r, uint32_t D, uint64_t partial_elems, ui
     t.partial = (uint64_t *)take(8 * partial_elems);
     t.partial_cap = partial_elems;
     t.lead = (Lead *)take(sizeof(Lead) * (uint64_t)lead_cap);
-    t.lead_lam = (float *)take(4ull * ((uint64_t)lead_cap + 1) * D);
+    t.lead_lam = (float *)take(4ull * (((uint64_t)lead_cap + 1) * D + kRowPad));
     t.lead_cap = lead_cap;
     t.lead_D = D;
     t.hv = (uint32_t *)take(4 * hv_cap);
@@ -3731,7 +3752,7 @@ netkv_status netkv_oracle_load(netkv_handle h, const netkv_oracle_t *o, void *st
         h->ru1 = h->ru2 = nullptr;
         h->have_route = false;
         h->have_snap = false;
-        if (dalloc(h->sl, (uint64_t)P * sl_pitch(D)) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
+        if (dalloc(h->sl, (uint64_t)P * sl_pitch(D) + kRowPad) != hipSuccess || dalloc(h->dbase, D) != hipSuccess ||
             dalloc(h->dxlim, D) != hipSuccess) {
             cleanup();
             return fail(h, NETKV_ENOMEM, "snapshot allocation failed");
@@ -3834,7 +3855,7 @@ netkv_status netkv_route2_load(netkv_handle h, const uint8_t *tier1, const float
     float *ua = nullptr, *ub = nullptr;
     auto drop = [&]() { dfree(a); dfree(b); dfree(ua); dfree(ub); };
     if (dalloc(a, npd) != hipSuccess || dalloc(b, npd) != hipSuccess || dalloc(ua, npd) != hipSuccess ||
-        dalloc(ub, npd) != hipSuccess || (!h->sr && dalloc(h->sr, (uint64_t)h->P * sl_pitch(h->D)) != hipSuccess)) {
+        dalloc(ub, npd) != hipSuccess || (!h->sr && dalloc(h->sr, (uint64_t)h->P * sl_pitch(h->D) + kRowPad) != hipSuccess)) {
         drop();
         return fail(h, NETKV_ENOMEM, "route map allocation failed");
     }
