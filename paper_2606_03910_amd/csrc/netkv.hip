@@ -283,6 +283,36 @@ __device__ inline uint32_t wave_min_u32_dpp(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Minima over the 64 lanes of three values at once (12 VALU instructions
+// where three wave_min_u32_dpp take 21).  permlane32_swap exchanges the
+// upper half of a with the lower half of b, so one min leaves, in lanes
+// 0-31, a's minimum over lanes l and l + 32 and, in lanes 32-63, b's.
+// permlane16_swap then exchanges that register's odd rows of 16 lanes with
+// c's even rows, and one min gives row 0 a's minimum over lanes i, i + 16,
+// i + 32, i + 48, row 2 b's, and rows 1 and 3 c's over the lower and upper
+// half.  A DPP minimum within each row finishes all of them: a in lane 0,
+// b in lane 32, c the lesser of lanes 16 and 48.  Every lane must be
+// active.
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ inline void wave_min3_u32(uint32_t a, uint32_t b, uint32_t c, uint32_t &ma, uint32_t &mb,
+                                     uint32_t &mc) {
+    const auto s32 = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+    const uint32_t x = min((uint32_t)s32[0], (uint32_t)s32[1]);
+    const auto s16 = __builtin_amdgcn_permlane16_swap(x, c, false, false);
+    uint32_t z = min((uint32_t)s16[0], (uint32_t)s16[1]);
+    z = min(z, dpp_u32<0xB1>(z));    // quad_perm 1,0,3,2
+    z = min(z, dpp_u32<0x4E>(z));    // quad_perm 2,3,0,1
+    z = min(z, dpp_u32<0x124>(z));   // row_ror 4
+    z = min(z, dpp_u32<0x128>(z));   // row_ror 8
+    ma = (uint32_t)__builtin_amdgcn_readlane((int)z, 0);
+    mb = (uint32_t)__builtin_amdgcn_readlane((int)z, 32);
+    mc = min((uint32_t)__builtin_amdgcn_readlane((int)z, 16), (uint32_t)__builtin_amdgcn_readlane((int)z, 48));
+}
+
 // Validate request r's header; returns false (and flags) if inconsistent.
 __device__ inline bool request_ok(const Reqs &rq, const Snap &s, uint32_t r, uint32_t &p,
                                   uint32_t &len, uint64_t &a, uint32_t &n) {
@@ -1343,8 +1373,11 @@ __device__ inline uint32_t route_cost(float x, float2 r1, float2 r2) {
 // runs, so its L2 holds the snapshot rows of its own prefills.
 constexpr uint32_t kMaxMergeGroups = 8;
 
+// Without per-pair outputs the kernel is held to 80 registers, so that a
+// SIMD keeps 6 wavefronts (the staged-route variant needs one register
+// more than that when left alone).
 template <int K, int W, int C, bool PAIRS, bool TWO, bool MERGE>
-__global__ __launch_bounds__(MERGE ? kWave * kMaxMergeGroups : kBlock)
+__global__ __launch_bounds__(MERGE ? kWave * kMaxMergeGroups : kBlock, PAIRS ? 1 : 6)
 void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__restrict__ cold,
                   const float *__restrict__ lead_lam, uint32_t lead_rows, const uint64_t *__restrict__ hashes,
                   const uint32_t *__restrict__ len_tokens, const uint64_t *__restrict__ hash_off,
@@ -1440,9 +1473,11 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
     uint32_t pc_bits = 0xFFFFFFFFu, pc_idx = 0xFFFFFFFFu;   // gathered keys (empty = ~0)
 
-    // one request: scoring-order position i, its record and the next one's
-    // (whose leader values are fetched while i is scored)
-    auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt, Hot &ahead) {
+    // one request's column costs (fp32 bits, ~0 where infeasible):
+    // scoring-order position i, its record and the next one's (whose leader
+    // values are fetched while i is scored); returns whether the next
+    // request's leader differs, whose values next_leader then takes
+    auto cost = [&](uint32_t i, const Hot &cur, const Hot &nxt, Hot &ahead, uint32_t (&cb)[C]) {
         // the lane offsets, tied to the request (an empty asm, no
         // instruction) so that the compiler keeps each column's offset
         // in the load's offset field instead of a register of its own
@@ -1469,7 +1504,6 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
         ahead = load_hot(hot, i + 2);
         uint32_t r_out = 0;
         if (PAIRS) r_out = load_cold(cold, i).r;
-        uint32_t cb[C];
         if ((int32_t)cur.lams < 0) {
             // matched on its own from block 0, in integers (exact)
             const uint32_t r = load_cold(cold, i).r;
@@ -1525,35 +1559,51 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
                 }
             }
         }
-        // the group's K best: least cost bits, then least decode index,
-        // i.e. the lowest lane holding the minimum in the first column
-        // that holds it
-        const uint32_t slot = i - g0;
-#pragma unroll
-        for (int r = 0; r < K; ++r) {
-            uint32_t lm = cb[0];
-#pragma unroll
-            for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
-            const uint32_t mn = wave_min_u32_dpp(lm);
-            if (mn == 0xFFFFFFFFu) break;  // no feasible candidate left (uniform)
-            uint32_t dm = 0;
-#pragma unroll
-            for (int q = 0; q < C; ++q) {
-                const lmask m = ballot(cb[q] == mn);
-                if (m) {
-                    const uint32_t l = (uint32_t)__builtin_ctzll(m);
-                    dm = base + q * kWave + l;
-                    if (r + 1 < K && lane == l) cb[q] = 0xFFFFFFFFu;
-                    break;
-                }
-            }
-            pc_bits = write_lane(mn, slot * K + (uint32_t)r, pc_bits);
-            pc_idx = write_lane(dm, slot * K + (uint32_t)r, pc_idx);
-        }
+        return nl;
+    };
+    auto next_leader = [&](bool nl) {
         if (nl) {
 #pragma unroll
             for (int q = 0; q < C; ++q) laml[q] = stg[q];
         }
+    };
+    auto lane_min = [&](const uint32_t (&cb)[C]) {
+        uint32_t lm = cb[0];
+#pragma unroll
+        for (int q = 1; q < C; ++q) lm = min(lm, cb[q]);
+        return lm;
+    };
+    // one of the group's best, of cost bits mn (uniform; ~0 when no
+    // feasible candidate is left, and nothing is kept): the least decode
+    // index holding it, i.e. the lowest lane holding it in the first column
+    // that holds it, whose cost is then removed; its key goes to lane e
+    auto place = [&](uint32_t e, uint32_t mn, uint32_t (&cb)[C], bool more) {
+        if (mn == 0xFFFFFFFFu) return false;
+        uint32_t dm = 0;
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            const lmask m = ballot(cb[q] == mn);
+            if (m) {
+                const uint32_t l = (uint32_t)__builtin_ctzll(m);
+                dm = base + q * kWave + l;
+                if (more && lane == l) cb[q] = 0xFFFFFFFFu;
+                break;
+            }
+        }
+        pc_bits = write_lane(mn, e, pc_bits);
+        pc_idx = write_lane(dm, e, pc_idx);
+        return true;
+    };
+    // one request scored and its K best kept: least cost bits, then least
+    // decode index
+    auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt, Hot &ahead) {
+        uint32_t cb[C];
+        const bool nl = cost(i, cur, nxt, ahead, cb);
+        const uint32_t slot = i - g0;
+#pragma unroll
+        for (int r = 0; r < K; ++r)
+            if (!place(slot * K + (uint32_t)r, wave_min_u32_dpp(lane_min(cb)), cb, r + 1 < K)) break;
+        next_leader(nl);
     };
 
     for (uint32_t g0 = i0; g0 < i1; g0 += kPer) {
@@ -1561,12 +1611,27 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
         uint32_t i = g0;
         // three requests per trip: each record is loaded into the registers
         // of the one whose step has just ended, so the records rotate
-        // without copies
+        // without copies; for K = 1 the three requests' minima are taken
+        // together (not with per-pair outputs or staged routes, whose
+        // variants would then need more registers than 6 wavefronts per
+        // SIMD leave)
         for (; i + 3 <= g1; i += 3) {
             Hot c2, c3, c4;
-            step(i, g0, c0, c1, c2);
-            step(i + 1, g0, c1, c2, c3);
-            step(i + 2, g0, c2, c3, c4);
+            if (K == 1 && !PAIRS && !TWO) {
+                uint32_t ca[C], cb[C], cc[C];
+                next_leader(cost(i, c0, c1, c2, ca));
+                next_leader(cost(i + 1, c1, c2, c3, cb));
+                next_leader(cost(i + 2, c2, c3, c4, cc));
+                uint32_t ma, mb, mc;
+                wave_min3_u32(lane_min(ca), lane_min(cb), lane_min(cc), ma, mb, mc);
+                place(i - g0, ma, ca, false);
+                place(i + 1 - g0, mb, cb, false);
+                place(i + 2 - g0, mc, cc, false);
+            } else {
+                step(i, g0, c0, c1, c2);
+                step(i + 1, g0, c1, c2, c3);
+                step(i + 2, g0, c2, c3, c4);
+            }
             c0 = c3;
             c1 = c4;
         }
@@ -1604,7 +1669,12 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
                 }
             }
         } else if (lane < (g1 - g0) * K) {
-            partial[((uint64_t)grp * n_req + g0) * K + lane] = key;
+            // the lane tied to the chunk (an empty asm, no instruction), so
+            // that the store's address is formed here instead of held in
+            // registers through the loop
+            uint32_t ln = lane;
+            asm("" : "+v"(ln) : "s"(g0));
+            partial[((uint64_t)grp * n_req + g0) * K + ln] = key;
         }
         pc_bits = 0xFFFFFFFFu;
         pc_idx = 0xFFFFFFFFu;
