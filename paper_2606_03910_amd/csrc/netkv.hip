@@ -1460,36 +1460,28 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     Hot c1 = load_hot(hot, i0 + 1);
     float2 rowv[C], rowv2[C];   // the current prefill's row (and its staged-route row)
     uint32_t rowcur = c0.row;
-    // the current leader's B_tok * j, and the next one's while it loads, as
+    // the current leader's B_tok * j (the next one's while it loads), as
     // fp32 bits: non-negative, so their order is that of the unsigned bits
-    uint32_t laml[C], stg[C];
+    uint32_t laml[C];
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         rowv[q] = load_row(slr, voff + q * kRowStep, c0.row);
         rowv2[q] = TWO ? load_row(srr, voff + q * kRowStep, c0.row) : rowv[q];
         laml[q] = load_lam(llr, loff + q * kLamStep, c0.lrow);
-        stg[q] = 0;
     }
     constexpr uint32_t kPer = kWave / K;   // requests whose keys one store writes
     uint32_t pc_bits = 0xFFFFFFFFu, pc_idx = 0xFFFFFFFFu;   // gathered keys (empty = ~0)
 
     // one request's column costs (fp32 bits, ~0 where infeasible):
     // scoring-order position i, its record and the next one's (whose leader
-    // values are fetched while i is scored); returns whether the next
-    // request's leader differs, whose values next_leader then takes
+    // values are fetched while i is scored)
     auto cost = [&](uint32_t i, const Hot &cur, const Hot &nxt, Hot &ahead, uint32_t (&cb)[C]) {
-        // the lane offsets, tied to the request (an empty asm, no
-        // instruction) so that the compiler keeps each column's offset
-        // in the load's offset field instead of a register of its own
-        uint32_t vo = voff, lo = loff;
-        asm("" : "+v"(vo), "+v"(lo) : "s"(i));
-        // the next request's leader values, if its leader row differs
-        const bool nl = nxt.lrow != cur.lrow;
-        if (nl) {
-#pragma unroll
-            for (int q = 0; q < C; ++q) stg[q] = load_lam(llr, lo + q * kLamStep, nxt.lrow);
-        }
+        // the lane offsets of the loads below are tied to the request (an
+        // empty asm, no instruction) so that each column's offset stays in
+        // the load's offset field instead of a register of its own
         if (cur.row != rowcur) {
+            uint32_t vo = voff;
+            asm("" : "+v"(vo) : "s"(i));
 #pragma unroll
             for (int q = 0; q < C; ++q) {
                 rowv[q] = load_row(slr, vo + q * kRowStep, cur.row);
@@ -1504,6 +1496,24 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
         ahead = load_hot(hot, i + 2);
         uint32_t r_out = 0;
         if (PAIRS) r_out = load_cold(cold, i).r;
+        // this request's prefix lengths B_tok * j (fp32 bits): its leader's,
+        // capped by its own common run with the leader; then the next
+        // request's leader values, if its leader row differs, are loaded
+        // over the current ones, whose last use this is (with staged routes,
+        // after the costs: there the kernel has no registers for both sets
+        // beside the costs' operands)
+        uint32_t lam[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) lam[q] = min(laml[q], cur.lams);
+        auto reload = [&]() {
+            if (nxt.lrow != cur.lrow) {
+                uint32_t lo = loff;
+                asm("" : "+v"(lo) : "s"(i));
+#pragma unroll
+                for (int q = 0; q < C; ++q) laml[q] = load_lam(llr, lo + q * kLamStep, nxt.lrow);
+            }
+        };
+        if (!TWO) reload();
         if ((int32_t)cur.lams < 0) {
             // matched on its own from block 0, in integers (exact)
             const uint32_t r = load_cold(cold, i).r;
@@ -1540,17 +1550,16 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
             if (!PAIRS && cur.len <= xall) {
 #pragma unroll
                 for (int q = 0; q < C; ++q)
-                    cb[q] = route_cost<TWO>(lenf - __uint_as_float(min(laml[q], cur.lams)), rowv[q], rowv2[q]);
+                    cb[q] = route_cost<TWO>(lenf - __uint_as_float(lam[q]), rowv[q], rowv2[q]);
             } else {
 #pragma unroll
                 for (int q = 0; q < C; ++q) {
-                    const float lam = __uint_as_float(min(laml[q], cur.lams));
-                    const float x = lenf - lam;
+                    const float x = lenf - __uint_as_float(lam[q]);
                     const bool feas = x <= xmf[q];
                     const float cost = __uint_as_float(route_cost<TWO>(x, rowv[q], rowv2[q]));
                     if (PAIRS && act[q]) {
                         const uint64_t o = (uint64_t)r_out * s.D + d[q];
-                        const uint32_t jq = (uint32_t)lam / bt;
+                        const uint32_t jq = (uint32_t)__uint_as_float(lam[q]) / bt;
                         if (po.j) po.j[o] = (uint16_t)(jq < 0xFFFFu ? jq : 0xFFFFu);
                         if (po.feas) po.feas[o] = feas ? 1 : 0;
                         if (po.score) po.score[o] = cost;
@@ -1559,13 +1568,7 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
                 }
             }
         }
-        return nl;
-    };
-    auto next_leader = [&](bool nl) {
-        if (nl) {
-#pragma unroll
-            for (int q = 0; q < C; ++q) laml[q] = stg[q];
-        }
+        if (TWO) reload();
     };
     auto lane_min = [&](const uint32_t (&cb)[C]) {
         uint32_t lm = cb[0];
@@ -1598,12 +1601,11 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
     // decode index
     auto step = [&](uint32_t i, uint32_t g0, const Hot &cur, const Hot &nxt, Hot &ahead) {
         uint32_t cb[C];
-        const bool nl = cost(i, cur, nxt, ahead, cb);
+        cost(i, cur, nxt, ahead, cb);
         const uint32_t slot = i - g0;
 #pragma unroll
         for (int r = 0; r < K; ++r)
             if (!place(slot * K + (uint32_t)r, wave_min_u32_dpp(lane_min(cb)), cb, r + 1 < K)) break;
-        next_leader(nl);
     };
 
     for (uint32_t g0 = i0; g0 < i1; g0 += kPer) {
@@ -1619,9 +1621,9 @@ void score_kernel(Snap s, Table t, const Hot *__restrict__ hot, const Cold *__re
             Hot c2, c3, c4;
             if (K == 1 && !PAIRS && !TWO) {
                 uint32_t ca[C], cb[C], cc[C];
-                next_leader(cost(i, c0, c1, c2, ca));
-                next_leader(cost(i + 1, c1, c2, c3, cb));
-                next_leader(cost(i + 2, c2, c3, c4, cc));
+                cost(i, c0, c1, c2, ca);
+                cost(i + 1, c1, c2, c3, cb);
+                cost(i + 2, c2, c3, c4, cc);
                 uint32_t ma, mb, mc;
                 wave_min3_u32(lane_min(ca), lane_min(cb), lane_min(cc), ma, mb, mc);
                 place(i - g0, ma, ca, false);
