@@ -173,6 +173,36 @@ def test_tuning_options_leave_results_unchanged(nk):
     sel.close()
 
 
+def test_six_columns_with_a_partial_second_group(nk):
+    """420 decodes at 6 decodes per lane: one whole group of 384 and one of
+    36, whose other columns read past the last decode (the next row, or the
+    padding after the last row for the last prefill) and must never be
+    selected.  Per-pair outputs and top-3 against the oracle; the top-1
+    kernel (three requests reduced together) bit-identical to the per-pair
+    kernel's top-1, with and without requests that skip the feasibility
+    test."""
+    cl = W.Cluster(8, 7, 5, 2)
+    cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=3000, cache_per_decode=4096)
+    assert cfg.n_decode == 420
+    for m_min in (None, 15 * 10 ** 9):
+        _say("six columns, partial second group, m_min", m_min)
+        snap, req, cache = _inputs(cfg, 21, "random")
+        if m_min is not None:
+            snap["m_min"] = m_min
+        assert (np.asarray(req["prefill"]) == cfg.n_prefill - 1).any()
+        sel = _gpu(nk, snap, cache)
+        nk.netkv_set_option(sel.h, nk.NETKV_OPT_COLS, 6)
+        o = oracle.select(snap, cache, req, k=3, pairs=True, n_threads=8)
+        g = _run(nk, sel, req, 3)
+        _check_all(g, o)
+        assert (g["idx"] < cfg.n_decode).all()
+        g1 = _run(nk, sel, req, 1)
+        g2 = _run(nk, sel, req, 1, pairs=False)
+        assert np.array_equal(g2["idx"], g1["idx"])
+        assert np.array_equal(g2["score"].view(np.uint32), g1["score"].view(np.uint32))
+        sel.close()
+
+
 def test_all_feasible_path_matches_general_path(nk):
     """A pool of whole wavefronts of decodes (384), where a request no
     longer than every feasibility limit of a decode group is scored without
