@@ -1746,7 +1746,8 @@ __global__ __launch_bounds__(256) void derive_scen_kernel(Snap s, const float *_
 
 constexpr uint32_t kSweepThreads = 256;   // requests per workgroup, one per thread, in batch order
 constexpr uint32_t kSweepScen = 32;       // scenarios per workgroup
-constexpr uint32_t kSweepMaxTab = 8192;   // largest P * Dp kept in LDS (two fp32 tables)
+constexpr uint32_t kSweepMaxTab = 8192;   // largest P * Dp kept in LDS (two fp32 tables; three when held)
+constexpr uint32_t kSweepHold = 3;        // scenario-table entries a thread holds while the previous is scored
 
 // Ascending top-K list of fp32 cost bits (unsigned order) and decodes:
 // insert (key, d) by min / median-of-three on the values and selects on the
@@ -1830,16 +1831,21 @@ __device__ inline void sweep_x(const Snap &s, const Table &t, const Reqs &rq, co
 }
 
 // One thread per request (batch order), kSweepScen scenarios per
-// workgroup.  LDS: the (L + load term) constants of every (p, d) and the
-// current scenario's seconds per token, rows of Dp = D | 1 (an odd pitch,
-// so lanes of different prefills read different banks).  NX decodes'
+// workgroup.  LDS: the (L + load term) constants of every (p, d) and two
+// buffers of one scenario's seconds per token, rows of Dp = D | 1 (an odd
+// pitch, so lanes of different prefills read different banks).  While a
+// scenario is scored from one buffer, each thread holds its share of the
+// next scenario's table (loaded before the scoring, at most kSweepHold
+// entries) and stores it into the other buffer afterwards, so one barrier
+// per scenario suffices and the loads' latency is hidden behind the
+// scoring; larger tables are copied before each scenario instead.  NX decodes'
 // tokens are held in registers; a pool of more decodes is taken NX at a
 // time and its tokens recomputed per scenario.  FULL: exactly NX decodes,
 // every decode index a compile-time constant (no bounds test per pair).
 // Writes the top-k of every scenario and counts, per scenario, the requests
 // whose selected tier / decode differs from the loaded snapshot's selection.
 template <int K, int NX, bool LDS, bool FULL>
-__global__ __launch_bounds__(kSweepThreads) void sweep_kernel(Snap s, Table t, Reqs rq, const Hot *__restrict__ hotr,
+__global__ __launch_bounds__(kSweepThreads, FULL ? (K == 1 ? 6 : 5) : 1) void sweep_kernel(Snap s, Table t, Reqs rq, const Hot *__restrict__ hotr,
                                                              const float *__restrict__ lead_lam,
                                                              const float *__restrict__ spt_scen, uint32_t n_scen,
                                                              const int32_t *__restrict__ base_idx,
@@ -1847,7 +1853,7 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_kernel(Snap s, Table t, R
                                                              int32_t *__restrict__ out_idx,
                                                              float *__restrict__ out_score,
                                                              unsigned long long *__restrict__ flips) {
-    extern __shared__ float tab[];   // LDS: [P][Dp] constants, then [P][Dp] seconds per token
+    extern __shared__ float tab[];   // LDS: [P][Dp] constants, then 2 x [P][Dp] seconds per token
     const uint32_t P = s.P, D = FULL ? (uint32_t)NX : s.D, Dp = D | 1u;
     const uint32_t r = blockIdx.x * kSweepThreads + threadIdx.x;
     const uint32_t s0 = blockIdx.y * kSweepScen;
@@ -1860,12 +1866,25 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_kernel(Snap s, Table t, R
         rec = hotr[r];
         p = rec.row / (s.slp * (uint32_t)sizeof(float2));
     }
-    float *tc = tab, *ts = tab + (uint64_t)P * Dp;
-    if (LDS)
+    float *tc = tab, *tsb = tab + (uint64_t)P * Dp;
+    // a scenario's seconds per token into LDS buffer b (all of them, by
+    // this workgroup's threads)
+    auto table_copy = [&](uint32_t sc, uint32_t b) {
+        const float *sp = spt_scen + (uint64_t)sc * P * D;
+        float *ts = tsb + (uint64_t)b * P * Dp;
+        for (uint32_t i = threadIdx.x; i < P * D; i += kSweepThreads) {
+            const uint32_t pp = i / D;
+            ts[pp * Dp + (i - pp * D)] = sp[i];
+        }
+    };
+    const bool held = P * D <= kSweepThreads * kSweepHold;
+    if (LDS) {
         for (uint32_t i = threadIdx.x; i < P * D; i += kSweepThreads) {
             const uint32_t pp = i / D, d = i - pp * D;
             tc[pp * Dp + d] = s.sl[(uint64_t)pp * s.slp + d].y;
         }
+        if (held && s0 < s1) table_copy(s0, 0);
+    }
     const bool one = FULL || D <= (uint32_t)NX;
     float xf[NX];
     if (valid && one) sweep_x<NX>(s, t, rq, rec, r, lead_lam, 0, xf);
@@ -1874,13 +1893,25 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_kernel(Snap s, Table t, R
     const uint32_t lrow = p * Dp;
     for (uint32_t sc = s0; sc < s1; ++sc) {
         const float *sp = spt_scen + (uint64_t)sc * P * D;
+        const uint32_t buf = held ? (sc - s0) & 1u : 0u;
+        const float *ts = tsb + (uint64_t)buf * P * Dp;
+        float nx[kSweepHold];   // this thread's share of the next scenario's table
         if (LDS) {
-            __syncthreads();   // the previous scenario's table is no longer read
-            for (uint32_t i = threadIdx.x; i < P * D; i += kSweepThreads) {
-                const uint32_t pp = i / D;
-                ts[pp * Dp + (i - pp * D)] = sp[i];
+            if (held) {
+                __syncthreads();   // this scenario's buffer is written and the other one no longer read
+                if (sc + 1 < s1) {
+                    const float *spn = sp + (uint64_t)P * D;
+#pragma unroll
+                    for (uint32_t h = 0; h < kSweepHold; ++h) {
+                        const uint32_t i = threadIdx.x + h * kSweepThreads;
+                        nx[h] = i < P * D ? spn[i] : 0.0f;
+                    }
+                }
+            } else {
+                __syncthreads();   // the previous scenario's table is no longer read
+                table_copy(sc, 0);
+                __syncthreads();
             }
-            __syncthreads();
         }
         uint32_t tk[K], ti[K];
 #pragma unroll
@@ -1908,6 +1939,17 @@ __global__ __launch_bounds__(kSweepThreads) void sweep_kernel(Snap s, Table t, R
                             topk_ins32<K>(tk, ti, __float_as_uint(fmaf(xf[u], spt, cst)), d);
                         }
                     }
+                }
+            }
+        }
+        if (LDS && held && sc + 1 < s1) {
+            float *tn = tsb + (uint64_t)(buf ^ 1u) * P * Dp;
+#pragma unroll
+            for (uint32_t h = 0; h < kSweepHold; ++h) {
+                const uint32_t i = threadIdx.x + h * kSweepThreads;
+                if (i < P * D) {
+                    const uint32_t pp = i / D;
+                    tn[pp * Dp + (i - pp * D)] = nx[h];
                 }
             }
         }
@@ -4339,7 +4381,9 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
     const Table t = make_table(h);
     const uint32_t Dp = (uint32_t)D | 1u;
     const bool lds = P * Dp <= kSweepMaxTab;
-    const size_t lds_bytes = lds ? 2 * P * Dp * sizeof(float) : 0;
+    // a third table (the next scenario's) when the threads hold its entries
+    const bool held = (uint64_t)P * D <= (uint64_t)kSweepThreads * kSweepHold;
+    const size_t lds_bytes = lds ? (held ? 3 : 2) * P * Dp * sizeof(float) : 0;
     const dim3 grid((uint32_t)((R + kSweepThreads - 1) / kSweepThreads), (n_scen + kSweepScen - 1) / kSweepScen);
     unsigned long long *fl = (unsigned long long *)out_flips;
     HIPCHK(h, time_begin(h, s));

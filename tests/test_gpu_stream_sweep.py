@@ -199,3 +199,58 @@ def test_prop2_counts_around_the_bound_on_the_gpu(nk):
     g2 = nk.to_numpy(out2["inversions"]).reshape(-1, 3)
     assert g2.tolist() == [[1, 0, 0], [0, 0, 1]] and np.array_equal(g2, oracle.tier_inversions(snap2, scen2))
     sel.close()
+
+
+@pytest.mark.parametrize("shape", [(W.Cluster(8, 5, 1, 1), 30), (W.Cluster(8, 5, 3, 1), 90)])
+def test_sweep_scenarios_match_the_selection_under_each(nk, shape):
+    """37 random congestion scenarios (a full group of 32 and a group of 5,
+    so the scenario tables alternate buffers over both an even and an odd
+    count) on pools of 30 decodes (a scenario table of 300 entries, held by
+    the threads while the previous scenario is scored) and 90 decodes (2,700
+    entries, copied per scenario; decodes taken 64 at a time), for k = 1, 4
+    and 8: every scenario's top-k equals, bit for bit, the batch selection
+    under a snapshot whose congestion is that scenario's, and two scenarios
+    match the oracle."""
+    cl, D = shape
+    cfg = W.scaled(W.CONFIGS["c2"], cluster=cl, n_requests=1500, cache_per_decode=4096)
+    assert cfg.n_decode == D
+    snap, req, cache = _inputs_sw(cfg, 41)
+    P, S = cfg.n_prefill, 37
+    rng = np.random.default_rng(43)
+    util_s = rng.uniform(0.0, 0.9, (S, P * D)).astype(np.float32)
+    sel = nk.Selector(0)
+    sel.load_snapshot(snap)
+    sel.load_cache(cache, 0.5)
+    rd = nk.requests_to_device(req, sel.device)
+    us = nk.to_device(util_s.reshape(-1), sel.device)
+    ocache = oracle.Cache(cache, n_threads=8)
+    for k in (1, 4, 8):
+        _say("sweep against selections, D", D, "k", k)
+        out = sel.rank_sweep(rd, us, k=k)
+        sel.sync_errors()
+        g_idx = nk.to_numpy(out["idx"]).reshape(S, -1, k)
+        g_sc = nk.to_numpy(out["score"]).reshape(S, -1, k)
+        for s in range(S):
+            one = dict(snap)
+            one["util"] = util_s[s]
+            ref = nk.Selector(0)
+            ref.load_snapshot(one)
+            ref.load_cache(cache, 0.5)
+            b = ref.select(nk.requests_to_device(req, ref.device), k=k)
+            ref.sync_errors()
+            assert np.array_equal(g_idx[s].reshape(-1), nk.to_numpy(b["idx"])), (k, s)
+            assert np.array_equal(g_sc[s].reshape(-1).view(np.uint32),
+                                  nk.to_numpy(b["score"]).view(np.uint32)), (k, s)
+            ref.close()
+            if s in (0, S - 1):
+                o = oracle.select(one, ocache, req, k=k, pairs=True, n_threads=8)
+                check_topk(g_idx[s], g_sc[s], o["idx"], o["cost"], o["feasible"])
+    sel.close()
+
+
+def _inputs_sw(cfg, seed):
+    snap = W.make_snapshot(cfg, seed, inflight="random")
+    ch = W.prefix_chains(cfg, seed)
+    req = W.make_requests(cfg, seed, chains=ch)
+    cache = W.make_caches(cfg, seed, chains=ch)
+    return snap, req, cache
