@@ -2843,6 +2843,8 @@ struct netkv_ctx {
     // events (so a caller's graph capture takes both branches)
     hipStream_t side = nullptr;
     hipEvent_t ev_fork0 = nullptr, ev_fork1 = nullptr, ev_join = nullptr;
+    // the ranking sweep's fork of Proposition 2's counts onto the same stream
+    hipEvent_t ev_inv_fork = nullptr, ev_inv_join = nullptr;
     // the flow simulation's work buffer (flowsim.hip)
     void *flow_buf = nullptr;
     uint64_t flow_buf_bytes = 0;
@@ -3743,6 +3745,8 @@ netkv_status netkv_create(netkv_handle *out, int device) {
         hipEventCreateWithFlags(&h->ev_fork0, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&h->ev_fork1, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&h->ev_inv_fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&h->ev_inv_join, hipEventDisableTiming) != hipSuccess ||
         hipMemset(h->errword, 0, 4) != hipSuccess || hipMemset(h->loadword, 0, 4) != hipSuccess) {
         netkv_destroy(h);
         return NETKV_EDEVICE;
@@ -3761,6 +3765,8 @@ void netkv_destroy(netkv_handle h) {
         if (h->ev_fork0) (void)hipEventDestroy(h->ev_fork0);
         if (h->ev_fork1) (void)hipEventDestroy(h->ev_fork1);
         if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+        if (h->ev_inv_fork) (void)hipEventDestroy(h->ev_inv_fork);
+        if (h->ev_inv_join) (void)hipEventDestroy(h->ev_inv_join);
         dfree(h->tier_map);
         dfree(h->util);
         dfree(h->n_inflight);
@@ -4347,15 +4353,38 @@ netkv_status netkv_rank_sweep(netkv_handle h, const netkv_requests_t *req, uint3
                            2ull * n_scen, 0ull);
         HIPCHK(h, hipGetLastError());
     }
+    // The caller's stream waits for the second stream when the call
+    // returns (every path), if the counts below were forked onto it.
+    struct Join {
+        hipStream_t s;
+        hipEvent_t e;
+        bool on = false;
+        ~Join() {
+            if (on) (void)hipStreamWaitEvent(s, e, 0);
+        }
+    } join{s, h->ev_inv_join};
     if (out_inversions) {
-        // Proposition 2's counts depend on the snapshot and the scenarios only
-        hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(3ull * n_scen, 256)), dim3(256), 0, s, out_inversions,
+        // Proposition 2's counts depend on the snapshot and the scenarios
+        // only.  When the selection below leaves the second stream free (a
+        // batch below kForkMinN requests) they run there, beside the
+        // selection and the sweep.
+        const bool fork = R > 0 && R < kForkMinN;
+        hipStream_t si = fork ? h->side : s;
+        if (fork) {
+            HIPCHK(h, hipEventRecord(h->ev_inv_fork, s));
+            HIPCHK(h, hipStreamWaitEvent(si, h->ev_inv_fork, 0));
+        }
+        hipLaunchKernelGGL(fill_u64_kernel, dim3(grid_for(3ull * n_scen, 256)), dim3(256), 0, si, out_inversions,
                            3ull * n_scen, 0ull);
         Bw64 bw;
         for (int i = 0; i < 4; ++i) bw.b[i] = h->bw64[i];
-        hipLaunchKernelGGL(tier_inv_kernel, dim3((uint32_t)((P * D + 255) / 256), n_scen), dim3(256), 0, s, sn, bw,
+        hipLaunchKernelGGL(tier_inv_kernel, dim3((uint32_t)((P * D + 255) / 256), n_scen), dim3(256), 0, si, sn, bw,
                            util_scen, (unsigned long long *)out_inversions);
         HIPCHK(h, hipGetLastError());
+        if (fork) {
+            HIPCHK(h, hipEventRecord(h->ev_inv_join, si));
+            join.on = true;
+        }
     }
     if (R == 0) return NETKV_OK;
     if ((st = ensure_seq(h, R, P, false, true))) return st;
