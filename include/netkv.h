@@ -427,8 +427,11 @@ netkv_status netkv_selection_bytes(netkv_handle h, const netkv_requests_t *req, 
  * iteration bound, which valid input never does); offsets that are not
  * non-decreasing, or that end past n_flows, make every instance invalid.
  * Each instance's flows are first sorted by arrival time (rocPRIM's
- * segmented radix sort).  Grows a work buffer of the handle to 38 B per
- * flow, 8 B per instance and the sort's temporary storage, plus, for more
+ * segmented radix sort), and the instances are started heaviest first (by
+ * the sum over their flows of bytes over the least capacity on the path;
+ * rocPRIM's radix sort), which only changes where each one runs.  Grows a
+ * work buffer of the handle to 38 B per flow, 24 B per instance and the
+ * two sorts' temporary storage, plus, for more
  * than 2,048 links (whose state then lives in device memory instead of
  * LDS), 17 B per link and instance.  EINVAL: NULL arrays, n_links = 0,
  * n_inst >= 2^31, n_flows >= 2^32. */

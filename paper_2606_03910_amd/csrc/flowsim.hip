@@ -24,6 +24,7 @@
 // depend on the reduction order; link counts are integers).
 
 #include <hip/hip_runtime.h>
+#include <rocprim/device/device_radix_sort.hpp>
 #include <rocprim/device/device_segmented_radix_sort.hpp>
 
 #include <cmath>
@@ -65,6 +66,7 @@ struct SimArgs {
     const uint32_t *arr;        // [n_flows] each instance's flows (offsets) in order of arrival
     const uint64_t *skey;       // [n_flows] their arrival times as sort keys, in that order
     const uint32_t *bad_off;    // nonzero: flow_off is not a valid partition of the flows
+    const uint32_t *order;      // [n_inst] the instance of each workgroup, heaviest first (or null)
     double *g_rem;
     uint32_t *g_cnt, *g_lk;
     uint8_t *g_sat;
@@ -413,7 +415,7 @@ __global__ __launch_bounds__(kSimThreads) void flow_sim_kernel(SimArgs a) {
     __shared__ SimCtl ctl;
     extern __shared__ __align__(8) unsigned char dyn[];   // the link state in LDS mode
     const uint32_t tid = threadIdx.x, lane = tid % 64, w = tid / 64;
-    const uint32_t inst = blockIdx.x;
+    const uint32_t inst = a.order ? a.order[blockIdx.x] : blockIdx.x;
     const uint32_t L = a.n_links;
     const uint64_t f0 = a.flow_off[inst], f1 = a.flow_off[inst + 1];
     const double *cap = a.cap + (uint64_t)inst * L;
@@ -878,13 +880,30 @@ __global__ __launch_bounds__(kSimThreads) void flow_check_kernel(const uint64_t 
 // ones), its offset in the instance as the value, and the instance's
 // segment (empty for every instance when the offsets are invalid, so that
 // the sort stays inside the flows).
+// Per instance: the arrival-order sort's keys and segments, and the
+// instance's weight for the launch order, the sum over its flows of bytes
+// over the least capacity on the path (its rank agrees closely with the
+// instance's count of filling rounds).  Instances share the CUs, and one
+// holds the call until its last instance ends: workgroups taking the
+// heaviest instances first spread them over the CUs, beside lighter ones.
+// The weight skips what the simulation rejects (paths outside the path
+// array, links past n_links, bytes that are negative or not finite), and is
+// summed in a fixed order, so the launch order is the same for the same
+// input; no instance's results depend on it.
 __global__ __launch_bounds__(kSimThreads) void flow_keys_kernel(const uint64_t *__restrict__ flow_off,
                                                                 const double *__restrict__ start,
                                                                 const uint32_t *__restrict__ bad_off,
+                                                                const double *__restrict__ cap, uint32_t n_links,
+                                                                const uint64_t *__restrict__ path_off,
+                                                                const uint32_t *__restrict__ path, uint64_t n_path,
+                                                                const double *__restrict__ bytes,
                                                                 uint64_t *__restrict__ keys,
                                                                 uint32_t *__restrict__ vals,
                                                                 uint32_t *__restrict__ seg_b,
-                                                                uint32_t *__restrict__ seg_e) {
+                                                                uint32_t *__restrict__ seg_e,
+                                                                uint32_t *__restrict__ wkey,
+                                                                uint32_t *__restrict__ widx) {
+    __shared__ double red[kSimThreads];
     const uint32_t inst = blockIdx.x;
     const bool ok = *bad_off == 0;
     const uint64_t f0 = ok ? flow_off[inst] : 0, f1 = ok ? flow_off[inst + 1] : 0;   // < 2^32 when ok
@@ -892,10 +911,34 @@ __global__ __launch_bounds__(kSimThreads) void flow_keys_kernel(const uint64_t *
         seg_b[inst] = (uint32_t)f0;
         seg_e[inst] = (uint32_t)f1;
     }
+    const double *c = cap + (uint64_t)inst * n_links;
+    double w = 0.0;
     for (uint64_t f = f0 + threadIdx.x; f < f1; f += kSimThreads) {
         const uint64_t u = (uint64_t)__double_as_longlong(start[f]);
         keys[f] = (u >> 63) ? ~u : (u | (1ull << 63));
         vals[f] = (uint32_t)(f - f0);
+        const uint64_t p0 = path_off[f], p1 = path_off[f + 1];
+        double cm = __builtin_inf();
+        if (p1 > p0 && p1 <= n_path)
+            for (uint64_t q = p0; q < p1; ++q) {
+                const uint32_t l = path[q];
+                if (l < n_links) cm = fmin(cm, c[l]);
+            }
+        const double b = bytes[f];
+        if (b >= 0.0 && isfinite(b) && cm > 0.0 && isfinite(cm)) w += b / cm;
+    }
+    red[threadIdx.x] = w;
+    __syncthreads();
+    for (uint32_t h = kSimThreads / 2; h > 0; h /= 2) {
+        if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        // descending weight as an ascending key (a weight is >= 0, so its
+        // fp32 bits grow with it)
+        const float wf = (float)red[0];
+        wkey[inst] = ~__float_as_uint(isfinite(wf) ? wf : 3.0e38f);
+        widx[inst] = inst;
     }
 }
 
@@ -935,8 +978,17 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         if (prev >= 0 && prev != dev) (void)hipSetDevice(prev);
         return netkv_internal_fail(h, NETKV_EDEVICE, "arrival sort size query failed");
     }
+    // the launch order's sort of the instances' weights
+    size_t isort_bytes = 0;
+    if (e == hipSuccess && n_flows)
+        e = rocprim::radix_sort_pairs(nullptr, isort_bytes, (const uint32_t *)nullptr, (uint32_t *)nullptr,
+                                      (const uint32_t *)nullptr, (uint32_t *)nullptr, n_inst, 0, 32, s);
+    if (e != hipSuccess) {
+        if (prev >= 0 && prev != dev) (void)hipSetDevice(prev);
+        return netkv_internal_fail(h, NETKV_EDEVICE, "launch-order sort size query failed");
+    }
     const uint64_t per_flow = align256(8 * n_flows) * 3 + align256(n_flows) * 2 + align256(4 * n_flows) * 3;
-    const uint64_t per_inst = 2 * align256(4ull * n_inst) + 256 + align256(sort_bytes);
+    const uint64_t per_inst = 6 * align256(4ull * n_inst) + 256 + align256(sort_bytes) + align256(isort_bytes);
     const uint64_t per_link = lds ? 0 : align256(8ull * n_inst * n_links) + 2 * align256(4ull * n_inst * n_links) +
                                             align256((uint64_t)n_inst * n_links);
     void *buf = nullptr;
@@ -986,6 +1038,16 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         p += 256;
         void *sort_tmp = p;
         p += align256(sort_bytes);
+        uint32_t *wkey = (uint32_t *)p;
+        p += align256(4ull * n_inst);
+        uint32_t *wkey2 = (uint32_t *)p;
+        p += align256(4ull * n_inst);
+        uint32_t *widx = (uint32_t *)p;
+        p += align256(4ull * n_inst);
+        uint32_t *order = (uint32_t *)p;
+        p += align256(4ull * n_inst);
+        void *isort_tmp = p;
+        p += align256(isort_bytes);
         if (!lds) {
             a.g_rem = (double *)p;
             p += align256(8ull * n_inst * n_links);
@@ -999,11 +1061,18 @@ extern "C" netkv_status netkv_flow_sim(netkv_handle h, uint32_t n_inst, uint32_t
         hipLaunchKernelGGL(flow_check_kernel, dim3(1), dim3(kSimThreads), 0, s, flow_off, n_inst, n_flows, bad_off);
         if (n_flows) {
             hipLaunchKernelGGL(flow_keys_kernel, dim3(n_inst), dim3(kSimThreads), 0, s, flow_off, start,
-                               (const uint32_t *)bad_off, (uint64_t *)a.remaining, a.mlist, seg_b, seg_e);
+                               (const uint32_t *)bad_off, cap, n_links, path_off, path, n_path, bytes,
+                               (uint64_t *)a.remaining, a.mlist, seg_b, seg_e, wkey, widx);
             size_t tb = sort_bytes;
             e = rocprim::segmented_radix_sort_pairs(sort_tmp, tb, (const uint64_t *)a.remaining, skey,
                                                     (const uint32_t *)a.mlist, arr, (unsigned)n_flows, n_inst,
                                                     (const uint32_t *)seg_b, (const uint32_t *)seg_e, 0, 64, s);
+            if (e == hipSuccess) {
+                size_t ib = isort_bytes;
+                e = rocprim::radix_sort_pairs(isort_tmp, ib, (const uint32_t *)wkey, wkey2, (const uint32_t *)widx,
+                                              order, n_inst, 0, 32, s);
+                a.order = order;
+            }
         }
         if (e == hipSuccess && lds)
             hipLaunchKernelGGL(flow_sim_kernel<true>, dim3(n_inst), dim3(kSimThreads), lds_link_bytes(n_links), s, a);
