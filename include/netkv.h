@@ -272,7 +272,10 @@ netkv_status netkv_route2_of(netkv_handle h, const netkv_requests_t *req, uint32
  *                           proposition);
  *   out_inversions[3*s+2] = all pairs whose strict snapshot order the
  *                           scenario does not keep;
- * evaluated in fp64 (the policy option does not apply to them).
+ * evaluated in fp64 (the policy option does not apply to them).  For a
+ * batch below 2^16 requests they run on the handle's second stream, forked
+ * from `stream` and joined back to it by events before the call returns,
+ * so ordering on `stream` (and a graph capture of it) covers them.
  * Asynchronous; grows internal buffers on first use (n_scen * P * D * 4
  * bytes of per-scenario factors, 16 bytes per request of records, and the
  * selection's buffers, see netkv_reserve).  Invalid requests get index -1
