@@ -3256,12 +3256,14 @@ hipError_t prefill_order(netkv_handle h, Scratch &sc, uint32_t n, uint32_t pbits
 
 uint32_t auto_run_len(uint64_t R, uint32_t ngroup) {
     // runs of 128 sorted requests, shortened (to 8 at least) while that
-    // leaves fewer than 8K wavefronts (measured on MI355X: on the
-    // 4,096-GPU workloads 128 beats both 64, which starts more runs with a
-    // full scan, and 256, which keeps fewer wavefronts in flight)
+    // leaves fewer than 32K wavefronts (measured on MI355X: 1,048,576
+    // requests of 25 blocks on 8 decode groups score fastest in runs of
+    // 128, 65,536 wavefronts, against 64, which starts more runs with a
+    // full scan, and 256; 262,144 requests of 191 blocks fastest in runs of
+    // 64, 32,768 wavefronts, against 32 and 128)
     const uint64_t work = R * ngroup;
     uint64_t rl = 128;
-    while (rl > 8 && work / rl < 8192) rl /= 2;
+    while (rl > 8 && work / rl < 32768) rl /= 2;
     return (uint32_t)rl;
 }
 
